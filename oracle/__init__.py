@@ -1,0 +1,221 @@
+"""CPU oracle for the SpectrumKV per-token mixed-precision KV transfer codec.
+
+TEST INFRASTRUCTURE ONLY: only the test suite, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import this package.  The GPU library
+never reads, links or calls anything here.
+
+This is a thin ctypes wrapper over ``skv_oracle.c`` (plain, single-threaded C);
+every function passes numpy arrays through unchanged and raises
+``OracleError`` on a nonzero status.  Arrays of binary16 values travel as
+``uint16`` bit patterns so that no conversion happens on the way in or out.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+OK, ERR_INVALID_ARG, ERR_BUDGET, ERR_CAPACITY, ERR_FORMAT = 0, 1, 2, 3, 4
+FP16, INT8, INT4, DROP = 0, 1, 2, 3
+KVNORM, ATTN, RECENCY = 0, 1, 2
+CHUNK_TOKENS = 256
+
+
+class OracleError(RuntimeError):
+    def __init__(self, status, what):
+        super().__init__(f"oracle {what} failed with status {status}")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
+                ("budget", ctypes.c_float), ("first_ratio", ctypes.c_float),
+                ("num_sink", ctypes.c_int32), ("decay", ctypes.c_float),
+                ("num_tiers", ctypes.c_int32), ("score_mode", ctypes.c_int32),
+                ("num_q_heads", ctypes.c_int32), ("obs_window", ctypes.c_int32)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("n_sink", ctypes.c_int32), ("n_fp16", ctypes.c_int32),
+                ("n_int8", ctypes.c_int32), ("n_int4", ctypes.c_int32),
+                ("n_drop", ctypes.c_int32), ("budget_units", ctypes.c_int64),
+                ("used_units", ctypes.c_int64)]
+
+
+def _load():
+    if not os.path.exists(_build.LIB) or os.path.getmtime(_build.LIB) < os.path.getmtime(_build.SRC):
+        _build.build()
+    lib = ctypes.CDLL(_build.LIB)
+    P = ctypes.POINTER
+    cfgp = P(Config)
+    vp = ctypes.c_void_p
+    sig = {
+        "ora_validate": (ctypes.c_int, [cfgp]),
+        "ora_plan": (ctypes.c_int, [cfgp, P(Plan)]),
+        "ora_payload_size": (ctypes.c_int, [cfgp, P(ctypes.c_uint64)]),
+        "ora_decay_table": (None, [ctypes.c_float, ctypes.c_int, ctypes.c_int32, vp]),
+        "ora_sumsq": (ctypes.c_int, [cfgp, vp, vp, ctypes.c_int32, P(ctypes.c_uint64), P(ctypes.c_uint64)]),
+        "ora_score": (ctypes.c_int, [cfgp, vp, vp, vp, vp]),
+        "ora_composite": (ctypes.c_uint64, [ctypes.c_double, ctypes.c_int32]),
+        "ora_assign": (ctypes.c_int, [cfgp, vp, vp]),
+        "ora_offsets": (None, [ctypes.c_int32, vp, vp, vp]),
+        "ora_encode_row": (ctypes.c_int, [ctypes.c_int, ctypes.c_int32, vp, vp, P(ctypes.c_float)]),
+        "ora_decode_row": (None, [ctypes.c_int, ctypes.c_int32, vp, ctypes.c_float, vp]),
+        "ora_pack": (ctypes.c_int, [cfgp, vp, vp, vp, vp, ctypes.c_uint64]),
+        "ora_check_header": (ctypes.c_int, [cfgp, vp, ctypes.c_uint64]),
+        "ora_unpack": (ctypes.c_int, [cfgp, vp, ctypes.c_uint64, vp, vp, vp, ctypes.c_int32, ctypes.c_int32]),
+        "ora_half_to_double": (ctypes.c_double, [ctypes.c_uint16]),
+        "ora_float_to_half": (ctypes.c_uint16, [ctypes.c_float]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def _ptr(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _u16(a):
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.float16:
+        a = a.view(np.uint16)
+    if a.dtype != np.uint16:
+        raise TypeError(f"expected float16/uint16 array, got {a.dtype}")
+    return a
+
+
+def config(num_layers, num_kv_heads, head_dim, num_tokens, budget, first_ratio=0.02, num_sink=-1,
+           decay=0.005, num_tiers=3, score_mode=KVNORM, num_q_heads=0, obs_window=0):
+    return Config(num_layers, num_kv_heads, head_dim, num_tokens, budget, first_ratio, num_sink,
+                  decay, num_tiers, score_mode, num_q_heads, obs_window)
+
+
+def validate(cfg):
+    return _lib.ora_validate(ctypes.byref(cfg))
+
+
+def plan(cfg):
+    p = Plan()
+    st = _lib.ora_plan(ctypes.byref(cfg), ctypes.byref(p))
+    if st:
+        raise OracleError(st, "plan")
+    return {f: getattr(p, f) for f, _ in Plan._fields_}
+
+
+def payload_size(cfg):
+    out = ctypes.c_uint64()
+    st = _lib.ora_payload_size(ctypes.byref(cfg), ctypes.byref(out))
+    if st:
+        raise OracleError(st, "payload_size")
+    return out.value
+
+
+def decay_table(decay, which, count):
+    out = np.empty(count, np.float64)
+    _lib.ora_decay_table(ctypes.c_float(decay), which, count, _ptr(out))
+    return out
+
+
+def sumsq(cfg, k, v, t):
+    """Exact sum of squares of token t over all layers/heads/K/V, in units of 2^-48."""
+    k, v = _u16(k), _u16(v)
+    hi, lo = ctypes.c_uint64(), ctypes.c_uint64()
+    _lib.ora_sumsq(ctypes.byref(cfg), _ptr(k), _ptr(v), t, ctypes.byref(hi), ctypes.byref(lo))
+    return (hi.value << 64) | lo.value
+
+
+def score(cfg, k, v, q=None):
+    k, v = _u16(k), _u16(v)
+    q = None if q is None else _u16(q)
+    out = np.empty(cfg.num_tokens, np.float64)
+    st = _lib.ora_score(ctypes.byref(cfg), _ptr(k), _ptr(v), _ptr(q), _ptr(out))
+    if st:
+        raise OracleError(st, "score")
+    return out
+
+
+def composite(key, t):
+    return _lib.ora_composite(float(key), int(t))
+
+
+def assign(cfg, key):
+    key = np.ascontiguousarray(key, np.float64)
+    out = np.empty(cfg.num_tokens, np.uint8)
+    st = _lib.ora_assign(ctypes.byref(cfg), _ptr(key), _ptr(out))
+    if st:
+        raise OracleError(st, "assign")
+    return out
+
+
+def offsets(tier):
+    tier = np.ascontiguousarray(tier, np.uint8)
+    n = tier.shape[0]
+    units = np.empty(n, np.uint32)
+    qrank = np.empty(n, np.uint32)
+    _lib.ora_offsets(n, _ptr(tier), _ptr(units), _ptr(qrank))
+    return units, qrank
+
+
+def encode_row(tier, row):
+    """Returns (payload bytes of the row, scale as float32, non-finite flag)."""
+    row = _u16(row)
+    d = row.shape[0]
+    width = {FP16: 2 * d, INT8: d, INT4: d // 2, DROP: 0}[int(tier)]
+    out = np.zeros(max(width, 1), np.uint8)
+    sc = ctypes.c_float(0.0)
+    bad = _lib.ora_encode_row(int(tier), d, _ptr(row), _ptr(out), ctypes.byref(sc))
+    return out[:width], np.float32(sc.value), bool(bad)
+
+
+def decode_row(tier, d, data, scale):
+    data = np.ascontiguousarray(data, np.uint8)
+    if data.size == 0:
+        data = np.zeros(1, np.uint8)
+    out = np.empty(d, np.uint16)
+    _lib.ora_decode_row(int(tier), d, _ptr(data), ctypes.c_float(scale), _ptr(out))
+    return out
+
+
+def pack(cfg, k, v, tier):
+    k, v = _u16(k), _u16(v)
+    tier = np.ascontiguousarray(tier, np.uint8)
+    size = payload_size(cfg)
+    out = np.empty(size, np.uint8)
+    st = _lib.ora_pack(ctypes.byref(cfg), _ptr(k), _ptr(v), _ptr(tier), _ptr(out), size)
+    if st:
+        raise OracleError(st, "pack")
+    return out
+
+
+def check_header(cfg, payload):
+    payload = np.ascontiguousarray(payload, np.uint8)
+    return _lib.ora_check_header(ctypes.byref(cfg), _ptr(payload), payload.size)
+
+
+def unpack(cfg, payload, k_cache, v_cache, block_table, block_size=16):
+    """Dequantizes into k_cache/v_cache (uint16 [L][num_blocks][block_size][H][d]) in place."""
+    payload = np.ascontiguousarray(payload, np.uint8)
+    block_table = np.ascontiguousarray(block_table, np.int32)
+    for c in (k_cache, v_cache):
+        if c.dtype != np.uint16 or not c.flags.c_contiguous:
+            raise TypeError("caches must be C-contiguous uint16 arrays")
+    num_blocks = k_cache.shape[1]
+    st = _lib.ora_unpack(ctypes.byref(cfg), _ptr(payload), payload.size, _ptr(k_cache),
+                         _ptr(v_cache), _ptr(block_table), num_blocks, block_size)
+    return st
+
+
+def half_to_double(h):
+    return _lib.ora_half_to_double(int(h))
+
+
+def float_to_half(f):
+    return _lib.ora_float_to_half(ctypes.c_float(f))

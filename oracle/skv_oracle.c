@@ -1,0 +1,627 @@
+/*
+ * skv_oracle.c -- CPU oracle for the SpectrumKV per-token mixed-precision KV
+ * transfer codec (arXiv 2606.08635).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is a plain, slow, single-threaded
+ * implementation of what the codec computes, written from the paper; where
+ * the paper leaves a choice open, the function that makes it states the
+ * reading taken.  Only the test suite, the smoke
+ * check and the benchmark's CPU-baseline leg may load it.  It shares no code,
+ * header, table or constant with the GPU library: it has its own binary16
+ * conversions (written from IEEE 754), its own plan arithmetic and its own
+ * payload writer and reader.
+ *
+ * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -shared -fPIC.
+ * Floating point follows the C abstract machine on x86-64 (SSE2,
+ * FLT_EVAL_METHOD == 0, round-to-nearest-even): every float or double
+ * operation below is one correctly rounded IEEE 754 operation.
+ *
+ * Functions and the passages they follow:
+ *   ora_plan            normalized budget (Sec. 2.1, eq. "budget"), the
+ *                       budget-to-tier mapping (Sec. 4.4), sink reservation
+ *                       (Sec. 4.4, Algorithm 1 step 2), the 2-tier drop rule
+ *                       (Sec. 7.4.3 / probe ablation).
+ *   ora_decay_table     the recency factor exp(-lambda*Delta) of eq.
+ *                       "importance" (Sec. 4.3).
+ *   ora_score           I_j = A_j exp(-lambda Delta_j) (Sec. 4.3) with the
+ *                       KV-norm fallback or an observation-window attention
+ *                       statistic (Sec. 3, Sec. 4.3).
+ *   ora_assign          sink pinning + importance-sorted assignment
+ *                       (Sec. 2.3 Prop. 1 "exchange argument"; Algorithm 1
+ *                       steps 2-3).
+ *   ora_pack            per-tier quantization of K and V, independently,
+ *                       into one mixed-precision payload (Algorithm 1 step 4;
+ *                       "standard symmetric" quantizer, Sec. 8).
+ *   ora_unpack          decode-side dequantization into a paged fp16 cache
+ *                       (Sec. 4.2, Fig. "sysarch").
+ * Every parity claim of the GPU path is made against these functions.
+ */
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Types and constants (the oracle's own copies; values are fixed by the      */
+/* payload format, not shared with the library).                              */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  int32_t num_layers;   /* L   */
+  int32_t num_kv_heads; /* H   */
+  int32_t head_dim;     /* d   */
+  int32_t num_tokens;   /* n   */
+  float budget;         /* b   */
+  float first_ratio;    /* rho */
+  int32_t num_sink;     /* -1: ceil(rho*n); >= 0: explicit */
+  float decay;          /* lambda */
+  int32_t num_tiers;    /* 2 or 3 */
+  int32_t score_mode;   /* 0 kv-norm, 1 attention, 2 recency */
+  int32_t num_q_heads;  /* attention mode */
+  int32_t obs_window;   /* attention mode */
+} ora_config;
+
+typedef struct {
+  int32_t n_sink, n_fp16, n_int8, n_int4, n_drop;
+  int64_t budget_units, used_units;
+} ora_plan_t;
+
+enum { ORA_OK = 0, ORA_ERR_INVALID_ARG = 1, ORA_ERR_BUDGET = 2,
+       ORA_ERR_CAPACITY = 3, ORA_ERR_FORMAT = 4 };
+enum { T_FP16 = 0, T_INT8 = 1, T_INT4 = 2, T_DROP = 3 };
+enum { MODE_KVNORM = 0, MODE_ATTN = 1, MODE_RECENCY = 2 };
+
+#define ORA_MAGIC 0x31564B53u /* bytes 'S','K','V','1' */
+#define ORA_VERSION 1u
+#define ORA_CHUNK 256          /* tokens per chunk-index entry */
+#define ORA_MAX_TOKENS (1 << 21)
+
+typedef unsigned __int128 u128;
+
+static uint64_t up256(uint64_t x) { return (x + 255u) & ~(uint64_t)255u; }
+
+/* ------------------------------------------------------------------------ */
+/* binary16 <-> binary32 / binary64, written from the IEEE 754 definition.     */
+/* ------------------------------------------------------------------------ */
+
+/* Exact value of a binary16 encoding. */
+double ora_half_to_double(uint16_t h) {
+  int sign = h >> 15, e = (h >> 10) & 31, m = h & 1023;
+  double v;
+  if (e == 0) v = ldexp((double)m, -24);              /* subnormal or zero */
+  else if (e == 31) v = m ? NAN : INFINITY;
+  else v = ldexp((double)(m + 1024), e - 25);         /* (1.m) * 2^(e-15) */
+  return sign ? -v : v;
+}
+
+/* Round a binary32 value to binary16, nearest-even.  NaN maps to 0x7E00. */
+uint16_t ora_float_to_half(float f) {
+  double x = (double)f; /* exact */
+  uint16_t sign = signbit(x) ? 0x8000 : 0;
+  double a = fabs(x);
+  if (isnan(x)) return 0x7E00;
+  if (a >= 65520.0) return sign | 0x7C00;            /* rounds to infinity */
+  if (a < ldexp(1.0, -14)) {                         /* subnormal range */
+    double q = nearbyint(ldexp(a, 24));              /* exact scaling, RNE */
+    return sign | (uint16_t)q;                       /* q==1024 -> min normal */
+  }
+  int E;
+  (void)frexp(a, &E);               /* a = f*2^E, f in [0.5,1): exponent E-1 */
+  int ex = E - 1;
+  double q = nearbyint(ldexp(a, 10 - ex));           /* in [1024, 2048] */
+  if (q == 2048.0) { q = 1024.0; ex += 1; }
+  if (ex + 15 >= 31) return sign | 0x7C00;
+  return sign | (uint16_t)(((ex + 15) << 10) | ((int)q - 1024));
+}
+
+static float half_to_float(uint16_t h) { return (float)ora_half_to_double(h); }
+
+/* ------------------------------------------------------------------------ */
+/* Validation and plan (Sec. 2.1 eq. "budget"; Sec. 4.4).                      */
+/* ------------------------------------------------------------------------ */
+
+static int valid_head_dim(int d) { return d == 32 || d == 64 || d == 128 || d == 256; }
+
+int ora_validate(const ora_config* c) {
+  if (!c) return ORA_ERR_INVALID_ARG;
+  if (c->num_layers < 1 || c->num_kv_heads < 1) return ORA_ERR_INVALID_ARG;
+  if (!valid_head_dim(c->head_dim)) return ORA_ERR_INVALID_ARG;
+  if (c->num_tokens < 1 || c->num_tokens > ORA_MAX_TOKENS) return ORA_ERR_INVALID_ARG;
+  if ((int64_t)c->num_layers * c->num_kv_heads > 65536) return ORA_ERR_INVALID_ARG;
+  if (!(c->budget > 0.0f && c->budget <= 1.0f)) return ORA_ERR_INVALID_ARG;
+  if (!(c->first_ratio >= 0.0f && c->first_ratio <= 1.0f)) return ORA_ERR_INVALID_ARG;
+  if (c->num_sink < -1) return ORA_ERR_INVALID_ARG;
+  if (!(c->decay >= 0.0f) || isinf(c->decay)) return ORA_ERR_INVALID_ARG;
+  if (2.0 * (double)c->decay * (double)(c->num_tokens - 1) > 700.0) return ORA_ERR_INVALID_ARG;
+  if (c->num_tiers != 2 && c->num_tiers != 3) return ORA_ERR_INVALID_ARG;
+  if (c->score_mode < MODE_KVNORM || c->score_mode > MODE_RECENCY) return ORA_ERR_INVALID_ARG;
+  if (c->score_mode == MODE_ATTN) {
+    if (c->num_q_heads < 1 || c->num_q_heads % c->num_kv_heads != 0) return ORA_ERR_INVALID_ARG;
+    if (c->obs_window < 1) return ORA_ERR_INVALID_ARG;
+    if ((c->num_q_heads / c->num_kv_heads) * c->obs_window > 256) return ORA_ERR_INVALID_ARG;
+  }
+  return ORA_OK;
+}
+
+/* Tier counts.  Costs in quarter units: fp16 4, int8 2, int4 1, drop 0, so the
+ * normalized budget b (eq. "budget") becomes the integer B = floor(4 b n). */
+int ora_plan(const ora_config* c, ora_plan_t* p) {
+  int st = ora_validate(c);
+  if (st) return st;
+  int64_t n = c->num_tokens;
+  int64_t s;
+  if (c->num_sink >= 0) s = c->num_sink < n ? c->num_sink : n;
+  else {
+    double want = ceil((double)c->first_ratio * (double)n); /* exact product */
+    s = want < (double)n ? (int64_t)want : n;
+  }
+  int64_t B = (int64_t)floor(4.0 * (double)c->budget * (double)n); /* exact */
+  if (4 * s > B) return ORA_ERR_BUDGET;
+  int64_t m = n - s, R = B - 4 * s;
+  int64_t n16 = 0, n8 = 0, n4 = 0, nd = 0;
+  if (R >= 2 * m) {                       /* b' >= 1/2: f16 = 2b'-1, f8 = 2-2b' */
+    n16 = (R - 2 * m) / 2;
+    n8 = m - n16;
+  } else if (c->num_tiers == 3 && R >= m) { /* 1/4 <= b' < 1/2: f8 = 4b'-1, f4 = 2-4b' */
+    n8 = R - m;
+    n4 = 2 * m - R;
+  } else if (c->num_tiers == 3) {          /* b' < 1/4: int4 first, drop the rest */
+    n4 = R;
+    nd = m - R;
+  } else {                                 /* 2-tier: int8 lowest, drop the rest */
+    n8 = R / 2;
+    nd = m - n8;
+  }
+  if (p) {
+    p->n_sink = (int32_t)s; p->n_fp16 = (int32_t)n16; p->n_int8 = (int32_t)n8;
+    p->n_int4 = (int32_t)n4; p->n_drop = (int32_t)nd;
+    p->budget_units = B;
+    p->used_units = 4 * (s + n16) + 2 * n8 + n4;
+  }
+  return ORA_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Payload geometry (format version 1, little-endian).                         */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+  uint64_t tiermap_off, chunkidx_off, layers_off;
+  uint64_t seg_bytes, seg_stride, scales_bytes, layer_stride, total;
+  int64_t nq, nchunks;
+} ora_geom;
+
+static void geometry(const ora_config* c, const ora_plan_t* p, ora_geom* g) {
+  uint64_t n = (uint64_t)c->num_tokens, d = (uint64_t)c->head_dim, H = (uint64_t)c->num_kv_heads;
+  g->nq = p->n_int8 + p->n_int4;
+  g->nchunks = (int64_t)((n + ORA_CHUNK - 1) / ORA_CHUNK);
+  g->tiermap_off = 256;
+  g->chunkidx_off = g->tiermap_off + up256((n + 3) / 4);
+  g->layers_off = g->chunkidx_off + up256((uint64_t)g->nchunks * 8u);
+  g->seg_bytes = (uint64_t)(p->n_sink + p->n_fp16) * 2 * d + (uint64_t)p->n_int8 * d +
+                 (uint64_t)p->n_int4 * (d / 2);
+  g->seg_stride = up256(g->seg_bytes);
+  g->scales_bytes = up256(2 * H * (uint64_t)g->nq * 4);
+  g->layer_stride = g->scales_bytes + 2 * H * g->seg_stride;
+  g->total = g->layers_off + (uint64_t)c->num_layers * g->layer_stride;
+}
+
+int ora_payload_size(const ora_config* c, uint64_t* bytes) {
+  ora_plan_t p;
+  int st = ora_plan(c, &p);
+  if (st) return st;
+  ora_geom g;
+  geometry(c, &p, &g);
+  *bytes = g.total;
+  return ORA_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Recency factor (Sec. 4.3, eq. "importance"): Delta = n-1-t for 0-based t.   */
+/* which == 1: exp(-lambda*Delta); which == 2: exp(-2*lambda*Delta).           */
+/* ------------------------------------------------------------------------ */
+
+void ora_decay_table(float decay, int which, int32_t count, double* out) {
+  double lam = (double)decay * (which == 2 ? 2.0 : 1.0);
+  for (int32_t dlt = 0; dlt < count; ++dlt) out[dlt] = exp(-(lam * (double)dlt));
+}
+
+/* ------------------------------------------------------------------------ */
+/* Scores (Sec. 4.3).                                                          */
+/* ------------------------------------------------------------------------ */
+
+/* (x * 2^24)^2 as an exact integer for a finite binary16 x; 0 for inf/NaN. */
+static u128 square_units(uint16_t h) {
+  int e = (h >> 10) & 31, m = h & 1023;
+  if (e == 31) return 0;
+  uint64_t mant = e ? (uint64_t)(m + 1024) : (uint64_t)m;
+  int sh = e ? e - 1 : 0;
+  u128 X = (u128)mant << sh;
+  return X * X;
+}
+
+/* Exact S_t = sum over layers, heads, K and V, and channels of x^2, in units
+ * of 2^-48, returned as two 64-bit halves. */
+int ora_sumsq(const ora_config* c, const uint16_t* k, const uint16_t* v, int32_t t,
+              uint64_t* hi, uint64_t* lo) {
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens, d = c->head_dim;
+  u128 S = 0;
+  for (int64_t l = 0; l < L; ++l)
+    for (int64_t h = 0; h < H; ++h) {
+      const uint16_t* kr = k + (((l * H + h) * n + t) * d);
+      const uint16_t* vr = v + (((l * H + h) * n + t) * d);
+      for (int64_t i = 0; i < d; ++i) S += square_units(kr[i]) + square_units(vr[i]);
+    }
+  *hi = (uint64_t)(S >> 64);
+  *lo = (uint64_t)S;
+  return ORA_OK;
+}
+
+/* Mean attention mass of every key over the observation queries of all layers
+ * and query heads (Sec. 3: aggregate over layers, heads and decode
+ * observations; Sec. 4.3: A_j observed or approximated).  Binary64 throughout.
+ * Query head hq reads KV head hq / (Hq/H).  No causal mask: the observation
+ * queries stand for decode steps, which see every prompt token. */
+static void attention_mass(const ora_config* c, const uint16_t* k, const uint16_t* q, double* A) {
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens, d = c->head_dim;
+  int64_t Hq = c->num_q_heads, W = c->obs_window, grp = Hq / H;
+  double inv_sqrt_d = 1.0 / sqrt((double)d);
+  double* z = (double*)malloc((size_t)n * sizeof(double));
+  double* qv = (double*)malloc((size_t)d * sizeof(double));
+  for (int64_t t = 0; t < n; ++t) A[t] = 0.0;
+  for (int64_t l = 0; l < L; ++l)
+    for (int64_t hq = 0; hq < Hq; ++hq) {
+      int64_t h = hq / grp;
+      for (int64_t w = 0; w < W; ++w) {
+        const uint16_t* qr = q + ((l * Hq + hq) * W + w) * d;
+        for (int64_t i = 0; i < d; ++i) qv[i] = ora_half_to_double(qr[i]);
+        double zmax = -INFINITY;
+        for (int64_t t = 0; t < n; ++t) {
+          const uint16_t* kr = k + ((l * H + h) * n + t) * d;
+          double dot = 0.0;
+          for (int64_t i = 0; i < d; ++i) dot += qv[i] * ora_half_to_double(kr[i]);
+          z[t] = dot * inv_sqrt_d;
+          if (z[t] > zmax) zmax = z[t];
+        }
+        double den = 0.0;
+        for (int64_t t = 0; t < n; ++t) { z[t] = exp(z[t] - zmax); den += z[t]; }
+        for (int64_t t = 0; t < n; ++t) A[t] += z[t] / den;
+      }
+    }
+  double count = (double)(L * Hq * W);
+  for (int64_t t = 0; t < n; ++t) A[t] /= count;
+  free(z);
+  free(qv);
+}
+
+/* key[t] for every token.  KV-norm mode ranks by I_t^2 = ||KV_t||^2 e^{-2 lambda Delta}
+ * (same order as I_t = ||KV_t|| e^{-lambda Delta}); attention mode by
+ * A_t e^{-lambda Delta}; recency mode by e^{-lambda Delta} (A = 1). */
+int ora_score(const ora_config* c, const uint16_t* k, const uint16_t* v, const uint16_t* q,
+              double* key) {
+  int st = ora_validate(c);
+  if (st) return st;
+  int32_t n = c->num_tokens;
+  double* w = (double*)malloc((size_t)n * sizeof(double));
+  if (c->score_mode == MODE_KVNORM) {
+    ora_decay_table(c->decay, 2, n, w);
+    for (int32_t t = 0; t < n; ++t) {
+      uint64_t hi, lo;
+      ora_sumsq(c, k, v, t, &hi, &lo);
+      u128 S = ((u128)hi << 64) | lo;
+      double s = ldexp((double)S, -48);  /* one rounding (u128 -> double), exact scaling */
+      key[t] = s * w[n - 1 - t];
+    }
+  } else if (c->score_mode == MODE_ATTN) {
+    if (!q) { free(w); return ORA_ERR_INVALID_ARG; }
+    ora_decay_table(c->decay, 1, n, w);
+    double* A = (double*)malloc((size_t)n * sizeof(double));
+    attention_mass(c, k, q, A);
+    for (int32_t t = 0; t < n; ++t) key[t] = A[t] * w[n - 1 - t];
+    free(A);
+  } else {
+    ora_decay_table(c->decay, 1, n, w);
+    for (int32_t t = 0; t < n; ++t) key[t] = w[n - 1 - t];
+  }
+  free(w);
+  return ORA_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Tier assignment (Sec. 2.3 Prop. 1; Algorithm 1 steps 2-3).                  */
+/* ------------------------------------------------------------------------ */
+
+/* Ranking key: the score's binary64 pattern cut to 32 fraction bits, with the
+ * token index below it, so equal (cut) scores rank the more recent token
+ * higher.  Scores that are NaN or not positive rank as +0. */
+uint64_t ora_composite(double key, int32_t t) {
+  uint64_t bits = 0;
+  if (key > 0.0) memcpy(&bits, &key, 8);
+  return ((bits >> 20) << 21) | (uint64_t)(uint32_t)t;
+}
+
+static int desc_u64(const void* a, const void* b) {
+  uint64_t x = *(const uint64_t*)a, y = *(const uint64_t*)b;
+  return x < y ? 1 : (x > y ? -1 : 0);
+}
+
+int ora_assign(const ora_config* c, const double* key, uint8_t* tier) {
+  ora_plan_t p;
+  int st = ora_plan(c, &p);
+  if (st) return st;
+  int32_t n = c->num_tokens, s = p.n_sink, m = n - s;
+  for (int32_t t = 0; t < s; ++t) tier[t] = T_FP16; /* sinks pinned before ranking */
+  uint64_t* cs = (uint64_t*)malloc((size_t)(m > 0 ? m : 1) * sizeof(uint64_t));
+  for (int32_t t = s; t < n; ++t) cs[t - s] = ora_composite(key[t], t);
+  qsort(cs, (size_t)m, sizeof(uint64_t), desc_u64);
+  for (int32_t r = 0; r < m; ++r) {
+    int32_t t = (int32_t)(cs[r] & ((1u << 21) - 1));
+    uint8_t tr;
+    if (r < p.n_fp16) tr = T_FP16;
+    else if (r < p.n_fp16 + p.n_int8) tr = T_INT8;
+    else if (r < p.n_fp16 + p.n_int8 + p.n_int4) tr = T_INT4;
+    else tr = T_DROP;
+    tier[t] = tr;
+  }
+  free(cs);
+  return ORA_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Row offsets and row codec.                                                  */
+/* ------------------------------------------------------------------------ */
+
+static int width_units(int tr) { return tr == T_FP16 ? 4 : tr == T_INT8 ? 2 : tr == T_INT4 ? 1 : 0; }
+
+/* units[t] = sum over u < t of the row width in units of d/2 bytes;
+ * qrank[t] = number of quantized (int8/int4) rows before t. */
+void ora_offsets(int32_t n, const uint8_t* tier, uint32_t* units, uint32_t* qrank) {
+  uint32_t u = 0, q = 0;
+  for (int32_t t = 0; t < n; ++t) {
+    units[t] = u;
+    qrank[t] = q;
+    u += (uint32_t)width_units(tier[t]);
+    q += (tier[t] == T_INT8 || tier[t] == T_INT4);
+  }
+}
+
+/* Symmetric per-row absmax quantizer ("standard symmetric", Sec. 8).  Writes
+ * the row's payload bytes to out and its scale to *scale; returns 1 if the
+ * row holds a non-finite element (scale NaN, codes zero), else 0. */
+int ora_encode_row(int tr, int32_t d, const uint16_t* x, uint8_t* out, float* scale) {
+  if (tr == T_FP16) {
+    for (int32_t i = 0; i < d; ++i) { out[2 * i] = (uint8_t)x[i]; out[2 * i + 1] = (uint8_t)(x[i] >> 8); }
+    return 0;
+  }
+  if (tr == T_DROP) return 0;
+  const int Q = tr == T_INT8 ? 127 : 7;
+  uint16_t amax = 0;
+  for (int32_t i = 0; i < d; ++i) {
+    uint16_t mag = x[i] & 0x7FFF;
+    if (mag > amax) amax = mag;
+  }
+  int32_t codes[256];
+  int bad = 0;
+  if (amax >= 0x7C00) {                 /* inf or NaN somewhere in the row */
+    uint32_t nanbits = 0x7FC00000u;
+    memcpy(scale, &nanbits, 4);
+    for (int32_t i = 0; i < d; ++i) codes[i] = 0;
+    bad = 1;
+  } else if (amax == 0) {
+    *scale = 0.0f;
+    for (int32_t i = 0; i < d; ++i) codes[i] = 0;
+  } else {
+    float a = half_to_float(amax);
+    *scale = a / (float)Q;
+    float r = (float)Q / a;
+    for (int32_t i = 0; i < d; ++i) {
+      float y = half_to_float(x[i]) * r;
+      float c = nearbyintf(y);
+      if (c > (float)Q) c = (float)Q;
+      if (c < (float)-Q) c = (float)-Q;
+      codes[i] = (int32_t)c;
+    }
+  }
+  if (tr == T_INT8) {
+    for (int32_t i = 0; i < d; ++i) out[i] = (uint8_t)(codes[i] & 0xFF);
+  } else {
+    for (int32_t i = 0; i < d / 2; ++i)
+      out[i] = (uint8_t)((codes[2 * i] & 0xF) | ((codes[2 * i + 1] & 0xF) << 4));
+  }
+  return bad;
+}
+
+/* Inverse of ora_encode_row: fp16 bits of the reconstructed row. */
+void ora_decode_row(int tr, int32_t d, const uint8_t* in, float scale, uint16_t* y) {
+  if (tr == T_FP16) {
+    for (int32_t i = 0; i < d; ++i) y[i] = (uint16_t)(in[2 * i] | (in[2 * i + 1] << 8));
+    return;
+  }
+  if (tr == T_DROP) {
+    for (int32_t i = 0; i < d; ++i) y[i] = 0;
+    return;
+  }
+  if (isnan(scale)) {
+    for (int32_t i = 0; i < d; ++i) y[i] = 0x7E00;
+    return;
+  }
+  for (int32_t i = 0; i < d; ++i) {
+    int32_t code;
+    if (tr == T_INT8) code = (int32_t)(int8_t)in[i];
+    else {
+      int32_t nib = (in[i / 2] >> (4 * (i & 1))) & 0xF;
+      code = nib >= 8 ? nib - 16 : nib;
+    }
+    y[i] = ora_float_to_half((float)code * scale);
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Payload writer (Algorithm 1 step 4) and reader (decode side, Sec. 4.2).     */
+/* ------------------------------------------------------------------------ */
+
+static void put32(uint8_t* p, uint32_t v) { memcpy(p, &v, 4); }
+static void put64(uint8_t* p, uint64_t v) { memcpy(p, &v, 8); }
+static uint32_t get32(const uint8_t* p) { uint32_t v; memcpy(&v, p, 4); return v; }
+static uint32_t fbits(float f) { uint32_t v; memcpy(&v, &f, 4); return v; }
+
+static void write_header(const ora_config* c, const ora_plan_t* p, const ora_geom* g, uint8_t* h) {
+  memset(h, 0, 256);
+  put32(h + 0, ORA_MAGIC);
+  put32(h + 4, ORA_VERSION);
+  put32(h + 8, (uint32_t)c->num_layers);
+  put32(h + 12, (uint32_t)c->num_kv_heads);
+  put32(h + 16, (uint32_t)c->head_dim);
+  put32(h + 20, (uint32_t)c->num_tokens);
+  put32(h + 24, (uint32_t)p->n_sink);
+  put32(h + 28, (uint32_t)c->num_tiers);
+  put32(h + 32, fbits(c->budget));
+  put32(h + 36, fbits(c->first_ratio));
+  put32(h + 40, fbits(c->decay));
+  put32(h + 44, (uint32_t)c->score_mode);
+  put32(h + 48, (uint32_t)p->n_fp16);
+  put32(h + 52, (uint32_t)p->n_int8);
+  put32(h + 56, (uint32_t)p->n_int4);
+  put32(h + 60, (uint32_t)p->n_drop);
+  put64(h + 64, (uint64_t)p->budget_units);
+  put64(h + 72, (uint64_t)p->used_units);
+  put64(h + 80, g->tiermap_off);
+  put64(h + 88, g->chunkidx_off);
+  put64(h + 96, g->layers_off);
+  put64(h + 104, g->seg_bytes);
+  put64(h + 112, g->seg_stride);
+  put64(h + 120, g->scales_bytes);
+  put64(h + 128, g->layer_stride);
+  put64(h + 136, g->total);
+  put32(h + 144, 0);             /* non-finite quantized rows */
+  put32(h + 148, 0);             /* status */
+  put32(h + 152, ORA_CHUNK);
+}
+
+int ora_pack(const ora_config* c, const uint16_t* k, const uint16_t* v, const uint8_t* tier,
+             uint8_t* payload, uint64_t capacity) {
+  ora_plan_t p;
+  int st = ora_plan(c, &p);
+  if (st) return st;
+  ora_geom g;
+  geometry(c, &p, &g);
+  if (capacity < g.total) return ORA_ERR_CAPACITY;
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens, d = c->head_dim;
+  /* The tier map must carry exactly the planned counts (sizes depend on them). */
+  int64_t cnt[4] = {0, 0, 0, 0};
+  for (int64_t t = 0; t < n; ++t) {
+    if (tier[t] > 3) return ORA_ERR_INVALID_ARG;
+    cnt[tier[t]]++;
+  }
+  if (cnt[T_FP16] != p.n_sink + p.n_fp16 || cnt[T_INT8] != p.n_int8 ||
+      cnt[T_INT4] != p.n_int4 || cnt[T_DROP] != p.n_drop)
+    return ORA_ERR_INVALID_ARG;
+
+  memset(payload, 0, g.total);
+  write_header(c, &p, &g, payload);
+  for (int64_t t = 0; t < n; ++t)
+    payload[g.tiermap_off + (uint64_t)t / 4] |= (uint8_t)(tier[t] << (2 * (t % 4)));
+  uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
+  uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
+  ora_offsets((int32_t)n, tier, units, qrank);
+  for (int64_t ch = 0; ch < g.nchunks; ++ch) {
+    put32(payload + g.chunkidx_off + 8 * ch, units[ch * ORA_CHUNK]);
+    put32(payload + g.chunkidx_off + 8 * ch + 4, qrank[ch * ORA_CHUNK]);
+  }
+  uint32_t nonfinite = 0;
+  uint64_t rowunit = (uint64_t)d / 2;
+  for (int64_t l = 0; l < L; ++l) {
+    uint8_t* lb = payload + g.layers_off + (uint64_t)l * g.layer_stride;
+    for (int kv = 0; kv < 2; ++kv)
+      for (int64_t h = 0; h < H; ++h) {
+        const uint16_t* src = (kv == 0 ? k : v) + ((l * H + h) * n) * d;
+        uint8_t* seg = lb + g.scales_bytes + (uint64_t)(kv * H + h) * g.seg_stride;
+        uint8_t* sc = lb + (uint64_t)(kv * H + h) * (uint64_t)g.nq * 4;
+        for (int64_t t = 0; t < n; ++t) {
+          float scale = 0.0f;
+          int bad = ora_encode_row(tier[t], (int32_t)d, src + t * d, seg + units[t] * rowunit, &scale);
+          if (tier[t] == T_INT8 || tier[t] == T_INT4) {
+            put32(sc + 4 * (uint64_t)qrank[t], fbits(scale));
+            nonfinite += (uint32_t)bad;
+          }
+        }
+      }
+  }
+  put32(payload + 144, nonfinite);
+  free(units);
+  free(qrank);
+  return ORA_OK;
+}
+
+/* Checks a payload header against the configuration. */
+int ora_check_header(const ora_config* c, const uint8_t* payload, uint64_t bytes) {
+  ora_plan_t p;
+  int st = ora_plan(c, &p);
+  if (st) return st;
+  ora_geom g;
+  geometry(c, &p, &g);
+  if (bytes < 256) return ORA_ERR_FORMAT;
+  uint8_t want[256];
+  write_header(c, &p, &g, want);
+  /* every field but the non-finite row count must match exactly */
+  if (memcmp(want, payload, 144) != 0) return ORA_ERR_FORMAT;
+  if (get32(payload + 148) != 0) return ORA_ERR_FORMAT;
+  if (memcmp(want + 152, payload + 152, 256 - 152) != 0) return ORA_ERR_FORMAT;
+  if (bytes < g.total) return ORA_ERR_FORMAT;
+  return ORA_OK;
+}
+
+int ora_unpack(const ora_config* c, const uint8_t* payload, uint64_t bytes, uint16_t* kc,
+               uint16_t* vc, const int32_t* block_table, int32_t num_blocks, int32_t block_size) {
+  int st = ora_check_header(c, payload, bytes);
+  if (st) return st;
+  if (block_size < 1 || num_blocks < 1) return ORA_ERR_INVALID_ARG;
+  ora_plan_t p;
+  ora_plan(c, &p);
+  ora_geom g;
+  geometry(c, &p, &g);
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens, d = c->head_dim;
+  uint8_t* tier = (uint8_t*)malloc((size_t)n);
+  int64_t cnt[4] = {0, 0, 0, 0};
+  for (int64_t t = 0; t < n; ++t) {
+    tier[t] = (payload[g.tiermap_off + (uint64_t)t / 4] >> (2 * (t % 4))) & 3;
+    cnt[tier[t]]++;
+  }
+  uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
+  uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
+  ora_offsets((int32_t)n, tier, units, qrank);
+  int bad = cnt[T_FP16] != p.n_sink + p.n_fp16 || cnt[T_INT8] != p.n_int8 ||
+            cnt[T_INT4] != p.n_int4 || cnt[T_DROP] != p.n_drop;
+  for (int64_t ch = 0; ch < g.nchunks && !bad; ++ch)
+    bad = get32(payload + g.chunkidx_off + 8 * ch) != units[ch * ORA_CHUNK] ||
+          get32(payload + g.chunkidx_off + 8 * ch + 4) != qrank[ch * ORA_CHUNK];
+  for (int64_t t = 0; t < (n + block_size - 1) / block_size && !bad; ++t)
+    bad = block_table[t] < 0 || block_table[t] >= num_blocks;
+  if (bad) {
+    free(tier); free(units); free(qrank);
+    return ORA_ERR_FORMAT;
+  }
+  uint64_t rowunit = (uint64_t)d / 2;
+  for (int64_t l = 0; l < L; ++l) {
+    const uint8_t* lb = payload + g.layers_off + (uint64_t)l * g.layer_stride;
+    for (int kv = 0; kv < 2; ++kv)
+      for (int64_t h = 0; h < H; ++h) {
+        const uint8_t* seg = lb + g.scales_bytes + (uint64_t)(kv * H + h) * g.seg_stride;
+        const uint8_t* sc = lb + (uint64_t)(kv * H + h) * (uint64_t)g.nq * 4;
+        uint16_t* cache = kv == 0 ? kc : vc;
+        for (int64_t t = 0; t < n; ++t) {
+          float scale = 0.0f;
+          if (tier[t] == T_INT8 || tier[t] == T_INT4) {
+            uint32_t b = get32(sc + 4 * (uint64_t)qrank[t]);
+            memcpy(&scale, &b, 4);
+          }
+          int64_t blk = block_table[t / block_size], slot = t % block_size;
+          uint16_t* dst = cache + (((l * num_blocks + blk) * block_size + slot) * H + h) * d;
+          ora_decode_row(tier[t], (int32_t)d, seg + units[t] * rowunit, scale, dst);
+        }
+      }
+  }
+  free(tier); free(units); free(qrank);
+  return ORA_OK;
+}
