@@ -1,0 +1,171 @@
+"""Benchmark of the KV transfer codec on one MI355X.
+
+One step = the whole hot path on one request: score (KV-norm x decay) ->
+assign tiers -> pack -> emulated link (device-to-device copy of the payload)
+-> unpack into the paged fp16 cache.  Inputs are resident in HBM before the
+timed region.  The reported metric is the paper-shaped codec throughput:
+fp16-equivalent bytes F = 4 L H d n per (pack + unpack) second.  Per-stage
+times come from HIP events recorded on the stream the library launches on.
+
+Prints one JSON line (see the keys below); with --gpus N > 1 it exits with a
+message, since the codec is measured on one GPU.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "KV codec GB/s (fp16-equivalent in, pack+unpack) and % of HBM peak, 7B-shape 32k"
+HBM_PEAK_GBS = 8000.0
+
+
+def algorithmic_bytes(w, plan, payload_bytes, block_size):
+    """Bytes the method must move per launch of pack and of unpack."""
+    L, H, d, n = w.layers, w.kv_heads, w.head_dim, w.tokens
+    row = 2 * d  # bytes of one fp16 row
+    kept = n - plan["n_drop"]
+    pack = 2 * L * H * kept * row + n + payload_bytes  # read kept K/V rows + tier map, write payload
+    unpack = payload_bytes + 4 * (-(-n // block_size)) + 2 * L * H * n * row  # read payload + table, write cache
+    return pack, unpack
+
+
+def cpu_baseline(w, layers: int):
+    """The oracle's pack + unpack, single-threaded, on the first `layers` layers
+    of the same request shape; GB/s of fp16-equivalent input like the metric."""
+    import numpy as np
+
+    import oracle
+    from paper_2606_08635_amd import workloads
+
+    n, H, d, bs = w.tokens, w.kv_heads, w.head_dim, 16
+    k, v = workloads.make_kv(layers, H, n, d, seed=0, outliers=w.outliers, device="cuda")
+    kh, vh = k.cpu().numpy().view(np.uint16), v.cpu().numpy().view(np.uint16)
+    ocfg = oracle.config(layers, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay,
+                         num_tiers=w.num_tiers)
+    tier = oracle.assign(ocfg, oracle.score(ocfg, kh, vh))
+    nb = workloads.blocks_for(n, bs)
+    bt = workloads.make_block_table(n, bs, nb, seed=0).numpy()
+    kc = np.zeros((layers, nb, bs, H, d), np.uint16)
+    vc = np.zeros_like(kc)
+    t0 = time.perf_counter()
+    payload = oracle.pack(ocfg, kh, vh, tier)
+    t1 = time.perf_counter()
+    st = oracle.unpack(ocfg, payload, kc, vc, bt, bs)
+    t2 = time.perf_counter()
+    assert st == oracle.OK
+    f16 = 4 * layers * H * d * n
+    return {"value": round(f16 / (t2 - t0) / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{layers} of {w.layers} layers of the {w.name} request ({f16 / 2**20:.0f} MiB fp16 K+V); "
+                      f"pack {t1 - t0:.2f} s, unpack {t2 - t1:.2f} s, single thread"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mistral7b_32k")
+    ap.add_argument("--cpu-layers", type=int, default=4, help="layers in the CPU-baseline sample (0: skip)")
+    ap.add_argument("--link", choices=["d2d", "host"], default="d2d")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures the codec on one GPU; --gpus {args.gpus} is not supported "
+              "(the codec has no multi-GPU path to time)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2606_08635_amd import skv, workloads
+
+    w = workloads.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    L, H, d, n, bs = w.layers, w.kv_heads, w.head_dim, w.tokens, 16
+    cfg = skv.config(L, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers)
+    codec = skv.Codec(cfg, dev)
+    k, v = workloads.make_kv(L, H, n, d, seed=0, outliers=w.outliers, device=dev)
+    nb = workloads.blocks_for(n, bs)
+    bt = workloads.make_block_table(n, bs, nb, seed=0, device=dev)
+    kc = torch.empty(L, nb, bs, H, d, dtype=torch.float16, device=dev)
+    vc = torch.empty_like(kc)
+    rx = torch.empty_like(codec.payload)
+    staging = torch.empty(codec.payload_bytes, dtype=torch.uint8, pin_memory=True) if args.link == "host" else None
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    def step(ev=None):
+        if ev: ev[0].record(stream)
+        skv.score(cfg, k, v, None, codec.scores, codec.ws)
+        if ev: ev[1].record(stream)
+        skv.assign_tiers(cfg, codec.scores, codec.tier)
+        if ev: ev[2].record(stream)
+        skv.pack(cfg, k, v, codec.tier, codec.payload, codec.status[0:1])
+        if ev: ev[3].record(stream)
+        skv.link(rx, codec.payload, codec.payload_bytes, staging)
+        if ev: ev[4].record(stream)
+        skv.unpack(cfg, rx, kc, vc, bt, bs, codec.status[1:2])
+        if ev: ev[5].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    status = codec.status.cpu().tolist()
+    if status != [0, 0]:
+        raise RuntimeError(f"codec reported status {status}")
+
+    names = ["score", "assign", "pack", "link", "unpack"]
+    stage_ms = {nm: sum(e[i].elapsed_time(e[i + 1]) for e in events) / args.steps for i, nm in enumerate(names)}
+    F = w.fp16_bytes
+    t_codec = (stage_ms["pack"] + stage_ms["unpack"]) / 1e3
+    pack_b, unpack_b = algorithmic_bytes(w, codec.plan, codec.payload_bytes, bs)
+    pack_gbs = pack_b / (stage_ms["pack"] / 1e3) / 1e9
+    unpack_gbs = unpack_b / (stage_ms["unpack"] / 1e3) / 1e9
+    dominant = "pack" if stage_ms["pack"] >= stage_ms["unpack"] else "unpack"
+    dom_bytes, dom_gbs = (pack_b, pack_gbs) if dominant == "pack" else (unpack_b, unpack_gbs)
+    alg_gbs = (pack_b + unpack_b) / t_codec / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(F / t_codec / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "layers": L, "kv_heads": H, "head_dim": d, "tokens": n,
+                   "budget": w.budget, "num_tiers": w.num_tiers, "first_ratio": w.first_ratio, "decay": w.decay,
+                   "score": "kvnorm", "block_size": bs, "link": args.link, "fp16_bytes": F,
+                   "payload_bytes": codec.payload_bytes},
+        "tokens_per_s": round(n / t_codec, 1),
+        "alg_gbps": round(alg_gbs, 2),
+        "pct_hbm_peak": round(100 * alg_gbs / HBM_PEAK_GBS, 2),
+        "stages_ms": {kk: round(vv, 4) for kk, vv in stage_ms.items()},
+        "pack_gbps": round(pack_gbs, 2),
+        "unpack_gbps": round(unpack_gbs, 2),
+        "roofline": {"bound": "hbm", "kernel": f"skv_{dominant}", "achieved": round(dom_gbs, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": dom_bytes},
+    }
+    if args.cpu_layers > 0:
+        del kc, vc, rx
+        torch.cuda.empty_cache()
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

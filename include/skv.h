@@ -1,0 +1,222 @@
+/*
+ * skv.h -- C ABI of the SpectrumKV per-token mixed-precision KV transfer codec
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The codec follows "SpectrumKV: Per-Token Mixed-Precision KV Cache Transfer
+ * for Prefill-Decode Disaggregated LLM Serving" (arXiv 2606.08635): on the
+ * prefill side it scores every prompt token (Sec. 4.3), pins the sink prefix
+ * and assigns each remaining token FP16, INT8 or INT4 (or drops it) by
+ * importance under a normalized byte budget (Sec. 2.1, Sec. 4.4, Algorithm 1
+ * steps 2-3), then quantizes K and V independently per tier into one
+ * compacted payload (Algorithm 1 step 4).  On the decode side it dequantizes
+ * the payload into an fp16 paged KV cache (Sec. 4.2, Fig. "sysarch").
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers named k, v, q_obs, score, tier, payload, k_cache, v_cache,
+ *    block_table, ws and dev_status are HIP device pointers (for example
+ *    torch tensors' data_ptr()).  They must be 16-byte aligned.  The caller
+ *    owns every buffer; the library allocates no device memory and keeps no
+ *    global state, so calls on different streams with different buffers are
+ *    independent.  Calls that share a buffer must be ordered by the caller.
+ *  - Device entry points only enqueue work on `stream` and never synchronize
+ *    with the host (skv_prepare is the one exception, see there).  A null
+ *    stream means the legacy default stream.
+ *  - Argument errors are detected on the host before anything is enqueued and
+ *    returned as a status.  Data-dependent problems (a payload that does not
+ *    match the configuration, out-of-range block-table entries, non-finite
+ *    inputs) are reported in device memory, without a host sync.
+ *  - K and V layout: binary16, [L][H][n][d] contiguous (layer, KV head, token,
+ *    channel).  Observation queries: binary16 [L][Hq][W][d].
+ *  - Paged cache layout: binary16 [L][num_blocks][block_size][H][d] for K and
+ *    for V; token t of the request lives in physical block block_table[t /
+ *    block_size], slot t % block_size.
+ *
+ * Payload format (version 1, little-endian, every section 256-byte aligned):
+ *   [header 256 B]
+ *   [tier map: 2 bits per token, token t in bits 2(t%4).. of byte t/4]
+ *   [chunk index: per 256-token chunk c, u32 row-width units and u32 quantized
+ *    rows before token 256c]
+ *   [layer 0][layer 1]...[layer L-1], each layer =
+ *     [fp32 scales: for K then V, for each head, one per quantized token in
+ *      token order][data: for K then V, for each head, one segment holding the
+ *      token rows in token order, FP16 rows 2d bytes, INT8 rows d bytes
+ *      (two's complement), INT4 rows d/2 bytes (element 2i in the low nibble
+ *      of byte i), DROP rows absent; segments padded to 256 B]
+ *   Header fields (byte offset: type): 0 u32 magic 0x31564B53 ("SKV1"),
+ *   4 u32 version, 8..20 i32 L, H, d, n, 24 i32 sinks, 28 i32 num_tiers,
+ *   32/36/40 f32 bits of budget, first_ratio, decay, 44 i32 score_mode,
+ *   48..60 i32 non-sink FP16 / INT8 / INT4 / DROP counts, 64/72 u64 budget and
+ *   used quarter-units, 80/88/96 u64 offsets of tier map, chunk index and
+ *   layer 0, 104 u64 segment bytes, 112 u64 segment stride, 120 u64 scale
+ *   section bytes per layer, 128 u64 layer stride, 136 u64 total bytes,
+ *   144 u32 quantized rows holding a non-finite value, 148 u32 pack status,
+ *   152 u32 tokens per chunk (256); all other bytes zero.
+ */
+#ifndef SKV_H_
+#define SKV_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SKV_ABI_VERSION 1
+
+typedef enum skv_status {
+  SKV_OK = 0,
+  SKV_ERR_INVALID_ARG = 1, /* bad shape, range, pointer or alignment           */
+  SKV_ERR_BUDGET = 2,      /* the sinks alone exceed the budget (4s > floor(4bn)) */
+  SKV_ERR_CAPACITY = 3,    /* output buffer smaller than skv_payload_size       */
+  SKV_ERR_FORMAT = 4,      /* payload_bytes too small for the configuration     */
+  SKV_ERR_DEVICE = 5       /* a HIP call or kernel launch failed                */
+} skv_status;
+
+/* Tier codes of the precision map (Sec. 2.1: c(16)=1, c(8)=1/2, c(4)=1/4;
+ * a dropped token costs 0, the selection view of Sec. 2.1). */
+enum { SKV_TIER_FP16 = 0, SKV_TIER_INT8 = 1, SKV_TIER_INT4 = 2, SKV_TIER_DROP = 3 };
+
+/* Importance statistic A_j of I_j = A_j exp(-lambda Delta_j) (Sec. 4.3). */
+enum {
+  SKV_SCORE_KVNORM = 0,  /* KV-norm fallback: squared Frobenius norm of the token's
+                            K and V over every layer and head, times
+                            exp(-2 lambda Delta) (the square of I_j, same order)  */
+  SKV_SCORE_ATTN = 1,    /* mean softmax mass from an observation window of
+                            queries, aggregated over layers and heads (Sec. 3)  */
+  SKV_SCORE_RECENCY = 2  /* A_j = 1: the recency factor alone                     */
+};
+
+/* Problem statement (Sec. 2.1, Sec. 4.3-4.5).  All fields are read, never
+ * written.  Validity: 1 <= L, H; L*H <= 65536; d in {32, 64, 128, 256};
+ * 1 <= n <= 2^21; 0 < budget <= 1; 0 <= first_ratio <= 1; num_sink >= -1;
+ * decay >= 0 and finite with 2*decay*(n-1) <= 700; num_tiers in {2, 3};
+ * attention mode: num_q_heads a multiple of H, obs_window >= 1 and
+ * (num_q_heads / H) * obs_window <= 256. */
+typedef struct skv_config {
+  int32_t num_layers;   /* L                                                      */
+  int32_t num_kv_heads; /* H (KV heads)                                           */
+  int32_t head_dim;     /* d                                                      */
+  int32_t num_tokens;   /* n (prompt length)                                      */
+  float budget;         /* b, normalized transfer budget, eq. "budget"            */
+  float first_ratio;    /* rho: sinks s = ceil(rho * n) when num_sink == -1       */
+  int32_t num_sink;     /* -1: use first_ratio; >= 0: explicit sink count (<= n)  */
+  float decay;          /* lambda of exp(-lambda Delta), Delta = n-1-t            */
+  int32_t num_tiers;    /* 3: FP16+INT8+INT4; 2: FP16+INT8 (INT4 disabled by the
+                           tolerance probe, Sec. 4.5)                             */
+  int32_t score_mode;   /* SKV_SCORE_*                                            */
+  int32_t num_q_heads;  /* attention mode: query heads Hq (grouped, Hq/H per KV)  */
+  int32_t obs_window;   /* attention mode: W observation queries per query head  */
+} skv_config;
+
+/* Tier counts of a configuration.  n_fp16/n_int8/n_int4/n_drop count the
+ * non-sink tokens; the n_sink sink tokens are FP16 as well.  Budget in
+ * quarter-units: budget_units = floor(4 b n), used_units = 4(n_sink + n_fp16)
+ * + 2 n_int8 + n_int4 <= budget_units. */
+typedef struct skv_plan {
+  int32_t n_sink, n_fp16, n_int8, n_int4, n_drop;
+  int64_t budget_units, used_units;
+} skv_plan;
+
+/* ABI version of the loaded library (SKV_ABI_VERSION at build time). */
+int32_t skv_abi_version(void);
+
+/* Human-readable name of a status code; never NULL. */
+const char* skv_status_string(skv_status status);
+
+/* Host only, pure.  Tier counts for cfg: sinks pinned first and charged to the
+ * budget (Sec. 4.4), then the budget-to-tier mapping of Sec. 4.4 over the
+ * remaining budget: b' >= 1/2 -> FP16 + INT8 (f16 = 2b'-1); 3-tier with
+ * 1/4 <= b' < 1/2 -> INT8 + INT4 (f8 = 4b'-1); 3-tier below 1/4 -> INT4 +
+ * DROP; 2-tier below 1/2 -> INT8 + DROP (Sec. 7.4.3).  Returns
+ * SKV_ERR_INVALID_ARG for an invalid cfg or null out, SKV_ERR_BUDGET when the
+ * sinks alone exceed the budget. */
+skv_status skv_plan_tiers(const skv_config* cfg, skv_plan* out);
+
+/* Host only.  Exact payload size in bytes for cfg (known before any scoring,
+ * because the tier counts depend only on cfg). */
+skv_status skv_payload_size(const skv_config* cfg, uint64_t* bytes);
+
+/* Host only.  Device workspace bytes needed by skv_prepare, skv_score and
+ * skv_assign_tiers for cfg (the decay table plus scratch). */
+skv_status skv_workspace_size(const skv_config* cfg, uint64_t* bytes);
+
+/* Fills the decay table exp(-lambda Delta) (attention and recency modes) or
+ * exp(-2 lambda Delta) (KV-norm mode), Delta = 0..n-1, at the start of ws.
+ * The table is evaluated on the host in binary64 with the C library's exp and
+ * copied to ws with a stream-ordered copy; this call waits for that copy
+ * before returning.  The table depends only on (decay, n, score_mode), so a
+ * workspace prepared once serves any number of skv_score calls with the same
+ * three values.  Sec. 4.3, eq. "importance". */
+skv_status skv_prepare(const skv_config* cfg, void* ws, hipStream_t stream);
+
+/* Scores every token (Sec. 4.3; Algorithm 1 step 2).  k, v: [L][H][n][d]
+ * binary16; q_obs: [L][Hq][W][d] binary16 in attention mode, else ignored;
+ * score: double[n], written.  ws must be prepared for cfg by skv_prepare.
+ * KV-norm mode: score[t] = RN64(RN64(S_t) * exp(-2 lambda (n-1-t))), S_t the
+ * exact sum of squares of token t's finite K and V elements over all layers
+ * and heads (non-finite elements contribute 0); the result is bit-exact.
+ * Attention mode: score[t] = A_t exp(-lambda (n-1-t)), A_t the mean over
+ * (layer, query head, observation query) of softmax over all n keys of
+ * q.k/sqrt(d), query head hq reading KV head hq/(Hq/H); fp32 MFMA logits, so
+ * within a stated relative tolerance of the binary64 definition.  Recency
+ * mode: score[t] = exp(-lambda (n-1-t)). */
+skv_status skv_score(const skv_config* cfg, const void* k, const void* v, const void* q_obs,
+                     double* score, void* ws, hipStream_t stream);
+
+/* Assigns tiers (Sec. 2.3 Prop. 1; Algorithm 1 steps 2-3).  score: double[n]
+ * (any values; NaN and non-positive scores rank as +0); tier: uint8[n],
+ * written.  Tokens t < n_sink get FP16.  The other tokens are ranked by
+ * descending composite key ((bits(score) >> 20) << 21) | t, i.e. by score cut
+ * to 32 fraction bits with ties going to the more recent token, and the first
+ * n_fp16 get FP16, the next n_int8 INT8, the next n_int4 INT4, the rest DROP.
+ * One workgroup, radix select; ws is not used and may be NULL. */
+skv_status skv_assign_tiers(const skv_config* cfg, const double* score, uint8_t* tier, void* ws,
+                            hipStream_t stream);
+
+/* Quantizes K and V per tier and packs the payload (Algorithm 1 step 4;
+ * "standard symmetric" quantizer, Sec. 8).  tier: uint8[n] whose counts must
+ * equal skv_plan_tiers(cfg) (sinks included in FP16).  payload: capacity bytes,
+ * at least skv_payload_size(cfg); exactly that many bytes are written.
+ * Per INT8/INT4 row (one row = one layer, K or V, head, token; Q = 127 / 7):
+ * a = max |x| (binary16), scale = RN32(a/Q), r = RN32(Q/a),
+ * code = clamp(rne(RN32(x r)), -Q, Q); a row with a non-finite element gets a
+ * NaN scale and zero codes and is counted in header field 144; an all-zero
+ * row gets scale 0.  FP16 rows are copied bit for bit.
+ * If the tier map is off plan (a value > 3 or wrong counts) the header status
+ * field is set to SKV_ERR_INVALID_ARG and nothing else is written.
+ * dev_status (may be NULL): receives the same status (0 on success). */
+skv_status skv_pack(const skv_config* cfg, const void* k, const void* v, const uint8_t* tier,
+                    void* payload, uint64_t capacity, uint32_t* dev_status, hipStream_t stream);
+
+/* Dequantizes a payload into the paged fp16 cache (Sec. 4.2: dequantize per
+ * tier after receipt).  INT8/INT4 elements become RN16(RN32(code * scale));
+ * FP16 rows are copied bit for bit; DROP rows are written as +0 (the consumer
+ * masks them, Sec. 5 "data hygiene"); elements of a row with a NaN scale are
+ * written as 0x7E00.  Cache slots of tokens >= n are not touched.
+ * block_table: int32[ceil(n / block_size)], each in [0, num_blocks);
+ * block_size >= 1.  dev_status (required): set to 0 on success or to
+ * SKV_ERR_FORMAT when the header, tier counts or chunk index disagree with cfg
+ * or a block-table entry is out of range; in that case nothing is written.
+ * Returns SKV_ERR_FORMAT (host-side) when payload_bytes is below
+ * skv_payload_size(cfg). */
+skv_status skv_unpack(const skv_config* cfg, const void* payload, uint64_t payload_bytes,
+                      void* k_cache, void* v_cache, const int32_t* block_table, int32_t num_blocks,
+                      int32_t block_size, uint32_t* dev_status, hipStream_t stream);
+
+/* Link emulation for a one-GPU setup (Sec. 4.2: the payload crosses the
+ * network between prefill and decode).  Copies `bytes` from src to dst on
+ * stream: device to device when host_staging is NULL, otherwise device to
+ * pinned host (host_staging, at least `bytes`, allocated with hipHostMalloc)
+ * and back to device. */
+skv_status skv_link(void* dst, const void* src, uint64_t bytes, void* host_staging,
+                    hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SKV_H_ */

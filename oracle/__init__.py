@@ -65,6 +65,8 @@ def _load():
         "ora_decode_row": (None, [ctypes.c_int, ctypes.c_int32, vp, ctypes.c_float, vp]),
         "ora_pack": (ctypes.c_int, [cfgp, vp, vp, vp, vp, ctypes.c_uint64]),
         "ora_check_header": (ctypes.c_int, [cfgp, vp, ctypes.c_uint64]),
+        "ora_geometry": (ctypes.c_int, [cfgp, vp]),
+        "ora_pack_meta": (ctypes.c_int, [cfgp, vp, vp, ctypes.c_uint64]),
         "ora_unpack": (ctypes.c_int, [cfgp, vp, ctypes.c_uint64, vp, vp, vp, ctypes.c_int32, ctypes.c_int32]),
         "ora_half_to_double": (ctypes.c_double, [ctypes.c_uint16]),
         "ora_float_to_half": (ctypes.c_uint16, [ctypes.c_float]),
@@ -193,6 +195,41 @@ def pack(cfg, k, v, tier):
     if st:
         raise OracleError(st, "pack")
     return out
+
+
+GEOMETRY_FIELDS = ("tiermap_off", "chunkidx_off", "layers_off", "seg_bytes", "seg_stride",
+                   "scales_bytes", "layer_stride", "total", "nq")
+
+
+def geometry(cfg):
+    out = np.zeros(len(GEOMETRY_FIELDS), np.uint64)
+    st = _lib.ora_geometry(ctypes.byref(cfg), _ptr(out))
+    if st:
+        raise OracleError(st, "geometry")
+    return {f: int(x) for f, x in zip(GEOMETRY_FIELDS, out)}
+
+
+def pack_meta(cfg, tier):
+    """Header, tier map and chunk index: the payload bytes before layer 0."""
+    tier = np.ascontiguousarray(tier, np.uint8)
+    size = geometry(cfg)["layers_off"]
+    out = np.empty(size, np.uint8)
+    st = _lib.ora_pack_meta(ctypes.byref(cfg), _ptr(tier), _ptr(out), size)
+    if st:
+        raise OracleError(st, "pack_meta")
+    return out
+
+
+def row_offset(cfg, geo, units, l, kv, h, t):
+    """Byte offset of row (layer l, K/V kv, head h, token t) in the payload."""
+    H, d = cfg.num_kv_heads, cfg.head_dim
+    return (geo["layers_off"] + l * geo["layer_stride"] + geo["scales_bytes"] + (kv * H + h) * geo["seg_stride"]
+            + int(units[t]) * (d // 2))
+
+
+def scale_offset(cfg, geo, qrank, l, kv, h, t):
+    H = cfg.num_kv_heads
+    return geo["layers_off"] + l * geo["layer_stride"] + ((kv * H + h) * geo["nq"] + int(qrank[t])) * 4
 
 
 def check_header(cfg, payload):

@@ -499,6 +499,54 @@ static void write_header(const ora_config* c, const ora_plan_t* p, const ora_geo
   put32(h + 152, ORA_CHUNK);
 }
 
+/* Header, 2-bit tier map and chunk index (the payload bytes before layer 0);
+ * also returns the per-token row offsets and scale ranks. */
+static void write_meta(const ora_config* c, const ora_plan_t* p, const ora_geom* g, const uint8_t* tier,
+                       uint32_t* units, uint32_t* qrank, uint8_t* payload) {
+  int64_t n = c->num_tokens;
+  write_header(c, p, g, payload);
+  for (int64_t t = 0; t < n; ++t)
+    payload[g->tiermap_off + (uint64_t)t / 4] |= (uint8_t)(tier[t] << (2 * (t % 4)));
+  ora_offsets((int32_t)n, tier, units, qrank);
+  for (int64_t ch = 0; ch < g->nchunks; ++ch) {
+    put32(payload + g->chunkidx_off + 8 * ch, units[ch * ORA_CHUNK]);
+    put32(payload + g->chunkidx_off + 8 * ch + 4, qrank[ch * ORA_CHUNK]);
+  }
+}
+
+/* Payload geometry: out = {tiermap_off, chunkidx_off, layers_off, seg_bytes,
+ * seg_stride, scales_bytes, layer_stride, total, nq}. */
+int ora_geometry(const ora_config* c, uint64_t* out) {
+  ora_plan_t p;
+  int st = ora_plan(c, &p);
+  if (st) return st;
+  ora_geom g;
+  geometry(c, &p, &g);
+  uint64_t v[9] = {g.tiermap_off, g.chunkidx_off, g.layers_off, g.seg_bytes, g.seg_stride,
+                   g.scales_bytes, g.layer_stride, g.total, (uint64_t)g.nq};
+  memcpy(out, v, sizeof(v));
+  return ORA_OK;
+}
+
+/* The payload's first layers_off bytes (header with a zero non-finite count,
+ * tier map, chunk index) for a tier map that is on plan. */
+int ora_pack_meta(const ora_config* c, const uint8_t* tier, uint8_t* out, uint64_t capacity) {
+  ora_plan_t p;
+  int st = ora_plan(c, &p);
+  if (st) return st;
+  ora_geom g;
+  geometry(c, &p, &g);
+  if (capacity < g.layers_off) return ORA_ERR_CAPACITY;
+  int64_t n = c->num_tokens;
+  uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
+  uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
+  memset(out, 0, g.layers_off);
+  write_meta(c, &p, &g, tier, units, qrank, out);
+  free(units);
+  free(qrank);
+  return ORA_OK;
+}
+
 int ora_pack(const ora_config* c, const uint16_t* k, const uint16_t* v, const uint8_t* tier,
              uint8_t* payload, uint64_t capacity) {
   ora_plan_t p;
@@ -519,16 +567,9 @@ int ora_pack(const ora_config* c, const uint16_t* k, const uint16_t* v, const ui
     return ORA_ERR_INVALID_ARG;
 
   memset(payload, 0, g.total);
-  write_header(c, &p, &g, payload);
-  for (int64_t t = 0; t < n; ++t)
-    payload[g.tiermap_off + (uint64_t)t / 4] |= (uint8_t)(tier[t] << (2 * (t % 4)));
   uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
-  ora_offsets((int32_t)n, tier, units, qrank);
-  for (int64_t ch = 0; ch < g.nchunks; ++ch) {
-    put32(payload + g.chunkidx_off + 8 * ch, units[ch * ORA_CHUNK]);
-    put32(payload + g.chunkidx_off + 8 * ch + 4, qrank[ch * ORA_CHUNK]);
-  }
+  write_meta(c, &p, &g, tier, units, qrank, payload);
   uint32_t nonfinite = 0;
   uint64_t rowunit = (uint64_t)d / 2;
   for (int64_t l = 0; l < L; ++l) {

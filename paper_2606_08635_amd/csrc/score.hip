@@ -1,0 +1,234 @@
+// Token scores (Sec. 4.3, eq. "importance"): KV-norm and recency modes.
+//
+// KV-norm mode ranks token t by I_t^2 = S_t * exp(-2 lambda (n-1-t)), where
+// S_t is the sum of squares of every finite K and V element of the token over
+// all layers and heads.  S_t is computed exactly, so the score is bit-exact
+// whatever the reduction order:
+//   * each binary16 x squares exactly in binary32 (22 significant bits), and
+//     y = x^2 * 2^8 is split into an integer part fl = floor(y) < 2^40 and a
+//     fraction y - fl, a multiple of 2^-40 below 1;
+//   * a thread adds at most 2^13 such terms into two binary64 accumulators,
+//     which stay exact (integers below 2^53, and multiples of 2^-40 below 2^13);
+//   * the accumulators become integers in units of 2^-48 and are combined in
+//     128-bit integer arithmetic across lanes and layer groups.
+// A non-finite input turns an accumulator into inf/NaN; only then does the
+// thread redo its sum with non-finite elements skipped.
+#include "device_util.h"
+#include "skv_internal.h"
+
+namespace skv {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxPairsPerGroup = 512;  // 2 tensors * 8 elements * 512 = 2^13 terms per thread
+
+struct U128 {
+  uint64_t lo, hi;
+};
+
+__device__ __forceinline__ U128 add128(U128 a, U128 b) {
+  U128 r;
+  r.lo = a.lo + b.lo;
+  r.hi = a.hi + b.hi + (r.lo < a.lo ? 1u : 0u);
+  return r;
+}
+
+// Correctly rounded (nearest-even) conversion of a 128-bit unsigned integer
+// to binary64.
+__device__ __forceinline__ double u128_to_double(U128 x) {
+  if (x.hi == 0 && x.lo == 0) return 0.0;
+  const int lz = x.hi ? __clzll(x.hi) : 64 + __clzll(x.lo);
+  uint64_t top, rest;
+  if (lz >= 64) {
+    top = x.lo << (lz - 64);
+    rest = 0;
+  } else if (lz == 0) {
+    top = x.hi;
+    rest = x.lo;
+  } else {
+    top = (x.hi << lz) | (x.lo >> (64 - lz));
+    rest = x.lo << lz;
+  }
+  uint64_t m = top >> 11;           // 53 significant bits
+  const uint64_t rb = top & 0x7FFu;  // the 11 bits below them
+  const bool up = rb > 0x400u || (rb == 0x400u && (rest != 0 || (m & 1u)));
+  m += up ? 1u : 0u;
+  return ldexp(static_cast<double>(m), 75 - lz);
+}
+
+__device__ __forceinline__ void acc_word(uint32_t w, double& ah, double& al) {
+  const float f0 = half_lo(w), f1 = half_hi(w);
+  const double y0 = static_cast<double>(f0 * f0) * 256.0;
+  const double y1 = static_cast<double>(f1 * f1) * 256.0;
+  const double g0 = floor(y0), g1 = floor(y1);
+  ah += g0;
+  al += y0 - g0;
+  ah += g1;
+  al += y1 - g1;
+}
+
+__device__ __forceinline__ void acc_word_finite(uint32_t w, double& ah, double& al) {
+  if (((w >> 10) & 31u) == 31u) w &= 0xFFFF0000u;
+  if (((w >> 26) & 31u) == 31u) w &= 0x0000FFFFu;
+  acc_word(w, ah, al);
+}
+
+__device__ __forceinline__ void acc16(u32x4 x, double& ah, double& al) {
+  acc_word(x.x, ah, al);
+  acc_word(x.y, ah, al);
+  acc_word(x.z, ah, al);
+  acc_word(x.w, ah, al);
+}
+
+// One block: TOK tokens x all LPR lanes of their rows, for the (layer, head)
+// pairs [p0, p1) of group blockIdx.y.  Writes the 128-bit partial sum of each
+// token in units of 2^-48 to partial[(group * n + t) * 2 + {0: lo, 1: hi}].
+template <int D>
+__global__ __launch_bounds__(kThreads) void kvnorm_partial(const uint16_t* __restrict__ k,
+                                                          const uint16_t* __restrict__ v, int n,
+                                                          int pairs, int pairs_per_group,
+                                                          uint64_t* __restrict__ partial) {
+  constexpr int LPR = D / 8;
+  constexpr int TOK = kThreads / LPR;
+  __shared__ U128 s_part[kThreads];
+  const int lane = threadIdx.x % LPR;
+  const int r = threadIdx.x / LPR;
+  const int t = blockIdx.x * TOK + r;
+  const int p0 = blockIdx.y * pairs_per_group;
+  const int p1 = min(pairs, p0 + pairs_per_group);
+  const size_t pair_stride = static_cast<size_t>(n) * D;  // elements between (l, h) pairs
+  double ah0 = 0.0, al0 = 0.0, ah1 = 0.0, al1 = 0.0;
+  if (t < n) {
+    const uint16_t* kp = k + static_cast<size_t>(p0) * pair_stride + static_cast<size_t>(t) * D + lane * 8;
+    const uint16_t* vp = v + static_cast<size_t>(p0) * pair_stride + static_cast<size_t>(t) * D + lane * 8;
+    int p = p0;
+    for (; p + 2 <= p1; p += 2) {
+      const u32x4 a = ld_nt16(kp), b = ld_nt16(vp);
+      const u32x4 c = ld_nt16(kp + pair_stride), e = ld_nt16(vp + pair_stride);
+      acc16(a, ah0, al0);
+      acc16(b, ah1, al1);
+      acc16(c, ah0, al0);
+      acc16(e, ah1, al1);
+      kp += 2 * pair_stride;
+      vp += 2 * pair_stride;
+    }
+    if (p < p1) {
+      acc16(ld_nt16(kp), ah0, al0);
+      acc16(ld_nt16(vp), ah1, al1);
+    }
+    double ah = ah0 + ah1, al = al0 + al1;  // both sums exact (< 2^53 units)
+    if (!(__builtin_isfinite(ah) && __builtin_isfinite(al))) {
+      // an infinity or NaN was read: redo this thread's sum without them
+      ah = 0.0;
+      al = 0.0;
+      const uint16_t* kq = k + static_cast<size_t>(p0) * pair_stride + static_cast<size_t>(t) * D + lane * 8;
+      const uint16_t* vq = v + static_cast<size_t>(p0) * pair_stride + static_cast<size_t>(t) * D + lane * 8;
+      for (int q = p0; q < p1; ++q) {
+        const u32x4 a = ld_nt16(kq), b = ld_nt16(vq);
+        acc_word_finite(a.x, ah, al);
+        acc_word_finite(a.y, ah, al);
+        acc_word_finite(a.z, ah, al);
+        acc_word_finite(a.w, ah, al);
+        acc_word_finite(b.x, ah, al);
+        acc_word_finite(b.y, ah, al);
+        acc_word_finite(b.z, ah, al);
+        acc_word_finite(b.w, ah, al);
+        kq += pair_stride;
+        vq += pair_stride;
+      }
+    }
+    // ah counts units of 2^-8 and al * 2^40 counts units of 2^-48; both are
+    // integers below 2^53.
+    const uint64_t a = static_cast<uint64_t>(ah);
+    const uint64_t b = static_cast<uint64_t>(al * 1099511627776.0);  // * 2^40, exact
+    U128 s;
+    s.lo = (a << 40) + b;
+    s.hi = (a >> 24) + (s.lo < b ? 1u : 0u);
+    s_part[threadIdx.x] = s;
+  } else {
+    s_part[threadIdx.x] = U128{0, 0};
+  }
+  __syncthreads();
+  if (lane == 0 && t < n) {
+    U128 s = s_part[threadIdx.x];
+#pragma unroll
+    for (int i = 1; i < LPR; ++i) s = add128(s, s_part[threadIdx.x + i]);
+    uint64_t* out = partial + (static_cast<size_t>(blockIdx.y) * n + t) * 2;
+    out[0] = s.lo;
+    out[1] = s.hi;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void kvnorm_finish(const uint64_t* __restrict__ partial,
+                                                         int groups, int n,
+                                                         const double* __restrict__ w2,
+                                                         double* __restrict__ score) {
+  const int t = blockIdx.x * kThreads + threadIdx.x;
+  if (t >= n) return;
+  U128 s{0, 0};
+  for (int g = 0; g < groups; ++g) {
+    const uint64_t* p = partial + (static_cast<size_t>(g) * n + t) * 2;
+    s = add128(s, U128{p[0], p[1]});
+  }
+  // RN64(S) then an exact scaling by 2^-48 (the result is 0 or >= 2^-48)
+  const double sd = u128_to_double(s) * 0x1p-48;
+  score[t] = sd * w2[n - 1 - t];
+}
+
+__global__ __launch_bounds__(kThreads) void recency_score(const double* __restrict__ w1, int n,
+                                                         double* __restrict__ score) {
+  const int t = blockIdx.x * kThreads + threadIdx.x;
+  if (t < n) score[t] = w1[n - 1 - t];
+}
+
+struct KvnormLaunch {
+  int pairs, groups, pairs_per_group, blocks_tok;
+};
+
+KvnormLaunch kvnorm_shape(const Geometry& g) {
+  KvnormLaunch s;
+  s.pairs = g.L * g.H;
+  const int tok = kThreads / (g.d / 8);
+  s.blocks_tok = (g.n + tok - 1) / tok;
+  // enough blocks to give every SIMD of the 256 CUs several waves, and few
+  // enough pairs per group that each thread's binary64 sums stay exact
+  int groups = (2048 + s.blocks_tok - 1) / s.blocks_tok;
+  groups = max(groups, (s.pairs + kMaxPairsPerGroup - 1) / kMaxPairsPerGroup);
+  groups = min(groups, s.pairs);
+  s.pairs_per_group = (s.pairs + groups - 1) / groups;
+  s.groups = (s.pairs + s.pairs_per_group - 1) / s.pairs_per_group;
+  return s;
+}
+
+}  // namespace
+
+uint64_t kvnorm_scratch_bytes(const Geometry& g) {
+  const KvnormLaunch s = kvnorm_shape(g);
+  return static_cast<uint64_t>(s.groups) * g.n * 16u;
+}
+
+hipError_t launch_score_kvnorm(const Geometry& g, const uint16_t* k, const uint16_t* v,
+                               const double* w2, uint64_t* partial, double* score,
+                               hipStream_t stream) {
+  const KvnormLaunch s = kvnorm_shape(g);
+  const dim3 grid(s.blocks_tok, s.groups);
+  switch (g.d) {
+    case 32: kvnorm_partial<32><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    case 64: kvnorm_partial<64><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    case 128: kvnorm_partial<128><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    case 256: kvnorm_partial<256><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  kvnorm_finish<<<(g.n + kThreads - 1) / kThreads, kThreads, 0, stream>>>(partial, s.groups, g.n, w2, score);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_recency(const Geometry& g, const double* w1, double* score,
+                                hipStream_t stream) {
+  recency_score<<<(g.n + kThreads - 1) / kThreads, kThreads, 0, stream>>>(w1, g.n, score);
+  return hipGetLastError();
+}
+
+}  // namespace skv

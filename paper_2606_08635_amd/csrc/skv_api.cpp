@@ -1,0 +1,333 @@
+// Host side of the C ABI declared in include/skv.h: argument checks, the tier
+// plan (Sec. 2.1 eq. "budget", Sec. 4.4), payload geometry, the decay table
+// and kernel launches.  Nothing here synchronizes with the device except
+// skv_prepare's one table upload.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <vector>
+
+#include "skv_internal.h"
+
+namespace skv {
+namespace {
+
+inline uint64_t round_up_256(uint64_t x) { return (x + 255u) / 256u * 256u; }
+
+inline bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+inline bool dev_ptr_ok(const void* p) { return p != nullptr && aligned(p, 16); }
+
+skv_status check_config(const skv_config* c) {
+  if (c == nullptr) return SKV_ERR_INVALID_ARG;
+  const int d = c->head_dim;
+  if (c->num_layers < 1 || c->num_kv_heads < 1) return SKV_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(c->num_layers) * c->num_kv_heads > 65536) return SKV_ERR_INVALID_ARG;
+  if (d != 32 && d != 64 && d != 128 && d != 256) return SKV_ERR_INVALID_ARG;
+  if (c->num_tokens < 1 || c->num_tokens > kMaxTokens) return SKV_ERR_INVALID_ARG;
+  if (!(c->budget > 0.0f) || !(c->budget <= 1.0f)) return SKV_ERR_INVALID_ARG;
+  if (!(c->first_ratio >= 0.0f) || !(c->first_ratio <= 1.0f)) return SKV_ERR_INVALID_ARG;
+  if (c->num_sink < -1) return SKV_ERR_INVALID_ARG;
+  if (!std::isfinite(c->decay) || !(c->decay >= 0.0f)) return SKV_ERR_INVALID_ARG;
+  if (2.0 * static_cast<double>(c->decay) * static_cast<double>(c->num_tokens - 1) > 700.0)
+    return SKV_ERR_INVALID_ARG;
+  if (c->num_tiers != 2 && c->num_tiers != 3) return SKV_ERR_INVALID_ARG;
+  switch (c->score_mode) {
+    case SKV_SCORE_KVNORM:
+    case SKV_SCORE_RECENCY:
+      break;
+    case SKV_SCORE_ATTN:
+      if (c->num_q_heads < 1 || c->num_q_heads % c->num_kv_heads != 0) return SKV_ERR_INVALID_ARG;
+      if (c->obs_window < 1) return SKV_ERR_INVALID_ARG;
+      if (static_cast<int64_t>(c->num_q_heads / c->num_kv_heads) * c->obs_window > 256)
+        return SKV_ERR_INVALID_ARG;
+      break;
+    default:
+      return SKV_ERR_INVALID_ARG;
+  }
+  return SKV_OK;
+}
+
+// Tier counts.  Everything is counted in quarter-units of the fp16 row cost
+// (FP16 4, INT8 2, INT4 1, DROP 0), so the budget b becomes B = floor(4 b n)
+// units; both products are exact in binary64 (24-bit b times n <= 2^21).
+skv_status plan_counts(const skv_config* c, skv_plan* p) {
+  const int64_t n = c->num_tokens;
+  int64_t sinks;
+  if (c->num_sink >= 0) {
+    sinks = std::min<int64_t>(c->num_sink, n);
+  } else {
+    const double want = std::ceil(static_cast<double>(c->first_ratio) * static_cast<double>(n));
+    sinks = want >= static_cast<double>(n) ? n : static_cast<int64_t>(want);
+  }
+  const int64_t units = static_cast<int64_t>(std::floor(4.0 * static_cast<double>(c->budget) * static_cast<double>(n)));
+  if (4 * sinks > units) return SKV_ERR_BUDGET;
+  const int64_t rest = n - sinks;     // ranked tokens
+  const int64_t left = units - 4 * sinks;  // their budget
+  int64_t f16 = 0, i8 = 0, i4 = 0, drop = 0;
+  if (left >= 2 * rest) {
+    // every ranked token affords INT8; the surplus buys FP16 upgrades (+2 units each)
+    f16 = (left - 2 * rest) / 2;
+    i8 = rest - f16;
+  } else if (c->num_tiers == 3) {
+    if (left >= rest) {
+      // every ranked token affords INT4; the surplus buys INT8 upgrades (+1 unit each)
+      i8 = left - rest;
+      i4 = rest - i8;
+    } else {
+      i4 = left;  // INT4 for as many tokens as the budget allows, the rest dropped
+      drop = rest - i4;
+    }
+  } else {
+    i8 = left / 2;  // INT4 disabled: INT8 is the lowest tier, the rest dropped
+    drop = rest - i8;
+  }
+  p->n_sink = static_cast<int32_t>(sinks);
+  p->n_fp16 = static_cast<int32_t>(f16);
+  p->n_int8 = static_cast<int32_t>(i8);
+  p->n_int4 = static_cast<int32_t>(i4);
+  p->n_drop = static_cast<int32_t>(drop);
+  p->budget_units = units;
+  p->used_units = 4 * (sinks + f16) + 2 * i8 + i4;
+  return SKV_OK;
+}
+
+inline uint32_t float_bits(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  return u;
+}
+
+inline void put_u64(HeaderImage* h, int byte_off, uint64_t v) {
+  h->w[byte_off / 4] = static_cast<uint32_t>(v);
+  h->w[byte_off / 4 + 1] = static_cast<uint32_t>(v >> 32);
+}
+
+}  // namespace
+
+skv_status make_geometry(const skv_config* cfg, Geometry* g, skv_plan* plan_out) {
+  skv_status st = check_config(cfg);
+  if (st != SKV_OK) return st;
+  skv_plan p;
+  st = plan_counts(cfg, &p);
+  if (st != SKV_OK) return st;
+  g->L = cfg->num_layers;
+  g->H = cfg->num_kv_heads;
+  g->d = cfg->head_dim;
+  g->n = cfg->num_tokens;
+  g->n_sink = p.n_sink;
+  g->n16 = p.n_fp16;
+  g->n8 = p.n_int8;
+  g->n4 = p.n_int4;
+  g->nd = p.n_drop;
+  g->budget_units = p.budget_units;
+  g->used_units = p.used_units;
+  g->nq = static_cast<int64_t>(p.n_int8) + p.n_int4;
+  g->nchunks = (g->n + kChunkTokens - 1) / kChunkTokens;
+  const uint64_t d = static_cast<uint64_t>(g->d), H = static_cast<uint64_t>(g->H);
+  g->tiermap_off = 256;
+  g->chunkidx_off = g->tiermap_off + round_up_256((static_cast<uint64_t>(g->n) + 3) / 4);
+  g->layers_off = g->chunkidx_off + round_up_256(8u * static_cast<uint64_t>(g->nchunks));
+  g->seg_bytes = static_cast<uint64_t>(p.n_sink + p.n_fp16) * (2 * d) +
+                 static_cast<uint64_t>(p.n_int8) * d + static_cast<uint64_t>(p.n_int4) * (d / 2);
+  g->seg_stride = round_up_256(g->seg_bytes);
+  g->scales_bytes = round_up_256(2 * H * static_cast<uint64_t>(g->nq) * 4u);
+  g->layer_stride = g->scales_bytes + 2 * H * g->seg_stride;
+  g->total = g->layers_off + static_cast<uint64_t>(g->L) * g->layer_stride;
+  if (plan_out) *plan_out = p;
+  return SKV_OK;
+}
+
+void fill_header(const skv_config* cfg, const Geometry& g, HeaderImage* h) {
+  std::memset(h, 0, sizeof(*h));
+  h->w[0] = kMagic;
+  h->w[1] = kVersion;
+  h->w[2] = static_cast<uint32_t>(g.L);
+  h->w[3] = static_cast<uint32_t>(g.H);
+  h->w[4] = static_cast<uint32_t>(g.d);
+  h->w[5] = static_cast<uint32_t>(g.n);
+  h->w[6] = static_cast<uint32_t>(g.n_sink);
+  h->w[7] = static_cast<uint32_t>(cfg->num_tiers);
+  h->w[8] = float_bits(cfg->budget);
+  h->w[9] = float_bits(cfg->first_ratio);
+  h->w[10] = float_bits(cfg->decay);
+  h->w[11] = static_cast<uint32_t>(cfg->score_mode);
+  h->w[12] = static_cast<uint32_t>(g.n16);
+  h->w[13] = static_cast<uint32_t>(g.n8);
+  h->w[14] = static_cast<uint32_t>(g.n4);
+  h->w[15] = static_cast<uint32_t>(g.nd);
+  put_u64(h, 64, static_cast<uint64_t>(g.budget_units));
+  put_u64(h, 72, static_cast<uint64_t>(g.used_units));
+  put_u64(h, 80, g.tiermap_off);
+  put_u64(h, 88, g.chunkidx_off);
+  put_u64(h, 96, g.layers_off);
+  put_u64(h, 104, g.seg_bytes);
+  put_u64(h, 112, g.seg_stride);
+  put_u64(h, 120, g.scales_bytes);
+  put_u64(h, 128, g.layer_stride);
+  put_u64(h, 136, g.total);
+  h->w[152 / 4] = static_cast<uint32_t>(kChunkTokens);
+}
+
+namespace {
+
+uint64_t decay_table_bytes(const skv_config* c) {
+  return round_up_256(8u * static_cast<uint64_t>(c->num_tokens));
+}
+
+uint64_t scratch_bytes(const skv_config* c) {
+  Geometry g{};
+  g.L = c->num_layers;
+  g.H = c->num_kv_heads;
+  g.d = c->head_dim;
+  g.n = c->num_tokens;
+  switch (c->score_mode) {
+    case SKV_SCORE_KVNORM: return kvnorm_scratch_bytes(g);
+    case SKV_SCORE_ATTN: return attn_scratch_bytes(g, c->num_q_heads, c->obs_window);
+    default: return 0;
+  }
+}
+
+inline skv_status launched(hipError_t e) { return e == hipSuccess ? SKV_OK : SKV_ERR_DEVICE; }
+
+}  // namespace
+}  // namespace skv
+
+using namespace skv;
+
+extern "C" {
+
+int32_t skv_abi_version(void) { return SKV_ABI_VERSION; }
+
+const char* skv_status_string(skv_status status) {
+  switch (status) {
+    case SKV_OK: return "ok";
+    case SKV_ERR_INVALID_ARG: return "invalid argument";
+    case SKV_ERR_BUDGET: return "sink tokens exceed the budget";
+    case SKV_ERR_CAPACITY: return "output buffer too small";
+    case SKV_ERR_FORMAT: return "payload does not match the configuration";
+    case SKV_ERR_DEVICE: return "HIP launch or copy failed";
+  }
+  return "unknown status";
+}
+
+skv_status skv_plan_tiers(const skv_config* cfg, skv_plan* out) {
+  if (out == nullptr) return SKV_ERR_INVALID_ARG;
+  Geometry g;
+  return make_geometry(cfg, &g, out);
+}
+
+skv_status skv_payload_size(const skv_config* cfg, uint64_t* bytes) {
+  if (bytes == nullptr) return SKV_ERR_INVALID_ARG;
+  Geometry g;
+  const skv_status st = make_geometry(cfg, &g, nullptr);
+  if (st == SKV_OK) *bytes = g.total;
+  return st;
+}
+
+skv_status skv_workspace_size(const skv_config* cfg, uint64_t* bytes) {
+  if (bytes == nullptr) return SKV_ERR_INVALID_ARG;
+  const skv_status st = check_config(cfg);
+  if (st != SKV_OK) return st;
+  *bytes = decay_table_bytes(cfg) + round_up_256(scratch_bytes(cfg));
+  return SKV_OK;
+}
+
+skv_status skv_prepare(const skv_config* cfg, void* ws, hipStream_t stream) {
+  skv_status st = check_config(cfg);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
+  const int n = cfg->num_tokens;
+  // exp(-lambda * Delta) for attention/recency scores, exp(-(2 lambda) * Delta)
+  // for the squared KV-norm score; the argument is exact in binary64
+  const double rate = static_cast<double>(cfg->decay) * (cfg->score_mode == SKV_SCORE_KVNORM ? 2.0 : 1.0);
+  std::vector<double> table(static_cast<size_t>(n));
+#pragma clang loop vectorize(disable)
+  for (int delta = 0; delta < n; ++delta) table[delta] = std::exp(-(rate * static_cast<double>(delta)));
+  if (hipMemcpyAsync(ws, table.data(), table.size() * sizeof(double), hipMemcpyHostToDevice, stream) != hipSuccess)
+    return SKV_ERR_DEVICE;
+  return hipStreamSynchronize(stream) == hipSuccess ? SKV_OK : SKV_ERR_DEVICE;
+}
+
+skv_status skv_score(const skv_config* cfg, const void* k, const void* v, const void* q_obs,
+                     double* score, void* ws, hipStream_t stream) {
+  skv_status st = check_config(cfg);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(score) || !dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
+  Geometry g{};
+  g.L = cfg->num_layers;
+  g.H = cfg->num_kv_heads;
+  g.d = cfg->head_dim;
+  g.n = cfg->num_tokens;
+  const double* table = static_cast<const double*>(ws);
+  void* scratch = static_cast<uint8_t*>(ws) + decay_table_bytes(cfg);
+  switch (cfg->score_mode) {
+    case SKV_SCORE_KVNORM:
+      if (!dev_ptr_ok(k) || !dev_ptr_ok(v)) return SKV_ERR_INVALID_ARG;
+      return launched(launch_score_kvnorm(g, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                                          table, static_cast<uint64_t*>(scratch), score, stream));
+    case SKV_SCORE_ATTN:
+      if (!dev_ptr_ok(k) || !dev_ptr_ok(q_obs)) return SKV_ERR_INVALID_ARG;
+      return launched(launch_score_attn(g, cfg->num_q_heads, cfg->obs_window, static_cast<const uint16_t*>(k),
+                                        static_cast<const uint16_t*>(q_obs), table, scratch, score, stream));
+    default:
+      return launched(launch_score_recency(g, table, score, stream));
+  }
+}
+
+skv_status skv_assign_tiers(const skv_config* cfg, const double* score, uint8_t* tier, void* ws,
+                            hipStream_t stream) {
+  (void)ws;
+  Geometry g;
+  const skv_status st = make_geometry(cfg, &g, nullptr);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(score) || !dev_ptr_ok(tier)) return SKV_ERR_INVALID_ARG;
+  return launched(launch_assign(g, score, tier, stream));
+}
+
+skv_status skv_pack(const skv_config* cfg, const void* k, const void* v, const uint8_t* tier,
+                    void* payload, uint64_t capacity, uint32_t* dev_status, hipStream_t stream) {
+  Geometry g;
+  const skv_status st = make_geometry(cfg, &g, nullptr);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(k) || !dev_ptr_ok(v) || !dev_ptr_ok(tier) || !dev_ptr_ok(payload))
+    return SKV_ERR_INVALID_ARG;
+  if (dev_status != nullptr && !aligned(dev_status, 4)) return SKV_ERR_INVALID_ARG;
+  if (capacity < g.total) return SKV_ERR_CAPACITY;
+  HeaderImage hdr;
+  fill_header(cfg, g, &hdr);
+  return launched(launch_pack(g, hdr, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), tier,
+                              static_cast<uint8_t*>(payload), dev_status, stream));
+}
+
+skv_status skv_unpack(const skv_config* cfg, const void* payload, uint64_t payload_bytes,
+                      void* k_cache, void* v_cache, const int32_t* block_table, int32_t num_blocks,
+                      int32_t block_size, uint32_t* dev_status, hipStream_t stream) {
+  Geometry g;
+  const skv_status st = make_geometry(cfg, &g, nullptr);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(payload) || !dev_ptr_ok(k_cache) || !dev_ptr_ok(v_cache)) return SKV_ERR_INVALID_ARG;
+  if (block_table == nullptr || !aligned(block_table, 4)) return SKV_ERR_INVALID_ARG;
+  if (dev_status == nullptr || !aligned(dev_status, 4)) return SKV_ERR_INVALID_ARG;
+  if (num_blocks < 1 || block_size < 1) return SKV_ERR_INVALID_ARG;
+  if (static_cast<uint64_t>(num_blocks) * static_cast<uint64_t>(block_size) > 0xFFFFFFFFull)
+    return SKV_ERR_INVALID_ARG;
+  if (payload_bytes < g.total) return SKV_ERR_FORMAT;
+  HeaderImage hdr;
+  fill_header(cfg, g, &hdr);
+  return launched(launch_unpack(g, hdr, static_cast<const uint8_t*>(payload), static_cast<uint16_t*>(k_cache),
+                                static_cast<uint16_t*>(v_cache), block_table, num_blocks, block_size,
+                                dev_status, stream));
+}
+
+skv_status skv_link(void* dst, const void* src, uint64_t bytes, void* host_staging,
+                    hipStream_t stream) {
+  if (bytes == 0) return SKV_OK;
+  if (dst == nullptr || src == nullptr) return SKV_ERR_INVALID_ARG;
+  if (host_staging == nullptr)
+    return launched(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream));
+  if (hipMemcpyAsync(host_staging, src, bytes, hipMemcpyDeviceToHost, stream) != hipSuccess)
+    return SKV_ERR_DEVICE;
+  return launched(hipMemcpyAsync(dst, host_staging, bytes, hipMemcpyHostToDevice, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,227 @@
+"""ctypes binding over ``libskv.so`` (the C ABI of ``include/skv.h``).
+
+Argument marshalling only: every function checks that the torch tensors it is
+given have the dtype, device and size the configuration implies (the C library
+cannot see device buffer sizes), passes their ``data_ptr()`` and the current
+HIP stream, and raises ``SkvError`` on a nonzero status.  All codec work runs
+in the library's HIP kernels; there is no fallback.  If ``libskv.so`` has not
+been built, the first call raises.
+"""
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libskv.so")
+
+OK, ERR_INVALID_ARG, ERR_BUDGET, ERR_CAPACITY, ERR_FORMAT, ERR_DEVICE = range(6)
+FP16, INT8, INT4, DROP = 0, 1, 2, 3
+KVNORM, ATTN, RECENCY = 0, 1, 2
+
+EXPORTED = ("skv_abi_version", "skv_status_string", "skv_plan_tiers", "skv_payload_size",
+            "skv_workspace_size", "skv_prepare", "skv_score", "skv_assign_tiers", "skv_pack",
+            "skv_unpack", "skv_link")
+
+
+class SkvError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("num_tokens", ctypes.c_int32),
+                ("budget", ctypes.c_float), ("first_ratio", ctypes.c_float),
+                ("num_sink", ctypes.c_int32), ("decay", ctypes.c_float),
+                ("num_tiers", ctypes.c_int32), ("score_mode", ctypes.c_int32),
+                ("num_q_heads", ctypes.c_int32), ("obs_window", ctypes.c_int32)]
+
+
+class Plan(ctypes.Structure):
+    _fields_ = [("n_sink", ctypes.c_int32), ("n_fp16", ctypes.c_int32),
+                ("n_int8", ctypes.c_int32), ("n_int4", ctypes.c_int32),
+                ("n_drop", ctypes.c_int32), ("budget_units", ctypes.c_int64),
+                ("used_units", ctypes.c_int64)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                               "(the codec has no non-HIP fallback)")
+        L = ctypes.CDLL(LIB_PATH)
+        P, vp, u64, i32 = ctypes.POINTER, ctypes.c_void_p, ctypes.c_uint64, ctypes.c_int32
+        cfgp = P(Config)
+        sigs = {
+            "skv_abi_version": (i32, []),
+            "skv_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+            "skv_plan_tiers": (ctypes.c_int, [cfgp, P(Plan)]),
+            "skv_payload_size": (ctypes.c_int, [cfgp, P(u64)]),
+            "skv_workspace_size": (ctypes.c_int, [cfgp, P(u64)]),
+            "skv_prepare": (ctypes.c_int, [cfgp, vp, vp]),
+            "skv_score": (ctypes.c_int, [cfgp, vp, vp, vp, vp, vp, vp]),
+            "skv_assign_tiers": (ctypes.c_int, [cfgp, vp, vp, vp, vp]),
+            "skv_pack": (ctypes.c_int, [cfgp, vp, vp, vp, vp, u64, vp, vp]),
+            "skv_unpack": (ctypes.c_int, [cfgp, vp, u64, vp, vp, vp, i32, i32, vp, vp]),
+            "skv_link": (ctypes.c_int, [vp, vp, u64, vp, vp]),
+        }
+        for name, (res, args) in sigs.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().skv_status_string(int(status)).decode()
+
+
+def config(num_layers, num_kv_heads, head_dim, num_tokens, budget, first_ratio=0.02, num_sink=-1,
+           decay=0.005, num_tiers=3, score_mode=KVNORM, num_q_heads=0, obs_window=0) -> Config:
+    return Config(num_layers, num_kv_heads, head_dim, num_tokens, budget, first_ratio, num_sink,
+                  decay, num_tiers, score_mode, num_q_heads, obs_window)
+
+
+def _check(status: int, what: str):
+    if status != OK:
+        raise SkvError(status, what)
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dev(t: Optional[torch.Tensor], dtype, numel: int, name: str) -> ctypes.c_void_p:
+    """Device pointer of a contiguous tensor holding at least `numel` elements of `dtype`."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, needs {numel}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def plan_tiers(cfg: Config) -> dict:
+    p = Plan()
+    _check(lib().skv_plan_tiers(ctypes.byref(cfg), ctypes.byref(p)), "skv_plan_tiers")
+    return {f: getattr(p, f) for f, _ in Plan._fields_}
+
+
+def payload_size(cfg: Config) -> int:
+    out = ctypes.c_uint64()
+    _check(lib().skv_payload_size(ctypes.byref(cfg), ctypes.byref(out)), "skv_payload_size")
+    return out.value
+
+
+def workspace_size(cfg: Config) -> int:
+    out = ctypes.c_uint64()
+    _check(lib().skv_workspace_size(ctypes.byref(cfg), ctypes.byref(out)), "skv_workspace_size")
+    return out.value
+
+
+def _kv_numel(cfg: Config) -> int:
+    return cfg.num_layers * cfg.num_kv_heads * cfg.num_tokens * cfg.head_dim
+
+
+def prepare(cfg: Config, ws: torch.Tensor, stream=None):
+    _check(lib().skv_prepare(ctypes.byref(cfg), _dev(ws, torch.uint8, workspace_size(cfg), "ws"),
+                             _stream(stream)), "skv_prepare")
+
+
+def score(cfg: Config, k: torch.Tensor, v: torch.Tensor, q_obs: Optional[torch.Tensor],
+          out: torch.Tensor, ws: torch.Tensor, stream=None):
+    n = _kv_numel(cfg)
+    kp = _dev(k, torch.float16, n, "k")
+    vp = _dev(v, torch.float16, n, "v") if cfg.score_mode != ATTN else ctypes.c_void_p(None)
+    qp = ctypes.c_void_p(None)
+    if cfg.score_mode == ATTN:
+        qn = cfg.num_layers * cfg.num_q_heads * cfg.obs_window * cfg.head_dim
+        qp = _dev(q_obs, torch.float16, qn, "q_obs")
+    _check(lib().skv_score(ctypes.byref(cfg), kp, vp, qp, _dev(out, torch.float64, cfg.num_tokens, "score"),
+                           _dev(ws, torch.uint8, workspace_size(cfg), "ws"), _stream(stream)), "skv_score")
+
+
+def assign_tiers(cfg: Config, scores: torch.Tensor, tier: torch.Tensor, stream=None):
+    _check(lib().skv_assign_tiers(ctypes.byref(cfg), _dev(scores, torch.float64, cfg.num_tokens, "score"),
+                                  _dev(tier, torch.uint8, cfg.num_tokens, "tier"), ctypes.c_void_p(None),
+                                  _stream(stream)), "skv_assign_tiers")
+
+
+def pack(cfg: Config, k: torch.Tensor, v: torch.Tensor, tier: torch.Tensor, payload: torch.Tensor,
+         dev_status: Optional[torch.Tensor] = None, stream=None):
+    n = _kv_numel(cfg)
+    st = ctypes.c_void_p(None) if dev_status is None else _dev(dev_status, torch.int32, 1, "dev_status")
+    _check(lib().skv_pack(ctypes.byref(cfg), _dev(k, torch.float16, n, "k"), _dev(v, torch.float16, n, "v"),
+                          _dev(tier, torch.uint8, cfg.num_tokens, "tier"),
+                          _dev(payload, torch.uint8, 0, "payload"), payload.numel(), st,
+                          _stream(stream)), "skv_pack")
+
+
+def unpack(cfg: Config, payload: torch.Tensor, k_cache: torch.Tensor, v_cache: torch.Tensor,
+           block_table: torch.Tensor, block_size: int, dev_status: torch.Tensor, stream=None):
+    """k_cache/v_cache: float16 [L][num_blocks][block_size][H][d]."""
+    if k_cache.dim() != 5 or k_cache.shape[2] != block_size or tuple(k_cache.shape) != tuple(v_cache.shape):
+        raise ValueError("caches must be [L][num_blocks][block_size][H][d] and alike")
+    L, nb, _, H, d = k_cache.shape
+    if (L, H, d) != (cfg.num_layers, cfg.num_kv_heads, cfg.head_dim):
+        raise ValueError("cache shape does not match the configuration")
+    nbt = -(-cfg.num_tokens // block_size)
+    _check(lib().skv_unpack(ctypes.byref(cfg), _dev(payload, torch.uint8, 0, "payload"), payload.numel(),
+                            _dev(k_cache, torch.float16, k_cache.numel(), "k_cache"),
+                            _dev(v_cache, torch.float16, v_cache.numel(), "v_cache"),
+                            _dev(block_table, torch.int32, nbt, "block_table"), nb, block_size,
+                            _dev(dev_status, torch.int32, 1, "dev_status"), _stream(stream)), "skv_unpack")
+
+
+def link(dst: torch.Tensor, src: torch.Tensor, nbytes: int, host_staging: Optional[torch.Tensor] = None,
+         stream=None):
+    """Emulated transfer of nbytes (device to device, or through pinned host memory)."""
+    if dst.numel() * dst.element_size() < nbytes or src.numel() * src.element_size() < nbytes:
+        raise ValueError("link buffers smaller than nbytes")
+    hs = ctypes.c_void_p(None)
+    if host_staging is not None:
+        if host_staging.is_cuda or not host_staging.is_pinned() or host_staging.numel() * host_staging.element_size() < nbytes:
+            raise ValueError("host_staging must be pinned host memory of at least nbytes")
+        hs = ctypes.c_void_p(host_staging.data_ptr())
+    _check(lib().skv_link(ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()), nbytes, hs,
+                          _stream(stream)), "skv_link")
+
+
+class Codec:
+    """Device buffers for one request shape: workspace (prepared), scores,
+    tier map, payload and status words, plus the encode/decode sequence."""
+
+    def __init__(self, cfg: Config, device="cuda"):
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.plan = plan_tiers(cfg)
+        self.payload_bytes = payload_size(cfg)
+        self.ws = torch.empty(workspace_size(cfg), dtype=torch.uint8, device=self.device)
+        self.scores = torch.empty(cfg.num_tokens, dtype=torch.float64, device=self.device)
+        self.tier = torch.empty(cfg.num_tokens, dtype=torch.uint8, device=self.device)
+        self.payload = torch.empty(self.payload_bytes, dtype=torch.uint8, device=self.device)
+        self.status = torch.zeros(2, dtype=torch.int32, device=self.device)
+        prepare(cfg, self.ws)
+
+    def encode(self, k, v, q_obs=None, stream=None):
+        score(self.cfg, k, v, q_obs, self.scores, self.ws, stream)
+        assign_tiers(self.cfg, self.scores, self.tier, stream)
+        pack(self.cfg, k, v, self.tier, self.payload, self.status[0:1], stream)
+        return self.payload
+
+    def decode(self, payload, k_cache, v_cache, block_table, block_size=16, stream=None):
+        unpack(self.cfg, payload, k_cache, v_cache, block_table, block_size, self.status[1:2], stream)

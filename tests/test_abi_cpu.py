@@ -1,0 +1,119 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/skv.h declares, and its host-only entry points (plan, sizes, argument
+checks) agree with the oracle.  No device work is enqueued here: every call
+either is host-only or fails its argument check before any HIP call."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_08635_amd import skv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "skv.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(skv.LIB_PATH):
+        from paper_2606_08635_amd import build
+        build.build()
+    return skv.lib()
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\w[\w\s\*]*?\b(skv_\w+)\s*\(", text, re.M)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert len(names) >= 11
+    for name in names:
+        assert hasattr(lib, name), name
+    assert sorted(skv.EXPORTED) == names
+    assert lib.skv_abi_version() == 1
+
+
+def _pair(L, H, d, n, b, **kw):
+    return skv.config(L, H, d, n, b, **kw), oracle.config(L, H, d, n, b, **kw)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_plan_and_payload_size_match_oracle(lib, seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(300):
+        L, H = int(rng.integers(1, 6)), int(rng.integers(1, 9))
+        d = int(rng.choice([32, 64, 128, 256]))
+        n = int(rng.integers(1, 70000))
+        b = float(np.float32(rng.uniform(0.01, 1.0)))
+        kw = dict(first_ratio=float(np.float32(rng.uniform(0, 0.1))), num_tiers=int(rng.integers(2, 4)),
+                  decay=0.0, num_sink=int(rng.choice([-1, -1, 0, 5])))
+        c, o = _pair(L, H, d, n, b, **kw)
+        try:
+            want = oracle.plan(o)
+        except oracle.OracleError as e:
+            with pytest.raises(skv.SkvError) as got:
+                skv.plan_tiers(c)
+            assert got.value.status == e.status
+            continue
+        assert skv.plan_tiers(c) == want
+        assert skv.payload_size(c) == oracle.payload_size(o)
+
+
+def test_invalid_configs_rejected_like_the_oracle(lib):
+    base = dict(num_layers=2, num_kv_heads=2, head_dim=64, num_tokens=1000, budget=0.5)
+    for field, value in [("head_dim", 48), ("head_dim", 512), ("num_tokens", 0), ("num_tokens", (1 << 21) + 1),
+                         ("budget", 0.0), ("budget", 1.5), ("budget", float("nan")), ("first_ratio", -0.1),
+                         ("num_tiers", 4), ("score_mode", 3), ("decay", -1.0), ("decay", float("inf")),
+                         ("decay", 1.0), ("num_sink", -2), ("num_layers", 0), ("num_kv_heads", 0)]:
+        c = skv.config(**base)
+        setattr(c, field, value)
+        o = oracle.config(**base)
+        setattr(o, field, value)
+        assert oracle.validate(o) == oracle.ERR_INVALID_ARG
+        with pytest.raises(skv.SkvError) as e:
+            skv.payload_size(c)
+        assert e.value.status == skv.ERR_INVALID_ARG
+    with pytest.raises(skv.SkvError) as e:
+        skv.plan_tiers(skv.config(1, 1, 64, 100, 0.1, num_sink=11))
+    assert e.value.status == skv.ERR_BUDGET
+
+
+def test_workspace_size(lib):
+    c = skv.config(32, 8, 128, 32768, 0.5)
+    ws = skv.workspace_size(c)
+    assert ws >= 8 * 32768 and ws % 256 == 0
+    c.score_mode = skv.RECENCY
+    assert skv.workspace_size(c) == 8 * 32768
+
+
+def test_host_side_argument_errors(lib):
+    """Bad pointers, capacities and sizes are refused before any device work."""
+    cfg = skv.config(2, 2, 64, 300, 0.5)
+    P = ctypes.c_void_p
+    fake = P(1 << 20)        # aligned, never dereferenced: the calls must fail first
+    odd = P((1 << 20) + 8)   # misaligned
+    total = skv.payload_size(cfg)
+    L = lib
+    by = ctypes.byref(cfg)
+    assert L.skv_pack(by, fake, fake, fake, fake, total - 1, None, None) == skv.ERR_CAPACITY
+    assert L.skv_pack(by, None, fake, fake, fake, total, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_pack(by, odd, fake, fake, fake, total, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_unpack(by, fake, total - 1, fake, fake, fake, 20, 16, fake, None) == skv.ERR_FORMAT
+    assert L.skv_unpack(by, fake, total, fake, fake, fake, 20, 16, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_unpack(by, fake, total, fake, fake, fake, 0, 16, fake, None) == skv.ERR_INVALID_ARG
+    assert L.skv_unpack(by, fake, total, fake, fake, fake, 1 << 30, 16, fake, None) == skv.ERR_INVALID_ARG
+    assert L.skv_score(by, fake, fake, None, odd, fake, None) == skv.ERR_INVALID_ARG
+    assert L.skv_score(None, fake, fake, None, fake, fake, None) == skv.ERR_INVALID_ARG
+    assert L.skv_assign_tiers(by, None, fake, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_prepare(by, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_link(None, fake, 16, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_link(fake, fake, 0, None, None) == skv.OK
+    attn = skv.config(2, 2, 64, 300, 0.5, score_mode=skv.ATTN, num_q_heads=4, obs_window=8)
+    assert L.skv_score(ctypes.byref(attn), fake, fake, None, fake, fake, None) == skv.ERR_INVALID_ARG
+    for s in range(6):
+        assert skv.status_string(s)
