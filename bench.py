@@ -21,6 +21,31 @@ sys.path.insert(0, ROOT)
 
 METRIC = "KV codec GB/s (fp16-equivalent in, pack+unpack) and % of HBM peak, 7B-shape 32k"
 HBM_PEAK_GBS = 8000.0
+CSRC = os.path.join(ROOT, "paper_2606_08635_amd", "csrc")
+
+# HBM bytes per dispatch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs (scaled by
+# a plain-copy calibration; see profiles/traffic_*.md), valid only for the
+# kernel sources they were taken on (first 16 hex digits of SHA-256 of each file).
+MEASURED_TRAFFIC = {
+    ("mistral7b_32k", "pack"): (6.5086e9, {"pack.hip": "da2a950f405453ac", "device_util.h": "060a3da049777381",
+                                           "tier_groups.h": "b2cb19a39c2cf076"}),
+    ("mistral7b_32k", "unpack"): (6.5125e9, {"unpack.hip": "feb944673636a152", "device_util.h": "060a3da049777381",
+                                             "tier_groups.h": "b2cb19a39c2cf076"}),
+}
+
+
+def measured_traffic(workload, kernel):
+    import hashlib
+
+    entry = MEASURED_TRAFFIC.get((workload, kernel))
+    if entry is None:
+        return None
+    nbytes, sources = entry
+    for name, digest in sources.items():
+        with open(os.path.join(CSRC, name), "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest()[:16] != digest:
+                return None  # the kernel changed since the counters were taken
+    return nbytes
 
 
 def algorithmic_bytes(w, plan, payload_bytes, block_size):
@@ -71,6 +96,11 @@ def main():
     ap.add_argument("--workload", default="mistral7b_32k")
     ap.add_argument("--cpu-layers", type=int, default=4, help="layers in the CPU-baseline sample (0: skip)")
     ap.add_argument("--link", choices=["d2d", "host"], default="d2d")
+    ap.add_argument("--score", choices=["kvnorm", "attn"], default="kvnorm",
+                    help="importance statistic; attn uses a W-query observation window per query head")
+    ap.add_argument("--obs-window", type=int, default=32)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="only copy a MIB-sized buffer with skv_link (reference for byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures the codec on one GPU; --gpus {args.gpus} is not supported "
@@ -81,13 +111,27 @@ def main():
 
     from paper_2606_08635_amd import skv, workloads
 
+    if args.calibrate_copy:
+        nbytes = args.calibrate_copy << 20
+        src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup + args.steps):
+            skv.link(dst, src, nbytes)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": nbytes, "copies": args.warmup + args.steps}), flush=True)
+        return
+
     w = workloads.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     L, H, d, n, bs = w.layers, w.kv_heads, w.head_dim, w.tokens, 16
-    cfg = skv.config(L, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers)
+    attn = args.score == "attn"
+    cfg = skv.config(L, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers,
+                     score_mode=skv.ATTN if attn else skv.KVNORM, num_q_heads=w.q_heads if attn else 0,
+                     obs_window=args.obs_window if attn else 0)
     codec = skv.Codec(cfg, dev)
     k, v = workloads.make_kv(L, H, n, d, seed=0, outliers=w.outliers, device=dev)
+    q_obs = workloads.make_qobs(L, w.q_heads, args.obs_window, d, seed=0, device=dev) if attn else None
     nb = workloads.blocks_for(n, bs)
     bt = workloads.make_block_table(n, bs, nb, seed=0, device=dev)
     kc = torch.empty(L, nb, bs, H, d, dtype=torch.float16, device=dev)
@@ -99,7 +143,7 @@ def main():
 
     def step(ev=None):
         if ev: ev[0].record(stream)
-        skv.score(cfg, k, v, None, codec.scores, codec.ws)
+        skv.score(cfg, k, v, q_obs, codec.scores, codec.ws)
         if ev: ev[1].record(stream)
         skv.assign_tiers(cfg, codec.scores, codec.tier)
         if ev: ev[2].record(stream)
@@ -148,7 +192,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "layers": L, "kv_heads": H, "head_dim": d, "tokens": n,
                    "budget": w.budget, "num_tiers": w.num_tiers, "first_ratio": w.first_ratio, "decay": w.decay,
-                   "score": "kvnorm", "block_size": bs, "link": args.link, "fp16_bytes": F,
+                   "score": args.score, "block_size": bs, "link": args.link, "fp16_bytes": F,
                    "payload_bytes": codec.payload_bytes},
         "tokens_per_s": round(n / t_codec, 1),
         "alg_gbps": round(alg_gbs, 2),
@@ -158,8 +202,18 @@ def main():
         "unpack_gbps": round(unpack_gbs, 2),
         "roofline": {"bound": "hbm", "kernel": f"skv_{dominant}", "achieved": round(dom_gbs, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(dom_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": None, "bytes_per_launch": dom_bytes},
+                     "traffic": measured_traffic(w.name, dominant), "bytes_per_launch": dom_bytes},
     }
+    if attn:
+        # two passes of Q.K^T over the observation rows: 2 * 2 * L * H * M * n * d flops, K read twice
+        rows = (w.q_heads // H) * args.obs_window
+        flops = 4.0 * L * H * rows * n * d
+        out["config"]["obs_window"] = args.obs_window
+        out["score_attn"] = {"ms": round(stage_ms["score"], 4), "tflops": round(flops / (stage_ms["score"] / 1e3) / 1e12, 2),
+                             "mfma_peak_tflops": 2500.0, "k_read_gbps": round(F / (stage_ms["score"] / 1e3) / 1e9, 2)}
+    else:
+        out["score_kvnorm"] = {"ms": round(stage_ms["score"], 4),
+                               "read_gbps": round(F / (stage_ms["score"] / 1e3) / 1e9, 2)}
     if args.cpu_layers > 0:
         del kc, vc, rx
         torch.cuda.empty_cache()
