@@ -39,6 +39,20 @@ __device__ __forceinline__ void st_nt4(void* p, uint32_t v) {
   __builtin_nontemporal_store(v, reinterpret_cast<uint32_t*>(p));
 }
 
+// Stores that are streaming (non-temporal) or ordinary, chosen at build time.
+template <bool NT>
+__device__ __forceinline__ void store16(void* p, u32x4 v) {
+  if constexpr (NT) st_nt16(p, v); else *reinterpret_cast<u32x4*>(p) = v;
+}
+template <bool NT>
+__device__ __forceinline__ void store8(void* p, u32x2 v) {
+  if constexpr (NT) st_nt8(p, v); else *reinterpret_cast<u32x2*>(p) = v;
+}
+template <bool NT>
+__device__ __forceinline__ void store4(void* p, uint32_t v) {
+  if constexpr (NT) st_nt4(p, v); else *reinterpret_cast<uint32_t*>(p) = v;
+}
+
 // DPP lane move inside 16-lane rows (row_mask/bank_mask all set).
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_mov(uint32_t v) {

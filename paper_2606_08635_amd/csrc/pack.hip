@@ -14,6 +14,14 @@
 namespace skv {
 namespace {
 
+// Build-time tuning knobs (defaults are the measured best on MI355X).
+#ifndef SKV_PACK_ROWS_IN_FLIGHT
+#define SKV_PACK_ROWS_IN_FLIGHT 4
+#endif
+#ifndef SKV_PACK_NT_STORE
+#define SKV_PACK_NT_STORE 1
+#endif
+
 constexpr int kPrepThreads = 1024;
 constexpr int kRowThreads = 256;  // == kChunkTokens: one token per thread in the scan
 constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
@@ -107,7 +115,7 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(
   constexpr int LPR = D / 8;                // lanes per row, 16 bytes each
   constexpr int RPI = kRowThreads / LPR;    // rows per block-wide iteration
   constexpr int ITERS = kChunkTokens / RPI;
-  constexpr int U = ITERS < 4 ? ITERS : 4;  // rows in flight per thread
+  constexpr int U = ITERS < SKV_PACK_ROWS_IN_FLIGHT ? ITERS : SKV_PACK_ROWS_IN_FLIGHT;  // rows in flight per thread
   __shared__ uint8_t s_tier[kChunkTokens];
   __shared__ uint32_t s_off[kChunkTokens];  // byte offset of the row inside its segment
   __shared__ uint32_t s_q[kChunkTokens];    // index of the row's scale
@@ -161,7 +169,7 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(
       const int tr = s_tier[r];
       const uint32_t amax = group_max<LPR>(absmax_bits8(x[u]));  // all lanes take part
       if (tr == kFP16) {
-        st_nt16(dst + s_off[r] + lane * 16, x[u]);
+        store16<SKV_PACK_NT_STORE>(dst + s_off[r] + lane * 16, x[u]);
       } else if (tr == kINT8 || tr == kINT4) {
         const int Q = tr == kINT8 ? 127 : 7;
         const float Qf = static_cast<float>(Q);
@@ -201,12 +209,12 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(
           u32x2 out;
           out.x = (codes[0] & 0xFFu) | ((codes[1] & 0xFFu) << 8) | ((codes[2] & 0xFFu) << 16) | (codes[3] << 24);
           out.y = (codes[4] & 0xFFu) | ((codes[5] & 0xFFu) << 8) | ((codes[6] & 0xFFu) << 16) | (codes[7] << 24);
-          st_nt8(row + lane * 8, out);
+          store8<SKV_PACK_NT_STORE>(row + lane * 8, out);
         } else {
           uint32_t out = 0;
 #pragma unroll
           for (int i = 0; i < 8; ++i) out |= (codes[i] & 0xFu) << (4 * i);
-          st_nt4(row + lane * 4, out);
+          store4<SKV_PACK_NT_STORE>(row + lane * 4, out);
         }
         if (lane == 0) scales[s_q[r]] = scale;
       }

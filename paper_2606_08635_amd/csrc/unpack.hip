@@ -16,6 +16,14 @@
 namespace skv {
 namespace {
 
+// Build-time tuning knobs (defaults are the measured best on MI355X).
+#ifndef SKV_UNPACK_ROWS_IN_FLIGHT
+#define SKV_UNPACK_ROWS_IN_FLIGHT 4
+#endif
+#ifndef SKV_UNPACK_NT_STORE
+#define SKV_UNPACK_NT_STORE 1
+#endif
+
 constexpr int kCheckThreads = 1024;
 constexpr int kRowThreads = 256;
 constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
@@ -115,6 +123,36 @@ __device__ __forceinline__ u32x4 dequant_int4(uint32_t w, float s) {
   return u32x4{o[0], o[1], o[2], o[3]};
 }
 
+
+// Loads one row slice of a lane (16 B of FP16, 8 B of INT8 codes or 4 B of
+// INT4 codes) and its scale.
+__device__ __forceinline__ void load_row(int tr, const uint8_t* row, const float* scale_ptr, int lane,
+                                         u32x4& raw, float& sc) {
+  raw = u32x4{0u, 0u, 0u, 0u};
+  sc = 0.0f;
+  if (tr == kFP16) {
+    raw = ld_nt16(row + lane * 16);
+  } else if (tr == kINT8) {
+    const u32x2 c = ld_nt8(row + lane * 8);
+    raw.x = c.x;
+    raw.y = c.y;
+    sc = *scale_ptr;
+  } else if (tr == kINT4) {
+    raw.x = ld_nt4(row + lane * 4);
+    sc = *scale_ptr;
+  }
+}
+
+// The lane's 8 output elements of a row: FP16 verbatim, DROP zeros, INT8/INT4
+// dequantized, a NaN scale giving 0x7E00.
+__device__ __forceinline__ u32x4 decode_row(int tr, u32x4 raw, float sc) {
+  if (tr == kINT8 || tr == kINT4) {
+    if (__builtin_isnan(sc)) return u32x4{0x7E007E00u, 0x7E007E00u, 0x7E007E00u, 0x7E007E00u};
+    return tr == kINT8 ? dequant_int8(u32x2{raw.x, raw.y}, sc) : dequant_int4(raw.x, sc);
+  }
+  return raw;
+}
+
 template <int D>
 __global__ __launch_bounds__(kRowThreads) void unpack_rows(
     const uint8_t* __restrict__ payload, uint16_t* __restrict__ k_cache,
@@ -125,7 +163,7 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(
   constexpr int LPR = D / 8;
   constexpr int RPI = kRowThreads / LPR;
   constexpr int ITERS = kChunkTokens / RPI;
-  constexpr int U = ITERS < 4 ? ITERS : 4;
+  constexpr int U = ITERS < SKV_UNPACK_ROWS_IN_FLIGHT ? ITERS : SKV_UNPACK_ROWS_IN_FLIGHT;
   __shared__ uint8_t s_tier[kChunkTokens];
   __shared__ uint32_t s_off[kChunkTokens];
   __shared__ uint32_t s_q[kChunkTokens];
@@ -175,38 +213,14 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = (it + u) * RPI + rsub;
-      const int tr = s_tier[r];
-      const uint8_t* row = src + s_off[r];
-      raw[u] = u32x4{0u, 0u, 0u, 0u};
-      sc[u] = 0.0f;
-      if (tr == kFP16) {
-        raw[u] = ld_nt16(row + lane * 16);
-      } else if (tr == kINT8) {
-        const u32x2 c = ld_nt8(row + lane * 8);
-        raw[u].x = c.x;
-        raw[u].y = c.y;
-        sc[u] = scales[s_q[r]];
-      } else if (tr == kINT4) {
-        raw[u].x = ld_nt4(row + lane * 4);
-        sc[u] = scales[s_q[r]];
-      }
+      load_row(s_tier[r], src + s_off[r], scales + s_q[r], lane, raw[u], sc[u]);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = (it + u) * RPI + rsub;
       const int tr = s_tier[r];
       if (tr == kAbsent) continue;
-      u32x4 out = raw[u];  // FP16: verbatim; DROP: zeros
-      if (tr == kINT8 || tr == kINT4) {
-        if (__builtin_isnan(sc[u])) {
-          out = u32x4{0x7E007E00u, 0x7E007E00u, 0x7E007E00u, 0x7E007E00u};
-        } else if (tr == kINT8) {
-          out = dequant_int8(u32x2{raw[u].x, raw[u].y}, sc[u]);
-        } else {
-          out = dequant_int4(raw[u].x, sc[u]);
-        }
-      }
-      st_nt16(cache + static_cast<size_t>(s_pos[r]) * H * D + lane * 8, out);
+      store16<SKV_UNPACK_NT_STORE>(cache + static_cast<size_t>(s_pos[r]) * H * D + lane * 8, decode_row(tr, raw[u], sc[u]));
     }
   }
 }
