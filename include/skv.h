@@ -121,6 +121,21 @@ typedef struct skv_plan {
   int64_t budget_units, used_units;
 } skv_plan;
 
+/* One request of a batched pack or unpack (see skv_pack_batch /
+ * skv_unpack_batch).  Every pointer is device memory, 16-byte aligned except
+ * block_table and dev_status (4-byte aligned). */
+typedef struct skv_request {
+  int32_t num_tokens;         /* n of this request (1 .. 2^21)                     */
+  int32_t reserved;           /* must be 0                                         */
+  const void* k;              /* pack: K, binary16 [L][H][n][d]                    */
+  const void* v;              /* pack: V, binary16 [L][H][n][d]                    */
+  const uint8_t* tier;        /* pack: tier map uint8[n], on plan                  */
+  void* payload;              /* pack: output; unpack: input                       */
+  uint64_t payload_bytes;     /* pack: capacity; unpack: bytes available           */
+  const int32_t* block_table; /* unpack: int32[ceil(n / block_size)]               */
+  uint32_t* dev_status;       /* pack: optional status word; unpack: required      */
+} skv_request;
+
 /* ABI version of the loaded library (SKV_ABI_VERSION at build time). */
 int32_t skv_abi_version(void);
 
@@ -206,6 +221,33 @@ skv_status skv_pack(const skv_config* cfg, const void* k, const void* v, const u
 skv_status skv_unpack(const skv_config* cfg, const void* payload, uint64_t payload_bytes,
                       void* k_cache, void* v_cache, const int32_t* block_table, int32_t num_blocks,
                       int32_t block_size, uint32_t* dev_status, hipStream_t stream);
+
+/* Batched, variable-length pack: `count` requests that share every field of
+ * cfg except num_tokens (ignored; each request carries its own n) are packed
+ * by one launch per kernel (up to 16 requests per launch; larger batches are
+ * split internally), so many short requests fill the GPU.  Only layers
+ * [layer_begin, layer_begin + layer_count) are packed: the payload is
+ * layer-major, so a request can be packed layer by layer and each layer
+ * block (its scales and segments, contiguous in the payload) sent as soon as
+ * it is written.  The call with layer_begin == 0 also validates the tier map
+ * and writes the header, tier map and chunk index; calls for later layers
+ * must follow it in stream order.  Per request, results and errors are those
+ * of skv_pack (status in the header and in dev_status when given).  Every
+ * request is checked before anything is enqueued.  Sec. 9 (future work:
+ * integration with a PD runtime and batching). */
+skv_status skv_pack_batch(const skv_config* cfg, const skv_request* reqs, int32_t count,
+                          int32_t layer_begin, int32_t layer_count, hipStream_t stream);
+
+/* Batched, variable-length unpack into one shared paged cache
+ * [L][num_blocks][block_size][H][d] (each request has its own block table,
+ * the tables must not overlap).  Layer ranges as in skv_pack_batch: the call
+ * with layer_begin == 0 checks every payload and writes each request's
+ * dev_status; calls for later layers (in stream order after it) write
+ * nothing for a request whose status is nonzero.  Per request, results and
+ * errors are those of skv_unpack. */
+skv_status skv_unpack_batch(const skv_config* cfg, const skv_request* reqs, int32_t count,
+                            void* k_cache, void* v_cache, int32_t num_blocks, int32_t block_size,
+                            int32_t layer_begin, int32_t layer_count, hipStream_t stream);
 
 /* Link emulation for a one-GPU setup (Sec. 4.2: the payload crosses the
  * network between prefill and decode).  Copies `bytes` from src to dst on

@@ -97,11 +97,6 @@ inline uint32_t float_bits(float f) {
   return u;
 }
 
-inline void put_u64(HeaderImage* h, int byte_off, uint64_t v) {
-  h->w[byte_off / 4] = static_cast<uint32_t>(v);
-  h->w[byte_off / 4 + 1] = static_cast<uint32_t>(v >> 32);
-}
-
 }  // namespace
 
 skv_status make_geometry(const skv_config* cfg, Geometry* g, skv_plan* plan_out) {
@@ -137,37 +132,6 @@ skv_status make_geometry(const skv_config* cfg, Geometry* g, skv_plan* plan_out)
   return SKV_OK;
 }
 
-void fill_header(const skv_config* cfg, const Geometry& g, HeaderImage* h) {
-  std::memset(h, 0, sizeof(*h));
-  h->w[0] = kMagic;
-  h->w[1] = kVersion;
-  h->w[2] = static_cast<uint32_t>(g.L);
-  h->w[3] = static_cast<uint32_t>(g.H);
-  h->w[4] = static_cast<uint32_t>(g.d);
-  h->w[5] = static_cast<uint32_t>(g.n);
-  h->w[6] = static_cast<uint32_t>(g.n_sink);
-  h->w[7] = static_cast<uint32_t>(cfg->num_tiers);
-  h->w[8] = float_bits(cfg->budget);
-  h->w[9] = float_bits(cfg->first_ratio);
-  h->w[10] = float_bits(cfg->decay);
-  h->w[11] = static_cast<uint32_t>(cfg->score_mode);
-  h->w[12] = static_cast<uint32_t>(g.n16);
-  h->w[13] = static_cast<uint32_t>(g.n8);
-  h->w[14] = static_cast<uint32_t>(g.n4);
-  h->w[15] = static_cast<uint32_t>(g.nd);
-  put_u64(h, 64, static_cast<uint64_t>(g.budget_units));
-  put_u64(h, 72, static_cast<uint64_t>(g.used_units));
-  put_u64(h, 80, g.tiermap_off);
-  put_u64(h, 88, g.chunkidx_off);
-  put_u64(h, 96, g.layers_off);
-  put_u64(h, 104, g.seg_bytes);
-  put_u64(h, 112, g.seg_stride);
-  put_u64(h, 120, g.scales_bytes);
-  put_u64(h, 128, g.layer_stride);
-  put_u64(h, 136, g.total);
-  h->w[152 / 4] = static_cast<uint32_t>(kChunkTokens);
-}
-
 namespace {
 
 uint64_t decay_table_bytes(const skv_config* c) {
@@ -188,6 +152,99 @@ uint64_t scratch_bytes(const skv_config* c) {
 }
 
 inline skv_status launched(hipError_t e) { return e == hipSuccess ? SKV_OK : SKV_ERR_DEVICE; }
+
+void fill_common(const skv_config* cfg, int32_t layer_begin, int32_t layer_count, BatchArgs* a) {
+  std::memset(a, 0, sizeof(*a));
+  a->L = cfg->num_layers;
+  a->H = cfg->num_kv_heads;
+  a->d = cfg->head_dim;
+  a->layer_begin = layer_begin;
+  a->layer_count = layer_count;
+  a->num_tiers = cfg->num_tiers;
+  a->score_mode = cfg->score_mode;
+  a->budget_bits = float_bits(cfg->budget);
+  a->rho_bits = float_bits(cfg->first_ratio);
+  a->decay_bits = float_bits(cfg->decay);
+}
+
+void fill_desc(const Geometry& g, const skv_request& q, ReqDesc* r) {
+  std::memset(r, 0, sizeof(*r));
+  r->k = static_cast<const uint16_t*>(q.k);
+  r->v = static_cast<const uint16_t*>(q.v);
+  r->tier = q.tier;
+  r->payload = static_cast<uint8_t*>(q.payload);
+  r->status = q.dev_status;
+  r->block_table = q.block_table;
+  r->chunkidx_off = g.chunkidx_off;
+  r->layers_off = g.layers_off;
+  r->seg_bytes = g.seg_bytes;
+  r->seg_stride = g.seg_stride;
+  r->scales_bytes = g.scales_bytes;
+  r->layer_stride = g.layer_stride;
+  r->total = g.total;
+  r->nq = g.nq;
+  r->budget_units = g.budget_units;
+  r->used_units = g.used_units;
+  r->n = g.n;
+  r->nchunks = static_cast<int32_t>(g.nchunks);
+  r->n_sink = g.n_sink;
+  r->n16 = g.n16;
+  r->n8 = g.n8;
+  r->n4 = g.n4;
+  r->nd = g.nd;
+}
+
+bool layer_range_ok(const skv_config* cfg, int32_t layer_begin, int32_t layer_count) {
+  return layer_begin >= 0 && layer_count >= 1 &&
+         static_cast<int64_t>(layer_begin) + layer_count <= cfg->num_layers;
+}
+
+// Validates every request (pack: unpack == false) and fills their geometry.
+skv_status check_requests(const skv_config* cfg, const skv_request* reqs, int32_t count, bool unpack,
+                          std::vector<Geometry>* geo) {
+  if (cfg == nullptr || reqs == nullptr || count < 1) return SKV_ERR_INVALID_ARG;
+  geo->resize(static_cast<size_t>(count));
+  for (int32_t i = 0; i < count; ++i) {
+    const skv_request& q = reqs[i];
+    if (q.reserved != 0) return SKV_ERR_INVALID_ARG;
+    skv_config c = *cfg;
+    c.num_tokens = q.num_tokens;
+    const skv_status st = make_geometry(&c, &(*geo)[i], nullptr);
+    if (st != SKV_OK) return st;
+    if (!dev_ptr_ok(q.payload)) return SKV_ERR_INVALID_ARG;
+    if (!unpack) {
+      if (!dev_ptr_ok(q.k) || !dev_ptr_ok(q.v) || !dev_ptr_ok(q.tier)) return SKV_ERR_INVALID_ARG;
+      if (q.dev_status != nullptr && !aligned(q.dev_status, 4)) return SKV_ERR_INVALID_ARG;
+      if (q.payload_bytes < (*geo)[i].total) return SKV_ERR_CAPACITY;
+    } else {
+      if (q.block_table == nullptr || !aligned(q.block_table, 4)) return SKV_ERR_INVALID_ARG;
+      if (q.dev_status == nullptr || !aligned(q.dev_status, 4)) return SKV_ERR_INVALID_ARG;
+      if (q.payload_bytes < (*geo)[i].total) return SKV_ERR_FORMAT;
+    }
+  }
+  return SKV_OK;
+}
+
+// Launches the requests kMaxBatch at a time.
+template <typename Launch>
+skv_status launch_batches(const skv_config* cfg, const skv_request* reqs, int32_t count,
+                          const std::vector<Geometry>& geo, int32_t layer_begin, int32_t layer_count,
+                          Launch launch) {
+  for (int32_t first = 0; first < count; first += kMaxBatch) {
+    BatchArgs a;
+    fill_common(cfg, layer_begin, layer_count, &a);
+    a.count = std::min<int32_t>(kMaxBatch, count - first);
+    uint64_t rows = 0;
+    for (int32_t i = 0; i < a.count; ++i) {
+      const Geometry& g = geo[static_cast<size_t>(first + i)];
+      fill_desc(g, reqs[first + i], &a.r[i]);
+      a.r[i].block_begin = rows;
+      rows += static_cast<uint64_t>(g.nchunks) * 2u * static_cast<uint64_t>(g.H) * static_cast<uint64_t>(layer_count);
+    }
+    if (launch(a, rows) != hipSuccess) return SKV_ERR_DEVICE;
+  }
+  return SKV_OK;
+}
 
 }  // namespace
 }  // namespace skv
@@ -284,39 +341,60 @@ skv_status skv_assign_tiers(const skv_config* cfg, const double* score, uint8_t*
   return launched(launch_assign(g, score, tier, stream));
 }
 
+skv_status skv_pack_batch(const skv_config* cfg, const skv_request* reqs, int32_t count,
+                          int32_t layer_begin, int32_t layer_count, hipStream_t stream) {
+  std::vector<Geometry> geo;
+  const skv_status st = check_requests(cfg, reqs, count, false, &geo);
+  if (st != SKV_OK) return st;
+  if (!layer_range_ok(cfg, layer_begin, layer_count)) return SKV_ERR_INVALID_ARG;
+  return launch_batches(cfg, reqs, count, geo, layer_begin, layer_count,
+                        [&](const BatchArgs& a, uint64_t rows) { return launch_pack(a, rows, stream); });
+}
+
+skv_status skv_unpack_batch(const skv_config* cfg, const skv_request* reqs, int32_t count, void* k_cache,
+                            void* v_cache, int32_t num_blocks, int32_t block_size, int32_t layer_begin,
+                            int32_t layer_count, hipStream_t stream) {
+  std::vector<Geometry> geo;
+  const skv_status st = check_requests(cfg, reqs, count, true, &geo);
+  if (st != SKV_OK) return st;
+  if (!layer_range_ok(cfg, layer_begin, layer_count)) return SKV_ERR_INVALID_ARG;
+  if (!dev_ptr_ok(k_cache) || !dev_ptr_ok(v_cache)) return SKV_ERR_INVALID_ARG;
+  if (num_blocks < 1 || block_size < 1) return SKV_ERR_INVALID_ARG;
+  if (static_cast<uint64_t>(num_blocks) * static_cast<uint64_t>(block_size) > 0xFFFFFFFFull)
+    return SKV_ERR_INVALID_ARG;
+  return launch_batches(cfg, reqs, count, geo, layer_begin, layer_count, [&](const BatchArgs& a, uint64_t rows) {
+    return launch_unpack(a, rows, static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache), num_blocks,
+                         block_size, stream);
+  });
+}
+
 skv_status skv_pack(const skv_config* cfg, const void* k, const void* v, const uint8_t* tier,
                     void* payload, uint64_t capacity, uint32_t* dev_status, hipStream_t stream) {
-  Geometry g;
-  const skv_status st = make_geometry(cfg, &g, nullptr);
-  if (st != SKV_OK) return st;
-  if (!dev_ptr_ok(k) || !dev_ptr_ok(v) || !dev_ptr_ok(tier) || !dev_ptr_ok(payload))
-    return SKV_ERR_INVALID_ARG;
-  if (dev_status != nullptr && !aligned(dev_status, 4)) return SKV_ERR_INVALID_ARG;
-  if (capacity < g.total) return SKV_ERR_CAPACITY;
-  HeaderImage hdr;
-  fill_header(cfg, g, &hdr);
-  return launched(launch_pack(g, hdr, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), tier,
-                              static_cast<uint8_t*>(payload), dev_status, stream));
+  if (cfg == nullptr) return SKV_ERR_INVALID_ARG;
+  skv_request q;
+  std::memset(&q, 0, sizeof(q));
+  q.num_tokens = cfg->num_tokens;
+  q.k = k;
+  q.v = v;
+  q.tier = tier;
+  q.payload = payload;
+  q.payload_bytes = capacity;
+  q.dev_status = dev_status;
+  return skv_pack_batch(cfg, &q, 1, 0, cfg->num_layers, stream);
 }
 
 skv_status skv_unpack(const skv_config* cfg, const void* payload, uint64_t payload_bytes,
                       void* k_cache, void* v_cache, const int32_t* block_table, int32_t num_blocks,
                       int32_t block_size, uint32_t* dev_status, hipStream_t stream) {
-  Geometry g;
-  const skv_status st = make_geometry(cfg, &g, nullptr);
-  if (st != SKV_OK) return st;
-  if (!dev_ptr_ok(payload) || !dev_ptr_ok(k_cache) || !dev_ptr_ok(v_cache)) return SKV_ERR_INVALID_ARG;
-  if (block_table == nullptr || !aligned(block_table, 4)) return SKV_ERR_INVALID_ARG;
-  if (dev_status == nullptr || !aligned(dev_status, 4)) return SKV_ERR_INVALID_ARG;
-  if (num_blocks < 1 || block_size < 1) return SKV_ERR_INVALID_ARG;
-  if (static_cast<uint64_t>(num_blocks) * static_cast<uint64_t>(block_size) > 0xFFFFFFFFull)
-    return SKV_ERR_INVALID_ARG;
-  if (payload_bytes < g.total) return SKV_ERR_FORMAT;
-  HeaderImage hdr;
-  fill_header(cfg, g, &hdr);
-  return launched(launch_unpack(g, hdr, static_cast<const uint8_t*>(payload), static_cast<uint16_t*>(k_cache),
-                                static_cast<uint16_t*>(v_cache), block_table, num_blocks, block_size,
-                                dev_status, stream));
+  if (cfg == nullptr) return SKV_ERR_INVALID_ARG;
+  skv_request q;
+  std::memset(&q, 0, sizeof(q));
+  q.num_tokens = cfg->num_tokens;
+  q.payload = const_cast<void*>(payload);
+  q.payload_bytes = payload_bytes;
+  q.block_table = block_table;
+  q.dev_status = dev_status;
+  return skv_unpack_batch(cfg, &q, 1, k_cache, v_cache, num_blocks, block_size, 0, cfg->num_layers, stream);
 }
 
 skv_status skv_link(void* dst, const void* src, uint64_t bytes, void* host_staging,

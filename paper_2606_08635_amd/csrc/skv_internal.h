@@ -26,12 +26,31 @@ struct Geometry {
   uint64_t seg_bytes, seg_stride, scales_bytes, layer_stride, total;
 };
 
-struct HeaderImage {
-  uint32_t w[64];  // the 256-byte payload header, as written by pack
+skv_status make_geometry(const skv_config* cfg, Geometry* g, skv_plan* plan_out);
+
+// One request of a pack/unpack launch: its buffers and payload geometry.
+struct ReqDesc {
+  const uint16_t* k;
+  const uint16_t* v;
+  const uint8_t* tier;
+  uint8_t* payload;
+  uint32_t* status;             // may be null for pack
+  const int32_t* block_table;   // unpack only
+  uint64_t block_begin;         // first flat workgroup of this request in the row launch
+  uint64_t chunkidx_off, layers_off, seg_bytes, seg_stride, scales_bytes, layer_stride, total;
+  int64_t nq, budget_units, used_units;
+  int32_t n, nchunks, n_sink, n16, n8, n4, nd, pad;
 };
 
-skv_status make_geometry(const skv_config* cfg, Geometry* g, skv_plan* plan_out);
-void fill_header(const skv_config* cfg, const Geometry& g, HeaderImage* h);
+constexpr int kMaxBatch = 16;  // requests per launch (descriptors travel as kernel arguments)
+
+// Everything a batched launch needs; fits the 4 KiB kernel-argument limit.
+struct BatchArgs {
+  int32_t count, L, H, d, layer_begin, layer_count, num_tiers, score_mode;
+  uint32_t budget_bits, rho_bits, decay_bits, pad;
+  ReqDesc r[kMaxBatch];
+};
+static_assert(sizeof(BatchArgs) <= 4000, "kernel arguments");
 
 // Kernel launchers.  Each returns the launch status; none synchronizes.
 hipError_t launch_score_kvnorm(const Geometry& g, const uint16_t* k, const uint16_t* v,
@@ -49,13 +68,12 @@ uint64_t attn_scratch_bytes(const Geometry& g, int32_t Hq, int32_t W);
 hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier,
                          hipStream_t stream);
 
-hipError_t launch_pack(const Geometry& g, const HeaderImage& hdr, const uint16_t* k,
-                       const uint16_t* v, const uint8_t* tier, uint8_t* payload,
-                       uint32_t* dev_status, hipStream_t stream);
-
-hipError_t launch_unpack(const Geometry& g, const HeaderImage& hdr, const uint8_t* payload,
-                         uint16_t* k_cache, uint16_t* v_cache, const int32_t* block_table,
-                         int32_t num_blocks, int32_t block_size, uint32_t* dev_status,
-                         hipStream_t stream);
+// Batched launches over a.count requests and layers [layer_begin, layer_begin +
+// layer_count); `rows` is the total number of row workgroups (sum of
+// nchunks * 2 * H * layer_count).  Pack writes the metadata when layer_begin
+// is 0; unpack checks the payloads when layer_begin is 0.
+hipError_t launch_pack(const BatchArgs& a, uint64_t rows, hipStream_t stream);
+hipError_t launch_unpack(const BatchArgs& a, uint64_t rows, uint16_t* k_cache, uint16_t* v_cache,
+                         int32_t num_blocks, int32_t block_size, hipStream_t stream);
 
 }  // namespace skv

@@ -93,4 +93,66 @@ __device__ __forceinline__ uint64_t block_exclusive_scan_1024(uint64_t x, uint64
   return base + inc - x;
 }
 
+// Word i (0..63) of the 256-byte payload header of request r, as pack writes it
+// (non-finite row count and status zero).  Layout: 0 magic, 1 version, 2..5
+// L, H, d, n, 6 sinks, 7 tiers, 8..10 budget / first-ratio / decay bits,
+// 11 score mode, 12..15 tier counts, 16..35 u64 budget units, used units,
+// tier-map, chunk-index and layer-0 offsets, segment bytes, segment stride,
+// scale bytes, layer stride, total bytes; 36 non-finite rows, 37 status,
+// 38 tokens per chunk.
+__device__ __forceinline__ uint32_t header_word(const BatchArgs& a, const ReqDesc& r, int i) {
+  auto lo = [](uint64_t x) { return static_cast<uint32_t>(x); };
+  auto hi = [](uint64_t x) { return static_cast<uint32_t>(x >> 32); };
+  switch (i) {
+    case 0: return kMagic;
+    case 1: return kVersion;
+    case 2: return static_cast<uint32_t>(a.L);
+    case 3: return static_cast<uint32_t>(a.H);
+    case 4: return static_cast<uint32_t>(a.d);
+    case 5: return static_cast<uint32_t>(r.n);
+    case 6: return static_cast<uint32_t>(r.n_sink);
+    case 7: return static_cast<uint32_t>(a.num_tiers);
+    case 8: return a.budget_bits;
+    case 9: return a.rho_bits;
+    case 10: return a.decay_bits;
+    case 11: return static_cast<uint32_t>(a.score_mode);
+    case 12: return static_cast<uint32_t>(r.n16);
+    case 13: return static_cast<uint32_t>(r.n8);
+    case 14: return static_cast<uint32_t>(r.n4);
+    case 15: return static_cast<uint32_t>(r.nd);
+    case 16: return lo(static_cast<uint64_t>(r.budget_units));
+    case 17: return hi(static_cast<uint64_t>(r.budget_units));
+    case 18: return lo(static_cast<uint64_t>(r.used_units));
+    case 19: return hi(static_cast<uint64_t>(r.used_units));
+    case 20: return 256u;  // tier map right after the header
+    case 21: return 0u;
+    case 22: return lo(r.chunkidx_off);
+    case 23: return hi(r.chunkidx_off);
+    case 24: return lo(r.layers_off);
+    case 25: return hi(r.layers_off);
+    case 26: return lo(r.seg_bytes);
+    case 27: return hi(r.seg_bytes);
+    case 28: return lo(r.seg_stride);
+    case 29: return hi(r.seg_stride);
+    case 30: return lo(r.scales_bytes);
+    case 31: return hi(r.scales_bytes);
+    case 32: return lo(r.layer_stride);
+    case 33: return hi(r.layer_stride);
+    case 34: return lo(r.total);
+    case 35: return hi(r.total);
+    case 38: return static_cast<uint32_t>(kChunkTokens);
+    default: return 0u;
+  }
+}
+constexpr int kHdrNonfinite = 36;
+constexpr int kHdrStatus = 37;
+
+// The request that owns flat workgroup `bid` of a batched row launch.
+__device__ __forceinline__ int request_of_block(const BatchArgs& a, uint64_t bid) {
+  int r = 0;
+  for (int i = 1; i < a.count; ++i)
+    if (a.r[i].block_begin <= bid) r = i;
+  return r;
+}
+
 }  // namespace skv

@@ -1,14 +1,16 @@
 // Decode-side dequantization into the fp16 paged cache (Sec. 4.2: only a
 // lightweight per-tier dequantization runs after receipt).
 //
-// unpack_check (one workgroup) compares the payload header with the one the
-// configuration implies, recounts the 2-bit tier map, re-derives the chunk
-// index and range-checks the block table; it writes the verdict to
-// *dev_status.  unpack_rows (one workgroup per 256-token chunk of one
-// (layer, K/V, head) segment) does nothing unless the verdict is 0; it
-// rebuilds the chunk's row offsets with a block scan, loads each row at its
-// tier's width, dequantizes in registers (RN16(RN32(code * scale))) and
-// writes 16 bytes per lane into the token's paged slot.
+// unpack_check (one workgroup per request) compares the payload header with
+// the one the configuration implies, recounts the 2-bit tier map, re-derives
+// the chunk index and range-checks the block table; it writes the verdict to
+// the request's status word.  unpack_rows (one workgroup per 256-token chunk
+// of one (layer, K/V, head) segment of one request) does nothing unless the
+// verdict is 0; it rebuilds the chunk's row offsets with a block scan, loads
+// each row at its tier's width, dequantizes in registers
+// (RN16(RN32(code * scale))) and writes 16 bytes per lane into the token's
+// paged slot.  Requests of a launch share the paged cache (each has its own
+// block table); a launch may cover a range of layers.
 #include "device_util.h"
 #include "skv_internal.h"
 #include "tier_groups.h"
@@ -27,18 +29,18 @@ namespace {
 constexpr int kCheckThreads = 1024;
 constexpr int kRowThreads = 256;
 constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
-constexpr int kHdrNonfinite = 144 / 4;
 constexpr int kAbsent = 4;  // slot past the end of the request
 
-__global__ __launch_bounds__(kCheckThreads) void unpack_check(
-    const uint8_t* __restrict__ payload, HeaderImage want, int n, int nchunks, int want16,
-    int want8, int want4, int wantd, uint64_t tiermap_off, uint64_t chunkidx_off,
-    const int32_t* __restrict__ block_table, int num_blocks, int block_size,
-    uint32_t* __restrict__ dev_status) {
+// grid: one workgroup per request
+__global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a, int num_blocks,
+                                                              int block_size) {
   __shared__ uint32_t s_chunk[kMaxChunks];
   __shared__ uint32_t s_cnt[4];
   __shared__ uint32_t s_bad;
   __shared__ uint64_t s_scan[16];
+  const ReqDesc& r = a.r[blockIdx.x];
+  const uint8_t* __restrict__ payload = r.payload;
+  const int n = r.n, nchunks = r.nchunks;
   const int tid = threadIdx.x;
   if (tid < 4) s_cnt[tid] = 0;
   if (tid == 0) s_bad = 0;
@@ -46,23 +48,23 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(
   bool bad = false;
   // header: every word but the non-finite row counter must match
   if (tid < 64 && tid != kHdrNonfinite)
-    bad |= reinterpret_cast<const uint32_t*>(payload)[tid] != want.w[tid];
+    bad |= reinterpret_cast<const uint32_t*>(payload)[tid] != header_word(a, r, tid);
   // block table entries in range
   const int nbt = (n + block_size - 1) / block_size;
   for (int i = tid; i < nbt; i += kCheckThreads) {
-    const int b = block_table[i];
+    const int b = r.block_table[i];
     bad |= b < 0 || b >= num_blocks;
   }
   if (bad) atomicOr(&s_bad, 1u);
   __syncthreads();
   if (s_bad) {  // header or table wrong: do not interpret the rest
-    if (tid == 0) *dev_status = static_cast<uint32_t>(SKV_ERR_FORMAT);
+    if (tid == 0) *r.status = static_cast<uint32_t>(SKV_ERR_FORMAT);
     return;
   }
   // tier counts and chunk sums from the 2-bit map
   const int ngroups = (n + kGroupTokens - 1) / kGroupTokens;
   uint32_t cnt[4] = {0, 0, 0, 0};
-  const uint8_t* map = payload + tiermap_off;
+  const uint8_t* map = payload + 256;
   for (int base = 0; base < ngroups; base += kCheckThreads) {
     const int g = base + tid;
     const TierGroup gi = g < ngroups ? group_from_map(map, n, g) : empty_group();
@@ -75,8 +77,8 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(
   for (int i = 0; i < 4; ++i)
     if (cnt[i]) atomicAdd(&s_cnt[i], cnt[i]);
   __syncthreads();
-  bad = s_cnt[0] != static_cast<uint32_t>(want16) || s_cnt[1] != static_cast<uint32_t>(want8) ||
-        s_cnt[2] != static_cast<uint32_t>(want4) || s_cnt[3] != static_cast<uint32_t>(wantd);
+  bad = s_cnt[0] != static_cast<uint32_t>(r.n_sink + r.n16) || s_cnt[1] != static_cast<uint32_t>(r.n8) ||
+        s_cnt[2] != static_cast<uint32_t>(r.n4) || s_cnt[3] != static_cast<uint32_t>(r.nd);
   // chunk index must equal the running sums
   const int per = (nchunks + kCheckThreads - 1) / kCheckThreads;
   const int c0 = min(nchunks, tid * per), c1 = min(nchunks, c0 + per);
@@ -84,7 +86,7 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(
   for (int c = c0; c < c1; ++c) run += (s_chunk[c] & 0xFFFFu) | (static_cast<uint64_t>(s_chunk[c] >> 16) << 32);
   const uint64_t ex = block_exclusive_scan_1024(run, s_scan);
   uint32_t ru = static_cast<uint32_t>(ex), rq = static_cast<uint32_t>(ex >> 32);
-  const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + chunkidx_off);
+  const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off);
   for (int c = c0; c < c1; ++c) {
     bad |= cidx[2 * c] != ru || cidx[2 * c + 1] != rq;
     ru += s_chunk[c] & 0xFFFFu;
@@ -92,7 +94,7 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(
   }
   if (bad) atomicOr(&s_bad, 1u);
   __syncthreads();
-  if (tid == 0) *dev_status = s_bad ? static_cast<uint32_t>(SKV_ERR_FORMAT) : 0u;
+  if (tid == 0) *r.status = s_bad ? static_cast<uint32_t>(SKV_ERR_FORMAT) : 0u;
 }
 
 // 8 signed codes (INT8: one per byte; INT4: one per nibble, element 2i low)
@@ -153,13 +155,11 @@ __device__ __forceinline__ u32x4 decode_row(int tr, u32x4 raw, float sc) {
   return raw;
 }
 
+// grid: sum over requests of nchunks * 2 * H * layer_count workgroups
 template <int D>
-__global__ __launch_bounds__(kRowThreads) void unpack_rows(
-    const uint8_t* __restrict__ payload, uint16_t* __restrict__ k_cache,
-    uint16_t* __restrict__ v_cache, const int32_t* __restrict__ block_table, int num_blocks,
-    int block_size, int n, int H, int nchunks, int64_t nq, uint64_t tiermap_off,
-    uint64_t chunkidx_off, uint64_t layers_off, uint64_t scales_bytes, uint64_t seg_stride,
-    uint64_t layer_stride, const uint32_t* __restrict__ dev_status) {
+__global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, uint16_t* __restrict__ k_cache,
+                                                           uint16_t* __restrict__ v_cache, int num_blocks,
+                                                           int block_size) {
   constexpr int LPR = D / 8;
   constexpr int RPI = kRowThreads / LPR;
   constexpr int ITERS = kChunkTokens / RPI;
@@ -170,27 +170,32 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(
   __shared__ uint32_t s_pos[kChunkTokens];  // physical block * block_size + slot
   __shared__ uint32_t s_scan[4];
 
-  if (*dev_status != 0u) return;  // payload rejected: write nothing
+  const uint64_t bid = blockIdx.x;
+  const ReqDesc& r = a.r[request_of_block(a, bid)];
+  if (*r.status != 0u) return;  // payload rejected: write nothing
 
-  const int chunk = blockIdx.x % nchunks;
-  const int seg = blockIdx.x / nchunks;
+  const uint8_t* __restrict__ payload = r.payload;
+  const int n = r.n, H = a.H, nchunks = r.nchunks;
+  const uint64_t local = bid - r.block_begin;
+  const int chunk = static_cast<int>(local % nchunks);
+  const int seg = static_cast<int>(local / nchunks);
   const int h = seg % H;
   const int kv = (seg / H) & 1;
-  const int l = seg / (2 * H);
+  const int l = a.layer_begin + seg / (2 * H);
   const int t0 = chunk * kChunkTokens;
   {
     const int t = t0 + threadIdx.x;
     int tr = kAbsent;
     uint32_t pos = 0;
     if (t < n) {
-      tr = (payload[tiermap_off + (t >> 2)] >> (2 * (t & 3))) & 3;
-      pos = static_cast<uint32_t>(block_table[t / block_size]) * static_cast<uint32_t>(block_size) +
+      tr = (payload[256 + (t >> 2)] >> (2 * (t & 3))) & 3;
+      pos = static_cast<uint32_t>(r.block_table[t / block_size]) * static_cast<uint32_t>(block_size) +
             static_cast<uint32_t>(t % block_size);
     }
     const uint32_t packed = tr == kAbsent ? 0u : (tier_units(tr) | (tier_quant(tr) << 16));
     uint32_t total;
     const uint32_t ex = block_exclusive_scan_256(packed, s_scan, &total);
-    const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + chunkidx_off) + 2 * chunk;
+    const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off) + 2 * chunk;
     s_tier[threadIdx.x] = static_cast<uint8_t>(tr);
     s_off[threadIdx.x] = (cidx[0] + (ex & 0xFFFFu)) * static_cast<uint32_t>(D / 2);
     s_q[threadIdx.x] = cidx[1] + (ex >> 16);
@@ -198,9 +203,9 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(
   }
   __syncthreads();
 
-  const uint8_t* lay = payload + layers_off + static_cast<uint64_t>(l) * layer_stride;
-  const uint8_t* src = lay + scales_bytes + static_cast<uint64_t>(kv * H + h) * seg_stride;
-  const float* scales = reinterpret_cast<const float*>(lay) + static_cast<uint64_t>(kv * H + h) * nq;
+  const uint8_t* lay = payload + r.layers_off + static_cast<uint64_t>(l) * r.layer_stride;
+  const uint8_t* src = lay + r.scales_bytes + static_cast<uint64_t>(kv * H + h) * r.seg_stride;
+  const float* scales = reinterpret_cast<const float*>(lay) + static_cast<uint64_t>(kv * H + h) * r.nq;
   uint16_t* cache = (kv ? v_cache : k_cache) + static_cast<size_t>(l) * num_blocks * block_size * H * D +
                     static_cast<size_t>(h) * D;
 
@@ -227,28 +232,20 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(
 
 }  // namespace
 
-hipError_t launch_unpack(const Geometry& g, const HeaderImage& hdr, const uint8_t* payload,
-                         uint16_t* k_cache, uint16_t* v_cache, const int32_t* block_table,
-                         int32_t num_blocks, int32_t block_size, uint32_t* dev_status,
-                         hipStream_t stream) {
-  const int nch = static_cast<int>(g.nchunks);
-  unpack_check<<<1, kCheckThreads, 0, stream>>>(payload, hdr, g.n, nch, g.n_sink + g.n16, g.n8,
-                                                 g.n4, g.nd, g.tiermap_off, g.chunkidx_off,
-                                                 block_table, num_blocks, block_size, dev_status);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const uint64_t blocks = static_cast<uint64_t>(g.nchunks) * 2u * g.L * g.H;
-#define SKV_UNPACK_ARGS payload, k_cache, v_cache, block_table, num_blocks, block_size, g.n, g.H, nch, \
-                        g.nq, g.tiermap_off, g.chunkidx_off, g.layers_off, g.scales_bytes,           \
-                        g.seg_stride, g.layer_stride, dev_status
-  switch (g.d) {
-    case 32: unpack_rows<32><<<blocks, kRowThreads, 0, stream>>>(SKV_UNPACK_ARGS); break;
-    case 64: unpack_rows<64><<<blocks, kRowThreads, 0, stream>>>(SKV_UNPACK_ARGS); break;
-    case 128: unpack_rows<128><<<blocks, kRowThreads, 0, stream>>>(SKV_UNPACK_ARGS); break;
-    case 256: unpack_rows<256><<<blocks, kRowThreads, 0, stream>>>(SKV_UNPACK_ARGS); break;
+hipError_t launch_unpack(const BatchArgs& a, uint64_t rows, uint16_t* k_cache, uint16_t* v_cache,
+                         int32_t num_blocks, int32_t block_size, hipStream_t stream) {
+  if (a.layer_begin == 0) {
+    unpack_check<<<a.count, kCheckThreads, 0, stream>>>(a, num_blocks, block_size);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  switch (a.d) {
+    case 32: unpack_rows<32><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size); break;
+    case 64: unpack_rows<64><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size); break;
+    case 128: unpack_rows<128><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size); break;
+    case 256: unpack_rows<256><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size); break;
     default: return hipErrorInvalidValue;
   }
-#undef SKV_UNPACK_ARGS
   return hipGetLastError();
 }
 

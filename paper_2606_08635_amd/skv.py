@@ -21,7 +21,7 @@ KVNORM, ATTN, RECENCY = 0, 1, 2
 
 EXPORTED = ("skv_abi_version", "skv_status_string", "skv_plan_tiers", "skv_payload_size",
             "skv_workspace_size", "skv_prepare", "skv_score", "skv_assign_tiers", "skv_pack",
-            "skv_unpack", "skv_link")
+            "skv_unpack", "skv_pack_batch", "skv_unpack_batch", "skv_link")
 
 
 class SkvError(RuntimeError):
@@ -37,6 +37,13 @@ class Config(ctypes.Structure):
                 ("num_sink", ctypes.c_int32), ("decay", ctypes.c_float),
                 ("num_tiers", ctypes.c_int32), ("score_mode", ctypes.c_int32),
                 ("num_q_heads", ctypes.c_int32), ("obs_window", ctypes.c_int32)]
+
+
+class Request(ctypes.Structure):
+    _fields_ = [("num_tokens", ctypes.c_int32), ("reserved", ctypes.c_int32), ("k", ctypes.c_void_p),
+                ("v", ctypes.c_void_p), ("tier", ctypes.c_void_p), ("payload", ctypes.c_void_p),
+                ("payload_bytes", ctypes.c_uint64), ("block_table", ctypes.c_void_p),
+                ("dev_status", ctypes.c_void_p)]
 
 
 class Plan(ctypes.Structure):
@@ -71,6 +78,8 @@ def lib():
             "skv_pack": (ctypes.c_int, [cfgp, vp, vp, vp, vp, u64, vp, vp]),
             "skv_unpack": (ctypes.c_int, [cfgp, vp, u64, vp, vp, vp, i32, i32, vp, vp]),
             "skv_link": (ctypes.c_int, [vp, vp, u64, vp, vp]),
+            "skv_pack_batch": (ctypes.c_int, [cfgp, P(Request), i32, i32, i32, vp]),
+            "skv_unpack_batch": (ctypes.c_int, [cfgp, P(Request), i32, vp, vp, i32, i32, i32, i32, vp]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -185,6 +194,59 @@ def unpack(cfg: Config, payload: torch.Tensor, k_cache: torch.Tensor, v_cache: t
                             _dev(v_cache, torch.float16, v_cache.numel(), "v_cache"),
                             _dev(block_table, torch.int32, nbt, "block_table"), nb, block_size,
                             _dev(dev_status, torch.int32, 1, "dev_status"), _stream(stream)), "skv_unpack")
+
+
+def _with_tokens(cfg: Config, n: int) -> Config:
+    c = Config.from_buffer_copy(cfg)
+    c.num_tokens = n
+    return c
+
+
+def pack_batch(cfg: Config, ks, vs, tiers, payloads, statuses=None, layer_begin=0, layer_count=None,
+               stream=None):
+    """Packs len(ks) requests (n taken from each tier map's length) in batched launches."""
+    count = len(ks)
+    reqs = (Request * count)()
+    for i in range(count):
+        n = tiers[i].numel()
+        c = _with_tokens(cfg, n)
+        kv_n = _kv_numel(c)
+        reqs[i].num_tokens = n
+        reqs[i].k = _dev(ks[i], torch.float16, kv_n, "k").value
+        reqs[i].v = _dev(vs[i], torch.float16, kv_n, "v").value
+        reqs[i].tier = _dev(tiers[i], torch.uint8, n, "tier").value
+        reqs[i].payload = _dev(payloads[i], torch.uint8, 0, "payload").value
+        reqs[i].payload_bytes = payloads[i].numel()
+        if statuses is not None:
+            reqs[i].dev_status = _dev(statuses[i], torch.int32, 1, "dev_status").value
+    lc = cfg.num_layers - layer_begin if layer_count is None else layer_count
+    _check(lib().skv_pack_batch(ctypes.byref(cfg), reqs, count, layer_begin, lc, _stream(stream)),
+           "skv_pack_batch")
+
+
+def unpack_batch(cfg: Config, payloads, token_counts, block_tables, k_cache: torch.Tensor,
+                 v_cache: torch.Tensor, block_size: int, statuses, layer_begin=0, layer_count=None,
+                 stream=None):
+    """Unpacks len(payloads) requests into one shared paged cache in batched launches."""
+    if k_cache.dim() != 5 or k_cache.shape[2] != block_size or tuple(k_cache.shape) != tuple(v_cache.shape):
+        raise ValueError("caches must be [L][num_blocks][block_size][H][d] and alike")
+    L, nb, _, H, d = k_cache.shape
+    if (L, H, d) != (cfg.num_layers, cfg.num_kv_heads, cfg.head_dim):
+        raise ValueError("cache shape does not match the configuration")
+    count = len(payloads)
+    reqs = (Request * count)()
+    for i in range(count):
+        n = int(token_counts[i])
+        reqs[i].num_tokens = n
+        reqs[i].payload = _dev(payloads[i], torch.uint8, 0, "payload").value
+        reqs[i].payload_bytes = payloads[i].numel()
+        reqs[i].block_table = _dev(block_tables[i], torch.int32, -(-n // block_size), "block_table").value
+        reqs[i].dev_status = _dev(statuses[i], torch.int32, 1, "dev_status").value
+    lc = cfg.num_layers - layer_begin if layer_count is None else layer_count
+    _check(lib().skv_unpack_batch(ctypes.byref(cfg), reqs, count,
+                                  _dev(k_cache, torch.float16, k_cache.numel(), "k_cache"),
+                                  _dev(v_cache, torch.float16, v_cache.numel(), "v_cache"), nb, block_size,
+                                  layer_begin, lc, _stream(stream)), "skv_unpack_batch")
 
 
 def link(dst: torch.Tensor, src: torch.Tensor, nbytes: int, host_staging: Optional[torch.Tensor] = None,

@@ -117,3 +117,32 @@ def test_host_side_argument_errors(lib):
     assert L.skv_score(ctypes.byref(attn), fake, fake, None, fake, fake, None) == skv.ERR_INVALID_ARG
     for s in range(6):
         assert skv.status_string(s)
+
+
+def test_batch_argument_errors(lib):
+    cfg = skv.config(2, 2, 64, 300, 0.5)
+    fake = 1 << 20
+    reqs = (skv.Request * 2)()
+    for i, n in enumerate((300, 77)):
+        c = skv.config(2, 2, 64, n, 0.5)
+        reqs[i].num_tokens, reqs[i].k, reqs[i].v, reqs[i].tier, reqs[i].payload = n, fake, fake, fake, fake
+        reqs[i].payload_bytes = skv.payload_size(c)
+        reqs[i].block_table, reqs[i].dev_status = fake, fake
+    by = ctypes.byref(cfg)
+    L = lib
+    # every check happens before any device work: the first failing request decides
+    reqs[1].payload_bytes -= 1
+    assert L.skv_pack_batch(by, reqs, 2, 0, 2, None) == skv.ERR_CAPACITY
+    assert L.skv_unpack_batch(by, reqs, 2, fake, fake, 100, 16, 0, 2, None) == skv.ERR_FORMAT
+    reqs[1].payload_bytes += 1
+    assert L.skv_pack_batch(by, reqs, 0, 0, 2, None) == skv.ERR_INVALID_ARG
+    assert L.skv_pack_batch(by, reqs, 2, 1, 2, None) == skv.ERR_INVALID_ARG   # layers past L
+    assert L.skv_pack_batch(by, reqs, 2, 0, 0, None) == skv.ERR_INVALID_ARG
+    reqs[0].reserved = 1
+    assert L.skv_pack_batch(by, reqs, 2, 0, 2, None) == skv.ERR_INVALID_ARG
+    reqs[0].reserved = 0
+    reqs[1].num_tokens = 0
+    assert L.skv_pack_batch(by, reqs, 2, 0, 2, None) == skv.ERR_INVALID_ARG
+    reqs[1].num_tokens = 77
+    reqs[1].dev_status = None
+    assert L.skv_unpack_batch(by, reqs, 2, fake, fake, 100, 16, 0, 2, None) == skv.ERR_INVALID_ARG

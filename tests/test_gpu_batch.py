@@ -1,0 +1,120 @@
+"""Batched, variable-length pack/unpack and layer-range calls vs the oracle.
+
+A batch of requests with different lengths packs to the same bytes as each
+request on its own (checked against the oracle's payloads), unpacks into one
+shared paged cache exactly as the oracle unpacks each request, batches larger
+than one launch's 16 requests are split transparently, a payload that fails
+its check only disables its own request, and packing or unpacking layer by
+layer in several calls gives the same bytes as one call.
+"""
+import pytest
+
+from gpu_helpers import *  # noqa: F401,F403
+
+pytestmark = pytest.mark.gpu
+
+L, H, d, B, TIERS = 2, 2, 64, 0.4, 3
+
+
+def _requests(lengths, seed0=0):
+    out = []
+    for i, n in enumerate(lengths):
+        cfg, ocfg = configs(L, H, d, n, B, TIERS)
+        k, v = workloads.make_kv(L, H, n, d, seed=seed0 + 16 * i)
+        key = oracle.score(ocfg, u16(k), u16(v))
+        tier = oracle.assign(ocfg, key)
+        out.append(dict(n=n, cfg=cfg, ocfg=ocfg, k=k, v=v, tier=tier, payload=oracle.pack(ocfg, u16(k), u16(v), tier)))
+    return out
+
+
+def _pool_tables(lengths, bs, seed):
+    nbs = [workloads.blocks_for(n, bs) for n in lengths]
+    pool = sum(nbs) + 3
+    perm = workloads.make_block_table(pool * bs, bs, pool, seed=seed)
+    tables, start = [], 0
+    for nb in nbs:
+        tables.append(perm[start:start + nb].contiguous())
+        start += nb
+    return pool, tables
+
+
+def _gpu_pack(reqs, layer_ranges=None):
+    cfg = reqs[0]["cfg"]
+    ks = [r["k"].cuda() for r in reqs]
+    vs = [r["v"].cuda() for r in reqs]
+    tiers = [torch.from_numpy(r["tier"]).cuda() for r in reqs]
+    pays = [torch.empty(r["payload"].size, dtype=torch.uint8, device="cuda") for r in reqs]
+    sts = [torch.full((1,), -1, dtype=torch.int32, device="cuda") for _ in reqs]
+    for lb, lc in (layer_ranges or [(0, L)]):
+        skv.pack_batch(cfg, ks, vs, tiers, pays, sts, layer_begin=lb, layer_count=lc)
+    torch.cuda.synchronize()
+    return pays, [int(s.item()) for s in sts]
+
+
+def _gpu_unpack(reqs, pays, tables, pool, bs, layer_ranges=None):
+    cfg = reqs[0]["cfg"]
+    kc, vc = caches(L, pool, bs, H, d, "cuda")
+    sts = [torch.full((1,), -1, dtype=torch.int32, device="cuda") for _ in reqs]
+    for lb, lc in (layer_ranges or [(0, L)]):
+        skv.unpack_batch(cfg, pays, [r["n"] for r in reqs], [t.cuda() for t in tables], kc, vc, bs, sts,
+                         layer_begin=lb, layer_count=lc)
+    torch.cuda.synchronize()
+    return kc, vc, [int(s.item()) for s in sts]
+
+
+def _oracle_unpack(reqs, payloads, tables, pool, bs):
+    okc = np.full((L, pool, bs, H, d), 0xABCD, np.uint16)
+    ovc = okc.copy()
+    sts = [oracle.unpack(r["ocfg"], p, okc, ovc, t.numpy(), bs) for r, p, t in zip(reqs, payloads, tables)]
+    return okc, ovc, sts
+
+
+@pytest.mark.parametrize("lengths", [[5, 17, 300, 777, 4099], [256, 256, 512], [33] * 20])
+def test_batch_matches_oracle(lengths):
+    say(f"batch {lengths[:6]}{'...' if len(lengths) > 6 else ''} ({len(lengths)} requests)")
+    reqs = _requests(lengths)
+    pays, sts = _gpu_pack(reqs)
+    assert sts == [0] * len(reqs)
+    for r, p in zip(reqs, pays):
+        assert np.array_equal(p.cpu().numpy(), r["payload"]), r["n"]
+    bs = 16
+    pool, tables = _pool_tables(lengths, bs, seed=3)
+    kc, vc, gst = _gpu_unpack(reqs, pays, tables, pool, bs)
+    okc, ovc, ost = _oracle_unpack(reqs, [r["payload"] for r in reqs], tables, pool, bs)
+    assert gst == [0] * len(reqs) and ost == [oracle.OK] * len(reqs)
+    assert np.array_equal(u16(kc), okc) and np.array_equal(u16(vc), ovc)
+
+
+def test_layer_ranges_equal_one_call():
+    global L
+    L_saved, L = L, 4
+    try:
+        lengths = [700, 129]
+        reqs = _requests(lengths, seed0=5)
+        full, _ = _gpu_pack(reqs)
+        parts, sts = _gpu_pack(reqs, layer_ranges=[(0, 1), (1, 2), (3, 1)])
+        assert sts == [0, 0]
+        for a, b, r in zip(full, parts, reqs):
+            assert torch.equal(a, b) and np.array_equal(a.cpu().numpy(), r["payload"])
+        bs = 16
+        pool, tables = _pool_tables(lengths, bs, seed=4)
+        kc1, vc1, _ = _gpu_unpack(reqs, full, tables, pool, bs)
+        kc2, vc2, st2 = _gpu_unpack(reqs, full, tables, pool, bs, layer_ranges=[(0, 2), (2, 1), (3, 1)])
+        assert st2 == [0, 0] and torch.equal(kc1.view(torch.int16), kc2.view(torch.int16))
+        assert torch.equal(vc1.view(torch.int16), vc2.view(torch.int16))
+    finally:
+        L = L_saved
+
+
+def test_bad_payload_only_disables_its_request():
+    lengths = [300, 500, 260]
+    reqs = _requests(lengths, seed0=9)
+    pays, _ = _gpu_pack(reqs)
+    pays[1][20] ^= 1  # token count in the header of request 1
+    bs = 16
+    pool, tables = _pool_tables(lengths, bs, seed=5)
+    kc, vc, sts = _gpu_unpack(reqs, pays, tables, pool, bs)
+    assert sts == [0, skv.ERR_FORMAT, 0]
+    okc, ovc, ost = _oracle_unpack([reqs[0], reqs[2]], [reqs[0]["payload"], reqs[2]["payload"]],
+                                   [tables[0], tables[2]], pool, bs)
+    assert np.array_equal(u16(kc), okc) and np.array_equal(u16(vc), ovc)  # request 1's blocks untouched
