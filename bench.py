@@ -88,6 +88,147 @@ def cpu_baseline(w, layers: int):
                       f"pack {t1 - t0:.2f} s, unpack {t2 - t1:.2f} s, single thread"}
 
 
+def _events(count):
+    import torch
+    return [torch.cuda.Event(enable_timing=True) for _ in range(count)]
+
+
+def run_batch(args, w):
+    """Per-request pack/unpack calls vs one batched launch per stage over the
+    workload's requests (NEXT-1).  Returns a JSON-able dict."""
+    import torch
+
+    from paper_2606_08635_amd import skv, workloads
+
+    L, H, d, bs = w.layers, w.kv_heads, w.head_dim, 16
+    lens = list(w.batch_tokens)
+    base = skv.config(L, H, d, lens[0], w.budget, first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers)
+    nbs = [workloads.blocks_for(n, bs) for n in lens]
+    perm = workloads.make_block_table(sum(nbs) * bs, bs, sum(nbs), seed=0, device="cuda")
+    tables, start = [], 0
+    for nb in nbs:
+        tables.append(perm[start:start + nb].contiguous())
+        start += nb
+    kc = torch.empty(L, sum(nbs), bs, H, d, dtype=torch.float16, device="cuda")
+    vc = torch.empty_like(kc)
+    codecs, ks, vs = [], [], []
+    for r, n in enumerate(lens):
+        k, v = workloads.make_kv(L, H, n, d, seed=16 * r, outliers=w.outliers, device="cuda")
+        c = skv.Codec(skv.config(L, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay,
+                                 num_tiers=w.num_tiers))
+        c.encode(k, v)
+        codecs.append(c)
+        ks.append(k)
+        vs.append(v)
+    torch.cuda.synchronize()
+    pays = [c.payload for c in codecs]
+    tiers = [c.tier for c in codecs]
+    pst = [c.status[0:1] for c in codecs]
+    ust = [c.status[1:2] for c in codecs]
+
+    def single():
+        for c, k, v in zip(codecs, ks, vs):
+            skv.pack(c.cfg, k, v, c.tier, c.payload, c.status[0:1])
+
+    def single_unpack():
+        for c, t in zip(codecs, tables):
+            skv.unpack(c.cfg, c.payload, kc, vc, t, bs, c.status[1:2])
+
+    def batched():
+        skv.pack_batch(base, ks, vs, tiers, pays, pst)
+
+    def batched_unpack():
+        skv.unpack_batch(base, pays, lens, tables, kc, vc, bs, ust)
+
+    out = {}
+    for name, fp, fu in (("per_request", single, single_unpack), ("batched", batched, batched_unpack)):
+        for _ in range(args.warmup):
+            fp()
+            fu()
+        ev = [_events(3) for _ in range(args.steps)]
+        for e in ev:
+            e[0].record()
+            fp()
+            e[1].record()
+            fu()
+            e[2].record()
+        torch.cuda.synchronize()
+        tp = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+        tu = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+        F = sum(4 * L * H * d * n for n in lens)
+        out[name] = {"pack_ms": round(tp, 4), "unpack_ms": round(tu, 4),
+                     "fp16eq_gbps": round(F / ((tp + tu) / 1e3) / 1e9, 2),
+                     "tokens_per_s": round(sum(lens) / ((tp + tu) / 1e3), 1)}
+        if any(int(c.status[0].item()) != 0 or int(c.status[1].item()) != 0 for c in codecs):
+            raise RuntimeError("codec reported a nonzero status")
+    return {"requests": len(lens), "tokens": sum(lens), **out}
+
+
+def run_pipeline(args, w, group):
+    """Prefill->decode handoff latency of one request: pack, link and unpack in
+    sequence vs layer groups pipelined over three streams (NEXT-1)."""
+    import torch
+
+    from paper_2606_08635_amd import skv, workloads
+
+    L, H, d, n, bs = w.layers, w.kv_heads, w.head_dim, w.tokens, 16
+    cfg = skv.config(L, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers)
+    codec = skv.Codec(cfg)
+    k, v = workloads.make_kv(L, H, n, d, seed=0, outliers=w.outliers, device="cuda")
+    codec.encode(k, v)
+    nb = workloads.blocks_for(n, bs)
+    bt = workloads.make_block_table(n, bs, nb, seed=0, device="cuda")
+    kc = torch.empty(L, nb, bs, H, d, dtype=torch.float16, device="cuda")
+    vc = torch.empty_like(kc)
+    rx = torch.empty_like(codec.payload)
+    geo = codec.payload[:256].cpu().numpy().view("<u8")
+    layers_off, layer_stride = int(geo[12]), int(geo[16])
+    torch.cuda.synchronize()
+    s_pack, s_link, s_unpack = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    rst = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def sequential():
+        skv.pack(cfg, k, v, codec.tier, codec.payload, codec.status[0:1])
+        skv.link(rx, codec.payload, codec.payload_bytes)
+        skv.unpack(cfg, rx, kc, vc, bt, bs, codec.status[1:2])
+
+    def pipelined():
+        for g0 in range(0, L, group):
+            gc = min(group, L - g0)
+            with torch.cuda.stream(s_pack):
+                skv.pack_batch(cfg, [k], [v], [codec.tier], [codec.payload], [codec.status[0:1]], g0, gc)
+                e1 = torch.cuda.Event()
+                e1.record()
+            lo = 0 if g0 == 0 else layers_off + g0 * layer_stride
+            hi = layers_off + (g0 + gc) * layer_stride
+            with torch.cuda.stream(s_link):
+                s_link.wait_event(e1)
+                skv.link(rx[lo:hi], codec.payload[lo:hi], hi - lo)
+                e2 = torch.cuda.Event()
+                e2.record()
+            with torch.cuda.stream(s_unpack):
+                s_unpack.wait_event(e2)
+                skv.unpack_batch(cfg, [rx], [n], [bt], kc, vc, bs, [rst], g0, gc)
+        torch.cuda.current_stream().wait_stream(s_unpack)
+
+    out = {"group_layers": group}
+    for name, fn in (("sequential", sequential), ("pipelined", pipelined)):
+        for _ in range(args.warmup):
+            fn()
+            torch.cuda.synchronize()
+        times = []
+        for _ in range(args.steps):
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            times.append((time.perf_counter() - t0) * 1e3)
+        times.sort()
+        out[name + "_ms"] = round(times[len(times) // 2], 4)
+    if int(rst.item()) != 0 or codec.status.cpu().tolist() != [0, 0]:
+        raise RuntimeError("codec reported a nonzero status")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -99,6 +240,10 @@ def main():
     ap.add_argument("--score", choices=["kvnorm", "attn"], default="kvnorm",
                     help="importance statistic; attn uses a W-query observation window per query head")
     ap.add_argument("--obs-window", type=int, default=32)
+    ap.add_argument("--mode", choices=["step", "batch", "pipeline"], default="step",
+                    help="step: the headline codec step; batch: per-request vs batched launches over "
+                         "a multi-request workload; pipeline: layer-pipelined handoff latency")
+    ap.add_argument("--group-layers", type=int, default=4, help="layers per pipeline stage (--mode pipeline)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer with skv_link (reference for byte counters)")
     args = ap.parse_args()
@@ -122,6 +267,15 @@ def main():
         return
 
     w = workloads.WORKLOADS[args.workload]
+    if args.mode == "batch":
+        if not w.batch_tokens:
+            w = workloads.WORKLOADS["long_batch"]
+        print(json.dumps({"mode": "batch", "workload": w.name, **run_batch(args, w)}), flush=True)
+        return
+    if args.mode == "pipeline":
+        print(json.dumps({"mode": "pipeline", "workload": w.name, **run_pipeline(args, w, args.group_layers)}),
+              flush=True)
+        return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     L, H, d, n, bs = w.layers, w.kv_heads, w.head_dim, w.tokens, 16

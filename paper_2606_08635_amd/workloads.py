@@ -125,6 +125,8 @@ WORKLOADS = {
     "mistral7b_32k": Workload("mistral7b_32k", 32, 8, 128, 32768, 0.5, 3, 32),
     "long_batch": Workload("long_batch", 32, 8, 128, 32768, 0.5, 3, 32,
                            batch_tokens=(32768, 24581, 16395, 8189)),
+    # many short prompts of one model: the case batching is for
+    "short_batch": Workload("short_batch", 32, 8, 128, 2048, 0.5, 3, 32, batch_tokens=(2048,) * 64),
 }
 
 
