@@ -52,7 +52,7 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
     const int g = base + tid;
     const TierGroup gi = g < ngroups ? group_from_bytes(tier, n, g) : empty_group();
 #pragma unroll
-    for (int i = 0; i < 4; ++i) cnt[i] += gi.cnt[i];
+    for (int i = 0; i < 4; ++i) cnt[i] += gi.count(i);
     bad |= gi.bad;
     const uint32_t u = sum16(gi.units), q = sum16(gi.quant);
     if ((tid % kGroupsPerChunk) == 0 && g < ngroups) s_chunk[g / kGroupsPerChunk] = u | (q << 16);

@@ -13,11 +13,13 @@ constexpr int kGroupTokens = 16;
 constexpr int kGroupsPerChunk = kChunkTokens / kGroupTokens;  // 16
 
 struct TierGroup {
-  uint32_t units;   // sum of row widths in units of d/2 bytes
-  uint32_t quant;   // number of INT8/INT4 rows
-  uint32_t map2;    // the 16 codes, 2 bits each (token 16g+j at bits 2j..2j+1)
-  uint32_t cnt[4];  // tokens per tier
-  bool bad;         // a code outside 0..3 (byte input only)
+  uint32_t units;  // sum of row widths in units of d/2 bytes
+  uint32_t quant;  // number of INT8/INT4 rows
+  uint32_t map2;   // the 16 codes, 2 bits each (token 16g+j at bits 2j..2j+1)
+  uint32_t cnt4;   // tokens per tier, one byte per tier (at most 16 each)
+  bool bad;        // a code outside 0..3 (byte input only)
+
+  __device__ __forceinline__ uint32_t count(int tier) const { return (cnt4 >> (8 * tier)) & 0xFFu; }
 };
 
 __device__ __forceinline__ void tally(TierGroup& gi, uint32_t code, int j) {
@@ -26,15 +28,14 @@ __device__ __forceinline__ void tally(TierGroup& gi, uint32_t code, int j) {
     gi.bad = true;
     return;
   }
-  gi.cnt[code]++;
-  gi.units += tier_units(static_cast<int>(code));
-  gi.quant += tier_quant(static_cast<int>(code));
+  gi.cnt4 += 1u << (8 * code);
+  gi.units += (0x124u >> (4 * code)) & 0xFu;  // 4, 2, 1, 0 for FP16, INT8, INT4, DROP
+  gi.quant += (0x6u >> code) & 1u;            // INT8 and INT4 carry a scale
 }
 
 __device__ __forceinline__ TierGroup empty_group() {
   TierGroup gi;
-  gi.units = gi.quant = gi.map2 = 0;
-  gi.cnt[0] = gi.cnt[1] = gi.cnt[2] = gi.cnt[3] = 0;
+  gi.units = gi.quant = gi.map2 = gi.cnt4 = 0;
   gi.bad = false;
   return gi;
 }

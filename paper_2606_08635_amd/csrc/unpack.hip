@@ -69,7 +69,7 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
     const int g = base + tid;
     const TierGroup gi = g < ngroups ? group_from_map(map, n, g) : empty_group();
 #pragma unroll
-    for (int i = 0; i < 4; ++i) cnt[i] += gi.cnt[i];
+    for (int i = 0; i < 4; ++i) cnt[i] += gi.count(i);
     const uint32_t u = sum16(gi.units), q = sum16(gi.quant);
     if ((tid % kGroupsPerChunk) == 0 && g < ngroups) s_chunk[g / kGroupsPerChunk] = u | (q << 16);
   }
