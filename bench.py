@@ -229,6 +229,72 @@ def run_pipeline(args, w, group):
     return out
 
 
+def run_upgrade(args, w):
+    """Cold-tier precision upgrade (NEXT-2) after the workload's codec step:
+    an upgrade payload for a token set is packed on the prefill side and
+    applied to the decoder's cache, in both modes.  Token sets: the lowest
+    tier present (INT4 and DROP tokens; the paper's INT4 -> FP16 case) and
+    every quantized or dropped token.  Returns a JSON-able dict."""
+    import numpy as np
+    import torch
+
+    from paper_2606_08635_amd import skv, workloads
+
+    L, H, d, n, bs = w.layers, w.kv_heads, w.head_dim, w.tokens, 16
+    cfg = skv.config(L, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers)
+    codec = skv.Codec(cfg)
+    k, v = workloads.make_kv(L, H, n, d, seed=0, outliers=w.outliers, device="cuda")
+    codec.encode(k, v)
+    nb = workloads.blocks_for(n, bs)
+    bt = workloads.make_block_table(n, bs, nb, seed=0, device="cuda")
+    kc = torch.empty(L, nb, bs, H, d, dtype=torch.float16, device="cuda")
+    vc = torch.empty_like(kc)
+    codec.decode(codec.payload, kc, vc, bt, bs)
+    tier = codec.tier.cpu().numpy()
+    sets = {"int4_drop": np.flatnonzero(tier >= skv.INT4), "below_fp16": np.flatnonzero(tier != skv.FP16)}
+    st = torch.zeros(2, dtype=torch.int32, device="cuda")
+    rows_per_token = 2 * L * H
+    out = {"workload": w.name, "tokens": n}
+    for set_name, toks in sets.items():
+        m = int(toks.size)
+        if m == 0:
+            continue
+        tok = torch.from_numpy(toks.astype(np.int32)).cuda()
+        res = {"m": m}
+        for mode, mname in ((skv.UPGRADE_FP16, "fp16"), (skv.UPGRADE_RESIDUAL8, "residual8")):
+            up = torch.empty(skv.upgrade_size(cfg, m, mode), dtype=torch.uint8, device="cuda")
+            kw, vw = kc.clone(), vc.clone()  # the decoder's cache, refreshed before every apply
+            for _ in range(args.warmup):
+                skv.pack_upgrade(cfg, k, v, codec.tier, tok, mode, up, st[0:1])
+                skv.unpack_upgrade(cfg, up, m, mode, kw, vw, bt, bs, st[1:2])
+            ev = [_events(3) for _ in range(args.steps)]
+            for e in ev:
+                kw.copy_(kc)
+                vw.copy_(vc)
+                e[0].record()
+                skv.pack_upgrade(cfg, k, v, codec.tier, tok, mode, up, st[0:1])
+                e[1].record()
+                skv.unpack_upgrade(cfg, up, m, mode, kw, vw, bt, bs, st[1:2])
+                e[2].record()
+            torch.cuda.synchronize()
+            if st.cpu().tolist() != [0, 0]:
+                raise RuntimeError(f"upgrade reported status {st.cpu().tolist()}")
+            tp = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
+            ta = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
+            rows = rows_per_token * m
+            row_out = 2 * d if mode == skv.UPGRADE_FP16 else d + 4
+            pack_b = rows * (2 * d + row_out)          # read fp16 rows, write upgrade rows (+ scales)
+            apply_b = rows * (row_out + 2 * d) + (0 if mode == skv.UPGRADE_FP16 else rows * 2 * d)
+            res[mname] = {"bytes": up.numel(), "bytes_per_elem": round(up.numel() / (rows * d), 4),
+                          "pack_ms": round(tp, 4), "apply_ms": round(ta, 4),
+                          "pack_gbps": round(pack_b / (tp / 1e3) / 1e9, 1),
+                          "apply_gbps": round(apply_b / (ta / 1e3) / 1e9, 1)}
+        out[set_name] = res
+    if codec.status.cpu().tolist() != [0, 0]:
+        raise RuntimeError("codec reported a nonzero status")
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -240,9 +306,10 @@ def main():
     ap.add_argument("--score", choices=["kvnorm", "attn"], default="kvnorm",
                     help="importance statistic; attn uses a W-query observation window per query head")
     ap.add_argument("--obs-window", type=int, default=32)
-    ap.add_argument("--mode", choices=["step", "batch", "pipeline"], default="step",
+    ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade"], default="step",
                     help="step: the headline codec step; batch: per-request vs batched launches over "
-                         "a multi-request workload; pipeline: layer-pipelined handoff latency")
+                         "a multi-request workload; pipeline: layer-pipelined handoff latency; "
+                         "upgrade: cold-tier precision upgrade after the step")
     ap.add_argument("--group-layers", type=int, default=4, help="layers per pipeline stage (--mode pipeline)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer with skv_link (reference for byte counters)")
@@ -275,6 +342,9 @@ def main():
     if args.mode == "pipeline":
         print(json.dumps({"mode": "pipeline", "workload": w.name, **run_pipeline(args, w, args.group_layers)}),
               flush=True)
+        return
+    if args.mode == "upgrade":
+        print(json.dumps({"mode": "upgrade", **run_upgrade(args, w)}), flush=True)
         return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)

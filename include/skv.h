@@ -249,6 +249,60 @@ skv_status skv_unpack_batch(const skv_config* cfg, const skv_request* reqs, int3
                             void* k_cache, void* v_cache, int32_t num_blocks, int32_t block_size,
                             int32_t layer_begin, int32_t layer_count, hipStream_t stream);
 
+/* Cold-tier precision upgrade (Sec. 4.2 and its architecture figure: tokens
+ * the decoder holds at low precision are upgraded by an on-demand fetch;
+ * Sec. 8, cold-tier fetch design).  Upgrade payload, little-endian, sections
+ * 256-byte aligned with zero padding:
+ *   bytes 0..75    header: u32 magic 0x55564B53, version 1, L, H, d, n, m,
+ *                  mode; u64 tokens_off, tiers_off, scales_off, data_off,
+ *                  total; u32 status (0); the rest of the 256 bytes zero
+ *   tokens_off     int32[m] upgraded tokens, strictly ascending
+ *   tiers_off      uint8[m] tier each token was sent at
+ *   scales_off     RESIDUAL8 only: binary32[L][2][H][m] residual scales
+ *   data_off       rows [L][2 (K,V)][H][m]: FP16 mode d binary16 values
+ *                  (2d bytes); RESIDUAL8 mode d int8 codes (d bytes). */
+typedef enum skv_upgrade_mode {
+  SKV_UPGRADE_FP16 = 0,      /* send the fp16 rows: the cache becomes exact        */
+  SKV_UPGRADE_RESIDUAL8 = 1  /* send e = RN32(x - held) as INT8 (absmax, Q = 127) */
+} skv_upgrade_mode;
+
+/* Host only.  Bytes of the upgrade payload for m tokens (1 <= m <= n) in
+ * `mode`.  SKV_ERR_INVALID_ARG for a bad cfg, m or mode. */
+skv_status skv_upgrade_size(const skv_config* cfg, int32_t m, int32_t mode, uint64_t* bytes);
+
+/* Builds an upgrade payload on the prefill side, which still holds K, V
+ * ([L][H][n][d] binary16) and the tier map tier (uint8[n]) the original
+ * payload was packed with.  tokens: int32[m] device array, strictly
+ * ascending, each in [0, n).  out: capacity bytes, at least
+ * skv_upgrade_size; exactly that many bytes are written.  RESIDUAL8: for each
+ * row, held = the row unpack wrote for its tier (the quantizer of skv_pack
+ * followed by its dequantization; +0 for DROP; 0x7E00 for a NaN-scale row),
+ * e = RN32(x - held) per element; a row whose e has a non-finite element gets
+ * a NaN scale and zero codes, an all-zero e gets scale 0, otherwise
+ * a = max |e|, scale = RN32(a/127), r = RN32(127/a),
+ * code = clamp(rne(RN32(e r)), -127, 127).  If the token list is not strictly
+ * ascending and in range, or a listed tier is > 3, the header status field is
+ * set to SKV_ERR_INVALID_ARG and only the header is written.  dev_status (may
+ * be NULL) receives the same status.  Host errors: SKV_ERR_INVALID_ARG,
+ * SKV_ERR_CAPACITY. */
+skv_status skv_pack_upgrade(const skv_config* cfg, const void* k, const void* v, const uint8_t* tier,
+                            const int32_t* tokens, int32_t m, int32_t mode, void* out, uint64_t capacity,
+                            uint32_t* dev_status, hipStream_t stream);
+
+/* Applies an upgrade payload in place to the paged cache that skv_unpack
+ * filled ([L][num_blocks][block_size][H][d], same block table).  FP16 mode
+ * overwrites the listed rows; RESIDUAL8 mode sets each element to
+ * RN16(RN32(held + RN32(code * scale))) and leaves rows with a NaN scale as
+ * they are.  m and mode are the values the payload was built with.
+ * dev_status (required) is set to 0, or to SKV_ERR_FORMAT when the header,
+ * token list, tiers or a block-table entry disagree with cfg, m and mode; in
+ * that case nothing is written.  Returns SKV_ERR_FORMAT (host-side) when
+ * bytes is below skv_upgrade_size. */
+skv_status skv_unpack_upgrade(const skv_config* cfg, const void* upgrade, uint64_t bytes, int32_t m,
+                              int32_t mode, void* k_cache, void* v_cache, const int32_t* block_table,
+                              int32_t num_blocks, int32_t block_size, uint32_t* dev_status,
+                              hipStream_t stream);
+
 /* Link emulation for a one-GPU setup (Sec. 4.2: the payload crosses the
  * network between prefill and decode).  Copies `bytes` from src to dst on
  * stream: device to device when host_staging is NULL, otherwise device to

@@ -68,6 +68,9 @@ def _load():
         "ora_geometry": (ctypes.c_int, [cfgp, vp]),
         "ora_pack_meta": (ctypes.c_int, [cfgp, vp, vp, ctypes.c_uint64]),
         "ora_unpack": (ctypes.c_int, [cfgp, vp, ctypes.c_uint64, vp, vp, vp, ctypes.c_int32, ctypes.c_int32]),
+        "ora_upgrade_size": (ctypes.c_int, [cfgp, ctypes.c_int32, ctypes.c_int32, P(ctypes.c_uint64)]),
+        "ora_pack_upgrade": (ctypes.c_int, [cfgp, vp, vp, vp, vp, ctypes.c_int32, ctypes.c_int32, vp, ctypes.c_uint64]),
+        "ora_unpack_upgrade": (ctypes.c_int, [cfgp, vp, ctypes.c_uint64, vp, vp, vp, ctypes.c_int32, ctypes.c_int32]),
         "ora_half_to_double": (ctypes.c_double, [ctypes.c_uint16]),
         "ora_float_to_half": (ctypes.c_uint16, [ctypes.c_float]),
     }
@@ -248,6 +251,39 @@ def unpack(cfg, payload, k_cache, v_cache, block_table, block_size=16):
     st = _lib.ora_unpack(ctypes.byref(cfg), _ptr(payload), payload.size, _ptr(k_cache),
                          _ptr(v_cache), _ptr(block_table), num_blocks, block_size)
     return st
+
+
+UPGRADE_FP16, UPGRADE_RESIDUAL8 = 0, 1
+
+
+def upgrade_size(cfg, m, mode):
+    out = ctypes.c_uint64()
+    st = _lib.ora_upgrade_size(ctypes.byref(cfg), m, mode, ctypes.byref(out))
+    if st:
+        raise OracleError(st, "upgrade_size")
+    return out.value
+
+
+def pack_upgrade(cfg, k, v, tier, tokens, mode):
+    """Upgrade payload for the listed tokens (ascending int32 indices)."""
+    k, v = _u16(k), _u16(v)
+    tier = np.ascontiguousarray(tier, np.uint8)
+    tokens = np.ascontiguousarray(tokens, np.int32)
+    size = upgrade_size(cfg, tokens.size, mode)
+    out = np.empty(size, np.uint8)
+    st = _lib.ora_pack_upgrade(ctypes.byref(cfg), _ptr(k), _ptr(v), _ptr(tier), _ptr(tokens), tokens.size, mode,
+                               _ptr(out), size)
+    if st:
+        raise OracleError(st, "pack_upgrade")
+    return out
+
+
+def unpack_upgrade(cfg, upgrade, k_cache, v_cache, block_table, block_size=16):
+    """Applies an upgrade payload to the caches in place; returns the status."""
+    upgrade = np.ascontiguousarray(upgrade, np.uint8)
+    block_table = np.ascontiguousarray(block_table, np.int32)
+    return _lib.ora_unpack_upgrade(ctypes.byref(cfg), _ptr(upgrade), upgrade.size, _ptr(k_cache), _ptr(v_cache),
+                                   _ptr(block_table), k_cache.shape[1], block_size)
 
 
 def half_to_double(h):

@@ -666,3 +666,193 @@ int ora_unpack(const ora_config* c, const uint8_t* payload, uint64_t bytes, uint
   free(tier); free(units); free(qrank);
   return ORA_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Cold-tier precision upgrade (Sec. 4.2, Fig. "sysarch": on-demand fetch that */
+/* upgrades tokens already present at low precision; Sec. 8 "cold-tier fetch */
+/* design").  The prefill side, which still holds the fp16 K/V and the tier   */
+/* map, sends for a listed set of tokens either the fp16 rows themselves       */
+/* (mode 0, exact) or the INT8-quantized residual between the fp16 row and    */
+/* the row the decoder reconstructed (mode 1); the decoder applies it in      */
+/* place in its paged cache.                                                   */
+/*                                                                             */
+/* Upgrade payload (version 1, little-endian, sections 256-byte aligned):     */
+/*   [header 256 B: u32 magic 0x55564B53 ("SKVU"), u32 version, i32 L, H, d,   */
+/*    n, m (listed tokens), mode; u64 offsets of tokens, tiers, scales, data;  */
+/*    u64 total; u32 status]                                                   */
+/*   [tokens: i32[m], ascending] [tiers: u8[m], each token's tier in the       */
+/*   original payload] [scales: fp32 [L][2][H][m], mode 1 only]                */
+/*   [data: [L][2][H][m] rows, 2d bytes (mode 0) or d bytes (mode 1)]          */
+/* ------------------------------------------------------------------------ */
+
+#define ORA_UPG_MAGIC 0x55564B53u /* bytes 'S','K','V','U' */
+
+typedef struct {
+  uint64_t tokens_off, tiers_off, scales_off, data_off, total, row_bytes;
+} ora_upg_geom;
+
+static int upg_geometry(const ora_config* c, int32_t m, int32_t mode, ora_upg_geom* g) {
+  int st = ora_validate(c);
+  if (st) return st;
+  if (m < 1 || m > c->num_tokens || (mode != 0 && mode != 1)) return ORA_ERR_INVALID_ARG;
+  uint64_t L = (uint64_t)c->num_layers, H = (uint64_t)c->num_kv_heads, d = (uint64_t)c->head_dim;
+  g->tokens_off = 256;
+  g->tiers_off = g->tokens_off + up256(4 * (uint64_t)m);
+  g->scales_off = g->tiers_off + up256((uint64_t)m);
+  g->data_off = g->scales_off + (mode == 1 ? up256(L * 2 * H * (uint64_t)m * 4) : 0);
+  g->row_bytes = mode == 0 ? 2 * d : d;
+  g->total = g->data_off + L * 2 * H * (uint64_t)m * g->row_bytes;
+  return ORA_OK;
+}
+
+int ora_upgrade_size(const ora_config* c, int32_t m, int32_t mode, uint64_t* bytes) {
+  ora_upg_geom g;
+  int st = upg_geometry(c, m, mode, &g);
+  if (st == ORA_OK) *bytes = g.total;
+  return st;
+}
+
+/* Reconstruction the decoder holds for one row after the original transfer. */
+static void held_row(int tr, int32_t d, const uint16_t* x, uint16_t* out) {
+  uint8_t enc[512];
+  float scale = 0.0f;
+  ora_encode_row(tr, d, x, enc, &scale);
+  ora_decode_row(tr, d, enc, scale, out);
+}
+
+static int upg_tokens_ok(int32_t n, const int32_t* tokens, int32_t m) {
+  for (int32_t i = 0; i < m; ++i) {
+    if (tokens[i] < 0 || tokens[i] >= n) return 0;
+    if (i > 0 && tokens[i] <= tokens[i - 1]) return 0;
+  }
+  return 1;
+}
+
+int ora_pack_upgrade(const ora_config* c, const uint16_t* k, const uint16_t* v, const uint8_t* tier,
+                     const int32_t* tokens, int32_t m, int32_t mode, uint8_t* out, uint64_t capacity) {
+  ora_upg_geom g;
+  int st = upg_geometry(c, m, mode, &g);
+  if (st) return st;
+  if (capacity < g.total) return ORA_ERR_CAPACITY;
+  if (!upg_tokens_ok(c->num_tokens, tokens, m)) return ORA_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < m; ++i)
+    if (tier[tokens[i]] > 3) return ORA_ERR_INVALID_ARG;
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens, d = c->head_dim;
+  memset(out, 0, g.total);
+  put32(out + 0, ORA_UPG_MAGIC);
+  put32(out + 4, 1);
+  put32(out + 8, (uint32_t)L);
+  put32(out + 12, (uint32_t)H);
+  put32(out + 16, (uint32_t)d);
+  put32(out + 20, (uint32_t)n);
+  put32(out + 24, (uint32_t)m);
+  put32(out + 28, (uint32_t)mode);
+  memcpy(out + 32, &g.tokens_off, 8);
+  memcpy(out + 40, &g.tiers_off, 8);
+  memcpy(out + 48, &g.scales_off, 8);
+  memcpy(out + 56, &g.data_off, 8);
+  memcpy(out + 64, &g.total, 8);
+  for (int32_t i = 0; i < m; ++i) {
+    put32(out + g.tokens_off + 4 * (uint64_t)i, (uint32_t)tokens[i]);
+    out[g.tiers_off + (uint64_t)i] = tier[tokens[i]];
+  }
+  uint16_t held[256];
+  for (int64_t l = 0; l < L; ++l)
+    for (int kv = 0; kv < 2; ++kv)
+      for (int64_t h = 0; h < H; ++h) {
+        const uint16_t* src = (kv == 0 ? k : v) + ((l * H + h) * n) * d;
+        uint64_t seg = (uint64_t)((l * 2 + kv) * H + h);
+        for (int32_t i = 0; i < m; ++i) {
+          const uint16_t* x = src + (int64_t)tokens[i] * d;
+          uint8_t* row = out + g.data_off + (seg * (uint64_t)m + (uint64_t)i) * g.row_bytes;
+          if (mode == 0) {
+            for (int64_t e = 0; e < d; ++e) { row[2 * e] = (uint8_t)x[e]; row[2 * e + 1] = (uint8_t)(x[e] >> 8); }
+            continue;
+          }
+          /* residual e = RN32(x - held) of every element, INT8 absmax quantized */
+          held_row(tier[tokens[i]], (int32_t)d, x, held);
+          float res[256];
+          int finite = 1;
+          float amax = 0.0f;
+          for (int64_t e = 0; e < d; ++e) {
+            float xf = half_to_float(x[e]), hf = half_to_float(held[e]);
+            res[e] = xf - hf;
+            if (!isfinite(res[e])) finite = 0;
+            else if (fabsf(res[e]) > amax) amax = fabsf(res[e]);
+          }
+          float scale;
+          uint8_t* sc = out + g.scales_off + (seg * (uint64_t)m + (uint64_t)i) * 4;
+          if (!finite) {
+            uint32_t nanbits = 0x7FC00000u;
+            memcpy(&scale, &nanbits, 4);
+            for (int64_t e = 0; e < d; ++e) row[e] = 0;
+          } else if (amax == 0.0f) {
+            scale = 0.0f;
+            for (int64_t e = 0; e < d; ++e) row[e] = 0;
+          } else {
+            scale = amax / 127.0f;
+            float r = 127.0f / amax;
+            for (int64_t e = 0; e < d; ++e) {
+              float q = nearbyintf(res[e] * r);
+              if (q > 127.0f) q = 127.0f;
+              if (q < -127.0f) q = -127.0f;
+              row[e] = (uint8_t)((int32_t)q & 0xFF);
+            }
+          }
+          put32(sc, fbits(scale));
+        }
+      }
+  return ORA_OK;
+}
+
+int ora_unpack_upgrade(const ora_config* c, const uint8_t* up, uint64_t bytes, uint16_t* kc, uint16_t* vc,
+                       const int32_t* block_table, int32_t num_blocks, int32_t block_size) {
+  int st = ora_validate(c);
+  if (st) return st;
+  if (bytes < 256 || get32(up) != ORA_UPG_MAGIC || get32(up + 4) != 1) return ORA_ERR_FORMAT;
+  int32_t m = (int32_t)get32(up + 24), mode = (int32_t)get32(up + 28);
+  ora_upg_geom g;
+  if (upg_geometry(c, m, mode, &g)) return ORA_ERR_FORMAT;
+  if (get32(up + 8) != (uint32_t)c->num_layers || get32(up + 12) != (uint32_t)c->num_kv_heads ||
+      get32(up + 16) != (uint32_t)c->head_dim || get32(up + 20) != (uint32_t)c->num_tokens)
+    return ORA_ERR_FORMAT;
+  uint64_t f[5];
+  memcpy(f, up + 32, 40);
+  if (f[0] != g.tokens_off || f[1] != g.tiers_off || f[2] != g.scales_off || f[3] != g.data_off || f[4] != g.total ||
+      bytes < g.total || get32(up + 72) != 0)
+    return ORA_ERR_FORMAT;
+  int32_t* tokens = (int32_t*)malloc((size_t)m * 4);
+  for (int32_t i = 0; i < m; ++i) tokens[i] = (int32_t)get32(up + g.tokens_off + 4 * (uint64_t)i);
+  int ok = upg_tokens_ok(c->num_tokens, tokens, m);
+  for (int32_t i = 0; i < m && ok; ++i) ok = up[g.tiers_off + (uint64_t)i] <= 3;
+  if (ok && (block_size < 1 || num_blocks < 1)) ok = 0;
+  for (int64_t b = 0; ok && b < ((int64_t)c->num_tokens + block_size - 1) / block_size; ++b)
+    ok = block_table[b] >= 0 && block_table[b] < num_blocks;
+  if (!ok) { free(tokens); return ORA_ERR_FORMAT; }
+  int64_t L = c->num_layers, H = c->num_kv_heads, d = c->head_dim;
+  for (int64_t l = 0; l < L; ++l)
+    for (int kv = 0; kv < 2; ++kv)
+      for (int64_t h = 0; h < H; ++h) {
+        uint64_t seg = (uint64_t)((l * 2 + kv) * H + h);
+        uint16_t* cache = kv == 0 ? kc : vc;
+        for (int32_t i = 0; i < m; ++i) {
+          int64_t t = tokens[i], blk = block_table[t / block_size], slot = t % block_size;
+          uint16_t* dst = cache + (((l * num_blocks + blk) * block_size + slot) * H + h) * d;
+          const uint8_t* row = up + g.data_off + (seg * (uint64_t)m + (uint64_t)i) * g.row_bytes;
+          if (mode == 0) {
+            for (int64_t e = 0; e < d; ++e) dst[e] = (uint16_t)(row[2 * e] | (row[2 * e + 1] << 8));
+            continue;
+          }
+          float scale;
+          uint32_t sb = get32(up + g.scales_off + (seg * (uint64_t)m + (uint64_t)i) * 4);
+          memcpy(&scale, &sb, 4);
+          if (isnan(scale)) continue; /* no usable residual: keep the held row */
+          for (int64_t e = 0; e < d; ++e) {
+            float corr = (float)(int32_t)(int8_t)row[e] * scale;
+            dst[e] = ora_float_to_half(half_to_float(dst[e]) + corr);
+          }
+        }
+      }
+  free(tokens);
+  return ORA_OK;
+}

@@ -10,6 +10,7 @@
 // A launch may cover a range of layers: the payload is layer-major, so the
 // layers of a request can be packed (and sent) in pieces.
 #include "device_util.h"
+#include "row_codec.h"
 #include "skv_internal.h"
 #include "tier_groups.h"
 
@@ -164,52 +165,12 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
       if (tr == kFP16) {
         store16<SKV_PACK_NT_STORE>(dst + s_off[row] + lane * 16, x[u]);
       } else if (tr == kINT8 || tr == kINT4) {
-        const int Q = tr == kINT8 ? 127 : 7;
-        const float Qf = static_cast<float>(Q);
-        float scale;
-        int32_t lo = 0x4B400000, hi = 0x4B400000;  // clamp window around 1.5 * 2^23
-        uint32_t codes[8];
-        if (amax >= 0x7C00u) {  // an infinity or NaN in the row
-          scale = __builtin_bit_cast(float, 0x7FC00000u);
-#pragma unroll
-          for (int i = 0; i < 8; ++i) codes[i] = 0;
-          if (lane == 0) atomicAdd(nonfinite, 1u);
-        } else if (amax == 0u) {
-          scale = 0.0f;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) codes[i] = 0;
-        } else {
-          const float amag = half_lo(amax);
-          scale = amag / Qf;  // correctly rounded binary32 division
-          const float rcp = Qf / amag;
-          lo -= Q;
-          hi += Q;
-          const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            // RN32(x * r), then round to an integer (nearest-even) by adding
-            // 1.5 * 2^23: the low mantissa bits of the sum are the code
-            const float y0 = half_lo(w[i]) * rcp;
-            const float y1 = half_hi(w[i]) * rcp;
-            const int32_t b0 = __builtin_bit_cast(int32_t, y0 + 12582912.0f);
-            const int32_t b1 = __builtin_bit_cast(int32_t, y1 + 12582912.0f);
-            codes[2 * i] = static_cast<uint32_t>(min(max(b0, lo), hi));
-            codes[2 * i + 1] = static_cast<uint32_t>(min(max(b1, lo), hi));
-          }
-        }
+        const LaneCodes q = quantize_lane(x[u], amax, tr == kINT8 ? 127 : 7);
+        if (q.nonfinite && lane == 0) atomicAdd(nonfinite, 1u);
         uint8_t* out_row = dst + s_off[row];
-        if (tr == kINT8) {
-          u32x2 out;
-          out.x = (codes[0] & 0xFFu) | ((codes[1] & 0xFFu) << 8) | ((codes[2] & 0xFFu) << 16) | (codes[3] << 24);
-          out.y = (codes[4] & 0xFFu) | ((codes[5] & 0xFFu) << 8) | ((codes[6] & 0xFFu) << 16) | (codes[7] << 24);
-          store8<SKV_PACK_NT_STORE>(out_row + lane * 8, out);
-        } else {
-          uint32_t out = 0;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) out |= (codes[i] & 0xFu) << (4 * i);
-          store4<SKV_PACK_NT_STORE>(out_row + lane * 4, out);
-        }
-        if (lane == 0) scales[s_q[row]] = scale;
+        if (tr == kINT8) store8<SKV_PACK_NT_STORE>(out_row + lane * 8, pack_int8(q));
+        else store4<SKV_PACK_NT_STORE>(out_row + lane * 4, pack_int4(q));
+        if (lane == 0) scales[s_q[row]] = q.scale;
       }
     }
   }

@@ -397,6 +397,59 @@ skv_status skv_unpack(const skv_config* cfg, const void* payload, uint64_t paylo
   return skv_unpack_batch(cfg, &q, 1, k_cache, v_cache, num_blocks, block_size, 0, cfg->num_layers, stream);
 }
 
+skv_status skv_upgrade_size(const skv_config* cfg, int32_t m, int32_t mode, uint64_t* bytes) {
+  if (bytes == nullptr) return SKV_ERR_INVALID_ARG;
+  const skv_status st = check_config(cfg);
+  if (st != SKV_OK) return st;
+  if (m < 1 || m > cfg->num_tokens || (mode != SKV_UPGRADE_FP16 && mode != SKV_UPGRADE_RESIDUAL8))
+    return SKV_ERR_INVALID_ARG;
+  *bytes = upgrade_bytes(cfg->num_layers, cfg->num_kv_heads, cfg->head_dim, m, mode, nullptr);
+  return SKV_OK;
+}
+
+skv_status skv_pack_upgrade(const skv_config* cfg, const void* k, const void* v, const uint8_t* tier,
+                            const int32_t* tokens, int32_t m, int32_t mode, void* out, uint64_t capacity,
+                            uint32_t* dev_status, hipStream_t stream) {
+  uint64_t need = 0;
+  const skv_status st = skv_upgrade_size(cfg, m, mode, &need);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(k) || !dev_ptr_ok(v) || !dev_ptr_ok(tier) || !dev_ptr_ok(out)) return SKV_ERR_INVALID_ARG;
+  if (tokens == nullptr || !aligned(tokens, 4)) return SKV_ERR_INVALID_ARG;
+  if (dev_status != nullptr && !aligned(dev_status, 4)) return SKV_ERR_INVALID_ARG;
+  if (capacity < need) return SKV_ERR_CAPACITY;
+  Geometry g{};
+  g.L = cfg->num_layers;
+  g.H = cfg->num_kv_heads;
+  g.d = cfg->head_dim;
+  g.n = cfg->num_tokens;
+  return launched(launch_pack_upgrade(g, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), tier,
+                                      tokens, m, mode, static_cast<uint8_t*>(out), dev_status, stream));
+}
+
+skv_status skv_unpack_upgrade(const skv_config* cfg, const void* upgrade, uint64_t bytes, int32_t m,
+                              int32_t mode, void* k_cache, void* v_cache, const int32_t* block_table,
+                              int32_t num_blocks, int32_t block_size, uint32_t* dev_status,
+                              hipStream_t stream) {
+  uint64_t need = 0;
+  const skv_status st = skv_upgrade_size(cfg, m, mode, &need);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(upgrade) || !dev_ptr_ok(k_cache) || !dev_ptr_ok(v_cache)) return SKV_ERR_INVALID_ARG;
+  if (block_table == nullptr || !aligned(block_table, 4)) return SKV_ERR_INVALID_ARG;
+  if (dev_status == nullptr || !aligned(dev_status, 4)) return SKV_ERR_INVALID_ARG;
+  if (num_blocks < 1 || block_size < 1) return SKV_ERR_INVALID_ARG;
+  if (static_cast<uint64_t>(num_blocks) * static_cast<uint64_t>(block_size) > 0xFFFFFFFFull)
+    return SKV_ERR_INVALID_ARG;
+  if (bytes < need) return SKV_ERR_FORMAT;
+  Geometry g{};
+  g.L = cfg->num_layers;
+  g.H = cfg->num_kv_heads;
+  g.d = cfg->head_dim;
+  g.n = cfg->num_tokens;
+  return launched(launch_unpack_upgrade(g, static_cast<const uint8_t*>(upgrade), m, mode,
+                                        static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache),
+                                        block_table, num_blocks, block_size, dev_status, stream));
+}
+
 skv_status skv_link(void* dst, const void* src, uint64_t bytes, void* host_staging,
                     hipStream_t stream) {
   if (bytes == 0) return SKV_OK;

@@ -73,6 +73,15 @@ hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier,
 // nchunks * 2 * H * layer_count).  Pack writes the metadata when layer_begin
 // is 0; unpack checks the payloads when layer_begin is 0.
 hipError_t launch_pack(const BatchArgs& a, uint64_t rows, hipStream_t stream);
+// Upgrade payload size; offsets (optional) receives tokens, tiers, scales and
+// data offsets, the total and the row bytes.
+uint64_t upgrade_bytes(int32_t L, int32_t H, int32_t d, int32_t m, int32_t mode, uint64_t* offsets);
+hipError_t launch_pack_upgrade(const Geometry& g, const uint16_t* k, const uint16_t* v, const uint8_t* tier,
+                               const int32_t* tokens, int32_t m, int32_t mode, uint8_t* out, uint32_t* status,
+                               hipStream_t stream);
+hipError_t launch_unpack_upgrade(const Geometry& g, const uint8_t* up, int32_t m, int32_t mode, uint16_t* k_cache,
+                                 uint16_t* v_cache, const int32_t* block_table, int32_t num_blocks,
+                                 int32_t block_size, uint32_t* status, hipStream_t stream);
 hipError_t launch_unpack(const BatchArgs& a, uint64_t rows, uint16_t* k_cache, uint16_t* v_cache,
                          int32_t num_blocks, int32_t block_size, hipStream_t stream);
 

@@ -12,6 +12,7 @@
 // paged slot.  Requests of a launch share the paged cache (each has its own
 // block table); a launch may cover a range of layers.
 #include "device_util.h"
+#include "row_codec.h"
 #include "skv_internal.h"
 #include "tier_groups.h"
 
@@ -97,35 +98,6 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
   if (tid == 0) *r.status = s_bad ? static_cast<uint32_t>(SKV_ERR_FORMAT) : 0u;
 }
 
-// 8 signed codes (INT8: one per byte; INT4: one per nibble, element 2i low)
-// times the row scale, rounded to binary32 and then to binary16.
-__device__ __forceinline__ u32x4 dequant_int8(u32x2 c, float s) {
-  const uint32_t w[2] = {c.x, c.y};
-  uint32_t o[4];
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const float f0 = static_cast<float>(static_cast<int32_t>(w[i] << 24) >> 24) * s;
-    const float f1 = static_cast<float>(static_cast<int32_t>(w[i] << 16) >> 24) * s;
-    const float f2 = static_cast<float>(static_cast<int32_t>(w[i] << 8) >> 24) * s;
-    const float f3 = static_cast<float>(static_cast<int32_t>(w[i]) >> 24) * s;
-    o[2 * i] = pack_half2(f0, f1);
-    o[2 * i + 1] = pack_half2(f2, f3);
-  }
-  return u32x4{o[0], o[1], o[2], o[3]};
-}
-
-__device__ __forceinline__ u32x4 dequant_int4(uint32_t w, float s) {
-  uint32_t o[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float f0 = static_cast<float>(static_cast<int32_t>(w << (28 - 8 * i)) >> 28) * s;
-    const float f1 = static_cast<float>(static_cast<int32_t>(w << (24 - 8 * i)) >> 28) * s;
-    o[i] = pack_half2(f0, f1);
-  }
-  return u32x4{o[0], o[1], o[2], o[3]};
-}
-
-
 // Loads one row slice of a lane (16 B of FP16, 8 B of INT8 codes or 4 B of
 // INT4 codes) and its scale.
 __device__ __forceinline__ void load_row(int tr, const uint8_t* row, const float* scale_ptr, int lane,
@@ -149,7 +121,7 @@ __device__ __forceinline__ void load_row(int tr, const uint8_t* row, const float
 // dequantized, a NaN scale giving 0x7E00.
 __device__ __forceinline__ u32x4 decode_row(int tr, u32x4 raw, float sc) {
   if (tr == kINT8 || tr == kINT4) {
-    if (__builtin_isnan(sc)) return u32x4{0x7E007E00u, 0x7E007E00u, 0x7E007E00u, 0x7E007E00u};
+    if (__builtin_isnan(sc)) return u32x4{kNaNHalf2, kNaNHalf2, kNaNHalf2, kNaNHalf2};
     return tr == kINT8 ? dequant_int8(u32x2{raw.x, raw.y}, sc) : dequant_int4(raw.x, sc);
   }
   return raw;

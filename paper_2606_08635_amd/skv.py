@@ -18,10 +18,12 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libskv.so")
 OK, ERR_INVALID_ARG, ERR_BUDGET, ERR_CAPACITY, ERR_FORMAT, ERR_DEVICE = range(6)
 FP16, INT8, INT4, DROP = 0, 1, 2, 3
 KVNORM, ATTN, RECENCY = 0, 1, 2
+UPGRADE_FP16, UPGRADE_RESIDUAL8 = 0, 1
 
 EXPORTED = ("skv_abi_version", "skv_status_string", "skv_plan_tiers", "skv_payload_size",
             "skv_workspace_size", "skv_prepare", "skv_score", "skv_assign_tiers", "skv_pack",
-            "skv_unpack", "skv_pack_batch", "skv_unpack_batch", "skv_link")
+            "skv_unpack", "skv_pack_batch", "skv_unpack_batch", "skv_link", "skv_upgrade_size",
+            "skv_pack_upgrade", "skv_unpack_upgrade")
 
 
 class SkvError(RuntimeError):
@@ -80,6 +82,9 @@ def lib():
             "skv_link": (ctypes.c_int, [vp, vp, u64, vp, vp]),
             "skv_pack_batch": (ctypes.c_int, [cfgp, P(Request), i32, i32, i32, vp]),
             "skv_unpack_batch": (ctypes.c_int, [cfgp, P(Request), i32, vp, vp, i32, i32, i32, i32, vp]),
+            "skv_upgrade_size": (ctypes.c_int, [cfgp, i32, i32, P(u64)]),
+            "skv_pack_upgrade": (ctypes.c_int, [cfgp, vp, vp, vp, vp, i32, i32, vp, u64, vp, vp]),
+            "skv_unpack_upgrade": (ctypes.c_int, [cfgp, vp, u64, i32, i32, vp, vp, vp, i32, i32, vp, vp]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -194,6 +199,43 @@ def unpack(cfg: Config, payload: torch.Tensor, k_cache: torch.Tensor, v_cache: t
                             _dev(v_cache, torch.float16, v_cache.numel(), "v_cache"),
                             _dev(block_table, torch.int32, nbt, "block_table"), nb, block_size,
                             _dev(dev_status, torch.int32, 1, "dev_status"), _stream(stream)), "skv_unpack")
+
+
+def upgrade_size(cfg: Config, m: int, mode: int) -> int:
+    out = ctypes.c_uint64()
+    _check(lib().skv_upgrade_size(ctypes.byref(cfg), m, mode, ctypes.byref(out)), "skv_upgrade_size")
+    return out.value
+
+
+def pack_upgrade(cfg: Config, k: torch.Tensor, v: torch.Tensor, tier: torch.Tensor, tokens: torch.Tensor,
+                 mode: int, out: torch.Tensor, dev_status: Optional[torch.Tensor] = None, stream=None):
+    """Upgrade payload for the listed tokens (int32, strictly ascending)."""
+    n = _kv_numel(cfg)
+    m = tokens.numel()
+    st = ctypes.c_void_p(None) if dev_status is None else _dev(dev_status, torch.int32, 1, "dev_status")
+    _check(lib().skv_pack_upgrade(ctypes.byref(cfg), _dev(k, torch.float16, n, "k"), _dev(v, torch.float16, n, "v"),
+                                  _dev(tier, torch.uint8, cfg.num_tokens, "tier"),
+                                  _dev(tokens, torch.int32, m, "tokens"), m, mode,
+                                  _dev(out, torch.uint8, 0, "out"), out.numel(), st, _stream(stream)),
+           "skv_pack_upgrade")
+
+
+def unpack_upgrade(cfg: Config, upgrade: torch.Tensor, m: int, mode: int, k_cache: torch.Tensor,
+                   v_cache: torch.Tensor, block_table: torch.Tensor, block_size: int, dev_status: torch.Tensor,
+                   stream=None):
+    """Applies an upgrade payload in place to caches filled by unpack."""
+    if k_cache.dim() != 5 or k_cache.shape[2] != block_size or tuple(k_cache.shape) != tuple(v_cache.shape):
+        raise ValueError("caches must be [L][num_blocks][block_size][H][d] and alike")
+    L, nb, _, H, d = k_cache.shape
+    if (L, H, d) != (cfg.num_layers, cfg.num_kv_heads, cfg.head_dim):
+        raise ValueError("cache shape does not match the configuration")
+    nbt = -(-cfg.num_tokens // block_size)
+    _check(lib().skv_unpack_upgrade(ctypes.byref(cfg), _dev(upgrade, torch.uint8, 0, "upgrade"), upgrade.numel(),
+                                    m, mode, _dev(k_cache, torch.float16, k_cache.numel(), "k_cache"),
+                                    _dev(v_cache, torch.float16, v_cache.numel(), "v_cache"),
+                                    _dev(block_table, torch.int32, nbt, "block_table"), nb, block_size,
+                                    _dev(dev_status, torch.int32, 1, "dev_status"), _stream(stream)),
+           "skv_unpack_upgrade")
 
 
 def _with_tokens(cfg: Config, n: int) -> Config:

@@ -146,3 +146,39 @@ def test_batch_argument_errors(lib):
     reqs[1].num_tokens = 77
     reqs[1].dev_status = None
     assert L.skv_unpack_batch(by, reqs, 2, fake, fake, 100, 16, 0, 2, None) == skv.ERR_INVALID_ARG
+
+
+def test_upgrade_size_and_argument_errors(lib):
+    rng = np.random.default_rng(7)
+    for _ in range(200):
+        L, H = int(rng.integers(1, 5)), int(rng.integers(1, 9))
+        d = int(rng.choice([32, 64, 128, 256]))
+        n = int(rng.integers(1, 40000))
+        m = int(rng.integers(0, n + 2))
+        mode = int(rng.integers(0, 3))
+        c, o = _pair(L, H, d, n, 0.5, decay=0.0)
+        try:
+            want = oracle.upgrade_size(o, m, mode)
+        except oracle.OracleError as e:
+            with pytest.raises(skv.SkvError) as got:
+                skv.upgrade_size(c, m, mode)
+            assert got.value.status == e.status == skv.ERR_INVALID_ARG
+            continue
+        assert skv.upgrade_size(c, m, mode) == want
+    cfg = skv.config(2, 2, 64, 300, 0.5)
+    by = ctypes.byref(cfg)
+    P = ctypes.c_void_p
+    fake, odd = P(1 << 20), P((1 << 20) + 8)
+    size = skv.upgrade_size(cfg, 10, skv.UPGRADE_RESIDUAL8)
+    L = lib
+    assert L.skv_pack_upgrade(by, fake, fake, fake, fake, 10, 1, fake, size - 1, None, None) == skv.ERR_CAPACITY
+    assert L.skv_pack_upgrade(by, fake, fake, fake, None, 10, 1, fake, size, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_pack_upgrade(by, fake, fake, fake, fake, 0, 1, fake, size, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_pack_upgrade(by, fake, fake, fake, fake, 301, 1, fake, size, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_pack_upgrade(by, fake, odd, fake, fake, 10, 1, fake, size, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_pack_upgrade(by, fake, fake, fake, fake, 10, 2, fake, size, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_unpack_upgrade(by, fake, size - 1, 10, 1, fake, fake, fake, 20, 16, fake, None) == skv.ERR_FORMAT
+    assert L.skv_unpack_upgrade(by, fake, size, 10, 1, fake, fake, fake, 20, 16, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_unpack_upgrade(by, fake, size, 10, 1, fake, fake, None, 20, 16, fake, None) == skv.ERR_INVALID_ARG
+    assert L.skv_unpack_upgrade(by, fake, size, 10, 1, fake, fake, fake, 0, 16, fake, None) == skv.ERR_INVALID_ARG
+    assert L.skv_unpack_upgrade(by, odd, size, 10, 1, fake, fake, fake, 20, 16, fake, None) == skv.ERR_INVALID_ARG
