@@ -14,46 +14,61 @@ struct LaneCodes {
   bool nonfinite;
 };
 
+// RN32(a / Q) and RN32(Q / a) for a positive finite binary16 magnitude a
+// (held in binary32) and Q in {7, 127}, without a full division: the quotient
+// from the constant RN32(1/Q), respectively the hardware reciprocal of a, plus
+// one Newton-Raphson correction (Markstein's scheme: residual by a fused
+// multiply-add, then a fused correction).  Checked exhaustively in exact
+// arithmetic to give the correctly rounded quotient for every such a and for
+// any reciprocal within 2 ulp of 1/a.
+__device__ __forceinline__ float scale_of(float a, float Qf, float inv_q) {
+  const float s0 = a * inv_q;
+  const float e = __builtin_fmaf(-s0, Qf, a);
+  return __builtin_fmaf(e, inv_q, s0);
+}
+__device__ __forceinline__ float recip_scale_of(float a, float Qf) {
+  const float r0 = __builtin_amdgcn_rcpf(a);
+  const float q0 = Qf * r0;
+  const float e = __builtin_fmaf(-q0, a, Qf);
+  return __builtin_fmaf(e, r0, q0);
+}
+
 // amax: the row's largest magnitude pattern (bits & 0x7FFF, reduced over the
-// row's lanes).  code = clamp(rne(RN32(x * RN32(Q / a))), -Q, Q).
+// row's lanes).  code = clamp(rne(RN32(x * RN32(Q / a))), -Q, Q); for a finite
+// row |RN32(x r)| < Q + 1/2 (checked exhaustively over a), so the clamp never
+// binds and is not executed.  Rounding to an integer adds 1.5 * 2^23: the low
+// mantissa bits of the sum hold the code in two's complement.
 __device__ __forceinline__ LaneCodes quantize_lane(u32x4 x, uint32_t amax, int Q) {
   LaneCodes out;
   out.nonfinite = amax >= 0x7C00u;
-  int32_t lo = 0x4B400000, hi = 0x4B400000;  // clamp window around 1.5 * 2^23
-  if (out.nonfinite) {
-    out.scale = __builtin_bit_cast(float, 0x7FC00000u);
-  } else if (amax == 0u) {
-    out.scale = 0.0f;
-  } else {
-    const float Qf = static_cast<float>(Q);
-    const float a = half_lo(amax);
-    out.scale = a / Qf;  // correctly rounded binary32 division
-    const float rcp = Qf / a;
-    lo -= Q;
-    hi += Q;
-    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  if (out.nonfinite || amax == 0u) {
+    out.scale = out.nonfinite ? __builtin_bit_cast(float, 0x7FC00000u) : 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      // RN32(x * r), then rounding to an integer (nearest-even) by adding
-      // 1.5 * 2^23: the low mantissa bits of the sum are the code
-      const float y0 = half_lo(w[i]) * rcp;
-      const float y1 = half_hi(w[i]) * rcp;
-      out.c[2 * i] = static_cast<uint32_t>(min(max(__builtin_bit_cast(int32_t, y0 + 12582912.0f), lo), hi));
-      out.c[2 * i + 1] = static_cast<uint32_t>(min(max(__builtin_bit_cast(int32_t, y1 + 12582912.0f), lo), hi));
-    }
+    for (int i = 0; i < 8; ++i) out.c[i] = 0x4B400000u;  // code 0
     return out;
   }
+  const float Qf = static_cast<float>(Q);
+  const float inv_q = Q == 127 ? 1.0f / 127.0f : 1.0f / 7.0f;  // RN32(1/Q), folded at compile time
+  const float a = half_lo(amax);
+  out.scale = scale_of(a, Qf, inv_q);
+  const float rcp = recip_scale_of(a, Qf);
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-  for (int i = 0; i < 8; ++i) out.c[i] = static_cast<uint32_t>(lo);  // code 0
+  for (int i = 0; i < 4; ++i) {
+    out.c[2 * i] = __builtin_bit_cast(uint32_t, half_lo(w[i]) * rcp + 12582912.0f);
+    out.c[2 * i + 1] = __builtin_bit_cast(uint32_t, half_hi(w[i]) * rcp + 12582912.0f);
+  }
   return out;
 }
 
-// 8 INT8 codes as 8 bytes, element order.
+// 8 INT8 codes as 8 bytes, element order (byte 0 of each code word).
 __device__ __forceinline__ u32x2 pack_int8(const LaneCodes& q) {
-  u32x2 out;
-  out.x = (q.c[0] & 0xFFu) | ((q.c[1] & 0xFFu) << 8) | ((q.c[2] & 0xFFu) << 16) | (q.c[3] << 24);
-  out.y = (q.c[4] & 0xFFu) | ((q.c[5] & 0xFFu) << 8) | ((q.c[6] & 0xFFu) << 16) | (q.c[7] << 24);
-  return out;
+  // perm selector 0x0c0c0400: bytes [lo.b0, hi.b0, 0, 0]; 0x05040100 joins two halves
+  const uint32_t p01 = __builtin_amdgcn_perm(q.c[1], q.c[0], 0x0c0c0400u);
+  const uint32_t p23 = __builtin_amdgcn_perm(q.c[3], q.c[2], 0x0c0c0400u);
+  const uint32_t p45 = __builtin_amdgcn_perm(q.c[5], q.c[4], 0x0c0c0400u);
+  const uint32_t p67 = __builtin_amdgcn_perm(q.c[7], q.c[6], 0x0c0c0400u);
+  return u32x2{__builtin_amdgcn_perm(p23, p01, 0x05040100u), __builtin_amdgcn_perm(p67, p45, 0x05040100u)};
 }
 
 // 8 INT4 codes as 4 bytes: element 2i in the low nibble of byte i.

@@ -70,28 +70,70 @@ __device__ __forceinline__ uint32_t upg_header_word(const UpgArgs& a, int i) {
   }
 }
 
+// The token list check shared by upg_prep and upg_check: every token in
+// [0, n), strictly ascending, and (tier != null) its tier at most 3.  Loads are
+// issued kListBatch at a time so the single workgroup keeps many in flight.
+constexpr int kListBatch = 8;
+
+__device__ __forceinline__ bool token_list_bad(const int32_t* tok, int m, int n, const uint8_t* tier_of_token,
+                                               const uint8_t* tier_of_entry) {
+  bool bad = false;
+  for (int base = threadIdx.x; base < m; base += kListBatch * kUpgCheckThreads) {
+    int t[kListBatch], prev[kListBatch];
+#pragma unroll
+    for (int u = 0; u < kListBatch; ++u) {
+      const int i = base + u * kUpgCheckThreads;
+      t[u] = i < m ? tok[i] : 0;
+      prev[u] = (i > 0 && i < m) ? tok[i - 1] : -1;
+    }
+    uint32_t tr[kListBatch];
+#pragma unroll
+    for (int u = 0; u < kListBatch; ++u) {
+      const int i = base + u * kUpgCheckThreads;
+      const bool in = t[u] >= 0 && t[u] < n;
+      bad |= !in || prev[u] >= t[u];
+      tr[u] = 0;
+      if (i < m && tier_of_token != nullptr && in) tr[u] = tier_of_token[t[u]];
+      if (i < m && tier_of_entry != nullptr) tr[u] = tier_of_entry[i];
+    }
+#pragma unroll
+    for (int u = 0; u < kListBatch; ++u) bad |= tr[u] > 3u;
+  }
+  return bad;
+}
+
 __global__ __launch_bounds__(kUpgCheckThreads) void upg_prep(const UpgArgs a) {
   __shared__ uint32_t s_bad;
   const int tid = threadIdx.x;
   if (tid == 0) s_bad = 0;
   __syncthreads();
-  bool bad = false;
-  for (int i = tid; i < a.m; i += kUpgCheckThreads) {
-    const int t = a.tokens[i];
-    bad |= t < 0 || t >= a.n || (i > 0 && a.tokens[i - 1] >= t);
-    if (t >= 0 && t < a.n) bad |= a.tier[t] > 3;
-  }
-  if (bad) atomicOr(&s_bad, 1u);
+  if (token_list_bad(a.tokens, a.m, a.n, a.tier, nullptr)) atomicOr(&s_bad, 1u);
   __syncthreads();
   const uint32_t status = s_bad ? static_cast<uint32_t>(SKV_ERR_INVALID_ARG) : 0u;
   uint8_t* up = a.up;
   if (tid < 64) reinterpret_cast<uint32_t*>(up)[tid] = tid == kUpgHdrStatus ? status : upg_header_word(a, tid);
   if (tid == 0 && a.status) *a.status = status;
   if (status) return;  // block-uniform
-  for (int i = tid; i < a.m; i += kUpgCheckThreads) {
-    const int t = a.tokens[i];
-    reinterpret_cast<int32_t*>(up + a.tokens_off)[i] = t;
-    up[a.tiers_off + i] = a.tier[t];
+  int32_t* out_tok = reinterpret_cast<int32_t*>(up + a.tokens_off);
+  uint8_t* out_tier = up + a.tiers_off;
+  for (int base = tid; base < a.m; base += kListBatch * kUpgCheckThreads) {
+    int t[kListBatch];
+#pragma unroll
+    for (int u = 0; u < kListBatch; ++u) {
+      const int i = base + u * kUpgCheckThreads;
+      t[u] = i < a.m ? a.tokens[i] : 0;
+    }
+    uint8_t tr[kListBatch];
+#pragma unroll
+    for (int u = 0; u < kListBatch; ++u) tr[u] = a.tier[t[u]];  // t in range: checked above
+#pragma unroll
+    for (int u = 0; u < kListBatch; ++u) {
+      const int i = base + u * kUpgCheckThreads;
+      if (i < a.m) {
+        out_tok[i] = t[u];
+        out_tier[i] = tr[u];
+      }
+    }
   }
   for (uint64_t b = a.tokens_off + 4ull * a.m + tid; b < a.tiers_off; b += kUpgCheckThreads) up[b] = 0;
   for (uint64_t b = a.tiers_off + static_cast<uint64_t>(a.m) + tid; b < a.scales_off; b += kUpgCheckThreads) up[b] = 0;
@@ -122,12 +164,34 @@ __device__ __forceinline__ u32x2 quantize_residual(const float (&e)[8], uint32_t
   return u32x2{0u, 0u};
 }
 
+// The upgrade row of one lane: mode 0 the fp16 values themselves; mode 1 the
+// INT8 residual codes against the held row (all lanes of a row take part in
+// the two row reductions).
+template <int LPR>
+__device__ __forceinline__ u32x2 residual_lane(int tr, u32x4 x, float* scale) {
+  const uint32_t amax = group_max<LPR>(absmax_bits8(x));
+  const u32x4 held = held_lane(tr, x, amax);
+  const uint32_t xs[4] = {x.x, x.y, x.z, x.w}, hs[4] = {held.x, held.y, held.z, held.w};
+  float e[8];
+  uint32_t emax = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    e[2 * j] = half_lo(xs[j]) - half_lo(hs[j]);
+    e[2 * j + 1] = half_hi(xs[j]) - half_hi(hs[j]);
+    emax = max(emax, __builtin_bit_cast(uint32_t, e[2 * j]) & 0x7FFFFFFFu);
+    emax = max(emax, __builtin_bit_cast(uint32_t, e[2 * j + 1]) & 0x7FFFFFFFu);
+  }
+  emax = group_max<LPR>(emax);
+  return quantize_residual(e, emax, scale);
+}
+
 // grid: ceil(m / 256) * 2 * L * H workgroups, chunk fastest
 template <int D, int MODE>
 __global__ __launch_bounds__(kUpgThreads) void upg_rows(const UpgArgs a) {
-  constexpr int LPR = D / 8;
-  constexpr int RPI = kUpgThreads / LPR;
+  constexpr int LPR = D / 8;                 // lanes per row, 16 bytes each
+  constexpr int RPI = kUpgThreads / LPR;     // rows per block-wide iteration
   constexpr int ITERS = kUpgThreads / RPI;
+  constexpr int U = ITERS < 4 ? ITERS : 4;   // rows in flight per thread
   __shared__ int32_t s_tok[kUpgThreads];
   __shared__ uint8_t s_tier[kUpgThreads];
   uint8_t* up = a.up;
@@ -146,33 +210,27 @@ __global__ __launch_bounds__(kUpgThreads) void upg_rows(const UpgArgs a) {
   const uint16_t* src = (kv ? a.v : a.k) + (static_cast<size_t>(l) * a.H + h) * static_cast<size_t>(a.n) * D;
   const uint64_t seg_rows = static_cast<uint64_t>(seg) * a.m;
   const int lane = threadIdx.x % LPR, rsub = threadIdx.x / LPR;
-#pragma unroll 4
-  for (int it = 0; it < ITERS; ++it) {
-    const int r = it * RPI + rsub;
-    const int i = i0 + r;
-    const bool live = i < a.m;
-    const u32x4 x = live ? ld_nt16(src + static_cast<size_t>(s_tok[r]) * D + lane * 8) : u32x4{0u, 0u, 0u, 0u};
-    if constexpr (MODE == 0) {
-      if (live) st_nt16(up + a.data_off + (seg_rows + i) * (2 * D) + lane * 16, x);
-    } else {
-      const uint32_t amax = group_max<LPR>(absmax_bits8(x));
-      const u32x4 held = held_lane(s_tier[r], x, amax);
-      const uint32_t xs[4] = {x.x, x.y, x.z, x.w}, hs[4] = {held.x, held.y, held.z, held.w};
-      float e[8];
-      uint32_t emax = 0;
+#pragma unroll 1
+  for (int it = 0; it < ITERS; it += U) {
+    u32x4 x[U];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        e[2 * j] = half_lo(xs[j]) - half_lo(hs[j]);
-        e[2 * j + 1] = half_hi(xs[j]) - half_hi(hs[j]);
-        emax = max(emax, __builtin_bit_cast(uint32_t, e[2 * j]) & 0x7FFFFFFFu);
-        emax = max(emax, __builtin_bit_cast(uint32_t, e[2 * j + 1]) & 0x7FFFFFFFu);
-      }
-      emax = group_max<LPR>(emax);
-      float scale;
-      const u32x2 codes = quantize_residual(e, emax, &scale);
-      if (live) {
-        st_nt8(up + a.data_off + (seg_rows + i) * D + lane * 8, codes);
-        if (lane == 0) reinterpret_cast<float*>(up + a.scales_off)[seg_rows + i] = scale;
+    for (int u = 0; u < U; ++u) {
+      const int r = (it + u) * RPI + rsub;
+      x[u] = i0 + r < a.m ? ld_nt16(src + static_cast<size_t>(s_tok[r]) * D + lane * 8) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int r = (it + u) * RPI + rsub;
+      const int i = i0 + r;
+      if constexpr (MODE == 0) {
+        if (i < a.m) st_nt16(up + a.data_off + (seg_rows + i) * (2 * D) + lane * 16, x[u]);
+      } else {
+        float scale;
+        const u32x2 codes = residual_lane<LPR>(s_tier[r], x[u], &scale);
+        if (i < a.m) {
+          st_nt8(up + a.data_off + (seg_rows + i) * D + lane * 8, codes);
+          if (lane == 0) reinterpret_cast<float*>(up + a.scales_off)[seg_rows + i] = scale;
+        }
       }
     }
   }
@@ -184,27 +242,45 @@ __global__ __launch_bounds__(kUpgCheckThreads) void upg_check(const UpgArgs a) {
   if (tid == 0) s_bad = 0;
   __syncthreads();
   const uint8_t* up = a.up;
-  bool bad = false;
-  if (tid <= kUpgHdrStatus) bad |= reinterpret_cast<const uint32_t*>(up)[tid] != upg_header_word(a, tid);
-  if (bad) atomicOr(&s_bad, 1u);
+  if (tid <= kUpgHdrStatus && reinterpret_cast<const uint32_t*>(up)[tid] != upg_header_word(a, tid))
+    atomicOr(&s_bad, 1u);
   __syncthreads();
   if (s_bad) {
     if (tid == 0) *a.status = static_cast<uint32_t>(SKV_ERR_FORMAT);
     return;
   }
-  const int32_t* tok = reinterpret_cast<const int32_t*>(up + a.tokens_off);
-  for (int i = tid; i < a.m; i += kUpgCheckThreads) {
-    const int t = tok[i];
-    bad |= t < 0 || t >= a.n || (i > 0 && tok[i - 1] >= t) || up[a.tiers_off + i] > 3;
-  }
+  bool bad = token_list_bad(reinterpret_cast<const int32_t*>(up + a.tokens_off), a.m, a.n, nullptr,
+                            up + a.tiers_off);
   const int nbt = (a.n + a.block_size - 1) / a.block_size;
-  for (int i = tid; i < nbt; i += kUpgCheckThreads) {
-    const int b = a.block_table[i];
-    bad |= b < 0 || b >= a.num_blocks;
+  for (int base = tid; base < nbt; base += kListBatch * kUpgCheckThreads) {
+    int b[kListBatch];
+#pragma unroll
+    for (int u = 0; u < kListBatch; ++u) {
+      const int i = base + u * kUpgCheckThreads;
+      b[u] = i < nbt ? a.block_table[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kListBatch; ++u) bad |= b[u] < 0 || b[u] >= a.num_blocks;
   }
   if (bad) atomicOr(&s_bad, 1u);
   __syncthreads();
   if (tid == 0) *a.status = s_bad ? static_cast<uint32_t>(SKV_ERR_FORMAT) : 0u;
+}
+
+// out = RN16(RN32(held + RN32(code * scale))) for the lane's 8 elements.
+__device__ __forceinline__ u32x4 add_residual(u32x4 held, u32x2 c, float scale) {
+  const uint32_t hs[4] = {held.x, held.y, held.z, held.w};
+  const uint32_t cw[2] = {c.x, c.y};
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t w = cw[j >> 1];
+    const int sh = 16 * (j & 1);
+    const float c0 = static_cast<float>(static_cast<int32_t>(w << (24 - sh)) >> 24) * scale;
+    const float c1 = static_cast<float>(static_cast<int32_t>(w << (16 - sh)) >> 24) * scale;
+    o[j] = pack_half2(half_lo(hs[j]) + c0, half_hi(hs[j]) + c1);
+  }
+  return u32x4{o[0], o[1], o[2], o[3]};
 }
 
 template <int D, int MODE>
@@ -212,6 +288,7 @@ __global__ __launch_bounds__(kUpgThreads) void upg_apply(const UpgArgs a) {
   constexpr int LPR = D / 8;
   constexpr int RPI = kUpgThreads / LPR;
   constexpr int ITERS = kUpgThreads / RPI;
+  constexpr int U = ITERS < 4 ? ITERS : 4;
   __shared__ uint32_t s_pos[kUpgThreads];
   if (*a.status != 0u) return;
   const uint8_t* up = a.up;
@@ -234,31 +311,43 @@ __global__ __launch_bounds__(kUpgThreads) void upg_apply(const UpgArgs a) {
                     static_cast<size_t>(h) * D;
   const uint64_t seg_rows = static_cast<uint64_t>(seg) * a.m;
   const int lane = threadIdx.x % LPR, rsub = threadIdx.x / LPR;
-#pragma unroll 4
-  for (int it = 0; it < ITERS; ++it) {
-    const int r = it * RPI + rsub;
-    const int i = i0 + r;
-    if (i >= a.m) continue;
-    uint16_t* dst = cache + static_cast<size_t>(s_pos[r]) * a.H * D + lane * 8;
+#pragma unroll 1
+  for (int it = 0; it < ITERS; it += U) {
     if constexpr (MODE == 0) {
-      st_nt16(dst, ld_nt16(up + a.data_off + (seg_rows + i) * (2 * D) + lane * 16));
-    } else {
-      const float scale = reinterpret_cast<const float*>(up + a.scales_off)[seg_rows + i];
-      if (__builtin_isnan(scale)) continue;  // no usable residual: keep the held row
-      const u32x2 c = ld_nt8(up + a.data_off + (seg_rows + i) * D + lane * 8);
-      const u32x4 held = *reinterpret_cast<const u32x4*>(dst);
-      const uint32_t hs[4] = {held.x, held.y, held.z, held.w};
-      const uint32_t cw[2] = {c.x, c.y};
-      uint32_t o[4];
+      u32x4 x[U];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t w = cw[j >> 1];
-        const int sh = 16 * (j & 1);
-        const float c0 = static_cast<float>(static_cast<int32_t>(w << (24 - sh)) >> 24) * scale;
-        const float c1 = static_cast<float>(static_cast<int32_t>(w << (16 - sh)) >> 24) * scale;
-        o[j] = pack_half2(half_lo(hs[j]) + c0, half_hi(hs[j]) + c1);
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + (it + u) * RPI + rsub;
+        if (i < a.m) x[u] = ld_nt16(up + a.data_off + (seg_rows + i) * (2 * D) + lane * 16);
       }
-      *reinterpret_cast<u32x4*>(dst) = u32x4{o[0], o[1], o[2], o[3]};
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = (it + u) * RPI + rsub;
+        if (i0 + r < a.m) st_nt16(cache + static_cast<size_t>(s_pos[r]) * a.H * D + lane * 8, x[u]);
+      }
+    } else {
+      u32x2 c[U];
+      u32x4 held[U];
+      float scale[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = (it + u) * RPI + rsub;
+        const int i = i0 + r;
+        scale[u] = __builtin_bit_cast(float, 0x7FC00000u);
+        if (i < a.m) {
+          scale[u] = reinterpret_cast<const float*>(up + a.scales_off)[seg_rows + i];
+          c[u] = ld_nt8(up + a.data_off + (seg_rows + i) * D + lane * 8);
+          held[u] = *reinterpret_cast<const u32x4*>(cache + static_cast<size_t>(s_pos[r]) * a.H * D + lane * 8);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int r = (it + u) * RPI + rsub;
+        // a NaN scale (also set for rows past m) keeps the held row
+        if (!__builtin_isnan(scale[u]))
+          *reinterpret_cast<u32x4*>(cache + static_cast<size_t>(s_pos[r]) * a.H * D + lane * 8) =
+              add_residual(held[u], c[u], scale[u]);
+      }
     }
   }
 }

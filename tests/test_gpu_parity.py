@@ -196,3 +196,47 @@ def test_link_emulation_round_trip():
     skv.link(z, x, x.numel(), host_staging=host)
     torch.cuda.synchronize()
     assert torch.equal(x, y) and torch.equal(x, z)
+
+
+@pytest.mark.parametrize("d", [32, 128])
+def test_every_binary16_row_maximum(d):
+    """Rows whose absmax runs over every positive finite binary16 value, once
+    as an INT8 and once as an INT4 row (the quantizer's quotients and code
+    range for all row maxima), with every other element a random pattern of
+    magnitude at most the row's maximum; payload and cache vs the oracle."""
+    L, H, n = 1, 1, 65536
+    cfg, ocfg = configs(L, H, d, n, 0.375, 3, num_sink=0)
+    plan = skv.plan_tiers(cfg)
+    assert (plan["n_int8"], plan["n_int4"]) == (32768, 32768)
+    rng = np.random.default_rng(d)
+    maxima = np.arange(1, 0x7C00, dtype=np.int64)
+    tier = np.full(n, oracle.INT4, np.uint8)
+    tier[rng.permutation(n)[:32768]] = oracle.INT8
+    planes = []
+    for plane in range(2):
+        amax = np.empty(n, np.int64)
+        for tr in (oracle.INT8, oracle.INT4):
+            rows = np.flatnonzero(tier == tr)
+            amax[rows] = np.resize(rng.permutation(maxima), rows.size)
+        mag = (rng.random((n, d)) * (amax[:, None] + 1)).astype(np.int64)
+        mag[np.arange(n), rng.integers(0, d, n)] = amax
+        sign = rng.integers(0, 2, (n, d)) << 15
+        planes.append(torch.from_numpy((mag | sign).astype(np.uint16).view(np.int16)).view(torch.float16)
+                      .reshape(L, H, n, d))
+    k, v = planes
+    say(f"every-maximum rows d={d}")
+    want = oracle.pack(ocfg, u16(k), u16(v), tier)
+    pay = torch.empty(want.size, dtype=torch.uint8, device="cuda")
+    st = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    skv.pack(cfg, k.cuda(), v.cuda(), torch.from_numpy(tier).cuda(), pay, st)
+    torch.cuda.synchronize()
+    assert int(st.item()) == 0
+    got = pay.cpu().numpy()
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} payload bytes differ, first at {bad[:8]}"
+    bs, nb = 16, n // 16
+    bt = workloads.make_block_table(n, bs, nb, seed=d)
+    okc, ovc, ost = oracle_decode(ocfg, want, L, H, d, bs, nb, bt.numpy())
+    kc, vc, gst = gpu_decode(cfg, pay, L, H, d, n, bs, nb, bt.cuda())
+    assert ost == 0 and gst == 0
+    assert np.array_equal(u16(kc), okc) and np.array_equal(u16(vc), ovc)
