@@ -27,10 +27,12 @@ CSRC = os.path.join(ROOT, "paper_2606_08635_amd", "csrc")
 # a plain-copy calibration; see profiles/traffic_*.md), valid only for the
 # kernel sources they were taken on (first 16 hex digits of SHA-256 of each file).
 MEASURED_TRAFFIC = {
-    ("mistral7b_32k", "pack"): (6.5086e9, {"pack.hip": "8658e854947fb809", "device_util.h": "187abc123a53519a",
-                                           "tier_groups.h": "f3e053754552f3f6", "skv_internal.h": "54ca5d3291e32470"}),
-    ("mistral7b_32k", "unpack"): (6.5126e9, {"unpack.hip": "a638da0b6197a8a5", "device_util.h": "187abc123a53519a",
-                                             "tier_groups.h": "f3e053754552f3f6", "skv_internal.h": "54ca5d3291e32470"}),
+    ("mistral7b_32k", "pack"): (6.5086e9, {"pack.hip": "a159b0197da6e8b0", "row_codec.h": "77df103bddc04308",
+                                           "device_util.h": "187abc123a53519a", "tier_groups.h": "f3e053754552f3f6",
+                                           "skv_internal.h": "a722bd6f24154b62"}),
+    ("mistral7b_32k", "unpack"): (6.5126e9, {"unpack.hip": "02842c07f7ff1b6a", "row_codec.h": "77df103bddc04308",
+                                             "device_util.h": "187abc123a53519a", "tier_groups.h": "f3e053754552f3f6",
+                                             "skv_internal.h": "a722bd6f24154b62"}),
 }
 
 
