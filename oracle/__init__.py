@@ -19,6 +19,7 @@ from . import build as _build
 OK, ERR_INVALID_ARG, ERR_BUDGET, ERR_CAPACITY, ERR_FORMAT = 0, 1, 2, 3, 4
 FP16, INT8, INT4, DROP = 0, 1, 2, 3
 KVNORM, ATTN, RECENCY = 0, 1, 2
+GRAN_TOKEN, GRAN_LAYER, GRAN_HEAD = 0, 1, 2
 CHUNK_TOKENS = 256
 
 
@@ -71,6 +72,16 @@ def _load():
         "ora_upgrade_size": (ctypes.c_int, [cfgp, ctypes.c_int32, ctypes.c_int32, P(ctypes.c_uint64)]),
         "ora_pack_upgrade": (ctypes.c_int, [cfgp, vp, vp, vp, vp, ctypes.c_int32, ctypes.c_int32, vp, ctypes.c_uint64]),
         "ora_unpack_upgrade": (ctypes.c_int, [cfgp, vp, ctypes.c_uint64, vp, vp, vp, ctypes.c_int32, ctypes.c_int32]),
+        "ora_group_count": (ctypes.c_int32, [cfgp, ctypes.c_int32]),
+        "ora_plan_group": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, ctypes.c_int32, P(Plan)]),
+        "ora_grouped_size": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, P(ctypes.c_uint64)]),
+        "ora_sumsq_group": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, vp, ctypes.c_int32, ctypes.c_int32,
+                                           P(ctypes.c_uint64), P(ctypes.c_uint64)]),
+        "ora_score_groups": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, vp, vp, vp]),
+        "ora_assign_groups": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, vp, vp]),
+        "ora_pack_groups": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, vp, vp, vp, vp, ctypes.c_uint64]),
+        "ora_unpack_groups": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, vp, ctypes.c_uint64, vp, vp, vp,
+                                             ctypes.c_int32, ctypes.c_int32]),
         "ora_half_to_double": (ctypes.c_double, [ctypes.c_uint16]),
         "ora_float_to_half": (ctypes.c_uint16, [ctypes.c_float]),
     }
@@ -284,6 +295,85 @@ def unpack_upgrade(cfg, upgrade, k_cache, v_cache, block_table, block_size=16):
     block_table = np.ascontiguousarray(block_table, np.int32)
     return _lib.ora_unpack_upgrade(ctypes.byref(cfg), _ptr(upgrade), upgrade.size, _ptr(k_cache), _ptr(v_cache),
                                    _ptr(block_table), k_cache.shape[1], block_size)
+
+
+def group_count(cfg, gran):
+    return _lib.ora_group_count(ctypes.byref(cfg), gran)
+
+
+def _budgets(budgets):
+    return None if budgets is None else np.ascontiguousarray(budgets, np.float32)
+
+
+def plan_group(cfg, gran, budgets, g):
+    p = Plan()
+    b = _budgets(budgets)
+    st = _lib.ora_plan_group(ctypes.byref(cfg), gran, _ptr(b), g, ctypes.byref(p))
+    if st:
+        raise OracleError(st, "plan_group")
+    return {f: getattr(p, f) for f, _ in Plan._fields_}
+
+
+def grouped_size(cfg, gran, budgets=None):
+    out = ctypes.c_uint64()
+    b = _budgets(budgets)
+    st = _lib.ora_grouped_size(ctypes.byref(cfg), gran, _ptr(b), ctypes.byref(out))
+    if st:
+        raise OracleError(st, "grouped_size")
+    return out.value
+
+
+def sumsq_group(cfg, gran, k, v, g, t):
+    """Exact sum of squares of token t over group g, in units of 2^-48 (int)."""
+    k, v = _u16(k), _u16(v)
+    hi, lo = ctypes.c_uint64(), ctypes.c_uint64()
+    _lib.ora_sumsq_group(ctypes.byref(cfg), gran, _ptr(k), _ptr(v), g, t, ctypes.byref(hi), ctypes.byref(lo))
+    return (hi.value << 64) | lo.value
+
+
+def score_groups(cfg, gran, k, v=None, q=None):
+    """float64 [G][n]: every group's score of every token."""
+    k = _u16(k)
+    v = None if v is None else _u16(v)
+    q = None if q is None else _u16(q)
+    G = group_count(cfg, gran)
+    out = np.empty((G, cfg.num_tokens), np.float64)
+    st = _lib.ora_score_groups(ctypes.byref(cfg), gran, _ptr(k), _ptr(v), _ptr(q), _ptr(out))
+    if st:
+        raise OracleError(st, "score_groups")
+    return out
+
+
+def assign_groups(cfg, gran, key, budgets=None):
+    """uint8 [G][n] tier maps."""
+    key = np.ascontiguousarray(key, np.float64)
+    b = _budgets(budgets)
+    tier = np.empty(key.shape, np.uint8)
+    st = _lib.ora_assign_groups(ctypes.byref(cfg), gran, _ptr(b), _ptr(key), _ptr(tier))
+    if st:
+        raise OracleError(st, "assign_groups")
+    return tier
+
+
+def pack_groups(cfg, gran, k, v, tier, budgets=None):
+    k, v = _u16(k), _u16(v)
+    tier = np.ascontiguousarray(tier, np.uint8)
+    b = _budgets(budgets)
+    size = grouped_size(cfg, gran, b)
+    out = np.empty(size, np.uint8)
+    st = _lib.ora_pack_groups(ctypes.byref(cfg), gran, _ptr(b), _ptr(k), _ptr(v), _ptr(tier), _ptr(out), size)
+    if st:
+        raise OracleError(st, "pack_groups")
+    return out
+
+
+def unpack_groups(cfg, gran, payload, k_cache, v_cache, block_table, block_size=16, budgets=None):
+    """Decodes a grouped payload into the caches in place; returns the status."""
+    payload = np.ascontiguousarray(payload, np.uint8)
+    block_table = np.ascontiguousarray(block_table, np.int32)
+    b = _budgets(budgets)
+    return _lib.ora_unpack_groups(ctypes.byref(cfg), gran, _ptr(b), _ptr(payload), payload.size, _ptr(k_cache),
+                                  _ptr(v_cache), _ptr(block_table), k_cache.shape[1], block_size)
 
 
 def half_to_double(h):

@@ -856,3 +856,442 @@ int ora_unpack_upgrade(const ora_config* c, const uint8_t* up, uint64_t bytes, u
   free(tokens);
   return ORA_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Per-layer and per-head tier maps.  The paper keeps one tier per token for  */
+/* every layer and head and names finer maps as the next step: a per-layer    */
+/* budget allocation favouring layers whose errors propagate furthest         */
+/* (Sec. 2.6, Sec. 6.10) and per-head or per-layer importance scores          */
+/* (Sec. 7.5, Sec. 9 (iii)).  Here the (layer, head) pairs are partitioned    */
+/* into groups -- one group (granularity 0, the paper's map), one per layer   */
+/* (1) or one per (layer, head) (2) -- and every group gets its own score,    */
+/* its own budget b_g, its own plan (the Sec. 4.4 mapping with sinks pinned,  */
+/* as above) and its own tier map; K and V of a pair share their group's map. */
+/*                                                                             */
+/* Grouped payload (version 1, little-endian, sections 256-byte aligned,      */
+/* zero padding):                                                              */
+/*   header 256 B: u32 words 0 magic 0x47564B53 ("SKVG"), 1 version, 2-5 L, H, */
+/*     d, n, 6 granularity, 7 G, 8 num_tiers, 9 score_mode, 10-12 bits of b,   */
+/*     rho, lambda, 13 num_sink (as configured), 14 chunk tokens (256),        */
+/*     15 zero; u64 at words 16, 18, ..., 30: group table, tier maps, tier-map */
+/*     stride, chunk indexes, chunk-index stride, segment table, layers,       */
+/*     total; u32 word 32 non-finite quantized rows, 33 status                 */
+/*   group table: G x 32 B, u32 [sinks, fp16, int8, int4, drop, bits of b_g,   */
+/*     quantized rows nq_g, zero]                                              */
+/*   G tier maps (2 bits per token, token t at bits 2(t%4) of byte t/4), each  */
+/*     padded to the tier-map stride                                           */
+/*   G chunk indexes (u32 row-width units and u32 quantized rows before every  */
+/*     256th token), each padded to the chunk-index stride                     */
+/*   segment table: for (layer, K/V, head) in that order, u64 offsets of the   */
+/*     segment's scales and of its rows                                        */
+/*   layers: [fp32 scales of the 2H segments, nq_g each, back to back, padded] */
+/*     [the 2H segments, rows in token order at their group's tier widths,     */
+/*     each padded to 256 B]                                                   */
+/* ------------------------------------------------------------------------ */
+
+#define ORA_GRP_MAGIC 0x47564B53u /* bytes 'S','K','V','G' */
+enum { GRAN_TOKEN = 0, GRAN_LAYER = 1, GRAN_HEAD = 2 };
+
+int32_t ora_group_count(const ora_config* c, int32_t gran) {
+  if (gran == GRAN_TOKEN) return 1;
+  if (gran == GRAN_LAYER) return c->num_layers;
+  if (gran == GRAN_HEAD) return c->num_layers * c->num_kv_heads;
+  return -1;
+}
+
+static int64_t group_of(const ora_config* c, int32_t gran, int64_t l, int64_t h) {
+  return gran == GRAN_TOKEN ? 0 : gran == GRAN_LAYER ? l : l * c->num_kv_heads + h;
+}
+
+/* Validates cfg, the granularity and every group budget, then plans every
+ * group (plans: G entries). */
+static int plan_groups(const ora_config* c, int32_t gran, const float* budgets, ora_plan_t* plans) {
+  int st = ora_validate(c);
+  if (st) return st;
+  int32_t G = ora_group_count(c, gran);
+  if (G < 1) return ORA_ERR_INVALID_ARG;
+  for (int32_t g = 0; g < G; ++g) {
+    ora_config cg = *c;
+    if (budgets) cg.budget = budgets[g];
+    st = ora_plan(&cg, plans ? &plans[g] : NULL);
+    if (st) return st;
+  }
+  return ORA_OK;
+}
+
+int ora_plan_group(const ora_config* c, int32_t gran, const float* budgets, int32_t g, ora_plan_t* p) {
+  int32_t G = ora_group_count(c, gran);
+  if (G < 1 || g < 0 || g >= G) return ORA_ERR_INVALID_ARG;
+  ora_plan_t* all = (ora_plan_t*)malloc((size_t)G * sizeof(ora_plan_t));
+  int st = plan_groups(c, gran, budgets, all);
+  if (!st) *p = all[g];
+  free(all);
+  return st;
+}
+
+typedef struct {
+  int32_t G;
+  int64_t nchunks;
+  uint64_t group_off, tiermaps_off, tiermap_stride, chunkidx_off, chunkidx_stride, segtab_off,
+      layers_off, total;
+} ora_ggeom;
+
+static uint64_t group_seg_bytes(const ora_plan_t* p, uint64_t d) {
+  return (uint64_t)(p->n_sink + p->n_fp16) * 2 * d + (uint64_t)p->n_int8 * d + (uint64_t)p->n_int4 * (d / 2);
+}
+
+/* Section offsets; segtab (optional, 2LH pairs of u64) receives every
+ * segment's scale and row offsets. */
+static void grouped_layout(const ora_config* c, int32_t gran, const ora_plan_t* plans, ora_ggeom* g,
+                           uint64_t* segtab) {
+  uint64_t L = (uint64_t)c->num_layers, H = (uint64_t)c->num_kv_heads, d = (uint64_t)c->head_dim;
+  uint64_t n = (uint64_t)c->num_tokens;
+  g->G = ora_group_count(c, gran);
+  g->nchunks = (int64_t)((n + ORA_CHUNK - 1) / ORA_CHUNK);
+  g->group_off = 256;
+  g->tiermaps_off = g->group_off + up256(32 * (uint64_t)g->G);
+  g->tiermap_stride = up256((n + 3) / 4);
+  g->chunkidx_off = g->tiermaps_off + (uint64_t)g->G * g->tiermap_stride;
+  g->chunkidx_stride = up256(8 * (uint64_t)g->nchunks);
+  g->segtab_off = g->chunkidx_off + (uint64_t)g->G * g->chunkidx_stride;
+  g->layers_off = g->segtab_off + up256(2 * L * H * 16);
+  uint64_t off = g->layers_off;
+  for (uint64_t l = 0; l < L; ++l) {
+    uint64_t nscales = 0;
+    for (int kv = 0; kv < 2; ++kv)
+      for (uint64_t h = 0; h < H; ++h) {
+        const ora_plan_t* p = &plans[group_of(c, gran, (int64_t)l, (int64_t)h)];
+        if (segtab) segtab[2 * ((l * 2 + (uint64_t)kv) * H + h)] = off + 4 * nscales;
+        nscales += (uint64_t)(p->n_int8 + p->n_int4);
+      }
+    uint64_t data = off + up256(4 * nscales);
+    for (int kv = 0; kv < 2; ++kv)
+      for (uint64_t h = 0; h < H; ++h) {
+        const ora_plan_t* p = &plans[group_of(c, gran, (int64_t)l, (int64_t)h)];
+        if (segtab) segtab[2 * ((l * 2 + (uint64_t)kv) * H + h) + 1] = data;
+        data += up256(group_seg_bytes(p, d));
+      }
+    off = data;
+  }
+  g->total = off;
+}
+
+int ora_grouped_size(const ora_config* c, int32_t gran, const float* budgets, uint64_t* bytes) {
+  int32_t G = ora_group_count(c, gran);
+  if (G < 1) return ORA_ERR_INVALID_ARG;
+  ora_plan_t* plans = (ora_plan_t*)malloc((size_t)G * sizeof(ora_plan_t));
+  int st = plan_groups(c, gran, budgets, plans);
+  if (!st) {
+    ora_ggeom g;
+    grouped_layout(c, gran, plans, &g, NULL);
+    *bytes = g.total;
+  }
+  free(plans);
+  return st;
+}
+
+/* Exact sum of squares of token t over the K and V elements of the pairs in
+ * group grp, in units of 2^-48. */
+int ora_sumsq_group(const ora_config* c, int32_t gran, const uint16_t* k, const uint16_t* v, int32_t grp,
+                    int32_t t, uint64_t* hi, uint64_t* lo) {
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens, d = c->head_dim;
+  u128 S = 0;
+  for (int64_t l = 0; l < L; ++l)
+    for (int64_t h = 0; h < H; ++h) {
+      if (group_of(c, gran, l, h) != grp) continue;
+      const uint16_t* kr = k + (((l * H + h) * n + t) * d);
+      const uint16_t* vr = v + (((l * H + h) * n + t) * d);
+      for (int64_t i = 0; i < d; ++i) S += square_units(kr[i]) + square_units(vr[i]);
+    }
+  *hi = (uint64_t)(S >> 64);
+  *lo = (uint64_t)S;
+  return ORA_OK;
+}
+
+/* Mean attention mass of every key over the observation rows of the query
+ * heads that read the group's KV heads (a layer: all Hq query heads of the
+ * layer; a (layer, KV head): its Hq/H query heads), binary64.  Same
+ * statistic and conventions as attention_mass, restricted to the group. */
+static void attention_mass_groups(const ora_config* c, int32_t gran, const uint16_t* k, const uint16_t* q,
+                                  double* A) {
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens, d = c->head_dim;
+  int64_t Hq = c->num_q_heads, W = c->obs_window, grp = Hq / H;
+  int64_t G = ora_group_count(c, gran);
+  double inv_sqrt_d = 1.0 / sqrt((double)d);
+  double* z = (double*)malloc((size_t)n * sizeof(double));
+  double* qv = (double*)malloc((size_t)d * sizeof(double));
+  for (int64_t i = 0; i < G * n; ++i) A[i] = 0.0;
+  for (int64_t l = 0; l < L; ++l)
+    for (int64_t hq = 0; hq < Hq; ++hq) {
+      int64_t h = hq / grp;
+      double* Ag = A + group_of(c, gran, l, h) * n;
+      for (int64_t w = 0; w < W; ++w) {
+        const uint16_t* qr = q + ((l * Hq + hq) * W + w) * d;
+        for (int64_t i = 0; i < d; ++i) qv[i] = ora_half_to_double(qr[i]);
+        double zmax = -INFINITY;
+        for (int64_t t = 0; t < n; ++t) {
+          const uint16_t* kr = k + ((l * H + h) * n + t) * d;
+          double dot = 0.0;
+          for (int64_t i = 0; i < d; ++i) dot += qv[i] * ora_half_to_double(kr[i]);
+          z[t] = dot * inv_sqrt_d;
+          if (z[t] > zmax) zmax = z[t];
+        }
+        double den = 0.0;
+        for (int64_t t = 0; t < n; ++t) { z[t] = exp(z[t] - zmax); den += z[t]; }
+        for (int64_t t = 0; t < n; ++t) Ag[t] += z[t] / den;
+      }
+    }
+  double rows = (double)(gran == GRAN_TOKEN ? L * Hq * W : gran == GRAN_LAYER ? Hq * W : grp * W);
+  for (int64_t i = 0; i < G * n; ++i) A[i] /= rows;
+  free(z);
+  free(qv);
+}
+
+/* key[g*n + t]: the score of token t in group g (eq. "importance" with the
+ * statistic restricted to the group's pairs). */
+int ora_score_groups(const ora_config* c, int32_t gran, const uint16_t* k, const uint16_t* v,
+                     const uint16_t* q, double* key) {
+  int st = ora_validate(c);
+  if (st) return st;
+  int32_t G = ora_group_count(c, gran);
+  if (G < 1) return ORA_ERR_INVALID_ARG;
+  int32_t n = c->num_tokens;
+  double* w = (double*)malloc((size_t)n * sizeof(double));
+  if (c->score_mode == MODE_KVNORM) {
+    ora_decay_table(c->decay, 2, n, w);
+    for (int32_t g = 0; g < G; ++g)
+      for (int32_t t = 0; t < n; ++t) {
+        uint64_t hi, lo;
+        ora_sumsq_group(c, gran, k, v, g, t, &hi, &lo);
+        u128 S = ((u128)hi << 64) | lo;
+        key[(int64_t)g * n + t] = ldexp((double)S, -48) * w[n - 1 - t];
+      }
+  } else if (c->score_mode == MODE_ATTN) {
+    if (!q) { free(w); return ORA_ERR_INVALID_ARG; }
+    ora_decay_table(c->decay, 1, n, w);
+    double* A = (double*)malloc((size_t)G * (size_t)n * sizeof(double));
+    attention_mass_groups(c, gran, k, q, A);
+    for (int32_t g = 0; g < G; ++g)
+      for (int32_t t = 0; t < n; ++t) key[(int64_t)g * n + t] = A[(int64_t)g * n + t] * w[n - 1 - t];
+    free(A);
+  } else {
+    ora_decay_table(c->decay, 1, n, w);
+    for (int32_t g = 0; g < G; ++g)
+      for (int32_t t = 0; t < n; ++t) key[(int64_t)g * n + t] = w[n - 1 - t];
+  }
+  free(w);
+  return ORA_OK;
+}
+
+/* tier[g*n + t]: Prop. 1's assignment within every group, under its budget. */
+int ora_assign_groups(const ora_config* c, int32_t gran, const float* budgets, const double* key,
+                      uint8_t* tier) {
+  int32_t G = ora_group_count(c, gran);
+  if (G < 1) return ORA_ERR_INVALID_ARG;
+  int st = plan_groups(c, gran, budgets, NULL);
+  if (st) return st;
+  int64_t n = c->num_tokens;
+  for (int32_t g = 0; g < G; ++g) {
+    ora_config cg = *c;
+    if (budgets) cg.budget = budgets[g];
+    st = ora_assign(&cg, key + g * n, tier + g * n);
+    if (st) return st;
+  }
+  return ORA_OK;
+}
+
+static void write_grouped_header(const ora_config* c, int32_t gran, const ora_ggeom* g, uint8_t* h) {
+  memset(h, 0, 256);
+  put32(h + 0, ORA_GRP_MAGIC);
+  put32(h + 4, ORA_VERSION);
+  put32(h + 8, (uint32_t)c->num_layers);
+  put32(h + 12, (uint32_t)c->num_kv_heads);
+  put32(h + 16, (uint32_t)c->head_dim);
+  put32(h + 20, (uint32_t)c->num_tokens);
+  put32(h + 24, (uint32_t)gran);
+  put32(h + 28, (uint32_t)g->G);
+  put32(h + 32, (uint32_t)c->num_tiers);
+  put32(h + 36, (uint32_t)c->score_mode);
+  put32(h + 40, fbits(c->budget));
+  put32(h + 44, fbits(c->first_ratio));
+  put32(h + 48, fbits(c->decay));
+  put32(h + 52, (uint32_t)c->num_sink);
+  put32(h + 56, ORA_CHUNK);
+  put64(h + 64, g->group_off);
+  put64(h + 72, g->tiermaps_off);
+  put64(h + 80, g->tiermap_stride);
+  put64(h + 88, g->chunkidx_off);
+  put64(h + 96, g->chunkidx_stride);
+  put64(h + 104, g->segtab_off);
+  put64(h + 112, g->layers_off);
+  put64(h + 120, g->total);
+  put32(h + 128, 0); /* non-finite quantized rows */
+  put32(h + 132, 0); /* status */
+}
+
+/* Everything before the layers: header, group table, tier maps, chunk
+ * indexes, segment table.  units/qrank receive every group's row offsets. */
+static void write_grouped_meta(const ora_config* c, int32_t gran, const float* budgets, const ora_plan_t* plans,
+                               const ora_ggeom* g, const uint64_t* segtab, const uint8_t* tier,
+                               uint32_t* units, uint32_t* qrank, uint8_t* out) {
+  int64_t n = c->num_tokens, L = c->num_layers, H = c->num_kv_heads;
+  write_grouped_header(c, gran, g, out);
+  for (int32_t grp = 0; grp < g->G; ++grp) {
+    const ora_plan_t* p = &plans[grp];
+    uint8_t* e = out + g->group_off + 32 * (uint64_t)grp;
+    put32(e + 0, (uint32_t)p->n_sink);
+    put32(e + 4, (uint32_t)p->n_fp16);
+    put32(e + 8, (uint32_t)p->n_int8);
+    put32(e + 12, (uint32_t)p->n_int4);
+    put32(e + 16, (uint32_t)p->n_drop);
+    put32(e + 20, fbits(budgets ? budgets[grp] : c->budget));
+    put32(e + 24, (uint32_t)(p->n_int8 + p->n_int4));
+    const uint8_t* tg = tier + (int64_t)grp * n;
+    uint8_t* map = out + g->tiermaps_off + (uint64_t)grp * g->tiermap_stride;
+    for (int64_t t = 0; t < n; ++t) map[t / 4] |= (uint8_t)(tg[t] << (2 * (t % 4)));
+    uint32_t* ug = units + (int64_t)grp * n;
+    uint32_t* qg = qrank + (int64_t)grp * n;
+    ora_offsets((int32_t)n, tg, ug, qg);
+    uint8_t* ci = out + g->chunkidx_off + (uint64_t)grp * g->chunkidx_stride;
+    for (int64_t ch = 0; ch < g->nchunks; ++ch) {
+      put32(ci + 8 * ch, ug[ch * ORA_CHUNK]);
+      put32(ci + 8 * ch + 4, qg[ch * ORA_CHUNK]);
+    }
+  }
+  for (int64_t s = 0; s < 2 * L * H; ++s) {
+    put64(out + g->segtab_off + 16 * (uint64_t)s, segtab[2 * s]);
+    put64(out + g->segtab_off + 16 * (uint64_t)s + 8, segtab[2 * s + 1]);
+  }
+}
+
+int ora_pack_groups(const ora_config* c, int32_t gran, const float* budgets, const uint16_t* k,
+                    const uint16_t* v, const uint8_t* tier, uint8_t* payload, uint64_t capacity) {
+  int32_t G = ora_group_count(c, gran);
+  if (G < 1) return ORA_ERR_INVALID_ARG;
+  ora_plan_t* plans = (ora_plan_t*)malloc((size_t)G * sizeof(ora_plan_t));
+  int st = plan_groups(c, gran, budgets, plans);
+  if (st) { free(plans); return st; }
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens, d = c->head_dim;
+  uint64_t* segtab = (uint64_t*)malloc((size_t)(4 * L * H) * sizeof(uint64_t));
+  ora_ggeom g;
+  grouped_layout(c, gran, plans, &g, segtab);
+  st = capacity < g.total ? ORA_ERR_CAPACITY : ORA_OK;
+  /* every group's map must carry exactly its planned counts */
+  for (int32_t grp = 0; grp < G && !st; ++grp) {
+    int64_t cnt[4] = {0, 0, 0, 0};
+    for (int64_t t = 0; t < n && !st; ++t) {
+      uint8_t tr = tier[(int64_t)grp * n + t];
+      if (tr > 3) st = ORA_ERR_INVALID_ARG;
+      else cnt[tr]++;
+    }
+    const ora_plan_t* p = &plans[grp];
+    if (!st && (cnt[T_FP16] != p->n_sink + p->n_fp16 || cnt[T_INT8] != p->n_int8 ||
+                cnt[T_INT4] != p->n_int4 || cnt[T_DROP] != p->n_drop))
+      st = ORA_ERR_INVALID_ARG;
+  }
+  if (st) { free(plans); free(segtab); return st; }
+  memset(payload, 0, g.total);
+  uint32_t* units = (uint32_t*)malloc((size_t)G * (size_t)n * 4);
+  uint32_t* qrank = (uint32_t*)malloc((size_t)G * (size_t)n * 4);
+  write_grouped_meta(c, gran, budgets, plans, &g, segtab, tier, units, qrank, payload);
+  uint32_t nonfinite = 0;
+  uint64_t rowunit = (uint64_t)d / 2;
+  for (int64_t l = 0; l < L; ++l)
+    for (int kv = 0; kv < 2; ++kv)
+      for (int64_t h = 0; h < H; ++h) {
+        int64_t grp = group_of(c, gran, l, h), s = (l * 2 + kv) * H + h;
+        const uint8_t* tg = tier + grp * n;
+        const uint32_t* ug = units + grp * n;
+        const uint32_t* qg = qrank + grp * n;
+        const uint16_t* src = (kv == 0 ? k : v) + ((l * H + h) * n) * d;
+        uint8_t* sc = payload + segtab[2 * s];
+        uint8_t* seg = payload + segtab[2 * s + 1];
+        for (int64_t t = 0; t < n; ++t) {
+          float scale = 0.0f;
+          int bad = ora_encode_row(tg[t], (int32_t)d, src + t * d, seg + ug[t] * rowunit, &scale);
+          if (tg[t] == T_INT8 || tg[t] == T_INT4) {
+            put32(sc + 4 * (uint64_t)qg[t], fbits(scale));
+            nonfinite += (uint32_t)bad;
+          }
+        }
+      }
+  put32(payload + 128, nonfinite);
+  free(units); free(qrank); free(plans); free(segtab);
+  return ORA_OK;
+}
+
+int ora_unpack_groups(const ora_config* c, int32_t gran, const float* budgets, const uint8_t* payload,
+                      uint64_t bytes, uint16_t* kc, uint16_t* vc, const int32_t* block_table,
+                      int32_t num_blocks, int32_t block_size) {
+  int32_t G = ora_group_count(c, gran);
+  if (G < 1) return ORA_ERR_INVALID_ARG;
+  if (block_size < 1 || num_blocks < 1) return ORA_ERR_INVALID_ARG;
+  ora_plan_t* plans = (ora_plan_t*)malloc((size_t)G * sizeof(ora_plan_t));
+  int st = plan_groups(c, gran, budgets, plans);
+  if (st) { free(plans); return st; }
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens, d = c->head_dim;
+  uint64_t* segtab = (uint64_t*)malloc((size_t)(4 * L * H) * sizeof(uint64_t));
+  ora_ggeom g;
+  grouped_layout(c, gran, plans, &g, segtab);
+  int bad = bytes < g.layers_off || bytes < g.total;
+  uint8_t* want = NULL;
+  uint8_t* tier = (uint8_t*)malloc((size_t)G * (size_t)n);
+  uint32_t* units = (uint32_t*)malloc((size_t)G * (size_t)n * 4);
+  uint32_t* qrank = (uint32_t*)malloc((size_t)G * (size_t)n * 4);
+  if (!bad) {
+    /* header (but the non-finite count), group table and segment table must be
+     * exactly what cfg, the granularity and the budgets imply */
+    uint8_t h[256];
+    write_grouped_header(c, gran, &g, h);
+    bad = memcmp(h, payload, 128) != 0 || get32(payload + 132) != 0 ||
+          memcmp(h + 136, payload + 136, 256 - 136) != 0;
+  }
+  for (int32_t grp = 0; grp < G && !bad; ++grp) {
+    const uint8_t* map = payload + g.tiermaps_off + (uint64_t)grp * g.tiermap_stride;
+    int64_t cnt[4] = {0, 0, 0, 0};
+    for (int64_t t = 0; t < n; ++t) {
+      uint8_t tr = (map[t / 4] >> (2 * (t % 4))) & 3;
+      tier[(int64_t)grp * n + t] = tr;
+      cnt[tr]++;
+    }
+    const ora_plan_t* p = &plans[grp];
+    bad = cnt[T_FP16] != p->n_sink + p->n_fp16 || cnt[T_INT8] != p->n_int8 ||
+          cnt[T_INT4] != p->n_int4 || cnt[T_DROP] != p->n_drop;
+  }
+  if (!bad) {
+    /* rebuild the metadata from the decoded maps and compare byte for byte */
+    want = (uint8_t*)calloc((size_t)g.layers_off, 1);
+    write_grouped_meta(c, gran, budgets, plans, &g, segtab, tier, units, qrank, want);
+    bad = memcmp(want + 136, payload + 136, (size_t)(g.layers_off - 136)) != 0;
+  }
+  for (int64_t b = 0; b < (n + block_size - 1) / block_size && !bad; ++b)
+    bad = block_table[b] < 0 || block_table[b] >= num_blocks;
+  if (bad) {
+    free(want); free(tier); free(units); free(qrank); free(plans); free(segtab);
+    return ORA_ERR_FORMAT;
+  }
+  uint64_t rowunit = (uint64_t)d / 2;
+  for (int64_t l = 0; l < L; ++l)
+    for (int kv = 0; kv < 2; ++kv)
+      for (int64_t h = 0; h < H; ++h) {
+        int64_t grp = group_of(c, gran, l, h), s = (l * 2 + kv) * H + h;
+        const uint8_t* tg = tier + grp * n;
+        const uint32_t* ug = units + grp * n;
+        const uint32_t* qg = qrank + grp * n;
+        const uint8_t* sc = payload + segtab[2 * s];
+        const uint8_t* seg = payload + segtab[2 * s + 1];
+        uint16_t* cache = kv == 0 ? kc : vc;
+        for (int64_t t = 0; t < n; ++t) {
+          float scale = 0.0f;
+          if (tg[t] == T_INT8 || tg[t] == T_INT4) {
+            uint32_t bits = get32(sc + 4 * (uint64_t)qg[t]);
+            memcpy(&scale, &bits, 4);
+          }
+          int64_t blk = block_table[t / block_size], slot = t % block_size;
+          uint16_t* dst = cache + (((l * num_blocks + blk) * block_size + slot) * H + h) * d;
+          ora_decode_row(tg[t], (int32_t)d, seg + ug[t] * rowunit, scale, dst);
+        }
+      }
+  free(want); free(tier); free(units); free(qrank); free(plans); free(segtab);
+  return ORA_OK;
+}
