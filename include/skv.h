@@ -303,6 +303,98 @@ skv_status skv_unpack_upgrade(const skv_config* cfg, const void* upgrade, uint64
                               int32_t num_blocks, int32_t block_size, uint32_t* dev_status,
                               hipStream_t stream);
 
+/* Per-layer and per-head tier maps: the extension the paper names as future
+ * work -- a per-layer budget allocation that favours layers whose errors are
+ * amplified the most (Sec. 2.6, Sec. 6.10) and per-head or per-layer
+ * importance scores (Sec. 7.5, Sec. 9 (iii)).  The (layer, KV head) pairs
+ * are split into G groups; each group has its own score, its own budget b_g
+ * (planned by the Sec. 4.4 mapping with sinks pinned, exactly as
+ * skv_plan_tiers does for b) and its own tier map, shared by K and V of its
+ * pairs.  Granularity SKV_GROUP_TOKEN (G = 1) is the paper's map;
+ * SKV_GROUP_LAYER (G = L, group l); SKV_GROUP_HEAD (G = L*H, group l*H + h;
+ * requires L*H <= 65535).
+ *
+ * Grouped payload, little-endian, sections 256-byte aligned, zero padding:
+ *   header 256 B: u32 words 0 magic 0x47564B53 ("SKVG"), 1 version 1, 2-5 L,
+ *     H, d, n, 6 granularity, 7 G, 8 num_tiers, 9 score_mode, 10-12 bits of
+ *     budget, first_ratio, decay, 13 num_sink as configured, 14 chunk tokens
+ *     (256), 15 zero; u64 at words 16, 18, ..., 30: offsets of the group
+ *     table, tier maps, tier-map stride, chunk indexes, chunk-index stride,
+ *     segment table, layers, and the total size; u32 word 32 the number of
+ *     quantized rows holding an inf/NaN, word 33 status; the rest zero
+ *   group table: G x 8 u32 [sinks, fp16, int8, int4, drop, bits of b_g,
+ *     quantized rows, 0]
+ *   G 2-bit tier maps (token t at bits 2(t%4) of byte t/4), each padded to the
+ *     tier-map stride; G chunk indexes (u32 row-width units in d/2 bytes and
+ *     u32 quantized rows before every 256th token), each padded to its stride
+ *   segment table: for (layer, K/V, head) in that order, u64 offsets of the
+ *     segment's scales and of its rows
+ *   layers: [fp32 scales of the layer's 2H segments back to back, padded]
+ *     [its 2H segments, rows in token order at their group's tier widths,
+ *     each padded to 256 B] */
+typedef enum skv_granularity {
+  SKV_GROUP_TOKEN = 0,
+  SKV_GROUP_LAYER = 1,
+  SKV_GROUP_HEAD = 2
+} skv_granularity;
+
+typedef struct skv_group_spec {
+  int32_t granularity;   /* skv_granularity                                      */
+  int32_t reserved;      /* must be 0                                             */
+  const float* budgets;  /* host, G budgets in (0, 1], or NULL: cfg->budget each */
+} skv_group_spec;
+
+/* Host only.  G for cfg and spec. */
+skv_status skv_group_count(const skv_config* cfg, const skv_group_spec* spec, int32_t* count);
+
+/* Host only.  out[g] (G entries): the plan of group g under b_g.  Errors as
+ * skv_plan_tiers, for the first group that fails; SKV_ERR_INVALID_ARG for a
+ * bad spec or budget. */
+skv_status skv_plan_groups(const skv_config* cfg, const skv_group_spec* spec, skv_plan* out);
+
+/* Host only.  Exact size of the grouped payload. */
+skv_status skv_grouped_payload_size(const skv_config* cfg, const skv_group_spec* spec, uint64_t* bytes);
+
+/* Host only.  Device workspace bytes for the grouped calls: the decay table,
+ * the group table, the segment table and score scratch. */
+skv_status skv_group_workspace_size(const skv_config* cfg, const skv_group_spec* spec, uint64_t* bytes);
+
+/* Plans the groups on the host and uploads the decay table (as skv_prepare),
+ * the group table and the segment table into ws; waits for the copy.  Every
+ * other grouped call takes a workspace prepared with the same cfg and spec. */
+skv_status skv_prepare_groups(const skv_config* cfg, const skv_group_spec* spec, void* ws, hipStream_t stream);
+
+/* Scores every token in every group: score is double[G][n].  The statistic of
+ * skv_score restricted to the group's pairs: KV-norm, the exact sum of
+ * squares over the group's K and V elements (bit-exact); attention, the mean
+ * softmax mass over the observation rows of the query heads that read the
+ * group's KV heads (same tolerance as skv_score); recency, the same for every
+ * group.  With SKV_GROUP_TOKEN the result equals skv_score's. */
+skv_status skv_score_groups(const skv_config* cfg, const skv_group_spec* spec, const void* k, const void* v,
+                            const void* q_obs, double* score, void* ws, hipStream_t stream);
+
+/* Assigns every group's tiers from its scores (skv_assign_tiers per group, with
+ * the group's plan): tier is uint8[G][n].  One workgroup per group. */
+skv_status skv_assign_groups(const skv_config* cfg, const skv_group_spec* spec, const double* score,
+                             uint8_t* tier, const void* ws, hipStream_t stream);
+
+/* Packs the grouped payload (rows quantized exactly as skv_pack; segment
+ * (l, K/V, h) uses its group's map).  tier: uint8[G][n], each map on its
+ * group's plan; otherwise the header status and dev_status become
+ * SKV_ERR_INVALID_ARG and no row is written.  dev_status may be NULL. */
+skv_status skv_pack_groups(const skv_config* cfg, const skv_group_spec* spec, const void* k, const void* v,
+                           const uint8_t* tier, const void* ws, void* payload, uint64_t capacity,
+                           uint32_t* dev_status, hipStream_t stream);
+
+/* Decodes a grouped payload into the paged cache (as skv_unpack).  Every
+ * metadata byte (all but the non-finite count) must be what cfg, spec and the
+ * payload's own tier maps imply and every block-table entry in range;
+ * otherwise dev_status (required) becomes SKV_ERR_FORMAT and nothing is
+ * written.  SKV_ERR_FORMAT (host) when payload_bytes is below the size. */
+skv_status skv_unpack_groups(const skv_config* cfg, const skv_group_spec* spec, const void* ws, const void* payload,
+                             uint64_t payload_bytes, void* k_cache, void* v_cache, const int32_t* block_table,
+                             int32_t num_blocks, int32_t block_size, uint32_t* dev_status, hipStream_t stream);
+
 /* Link emulation for a one-GPU setup (Sec. 4.2: the payload crosses the
  * network between prefill and decode).  Copies `bytes` from src to dst on
  * stream: device to device when host_staging is NULL, otherwise device to

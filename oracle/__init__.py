@@ -82,6 +82,8 @@ def _load():
         "ora_pack_groups": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, vp, vp, vp, vp, ctypes.c_uint64]),
         "ora_unpack_groups": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, vp, ctypes.c_uint64, vp, vp, vp,
                                              ctypes.c_int32, ctypes.c_int32]),
+        "ora_pack_groups_meta": (ctypes.c_int, [cfgp, ctypes.c_int32, vp, vp, vp, ctypes.c_uint64,
+                                                P(ctypes.c_uint64)]),
         "ora_half_to_double": (ctypes.c_double, [ctypes.c_uint16]),
         "ora_float_to_half": (ctypes.c_uint16, [ctypes.c_float]),
     }
@@ -365,6 +367,20 @@ def pack_groups(cfg, gran, k, v, tier, budgets=None):
     if st:
         raise OracleError(st, "pack_groups")
     return out
+
+
+def pack_groups_meta(cfg, gran, tier, budgets=None):
+    """The grouped payload's bytes before the layers (header, group table, tier
+    maps, chunk indexes, segment table) for on-plan tier maps."""
+    tier = np.ascontiguousarray(tier, np.uint8)
+    b = _budgets(budgets)
+    size = grouped_size(cfg, gran, b)
+    out = np.empty(size, np.uint8)
+    lo = ctypes.c_uint64()
+    st = _lib.ora_pack_groups_meta(ctypes.byref(cfg), gran, _ptr(b), _ptr(tier), _ptr(out), size, ctypes.byref(lo))
+    if st:
+        raise OracleError(st, "pack_groups_meta")
+    return out[:lo.value].copy()
 
 
 def unpack_groups(cfg, gran, payload, k_cache, v_cache, block_table, block_size=16, budgets=None):

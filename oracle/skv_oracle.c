@@ -1295,3 +1295,27 @@ int ora_unpack_groups(const ora_config* c, int32_t gran, const float* budgets, c
   free(want); free(tier); free(units); free(qrank); free(plans); free(segtab);
   return ORA_OK;
 }
+
+/* The grouped payload's first layers_off bytes (header with a zero non-finite
+ * count, group table, tier maps, chunk indexes, segment table) for tier maps
+ * on their plans; *layers_off receives their size. */
+int ora_pack_groups_meta(const ora_config* c, int32_t gran, const float* budgets, const uint8_t* tier,
+                         uint8_t* out, uint64_t capacity, uint64_t* layers_off) {
+  int32_t G = ora_group_count(c, gran);
+  if (G < 1) return ORA_ERR_INVALID_ARG;
+  ora_plan_t* plans = (ora_plan_t*)malloc((size_t)G * sizeof(ora_plan_t));
+  int st = plan_groups(c, gran, budgets, plans);
+  if (st) { free(plans); return st; }
+  int64_t L = c->num_layers, H = c->num_kv_heads, n = c->num_tokens;
+  uint64_t* segtab = (uint64_t*)malloc((size_t)(4 * L * H) * sizeof(uint64_t));
+  ora_ggeom g;
+  grouped_layout(c, gran, plans, &g, segtab);
+  *layers_off = g.layers_off;
+  if (capacity < g.layers_off) { free(plans); free(segtab); return ORA_ERR_CAPACITY; }
+  uint32_t* units = (uint32_t*)malloc((size_t)G * (size_t)n * 4);
+  uint32_t* qrank = (uint32_t*)malloc((size_t)G * (size_t)n * 4);
+  memset(out, 0, g.layers_off);
+  write_grouped_meta(c, gran, budgets, plans, &g, segtab, tier, units, qrank, out);
+  free(units); free(qrank); free(plans); free(segtab);
+  return ORA_OK;
+}

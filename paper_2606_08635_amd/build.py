@@ -16,7 +16,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libskv.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["skv_api.cpp", "score.hip", "attn.hip", "select.hip", "pack.hip", "unpack.hip", "upgrade.hip"]
+SOURCES = ["skv_api.cpp", "score.hip", "attn.hip", "select.hip", "pack.hip", "unpack.hip", "upgrade.hip", "groups.hip"]
 FLAGS = [
     "-x", "hip", "-std=c++17", "-O3", "--offload-arch=gfx950", "-fPIC",
     "-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt",

@@ -222,6 +222,19 @@ __global__ __launch_bounds__(256) void attn_finish(const float* __restrict__ col
   score[t] = (a * inv_rows) * w1[n - 1 - t];
 }
 
+// grid: (token blocks, groups).  Group g sums the column sums of its
+// pairs_per_group consecutive (layer, KV head) pairs.
+__global__ __launch_bounds__(256) void attn_finish_groups(const float* __restrict__ colsum, int pairs_per_group,
+                                                          int n, double inv_rows, const double* __restrict__ w1,
+                                                          double* __restrict__ score) {
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= n) return;
+  double a = 0.0;
+  const size_t lh0 = static_cast<size_t>(blockIdx.y) * pairs_per_group;
+  for (int j = 0; j < pairs_per_group; ++j) a += static_cast<double>(colsum[(lh0 + j) * n + t]);
+  score[static_cast<size_t>(blockIdx.y) * n + t] = (a * inv_rows) * w1[n - 1 - t];
+}
+
 inline uint64_t up256(uint64_t x) { return (x + 255u) / 256u * 256u; }
 
 struct AttnShape {
@@ -282,6 +295,30 @@ hipError_t launch_score_attn(const Geometry& g, int32_t Hq, int32_t W, const uin
   if (e != hipSuccess) return e;
   const double inv_rows = 1.0 / (static_cast<double>(g.L) * Hq * W);
   attn_finish<<<(g.n + 255) / 256, 256, 0, stream>>>(colsum, s.LH, g.n, inv_rows, w1, score);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_attn_groups(const Geometry& g, int32_t gran, int32_t G, int32_t Hq, int32_t W,
+                                    const uint16_t* k, const uint16_t* q, const double* w1, void* scratch,
+                                    double* score, hipStream_t stream) {
+  const AttnShape s = attn_shape(g, Hq, W);
+  uint8_t* base = static_cast<uint8_t*>(scratch);
+  float2* pstat = reinterpret_cast<float2*>(base);
+  float* cstat = reinterpret_cast<float*>(base + s.pstat_bytes);
+  float* colsum = reinterpret_cast<float*>(base + s.pstat_bytes + s.cstat_bytes);
+  hipError_t e;
+  switch (g.d) {
+    case 32: e = launch_d<32>(g, s, Hq, W, k, q, pstat, cstat, colsum, stream); break;
+    case 64: e = launch_d<64>(g, s, Hq, W, k, q, pstat, cstat, colsum, stream); break;
+    case 128: e = launch_d<128>(g, s, Hq, W, k, q, pstat, cstat, colsum, stream); break;
+    case 256: e = launch_d<256>(g, s, Hq, W, k, q, pstat, cstat, colsum, stream); break;
+    default: return hipErrorInvalidValue;
+  }
+  if (e != hipSuccess) return e;
+  const int pairs_per_group = s.LH / G;  // L*H, H or 1
+  const double inv_rows = 1.0 / (static_cast<double>(pairs_per_group) * (Hq / g.H) * W);
+  const dim3 grid((g.n + 255) / 256, G);
+  attn_finish_groups<<<grid, 256, 0, stream>>>(colsum, pairs_per_group, g.n, inv_rows, w1, score);
   return hipGetLastError();
 }
 

@@ -11,6 +11,7 @@
 // layers of a request can be packed (and sent) in pieces.
 #include "device_util.h"
 #include "row_codec.h"
+#include "row_stream.h"
 #include "skv_internal.h"
 #include "tier_groups.h"
 
@@ -26,9 +27,7 @@ namespace {
 #endif
 
 constexpr int kPrepThreads = 1024;
-constexpr int kRowThreads = 256;  // == kChunkTokens: one token per thread in the scan
 constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
-static_assert(kRowThreads == kChunkTokens, "one scan slot per token of a chunk");
 
 // grid: one workgroup per request
 __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
@@ -101,15 +100,7 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
 // grid: sum over requests of nchunks * 2 * H * layer_count workgroups
 template <int D>
 __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
-  constexpr int LPR = D / 8;                // lanes per row, 16 bytes each
-  constexpr int RPI = kRowThreads / LPR;    // rows per block-wide iteration
-  constexpr int ITERS = kChunkTokens / RPI;
-  constexpr int U = ITERS < SKV_PACK_ROWS_IN_FLIGHT ? ITERS : SKV_PACK_ROWS_IN_FLIGHT;  // rows in flight per thread
-  __shared__ uint8_t s_tier[kChunkTokens];
-  __shared__ uint32_t s_off[kChunkTokens];  // byte offset of the row inside its segment
-  __shared__ uint32_t s_q[kChunkTokens];    // index of the row's scale
-  __shared__ uint32_t s_scan[4];
-
+  __shared__ ChunkLds s;
   const uint64_t bid = blockIdx.x;
   const ReqDesc& r = a.r[request_of_block(a, bid)];
   uint8_t* __restrict__ payload = r.payload;
@@ -128,14 +119,8 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   // row offsets of this chunk: chunk-index base + block exclusive scan
   {
     const int t = t0 + threadIdx.x;
-    const int tr = t < n ? r.tier[t] : kDROP;
-    const uint32_t packed = tier_units(tr) | (tier_quant(tr) << 16);
-    uint32_t total;
-    const uint32_t ex = block_exclusive_scan_256(packed, s_scan, &total);
-    const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off) + 2 * chunk;
-    s_tier[threadIdx.x] = static_cast<uint8_t>(tr);
-    s_off[threadIdx.x] = (cidx[0] + (ex & 0xFFFFu)) * static_cast<uint32_t>(D / 2);
-    s_q[threadIdx.x] = cidx[1] + (ex >> 16);
+    chunk_layout<D>(s, t < n ? r.tier[t] : kDROP,
+                    reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off) + 2 * chunk);
   }
   __syncthreads();
 
@@ -143,37 +128,9 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   uint8_t* lay = payload + r.layers_off + static_cast<uint64_t>(l) * r.layer_stride;
   uint8_t* dst = lay + r.scales_bytes + static_cast<uint64_t>(kv * H + h) * r.seg_stride;
   float* scales = reinterpret_cast<float*>(lay) + static_cast<uint64_t>(kv * H + h) * r.nq;
-  uint32_t* nonfinite = reinterpret_cast<uint32_t*>(payload) + kHdrNonfinite;
-
-  const int lane = threadIdx.x % LPR;
-  const int rsub = threadIdx.x / LPR;
-#pragma unroll 1
-  for (int it = 0; it < ITERS; it += U) {
-    u32x4 x[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int row = (it + u) * RPI + rsub;
-      const int t = t0 + row;
-      x[u] = u32x4{0u, 0u, 0u, 0u};
-      if (t < n && s_tier[row] != kDROP) x[u] = ld_nt16(src + static_cast<size_t>(t) * D + lane * 8);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int row = (it + u) * RPI + rsub;
-      const int tr = s_tier[row];
-      const uint32_t amax = group_max<LPR>(absmax_bits8(x[u]));  // all lanes take part
-      if (tr == kFP16) {
-        store16<SKV_PACK_NT_STORE>(dst + s_off[row] + lane * 16, x[u]);
-      } else if (tr == kINT8 || tr == kINT4) {
-        const LaneCodes q = quantize_lane(x[u], amax, tr == kINT8 ? 127 : 7);
-        if (q.nonfinite && lane == 0) atomicAdd(nonfinite, 1u);
-        uint8_t* out_row = dst + s_off[row];
-        if (tr == kINT8) store8<SKV_PACK_NT_STORE>(out_row + lane * 8, pack_int8(q));
-        else store4<SKV_PACK_NT_STORE>(out_row + lane * 4, pack_int4(q));
-        if (lane == 0) scales[s_q[row]] = q.scale;
-      }
-    }
-  }
+  pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, src, dst, scales,
+                                                            reinterpret_cast<uint32_t*>(payload) + kHdrNonfinite,
+                                                            t0, n);
 
   // padding: segment tail (last chunk) and the layer's scale-section tail
   if (chunk == nchunks - 1) {

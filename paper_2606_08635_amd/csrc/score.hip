@@ -175,6 +175,30 @@ __global__ __launch_bounds__(kThreads) void kvnorm_finish(const uint64_t* __rest
   score[t] = sd * w2[n - 1 - t];
 }
 
+// grid: (token blocks, groups).  Group g's sum is the sum of its
+// parts_per_group consecutive partials.
+__global__ __launch_bounds__(kThreads) void kvnorm_finish_groups(const uint64_t* __restrict__ partial,
+                                                                int parts_per_group, int n,
+                                                                const double* __restrict__ w2,
+                                                                double* __restrict__ score) {
+  const int t = blockIdx.x * kThreads + threadIdx.x;
+  if (t >= n) return;
+  U128 s{0, 0};
+  for (int j = 0; j < parts_per_group; ++j) {
+    const uint64_t* p = partial + ((static_cast<size_t>(blockIdx.y) * parts_per_group + j) * n + t) * 2;
+    s = add128(s, U128{p[0], p[1]});
+  }
+  const double sd = u128_to_double(s) * 0x1p-48;
+  score[static_cast<size_t>(blockIdx.y) * n + t] = sd * w2[n - 1 - t];
+}
+
+// grid: (token blocks, groups)
+__global__ __launch_bounds__(kThreads) void recency_score_groups(const double* __restrict__ w1, int n,
+                                                                double* __restrict__ score) {
+  const int t = blockIdx.x * kThreads + threadIdx.x;
+  if (t < n) score[static_cast<size_t>(blockIdx.y) * n + t] = w1[n - 1 - t];
+}
+
 __global__ __launch_bounds__(kThreads) void recency_score(const double* __restrict__ w1, int n,
                                                          double* __restrict__ score) {
   const int t = blockIdx.x * kThreads + threadIdx.x;
@@ -200,7 +224,59 @@ KvnormLaunch kvnorm_shape(const Geometry& g) {
   return s;
 }
 
+// Partials aligned to the groups of a granularity: a group's pairs are
+// consecutive (pair p = l * H + h), so parts of pairs_per_part pairs never
+// straddle two groups.
+KvnormLaunch kvnorm_shape_groups(const Geometry& g, int gran, int* parts_per_group) {
+  if (gran == SKV_GROUP_TOKEN) {
+    const KvnormLaunch s = kvnorm_shape(g);
+    *parts_per_group = s.groups;
+    return s;
+  }
+  KvnormLaunch s;
+  s.pairs = g.L * g.H;
+  const int tok = kThreads / (g.d / 8);
+  s.blocks_tok = (g.n + tok - 1) / tok;
+  s.pairs_per_group = (gran == SKV_GROUP_LAYER && g.H <= kMaxPairsPerGroup) ? g.H : 1;
+  s.groups = s.pairs / s.pairs_per_group;
+  *parts_per_group = gran == SKV_GROUP_LAYER ? g.H / s.pairs_per_group : 1;
+  return s;
+}
+
 }  // namespace
+
+uint64_t kvnorm_scratch_bytes_groups(const Geometry& g, int32_t gran) {
+  int ppg;
+  const KvnormLaunch s = kvnorm_shape_groups(g, gran, &ppg);
+  return static_cast<uint64_t>(s.groups) * g.n * 16u;
+}
+
+hipError_t launch_score_kvnorm_groups(const Geometry& g, int32_t gran, int32_t G, const uint16_t* k,
+                                      const uint16_t* v, const double* w2, uint64_t* partial, double* score,
+                                      hipStream_t stream) {
+  int ppg;
+  const KvnormLaunch s = kvnorm_shape_groups(g, gran, &ppg);
+  const dim3 grid(s.blocks_tok, s.groups);
+  switch (g.d) {
+    case 32: kvnorm_partial<32><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    case 64: kvnorm_partial<64><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    case 128: kvnorm_partial<128><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    case 256: kvnorm_partial<256><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 fgrid((g.n + kThreads - 1) / kThreads, G);
+  kvnorm_finish_groups<<<fgrid, kThreads, 0, stream>>>(partial, ppg, g.n, w2, score);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_recency_groups(const Geometry& g, int32_t G, const double* w1, double* score,
+                                       hipStream_t stream) {
+  const dim3 grid((g.n + kThreads - 1) / kThreads, G);
+  recency_score_groups<<<grid, kThreads, 0, stream>>>(w1, g.n, score);
+  return hipGetLastError();
+}
 
 uint64_t kvnorm_scratch_bytes(const Geometry& g) {
   const KvnormLaunch s = kvnorm_shape(g);

@@ -52,9 +52,9 @@ struct RunCounter {
   }
 };
 
-__global__ __launch_bounds__(kSelThreads) void assign_tiers(const double* __restrict__ score,
-                                                            uint8_t* __restrict__ tier, int n,
-                                                            int n_sink, int n16, int n8, int n4) {
+// The whole assignment of one score row by one 1024-thread workgroup.
+__device__ __forceinline__ void assign_row(const double* __restrict__ score, uint8_t* __restrict__ tier, int n,
+                                           int n_sink, int n16, int n8, int n4) {
   __shared__ __attribute__((aligned(16))) uint32_t hist[3][kBins];
   __shared__ uint64_t s_prefix[3];
   __shared__ uint32_t s_rank[3];  // remaining rank (1-based) inside the current prefix
@@ -166,11 +166,34 @@ __global__ __launch_bounds__(kSelThreads) void assign_tiers(const double* __rest
   }
 }
 
+__global__ __launch_bounds__(kSelThreads) void assign_tiers(const double* __restrict__ score,
+                                                            uint8_t* __restrict__ tier, int n,
+                                                            int n_sink, int n16, int n8, int n4) {
+  assign_row(score, tier, n, n_sink, n16, n8, n4);
+}
+
+// grid: one workgroup per group; plan counts from the group table
+// (u32 [sinks, fp16, int8, int4, ...], 32 bytes per group).
+__global__ __launch_bounds__(kSelThreads) void assign_tiers_groups(const double* __restrict__ score,
+                                                                   uint8_t* __restrict__ tier, int n,
+                                                                   const uint32_t* __restrict__ group_table) {
+  const uint32_t* e = group_table + 8 * blockIdx.x;
+  const size_t row = static_cast<size_t>(blockIdx.x) * n;
+  assign_row(score + row, tier + row, n, static_cast<int>(e[0]), static_cast<int>(e[1]), static_cast<int>(e[2]),
+             static_cast<int>(e[3]));
+}
+
 }  // namespace
 
 hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier,
                          hipStream_t stream) {
   assign_tiers<<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
+  return hipGetLastError();
+}
+
+hipError_t launch_assign_groups(int32_t G, int32_t n, const uint32_t* group_table, const double* score,
+                                uint8_t* tier, hipStream_t stream) {
+  assign_tiers_groups<<<G, kSelThreads, 0, stream>>>(score, tier, n, group_table);
   return hipGetLastError();
 }
 

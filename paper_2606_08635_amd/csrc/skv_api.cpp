@@ -246,6 +246,127 @@ skv_status launch_batches(const skv_config* cfg, const skv_request* reqs, int32_
   return SKV_OK;
 }
 
+// ---- per-layer / per-head tier maps ----
+
+int32_t group_count(const skv_config* c, int32_t gran) {
+  switch (gran) {
+    case SKV_GROUP_TOKEN: return 1;
+    case SKV_GROUP_LAYER: return c->num_layers;
+    case SKV_GROUP_HEAD: return c->num_layers * c->num_kv_heads;
+    default: return -1;
+  }
+}
+
+struct GroupHost {
+  GroupLaunch gl;
+  std::vector<skv_plan> plans;
+  std::vector<uint32_t> table;   // G x 8 words
+  std::vector<uint64_t> segtab;  // 2LH x {scales offset, rows offset}
+  uint64_t ws_group_off, ws_segtab_off, ws_scratch_off, ws_total;
+};
+
+// Validates cfg and spec, plans every group and lays out the grouped payload
+// and the workspace.
+skv_status group_host(const skv_config* cfg, const skv_group_spec* spec, GroupHost* out) {
+  skv_status st = check_config(cfg);
+  if (st != SKV_OK) return st;
+  if (spec == nullptr || spec->reserved != 0) return SKV_ERR_INVALID_ARG;
+  const int32_t gran = spec->granularity, G = group_count(cfg, gran);
+  if (G < 1) return SKV_ERR_INVALID_ARG;
+  const int64_t L = cfg->num_layers, H = cfg->num_kv_heads, n = cfg->num_tokens, d = cfg->head_dim;
+  if (L * H > 65535) return SKV_ERR_INVALID_ARG;  // a grid dimension holds the (layer, head) pairs
+  out->plans.assign(static_cast<size_t>(G), skv_plan{});
+  out->table.assign(8u * static_cast<size_t>(G), 0u);
+  for (int32_t g = 0; g < G; ++g) {
+    skv_config c = *cfg;
+    if (spec->budgets != nullptr) {
+      const float b = spec->budgets[g];
+      if (!(b > 0.0f) || !(b <= 1.0f)) return SKV_ERR_INVALID_ARG;
+      c.budget = b;
+    }
+    skv_plan& p = out->plans[static_cast<size_t>(g)];
+    st = plan_counts(&c, &p);
+    if (st != SKV_OK) return st;
+    uint32_t* e = &out->table[8u * static_cast<size_t>(g)];
+    e[0] = static_cast<uint32_t>(p.n_sink);
+    e[1] = static_cast<uint32_t>(p.n_fp16);
+    e[2] = static_cast<uint32_t>(p.n_int8);
+    e[3] = static_cast<uint32_t>(p.n_int4);
+    e[4] = static_cast<uint32_t>(p.n_drop);
+    e[5] = float_bits(c.budget);
+    e[6] = static_cast<uint32_t>(p.n_int8 + p.n_int4);
+  }
+  GroupLaunch& gl = out->gl;
+  std::memset(&gl, 0, sizeof(gl));
+  gl.L = cfg->num_layers;
+  gl.H = cfg->num_kv_heads;
+  gl.d = cfg->head_dim;
+  gl.n = cfg->num_tokens;
+  gl.gran = gran;
+  gl.G = G;
+  gl.nchunks = static_cast<int32_t>((n + kChunkTokens - 1) / kChunkTokens);
+  gl.num_tiers = cfg->num_tiers;
+  gl.score_mode = cfg->score_mode;
+  gl.num_sink = cfg->num_sink;
+  gl.budget_bits = float_bits(cfg->budget);
+  gl.rho_bits = float_bits(cfg->first_ratio);
+  gl.decay_bits = float_bits(cfg->decay);
+  gl.group_off = 256;
+  gl.tiermaps_off = gl.group_off + round_up_256(32u * static_cast<uint64_t>(G));
+  gl.tiermap_stride = round_up_256((static_cast<uint64_t>(n) + 3) / 4);
+  gl.chunkidx_off = gl.tiermaps_off + static_cast<uint64_t>(G) * gl.tiermap_stride;
+  gl.chunkidx_stride = round_up_256(8u * static_cast<uint64_t>(gl.nchunks));
+  gl.segtab_off = gl.chunkidx_off + static_cast<uint64_t>(G) * gl.chunkidx_stride;
+  gl.layers_off = gl.segtab_off + round_up_256(32u * static_cast<uint64_t>(L * H));
+  out->segtab.assign(4u * static_cast<size_t>(L * H), 0u);
+  uint64_t off = gl.layers_off;
+  for (int64_t l = 0; l < L; ++l) {
+    auto group = [&](int64_t h) -> const uint32_t* {
+      const int64_t g = gran == SKV_GROUP_TOKEN ? 0 : gran == SKV_GROUP_LAYER ? l : l * H + h;
+      return &out->table[8u * static_cast<size_t>(g)];
+    };
+    uint64_t nscales = 0;
+    for (int kv = 0; kv < 2; ++kv)
+      for (int64_t h = 0; h < H; ++h) {
+        out->segtab[2u * static_cast<size_t>((l * 2 + kv) * H + h)] = off + 4u * nscales;
+        nscales += group(h)[6];
+      }
+    uint64_t data = off + round_up_256(4u * nscales);
+    for (int kv = 0; kv < 2; ++kv)
+      for (int64_t h = 0; h < H; ++h) {
+        const uint32_t* e = group(h);
+        out->segtab[2u * static_cast<size_t>((l * 2 + kv) * H + h) + 1] = data;
+        const uint64_t bytes = static_cast<uint64_t>(e[0] + e[1]) * (2u * d) + static_cast<uint64_t>(e[2]) * d +
+                               static_cast<uint64_t>(e[3]) * (d / 2);
+        data += round_up_256(bytes);
+      }
+    off = data;
+  }
+  gl.total = off;
+  out->ws_group_off = decay_table_bytes(cfg);
+  out->ws_segtab_off = out->ws_group_off + round_up_256(32u * static_cast<uint64_t>(G));
+  out->ws_scratch_off = out->ws_segtab_off + round_up_256(32u * static_cast<uint64_t>(L * H));
+  Geometry geo{};
+  geo.L = gl.L;
+  geo.H = gl.H;
+  geo.d = gl.d;
+  geo.n = gl.n;
+  uint64_t scratch = 0;
+  if (cfg->score_mode == SKV_SCORE_KVNORM) scratch = kvnorm_scratch_bytes_groups(geo, gran);
+  if (cfg->score_mode == SKV_SCORE_ATTN) scratch = attn_scratch_bytes(geo, cfg->num_q_heads, cfg->obs_window);
+  out->ws_total = out->ws_scratch_off + round_up_256(scratch);
+  return SKV_OK;
+}
+
+// The launch description with its table pointers inside the workspace ws.
+GroupLaunch group_launch(const GroupHost& gh, const void* ws) {
+  GroupLaunch gl = gh.gl;
+  const uint8_t* base = static_cast<const uint8_t*>(ws);
+  gl.group_table = reinterpret_cast<const uint32_t*>(base + gh.ws_group_off);
+  gl.segtab = reinterpret_cast<const uint64_t*>(base + gh.ws_segtab_off);
+  return gl;
+}
+
 }  // namespace
 }  // namespace skv
 
@@ -459,6 +580,135 @@ skv_status skv_link(void* dst, const void* src, uint64_t bytes, void* host_stagi
   if (hipMemcpyAsync(host_staging, src, bytes, hipMemcpyDeviceToHost, stream) != hipSuccess)
     return SKV_ERR_DEVICE;
   return launched(hipMemcpyAsync(dst, host_staging, bytes, hipMemcpyHostToDevice, stream));
+}
+
+skv_status skv_group_count(const skv_config* cfg, const skv_group_spec* spec, int32_t* count) {
+  if (count == nullptr) return SKV_ERR_INVALID_ARG;
+  const skv_status st = check_config(cfg);
+  if (st != SKV_OK) return st;
+  if (spec == nullptr || spec->reserved != 0) return SKV_ERR_INVALID_ARG;
+  const int32_t G = group_count(cfg, spec->granularity);
+  if (G < 1) return SKV_ERR_INVALID_ARG;
+  *count = G;
+  return SKV_OK;
+}
+
+skv_status skv_plan_groups(const skv_config* cfg, const skv_group_spec* spec, skv_plan* out) {
+  if (out == nullptr) return SKV_ERR_INVALID_ARG;
+  GroupHost gh;
+  const skv_status st = group_host(cfg, spec, &gh);
+  if (st != SKV_OK) return st;
+  std::copy(gh.plans.begin(), gh.plans.end(), out);
+  return SKV_OK;
+}
+
+skv_status skv_grouped_payload_size(const skv_config* cfg, const skv_group_spec* spec, uint64_t* bytes) {
+  if (bytes == nullptr) return SKV_ERR_INVALID_ARG;
+  GroupHost gh;
+  const skv_status st = group_host(cfg, spec, &gh);
+  if (st == SKV_OK) *bytes = gh.gl.total;
+  return st;
+}
+
+skv_status skv_group_workspace_size(const skv_config* cfg, const skv_group_spec* spec, uint64_t* bytes) {
+  if (bytes == nullptr) return SKV_ERR_INVALID_ARG;
+  GroupHost gh;
+  const skv_status st = group_host(cfg, spec, &gh);
+  if (st == SKV_OK) *bytes = gh.ws_total;
+  return st;
+}
+
+skv_status skv_prepare_groups(const skv_config* cfg, const skv_group_spec* spec, void* ws, hipStream_t stream) {
+  GroupHost gh;
+  const skv_status st = group_host(cfg, spec, &gh);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
+  // decay table (as skv_prepare), group table and segment table in one upload
+  std::vector<uint8_t> host(static_cast<size_t>(gh.ws_scratch_off), 0u);
+  const int n = cfg->num_tokens;
+  const double rate = static_cast<double>(cfg->decay) * (cfg->score_mode == SKV_SCORE_KVNORM ? 2.0 : 1.0);
+  double* table = reinterpret_cast<double*>(host.data());
+#pragma clang loop vectorize(disable)
+  for (int delta = 0; delta < n; ++delta) table[delta] = std::exp(-(rate * static_cast<double>(delta)));
+  std::memcpy(host.data() + gh.ws_group_off, gh.table.data(), gh.table.size() * sizeof(uint32_t));
+  std::memcpy(host.data() + gh.ws_segtab_off, gh.segtab.data(), gh.segtab.size() * sizeof(uint64_t));
+  if (hipMemcpyAsync(ws, host.data(), host.size(), hipMemcpyHostToDevice, stream) != hipSuccess)
+    return SKV_ERR_DEVICE;
+  return hipStreamSynchronize(stream) == hipSuccess ? SKV_OK : SKV_ERR_DEVICE;
+}
+
+skv_status skv_score_groups(const skv_config* cfg, const skv_group_spec* spec, const void* k, const void* v,
+                            const void* q_obs, double* score, void* ws, hipStream_t stream) {
+  GroupHost gh;
+  const skv_status st = group_host(cfg, spec, &gh);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(score) || !dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
+  Geometry g{};
+  g.L = cfg->num_layers;
+  g.H = cfg->num_kv_heads;
+  g.d = cfg->head_dim;
+  g.n = cfg->num_tokens;
+  const double* table = static_cast<const double*>(ws);
+  void* scratch = static_cast<uint8_t*>(ws) + gh.ws_scratch_off;
+  const int32_t gran = spec->granularity, G = gh.gl.G;
+  switch (cfg->score_mode) {
+    case SKV_SCORE_KVNORM:
+      if (!dev_ptr_ok(k) || !dev_ptr_ok(v)) return SKV_ERR_INVALID_ARG;
+      return launched(launch_score_kvnorm_groups(g, gran, G, static_cast<const uint16_t*>(k),
+                                                 static_cast<const uint16_t*>(v), table,
+                                                 static_cast<uint64_t*>(scratch), score, stream));
+    case SKV_SCORE_ATTN:
+      if (!dev_ptr_ok(k) || !dev_ptr_ok(q_obs)) return SKV_ERR_INVALID_ARG;
+      return launched(launch_score_attn_groups(g, gran, G, cfg->num_q_heads, cfg->obs_window,
+                                               static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(q_obs),
+                                               table, scratch, score, stream));
+    default:
+      return launched(launch_score_recency_groups(g, G, table, score, stream));
+  }
+}
+
+skv_status skv_assign_groups(const skv_config* cfg, const skv_group_spec* spec, const double* score,
+                             uint8_t* tier, const void* ws, hipStream_t stream) {
+  GroupHost gh;
+  const skv_status st = group_host(cfg, spec, &gh);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(score) || tier == nullptr || !dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
+  const GroupLaunch gl = group_launch(gh, ws);
+  return launched(launch_assign_groups(gl.G, gl.n, gl.group_table, score, tier, stream));
+}
+
+skv_status skv_pack_groups(const skv_config* cfg, const skv_group_spec* spec, const void* k, const void* v,
+                           const uint8_t* tier, const void* ws, void* payload, uint64_t capacity,
+                           uint32_t* dev_status, hipStream_t stream) {
+  GroupHost gh;
+  const skv_status st = group_host(cfg, spec, &gh);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(k) || !dev_ptr_ok(v) || tier == nullptr || !dev_ptr_ok(ws) || !dev_ptr_ok(payload))
+    return SKV_ERR_INVALID_ARG;
+  if (dev_status != nullptr && !aligned(dev_status, 4)) return SKV_ERR_INVALID_ARG;
+  if (capacity < gh.gl.total) return SKV_ERR_CAPACITY;
+  return launched(launch_pack_groups(group_launch(gh, ws), static_cast<const uint16_t*>(k),
+                                     static_cast<const uint16_t*>(v), tier, static_cast<uint8_t*>(payload),
+                                     dev_status, stream));
+}
+
+skv_status skv_unpack_groups(const skv_config* cfg, const skv_group_spec* spec, const void* ws, const void* payload,
+                             uint64_t payload_bytes, void* k_cache, void* v_cache, const int32_t* block_table,
+                             int32_t num_blocks, int32_t block_size, uint32_t* dev_status, hipStream_t stream) {
+  GroupHost gh;
+  const skv_status st = group_host(cfg, spec, &gh);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(ws) || !dev_ptr_ok(payload) || !dev_ptr_ok(k_cache) || !dev_ptr_ok(v_cache))
+    return SKV_ERR_INVALID_ARG;
+  if (block_table == nullptr || !aligned(block_table, 4)) return SKV_ERR_INVALID_ARG;
+  if (dev_status == nullptr || !aligned(dev_status, 4)) return SKV_ERR_INVALID_ARG;
+  if (num_blocks < 1 || block_size < 1) return SKV_ERR_INVALID_ARG;
+  if (static_cast<uint64_t>(num_blocks) * static_cast<uint64_t>(block_size) > 0xFFFFFFFFull)
+    return SKV_ERR_INVALID_ARG;
+  if (payload_bytes < gh.gl.total) return SKV_ERR_FORMAT;
+  return launched(launch_unpack_groups(group_launch(gh, ws), static_cast<const uint8_t*>(payload),
+                                       static_cast<uint16_t*>(k_cache), static_cast<uint16_t*>(v_cache), block_table,
+                                       num_blocks, block_size, dev_status, stream));
 }
 
 }  // extern "C"

@@ -85,4 +85,32 @@ hipError_t launch_unpack_upgrade(const Geometry& g, const uint8_t* up, int32_t m
 hipError_t launch_unpack(const BatchArgs& a, uint64_t rows, uint16_t* k_cache, uint16_t* v_cache,
                          int32_t num_blocks, int32_t block_size, hipStream_t stream);
 
+// Per-layer / per-head tier maps: everything a grouped launch needs.  The
+// group table (G x 8 words: sinks, fp16, int8, int4, drop, bits of b_g,
+// quantized rows, 0) and the segment table (2LH x {scales offset, rows
+// offset}) live in the caller's workspace, written by skv_prepare_groups.
+struct GroupLaunch {
+  const uint32_t* group_table;
+  const uint64_t* segtab;
+  int32_t L, H, d, n, gran, G, nchunks, num_tiers, score_mode, num_sink;
+  uint32_t budget_bits, rho_bits, decay_bits;
+  uint64_t group_off, tiermaps_off, tiermap_stride, chunkidx_off, chunkidx_stride, segtab_off, layers_off, total;
+};
+hipError_t launch_pack_groups(const GroupLaunch& gl, const uint16_t* k, const uint16_t* v, const uint8_t* tier,
+                              uint8_t* payload, uint32_t* status, hipStream_t stream);
+hipError_t launch_unpack_groups(const GroupLaunch& gl, const uint8_t* payload, uint16_t* k_cache, uint16_t* v_cache,
+                                const int32_t* block_table, int32_t num_blocks, int32_t block_size,
+                                uint32_t* status, hipStream_t stream);
+hipError_t launch_assign_groups(int32_t G, int32_t n, const uint32_t* group_table, const double* score,
+                                uint8_t* tier, hipStream_t stream);
+uint64_t kvnorm_scratch_bytes_groups(const Geometry& g, int32_t gran);
+hipError_t launch_score_kvnorm_groups(const Geometry& g, int32_t gran, int32_t G, const uint16_t* k,
+                                      const uint16_t* v, const double* w2, uint64_t* partial, double* score,
+                                      hipStream_t stream);
+hipError_t launch_score_recency_groups(const Geometry& g, int32_t G, const double* w1, double* score,
+                                       hipStream_t stream);
+hipError_t launch_score_attn_groups(const Geometry& g, int32_t gran, int32_t G, int32_t Hq, int32_t W,
+                                    const uint16_t* k, const uint16_t* q, const double* w1, void* scratch,
+                                    double* score, hipStream_t stream);
+
 }  // namespace skv

@@ -40,11 +40,12 @@ __device__ __forceinline__ TierGroup empty_group() {
   return gi;
 }
 
-// Codes from a uint8[n] tier array (16-byte aligned).
+// Codes from a uint8[n] tier array (16-byte loads where the group is
+// 16-byte aligned, as it always is for an aligned array; bytes otherwise).
 __device__ __forceinline__ TierGroup group_from_bytes(const uint8_t* __restrict__ tier, int n, int g) {
   TierGroup gi = empty_group();
   const int t0 = g * kGroupTokens;
-  if (t0 + kGroupTokens <= n) {
+  if (t0 + kGroupTokens <= n && (reinterpret_cast<uintptr_t>(tier + t0) & 15u) == 0) {
     const u32x4 w = *reinterpret_cast<const u32x4*>(tier + t0);
     const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll

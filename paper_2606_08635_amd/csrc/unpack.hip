@@ -13,6 +13,7 @@
 // block table); a launch may cover a range of layers.
 #include "device_util.h"
 #include "row_codec.h"
+#include "row_stream.h"
 #include "skv_internal.h"
 #include "tier_groups.h"
 
@@ -28,9 +29,7 @@ namespace {
 #endif
 
 constexpr int kCheckThreads = 1024;
-constexpr int kRowThreads = 256;
 constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
-constexpr int kAbsent = 4;  // slot past the end of the request
 
 // grid: one workgroup per request
 __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a, int num_blocks,
@@ -98,50 +97,12 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
   if (tid == 0) *r.status = s_bad ? static_cast<uint32_t>(SKV_ERR_FORMAT) : 0u;
 }
 
-// Loads one row slice of a lane (16 B of FP16, 8 B of INT8 codes or 4 B of
-// INT4 codes) and its scale.
-__device__ __forceinline__ void load_row(int tr, const uint8_t* row, const float* scale_ptr, int lane,
-                                         u32x4& raw, float& sc) {
-  raw = u32x4{0u, 0u, 0u, 0u};
-  sc = 0.0f;
-  if (tr == kFP16) {
-    raw = ld_nt16(row + lane * 16);
-  } else if (tr == kINT8) {
-    const u32x2 c = ld_nt8(row + lane * 8);
-    raw.x = c.x;
-    raw.y = c.y;
-    sc = *scale_ptr;
-  } else if (tr == kINT4) {
-    raw.x = ld_nt4(row + lane * 4);
-    sc = *scale_ptr;
-  }
-}
-
-// The lane's 8 output elements of a row: FP16 verbatim, DROP zeros, INT8/INT4
-// dequantized, a NaN scale giving 0x7E00.
-__device__ __forceinline__ u32x4 decode_row(int tr, u32x4 raw, float sc) {
-  if (tr == kINT8 || tr == kINT4) {
-    if (__builtin_isnan(sc)) return u32x4{kNaNHalf2, kNaNHalf2, kNaNHalf2, kNaNHalf2};
-    return tr == kINT8 ? dequant_int8(u32x2{raw.x, raw.y}, sc) : dequant_int4(raw.x, sc);
-  }
-  return raw;
-}
-
 // grid: sum over requests of nchunks * 2 * H * layer_count workgroups
 template <int D>
 __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, uint16_t* __restrict__ k_cache,
                                                            uint16_t* __restrict__ v_cache, int num_blocks,
                                                            int block_size) {
-  constexpr int LPR = D / 8;
-  constexpr int RPI = kRowThreads / LPR;
-  constexpr int ITERS = kChunkTokens / RPI;
-  constexpr int U = ITERS < SKV_UNPACK_ROWS_IN_FLIGHT ? ITERS : SKV_UNPACK_ROWS_IN_FLIGHT;
-  __shared__ uint8_t s_tier[kChunkTokens];
-  __shared__ uint32_t s_off[kChunkTokens];
-  __shared__ uint32_t s_q[kChunkTokens];
-  __shared__ uint32_t s_pos[kChunkTokens];  // physical block * block_size + slot
-  __shared__ uint32_t s_scan[4];
-
+  __shared__ ChunkLds s;
   const uint64_t bid = blockIdx.x;
   const ReqDesc& r = a.r[request_of_block(a, bid)];
   if (*r.status != 0u) return;  // payload rejected: write nothing
@@ -164,14 +125,8 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
       pos = static_cast<uint32_t>(r.block_table[t / block_size]) * static_cast<uint32_t>(block_size) +
             static_cast<uint32_t>(t % block_size);
     }
-    const uint32_t packed = tr == kAbsent ? 0u : (tier_units(tr) | (tier_quant(tr) << 16));
-    uint32_t total;
-    const uint32_t ex = block_exclusive_scan_256(packed, s_scan, &total);
-    const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off) + 2 * chunk;
-    s_tier[threadIdx.x] = static_cast<uint8_t>(tr);
-    s_off[threadIdx.x] = (cidx[0] + (ex & 0xFFFFu)) * static_cast<uint32_t>(D / 2);
-    s_q[threadIdx.x] = cidx[1] + (ex >> 16);
-    s_pos[threadIdx.x] = pos;
+    chunk_layout<D>(s, tr, reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off) + 2 * chunk);
+    s.pos[threadIdx.x] = pos;
   }
   __syncthreads();
 
@@ -180,26 +135,7 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
   const float* scales = reinterpret_cast<const float*>(lay) + static_cast<uint64_t>(kv * H + h) * r.nq;
   uint16_t* cache = (kv ? v_cache : k_cache) + static_cast<size_t>(l) * num_blocks * block_size * H * D +
                     static_cast<size_t>(h) * D;
-
-  const int lane = threadIdx.x % LPR;
-  const int rsub = threadIdx.x / LPR;
-#pragma unroll 1
-  for (int it = 0; it < ITERS; it += U) {
-    u32x4 raw[U];
-    float sc[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int r = (it + u) * RPI + rsub;
-      load_row(s_tier[r], src + s_off[r], scales + s_q[r], lane, raw[u], sc[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int r = (it + u) * RPI + rsub;
-      const int tr = s_tier[r];
-      if (tr == kAbsent) continue;
-      store16<SKV_UNPACK_NT_STORE>(cache + static_cast<size_t>(s_pos[r]) * H * D + lane * 8, decode_row(tr, raw[u], sc[u]));
-    }
-  }
+  unpack_chunk<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, scales, cache, H);
 }
 
 }  // namespace

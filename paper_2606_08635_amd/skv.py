@@ -19,11 +19,14 @@ OK, ERR_INVALID_ARG, ERR_BUDGET, ERR_CAPACITY, ERR_FORMAT, ERR_DEVICE = range(6)
 FP16, INT8, INT4, DROP = 0, 1, 2, 3
 KVNORM, ATTN, RECENCY = 0, 1, 2
 UPGRADE_FP16, UPGRADE_RESIDUAL8 = 0, 1
+GROUP_TOKEN, GROUP_LAYER, GROUP_HEAD = 0, 1, 2
 
 EXPORTED = ("skv_abi_version", "skv_status_string", "skv_plan_tiers", "skv_payload_size",
             "skv_workspace_size", "skv_prepare", "skv_score", "skv_assign_tiers", "skv_pack",
             "skv_unpack", "skv_pack_batch", "skv_unpack_batch", "skv_link", "skv_upgrade_size",
-            "skv_pack_upgrade", "skv_unpack_upgrade")
+            "skv_pack_upgrade", "skv_unpack_upgrade", "skv_group_count", "skv_plan_groups",
+            "skv_grouped_payload_size", "skv_group_workspace_size", "skv_prepare_groups", "skv_score_groups",
+            "skv_assign_groups", "skv_pack_groups", "skv_unpack_groups")
 
 
 class SkvError(RuntimeError):
@@ -46,6 +49,11 @@ class Request(ctypes.Structure):
                 ("v", ctypes.c_void_p), ("tier", ctypes.c_void_p), ("payload", ctypes.c_void_p),
                 ("payload_bytes", ctypes.c_uint64), ("block_table", ctypes.c_void_p),
                 ("dev_status", ctypes.c_void_p)]
+
+
+class GroupSpec(ctypes.Structure):
+    _fields_ = [("granularity", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("budgets", ctypes.POINTER(ctypes.c_float))]
 
 
 class Plan(ctypes.Structure):
@@ -83,6 +91,15 @@ def lib():
             "skv_pack_batch": (ctypes.c_int, [cfgp, P(Request), i32, i32, i32, vp]),
             "skv_unpack_batch": (ctypes.c_int, [cfgp, P(Request), i32, vp, vp, i32, i32, i32, i32, vp]),
             "skv_upgrade_size": (ctypes.c_int, [cfgp, i32, i32, P(u64)]),
+            "skv_group_count": (ctypes.c_int, [cfgp, P(GroupSpec), P(i32)]),
+            "skv_plan_groups": (ctypes.c_int, [cfgp, P(GroupSpec), P(Plan)]),
+            "skv_grouped_payload_size": (ctypes.c_int, [cfgp, P(GroupSpec), P(u64)]),
+            "skv_group_workspace_size": (ctypes.c_int, [cfgp, P(GroupSpec), P(u64)]),
+            "skv_prepare_groups": (ctypes.c_int, [cfgp, P(GroupSpec), vp, vp]),
+            "skv_score_groups": (ctypes.c_int, [cfgp, P(GroupSpec), vp, vp, vp, vp, vp, vp]),
+            "skv_assign_groups": (ctypes.c_int, [cfgp, P(GroupSpec), vp, vp, vp, vp]),
+            "skv_pack_groups": (ctypes.c_int, [cfgp, P(GroupSpec), vp, vp, vp, vp, vp, u64, vp, vp]),
+            "skv_unpack_groups": (ctypes.c_int, [cfgp, P(GroupSpec), vp, vp, u64, vp, vp, vp, i32, i32, vp, vp]),
             "skv_pack_upgrade": (ctypes.c_int, [cfgp, vp, vp, vp, vp, i32, i32, vp, u64, vp, vp]),
             "skv_unpack_upgrade": (ctypes.c_int, [cfgp, vp, u64, i32, i32, vp, vp, vp, i32, i32, vp, vp]),
         }
@@ -236,6 +253,111 @@ def unpack_upgrade(cfg: Config, upgrade: torch.Tensor, m: int, mode: int, k_cach
                                     _dev(block_table, torch.int32, nbt, "block_table"), nb, block_size,
                                     _dev(dev_status, torch.int32, 1, "dev_status"), _stream(stream)),
            "skv_unpack_upgrade")
+
+
+class Groups:
+    """A granularity and optional per-group budgets (host float32 array of G
+    entries in (0, 1]) for the grouped calls; keeps the budget array alive."""
+
+    def __init__(self, granularity: int, budgets=None):
+        import numpy as np
+
+        self.budgets = None if budgets is None else np.ascontiguousarray(budgets, np.float32)
+        ptr = None if self.budgets is None else self.budgets.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+        self.spec = GroupSpec(granularity, 0, ptr)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.spec)
+
+
+def group_count(cfg: Config, groups: Groups) -> int:
+    out = ctypes.c_int32()
+    _check(lib().skv_group_count(ctypes.byref(cfg), groups.ref, ctypes.byref(out)), "skv_group_count")
+    return out.value
+
+
+def plan_groups(cfg: Config, groups: Groups) -> list:
+    G = group_count(cfg, groups)
+    plans = (Plan * G)()
+    _check(lib().skv_plan_groups(ctypes.byref(cfg), groups.ref, plans), "skv_plan_groups")
+    return [{f: getattr(p, f) for f, _ in Plan._fields_} for p in plans]
+
+
+def grouped_payload_size(cfg: Config, groups: Groups) -> int:
+    out = ctypes.c_uint64()
+    _check(lib().skv_grouped_payload_size(ctypes.byref(cfg), groups.ref, ctypes.byref(out)),
+           "skv_grouped_payload_size")
+    return out.value
+
+
+def group_workspace_size(cfg: Config, groups: Groups) -> int:
+    out = ctypes.c_uint64()
+    _check(lib().skv_group_workspace_size(ctypes.byref(cfg), groups.ref, ctypes.byref(out)),
+           "skv_group_workspace_size")
+    return out.value
+
+
+def prepare_groups(cfg: Config, groups: Groups, ws: torch.Tensor, stream=None):
+    _check(lib().skv_prepare_groups(ctypes.byref(cfg), groups.ref,
+                                    _dev(ws, torch.uint8, group_workspace_size(cfg, groups), "ws"),
+                                    _stream(stream)), "skv_prepare_groups")
+
+
+def score_groups(cfg: Config, groups: Groups, k: torch.Tensor, v: Optional[torch.Tensor],
+                 q_obs: Optional[torch.Tensor], out: torch.Tensor, ws: torch.Tensor, stream=None):
+    n = _kv_numel(cfg)
+    G = group_count(cfg, groups)
+    kp = _dev(k, torch.float16, n, "k")
+    vp = _dev(v, torch.float16, n, "v") if cfg.score_mode != ATTN else ctypes.c_void_p(None)
+    qp = ctypes.c_void_p(None)
+    if cfg.score_mode == ATTN:
+        qp = _dev(q_obs, torch.float16, cfg.num_layers * cfg.num_q_heads * cfg.obs_window * cfg.head_dim, "q_obs")
+    _check(lib().skv_score_groups(ctypes.byref(cfg), groups.ref, kp, vp, qp,
+                                  _dev(out, torch.float64, G * cfg.num_tokens, "score"),
+                                  _dev(ws, torch.uint8, group_workspace_size(cfg, groups), "ws"), _stream(stream)),
+           "skv_score_groups")
+
+
+def assign_groups(cfg: Config, groups: Groups, scores: torch.Tensor, tier: torch.Tensor, ws: torch.Tensor,
+                  stream=None):
+    G = group_count(cfg, groups)
+    _check(lib().skv_assign_groups(ctypes.byref(cfg), groups.ref,
+                                   _dev(scores, torch.float64, G * cfg.num_tokens, "score"),
+                                   _dev(tier, torch.uint8, G * cfg.num_tokens, "tier"),
+                                   _dev(ws, torch.uint8, group_workspace_size(cfg, groups), "ws"),
+                                   _stream(stream)), "skv_assign_groups")
+
+
+def pack_groups(cfg: Config, groups: Groups, k: torch.Tensor, v: torch.Tensor, tier: torch.Tensor,
+                ws: torch.Tensor, payload: torch.Tensor, dev_status: Optional[torch.Tensor] = None, stream=None):
+    n = _kv_numel(cfg)
+    G = group_count(cfg, groups)
+    st = ctypes.c_void_p(None) if dev_status is None else _dev(dev_status, torch.int32, 1, "dev_status")
+    _check(lib().skv_pack_groups(ctypes.byref(cfg), groups.ref, _dev(k, torch.float16, n, "k"),
+                                 _dev(v, torch.float16, n, "v"), _dev(tier, torch.uint8, G * cfg.num_tokens, "tier"),
+                                 _dev(ws, torch.uint8, group_workspace_size(cfg, groups), "ws"),
+                                 _dev(payload, torch.uint8, 0, "payload"), payload.numel(), st, _stream(stream)),
+           "skv_pack_groups")
+
+
+def unpack_groups(cfg: Config, groups: Groups, ws: torch.Tensor, payload: torch.Tensor, k_cache: torch.Tensor,
+                  v_cache: torch.Tensor, block_table: torch.Tensor, block_size: int, dev_status: torch.Tensor,
+                  stream=None):
+    if k_cache.dim() != 5 or k_cache.shape[2] != block_size or tuple(k_cache.shape) != tuple(v_cache.shape):
+        raise ValueError("caches must be [L][num_blocks][block_size][H][d] and alike")
+    L, nb, _, H, d = k_cache.shape
+    if (L, H, d) != (cfg.num_layers, cfg.num_kv_heads, cfg.head_dim):
+        raise ValueError("cache shape does not match the configuration")
+    nbt = -(-cfg.num_tokens // block_size)
+    _check(lib().skv_unpack_groups(ctypes.byref(cfg), groups.ref,
+                                   _dev(ws, torch.uint8, group_workspace_size(cfg, groups), "ws"),
+                                   _dev(payload, torch.uint8, 0, "payload"), payload.numel(),
+                                   _dev(k_cache, torch.float16, k_cache.numel(), "k_cache"),
+                                   _dev(v_cache, torch.float16, v_cache.numel(), "v_cache"),
+                                   _dev(block_table, torch.int32, nbt, "block_table"), nb, block_size,
+                                   _dev(dev_status, torch.int32, 1, "dev_status"), _stream(stream)),
+           "skv_unpack_groups")
 
 
 def _with_tokens(cfg: Config, n: int) -> Config:

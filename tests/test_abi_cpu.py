@@ -182,3 +182,63 @@ def test_upgrade_size_and_argument_errors(lib):
     assert L.skv_unpack_upgrade(by, fake, size, 10, 1, fake, fake, None, 20, 16, fake, None) == skv.ERR_INVALID_ARG
     assert L.skv_unpack_upgrade(by, fake, size, 10, 1, fake, fake, fake, 0, 16, fake, None) == skv.ERR_INVALID_ARG
     assert L.skv_unpack_upgrade(by, odd, size, 10, 1, fake, fake, fake, 20, 16, fake, None) == skv.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_grouped_plans_and_sizes_match_oracle(lib, seed):
+    rng = np.random.default_rng(100 + seed)
+    for _ in range(120):
+        L, H = int(rng.integers(1, 6)), int(rng.integers(1, 9))
+        d = int(rng.choice([32, 64, 128, 256]))
+        n = int(rng.integers(1, 40000))
+        gran = int(rng.integers(0, 3))
+        kw = dict(num_tiers=int(rng.integers(2, 4)), decay=0.0, num_sink=int(rng.choice([-1, -1, 0, 3])))
+        c, o = _pair(L, H, d, n, float(np.float32(rng.uniform(0.05, 1.0))), **kw)
+        G = oracle.group_count(o, gran)
+        budgets = None if rng.random() < 0.3 else np.float32(rng.uniform(0.02, 1.0, G))
+        groups = skv.Groups(gran, budgets)
+        assert skv.group_count(c, groups) == G
+        try:
+            want = oracle.grouped_size(o, gran, budgets)
+        except oracle.OracleError as e:
+            with pytest.raises(skv.SkvError) as got:
+                skv.grouped_payload_size(c, groups)
+            assert got.value.status == e.status
+            continue
+        assert skv.grouped_payload_size(c, groups) == want
+        assert skv.plan_groups(c, groups) == [oracle.plan_group(o, gran, budgets, g) for g in range(G)]
+        assert skv.group_workspace_size(c, groups) % 256 == 0
+
+
+def test_grouped_argument_errors(lib):
+    cfg = skv.config(2, 2, 64, 300, 0.5)
+    by = ctypes.byref(cfg)
+    P = ctypes.c_void_p
+    fake, odd = P(1 << 20), P((1 << 20) + 8)
+    for gran, budgets in ((3, None), (-1, None), (skv.GROUP_LAYER, [0.5, 0.0]), (skv.GROUP_LAYER, [0.5, 1.5]),
+                          (skv.GROUP_HEAD, [0.5, 0.5, float("nan"), 0.5])):
+        with pytest.raises(skv.SkvError) as e:
+            skv.grouped_payload_size(cfg, skv.Groups(gran, budgets))
+        assert e.value.status == skv.ERR_INVALID_ARG
+    g = skv.Groups(skv.GROUP_LAYER, [0.9, 0.1])
+    g.spec.reserved = 1
+    with pytest.raises(skv.SkvError):
+        skv.group_count(cfg, g)
+    with pytest.raises(skv.SkvError) as e:  # sinks alone exceed a group's budget
+        skv.plan_groups(skv.config(2, 1, 64, 100, 0.5, num_sink=20), skv.Groups(skv.GROUP_LAYER, [0.5, 0.04]))
+    assert e.value.status == skv.ERR_BUDGET
+    with pytest.raises(skv.SkvError):  # too many (layer, head) pairs for one grid dimension
+        skv.grouped_payload_size(skv.config(256, 256, 32, 10, 0.5), skv.Groups(skv.GROUP_HEAD))
+    g = skv.Groups(skv.GROUP_HEAD)
+    total = skv.grouped_payload_size(cfg, g)
+    L = lib
+    assert L.skv_pack_groups(by, g.ref, fake, fake, fake, fake, fake, total - 1, None, None) == skv.ERR_CAPACITY
+    assert L.skv_pack_groups(by, g.ref, fake, odd, fake, fake, fake, total, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_pack_groups(by, g.ref, fake, fake, fake, None, fake, total, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_unpack_groups(by, g.ref, fake, fake, total - 1, fake, fake, fake, 20, 16, fake, None) == skv.ERR_FORMAT
+    assert L.skv_unpack_groups(by, g.ref, fake, fake, total, fake, fake, fake, 20, 16, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_unpack_groups(by, g.ref, fake, fake, total, fake, fake, fake, 0, 16, fake, None) == skv.ERR_INVALID_ARG
+    assert L.skv_score_groups(by, g.ref, fake, fake, None, odd, fake, None) == skv.ERR_INVALID_ARG
+    assert L.skv_assign_groups(by, g.ref, fake, fake, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_prepare_groups(by, g.ref, None, None) == skv.ERR_INVALID_ARG
+    assert L.skv_score_groups(by, None, fake, fake, None, fake, fake, None) == skv.ERR_INVALID_ARG

@@ -240,3 +240,20 @@ def test_grouped_payload_errors():
     table[0] = nb
     assert status(pay, table) == oracle.ERR_FORMAT
     assert status(pay[:-1]) == oracle.ERR_FORMAT
+
+
+@pytest.mark.parametrize("gran", GRANS)
+def test_metadata_writer_matches_the_packed_payload(gran):
+    L, H, d, n = 2, 3, 64, 700
+    cfg = oracle.config(L, H, d, n, 0.45)
+    k, v = _kv(L, H, n, d, 17)
+    G = oracle.group_count(cfg, gran)
+    budgets = np.float32(np.linspace(0.3, 0.8, G))
+    tier = oracle.assign_groups(cfg, gran, oracle.score_groups(cfg, gran, k, v), budgets)
+    pay = oracle.pack_groups(cfg, gran, k, v, tier, budgets)
+    meta = oracle.pack_groups_meta(cfg, gran, tier, budgets)
+    lo = int(pay[112:120].view(np.uint64)[0])
+    assert meta.size == lo
+    want = pay[:lo].copy()
+    want[128:132] = 0  # the metadata writer leaves the non-finite count at zero
+    assert np.array_equal(meta, want)
