@@ -297,6 +297,62 @@ def run_upgrade(args, w):
     return out
 
 
+def run_groups(args, w):
+    """Per-layer and per-head tier maps (NEXT-3) on the workload's request:
+    score -> assign -> pack -> unpack with one map per layer (budgets falling
+    linearly from 0.7 to 0.3, mean 0.5) and with one map per (layer, head) at
+    the workload's budget.  Returns a JSON-able dict."""
+    import numpy as np
+    import torch
+
+    from paper_2606_08635_amd import skv, workloads
+
+    L, H, d, n, bs = w.layers, w.kv_heads, w.head_dim, w.tokens, 16
+    cfg = skv.config(L, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers)
+    k, v = workloads.make_kv(L, H, n, d, seed=0, outliers=w.outliers, device="cuda")
+    nb = workloads.blocks_for(n, bs)
+    bt = workloads.make_block_table(n, bs, nb, seed=0, device="cuda")
+    kc = torch.empty(L, nb, bs, H, d, dtype=torch.float16, device="cuda")
+    vc = torch.empty_like(kc)
+    out = {"workload": w.name}
+    for name, gran, budgets in (("per_layer", skv.GROUP_LAYER, np.float32(np.linspace(0.7, 0.3, L))),
+                                ("per_head", skv.GROUP_HEAD, None)):
+        groups = skv.Groups(gran, budgets)
+        G = skv.group_count(cfg, groups)
+        ws = torch.empty(skv.group_workspace_size(cfg, groups), dtype=torch.uint8, device="cuda")
+        skv.prepare_groups(cfg, groups, ws)
+        sc = torch.empty(G * n, dtype=torch.float64, device="cuda")
+        tier = torch.empty(G * n, dtype=torch.uint8, device="cuda")
+        pay = torch.empty(skv.grouped_payload_size(cfg, groups), dtype=torch.uint8, device="cuda")
+        st = torch.zeros(2, dtype=torch.int32, device="cuda")
+
+        def step(ev=None):
+            if ev: ev[0].record()
+            skv.score_groups(cfg, groups, k, v, None, sc, ws)
+            if ev: ev[1].record()
+            skv.assign_groups(cfg, groups, sc, tier, ws)
+            if ev: ev[2].record()
+            skv.pack_groups(cfg, groups, k, v, tier, ws, pay, st[0:1])
+            if ev: ev[3].record()
+            skv.unpack_groups(cfg, groups, ws, pay, kc, vc, bt, bs, st[1:2])
+            if ev: ev[4].record()
+
+        for _ in range(args.warmup):
+            step()
+        evs = [_events(5) for _ in range(args.steps)]
+        for e in evs:
+            step(e)
+        torch.cuda.synchronize()
+        if st.cpu().tolist() != [0, 0]:
+            raise RuntimeError(f"grouped codec reported status {st.cpu().tolist()}")
+        ms = {nm: sum(e[i].elapsed_time(e[i + 1]) for e in evs) / args.steps
+              for i, nm in enumerate(("score", "assign", "pack", "unpack"))}
+        t = (ms["pack"] + ms["unpack"]) / 1e3
+        out[name] = {"groups": G, "payload_bytes": pay.numel(), "stages_ms": {a: round(b, 4) for a, b in ms.items()},
+                     "fp16eq_gbps": round(w.fp16_bytes / t / 1e9, 2)}
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -308,10 +364,11 @@ def main():
     ap.add_argument("--score", choices=["kvnorm", "attn"], default="kvnorm",
                     help="importance statistic; attn uses a W-query observation window per query head")
     ap.add_argument("--obs-window", type=int, default=32)
-    ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade"], default="step",
+    ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade", "groups"], default="step",
                     help="step: the headline codec step; batch: per-request vs batched launches over "
                          "a multi-request workload; pipeline: layer-pipelined handoff latency; "
-                         "upgrade: cold-tier precision upgrade after the step")
+                         "upgrade: cold-tier precision upgrade after the step; "
+                         "groups: per-layer and per-head tier maps")
     ap.add_argument("--group-layers", type=int, default=4, help="layers per pipeline stage (--mode pipeline)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer with skv_link (reference for byte counters)")
@@ -347,6 +404,9 @@ def main():
         return
     if args.mode == "upgrade":
         print(json.dumps({"mode": "upgrade", **run_upgrade(args, w)}), flush=True)
+        return
+    if args.mode == "groups":
+        print(json.dumps({"mode": "groups", **run_groups(args, w)}), flush=True)
         return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)

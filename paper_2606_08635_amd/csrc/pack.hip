@@ -108,9 +108,10 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   if (hdr[kHdrStatus] != 0u) return;  // tier map off plan: nothing to pack
 
   const int n = r.n, H = a.H, nchunks = r.nchunks;
-  const uint64_t local = bid - r.block_begin;
-  const int chunk = static_cast<int>(local % nchunks);
-  const int seg = static_cast<int>(local / nchunks);  // ((l - layer_begin) * 2 + kv) * H + h
+  // a launch has fewer than 2^32 workgroups: 32-bit index arithmetic
+  const uint32_t local = static_cast<uint32_t>(bid - r.block_begin);
+  const int chunk = static_cast<int>(local % static_cast<uint32_t>(nchunks));
+  const int seg = static_cast<int>(local / static_cast<uint32_t>(nchunks));  // ((l - layer_begin) * 2 + kv) * H + h
   const int h = seg % H;
   const int kv = (seg / H) & 1;
   const int l = a.layer_begin + seg / (2 * H);

@@ -80,13 +80,15 @@ __device__ __forceinline__ void acc16(u32x4 x, double& ah, double& al) {
   acc_word(x.w, ah, al);
 }
 
-// One block: TOK tokens x all LPR lanes of their rows, for the (layer, head)
-// pairs [p0, p1) of group blockIdx.y.  Writes the 128-bit partial sum of each
-// token in units of 2^-48 to partial[(group * n + t) * 2 + {0: lo, 1: hi}].
+// One block: TOK tokens x all LPR lanes of their rows, for parts_per_block
+// consecutive parts starting at part blockIdx.y * parts_per_block; part j
+// covers the (layer, head) pairs [j * pairs_per_group, (j + 1) *
+// pairs_per_group).  Writes the 128-bit partial sum of each token and part in
+// units of 2^-48 to partial[(part * n + t) * 2 + {0: lo, 1: hi}].
 template <int D>
 __global__ __launch_bounds__(kThreads) void kvnorm_partial(const uint16_t* __restrict__ k,
                                                           const uint16_t* __restrict__ v, int n,
-                                                          int pairs, int pairs_per_group,
+                                                          int pairs, int pairs_per_group, int parts_per_block,
                                                           uint64_t* __restrict__ partial) {
   constexpr int LPR = D / 8;
   constexpr int TOK = kThreads / LPR;
@@ -94,7 +96,10 @@ __global__ __launch_bounds__(kThreads) void kvnorm_partial(const uint16_t* __res
   const int lane = threadIdx.x % LPR;
   const int r = threadIdx.x / LPR;
   const int t = blockIdx.x * TOK + r;
-  const int p0 = blockIdx.y * pairs_per_group;
+  for (int pb = 0; pb < parts_per_block; ++pb) {  // block-uniform
+  const int part = blockIdx.y * parts_per_block + pb;
+  const int p0 = part * pairs_per_group;
+  if (p0 >= pairs) break;
   const int p1 = min(pairs, p0 + pairs_per_group);
   const size_t pair_stride = static_cast<size_t>(n) * D;  // elements between (l, h) pairs
   double ah0 = 0.0, al0 = 0.0, ah1 = 0.0, al1 = 0.0;
@@ -153,9 +158,11 @@ __global__ __launch_bounds__(kThreads) void kvnorm_partial(const uint16_t* __res
     U128 s = s_part[threadIdx.x];
 #pragma unroll
     for (int i = 1; i < LPR; ++i) s = add128(s, s_part[threadIdx.x + i]);
-    uint64_t* out = partial + (static_cast<size_t>(blockIdx.y) * n + t) * 2;
+    uint64_t* out = partial + (static_cast<size_t>(part) * n + t) * 2;
     out[0] = s.lo;
     out[1] = s.hi;
+  }
+  __syncthreads();  // s_part is reused by the next part
   }
 }
 
@@ -207,6 +214,7 @@ __global__ __launch_bounds__(kThreads) void recency_score(const double* __restri
 
 struct KvnormLaunch {
   int pairs, groups, pairs_per_group, blocks_tok;
+  int parts_per_block = 1;
 };
 
 KvnormLaunch kvnorm_shape(const Geometry& g) {
@@ -214,11 +222,12 @@ KvnormLaunch kvnorm_shape(const Geometry& g) {
   s.pairs = g.L * g.H;
   const int tok = kThreads / (g.d / 8);
   s.blocks_tok = (g.n + tok - 1) / tok;
-  // enough blocks to give every SIMD of the 256 CUs several waves, and few
-  // enough pairs per group that each thread's binary64 sums stay exact
-  int groups = (2048 + s.blocks_tok - 1) / s.blocks_tok;
+  // enough blocks (about 256 per CU) that many loads are in flight on every
+  // CU, and few enough pairs per group that each thread's binary64 sums stay
+  // exact
+  int groups = (65536 + s.blocks_tok - 1) / s.blocks_tok;
   groups = max(groups, (s.pairs + kMaxPairsPerGroup - 1) / kMaxPairsPerGroup);
-  groups = min(groups, s.pairs);
+  groups = min(min(groups, s.pairs), 32768);  // a grid's y extent stays below 65536
   s.pairs_per_group = (s.pairs + groups - 1) / groups;
   s.groups = (s.pairs + s.pairs_per_group - 1) / s.pairs_per_group;
   return s;
@@ -240,6 +249,9 @@ KvnormLaunch kvnorm_shape_groups(const Geometry& g, int gran, int* parts_per_gro
   s.pairs_per_group = (gran == SKV_GROUP_LAYER && g.H <= kMaxPairsPerGroup) ? g.H : 1;
   s.groups = s.pairs / s.pairs_per_group;
   *parts_per_group = gran == SKV_GROUP_LAYER ? g.H / s.pairs_per_group : 1;
+  // one part per pair: a block covers several parts (written separately) so
+  // that it streams as much as a block of the coarser shapes
+  if (s.pairs_per_group == 1) s.parts_per_block = min(8, s.groups);
   return s;
 }
 
@@ -256,12 +268,13 @@ hipError_t launch_score_kvnorm_groups(const Geometry& g, int32_t gran, int32_t G
                                       hipStream_t stream) {
   int ppg;
   const KvnormLaunch s = kvnorm_shape_groups(g, gran, &ppg);
-  const dim3 grid(s.blocks_tok, s.groups);
+  const dim3 grid(s.blocks_tok, (s.groups + s.parts_per_block - 1) / s.parts_per_block);
+  const int ppb = s.parts_per_block;
   switch (g.d) {
-    case 32: kvnorm_partial<32><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
-    case 64: kvnorm_partial<64><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
-    case 128: kvnorm_partial<128><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
-    case 256: kvnorm_partial<256><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    case 32: kvnorm_partial<32><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
+    case 64: kvnorm_partial<64><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
+    case 128: kvnorm_partial<128><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
+    case 256: kvnorm_partial<256><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
@@ -287,12 +300,13 @@ hipError_t launch_score_kvnorm(const Geometry& g, const uint16_t* k, const uint1
                                const double* w2, uint64_t* partial, double* score,
                                hipStream_t stream) {
   const KvnormLaunch s = kvnorm_shape(g);
-  const dim3 grid(s.blocks_tok, s.groups);
+  const dim3 grid(s.blocks_tok, (s.groups + s.parts_per_block - 1) / s.parts_per_block);
+  const int ppb = s.parts_per_block;
   switch (g.d) {
-    case 32: kvnorm_partial<32><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
-    case 64: kvnorm_partial<64><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
-    case 128: kvnorm_partial<128><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
-    case 256: kvnorm_partial<256><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, partial); break;
+    case 32: kvnorm_partial<32><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
+    case 64: kvnorm_partial<64><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
+    case 128: kvnorm_partial<128><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
+    case 256: kvnorm_partial<256><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
     default: return hipErrorInvalidValue;
   }
   hipError_t e = hipGetLastError();
