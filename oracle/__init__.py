@@ -19,6 +19,8 @@ from . import build as _build
 OK, ERR_INVALID_ARG, ERR_BUDGET, ERR_CAPACITY, ERR_FORMAT = 0, 1, 2, 3, 4
 FP16, INT8, INT4, DROP = 0, 1, 2, 3
 KVNORM, ATTN, RECENCY = 0, 1, 2
+# quantizer variant descriptor bits: group size (0 row, 1: 64, 2: 32), asymmetric, binary16 metadata
+QUANT_GROUP64, QUANT_GROUP32, QUANT_ASYM, QUANT_FP16 = 1, 2, 4, 8
 GRAN_TOKEN, GRAN_LAYER, GRAN_HEAD = 0, 1, 2
 CHUNK_TOKENS = 256
 
@@ -35,7 +37,8 @@ class Config(ctypes.Structure):
                 ("budget", ctypes.c_float), ("first_ratio", ctypes.c_float),
                 ("num_sink", ctypes.c_int32), ("decay", ctypes.c_float),
                 ("num_tiers", ctypes.c_int32), ("score_mode", ctypes.c_int32),
-                ("num_q_heads", ctypes.c_int32), ("obs_window", ctypes.c_int32)]
+                ("num_q_heads", ctypes.c_int32), ("obs_window", ctypes.c_int32),
+                ("quant_int8", ctypes.c_int32), ("quant_int4", ctypes.c_int32)]
 
 
 class Plan(ctypes.Structure):
@@ -64,6 +67,9 @@ def _load():
         "ora_offsets": (None, [ctypes.c_int32, vp, vp, vp]),
         "ora_encode_row": (ctypes.c_int, [ctypes.c_int, ctypes.c_int32, vp, vp, P(ctypes.c_float)]),
         "ora_decode_row": (None, [ctypes.c_int, ctypes.c_int32, vp, ctypes.c_float, vp]),
+        "ora_encode_row_q": (ctypes.c_int, [ctypes.c_int, ctypes.c_int32, ctypes.c_int32, vp, vp, vp]),
+        "ora_decode_row_q": (None, [ctypes.c_int, ctypes.c_int32, ctypes.c_int32, vp, vp, vp]),
+        "ora_scale_offsets": (None, [ctypes.c_int32, vp, ctypes.c_uint64, ctypes.c_uint64, vp]),
         "ora_pack": (ctypes.c_int, [cfgp, vp, vp, vp, vp, ctypes.c_uint64]),
         "ora_check_header": (ctypes.c_int, [cfgp, vp, ctypes.c_uint64]),
         "ora_geometry": (ctypes.c_int, [cfgp, vp]),
@@ -111,9 +117,9 @@ def _u16(a):
 
 
 def config(num_layers, num_kv_heads, head_dim, num_tokens, budget, first_ratio=0.02, num_sink=-1,
-           decay=0.005, num_tiers=3, score_mode=KVNORM, num_q_heads=0, obs_window=0):
+           decay=0.005, num_tiers=3, score_mode=KVNORM, num_q_heads=0, obs_window=0, quant_int8=0, quant_int4=0):
     return Config(num_layers, num_kv_heads, head_dim, num_tokens, budget, first_ratio, num_sink,
-                  decay, num_tiers, score_mode, num_q_heads, obs_window)
+                  decay, num_tiers, score_mode, num_q_heads, obs_window, quant_int8, quant_int4)
 
 
 def validate(cfg):
@@ -193,6 +199,44 @@ def encode_row(tier, row):
     return out[:width], np.float32(sc.value), bool(bad)
 
 
+def meta_bytes(q, d):
+    """Metadata bytes of one quantized row under variant descriptor q."""
+    g = d if q & 3 == 0 else (64 if q & 3 == 1 else 32)
+    g = min(g, d)
+    return (d // g) * (2 if q & QUANT_ASYM else 1) * (2 if q & QUANT_FP16 else 4)
+
+
+def encode_row_q(tier, q, row):
+    """Returns (payload bytes of the row, its metadata bytes, non-finite flag)."""
+    row = _u16(row)
+    d = row.shape[0]
+    width = {FP16: 2 * d, INT8: d, INT4: d // 2, DROP: 0}[int(tier)]
+    out = np.zeros(max(width, 1), np.uint8)
+    mb = meta_bytes(q, d) if int(tier) in (INT8, INT4) else 0
+    meta = np.zeros(max(mb, 1), np.uint8)
+    bad = _lib.ora_encode_row_q(int(tier), q, d, _ptr(row), _ptr(out), _ptr(meta))
+    return out[:width], meta[:mb], bool(bad)
+
+
+def decode_row_q(tier, q, d, data, meta):
+    data = np.ascontiguousarray(data, np.uint8)
+    meta = np.ascontiguousarray(meta, np.uint8)
+    if data.size == 0:
+        data = np.zeros(1, np.uint8)
+    if meta.size == 0:
+        meta = np.zeros(1, np.uint8)
+    out = np.empty(d, np.uint16)
+    _lib.ora_decode_row_q(int(tier), q, d, _ptr(data), _ptr(meta), _ptr(out))
+    return out
+
+
+def scale_offsets(tier, e8, e4):
+    tier = np.ascontiguousarray(tier, np.uint8)
+    out = np.empty(tier.size, np.uint32)
+    _lib.ora_scale_offsets(tier.size, _ptr(tier), e8, e4, _ptr(out))
+    return out
+
+
 def decode_row(tier, d, data, scale):
     data = np.ascontiguousarray(data, np.uint8)
     if data.size == 0:
@@ -214,7 +258,7 @@ def pack(cfg, k, v, tier):
 
 
 GEOMETRY_FIELDS = ("tiermap_off", "chunkidx_off", "layers_off", "seg_bytes", "seg_stride",
-                   "scales_bytes", "layer_stride", "total", "nq")
+                   "scales_bytes", "layer_stride", "total", "nq", "seg_scale_bytes")
 
 
 def geometry(cfg):

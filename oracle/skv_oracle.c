@@ -60,6 +60,8 @@ typedef struct {
   int32_t score_mode;   /* 0 kv-norm, 1 attention, 2 recency */
   int32_t num_q_heads;  /* attention mode */
   int32_t obs_window;   /* attention mode */
+  int32_t quant_int8;   /* quantizer variant of the INT8 tier (0: row-wise symmetric, fp32 scale) */
+  int32_t quant_int4;   /* quantizer variant of the INT4 tier */
 } ora_config;
 
 typedef struct {
@@ -118,6 +120,35 @@ uint16_t ora_float_to_half(float f) {
 static float half_to_float(uint16_t h) { return (float)ora_half_to_double(h); }
 
 /* ------------------------------------------------------------------------ */
+/* Quantizer variants within a tier.  The paper leaves the quantizer of each  */
+/* tier open (Sec. 6.10 and Sec. 8: any per-tier scheme applies within a tier, */
+/* e.g. KIVI-style asymmetric quantization; Sec. 10 on KIVI and KVQuant).  A   */
+/* variant descriptor selects, per quantized tier:                             */
+/*   bits 0-1  elements per scale group: 0 the whole row (d), 1 64, 2 32       */
+/*             (capped at d);                                                  */
+/*   bit 2     asymmetric: per group minimum lo and scale (max - min)/M, codes */
+/*             0..M (M = 255 or 15), instead of symmetric absmax codes -Q..Q;  */
+/*   bit 3     group scale (and minimum) stored as binary16 instead of fp32.   */
+/* Descriptor 0 is the row-wise symmetric quantizer with fp32 scales used      */
+/* everywhere else in this file.                                               */
+/* ------------------------------------------------------------------------ */
+
+enum { QV_ASYM = 4, QV_FP16 = 8 };
+
+static int qv_valid(int32_t q) { return (q & ~15) == 0 && (q & 3) != 3; }
+
+static int32_t qv_group(int32_t q, int32_t d) {
+  int32_t g = (q & 3) == 0 ? d : (q & 3) == 1 ? 64 : 32;
+  return g < d ? g : d;
+}
+
+/* Metadata bytes of one quantized row under descriptor q. */
+static uint64_t qv_entry_bytes(int32_t q, int32_t d) {
+  uint64_t groups = (uint64_t)(d / qv_group(q, d));
+  return groups * ((q & QV_ASYM) ? 2u : 1u) * ((q & QV_FP16) ? 2u : 4u);
+}
+
+/* ------------------------------------------------------------------------ */
 /* Validation and plan (Sec. 2.1 eq. "budget"; Sec. 4.4).                      */
 /* ------------------------------------------------------------------------ */
 
@@ -136,6 +167,7 @@ int ora_validate(const ora_config* c) {
   if (2.0 * (double)c->decay * (double)(c->num_tokens - 1) > 700.0) return ORA_ERR_INVALID_ARG;
   if (c->num_tiers != 2 && c->num_tiers != 3) return ORA_ERR_INVALID_ARG;
   if (c->score_mode < MODE_KVNORM || c->score_mode > MODE_RECENCY) return ORA_ERR_INVALID_ARG;
+  if (!qv_valid(c->quant_int8) || !qv_valid(c->quant_int4)) return ORA_ERR_INVALID_ARG;
   if (c->score_mode == MODE_ATTN) {
     if (c->num_q_heads < 1 || c->num_q_heads % c->num_kv_heads != 0) return ORA_ERR_INVALID_ARG;
     if (c->obs_window < 1) return ORA_ERR_INVALID_ARG;
@@ -190,19 +222,26 @@ typedef struct {
   uint64_t tiermap_off, chunkidx_off, layers_off;
   uint64_t seg_bytes, seg_stride, scales_bytes, layer_stride, total;
   int64_t nq, nchunks;
+  uint64_t e8, e4;          /* metadata bytes of an INT8 / INT4 row */
+  uint64_t seg_scale_bytes; /* metadata bytes of one segment: n8 e8 + n4 e4 */
+  uint64_t cidx_entry;      /* chunk-index entry bytes: 8 (both descriptors 0) or 16 */
 } ora_geom;
 
 static void geometry(const ora_config* c, const ora_plan_t* p, ora_geom* g) {
   uint64_t n = (uint64_t)c->num_tokens, d = (uint64_t)c->head_dim, H = (uint64_t)c->num_kv_heads;
   g->nq = p->n_int8 + p->n_int4;
   g->nchunks = (int64_t)((n + ORA_CHUNK - 1) / ORA_CHUNK);
+  g->e8 = qv_entry_bytes(c->quant_int8, (int32_t)d);
+  g->e4 = qv_entry_bytes(c->quant_int4, (int32_t)d);
+  g->seg_scale_bytes = (uint64_t)p->n_int8 * g->e8 + (uint64_t)p->n_int4 * g->e4;
+  g->cidx_entry = (c->quant_int8 || c->quant_int4) ? 16u : 8u;
   g->tiermap_off = 256;
   g->chunkidx_off = g->tiermap_off + up256((n + 3) / 4);
-  g->layers_off = g->chunkidx_off + up256((uint64_t)g->nchunks * 8u);
+  g->layers_off = g->chunkidx_off + up256((uint64_t)g->nchunks * g->cidx_entry);
   g->seg_bytes = (uint64_t)(p->n_sink + p->n_fp16) * 2 * d + (uint64_t)p->n_int8 * d +
                  (uint64_t)p->n_int4 * (d / 2);
   g->seg_stride = up256(g->seg_bytes);
-  g->scales_bytes = up256(2 * H * (uint64_t)g->nq * 4);
+  g->scales_bytes = up256(2 * H * g->seg_scale_bytes);
   g->layer_stride = g->scales_bytes + 2 * H * g->seg_stride;
   g->total = g->layers_off + (uint64_t)c->num_layers * g->layer_stride;
 }
@@ -386,6 +425,17 @@ void ora_offsets(int32_t n, const uint8_t* tier, uint32_t* units, uint32_t* qran
   }
 }
 
+/* sbytes[t] = metadata bytes of the quantized rows before t (e8 per INT8
+ * row, e4 per INT4 row): where row t's scales start inside its segment's
+ * metadata. */
+void ora_scale_offsets(int32_t n, const uint8_t* tier, uint64_t e8, uint64_t e4, uint32_t* sbytes) {
+  uint64_t b = 0;
+  for (int32_t t = 0; t < n; ++t) {
+    sbytes[t] = (uint32_t)b;
+    b += tier[t] == T_INT8 ? e8 : tier[t] == T_INT4 ? e4 : 0;
+  }
+}
+
 /* Symmetric per-row absmax quantizer ("standard symmetric", Sec. 8).  Writes
  * the row's payload bytes to out and its scale to *scale; returns 1 if the
  * row holds a non-finite element (scale NaN, codes zero), else 0. */
@@ -457,6 +507,167 @@ void ora_decode_row(int tr, int32_t d, const uint8_t* in, float scale, uint16_t*
   }
 }
 
+static void put32(uint8_t* p, uint32_t v);
+static uint32_t get32(const uint8_t* p);
+static uint32_t fbits(float f);
+
+/* Order key of a binary16 pattern that sorts finite values numerically with
+ * -0 below +0 (IEEE totalOrder restricted to finite values). */
+static uint32_t order_key(uint16_t h) { return (h & 0x8000u) ? (uint32_t)(~h & 0xFFFFu) : (uint32_t)(h | 0x8000u); }
+
+static void put16(uint8_t* p, uint16_t v) { memcpy(p, &v, 2); }
+static uint16_t get16(const uint8_t* p) { uint16_t v; memcpy(&v, p, 2); return v; }
+
+/* Row quantizer under variant descriptor q (see the variant section above).
+ * Per group of gs elements:
+ *   symmetric: a = max |x|; a non-finite element gives a NaN scale and zero
+ *     codes, a = 0 a zero scale and zero codes; otherwise with an fp32 scale
+ *     s = RN32(a/Q), r = RN32(Q/a), and with a binary16 scale s = RN16(RN32(a/Q))
+ *     (zero codes if that underflows to 0), r = RN32(1/s);
+ *     code = clamp(rne(RN32(x r)), -Q, Q).
+ *   asymmetric: lo = min x, hi = max x (-0 below +0); non-finite gives NaN
+ *     scale and minimum and zero codes; range = RN32(hi - lo); range = 0 gives
+ *     a zero scale and zero codes; otherwise s = RN32(range/M) (binary16: RN16
+ *     of that, zero codes on underflow), r = RN32(M/range) (binary16:
+ *     RN32(1/s)); code = clamp(rne(RN32(RN32(x - lo) r)), 0, M).
+ * Codes are stored as for descriptor 0 (signed byte / nibble), asymmetric codes
+ * as unsigned byte / nibble.  Metadata per group: s, then lo if asymmetric,
+ * each fp32 or binary16.  Returns 1 if a group held a non-finite element.
+ * Descriptor 0 is ora_encode_row with its fp32 scale in the metadata. */
+int ora_encode_row_q(int tr, int32_t q, int32_t d, const uint16_t* x, uint8_t* out, uint8_t* meta) {
+  if (tr == T_FP16 || tr == T_DROP || q == 0) {
+    float scale = 0.0f;
+    int bad = ora_encode_row(tr, d, x, out, &scale);
+    if (tr == T_INT8 || tr == T_INT4) put32(meta, fbits(scale));
+    return bad;
+  }
+  const int asym = (q & QV_ASYM) != 0, f16 = (q & QV_FP16) != 0;
+  const int32_t gs = qv_group(q, d);
+  const int Q = tr == T_INT8 ? 127 : 7, M = tr == T_INT8 ? 255 : 15;
+  const uint64_t eb = f16 ? 2u : 4u;
+  int32_t codes[256];
+  int bad_any = 0;
+  for (int32_t g0 = 0; g0 < d; g0 += gs) {
+    uint8_t* m = meta + (uint64_t)(g0 / gs) * (asym ? 2u : 1u) * eb;
+    int bad = 0;
+    uint16_t amax = 0, lo = x[g0], hi = x[g0];
+    for (int32_t i = g0; i < g0 + gs; ++i) {
+      if ((x[i] & 0x7C00u) == 0x7C00u) bad = 1;
+      if ((x[i] & 0x7FFFu) > amax) amax = x[i] & 0x7FFFu;
+      if (order_key(x[i]) < order_key(lo)) lo = x[i];
+      if (order_key(x[i]) > order_key(hi)) hi = x[i];
+    }
+    float scale = 0.0f, r = 0.0f, lof = 0.0f;
+    uint16_t s16 = 0;
+    int zero = 0;
+    if (bad) {
+      uint32_t nanbits = 0x7FC00000u;
+      memcpy(&scale, &nanbits, 4);
+      memcpy(&lof, &nanbits, 4);
+      s16 = 0x7E00;
+      zero = 1;
+      bad_any = 1;
+    } else if (!asym) {
+      if (amax == 0) {
+        zero = 1;
+      } else {
+        float a = half_to_float(amax);
+        scale = a / (float)Q;
+        if (f16) {
+          s16 = ora_float_to_half(scale);
+          scale = half_to_float(s16);
+          if (s16 == 0) zero = 1;
+          else r = 1.0f / scale;
+        } else {
+          r = (float)Q / a;
+        }
+      }
+    } else {
+      lof = half_to_float(lo);
+      float range = half_to_float(hi) - lof;
+      if (range == 0.0f) {
+        zero = 1;
+      } else {
+        scale = range / (float)M;
+        if (f16) {
+          s16 = ora_float_to_half(scale);
+          scale = half_to_float(s16);
+          if (s16 == 0) zero = 1;
+          else r = 1.0f / scale;
+        } else {
+          r = (float)M / range;
+        }
+      }
+    }
+    for (int32_t i = g0; i < g0 + gs; ++i) {
+      if (zero) { codes[i] = 0; continue; }
+      float c;
+      if (!asym) {
+        c = nearbyintf(half_to_float(x[i]) * r);
+        if (c > (float)Q) c = (float)Q;
+        if (c < (float)-Q) c = (float)-Q;
+      } else {
+        float dlt = half_to_float(x[i]) - lof;
+        c = nearbyintf(dlt * r);
+        if (c > (float)M) c = (float)M;
+        if (c < 0.0f) c = 0.0f;
+      }
+      codes[i] = (int32_t)c;
+    }
+    if (f16) {
+      put16(m, bad ? (uint16_t)0x7E00 : s16);
+      if (asym) put16(m + 2, bad ? (uint16_t)0x7E00 : lo);
+    } else {
+      put32(m, fbits(scale));
+      if (asym) put32(m + 4, fbits(lof));
+    }
+  }
+  if (tr == T_INT8) {
+    for (int32_t i = 0; i < d; ++i) out[i] = (uint8_t)(codes[i] & 0xFF);
+  } else {
+    for (int32_t i = 0; i < d / 2; ++i)
+      out[i] = (uint8_t)((codes[2 * i] & 0xF) | ((codes[2 * i + 1] & 0xF) << 4));
+  }
+  return bad_any;
+}
+
+/* Inverse of ora_encode_row_q: per group, a NaN scale gives 0x7E00;
+ * symmetric x^ = RN16(RN32(code s)); asymmetric x^ = RN16(RN32(RN32(code s) + lo)). */
+void ora_decode_row_q(int tr, int32_t q, int32_t d, const uint8_t* in, const uint8_t* meta, uint16_t* y) {
+  if (tr == T_FP16 || tr == T_DROP || q == 0) {
+    float scale = 0.0f;
+    if (tr == T_INT8 || tr == T_INT4) {
+      uint32_t b = get32(meta);
+      memcpy(&scale, &b, 4);
+    }
+    ora_decode_row(tr, d, in, scale, y);
+    return;
+  }
+  const int asym = (q & QV_ASYM) != 0, f16 = (q & QV_FP16) != 0;
+  const int32_t gs = qv_group(q, d);
+  const uint64_t eb = f16 ? 2u : 4u;
+  for (int32_t g0 = 0; g0 < d; g0 += gs) {
+    const uint8_t* m = meta + (uint64_t)(g0 / gs) * (asym ? 2u : 1u) * eb;
+    float scale, lo = 0.0f;
+    if (f16) {
+      scale = half_to_float(get16(m));
+      if (asym) lo = half_to_float(get16(m + 2));
+    } else {
+      uint32_t b = get32(m);
+      memcpy(&scale, &b, 4);
+      if (asym) { b = get32(m + 4); memcpy(&lo, &b, 4); }
+    }
+    for (int32_t i = g0; i < g0 + gs; ++i) {
+      if (isnan(scale)) { y[i] = 0x7E00; continue; }
+      int32_t nib = tr == T_INT8 ? in[i] : (in[i / 2] >> (4 * (i & 1))) & 0xF;
+      int32_t code = asym ? nib : tr == T_INT8 ? (int32_t)(int8_t)in[i] : (nib >= 8 ? nib - 16 : nib);
+      float v = (float)code * scale;
+      if (asym) v = v + lo;
+      y[i] = ora_float_to_half(v);
+    }
+  }
+}
+
 /* ------------------------------------------------------------------------ */
 /* Payload writer (Algorithm 1 step 4) and reader (decode side, Sec. 4.2).     */
 /* ------------------------------------------------------------------------ */
@@ -497,33 +708,38 @@ static void write_header(const ora_config* c, const ora_plan_t* p, const ora_geo
   put32(h + 144, 0);             /* non-finite quantized rows */
   put32(h + 148, 0);             /* status */
   put32(h + 152, ORA_CHUNK);
+  put32(h + 156, (uint32_t)c->quant_int8);
+  put32(h + 160, (uint32_t)c->quant_int4);
 }
 
 /* Header, 2-bit tier map and chunk index (the payload bytes before layer 0);
  * also returns the per-token row offsets and scale ranks. */
 static void write_meta(const ora_config* c, const ora_plan_t* p, const ora_geom* g, const uint8_t* tier,
-                       uint32_t* units, uint32_t* qrank, uint8_t* payload) {
+                       uint32_t* units, uint32_t* qrank, uint32_t* sbytes, uint8_t* payload) {
   int64_t n = c->num_tokens;
   write_header(c, p, g, payload);
   for (int64_t t = 0; t < n; ++t)
     payload[g->tiermap_off + (uint64_t)t / 4] |= (uint8_t)(tier[t] << (2 * (t % 4)));
   ora_offsets((int32_t)n, tier, units, qrank);
+  ora_scale_offsets((int32_t)n, tier, g->e8, g->e4, sbytes);
   for (int64_t ch = 0; ch < g->nchunks; ++ch) {
-    put32(payload + g->chunkidx_off + 8 * ch, units[ch * ORA_CHUNK]);
-    put32(payload + g->chunkidx_off + 8 * ch + 4, qrank[ch * ORA_CHUNK]);
+    uint8_t* e = payload + g->chunkidx_off + g->cidx_entry * (uint64_t)ch;
+    put32(e, units[ch * ORA_CHUNK]);
+    put32(e + 4, qrank[ch * ORA_CHUNK]);
+    if (g->cidx_entry == 16) put32(e + 8, sbytes[ch * ORA_CHUNK]); /* metadata bytes before the chunk */
   }
 }
 
 /* Payload geometry: out = {tiermap_off, chunkidx_off, layers_off, seg_bytes,
- * seg_stride, scales_bytes, layer_stride, total, nq}. */
+ * seg_stride, scales_bytes, layer_stride, total, nq, seg_scale_bytes}. */
 int ora_geometry(const ora_config* c, uint64_t* out) {
   ora_plan_t p;
   int st = ora_plan(c, &p);
   if (st) return st;
   ora_geom g;
   geometry(c, &p, &g);
-  uint64_t v[9] = {g.tiermap_off, g.chunkidx_off, g.layers_off, g.seg_bytes, g.seg_stride,
-                   g.scales_bytes, g.layer_stride, g.total, (uint64_t)g.nq};
+  uint64_t v[10] = {g.tiermap_off, g.chunkidx_off, g.layers_off, g.seg_bytes, g.seg_stride,
+                    g.scales_bytes, g.layer_stride, g.total, (uint64_t)g.nq, g.seg_scale_bytes};
   memcpy(out, v, sizeof(v));
   return ORA_OK;
 }
@@ -540,10 +756,12 @@ int ora_pack_meta(const ora_config* c, const uint8_t* tier, uint8_t* out, uint64
   int64_t n = c->num_tokens;
   uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
+  uint32_t* sbytes = (uint32_t*)malloc((size_t)n * 4);
   memset(out, 0, g.layers_off);
-  write_meta(c, &p, &g, tier, units, qrank, out);
+  write_meta(c, &p, &g, tier, units, qrank, sbytes, out);
   free(units);
   free(qrank);
+  free(sbytes);
   return ORA_OK;
 }
 
@@ -569,7 +787,8 @@ int ora_pack(const ora_config* c, const uint16_t* k, const uint16_t* v, const ui
   memset(payload, 0, g.total);
   uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
-  write_meta(c, &p, &g, tier, units, qrank, payload);
+  uint32_t* sbytes = (uint32_t*)malloc((size_t)n * 4);
+  write_meta(c, &p, &g, tier, units, qrank, sbytes, payload);
   uint32_t nonfinite = 0;
   uint64_t rowunit = (uint64_t)d / 2;
   for (int64_t l = 0; l < L; ++l) {
@@ -578,20 +797,18 @@ int ora_pack(const ora_config* c, const uint16_t* k, const uint16_t* v, const ui
       for (int64_t h = 0; h < H; ++h) {
         const uint16_t* src = (kv == 0 ? k : v) + ((l * H + h) * n) * d;
         uint8_t* seg = lb + g.scales_bytes + (uint64_t)(kv * H + h) * g.seg_stride;
-        uint8_t* sc = lb + (uint64_t)(kv * H + h) * (uint64_t)g.nq * 4;
+        uint8_t* sc = lb + (uint64_t)(kv * H + h) * g.seg_scale_bytes;
         for (int64_t t = 0; t < n; ++t) {
-          float scale = 0.0f;
-          int bad = ora_encode_row(tier[t], (int32_t)d, src + t * d, seg + units[t] * rowunit, &scale);
-          if (tier[t] == T_INT8 || tier[t] == T_INT4) {
-            put32(sc + 4 * (uint64_t)qrank[t], fbits(scale));
-            nonfinite += (uint32_t)bad;
-          }
+          int32_t q = tier[t] == T_INT8 ? c->quant_int8 : c->quant_int4;
+          int bad = ora_encode_row_q(tier[t], q, (int32_t)d, src + t * d, seg + units[t] * rowunit, sc + sbytes[t]);
+          if (tier[t] == T_INT8 || tier[t] == T_INT4) nonfinite += (uint32_t)bad;
         }
       }
   }
   put32(payload + 144, nonfinite);
   free(units);
   free(qrank);
+  free(sbytes);
   return ORA_OK;
 }
 
@@ -631,16 +848,20 @@ int ora_unpack(const ora_config* c, const uint8_t* payload, uint64_t bytes, uint
   }
   uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
+  uint32_t* sbytes = (uint32_t*)malloc((size_t)n * 4);
   ora_offsets((int32_t)n, tier, units, qrank);
+  ora_scale_offsets((int32_t)n, tier, g.e8, g.e4, sbytes);
   int bad = cnt[T_FP16] != p.n_sink + p.n_fp16 || cnt[T_INT8] != p.n_int8 ||
             cnt[T_INT4] != p.n_int4 || cnt[T_DROP] != p.n_drop;
-  for (int64_t ch = 0; ch < g.nchunks && !bad; ++ch)
-    bad = get32(payload + g.chunkidx_off + 8 * ch) != units[ch * ORA_CHUNK] ||
-          get32(payload + g.chunkidx_off + 8 * ch + 4) != qrank[ch * ORA_CHUNK];
+  for (int64_t ch = 0; ch < g.nchunks && !bad; ++ch) {
+    const uint8_t* e = payload + g.chunkidx_off + g.cidx_entry * (uint64_t)ch;
+    bad = get32(e) != units[ch * ORA_CHUNK] || get32(e + 4) != qrank[ch * ORA_CHUNK];
+    if (!bad && g.cidx_entry == 16) bad = get32(e + 8) != sbytes[ch * ORA_CHUNK] || get32(e + 12) != 0;
+  }
   for (int64_t t = 0; t < (n + block_size - 1) / block_size && !bad; ++t)
     bad = block_table[t] < 0 || block_table[t] >= num_blocks;
   if (bad) {
-    free(tier); free(units); free(qrank);
+    free(tier); free(units); free(qrank); free(sbytes);
     return ORA_ERR_FORMAT;
   }
   uint64_t rowunit = (uint64_t)d / 2;
@@ -649,21 +870,17 @@ int ora_unpack(const ora_config* c, const uint8_t* payload, uint64_t bytes, uint
     for (int kv = 0; kv < 2; ++kv)
       for (int64_t h = 0; h < H; ++h) {
         const uint8_t* seg = lb + g.scales_bytes + (uint64_t)(kv * H + h) * g.seg_stride;
-        const uint8_t* sc = lb + (uint64_t)(kv * H + h) * (uint64_t)g.nq * 4;
+        const uint8_t* sc = lb + (uint64_t)(kv * H + h) * g.seg_scale_bytes;
         uint16_t* cache = kv == 0 ? kc : vc;
         for (int64_t t = 0; t < n; ++t) {
-          float scale = 0.0f;
-          if (tier[t] == T_INT8 || tier[t] == T_INT4) {
-            uint32_t b = get32(sc + 4 * (uint64_t)qrank[t]);
-            memcpy(&scale, &b, 4);
-          }
+          int32_t q = tier[t] == T_INT8 ? c->quant_int8 : c->quant_int4;
           int64_t blk = block_table[t / block_size], slot = t % block_size;
           uint16_t* dst = cache + (((l * num_blocks + blk) * block_size + slot) * H + h) * d;
-          ora_decode_row(tier[t], (int32_t)d, seg + units[t] * rowunit, scale, dst);
+          ora_decode_row_q(tier[t], q, (int32_t)d, seg + units[t] * rowunit, sc + sbytes[t], dst);
         }
       }
   }
-  free(tier); free(units); free(qrank);
+  free(tier); free(units); free(qrank); free(sbytes);
   return ORA_OK;
 }
 
@@ -694,6 +911,7 @@ typedef struct {
 static int upg_geometry(const ora_config* c, int32_t m, int32_t mode, ora_upg_geom* g) {
   int st = ora_validate(c);
   if (st) return st;
+  if (c->quant_int8 || c->quant_int4) return ORA_ERR_INVALID_ARG; /* held rows use descriptor 0 */
   if (m < 1 || m > c->num_tokens || (mode != 0 && mode != 1)) return ORA_ERR_INVALID_ARG;
   uint64_t L = (uint64_t)c->num_layers, H = (uint64_t)c->num_kv_heads, d = (uint64_t)c->head_dim;
   g->tokens_off = 256;
@@ -908,6 +1126,7 @@ static int64_t group_of(const ora_config* c, int32_t gran, int64_t l, int64_t h)
 static int plan_groups(const ora_config* c, int32_t gran, const float* budgets, ora_plan_t* plans) {
   int st = ora_validate(c);
   if (st) return st;
+  if (c->quant_int8 || c->quant_int4) return ORA_ERR_INVALID_ARG; /* grouped payloads use descriptor 0 */
   int32_t G = ora_group_count(c, gran);
   if (G < 1) return ORA_ERR_INVALID_ARG;
   for (int32_t g = 0; g < G; ++g) {
