@@ -353,6 +353,57 @@ def run_groups(args, w):
     return out
 
 
+def run_quant(args, w):
+    """Per-tier quantizer variants (NEXT-4) on the workload's request: pack
+    and unpack times and payload/metadata sizes for a few descriptor pairs
+    (INT8 tier, INT4 tier).  Returns a JSON-able dict."""
+    import torch
+
+    from paper_2606_08635_amd import skv, workloads
+
+    L, H, d, n, bs = w.layers, w.kv_heads, w.head_dim, w.tokens, 16
+    k, v = workloads.make_kv(L, H, n, d, seed=0, outliers=w.outliers, device="cuda")
+    nb = workloads.blocks_for(n, bs)
+    bt = workloads.make_block_table(n, bs, nb, seed=0, device="cuda")
+    kc = torch.empty(L, nb, bs, H, d, dtype=torch.float16, device="cuda")
+    vc = torch.empty_like(kc)
+    variants = {
+        "row_sym_fp32": (0, 0),
+        "row_sym_fp16": (skv.QUANT_FP16, skv.QUANT_FP16),
+        "g32_sym_fp16": (skv.QUANT_GROUP32 | skv.QUANT_FP16, skv.QUANT_GROUP32 | skv.QUANT_FP16),
+        "int4_g32_asym_fp16": (0, skv.QUANT_GROUP32 | skv.QUANT_ASYM | skv.QUANT_FP16),
+        "g64_asym_fp32": (skv.QUANT_GROUP64 | skv.QUANT_ASYM, skv.QUANT_GROUP64 | skv.QUANT_ASYM),
+    }
+    out = {"workload": w.name}
+    for name, (q8, q4) in variants.items():
+        cfg = skv.config(L, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers,
+                         quant_int8=q8, quant_int4=q4)
+        codec = skv.Codec(cfg)
+        codec.encode(k, v)
+        for _ in range(args.warmup):
+            skv.pack(cfg, k, v, codec.tier, codec.payload, codec.status[0:1])
+            skv.unpack(cfg, codec.payload, kc, vc, bt, bs, codec.status[1:2])
+        evs = [_events(3) for _ in range(args.steps)]
+        for e in evs:
+            e[0].record()
+            skv.pack(cfg, k, v, codec.tier, codec.payload, codec.status[0:1])
+            e[1].record()
+            skv.unpack(cfg, codec.payload, kc, vc, bt, bs, codec.status[1:2])
+            e[2].record()
+        torch.cuda.synchronize()
+        if codec.status.cpu().tolist() != [0, 0]:
+            raise RuntimeError(f"codec reported status {codec.status.cpu().tolist()}")
+        tp = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
+        tu = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
+        geo = codec.payload[:256].cpu().numpy().view("<u8")
+        out[name] = {"quant_int8": q8, "quant_int4": q4, "payload_bytes": codec.payload_bytes,
+                     "metadata_bytes_per_layer": int(geo[15]), "pack_ms": round(tp, 4), "unpack_ms": round(tu, 4),
+                     "fp16eq_gbps": round(w.fp16_bytes / ((tp + tu) / 1e3) / 1e9, 2)}
+        del codec
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -364,11 +415,11 @@ def main():
     ap.add_argument("--score", choices=["kvnorm", "attn"], default="kvnorm",
                     help="importance statistic; attn uses a W-query observation window per query head")
     ap.add_argument("--obs-window", type=int, default=32)
-    ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade", "groups"], default="step",
+    ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade", "groups", "quant"], default="step",
                     help="step: the headline codec step; batch: per-request vs batched launches over "
                          "a multi-request workload; pipeline: layer-pipelined handoff latency; "
                          "upgrade: cold-tier precision upgrade after the step; "
-                         "groups: per-layer and per-head tier maps")
+                         "groups: per-layer and per-head tier maps; quant: per-tier quantizer variants")
     ap.add_argument("--group-layers", type=int, default=4, help="layers per pipeline stage (--mode pipeline)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer with skv_link (reference for byte counters)")
@@ -407,6 +458,9 @@ def main():
         return
     if args.mode == "groups":
         print(json.dumps({"mode": "groups", **run_groups(args, w)}), flush=True)
+        return
+    if args.mode == "quant":
+        print(json.dumps({"mode": "quant", **run_quant(args, w)}), flush=True)
         return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)

@@ -65,7 +65,7 @@
 extern "C" {
 #endif
 
-#define SKV_ABI_VERSION 1
+#define SKV_ABI_VERSION 2
 
 typedef enum skv_status {
   SKV_OK = 0,
@@ -110,7 +110,33 @@ typedef struct skv_config {
   int32_t score_mode;   /* SKV_SCORE_*                                            */
   int32_t num_q_heads;  /* attention mode: query heads Hq (grouped, Hq/H per KV)  */
   int32_t obs_window;   /* attention mode: W observation queries per query head  */
+  int32_t quant_int8;   /* quantizer variant of the INT8 tier (SKV_QUANT_*; 0 =
+                           row-wise symmetric absmax with an fp32 scale)         */
+  int32_t quant_int4;   /* quantizer variant of the INT4 tier                    */
 } skv_config;
+
+/* Quantizer variant descriptor bits (the quantizer inside a tier is a free
+ * choice: Sec. 6.10, Sec. 8; KIVI-style asymmetric, Sec. 8 and Sec. 10).
+ * Bits 0-1: elements per scale group, 0 = the whole row (d), SKV_QUANT_GROUP64,
+ * SKV_QUANT_GROUP32 (capped at d); SKV_QUANT_ASYM: asymmetric codes 0..M
+ * (M = 255 / 15) with the group minimum lo as zero point, x^ = code s + lo;
+ * SKV_QUANT_FP16: s (and lo) stored as binary16.  Per group, symmetric:
+ * s = RN32(a/Q), r = RN32(Q/a), a = max |x|; binary16: s = RN16(RN32(a/Q)),
+ * r = RN32(1/s); code = clamp(rne(RN32(x r)), -Q, Q).  Asymmetric: lo, hi the
+ * minimum and maximum (-0 below +0), range = RN32(hi - lo), s = RN32(range/M),
+ * r = RN32(M/range) (binary16: s = RN16(RN32(range/M)), r = RN32(1/s)),
+ * code = clamp(rne(RN32(RN32(x - lo) r)), 0, M); decode RN16(RN32(RN32(code s)
+ * + lo)).  A group with an inf/NaN gets NaN metadata and decodes to 0x7E00; a
+ * zero a or range, or a binary16 s that underflows, gives zero codes.  With
+ * any nonzero descriptor the payload stores per quantized row its groups'
+ * metadata (s, then lo if asymmetric; fp32 or binary16) in token order, and
+ * chunk-index entries are 16 bytes: {units, quantized rows, metadata bytes
+ * before the chunk, 0}; header words 39 and 40 hold the two descriptors.
+ * The cold-tier upgrade and the grouped calls require both descriptors 0. */
+#define SKV_QUANT_GROUP64 1
+#define SKV_QUANT_GROUP32 2
+#define SKV_QUANT_ASYM 4
+#define SKV_QUANT_FP16 8
 
 /* Tier counts of a configuration.  n_fp16/n_int8/n_int4/n_drop count the
  * non-sink tokens; the n_sink sink tokens are FP16 as well.  Budget in

@@ -12,6 +12,7 @@
 #include "device_util.h"
 #include "row_codec.h"
 #include "row_stream.h"
+#include "row_variants.h"
 #include "skv_internal.h"
 #include "tier_groups.h"
 
@@ -32,15 +33,18 @@ constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
 // grid: one workgroup per request
 __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
   __shared__ uint32_t s_chunk[kMaxChunks];  // per chunk: units | quant << 16
+  __shared__ uint32_t s_meta[kMaxChunks];   // per chunk: metadata bytes (variant descriptors)
   __shared__ uint32_t s_cnt[4];
   __shared__ uint32_t s_bad;
   __shared__ uint64_t s_scan[16];
+  __shared__ uint64_t s_scan2[16];
   const ReqDesc& r = a.r[blockIdx.x];
   const uint8_t* __restrict__ tier = r.tier;
   uint8_t* __restrict__ payload = r.payload;
   const int n = r.n, nchunks = r.nchunks;
   const int tid = threadIdx.x;
   const int ngroups = (n + kGroupTokens - 1) / kGroupTokens;
+  const bool variant = (a.q8 | a.q4) != 0;  // launch-uniform
   if (tid < 4) s_cnt[tid] = 0;
   if (tid == 0) s_bad = 0;
   __syncthreads();
@@ -55,7 +59,11 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
     for (int i = 0; i < 4; ++i) cnt[i] += gi.count(i);
     bad |= gi.bad;
     const uint32_t u = sum16(gi.units), q = sum16(gi.quant);
-    if ((tid % kGroupsPerChunk) == 0 && g < ngroups) s_chunk[g / kGroupsPerChunk] = u | (q << 16);
+    const uint32_t m = sum16(gi.count(kINT8) * a.e8 + gi.count(kINT4) * a.e4);
+    if ((tid % kGroupsPerChunk) == 0 && g < ngroups) {
+      s_chunk[g / kGroupsPerChunk] = u | (q << 16);
+      s_meta[g / kGroupsPerChunk] = m;
+    }
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -81,13 +89,29 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
   const uint64_t ex = block_exclusive_scan_1024(run, s_scan);
   uint32_t ru = static_cast<uint32_t>(ex), rq = static_cast<uint32_t>(ex >> 32);
   uint32_t* cidx = reinterpret_cast<uint32_t*>(payload + r.chunkidx_off);
-  for (int c = c0; c < c1; ++c) {
-    cidx[2 * c] = ru;
-    cidx[2 * c + 1] = rq;
-    ru += s_chunk[c] & 0xFFFFu;
-    rq += s_chunk[c] >> 16;
+  if (!variant) {
+    for (int c = c0; c < c1; ++c) {
+      cidx[2 * c] = ru;
+      cidx[2 * c + 1] = rq;
+      ru += s_chunk[c] & 0xFFFFu;
+      rq += s_chunk[c] >> 16;
+    }
+  } else {  // 16-byte entries {units, quantized rows, metadata bytes, 0}
+    uint64_t mrun = 0;
+    for (int c = c0; c < c1; ++c) mrun += s_meta[c];
+    uint32_t rm = static_cast<uint32_t>(block_exclusive_scan_1024(mrun, s_scan2));
+    for (int c = c0; c < c1; ++c) {
+      cidx[4 * c] = ru;
+      cidx[4 * c + 1] = rq;
+      cidx[4 * c + 2] = rm;
+      cidx[4 * c + 3] = 0u;
+      ru += s_chunk[c] & 0xFFFFu;
+      rq += s_chunk[c] >> 16;
+      rm += s_meta[c];
+    }
   }
-  for (uint64_t b = r.chunkidx_off + 8ull * nchunks + 4ull * tid; b < r.layers_off; b += 4ull * kPrepThreads)
+  const uint64_t entry = variant ? 16u : 8u;
+  for (uint64_t b = r.chunkidx_off + entry * nchunks + 4ull * tid; b < r.layers_off; b += 4ull * kPrepThreads)
     *reinterpret_cast<uint32_t*>(payload + b) = 0u;
 
   // 4. the 2-bit tier map (4 bytes per group of 16 tokens), then its padding
@@ -97,8 +121,9 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
     *reinterpret_cast<uint32_t*>(payload + b) = 0u;
 }
 
-// grid: sum over requests of nchunks * 2 * H * layer_count workgroups
-template <int D>
+// grid: sum over requests of nchunks * 2 * H * layer_count workgroups.
+// VARIANT: some tier uses a quantizer variant (row_variants.h).
+template <int D, bool VARIANT>
 __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   __shared__ ChunkLds s;
   const uint64_t bid = blockIdx.x;
@@ -118,20 +143,26 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   const int t0 = chunk * kChunkTokens;
 
   // row offsets of this chunk: chunk-index base + block exclusive scan
+  const VarCfg var{a.q8, a.q4, a.e8, a.e4};
   {
     const int t = t0 + threadIdx.x;
-    chunk_layout<D>(s, t < n ? r.tier[t] : kDROP,
-                    reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off) + 2 * chunk);
+    const int tr = t < n ? r.tier[t] : kDROP;
+    const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off);
+    if constexpr (VARIANT) chunk_layout_var<D>(s, tr, cidx + 4 * chunk, var);
+    else chunk_layout<D>(s, tr, cidx + 2 * chunk);
   }
   __syncthreads();
 
   const uint16_t* src = (kv ? r.v : r.k) + (static_cast<size_t>(l) * H + h) * static_cast<size_t>(n) * D;
   uint8_t* lay = payload + r.layers_off + static_cast<uint64_t>(l) * r.layer_stride;
   uint8_t* dst = lay + r.scales_bytes + static_cast<uint64_t>(kv * H + h) * r.seg_stride;
-  float* scales = reinterpret_cast<float*>(lay) + static_cast<uint64_t>(kv * H + h) * r.nq;
-  pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, src, dst, scales,
-                                                            reinterpret_cast<uint32_t*>(payload) + kHdrNonfinite,
-                                                            t0, n);
+  uint8_t* meta = lay + static_cast<uint64_t>(kv * H + h) * r.seg_scale_bytes;
+  uint32_t* nonfinite = reinterpret_cast<uint32_t*>(payload) + kHdrNonfinite;
+  if constexpr (VARIANT)
+    pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, src, dst, meta, nonfinite, t0, n, var);
+  else
+    pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, src, dst, reinterpret_cast<float*>(meta), nonfinite,
+                                                              t0, n);
 
   // padding: segment tail (last chunk) and the layer's scale-section tail
   if (chunk == nchunks - 1) {
@@ -139,7 +170,7 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
       st_nt16(dst + b, u32x4{0u, 0u, 0u, 0u});
   }
   if (chunk == 0 && kv == 0 && h == 0) {
-    const uint64_t used = 2ull * H * static_cast<uint64_t>(r.nq) * 4u;
+    const uint64_t used = 2ull * H * r.seg_scale_bytes;
     for (uint64_t b = used + 4ull * threadIdx.x; b < r.scales_bytes; b += 4ull * kRowThreads)
       *reinterpret_cast<uint32_t*>(lay + b) = 0u;
   }
@@ -153,11 +184,16 @@ hipError_t launch_pack(const BatchArgs& a, uint64_t rows, hipStream_t stream) {
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  switch (a.d) {
-    case 32: pack_rows<32><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 64: pack_rows<64><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 128: pack_rows<128><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 256: pack_rows<256><<<rows, kRowThreads, 0, stream>>>(a); break;
+  const bool variant = (a.q8 | a.q4) != 0;
+  switch (a.d * 2 + (variant ? 1 : 0)) {
+    case 64: pack_rows<32, false><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 128: pack_rows<64, false><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 256: pack_rows<128, false><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 512: pack_rows<256, false><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 65: pack_rows<32, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 129: pack_rows<64, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 257: pack_rows<128, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 513: pack_rows<256, true><<<rows, kRowThreads, 0, stream>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -31,6 +31,8 @@ skv_status check_config(const skv_config* c) {
   if (2.0 * static_cast<double>(c->decay) * static_cast<double>(c->num_tokens - 1) > 700.0)
     return SKV_ERR_INVALID_ARG;
   if (c->num_tiers != 2 && c->num_tiers != 3) return SKV_ERR_INVALID_ARG;
+  for (const int32_t q : {c->quant_int8, c->quant_int4})
+    if ((q & ~15) != 0 || (q & 3) == 3) return SKV_ERR_INVALID_ARG;
   switch (c->score_mode) {
     case SKV_SCORE_KVNORM:
     case SKV_SCORE_RECENCY:
@@ -91,6 +93,13 @@ skv_status plan_counts(const skv_config* c, skv_plan* p) {
   return SKV_OK;
 }
 
+// Metadata bytes of one quantized row under variant descriptor q.
+inline uint32_t variant_meta_bytes(int32_t q, int32_t d) {
+  int32_t gs = (q & 3) == 0 ? d : (q & 3) == 1 ? 64 : 32;
+  gs = std::min(gs, d);
+  return static_cast<uint32_t>(d / gs) * ((q & SKV_QUANT_ASYM) ? 2u : 1u) * ((q & SKV_QUANT_FP16) ? 2u : 4u);
+}
+
 inline uint32_t float_bits(float f) {
   uint32_t u;
   std::memcpy(&u, &f, 4);
@@ -117,15 +126,21 @@ skv_status make_geometry(const skv_config* cfg, Geometry* g, skv_plan* plan_out)
   g->budget_units = p.budget_units;
   g->used_units = p.used_units;
   g->nq = static_cast<int64_t>(p.n_int8) + p.n_int4;
+  g->q8 = cfg->quant_int8;
+  g->q4 = cfg->quant_int4;
+  g->e8 = variant_meta_bytes(g->q8, cfg->head_dim);
+  g->e4 = variant_meta_bytes(g->q4, cfg->head_dim);
+  g->seg_scale_bytes = static_cast<uint64_t>(p.n_int8) * g->e8 + static_cast<uint64_t>(p.n_int4) * g->e4;
+  g->cidx_entry = (g->q8 | g->q4) ? 16u : 8u;
   g->nchunks = (g->n + kChunkTokens - 1) / kChunkTokens;
   const uint64_t d = static_cast<uint64_t>(g->d), H = static_cast<uint64_t>(g->H);
   g->tiermap_off = 256;
   g->chunkidx_off = g->tiermap_off + round_up_256((static_cast<uint64_t>(g->n) + 3) / 4);
-  g->layers_off = g->chunkidx_off + round_up_256(8u * static_cast<uint64_t>(g->nchunks));
+  g->layers_off = g->chunkidx_off + round_up_256(g->cidx_entry * static_cast<uint64_t>(g->nchunks));
   g->seg_bytes = static_cast<uint64_t>(p.n_sink + p.n_fp16) * (2 * d) +
                  static_cast<uint64_t>(p.n_int8) * d + static_cast<uint64_t>(p.n_int4) * (d / 2);
   g->seg_stride = round_up_256(g->seg_bytes);
-  g->scales_bytes = round_up_256(2 * H * static_cast<uint64_t>(g->nq) * 4u);
+  g->scales_bytes = round_up_256(2 * H * g->seg_scale_bytes);
   g->layer_stride = g->scales_bytes + 2 * H * g->seg_stride;
   g->total = g->layers_off + static_cast<uint64_t>(g->L) * g->layer_stride;
   if (plan_out) *plan_out = p;
@@ -165,6 +180,10 @@ void fill_common(const skv_config* cfg, int32_t layer_begin, int32_t layer_count
   a->budget_bits = float_bits(cfg->budget);
   a->rho_bits = float_bits(cfg->first_ratio);
   a->decay_bits = float_bits(cfg->decay);
+  a->q8 = cfg->quant_int8;
+  a->q4 = cfg->quant_int4;
+  a->e8 = variant_meta_bytes(cfg->quant_int8, cfg->head_dim);
+  a->e4 = variant_meta_bytes(cfg->quant_int4, cfg->head_dim);
 }
 
 void fill_desc(const Geometry& g, const skv_request& q, ReqDesc* r) {
@@ -178,6 +197,7 @@ void fill_desc(const Geometry& g, const skv_request& q, ReqDesc* r) {
   r->chunkidx_off = g.chunkidx_off;
   r->layers_off = g.layers_off;
   r->seg_bytes = g.seg_bytes;
+  r->seg_scale_bytes = g.seg_scale_bytes;
   r->seg_stride = g.seg_stride;
   r->scales_bytes = g.scales_bytes;
   r->layer_stride = g.layer_stride;
@@ -270,6 +290,7 @@ struct GroupHost {
 skv_status group_host(const skv_config* cfg, const skv_group_spec* spec, GroupHost* out) {
   skv_status st = check_config(cfg);
   if (st != SKV_OK) return st;
+  if (cfg->quant_int8 != 0 || cfg->quant_int4 != 0) return SKV_ERR_INVALID_ARG;  // descriptor 0 only
   if (spec == nullptr || spec->reserved != 0) return SKV_ERR_INVALID_ARG;
   const int32_t gran = spec->granularity, G = group_count(cfg, gran);
   if (G < 1) return SKV_ERR_INVALID_ARG;
@@ -522,6 +543,7 @@ skv_status skv_upgrade_size(const skv_config* cfg, int32_t m, int32_t mode, uint
   if (bytes == nullptr) return SKV_ERR_INVALID_ARG;
   const skv_status st = check_config(cfg);
   if (st != SKV_OK) return st;
+  if (cfg->quant_int8 != 0 || cfg->quant_int4 != 0) return SKV_ERR_INVALID_ARG;  // held rows use descriptor 0
   if (m < 1 || m > cfg->num_tokens || (mode != SKV_UPGRADE_FP16 && mode != SKV_UPGRADE_RESIDUAL8))
     return SKV_ERR_INVALID_ARG;
   *bytes = upgrade_bytes(cfg->num_layers, cfg->num_kv_heads, cfg->head_dim, m, mode, nullptr);

@@ -21,6 +21,9 @@ struct Geometry {
   int32_t n_sink, n16, n8, n4, nd;
   int64_t budget_units, used_units;
   int64_t nq;       // quantized rows per segment (n8 + n4)
+  int32_t q8, q4;   // quantizer variant descriptors (0: row-wise symmetric, fp32 scale)
+  uint32_t e8, e4;  // metadata bytes of an INT8 / INT4 row
+  uint64_t seg_scale_bytes, cidx_entry;  // metadata bytes of a segment; chunk-index entry bytes (8 or 16)
   int64_t nchunks;  // ceil(n / 256)
   uint64_t tiermap_off, chunkidx_off, layers_off;
   uint64_t seg_bytes, seg_stride, scales_bytes, layer_stride, total;
@@ -38,6 +41,7 @@ struct ReqDesc {
   const int32_t* block_table;   // unpack only
   uint64_t block_begin;         // first flat workgroup of this request in the row launch
   uint64_t chunkidx_off, layers_off, seg_bytes, seg_stride, scales_bytes, layer_stride, total;
+  uint64_t seg_scale_bytes;  // metadata bytes of one segment (4 * nq for descriptor 0)
   int64_t nq, budget_units, used_units;
   int32_t n, nchunks, n_sink, n16, n8, n4, nd, pad;
 };
@@ -48,6 +52,8 @@ constexpr int kMaxBatch = 16;  // requests per launch (descriptors travel as ker
 struct BatchArgs {
   int32_t count, L, H, d, layer_begin, layer_count, num_tiers, score_mode;
   uint32_t budget_bits, rho_bits, decay_bits, pad;
+  int32_t q8, q4;    // quantizer variant descriptors of the INT8 and INT4 tiers
+  uint32_t e8, e4;   // metadata bytes of an INT8 / INT4 row
   ReqDesc r[kMaxBatch];
 };
 static_assert(sizeof(BatchArgs) <= 4000, "kernel arguments");

@@ -143,6 +143,8 @@ __device__ __forceinline__ uint32_t header_word(const BatchArgs& a, const ReqDes
     case 34: return lo(r.total);
     case 35: return hi(r.total);
     case 38: return static_cast<uint32_t>(kChunkTokens);
+    case 39: return static_cast<uint32_t>(a.q8);
+    case 40: return static_cast<uint32_t>(a.q4);
     default: return 0u;
   }
 }

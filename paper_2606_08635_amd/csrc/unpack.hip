@@ -14,6 +14,7 @@
 #include "device_util.h"
 #include "row_codec.h"
 #include "row_stream.h"
+#include "row_variants.h"
 #include "skv_internal.h"
 #include "tier_groups.h"
 
@@ -35,10 +36,13 @@ constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
 __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a, int num_blocks,
                                                               int block_size) {
   __shared__ uint32_t s_chunk[kMaxChunks];
+  __shared__ uint32_t s_meta[kMaxChunks];  // per chunk: metadata bytes (variant descriptors)
   __shared__ uint32_t s_cnt[4];
   __shared__ uint32_t s_bad;
   __shared__ uint64_t s_scan[16];
+  __shared__ uint64_t s_scan2[16];
   const ReqDesc& r = a.r[blockIdx.x];
+  const bool variant = (a.q8 | a.q4) != 0;  // launch-uniform
   const uint8_t* __restrict__ payload = r.payload;
   const int n = r.n, nchunks = r.nchunks;
   const int tid = threadIdx.x;
@@ -71,7 +75,11 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
 #pragma unroll
     for (int i = 0; i < 4; ++i) cnt[i] += gi.count(i);
     const uint32_t u = sum16(gi.units), q = sum16(gi.quant);
-    if ((tid % kGroupsPerChunk) == 0 && g < ngroups) s_chunk[g / kGroupsPerChunk] = u | (q << 16);
+    const uint32_t m = sum16(gi.count(kINT8) * a.e8 + gi.count(kINT4) * a.e4);
+    if ((tid % kGroupsPerChunk) == 0 && g < ngroups) {
+      s_chunk[g / kGroupsPerChunk] = u | (q << 16);
+      s_meta[g / kGroupsPerChunk] = m;
+    }
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -87,18 +95,31 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
   const uint64_t ex = block_exclusive_scan_1024(run, s_scan);
   uint32_t ru = static_cast<uint32_t>(ex), rq = static_cast<uint32_t>(ex >> 32);
   const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off);
-  for (int c = c0; c < c1; ++c) {
-    bad |= cidx[2 * c] != ru || cidx[2 * c + 1] != rq;
-    ru += s_chunk[c] & 0xFFFFu;
-    rq += s_chunk[c] >> 16;
+  if (!variant) {
+    for (int c = c0; c < c1; ++c) {
+      bad |= cidx[2 * c] != ru || cidx[2 * c + 1] != rq;
+      ru += s_chunk[c] & 0xFFFFu;
+      rq += s_chunk[c] >> 16;
+    }
+  } else {
+    uint64_t mrun = 0;
+    for (int c = c0; c < c1; ++c) mrun += s_meta[c];
+    uint32_t rm = static_cast<uint32_t>(block_exclusive_scan_1024(mrun, s_scan2));
+    for (int c = c0; c < c1; ++c) {
+      bad |= cidx[4 * c] != ru || cidx[4 * c + 1] != rq || cidx[4 * c + 2] != rm || cidx[4 * c + 3] != 0u;
+      ru += s_chunk[c] & 0xFFFFu;
+      rq += s_chunk[c] >> 16;
+      rm += s_meta[c];
+    }
   }
   if (bad) atomicOr(&s_bad, 1u);
   __syncthreads();
   if (tid == 0) *r.status = s_bad ? static_cast<uint32_t>(SKV_ERR_FORMAT) : 0u;
 }
 
-// grid: sum over requests of nchunks * 2 * H * layer_count workgroups
-template <int D>
+// grid: sum over requests of nchunks * 2 * H * layer_count workgroups.
+// VARIANT: some tier uses a quantizer variant (row_variants.h).
+template <int D, bool VARIANT>
 __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, uint16_t* __restrict__ k_cache,
                                                            uint16_t* __restrict__ v_cache, int num_blocks,
                                                            int block_size) {
@@ -126,17 +147,24 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
       pos = static_cast<uint32_t>(r.block_table[t / block_size]) * static_cast<uint32_t>(block_size) +
             static_cast<uint32_t>(t % block_size);
     }
-    chunk_layout<D>(s, tr, reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off) + 2 * chunk);
+    const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off);
+    if constexpr (VARIANT) chunk_layout_var<D>(s, tr, cidx + 4 * chunk, VarCfg{a.q8, a.q4, a.e8, a.e4});
+    else chunk_layout<D>(s, tr, cidx + 2 * chunk);
     s.pos[threadIdx.x] = pos;
   }
   __syncthreads();
 
   const uint8_t* lay = payload + r.layers_off + static_cast<uint64_t>(l) * r.layer_stride;
   const uint8_t* src = lay + r.scales_bytes + static_cast<uint64_t>(kv * H + h) * r.seg_stride;
-  const float* scales = reinterpret_cast<const float*>(lay) + static_cast<uint64_t>(kv * H + h) * r.nq;
+  const uint8_t* meta = lay + static_cast<uint64_t>(kv * H + h) * r.seg_scale_bytes;
   uint16_t* cache = (kv ? v_cache : k_cache) + static_cast<size_t>(l) * num_blocks * block_size * H * D +
                     static_cast<size_t>(h) * D;
-  unpack_chunk<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, scales, cache, H);
+  if constexpr (VARIANT)
+    unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, meta, cache, H,
+                                                                         VarCfg{a.q8, a.q4, a.e8, a.e4});
+  else
+    unpack_chunk<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, reinterpret_cast<const float*>(meta),
+                                                                     cache, H);
 }
 
 }  // namespace
@@ -148,13 +176,21 @@ hipError_t launch_unpack(const BatchArgs& a, uint64_t rows, uint16_t* k_cache, u
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  switch (a.d) {
-    case 32: unpack_rows<32><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size); break;
-    case 64: unpack_rows<64><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size); break;
-    case 128: unpack_rows<128><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size); break;
-    case 256: unpack_rows<256><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size); break;
+  const bool variant = (a.q8 | a.q4) != 0;
+#define SKV_UNPACK_LAUNCH(D, V) \
+  unpack_rows<D, V><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size)
+  switch (a.d * 2 + (variant ? 1 : 0)) {
+    case 64: SKV_UNPACK_LAUNCH(32, false); break;
+    case 128: SKV_UNPACK_LAUNCH(64, false); break;
+    case 256: SKV_UNPACK_LAUNCH(128, false); break;
+    case 512: SKV_UNPACK_LAUNCH(256, false); break;
+    case 65: SKV_UNPACK_LAUNCH(32, true); break;
+    case 129: SKV_UNPACK_LAUNCH(64, true); break;
+    case 257: SKV_UNPACK_LAUNCH(128, true); break;
+    case 513: SKV_UNPACK_LAUNCH(256, true); break;
     default: return hipErrorInvalidValue;
   }
+#undef SKV_UNPACK_LAUNCH
   return hipGetLastError();
 }
 

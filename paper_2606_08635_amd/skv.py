@@ -20,6 +20,8 @@ FP16, INT8, INT4, DROP = 0, 1, 2, 3
 KVNORM, ATTN, RECENCY = 0, 1, 2
 UPGRADE_FP16, UPGRADE_RESIDUAL8 = 0, 1
 GROUP_TOKEN, GROUP_LAYER, GROUP_HEAD = 0, 1, 2
+QUANT_GROUP64, QUANT_GROUP32, QUANT_ASYM, QUANT_FP16 = 1, 2, 4, 8
+ABI_VERSION = 2
 
 EXPORTED = ("skv_abi_version", "skv_status_string", "skv_plan_tiers", "skv_payload_size",
             "skv_workspace_size", "skv_prepare", "skv_score", "skv_assign_tiers", "skv_pack",
@@ -41,7 +43,8 @@ class Config(ctypes.Structure):
                 ("budget", ctypes.c_float), ("first_ratio", ctypes.c_float),
                 ("num_sink", ctypes.c_int32), ("decay", ctypes.c_float),
                 ("num_tiers", ctypes.c_int32), ("score_mode", ctypes.c_int32),
-                ("num_q_heads", ctypes.c_int32), ("obs_window", ctypes.c_int32)]
+                ("num_q_heads", ctypes.c_int32), ("obs_window", ctypes.c_int32),
+                ("quant_int8", ctypes.c_int32), ("quant_int4", ctypes.c_int32)]
 
 
 class Request(ctypes.Structure):
@@ -116,9 +119,10 @@ def status_string(status: int) -> str:
 
 
 def config(num_layers, num_kv_heads, head_dim, num_tokens, budget, first_ratio=0.02, num_sink=-1,
-           decay=0.005, num_tiers=3, score_mode=KVNORM, num_q_heads=0, obs_window=0) -> Config:
+           decay=0.005, num_tiers=3, score_mode=KVNORM, num_q_heads=0, obs_window=0, quant_int8=0,
+           quant_int4=0) -> Config:
     return Config(num_layers, num_kv_heads, head_dim, num_tokens, budget, first_ratio, num_sink,
-                  decay, num_tiers, score_mode, num_q_heads, obs_window)
+                  decay, num_tiers, score_mode, num_q_heads, obs_window, quant_int8, quant_int4)
 
 
 def _check(status: int, what: str):

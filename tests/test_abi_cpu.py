@@ -35,7 +35,7 @@ def test_every_declared_symbol_is_exported(lib):
     for name in names:
         assert hasattr(lib, name), name
     assert sorted(skv.EXPORTED) == names
-    assert lib.skv_abi_version() == 1
+    assert lib.skv_abi_version() == skv.ABI_VERSION == 2
 
 
 def _pair(L, H, d, n, b, **kw):
@@ -51,7 +51,8 @@ def test_plan_and_payload_size_match_oracle(lib, seed):
         n = int(rng.integers(1, 70000))
         b = float(np.float32(rng.uniform(0.01, 1.0)))
         kw = dict(first_ratio=float(np.float32(rng.uniform(0, 0.1))), num_tiers=int(rng.integers(2, 4)),
-                  decay=0.0, num_sink=int(rng.choice([-1, -1, 0, 5])))
+                  decay=0.0, num_sink=int(rng.choice([-1, -1, 0, 5])),
+                  quant_int8=int(rng.choice([0, 0, 1, 2, 4, 8, 13, 14])), quant_int4=int(rng.choice([0, 0, 5, 10, 12])))
         c, o = _pair(L, H, d, n, b, **kw)
         try:
             want = oracle.plan(o)
@@ -69,7 +70,8 @@ def test_invalid_configs_rejected_like_the_oracle(lib):
     for field, value in [("head_dim", 48), ("head_dim", 512), ("num_tokens", 0), ("num_tokens", (1 << 21) + 1),
                          ("budget", 0.0), ("budget", 1.5), ("budget", float("nan")), ("first_ratio", -0.1),
                          ("num_tiers", 4), ("score_mode", 3), ("decay", -1.0), ("decay", float("inf")),
-                         ("decay", 1.0), ("num_sink", -2), ("num_layers", 0), ("num_kv_heads", 0)]:
+                         ("decay", 1.0), ("num_sink", -2), ("num_layers", 0), ("num_kv_heads", 0),
+                         ("quant_int8", 3), ("quant_int4", 16), ("quant_int4", -1)]:
         c = skv.config(**base)
         setattr(c, field, value)
         o = oracle.config(**base)
