@@ -25,28 +25,33 @@ CSRC = os.path.join(ROOT, "paper_2606_08635_amd", "csrc")
 
 # HBM bytes per dispatch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs (scaled by
 # a plain-copy calibration; see profiles/traffic_*.md), valid only for the
-# kernel sources they were taken on (first 16 hex digits of SHA-256 of each file).
+# kernel sources they were taken on: the first 16 hex digits of SHA-256 over
+# the kernel's .hip file and every header of the library (source_digest).
 MEASURED_TRAFFIC = {
-    ("mistral7b_32k", "pack"): (6.5086e9, {"pack.hip": "a159b0197da6e8b0", "row_codec.h": "77df103bddc04308",
-                                           "device_util.h": "187abc123a53519a", "tier_groups.h": "f3e053754552f3f6",
-                                           "skv_internal.h": "a722bd6f24154b62"}),
-    ("mistral7b_32k", "unpack"): (6.5126e9, {"unpack.hip": "02842c07f7ff1b6a", "row_codec.h": "77df103bddc04308",
-                                             "device_util.h": "187abc123a53519a", "tier_groups.h": "f3e053754552f3f6",
-                                             "skv_internal.h": "a722bd6f24154b62"}),
+    ("mistral7b_32k", "pack"): (6.5086e9, "pack.hip", "f1453a60af494d45"),
+    ("mistral7b_32k", "unpack"): (6.5125e9, "unpack.hip", "f372993299081d4d"),
 }
 
 
-def measured_traffic(workload, kernel):
+def source_digest(kernel_file):
+    import glob
     import hashlib
 
+    h = hashlib.sha256()
+    for path in [os.path.join(CSRC, kernel_file)] + sorted(glob.glob(os.path.join(CSRC, "*.h"))):
+        h.update(os.path.basename(path).encode())
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
     entry = MEASURED_TRAFFIC.get((workload, kernel))
     if entry is None:
         return None
-    nbytes, sources = entry
-    for name, digest in sources.items():
-        with open(os.path.join(CSRC, name), "rb") as f:
-            if hashlib.sha256(f.read()).hexdigest()[:16] != digest:
-                return None  # the kernel changed since the counters were taken
+    nbytes, kernel_file, digest = entry
+    if source_digest(kernel_file) != digest:
+        return None  # the kernel changed since the counters were taken
     return nbytes
 
 
