@@ -5,15 +5,21 @@
 // M = G*W observation rows q_m (contiguous in q_obs).  With z[m,t] = q_m.k_t/sqrt(d),
 //   A_t = (1 / (L*Hq*W)) * sum over (l, h, m) of softmax_t(z[m, :])[t].
 // Q.K^T is a dense contraction, so it runs on the matrix cores
-// (v_mfma_f32_32x32x16_f16: a 32-row block of queries times a 32-key tile,
-// fp32 accumulation; binary16 products are exact in fp32).
+// (v_mfma_f32_32x32x16_f16, fp32 accumulation; binary16 products are exact
+// in fp32).  A workgroup owns 1024 keys of one (l, h); its four waves take
+// one 32-row query tile each (with fewer tiles, the key tiles are split into
+// interleaved streams), so the keys are read from HBM once per pass and
+// shared by the waves through the caches; the next key tile is loaded while
+// the current one is multiplied.
 //   attn_stats:   per (l, h, key block) and row, the row maximum and the sum
-//                 of exp(z - max) over the block's keys (lane-local online
-//                 update, one lane merge at the end, waves merged in order);
+//                 of exp(z - max) over the block's keys (keys as MFMA rows, so
+//                 a lane updates one query's running max and sum: one
+//                 exponential per logit; streams merged in order);
 //   attn_merge:   per (l, h, row), the blocks merged in key order into
 //                 c = max + log(sum);
 //   attn_colsum:  recomputes z, p = exp(z - c), and sums p over the rows of
-//                 the group for every key (one write per (l, h, key));
+//                 the group for every key (queries as MFMA rows; lane-halves
+//                 and waves added in fixed order);
 //   attn_finish:  per key, the (l, h) partial sums added in fixed order in
 //                 binary64, times 1/(L Hq W) and exp(-lambda Delta).
 // Every reduction has a fixed order, so the scores are deterministic; they
@@ -28,12 +34,16 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kWaves = 4;
-constexpr int kTilesPerWave = 4;                        // 32-key tiles per wave
-constexpr int kBlockKeys = kWaves * kTilesPerWave * 32;  // 512 keys per workgroup
+constexpr int kBlockKeys = 1024;              // keys per workgroup
+constexpr int kTiles = kBlockKeys / 32;       // 32-key tiles per workgroup
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
 
 // Row of accumulator register r in lane-half hf of a 32x32 MFMA result
 // (the column is lane % 32).
 __device__ __forceinline__ int acc_row(int r, int hf) { return 8 * (r >> 2) + 4 * hf + (r & 3); }
+
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // Stats of one row, merged: (m, s) stands for s * exp(m); m = -inf means empty.
 __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2) {
@@ -43,105 +53,148 @@ __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2
   m = mm;
 }
 
+// The same in base-2 units scaled by alpha: (m, s) stands for s * 2^(alpha m).
+__device__ __forceinline__ void lse_merge2(float& m, float& s, float m2, float s2, float alpha) {
+  const float mm = fmaxf(m, m2);
+  if (mm == -INFINITY) return;
+  s = s * exp2_fast((m - mm) * alpha) + s2 * exp2_fast((m2 - mm) * alpha);
+  m = mm;
+}
+
+// The 16-byte operand slice of row `row` for MFMA k-step s in lane-half hf:
+// elements 16 s + 8 hf .. + 8 (zeros when the row is absent).
 template <int D>
-__device__ __forceinline__ half8 load_row16(const uint16_t* row, int col, bool ok) {
-  if (!ok) return half8{};
-  return __builtin_bit_cast(half8, ld_nt16(row + col));
-}
-
-// Q operand of M-tile `mt`, K-step s: row mt*32 + lane%32, columns 16s + 8hf .. +8.
-template <int D, int MTG>
-__device__ __forceinline__ void load_q(const uint16_t* q, int M, int mt0, int mt_count, half8 (&qr)[MTG][D / 16]) {
-  const int i = threadIdx.x & 31, hf = (threadIdx.x >> 5) & 1;
-#pragma unroll
-  for (int a = 0; a < MTG; ++a) {
-    const int row = (mt0 + a) * 32 + i;
-    const bool ok = a < mt_count && row < M;
-#pragma unroll
-    for (int s = 0; s < D / 16; ++s) qr[a][s] = load_row16<D>(q + static_cast<size_t>(ok ? row : 0) * D, 16 * s + 8 * hf, ok);
-  }
-}
-
-template <int D, int MTG>
-__device__ __forceinline__ void logits(const half8 (&qr)[MTG][D / 16], const half8 (&kr)[D / 16], int mt_count,
-                                       floatx16 (&acc)[MTG]) {
-#pragma unroll
-  for (int a = 0; a < MTG; ++a) {
-    acc[a] = floatx16{};
-    if (a < mt_count) {
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s) acc[a] = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[a][s], kr[s], acc[a], 0, 0, 0);
-    }
-  }
-}
-
-template <int D>
-__device__ __forceinline__ void load_k(const uint16_t* kbase, int n, int t, half8 (&kr)[D / 16]) {
+__device__ __forceinline__ void load_rows(const uint16_t* base, int row, bool ok, half8 (&out)[D / 16]) {
   const int hf = (threadIdx.x >> 5) & 1;
-  const bool ok = t < n;
+  const uint16_t* p = base + static_cast<size_t>(ok ? row : 0) * D + 8 * hf;
 #pragma unroll
-  for (int s = 0; s < D / 16; ++s) kr[s] = load_row16<D>(kbase + static_cast<size_t>(ok ? t : 0) * D, 16 * s + 8 * hf, ok);
+  for (int s = 0; s < D / 16; ++s) out[s] = ok ? __builtin_bit_cast(half8, *reinterpret_cast<const u32x4*>(p + 16 * s)) : half8{};
 }
 
-// grid (L*H, key blocks); scratch pstat[(lh * nkb + kb) * Mpad + row] = (max, sum)
-template <int D, int MTG>
+// Work of wave w in round r: query tiles r*4 .. r*4+qg-1 (qg = min(4, MT - 4r))
+// are spread over the waves; with fewer than 4 tiles the key tiles of the
+// block are split into nstreams interleaved streams so every wave works.
+struct WaveRole {
+  int qg, nstreams, qtile, stream;
+  bool active;
+};
+__device__ __forceinline__ WaveRole wave_role(int MT, int round, int wave) {
+  WaveRole r;
+  r.qg = min(4, MT - 4 * round);
+  r.nstreams = r.qg == 1 ? 4 : r.qg == 2 ? 2 : 1;
+  r.active = wave < r.qg * r.nstreams;
+  r.qtile = 4 * round + wave % r.qg;
+  r.stream = wave / r.qg;
+  return r;
+}
+
+template <int N>
+__device__ __forceinline__ float tree_max(float (&v)[N]) {
+#pragma unroll
+  for (int w = N / 2; w >= 1; w /= 2)
+#pragma unroll
+    for (int i = 0; i < w; ++i) v[i] = fmaxf(v[i], v[i + w]);
+  return v[0];
+}
+template <int N>
+__device__ __forceinline__ float tree_sum(float (&v)[N]) {
+#pragma unroll
+  for (int w = N / 2; w >= 1; w /= 2)
+#pragma unroll
+    for (int i = 0; i < w; ++i) v[i] = v[i] + v[i + w];
+  return v[0];
+}
+
+// Online (max, sum) update of one query with the 16 logits of a tile held by
+// this lane (y = acc * alpha, base-2 units).  MASK: keys t0 + acc_row >= n
+// are excluded.  m is kept in y units.
+template <bool MASK>
+__device__ __forceinline__ void tile_update(const floatx16& acc, float alpha, int t0, int hf, int n, float& m,
+                                            float& sum) {
+  float y[16], t[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    y[r] = acc[r] * alpha;
+    if (MASK && t0 + acc_row(r, hf) >= n) y[r] = -INFINITY;
+    t[r] = y[r];
+  }
+  const float tmax = tree_max<16>(t);
+  if (MASK && tmax == -INFINITY) return;
+  const float mn = fmaxf(m, tmax);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) y[r] = exp2_fast(y[r] - mn);
+  sum = sum * exp2_fast(m - mn) + tree_sum<16>(y);
+  m = mn;
+}
+
+// grid (L*H, key blocks); pstat[(lh * nkb + kb) * Mpad + row] = (max of z, sum of exp(z - max))
+// over the block's keys.  The logits are formed transposed (keys as MFMA rows,
+// queries as columns), so a lane holds 16 keys of one query and keeps that
+// query's running (max, sum) in two registers: one exponential per logit.
+template <int D>
 __global__ __launch_bounds__(kWaves * 64) void attn_stats(const uint16_t* __restrict__ k,
                                                           const uint16_t* __restrict__ q, int n, int H,
                                                           int Hq, int W, float scale,
                                                           float2* __restrict__ pstat) {
   const int lh = blockIdx.x, kb = blockIdx.y, nkb = gridDim.y;
   const int l = lh / H, h = lh % H, G = Hq / H, M = G * W, MT = (M + 31) / 32, Mpad = MT * 32;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, hf = lane >> 5;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, hf = lane >> 5, j = lane & 31;
   const uint16_t* kbase = k + static_cast<size_t>(lh) * n * D;
   const uint16_t* qbase = q + (static_cast<size_t>(l) * Hq + static_cast<size_t>(h) * G) * W * D;
-  __shared__ float2 s_stat[kWaves][256];
-  for (int mt0 = 0; mt0 < MT; mt0 += MTG) {
-    const int mt_count = min(MTG, MT - mt0);
-    half8 qr[MTG][D / 16];
-    load_q<D, MTG>(qbase, M, mt0, mt_count, qr);
-    float m[MTG][16], s[MTG][16];
+  const float alpha = scale * kLog2e;
+  const int key0 = kb * kBlockKeys;
+  __shared__ float2 s_stat[kWaves][32];
+  for (int round = 0; 4 * round < MT; ++round) {
+    const WaveRole role = wave_role(MT, round, wave);
+    if (role.active) {
+      half8 qr[D / 16];
+      const int qrow = role.qtile * 32 + j;
+      load_rows<D>(qbase, qrow, qrow < M, qr);
+      float m = -INFINITY, sum = 0.0f;  // m in base-2 units (logit * scale * log2 e)
+      // two tiles per step: the second tile's MFMAs run while the first
+      // tile's exponentials are computed; the next pair is loaded meanwhile
+      const int st = role.nstreams;
+      half8 ka[D / 16], kb2[D / 16];
+      const int i0 = role.stream;
+      load_rows<D>(kbase, key0 + i0 * 32 + j, key0 + i0 * 32 + j < n, ka);
+      if (i0 + st < kTiles) load_rows<D>(kbase, key0 + (i0 + st) * 32 + j, key0 + (i0 + st) * 32 + j < n, kb2);
+      for (int i = i0; i < kTiles && key0 + i * 32 < n; i += 2 * st) {  // wave-uniform bounds
+        const int i1 = i + st;
+        const bool has1 = i1 < kTiles && key0 + i1 * 32 < n;
+        floatx16 a0{}, a1{};
 #pragma unroll
-    for (int a = 0; a < MTG; ++a)
+        for (int s = 0; s < D / 16; ++s) a0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ka[s], qr[s], a0, 0, 0, 0);
+        if (has1) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) { m[a][r] = -INFINITY; s[a][r] = 0.0f; }
-    for (int i = 0; i < kTilesPerWave; ++i) {
-      const int t0 = (kb * kWaves * kTilesPerWave + wave * kTilesPerWave + i) * 32;
-      const int t = t0 + (lane & 31);
-      half8 kr[D / 16];
-      load_k<D>(kbase, n, t, kr);
-      floatx16 acc[MTG];
-      logits<D, MTG>(qr, kr, mt_count, acc);
-#pragma unroll
-      for (int a = 0; a < MTG; ++a)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = (mt0 + a) * 32 + acc_row(r, hf);
-          if (a < mt_count && row < M && t < n) {
-            const float z = acc[a][r] * scale;
-            const float e = __expf(-fabsf(z - m[a][r]));  // one exponential per logit
-            if (z > m[a][r]) { s[a][r] = s[a][r] * e + 1.0f; m[a][r] = z; }
-            else { s[a][r] += e; }
-          }
+          for (int s = 0; s < D / 16; ++s) a1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(kb2[s], qr[s], a1, 0, 0, 0);
         }
-    }
-    // merge the 32 lanes that share a lane-half (same rows, different keys)
-#pragma unroll
-    for (int a = 0; a < MTG; ++a)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-#pragma unroll
-        for (int o = 1; o < 32; o <<= 1) {
-          const float m2 = __shfl_xor(m[a][r], o), s2 = __shfl_xor(s[a][r], o);
-          lse_merge(m[a][r], s[a][r], m2, s2);
+        const int n0 = i + 2 * st, n1 = i + 3 * st;
+        if (n0 < kTiles) load_rows<D>(kbase, key0 + n0 * 32 + j, key0 + n0 * 32 + j < n, ka);
+        if (n1 < kTiles) load_rows<D>(kbase, key0 + n1 * 32 + j, key0 + n1 * 32 + j < n, kb2);
+        const int t0 = key0 + i * 32;
+        if (t0 + 32 <= n) tile_update<false>(a0, alpha, t0, hf, n, m, sum);
+        else tile_update<true>(a0, alpha, t0, hf, n, m, sum);
+        if (has1) {
+          const int t1 = key0 + i1 * 32;
+          if (t1 + 32 <= n) tile_update<false>(a1, alpha, t1, hf, n, m, sum);
+          else tile_update<true>(a1, alpha, t1, hf, n, m, sum);
         }
-        if ((lane & 31) == 0 && a < mt_count) s_stat[wave][(mt0 + a) * 32 + acc_row(r, hf) - mt0 * 32] = float2{m[a][r], s[a][r]};
       }
+      // the two lane-halves saw different keys of the same query
+      lse_merge2(m, sum, __shfl_xor(m, 32), __shfl_xor(sum, 32), 1.0f);
+      if (hf == 0) s_stat[wave][j] = float2{m, sum};
+    }
     __syncthreads();
-    // the four waves cover consecutive key ranges: merge them in order
-    for (int row = threadIdx.x; row < mt_count * 32; row += kWaves * 64) {
+    // merge the streams of each query in stream order; m to z units
+    for (int idx = threadIdx.x; idx < role.qg * 32; idx += kWaves * 64) {
+      const int qt = idx / 32, jj = idx % 32;
       float mm = -INFINITY, ss = 0.0f;
-      for (int w = 0; w < kWaves; ++w) lse_merge(mm, ss, s_stat[w][row].x, s_stat[w][row].y);
-      pstat[(static_cast<size_t>(lh) * nkb + kb) * Mpad + mt0 * 32 + row] = float2{mm, ss};
+      for (int st = 0; st < role.nstreams; ++st) {
+        const float2 v = s_stat[st * role.qg + qt][jj];
+        lse_merge2(mm, ss, v.x, v.y, 1.0f);
+      }
+      // (max, sum) in logit units: max z = m / log2(e)
+      pstat[(static_cast<size_t>(lh) * nkb + kb) * Mpad + (4 * round + qt) * 32 + jj] = float2{mm * kLn2, ss};
     }
     __syncthreads();
   }
@@ -161,8 +214,11 @@ __global__ __launch_bounds__(256) void attn_merge(const float2* __restrict__ pst
   cstat[idx] = row < M ? mm + __logf(ss) : INFINITY;  // padding rows: exp(z - inf) = 0
 }
 
-// grid (L*H, key blocks); colsum[lh * n + t] = sum over the group's rows of p[row, t]
-template <int D, int MTG>
+// grid (L*H, key blocks); colsum[lh * n + t] = sum over the group's rows of p[row, t].
+// Logits with queries as MFMA rows: a lane holds 16 rows of one key and sums
+// their probabilities; the lane-halves and the waves (query tiles and rounds)
+// are added in fixed order through shared memory.
+template <int D>
 __global__ __launch_bounds__(kWaves * 64) void attn_colsum(const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ q, int n, int H,
                                                            int Hq, int W, float scale,
@@ -170,45 +226,59 @@ __global__ __launch_bounds__(kWaves * 64) void attn_colsum(const uint16_t* __res
                                                            float* __restrict__ colsum) {
   const int lh = blockIdx.x, kb = blockIdx.y;
   const int l = lh / H, h = lh % H, G = Hq / H, M = G * W, MT = (M + 31) / 32, Mpad = MT * 32;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, hf = lane >> 5;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, hf = lane >> 5, j = lane & 31;
   const uint16_t* kbase = k + static_cast<size_t>(lh) * n * D;
   const uint16_t* qbase = q + (static_cast<size_t>(l) * Hq + static_cast<size_t>(h) * G) * W * D;
-  float col[kTilesPerWave];
+  const float alpha = scale * kLog2e;
+  const int key0 = kb * kBlockKeys;
+  __shared__ float s_col[kWaves][kBlockKeys];
+  for (int idx = threadIdx.x; idx < kWaves * kBlockKeys; idx += kWaves * 64) (&s_col[0][0])[idx] = 0.0f;
+  __syncthreads();
+  for (int round = 0; 4 * round < MT; ++round) {
+    const WaveRole role = wave_role(MT, round, wave);
+    if (!role.active) continue;
+    half8 qr[D / 16];
+    const int qrow = role.qtile * 32 + j;
+    load_rows<D>(qbase, qrow, qrow < M, qr);
+    float beta[16];  // c * log2(e) of the lane's 16 rows; +inf for padding rows
 #pragma unroll
-  for (int i = 0; i < kTilesPerWave; ++i) col[i] = 0.0f;
-  for (int mt0 = 0; mt0 < MT; mt0 += MTG) {
-    const int mt_count = min(MTG, MT - mt0);
-    half8 qr[MTG][D / 16];
-    load_q<D, MTG>(qbase, M, mt0, mt_count, qr);
-    float c[MTG][16];
+    for (int r = 0; r < 16; ++r)
+      beta[r] = cstat[static_cast<size_t>(lh) * Mpad + role.qtile * 32 + acc_row(r, hf)] * kLog2e;
+    // sum over the lane's 16 rows of p = 2^(acc * alpha - beta), then over both lane-halves
+    auto colsum_tile = [&](const floatx16& acc, int i) {
+      float e[16];
 #pragma unroll
-    for (int a = 0; a < MTG; ++a)
+      for (int r = 0; r < 16; ++r) e[r] = exp2_fast(__builtin_fmaf(acc[r], alpha, -beta[r]));
+      float p = tree_sum<16>(e);
+      p += __shfl_xor(p, 32);  // the other lane-half holds the other 16 rows
+      if (hf == 0) s_col[wave][i * 32 + j] += p;
+    };
+    const int st = role.nstreams;
+    half8 ka[D / 16], kb2[D / 16];
+    const int i0 = role.stream;
+    load_rows<D>(kbase, key0 + i0 * 32 + j, key0 + i0 * 32 + j < n, ka);
+    if (i0 + st < kTiles) load_rows<D>(kbase, key0 + (i0 + st) * 32 + j, key0 + (i0 + st) * 32 + j < n, kb2);
+    for (int i = i0; i < kTiles && key0 + i * 32 < n; i += 2 * st) {  // wave-uniform bounds
+      const int i1 = i + st;
+      const bool has1 = i1 < kTiles && key0 + i1 * 32 < n;
+      floatx16 a0{}, a1{};
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = (mt0 + a) * 32 + acc_row(r, hf);
-        c[a][r] = (a < mt_count) ? cstat[static_cast<size_t>(lh) * Mpad + row] : INFINITY;
+      for (int s = 0; s < D / 16; ++s) a0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[s], ka[s], a0, 0, 0, 0);
+      if (has1) {
+#pragma unroll
+        for (int s = 0; s < D / 16; ++s) a1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[s], kb2[s], a1, 0, 0, 0);
       }
-#pragma unroll
-    for (int i = 0; i < kTilesPerWave; ++i) {
-      const int t0 = (kb * kWaves * kTilesPerWave + wave * kTilesPerWave + i) * 32;
-      const int t = t0 + (lane & 31);
-      half8 kr[D / 16];
-      load_k<D>(kbase, n, t, kr);
-      floatx16 acc[MTG];
-      logits<D, MTG>(qr, kr, mt_count, acc);
-      float sum = 0.0f;
-#pragma unroll
-      for (int a = 0; a < MTG; ++a)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sum += __expf(acc[a][r] * scale - c[a][r]);
-      col[i] += sum;
+      const int n0 = i + 2 * st, n1 = i + 3 * st;
+      if (n0 < kTiles) load_rows<D>(kbase, key0 + n0 * 32 + j, key0 + n0 * 32 + j < n, ka);
+      if (n1 < kTiles) load_rows<D>(kbase, key0 + n1 * 32 + j, key0 + n1 * 32 + j < n, kb2);
+      colsum_tile(a0, i);
+      if (has1) colsum_tile(a1, i1);
     }
   }
-#pragma unroll
-  for (int i = 0; i < kTilesPerWave; ++i) {
-    const float total = col[i] + __shfl_xor(col[i], 32);  // the two lane-halves hold different rows
-    const int t = (kb * kWaves * kTilesPerWave + wave * kTilesPerWave + i) * 32 + (lane & 31);
-    if (lane < 32 && t < n) colsum[static_cast<size_t>(lh) * n + t] = total;
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < kBlockKeys; idx += kWaves * 64) {
+    const int t = key0 + idx;
+    if (t < n) colsum[static_cast<size_t>(lh) * n + t] = ((s_col[0][idx] + s_col[1][idx]) + s_col[2][idx]) + s_col[3][idx];
   }
 }
 
@@ -218,7 +288,15 @@ __global__ __launch_bounds__(256) void attn_finish(const float* __restrict__ col
   const int t = blockIdx.x * 256 + threadIdx.x;
   if (t >= n) return;
   double a = 0.0;
-  for (int lh = 0; lh < LH; ++lh) a += static_cast<double>(colsum[static_cast<size_t>(lh) * n + t]);
+  int lh = 0;
+  for (; lh + 8 <= LH; lh += 8) {  // eight loads in flight, added in (l, h) order
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = colsum[static_cast<size_t>(lh + u) * n + t];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) a += static_cast<double>(v[u]);
+  }
+  for (; lh < LH; ++lh) a += static_cast<double>(colsum[static_cast<size_t>(lh) * n + t]);
   score[t] = (a * inv_rows) * w1[n - 1 - t];
 }
 
@@ -257,16 +335,15 @@ AttnShape attn_shape(const Geometry& g, int32_t Hq, int32_t W) {
 template <int D>
 hipError_t launch_d(const Geometry& g, const AttnShape& s, int Hq, int W, const uint16_t* k, const uint16_t* q,
                     float2* pstat, float* cstat, float* colsum, hipStream_t stream) {
-  constexpr int MTG = 2;  // 32-row query tiles held in registers at a time
   const float scale = static_cast<float>(1.0 / sqrt(static_cast<double>(D)));
   const dim3 grid(s.LH, s.nkb);
-  attn_stats<D, MTG><<<grid, kWaves * 64, 0, stream>>>(k, q, g.n, g.H, Hq, W, scale, pstat);
+  attn_stats<D><<<grid, kWaves * 64, 0, stream>>>(k, q, g.n, g.H, Hq, W, scale, pstat);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   attn_merge<<<(s.LH * s.Mpad + 255) / 256, 256, 0, stream>>>(pstat, s.LH, s.nkb, s.Mpad, s.M, cstat);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  attn_colsum<D, MTG><<<grid, kWaves * 64, 0, stream>>>(k, q, g.n, g.H, Hq, W, scale, cstat, colsum);
+  attn_colsum<D><<<grid, kWaves * 64, 0, stream>>>(k, q, g.n, g.H, Hq, W, scale, cstat, colsum);
   return hipGetLastError();
 }
 
