@@ -8,9 +8,15 @@
 // (v_mfma_f32_32x32x16_f16, fp32 accumulation; binary16 products are exact
 // in fp32).  A workgroup owns 1024 keys of one (l, h); its four waves take
 // one 32-row query tile each (with fewer tiles, the key tiles are split into
-// interleaved streams), so the keys are read from HBM once per pass and
-// shared by the waves through the caches; the next key tile is loaded while
-// the current one is multiplied.
+// interleaved streams).  The keys pass through shared memory in stages of
+// 8-16 KB (32 KB at d = 256), filled by gfx950's direct global-to-LDS loads:
+// each key byte leaves HBM once per pass with contiguous 16-byte reads and
+// never occupies registers on the way, and the next stage is in flight while
+// the current one is multiplied.  The waves take their MFMA operands from the
+// stage through an XOR swizzle that keeps the 16-byte operand reads free of
+// bank conflicts; the wave role is scalar and the stage and tile loops are
+// unrolled, so control flow is scalar and every operand read is one lane
+// address plus an immediate.
 //   attn_stats:   per (l, h, key block) and row, the row maximum and the sum
 //                 of exp(z - max) over the block's keys (keys as MFMA rows, so
 //                 a lane updates one query's running max and sum: one
@@ -33,9 +39,12 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
+#ifndef SKV_ATTN_BUFFERS
+#define SKV_ATTN_BUFFERS 2  // key stages resident per workgroup (d <= 128)
+#endif
+
 constexpr int kWaves = 4;
 constexpr int kBlockKeys = 1024;              // keys per workgroup
-constexpr int kTiles = kBlockKeys / 32;       // 32-key tiles per workgroup
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -61,14 +70,123 @@ __device__ __forceinline__ void lse_merge2(float& m, float& s, float m2, float s
   m = mm;
 }
 
-// The 16-byte operand slice of row `row` for MFMA k-step s in lane-half hf:
-// elements 16 s + 8 hf .. + 8 (zeros when the row is absent).
+// The 16-byte operand slice of global row `row` for MFMA k-step s in
+// lane-half hf: elements 16 s + 8 hf .. + 8 (zeros when the row is absent).
 template <int D>
 __device__ __forceinline__ void load_rows(const uint16_t* base, int row, bool ok, half8 (&out)[D / 16]) {
   const int hf = (threadIdx.x >> 5) & 1;
   const uint16_t* p = base + static_cast<size_t>(ok ? row : 0) * D + 8 * hf;
 #pragma unroll
   for (int s = 0; s < D / 16; ++s) out[s] = ok ? __builtin_bit_cast(half8, *reinterpret_cast<const u32x4*>(p + 16 * s)) : half8{};
+}
+
+// A stage of keys in shared memory: kKeys rows of D binary16 values, filled
+// by direct global-to-LDS loads.  Each 16-byte load of a wave lands at LDS
+// address base + 16 * lane, so a stage is written as consecutive 16-byte
+// pieces; piece p holds row p / kCpr, chunk (p % kCpr) ^ swz(row) of the keys
+// (kCpr = D / 8 chunks of 8 elements per row).  The XOR swizzle spreads the
+// 16-byte operand reads of 8 consecutive rows (same chunk) over all 32 banks;
+// it depends on the row only modulo 32, so a lane's read offsets are the same
+// for every tile and every stage.
+template <int D>
+struct Stage {
+  static constexpr int kTiles = D < 128 ? 4 : 2;                 // 32-key tiles per stage
+  static constexpr int kKeys = kTiles * 32;
+  static constexpr int kCpr = D / 8;                             // 16-byte chunks per row
+  static constexpr int kRowsPer128 = kCpr >= 8 ? 1 : 8 / kCpr;   // rows sharing one 128-byte bank line
+  static constexpr int kPieces = kKeys * kCpr / (kWaves * 64);   // 16-byte loads per thread per stage
+  static constexpr int kTileBytes = 32 * D * 2;
+  static constexpr int kBytes = kKeys * D * 2;
+  // one stage being multiplied, the others in flight; at d = 256 a stage is 32 KB
+  static constexpr int kBuffers = D >= 256 ? 2 : SKV_ATTN_BUFFERS;
+  // register budget: four waves per SIMD up to d = 128 (no spills), two at d = 256
+  static constexpr int kWavesPerSimd = D >= 256 ? 2 : 4;
+  static_assert(kPieces * kWaves * 64 == kKeys * kCpr, "a stage is whole 16-byte pieces per thread");
+  static_assert(kBlockKeys % kKeys == 0, "a block is whole stages");
+  static_assert(kBuffers >= 2 && kBuffers <= 4 && (kBuffers - 2) * kPieces < 64, "outstanding loads fit vmcnt");
+  __device__ static __forceinline__ int swz(int row) { return (row / kRowsPer128) % kCpr; }
+};
+
+// Waits until at most N of this wave's vector memory loads are outstanding
+// (loads complete in issue order, so the older ones have landed).
+template <int N>
+__device__ __forceinline__ void wait_loads() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  asm volatile("" ::: "memory");
+  // s_waitcnt: vmcnt bits 3:0 and 15:14; expcnt (6:4) and lgkmcnt (11:8) at their maxima
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+  asm volatile("" ::: "memory");
+}
+
+// Waits until the loads of a stage have landed when `later` stages were
+// issued after it (later <= 2).
+template <int D>
+__device__ __forceinline__ void wait_stage(int later) {
+  constexpr int P = Stage<D>::kPieces;
+  if (later == 0) wait_loads<0>();
+  else if (later == 1) wait_loads<P>();
+  else wait_loads<2 * P>();
+}
+
+// Workgroup barrier for shared memory only: waits for this wave's LDS
+// accesses (lgkmcnt 0) but, unlike __syncthreads, not for the global loads in
+// flight; the empty asm statements keep the compiler from moving memory
+// accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// One direct global-to-LDS load: the 16 bytes at src (per lane) land at LDS
+// byte address lds_base + 16 * lane.  Issued from inline assembly so that the
+// compiler does not count it among its own loads: the stage loop waits for it
+// explicitly (wait_stage), and the compiler's own waits for its loads stay
+// correct because they can only wait longer.
+__device__ __forceinline__ void load_to_lds(const void* src, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base) : "memory", "m0");
+}
+
+// Issues the direct loads of keys t0 .. t0 + kKeys - 1 into the stage at sk.
+// Rows at or beyond n repeat row n - 1 (a valid address); their logits are
+// masked or never stored.
+template <int D>
+__device__ __forceinline__ void stage_issue(const uint16_t* kbase, int t0, int n, uint8_t* sk, int wave) {
+  using S = Stage<D>;
+  const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t*)sk));
+#pragma unroll
+  for (int u = 0; u < S::kPieces; ++u) {
+    const int p = u * kWaves * 64 + static_cast<int>(threadIdx.x);
+    const int row = p / S::kCpr, chunk = (p % S::kCpr) ^ S::swz(row);
+    const uint16_t* src = kbase + static_cast<size_t>(min(t0 + row, n - 1)) * D + 8 * chunk;
+    load_to_lds(src, __builtin_amdgcn_readfirstlane(base + static_cast<uint32_t>((u * kWaves * 64 + wave * 64) * 16)));
+  }
+}
+
+typedef __attribute__((address_space(3))) const half8* lds_half8_ptr;
+
+// LDS byte addresses of this lane's MFMA operand slices in the first tile of
+// the stage area at s_k: row j, elements 16 s + 8 hf .. + 8 (chunk 2 s + hf,
+// swizzled).  Other tiles and stages add a constant.
+template <int D>
+__device__ __forceinline__ void lane_addresses(const uint8_t* s_k, uint32_t (&addr)[D / 16]) {
+  const int hf = (threadIdx.x >> 5) & 1, j = threadIdx.x & 31;
+  const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const uint8_t*)s_k));
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) {
+    addr[s] = base + static_cast<uint32_t>(j * D * 2 + 16 * ((2 * s + hf) ^ Stage<D>::swz(j)));
+    asm volatile("" : "+v"(addr[s]));  // one register per slice: tile offsets fold into the reads
+  }
+}
+
+// The MFMA operand of one tile; `offset` is the tile's byte offset in the
+// stage area (a constant once the stage and tile loops are unrolled, so it
+// becomes the instruction's immediate offset).
+template <int D>
+__device__ __forceinline__ void stage_rows(const uint32_t (&addr)[D / 16], uint32_t offset, half8 (&out)[D / 16]) {
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) out[s] = *reinterpret_cast<lds_half8_ptr>(static_cast<uintptr_t>(addr[s] + offset));
 }
 
 // Work of wave w in round r: query tiles r*4 .. r*4+qg-1 (qg = min(4, MT - 4r))
@@ -105,25 +223,42 @@ __device__ __forceinline__ float tree_sum(float (&v)[N]) {
   return v[0];
 }
 
-// Online (max, sum) update of one query with the 16 logits of a tile held by
-// this lane (y = acc * alpha, base-2 units).  MASK: keys t0 + acc_row >= n
-// are excluded.  m is kept in y units.
+// Online update of one query's (m, sum) with the 16 logits of a tile held by
+// this lane; (m, sum) stands for sum * 2^m in base-2 units (logit * alpha).
+// The reference m is raised lazily: the tile is first exponentiated against
+// the current m (one FMA and one exponential per logit); only when its sum
+// leaves [0, 2^32] (m still -inf, a logit 32 binades above m, or a NaN) is
+// the tile redone against max(m, tile maximum) and the running sum rescaled.
+// m is always the maximum of some earlier tile, so every term that
+// underflows is below 2^-126 of a term already in the sum.  MASK: keys
+// t0 + acc_row >= n are excluded.
 template <bool MASK>
 __device__ __forceinline__ void tile_update(const floatx16& acc, float alpha, int t0, int hf, int n, float& m,
                                             float& sum) {
+  float x[16], e[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    x[r] = acc[r];
+    if (MASK && t0 + acc_row(r, hf) >= n) x[r] = -INFINITY;
+    e[r] = exp2_fast(__builtin_fmaf(x[r], alpha, -m));
+  }
+  const float s = tree_sum<16>(e);
+  if (s <= 0x1p32f) {
+    sum += s;
+    return;
+  }
   float y[16], t[16];
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    y[r] = acc[r] * alpha;
-    if (MASK && t0 + acc_row(r, hf) >= n) y[r] = -INFINITY;
+    y[r] = x[r] * alpha;
     t[r] = y[r];
   }
   const float tmax = tree_max<16>(t);
-  if (MASK && tmax == -INFINITY) return;
+  if (tmax == -INFINITY) return;  // every key masked (and m = -inf)
   const float mn = fmaxf(m, tmax);
 #pragma unroll
-  for (int r = 0; r < 16; ++r) y[r] = exp2_fast(y[r] - mn);
-  sum = sum * exp2_fast(m - mn) + tree_sum<16>(y);
+  for (int r = 0; r < 16; ++r) e[r] = exp2_fast(y[r] - mn);
+  sum = sum * exp2_fast(m - mn) + tree_sum<16>(e);
   m = mn;
 }
 
@@ -131,55 +266,69 @@ __device__ __forceinline__ void tile_update(const floatx16& acc, float alpha, in
 // over the block's keys.  The logits are formed transposed (keys as MFMA rows,
 // queries as columns), so a lane holds 16 keys of one query and keeps that
 // query's running (max, sum) in two registers: one exponential per logit.
+// The stage loop is unrolled over the stage buffers and the tiles of a stage,
+// so every shared-memory read is a lane offset plus an immediate.
 template <int D>
-__global__ __launch_bounds__(kWaves * 64) void attn_stats(const uint16_t* __restrict__ k,
-                                                          const uint16_t* __restrict__ q, int n, int H,
-                                                          int Hq, int W, float scale,
-                                                          float2* __restrict__ pstat) {
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Stage<D>::kWavesPerSimd))) void attn_stats(
+    const uint16_t* __restrict__ k, const uint16_t* __restrict__ q, int n, int H, int Hq, int W, float scale,
+    float2* __restrict__ pstat) {
+  using S = Stage<D>;
   const int lh = blockIdx.x, kb = blockIdx.y, nkb = gridDim.y;
   const int l = lh / H, h = lh % H, G = Hq / H, M = G * W, MT = (M + 31) / 32, Mpad = MT * 32;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, hf = lane >> 5, j = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);  // uniform per wave
+  const int lane = threadIdx.x & 63, hf = lane >> 5, j = lane & 31;
   const uint16_t* kbase = k + static_cast<size_t>(lh) * n * D;
   const uint16_t* qbase = q + (static_cast<size_t>(l) * Hq + static_cast<size_t>(h) * G) * W * D;
   const float alpha = scale * kLog2e;
   const int key0 = kb * kBlockKeys;
+  const int nstages = (min(n - key0, kBlockKeys) + S::kKeys - 1) / S::kKeys;
+  __shared__ __align__(16) uint8_t s_k[S::kBuffers * S::kBytes];
   __shared__ float2 s_stat[kWaves][32];
+  uint32_t raddr[D / 16];
+  lane_addresses<D>(s_k, raddr);
   for (int round = 0; 4 * round < MT; ++round) {
     const WaveRole role = wave_role(MT, round, wave);
-    if (role.active) {
-      half8 qr[D / 16];
-      const int qrow = role.qtile * 32 + j;
-      load_rows<D>(qbase, qrow, qrow < M, qr);
-      float m = -INFINITY, sum = 0.0f;  // m in base-2 units (logit * scale * log2 e)
-      // two tiles per step: the second tile's MFMAs run while the first
-      // tile's exponentials are computed; the next pair is loaded meanwhile
-      const int st = role.nstreams;
-      half8 ka[D / 16], kb2[D / 16];
-      const int i0 = role.stream;
-      load_rows<D>(kbase, key0 + i0 * 32 + j, key0 + i0 * 32 + j < n, ka);
-      if (i0 + st < kTiles) load_rows<D>(kbase, key0 + (i0 + st) * 32 + j, key0 + (i0 + st) * 32 + j < n, kb2);
-      for (int i = i0; i < kTiles && key0 + i * 32 < n; i += 2 * st) {  // wave-uniform bounds
-        const int i1 = i + st;
-        const bool has1 = i1 < kTiles && key0 + i1 * 32 < n;
-        floatx16 a0{}, a1{};
+    // up to kBuffers - 1 later stages are in flight while a stage is
+    // multiplied; the query rows are waited for once, with stage 0, so that
+    // no load of the compiler's own is pending inside the stage loop
+    stage_issue<D>(kbase, key0, n, s_k, wave);
+    half8 qr[D / 16];
+    const int qrow = role.qtile * 32 + j;
+    if (role.active) load_rows<D>(qbase, qrow, qrow < M, qr);
+    wait_loads<0>();
+    for (int st = 1; st < S::kBuffers - 1 && st < nstages; ++st)
+      stage_issue<D>(kbase, key0 + st * S::kKeys, n, s_k + st * S::kBytes, wave);
+    float m = -INFINITY, sum = 0.0f;  // m in base-2 units (logit * scale * log2 e)
+    for (int st0 = 0; st0 < nstages; st0 += S::kBuffers) {
 #pragma unroll
-        for (int s = 0; s < D / 16; ++s) a0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ka[s], qr[s], a0, 0, 0, 0);
-        if (has1) {
+      for (int b = 0; b < S::kBuffers; ++b) {
+        const int st = st0 + b;  // stage st lives in buffer b
+        if (st >= nstages) break;
+        wait_stage<D>(min(S::kBuffers - 2, nstages - 1 - st));  // later stages may still be loading
+        // every thread's pieces of stage st have landed, and every wave is done
+        // with stage st - 1, whose buffer the next issue overwrites
+        lds_barrier();
+        if (st + S::kBuffers - 1 < nstages)
+          stage_issue<D>(kbase, key0 + (st + S::kBuffers - 1) * S::kKeys, n,
+                         s_k + ((b + S::kBuffers - 1) % S::kBuffers) * S::kBytes, wave);
+        if (!role.active) continue;
+        const int ts = key0 + st * S::kKeys;  // first key of the stage
 #pragma unroll
-          for (int s = 0; s < D / 16; ++s) a1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(kb2[s], qr[s], a1, 0, 0, 0);
-        }
-        const int n0 = i + 2 * st, n1 = i + 3 * st;
-        if (n0 < kTiles) load_rows<D>(kbase, key0 + n0 * 32 + j, key0 + n0 * 32 + j < n, ka);
-        if (n1 < kTiles) load_rows<D>(kbase, key0 + n1 * 32 + j, key0 + n1 * 32 + j < n, kb2);
-        const int t0 = key0 + i * 32;
-        if (t0 + 32 <= n) tile_update<false>(a0, alpha, t0, hf, n, m, sum);
-        else tile_update<true>(a0, alpha, t0, hf, n, m, sum);
-        if (has1) {
-          const int t1 = key0 + i1 * 32;
-          if (t1 + 32 <= n) tile_update<false>(a1, alpha, t1, hf, n, m, sum);
-          else tile_update<true>(a1, alpha, t1, hf, n, m, sum);
+        for (int ti = 0; ti < S::kTiles; ++ti) {
+          // this wave's tiles: global tile index = stream (mod nstreams, a power of two)
+          const int t0 = ts + ti * 32;
+          if (((st * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
+          half8 kr[D / 16];
+          stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
+          floatx16 acc{};
+#pragma unroll
+          for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[s], qr[s], acc, 0, 0, 0);
+          if (t0 + 32 <= n) tile_update<false>(acc, alpha, t0, hf, n, m, sum);
+          else tile_update<true>(acc, alpha, t0, hf, n, m, sum);
         }
       }
+    }
+    if (role.active) {
       // the two lane-halves saw different keys of the same query
       lse_merge2(m, sum, __shfl_xor(m, 32), __shfl_xor(sum, 32), 1.0f);
       if (hf == 0) s_stat[wave][j] = float2{m, sum};
@@ -216,69 +365,95 @@ __global__ __launch_bounds__(256) void attn_merge(const float2* __restrict__ pst
 
 // grid (L*H, key blocks); colsum[lh * n + t] = sum over the group's rows of p[row, t].
 // Logits with queries as MFMA rows: a lane holds 16 rows of one key and sums
-// their probabilities; the lane-halves and the waves (query tiles and rounds)
-// are added in fixed order through shared memory.
+// their probabilities, the two lane-halves are added by a shuffle, and the
+// query tiles of a stage are added in tile order from shared memory one stage
+// later (rounds of query tiles add onto the stored sums in round order).
 template <int D>
-__global__ __launch_bounds__(kWaves * 64) void attn_colsum(const uint16_t* __restrict__ k,
-                                                           const uint16_t* __restrict__ q, int n, int H,
-                                                           int Hq, int W, float scale,
-                                                           const float* __restrict__ cstat,
-                                                           float* __restrict__ colsum) {
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Stage<D>::kWavesPerSimd))) void attn_colsum(
+    const uint16_t* __restrict__ k, const uint16_t* __restrict__ q, int n, int H, int Hq, int W, float scale,
+    const float* __restrict__ cstat, float* __restrict__ colsum) {
+  using S = Stage<D>;
   const int lh = blockIdx.x, kb = blockIdx.y;
   const int l = lh / H, h = lh % H, G = Hq / H, M = G * W, MT = (M + 31) / 32, Mpad = MT * 32;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, hf = lane >> 5, j = lane & 31;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);  // uniform per wave
+  const int lane = threadIdx.x & 63, hf = lane >> 5, j = lane & 31;
   const uint16_t* kbase = k + static_cast<size_t>(lh) * n * D;
   const uint16_t* qbase = q + (static_cast<size_t>(l) * Hq + static_cast<size_t>(h) * G) * W * D;
+  float* out = colsum + static_cast<size_t>(lh) * n;
   const float alpha = scale * kLog2e;
   const int key0 = kb * kBlockKeys;
-  __shared__ float s_col[kWaves][kBlockKeys];
-  for (int idx = threadIdx.x; idx < kWaves * kBlockKeys; idx += kWaves * 64) (&s_col[0][0])[idx] = 0.0f;
-  __syncthreads();
+  const int nstages = (min(n - key0, kBlockKeys) + S::kKeys - 1) / S::kKeys;
+  __shared__ __align__(16) uint8_t s_k[S::kBuffers * S::kBytes];
+  __shared__ float s_part[2][kWaves][S::kKeys];  // per stage (double-buffered), per wave, per key
+  uint32_t raddr[D / 16];
+  lane_addresses<D>(s_k, raddr);
   for (int round = 0; 4 * round < MT; ++round) {
     const WaveRole role = wave_role(MT, round, wave);
-    if (!role.active) continue;
+    stage_issue<D>(kbase, key0, n, s_k, wave);
     half8 qr[D / 16];
-    const int qrow = role.qtile * 32 + j;
-    load_rows<D>(qbase, qrow, qrow < M, qr);
     float beta[16];  // c * log2(e) of the lane's 16 rows; +inf for padding rows
+    if (role.active) {
+      const int qrow = role.qtile * 32 + j;
+      load_rows<D>(qbase, qrow, qrow < M, qr);
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      beta[r] = cstat[static_cast<size_t>(lh) * Mpad + role.qtile * 32 + acc_row(r, hf)] * kLog2e;
-    // sum over the lane's 16 rows of p = 2^(acc * alpha - beta), then over both lane-halves
-    auto colsum_tile = [&](const floatx16& acc, int i) {
-      float e[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) e[r] = exp2_fast(__builtin_fmaf(acc[r], alpha, -beta[r]));
-      float p = tree_sum<16>(e);
-      p += __shfl_xor(p, 32);  // the other lane-half holds the other 16 rows
-      if (hf == 0) s_col[wave][i * 32 + j] += p;
-    };
-    const int st = role.nstreams;
-    half8 ka[D / 16], kb2[D / 16];
-    const int i0 = role.stream;
-    load_rows<D>(kbase, key0 + i0 * 32 + j, key0 + i0 * 32 + j < n, ka);
-    if (i0 + st < kTiles) load_rows<D>(kbase, key0 + (i0 + st) * 32 + j, key0 + (i0 + st) * 32 + j < n, kb2);
-    for (int i = i0; i < kTiles && key0 + i * 32 < n; i += 2 * st) {  // wave-uniform bounds
-      const int i1 = i + st;
-      const bool has1 = i1 < kTiles && key0 + i1 * 32 < n;
-      floatx16 a0{}, a1{};
-#pragma unroll
-      for (int s = 0; s < D / 16; ++s) a0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[s], ka[s], a0, 0, 0, 0);
-      if (has1) {
-#pragma unroll
-        for (int s = 0; s < D / 16; ++s) a1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[s], kb2[s], a1, 0, 0, 0);
-      }
-      const int n0 = i + 2 * st, n1 = i + 3 * st;
-      if (n0 < kTiles) load_rows<D>(kbase, key0 + n0 * 32 + j, key0 + n0 * 32 + j < n, ka);
-      if (n1 < kTiles) load_rows<D>(kbase, key0 + n1 * 32 + j, key0 + n1 * 32 + j < n, kb2);
-      colsum_tile(a0, i);
-      if (has1) colsum_tile(a1, i1);
+      for (int r = 0; r < 16; ++r)
+        beta[r] = cstat[static_cast<size_t>(lh) * Mpad + role.qtile * 32 + acc_row(r, hf)] * kLog2e;
     }
-  }
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < kBlockKeys; idx += kWaves * 64) {
-    const int t = key0 + idx;
-    if (t < n) colsum[static_cast<size_t>(lh) * n + t] = ((s_col[0][idx] + s_col[1][idx]) + s_col[2][idx]) + s_col[3][idx];
+    // adds the query tiles' partial sums of stage st (tile order) onto the
+    // stored sums (round order); thread i owns key i of every stage
+    auto flush = [&](int st) {
+      const int i = threadIdx.x;
+      const int t = key0 + st * S::kKeys + i;
+      if (i < S::kKeys && t < n) {
+        const int stream = (st * S::kTiles + i / 32) & (role.nstreams - 1);
+        float v = s_part[st & 1][stream * role.qg][i];
+        for (int qt = 1; qt < role.qg; ++qt) v += s_part[st & 1][stream * role.qg + qt][i];
+        out[t] = round == 0 ? v : out[t] + v;
+      }
+    };
+    // the query rows and row constants are waited for once, with stage 0;
+    // up to kBuffers - 1 later stages are in flight while a stage is multiplied
+    wait_loads<0>();
+    for (int st = 1; st < S::kBuffers - 1 && st < nstages; ++st)
+      stage_issue<D>(kbase, key0 + st * S::kKeys, n, s_k + st * S::kBytes, wave);
+    for (int st0 = 0; st0 < nstages; st0 += S::kBuffers) {
+#pragma unroll
+      for (int b = 0; b < S::kBuffers; ++b) {
+        const int st = st0 + b;  // stage st lives in buffer b
+        if (st >= nstages) break;
+        wait_stage<D>(min(S::kBuffers - 2, nstages - 1 - st));  // later stages may still be loading
+        // stage st has landed everywhere; every wave is done with stage st - 1
+        // (its buffer is reloaded next) and has written its partial sums
+        lds_barrier();
+        if (st + S::kBuffers - 1 < nstages)
+          stage_issue<D>(kbase, key0 + (st + S::kBuffers - 1) * S::kKeys, n,
+                         s_k + ((b + S::kBuffers - 1) % S::kBuffers) * S::kBytes, wave);
+        if (st > 0) flush(st - 1);
+        if (!role.active) continue;
+        float* part = s_part[st & 1][wave];
+        const int ts = key0 + st * S::kKeys;
+#pragma unroll
+        for (int ti = 0; ti < S::kTiles; ++ti) {
+          const int t0 = ts + ti * 32;
+          if (((st * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
+          half8 kr[D / 16];
+          stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
+          floatx16 acc{};
+#pragma unroll
+          for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[s], kr[s], acc, 0, 0, 0);
+          // sum over the lane's 16 rows of p = 2^(acc * alpha - beta), then over both lane-halves
+          float e[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) e[r] = exp2_fast(__builtin_fmaf(acc[r], alpha, -beta[r]));
+          float p = tree_sum<16>(e);
+          p += __shfl_xor(p, 32);  // the other lane-half holds the other 16 rows
+          if (hf == 0) part[ti * 32 + j] = p;
+        }
+      }
+    }
+    lds_barrier();
+    flush(nstages - 1);
+    __syncthreads();  // the next round's first loads overwrite the first stage buffers
   }
 }
 

@@ -22,6 +22,8 @@ CASES = [
     (1, 1, 2, 40, 256, 1000, 0.3, 2),    # 80 rows: three tiles in two register groups
     (2, 4, 4, 1, 32, 33, 0.6, 3),        # one query row per group, 33 keys
     (3, 2, 8, 16, 128, 2500, 0.5, 3),    # 64 rows, several key blocks
+    (1, 1, 8, 20, 128, 3100, 0.5, 3),    # 160 rows: a second round of query tiles, ragged last block
+    (1, 2, 6, 3, 32, 2100, 0.5, 3),      # 9 rows: four key streams over eight-tile stages
 ]
 
 
