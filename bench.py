@@ -5,7 +5,12 @@ assign tiers -> pack -> emulated link (device-to-device copy of the payload)
 -> unpack into the paged fp16 cache.  Inputs are resident in HBM before the
 timed region.  The reported metric is the paper-shaped codec throughput:
 fp16-equivalent bytes F = 4 L H d n per (pack + unpack) second.  Per-stage
-times come from HIP events recorded on the stream the library launches on.
+times come from HIP events recorded on the stream the library launches on;
+before each stage a 1 GiB write evicts the 256 MB Infinity Cache (outside the
+events; --no-flush skips it).  The line also carries the p10/p50/p90 of the
+per-step pack + unpack time, a same-process device copy of F bytes as the
+achievable-bandwidth reference, and the oracle's host rate on one thread and
+on every host thread (cpu_baseline).
 
 Prints one JSON line (see the keys below); with --gpus N > 1 it exits with a
 message, since the codec is measured on one GPU.
@@ -65,34 +70,79 @@ def algorithmic_bytes(w, plan, payload_bytes, block_size):
     return pack, unpack
 
 
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
+
+
+def _host_threads(cap=16):
+    """Host cores this process may use, capped at the per-GPU share of the box."""
+    try:
+        return max(1, min(cap, len(os.sched_getaffinity(0))))
+    except AttributeError:
+        return max(1, min(cap, os.cpu_count() or 1))
+
+
 def cpu_baseline(w, layers: int):
-    """The oracle's pack + unpack, single-threaded, on the first `layers` layers
-    of the same request shape; GB/s of fp16-equivalent input like the metric."""
+    """The oracle's pack + unpack on the host, as it stands: single-threaded on
+    the first `layers` layers of the same request shape, then one oracle call
+    per layer on every host thread at once (one layer each; the C oracle runs
+    without the GIL).  GB/s of fp16-equivalent input like the metric; `value`
+    is the all-thread rate, `cores` the threads it used."""
+    import concurrent.futures
+
     import numpy as np
 
     import oracle
     from paper_2606_08635_amd import workloads
 
     n, H, d, bs = w.tokens, w.kv_heads, w.head_dim, 16
-    k, v = workloads.make_kv(layers, H, n, d, seed=0, outliers=w.outliers, device="cuda")
+    threads = _host_threads()
+    nl = max(layers, threads)
+    k, v = workloads.make_kv(nl, H, n, d, seed=0, outliers=w.outliers, device="cuda")
     kh, vh = k.cpu().numpy().view(np.uint16), v.cpu().numpy().view(np.uint16)
-    ocfg = oracle.config(layers, H, d, n, w.budget, first_ratio=w.first_ratio, decay=w.decay,
-                         num_tiers=w.num_tiers)
-    tier = oracle.assign(ocfg, oracle.score(ocfg, kh, vh))
+    del k, v
+    kw = dict(first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers)
+    ocfg = oracle.config(layers, H, d, n, w.budget, **kw)
+    tier = oracle.assign(ocfg, oracle.score(ocfg, kh[:layers], vh[:layers]))
     nb = workloads.blocks_for(n, bs)
     bt = workloads.make_block_table(n, bs, nb, seed=0).numpy()
     kc = np.zeros((layers, nb, bs, H, d), np.uint16)
     vc = np.zeros_like(kc)
     t0 = time.perf_counter()
-    payload = oracle.pack(ocfg, kh, vh, tier)
+    payload = oracle.pack(ocfg, kh[:layers], vh[:layers], tier)
     t1 = time.perf_counter()
     st = oracle.unpack(ocfg, payload, kc, vc, bt, bs)
     t2 = time.perf_counter()
     assert st == oracle.OK
-    f16 = 4 * layers * H * d * n
-    return {"value": round(f16 / (t2 - t0) / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{layers} of {w.layers} layers of the {w.name} request ({f16 / 2**20:.0f} MiB fp16 K+V); "
-                      f"pack {t1 - t0:.2f} s, unpack {t2 - t1:.2f} s, single thread"}
+    single = 4 * layers * H * d * n / (t2 - t0) / 1e9
+    del payload, kc, vc
+
+    cfg1 = oracle.config(1, H, d, n, w.budget, **kw)
+
+    def one_layer(l):
+        kc1 = np.zeros((1, nb, bs, H, d), np.uint16)
+        vc1 = np.zeros_like(kc1)
+        pay = oracle.pack(cfg1, kh[l:l + 1], vh[l:l + 1], tier)
+        return oracle.unpack(cfg1, pay, kc1, vc1, bt, bs)
+
+    with concurrent.futures.ThreadPoolExecutor(threads) as ex:
+        t3 = time.perf_counter()
+        codes = list(ex.map(one_layer, range(threads)))
+        t4 = time.perf_counter()
+    assert all(c == oracle.OK for c in codes)
+    multi = 4 * threads * H * d * n / (t4 - t3) / 1e9
+    return {"value": round(multi, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "single_thread_value": round(single, 4),
+            "sample": f"{w.name} request shape ({H} KV heads x {d} dim x {n} tokens per layer) on {_cpu_model()}: "
+                      f"{layers} layers on one thread (pack {t1 - t0:.2f} s, unpack {t2 - t1:.2f} s), then "
+                      f"{threads} layers, one per thread on {threads} threads ({t4 - t3:.2f} s)"}
 
 
 def _events(count):
@@ -420,6 +470,8 @@ def main():
     ap.add_argument("--score", choices=["kvnorm", "attn"], default="kvnorm",
                     help="importance statistic; attn uses a W-query observation window per query head")
     ap.add_argument("--obs-window", type=int, default=32)
+    ap.add_argument("--no-flush", dest="flush_cache", action="store_false",
+                    help="do not evict the Infinity Cache (1 GiB write) before each stage")
     ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade", "groups", "quant"], default="step",
                     help="step: the headline codec step; batch: per-request vs batched launches over "
                          "a multi-request workload; pipeline: layer-pipelined handoff latency; "
@@ -486,23 +538,28 @@ def main():
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
+    # A 1 GiB write between stages evicts the 256 MB Infinity Cache, so no stage
+    # reads what the previous one left there; it runs outside the stage events.
+    flush_buf = torch.empty(1 << 30, dtype=torch.uint8, device=dev) if args.flush_cache else None
+    names = ["score", "assign", "pack", "link", "unpack"]
+
     def step(ev=None):
-        if ev: ev[0].record(stream)
-        skv.score(cfg, k, v, q_obs, codec.scores, codec.ws)
-        if ev: ev[1].record(stream)
-        skv.assign_tiers(cfg, codec.scores, codec.tier)
-        if ev: ev[2].record(stream)
-        skv.pack(cfg, k, v, codec.tier, codec.payload, codec.status[0:1])
-        if ev: ev[3].record(stream)
-        skv.link(rx, codec.payload, codec.payload_bytes, staging)
-        if ev: ev[4].record(stream)
-        skv.unpack(cfg, rx, kc, vc, bt, bs, codec.status[1:2])
-        if ev: ev[5].record(stream)
+        calls = [lambda: skv.score(cfg, k, v, q_obs, codec.scores, codec.ws),
+                 lambda: skv.assign_tiers(cfg, codec.scores, codec.tier),
+                 lambda: skv.pack(cfg, k, v, codec.tier, codec.payload, codec.status[0:1]),
+                 lambda: skv.link(rx, codec.payload, codec.payload_bytes, staging),
+                 lambda: skv.unpack(cfg, rx, kc, vc, bt, bs, codec.status[1:2])]
+        for i, call in enumerate(calls):
+            if flush_buf is not None:
+                flush_buf.fill_(i)
+            if ev: ev[2 * i].record(stream)
+            call()
+            if ev: ev[2 * i + 1].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * len(names))] for _ in range(args.steps)]
     t0 = time.perf_counter()
     for i in range(args.steps):
         step(events[i])
@@ -512,8 +569,24 @@ def main():
     if status != [0, 0]:
         raise RuntimeError(f"codec reported status {status}")
 
-    names = ["score", "assign", "pack", "link", "unpack"]
-    stage_ms = {nm: sum(e[i].elapsed_time(e[i + 1]) for e in events) / args.steps for i, nm in enumerate(names)}
+    per_step = [{nm: e[2 * i].elapsed_time(e[2 * i + 1]) for i, nm in enumerate(names)} for e in events]
+    codec_ms = sorted(p["pack"] + p["unpack"] for p in per_step)
+
+    def pct(q):
+        return codec_ms[min(len(codec_ms) - 1, int(q * (len(codec_ms) - 1) + 0.5))]
+
+    # achievable-bandwidth reference in the same process: a runtime copy of the
+    # F bytes of K and V into the cache buffers (F read + F written)
+    ce = _events(2)
+    ce[0].record(stream)
+    for _ in range(3):
+        skv.link(kc, k, k.numel() * 2)
+        skv.link(vc, v, v.numel() * 2)
+    ce[1].record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 3 * 2 * w.fp16_bytes / (ce[0].elapsed_time(ce[1]) / 1e3) / 1e9
+
+    stage_ms = {nm: sum(p[nm] for p in per_step) / args.steps for nm in names}
     F = w.fp16_bytes
     t_codec = (stage_ms["pack"] + stage_ms["unpack"]) / 1e3
     pack_b, unpack_b = algorithmic_bytes(w, codec.plan, codec.payload_bytes, bs)
@@ -543,6 +616,11 @@ def main():
         "alg_gbps": round(alg_gbs, 2),
         "pct_hbm_peak": round(100 * alg_gbs / HBM_PEAK_GBS, 2),
         "stages_ms": {kk: round(vv, 4) for kk, vv in stage_ms.items()},
+        "codec_ms": {"mean": round(t_codec * 1e3, 4), "p10": round(pct(0.1), 4), "p50": round(pct(0.5), 4),
+                     "p90": round(pct(0.9), 4)},
+        "hot_path_ms_per_step": round(sum(stage_ms.values()), 4),
+        "cache_flushed": bool(args.flush_cache),
+        "copy_ref_gbps": round(copy_gbs, 2),
         "pack_gbps": round(pack_gbs, 2),
         "unpack_gbps": round(unpack_gbs, 2),
         "roofline": {"bound": "hbm", "kernel": f"skv_{dominant}", "achieved": round(dom_gbs, 2),
@@ -560,7 +638,7 @@ def main():
         out["score_kvnorm"] = {"ms": round(stage_ms["score"], 4),
                                "read_gbps": round(F / (stage_ms["score"] / 1e3) / 1e9, 2)}
     if args.cpu_layers > 0:
-        del kc, vc, rx
+        del kc, vc, rx, flush_buf
         torch.cuda.empty_cache()
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers)
     print(json.dumps(out), flush=True)
