@@ -20,7 +20,7 @@ OK, ERR_INVALID_ARG, ERR_BUDGET, ERR_CAPACITY, ERR_FORMAT = 0, 1, 2, 3, 4
 FP16, INT8, INT4, DROP = 0, 1, 2, 3
 KVNORM, ATTN, RECENCY = 0, 1, 2
 # quantizer variant descriptor bits: group size (0 row, 1: 64, 2: 32), asymmetric, binary16 metadata
-QUANT_GROUP64, QUANT_GROUP32, QUANT_ASYM, QUANT_FP16 = 1, 2, 4, 8
+QUANT_GROUP64, QUANT_GROUP32, QUANT_ASYM, QUANT_FP16, QUANT_CHANNEL = 1, 2, 4, 8, 16
 GRAN_TOKEN, GRAN_LAYER, GRAN_HEAD = 0, 1, 2
 CHUNK_TOKENS = 256
 
@@ -258,7 +258,8 @@ def pack(cfg, k, v, tier):
 
 
 GEOMETRY_FIELDS = ("tiermap_off", "chunkidx_off", "layers_off", "seg_bytes", "seg_stride",
-                   "scales_bytes", "layer_stride", "total", "nq", "seg_scale_bytes")
+                   "scales_bytes", "layer_stride", "total", "nq", "seg_scale_bytes",
+                   "seg_scale_bytes_k", "chan_block", "channel_bytes")
 
 
 def geometry(cfg):

@@ -128,24 +128,35 @@ static float half_to_float(uint16_t h) { return (float)ora_half_to_double(h); }
 /*             (capped at d);                                                  */
 /*   bit 2     asymmetric: per group minimum lo and scale (max - min)/M, codes */
 /*             0..M (M = 255 or 15), instead of symmetric absmax codes -Q..Q;  */
-/*   bit 3     group scale (and minimum) stored as binary16 instead of fp32.   */
+/*   bit 3     group scale (and minimum) stored as binary16 instead of fp32;   */
+/*   bit 4     per-channel key scales (KIVI-style key quantization, Sec. 8 and */
+/*             Sec. 10): the K rows of the tier inside each 256-token chunk    */
+/*             form one group per channel (the chunk's rows of that tier, one  */
+/*             element each), quantized with bits 2-3; V rows keep the        */
+/*             per-row groups of bits 0-3.                                     */
 /* Descriptor 0 is the row-wise symmetric quantizer with fp32 scales used      */
 /* everywhere else in this file.                                               */
 /* ------------------------------------------------------------------------ */
 
-enum { QV_ASYM = 4, QV_FP16 = 8 };
+enum { QV_ASYM = 4, QV_FP16 = 8, QV_CHANNEL = 16 };
 
-static int qv_valid(int32_t q) { return (q & ~15) == 0 && (q & 3) != 3; }
+static int qv_valid(int32_t q) { return (q & ~31) == 0 && (q & 3) != 3; }
 
 static int32_t qv_group(int32_t q, int32_t d) {
   int32_t g = (q & 3) == 0 ? d : (q & 3) == 1 ? 64 : 32;
   return g < d ? g : d;
 }
 
-/* Metadata bytes of one quantized row under descriptor q. */
+/* Bytes of one group's metadata (s, then lo if asymmetric). */
+static uint64_t qv_group_entry(int32_t q) { return ((q & QV_ASYM) ? 2u : 1u) * ((q & QV_FP16) ? 2u : 4u); }
+
+/* Per-row metadata bytes of one quantized row under descriptor q (the row's
+ * groups); K rows of a per-channel tier carry none (is_k). */
 static uint64_t qv_entry_bytes(int32_t q, int32_t d) {
-  uint64_t groups = (uint64_t)(d / qv_group(q, d));
-  return groups * ((q & QV_ASYM) ? 2u : 1u) * ((q & QV_FP16) ? 2u : 4u);
+  return (uint64_t)(d / qv_group(q, d)) * qv_group_entry(q);
+}
+static uint64_t qv_row_bytes(int32_t q, int32_t d, int is_k) {
+  return (is_k && (q & QV_CHANNEL)) ? 0u : qv_entry_bytes(q, d);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -222,18 +233,28 @@ typedef struct {
   uint64_t tiermap_off, chunkidx_off, layers_off;
   uint64_t seg_bytes, seg_stride, scales_bytes, layer_stride, total;
   int64_t nq, nchunks;
-  uint64_t e8, e4;          /* metadata bytes of an INT8 / INT4 row */
-  uint64_t seg_scale_bytes; /* metadata bytes of one segment: n8 e8 + n4 e4 */
-  uint64_t cidx_entry;      /* chunk-index entry bytes: 8 (both descriptors 0) or 16 */
+  uint64_t e8, e4;            /* per-row metadata bytes of a V row (INT8 / INT4) */
+  uint64_t ek8, ek4;          /* the same for a K row (0 for a per-channel tier) */
+  uint64_t seg_scale_bytes;   /* per-row metadata of one V segment: n8 e8 + n4 e4 */
+  uint64_t seg_scale_bytes_k; /* the same for a K segment: n8 ek8 + n4 ek4 */
+  uint64_t chan_block;        /* per-channel parameters of one (head, chunk) */
+  uint64_t channel_bytes;     /* the layer's per-channel area (256-aligned) */
+  uint64_t cidx_entry;        /* chunk-index entry bytes: 8 (both descriptors 0) or 16 */
 } ora_geom;
 
 static void geometry(const ora_config* c, const ora_plan_t* p, ora_geom* g) {
   uint64_t n = (uint64_t)c->num_tokens, d = (uint64_t)c->head_dim, H = (uint64_t)c->num_kv_heads;
   g->nq = p->n_int8 + p->n_int4;
   g->nchunks = (int64_t)((n + ORA_CHUNK - 1) / ORA_CHUNK);
-  g->e8 = qv_entry_bytes(c->quant_int8, (int32_t)d);
-  g->e4 = qv_entry_bytes(c->quant_int4, (int32_t)d);
+  g->e8 = qv_row_bytes(c->quant_int8, (int32_t)d, 0);
+  g->e4 = qv_row_bytes(c->quant_int4, (int32_t)d, 0);
+  g->ek8 = qv_row_bytes(c->quant_int8, (int32_t)d, 1);
+  g->ek4 = qv_row_bytes(c->quant_int4, (int32_t)d, 1);
   g->seg_scale_bytes = (uint64_t)p->n_int8 * g->e8 + (uint64_t)p->n_int4 * g->e4;
+  g->seg_scale_bytes_k = (uint64_t)p->n_int8 * g->ek8 + (uint64_t)p->n_int4 * g->ek4;
+  g->chan_block = ((c->quant_int8 & QV_CHANNEL) ? d * qv_group_entry(c->quant_int8) : 0u) +
+                  ((c->quant_int4 & QV_CHANNEL) ? d * qv_group_entry(c->quant_int4) : 0u);
+  g->channel_bytes = up256(H * (uint64_t)g->nchunks * g->chan_block);
   g->cidx_entry = (c->quant_int8 || c->quant_int4) ? 16u : 8u;
   g->tiermap_off = 256;
   g->chunkidx_off = g->tiermap_off + up256((n + 3) / 4);
@@ -241,8 +262,8 @@ static void geometry(const ora_config* c, const ora_plan_t* p, ora_geom* g) {
   g->seg_bytes = (uint64_t)(p->n_sink + p->n_fp16) * 2 * d + (uint64_t)p->n_int8 * d +
                  (uint64_t)p->n_int4 * (d / 2);
   g->seg_stride = up256(g->seg_bytes);
-  g->scales_bytes = up256(2 * H * g->seg_scale_bytes);
-  g->layer_stride = g->scales_bytes + 2 * H * g->seg_stride;
+  g->scales_bytes = up256(H * (g->seg_scale_bytes_k + g->seg_scale_bytes));
+  g->layer_stride = g->scales_bytes + g->channel_bytes + 2 * H * g->seg_stride;
   g->total = g->layers_off + (uint64_t)c->num_layers * g->layer_stride;
 }
 
@@ -518,8 +539,9 @@ static uint32_t order_key(uint16_t h) { return (h & 0x8000u) ? (uint32_t)(~h & 0
 static void put16(uint8_t* p, uint16_t v) { memcpy(p, &v, 2); }
 static uint16_t get16(const uint8_t* p) { uint16_t v; memcpy(&v, p, 2); return v; }
 
-/* Row quantizer under variant descriptor q (see the variant section above).
- * Per group of gs elements:
+/* One quantization group under descriptor q's bits 2-3 (tier tr): the cnt
+ * binary16 values x[0], x[stride], ...  Writes the codes to codes[0..cnt) and
+ * the group's metadata (s, then lo if asymmetric; fp32 or binary16) at m.
  *   symmetric: a = max |x|; a non-finite element gives a NaN scale and zero
  *     codes, a = 0 a zero scale and zero codes; otherwise with an fp32 scale
  *     s = RN32(a/Q), r = RN32(Q/a), and with a binary16 scale s = RN16(RN32(a/Q))
@@ -530,110 +552,137 @@ static uint16_t get16(const uint8_t* p) { uint16_t v; memcpy(&v, p, 2); return v
  *     a zero scale and zero codes; otherwise s = RN32(range/M) (binary16: RN16
  *     of that, zero codes on underflow), r = RN32(M/range) (binary16:
  *     RN32(1/s)); code = clamp(rne(RN32(RN32(x - lo) r)), 0, M).
- * Codes are stored as for descriptor 0 (signed byte / nibble), asymmetric codes
- * as unsigned byte / nibble.  Metadata per group: s, then lo if asymmetric,
- * each fp32 or binary16.  Returns 1 if a group held a non-finite element.
- * Descriptor 0 is ora_encode_row with its fp32 scale in the metadata. */
-int ora_encode_row_q(int tr, int32_t q, int32_t d, const uint16_t* x, uint8_t* out, uint8_t* meta) {
-  if (tr == T_FP16 || tr == T_DROP || q == 0) {
-    float scale = 0.0f;
-    int bad = ora_encode_row(tr, d, x, out, &scale);
-    if (tr == T_INT8 || tr == T_INT4) put32(meta, fbits(scale));
-    return bad;
-  }
+ * Returns 1 if the group held a non-finite element. */
+static int quant_group(int tr, int32_t q, const uint16_t* x, int64_t stride, int64_t cnt, int32_t* codes,
+                       uint8_t* m) {
   const int asym = (q & QV_ASYM) != 0, f16 = (q & QV_FP16) != 0;
-  const int32_t gs = qv_group(q, d);
   const int Q = tr == T_INT8 ? 127 : 7, M = tr == T_INT8 ? 255 : 15;
-  const uint64_t eb = f16 ? 2u : 4u;
-  int32_t codes[256];
-  int bad_any = 0;
-  for (int32_t g0 = 0; g0 < d; g0 += gs) {
-    uint8_t* m = meta + (uint64_t)(g0 / gs) * (asym ? 2u : 1u) * eb;
-    int bad = 0;
-    uint16_t amax = 0, lo = x[g0], hi = x[g0];
-    for (int32_t i = g0; i < g0 + gs; ++i) {
-      if ((x[i] & 0x7C00u) == 0x7C00u) bad = 1;
-      if ((x[i] & 0x7FFFu) > amax) amax = x[i] & 0x7FFFu;
-      if (order_key(x[i]) < order_key(lo)) lo = x[i];
-      if (order_key(x[i]) > order_key(hi)) hi = x[i];
-    }
-    float scale = 0.0f, r = 0.0f, lof = 0.0f;
-    uint16_t s16 = 0;
-    int zero = 0;
-    if (bad) {
-      uint32_t nanbits = 0x7FC00000u;
-      memcpy(&scale, &nanbits, 4);
-      memcpy(&lof, &nanbits, 4);
-      s16 = 0x7E00;
+  int bad = 0;
+  uint16_t amax = 0, lo = x[0], hi = x[0];
+  for (int64_t i = 0; i < cnt; ++i) {
+    uint16_t v = x[i * stride];
+    if ((v & 0x7C00u) == 0x7C00u) bad = 1;
+    if ((v & 0x7FFFu) > amax) amax = v & 0x7FFFu;
+    if (order_key(v) < order_key(lo)) lo = v;
+    if (order_key(v) > order_key(hi)) hi = v;
+  }
+  float scale = 0.0f, r = 0.0f, lof = 0.0f;
+  uint16_t s16 = 0;
+  int zero = 0;
+  if (bad) {
+    uint32_t nanbits = 0x7FC00000u;
+    memcpy(&scale, &nanbits, 4);
+    memcpy(&lof, &nanbits, 4);
+    s16 = 0x7E00;
+    zero = 1;
+  } else if (!asym) {
+    if (amax == 0) {
       zero = 1;
-      bad_any = 1;
-    } else if (!asym) {
-      if (amax == 0) {
-        zero = 1;
-      } else {
-        float a = half_to_float(amax);
-        scale = a / (float)Q;
-        if (f16) {
-          s16 = ora_float_to_half(scale);
-          scale = half_to_float(s16);
-          if (s16 == 0) zero = 1;
-          else r = 1.0f / scale;
-        } else {
-          r = (float)Q / a;
-        }
-      }
     } else {
-      lof = half_to_float(lo);
-      float range = half_to_float(hi) - lof;
-      if (range == 0.0f) {
-        zero = 1;
+      float a = half_to_float(amax);
+      scale = a / (float)Q;
+      if (f16) {
+        s16 = ora_float_to_half(scale);
+        scale = half_to_float(s16);
+        if (s16 == 0) zero = 1;
+        else r = 1.0f / scale;
       } else {
-        scale = range / (float)M;
-        if (f16) {
-          s16 = ora_float_to_half(scale);
-          scale = half_to_float(s16);
-          if (s16 == 0) zero = 1;
-          else r = 1.0f / scale;
-        } else {
-          r = (float)M / range;
-        }
+        r = (float)Q / a;
       }
     }
-    for (int32_t i = g0; i < g0 + gs; ++i) {
-      if (zero) { codes[i] = 0; continue; }
-      float c;
-      if (!asym) {
-        c = nearbyintf(half_to_float(x[i]) * r);
-        if (c > (float)Q) c = (float)Q;
-        if (c < (float)-Q) c = (float)-Q;
-      } else {
-        float dlt = half_to_float(x[i]) - lof;
-        c = nearbyintf(dlt * r);
-        if (c > (float)M) c = (float)M;
-        if (c < 0.0f) c = 0.0f;
-      }
-      codes[i] = (int32_t)c;
-    }
-    if (f16) {
-      put16(m, bad ? (uint16_t)0x7E00 : s16);
-      if (asym) put16(m + 2, bad ? (uint16_t)0x7E00 : lo);
+  } else {
+    lof = half_to_float(lo);
+    float range = half_to_float(hi) - lof;
+    if (range == 0.0f) {
+      zero = 1;
     } else {
-      put32(m, fbits(scale));
-      if (asym) put32(m + 4, fbits(lof));
+      scale = range / (float)M;
+      if (f16) {
+        s16 = ora_float_to_half(scale);
+        scale = half_to_float(s16);
+        if (s16 == 0) zero = 1;
+        else r = 1.0f / scale;
+      } else {
+        r = (float)M / range;
+      }
     }
   }
+  for (int64_t i = 0; i < cnt; ++i) {
+    if (zero) { codes[i] = 0; continue; }
+    float c, xv = half_to_float(x[i * stride]);
+    if (!asym) {
+      c = nearbyintf(xv * r);
+      if (c > (float)Q) c = (float)Q;
+      if (c < (float)-Q) c = (float)-Q;
+    } else {
+      float dlt = xv - lof;
+      c = nearbyintf(dlt * r);
+      if (c > (float)M) c = (float)M;
+      if (c < 0.0f) c = 0.0f;
+    }
+    codes[i] = (int32_t)c;
+  }
+  if (f16) {
+    put16(m, bad ? (uint16_t)0x7E00 : s16);
+    if (asym) put16(m + 2, bad ? (uint16_t)0x7E00 : lo);
+  } else {
+    put32(m, fbits(scale));
+    if (asym) put32(m + 4, fbits(lof));
+  }
+  return bad;
+}
+
+/* Stores d codes of tier tr: a byte each (INT8), or two nibbles per byte,
+ * even element in the low nibble (INT4). */
+static void store_codes(int tr, int32_t d, const int32_t* codes, uint8_t* out) {
   if (tr == T_INT8) {
     for (int32_t i = 0; i < d; ++i) out[i] = (uint8_t)(codes[i] & 0xFF);
   } else {
     for (int32_t i = 0; i < d / 2; ++i)
       out[i] = (uint8_t)((codes[2 * i] & 0xF) | ((codes[2 * i + 1] & 0xF) << 4));
   }
+}
+
+/* Row quantizer under variant descriptor q (see the variant section above):
+ * the row's groups of qv_group(q, d) elements, each by quant_group.  Codes are
+ * stored as for descriptor 0 (signed byte / nibble), asymmetric codes as
+ * unsigned byte / nibble.  Metadata: per group s, then lo if asymmetric.
+ * Returns 1 if a group held a non-finite element.  Descriptor 0 is
+ * ora_encode_row with its fp32 scale in the metadata.  Bit 4 (per-channel K)
+ * does not enter a row's own quantization. */
+int ora_encode_row_q(int tr, int32_t q, int32_t d, const uint16_t* x, uint8_t* out, uint8_t* meta) {
+  q &= ~QV_CHANNEL;
+  if (tr == T_FP16 || tr == T_DROP || q == 0) {
+    float scale = 0.0f;
+    int bad = ora_encode_row(tr, d, x, out, &scale);
+    if (tr == T_INT8 || tr == T_INT4) put32(meta, fbits(scale));
+    return bad;
+  }
+  const int32_t gs = qv_group(q, d);
+  int32_t codes[256];
+  int bad_any = 0;
+  for (int32_t g0 = 0; g0 < d; g0 += gs)
+    bad_any |= quant_group(tr, q, x + g0, 1, gs, codes + g0, meta + (uint64_t)(g0 / gs) * qv_group_entry(q));
+  store_codes(tr, d, codes, out);
   return bad_any;
 }
 
-/* Inverse of ora_encode_row_q: per group, a NaN scale gives 0x7E00;
- * symmetric x^ = RN16(RN32(code s)); asymmetric x^ = RN16(RN32(RN32(code s) + lo)). */
+/* Decodes one code of tier tr under descriptor bits 2 (asymmetric) with the
+ * group's s and lo: a NaN s gives 0x7E00; symmetric x^ = RN16(RN32(code s));
+ * asymmetric x^ = RN16(RN32(RN32(code s) + lo)).  raw is the stored byte
+ * (INT8) or nibble (INT4). */
+static uint16_t decode_code(int tr, int asym, uint32_t raw, float scale, float lo) {
+  if (isnan(scale)) return 0x7E00;
+  int32_t code = asym ? (int32_t)raw
+                      : tr == T_INT8 ? (int32_t)(int8_t)(uint8_t)raw : ((int32_t)raw >= 8 ? (int32_t)raw - 16 : (int32_t)raw);
+  float v = (float)code * scale;
+  if (asym) v = v + lo;
+  return ora_float_to_half(v);
+}
+
+/* Inverse of ora_encode_row_q: per group, decode_code with the group's s, lo. */
 void ora_decode_row_q(int tr, int32_t q, int32_t d, const uint8_t* in, const uint8_t* meta, uint16_t* y) {
+  q &= ~QV_CHANNEL;
   if (tr == T_FP16 || tr == T_DROP || q == 0) {
     float scale = 0.0f;
     if (tr == T_INT8 || tr == T_INT4) {
@@ -645,9 +694,8 @@ void ora_decode_row_q(int tr, int32_t q, int32_t d, const uint8_t* in, const uin
   }
   const int asym = (q & QV_ASYM) != 0, f16 = (q & QV_FP16) != 0;
   const int32_t gs = qv_group(q, d);
-  const uint64_t eb = f16 ? 2u : 4u;
   for (int32_t g0 = 0; g0 < d; g0 += gs) {
-    const uint8_t* m = meta + (uint64_t)(g0 / gs) * (asym ? 2u : 1u) * eb;
+    const uint8_t* m = meta + (uint64_t)(g0 / gs) * qv_group_entry(q);
     float scale, lo = 0.0f;
     if (f16) {
       scale = half_to_float(get16(m));
@@ -658,12 +706,8 @@ void ora_decode_row_q(int tr, int32_t q, int32_t d, const uint8_t* in, const uin
       if (asym) { b = get32(m + 4); memcpy(&lo, &b, 4); }
     }
     for (int32_t i = g0; i < g0 + gs; ++i) {
-      if (isnan(scale)) { y[i] = 0x7E00; continue; }
-      int32_t nib = tr == T_INT8 ? in[i] : (in[i / 2] >> (4 * (i & 1))) & 0xF;
-      int32_t code = asym ? nib : tr == T_INT8 ? (int32_t)(int8_t)in[i] : (nib >= 8 ? nib - 16 : nib);
-      float v = (float)code * scale;
-      if (asym) v = v + lo;
-      y[i] = ora_float_to_half(v);
+      uint32_t raw = tr == T_INT8 ? in[i] : (uint32_t)(in[i / 2] >> (4 * (i & 1))) & 0xFu;
+      y[i] = decode_code(tr, asym, raw, scale, lo);
     }
   }
 }
@@ -710,36 +754,92 @@ static void write_header(const ora_config* c, const ora_plan_t* p, const ora_geo
   put32(h + 152, ORA_CHUNK);
   put32(h + 156, (uint32_t)c->quant_int8);
   put32(h + 160, (uint32_t)c->quant_int4);
+  put64(h + 168, g->channel_bytes);
 }
 
+static int any_channel(const ora_config* c) { return ((c->quant_int8 | c->quant_int4) & QV_CHANNEL) != 0; }
+
 /* Header, 2-bit tier map and chunk index (the payload bytes before layer 0);
- * also returns the per-token row offsets and scale ranks. */
+ * also returns the per-token row offsets, scale ranks and per-row metadata
+ * offsets of V segments (sbytes) and K segments (sbytes_k). */
 static void write_meta(const ora_config* c, const ora_plan_t* p, const ora_geom* g, const uint8_t* tier,
-                       uint32_t* units, uint32_t* qrank, uint32_t* sbytes, uint8_t* payload) {
+                       uint32_t* units, uint32_t* qrank, uint32_t* sbytes, uint32_t* sbytes_k, uint8_t* payload) {
   int64_t n = c->num_tokens;
   write_header(c, p, g, payload);
   for (int64_t t = 0; t < n; ++t)
     payload[g->tiermap_off + (uint64_t)t / 4] |= (uint8_t)(tier[t] << (2 * (t % 4)));
   ora_offsets((int32_t)n, tier, units, qrank);
   ora_scale_offsets((int32_t)n, tier, g->e8, g->e4, sbytes);
+  ora_scale_offsets((int32_t)n, tier, g->ek8, g->ek4, sbytes_k);
   for (int64_t ch = 0; ch < g->nchunks; ++ch) {
     uint8_t* e = payload + g->chunkidx_off + g->cidx_entry * (uint64_t)ch;
     put32(e, units[ch * ORA_CHUNK]);
     put32(e + 4, qrank[ch * ORA_CHUNK]);
-    if (g->cidx_entry == 16) put32(e + 8, sbytes[ch * ORA_CHUNK]); /* metadata bytes before the chunk */
+    if (g->cidx_entry == 16) {
+      put32(e + 8, sbytes[ch * ORA_CHUNK]); /* V-side metadata bytes before the chunk */
+      put32(e + 12, any_channel(c) ? sbytes_k[ch * ORA_CHUNK] : 0u); /* K side, if it differs */
+    }
   }
 }
 
+/* Per-row metadata of segment (kv, h) within its layer: the H K segments, then
+ * the H V segments. */
+static uint64_t seg_meta_off(const ora_geom* g, int64_t H, int kv, int64_t h) {
+  return kv == 0 ? (uint64_t)h * g->seg_scale_bytes_k
+                 : (uint64_t)H * g->seg_scale_bytes_k + (uint64_t)h * g->seg_scale_bytes;
+}
+
+/* Per-channel parameters of K head h, chunk ch, tier tr within its layer:
+ * after the per-row metadata, one block per (head, chunk), the INT8 entries
+ * (if that tier is per-channel) before the INT4 entries. */
+static uint64_t chan_off(const ora_config* c, const ora_geom* g, int64_t h, int64_t ch, int tr) {
+  uint64_t off = g->scales_bytes + ((uint64_t)h * (uint64_t)g->nchunks + (uint64_t)ch) * g->chan_block;
+  if (tr == T_INT4 && (c->quant_int8 & QV_CHANNEL))
+    off += (uint64_t)c->head_dim * qv_group_entry(c->quant_int8);
+  return off;
+}
+
+/* Per-channel K quantization of chunk [t0, t1) for tier tr (descriptor q with
+ * bit 4): channel i's group is {src[t][i] : t in the chunk, tier[t] == tr},
+ * quantized by quant_group; codes go to each row's data slot, the d group
+ * entries to blk (left zero when the chunk has no row of the tier).  Returns
+ * the number of those rows holding a non-finite element. */
+static uint32_t pack_channel_chunk(int tr, int32_t q, int32_t d, const uint16_t* src, const uint8_t* tier,
+                                   int64_t t0, int64_t t1, const uint32_t* units, uint8_t* seg, uint8_t* blk) {
+  int64_t rows[ORA_CHUNK], cnt = 0;
+  for (int64_t t = t0; t < t1; ++t)
+    if (tier[t] == tr) rows[cnt++] = t;
+  if (cnt == 0) return 0;
+  uint16_t vals[ORA_CHUNK];
+  int32_t codes[ORA_CHUNK];
+  int32_t* rc = (int32_t*)malloc((size_t)cnt * (size_t)d * sizeof(int32_t));
+  for (int32_t i = 0; i < d; ++i) {
+    for (int64_t j = 0; j < cnt; ++j) vals[j] = src[rows[j] * d + i];
+    quant_group(tr, q, vals, 1, cnt, codes, blk + (uint64_t)i * qv_group_entry(q));
+    for (int64_t j = 0; j < cnt; ++j) rc[j * d + i] = codes[j];
+  }
+  uint32_t bad = 0;
+  for (int64_t j = 0; j < cnt; ++j) {
+    store_codes(tr, d, rc + j * d, seg + (uint64_t)units[rows[j]] * ((uint64_t)d / 2));
+    for (int32_t i = 0; i < d; ++i)
+      if ((src[rows[j] * d + i] & 0x7C00u) == 0x7C00u) { ++bad; break; }
+  }
+  free(rc);
+  return bad;
+}
+
 /* Payload geometry: out = {tiermap_off, chunkidx_off, layers_off, seg_bytes,
- * seg_stride, scales_bytes, layer_stride, total, nq, seg_scale_bytes}. */
+ * seg_stride, scales_bytes, layer_stride, total, nq, seg_scale_bytes,
+ * seg_scale_bytes_k, chan_block, channel_bytes}. */
 int ora_geometry(const ora_config* c, uint64_t* out) {
   ora_plan_t p;
   int st = ora_plan(c, &p);
   if (st) return st;
   ora_geom g;
   geometry(c, &p, &g);
-  uint64_t v[10] = {g.tiermap_off, g.chunkidx_off, g.layers_off, g.seg_bytes, g.seg_stride,
-                    g.scales_bytes, g.layer_stride, g.total, (uint64_t)g.nq, g.seg_scale_bytes};
+  uint64_t v[13] = {g.tiermap_off, g.chunkidx_off, g.layers_off, g.seg_bytes, g.seg_stride,
+                    g.scales_bytes, g.layer_stride, g.total, (uint64_t)g.nq, g.seg_scale_bytes,
+                    g.seg_scale_bytes_k, g.chan_block, g.channel_bytes};
   memcpy(out, v, sizeof(v));
   return ORA_OK;
 }
@@ -757,11 +857,13 @@ int ora_pack_meta(const ora_config* c, const uint8_t* tier, uint8_t* out, uint64
   uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* sbytes = (uint32_t*)malloc((size_t)n * 4);
+  uint32_t* sbytes_k = (uint32_t*)malloc((size_t)n * 4);
   memset(out, 0, g.layers_off);
-  write_meta(c, &p, &g, tier, units, qrank, sbytes, out);
+  write_meta(c, &p, &g, tier, units, qrank, sbytes, sbytes_k, out);
   free(units);
   free(qrank);
   free(sbytes);
+  free(sbytes_k);
   return ORA_OK;
 }
 
@@ -788,7 +890,8 @@ int ora_pack(const ora_config* c, const uint16_t* k, const uint16_t* v, const ui
   uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* sbytes = (uint32_t*)malloc((size_t)n * 4);
-  write_meta(c, &p, &g, tier, units, qrank, sbytes, payload);
+  uint32_t* sbytes_k = (uint32_t*)malloc((size_t)n * 4);
+  write_meta(c, &p, &g, tier, units, qrank, sbytes, sbytes_k, payload);
   uint32_t nonfinite = 0;
   uint64_t rowunit = (uint64_t)d / 2;
   for (int64_t l = 0; l < L; ++l) {
@@ -796,19 +899,32 @@ int ora_pack(const ora_config* c, const uint16_t* k, const uint16_t* v, const ui
     for (int kv = 0; kv < 2; ++kv)
       for (int64_t h = 0; h < H; ++h) {
         const uint16_t* src = (kv == 0 ? k : v) + ((l * H + h) * n) * d;
-        uint8_t* seg = lb + g.scales_bytes + (uint64_t)(kv * H + h) * g.seg_stride;
-        uint8_t* sc = lb + (uint64_t)(kv * H + h) * g.seg_scale_bytes;
+        uint8_t* seg = lb + g.scales_bytes + g.channel_bytes + (uint64_t)(kv * H + h) * g.seg_stride;
+        uint8_t* sc = lb + seg_meta_off(&g, H, kv, h);
+        const uint32_t* so = kv == 0 ? sbytes_k : sbytes;
         for (int64_t t = 0; t < n; ++t) {
           int32_t q = tier[t] == T_INT8 ? c->quant_int8 : c->quant_int4;
-          int bad = ora_encode_row_q(tier[t], q, (int32_t)d, src + t * d, seg + units[t] * rowunit, sc + sbytes[t]);
-          if (tier[t] == T_INT8 || tier[t] == T_INT4) nonfinite += (uint32_t)bad;
+          int quant = tier[t] == T_INT8 || tier[t] == T_INT4;
+          if (kv == 0 && quant && (q & QV_CHANNEL)) continue; /* per-channel K rows: per chunk below */
+          int bad = ora_encode_row_q(tier[t], q, (int32_t)d, src + t * d, seg + units[t] * rowunit, sc + so[t]);
+          if (quant) nonfinite += (uint32_t)bad;
         }
+        if (kv == 0)
+          for (int64_t ch = 0; ch < g.nchunks; ++ch)
+            for (int tr = T_INT8; tr <= T_INT4; ++tr) {
+              int32_t q = tr == T_INT8 ? c->quant_int8 : c->quant_int4;
+              if (!(q & QV_CHANNEL)) continue;
+              int64_t t1 = (ch + 1) * ORA_CHUNK < n ? (ch + 1) * ORA_CHUNK : n;
+              nonfinite += pack_channel_chunk(tr, q, (int32_t)d, src, tier, ch * ORA_CHUNK, t1, units, seg,
+                                              lb + chan_off(c, &g, h, ch, tr));
+            }
       }
   }
   put32(payload + 144, nonfinite);
   free(units);
   free(qrank);
   free(sbytes);
+  free(sbytes_k);
   return ORA_OK;
 }
 
@@ -849,19 +965,23 @@ int ora_unpack(const ora_config* c, const uint8_t* payload, uint64_t bytes, uint
   uint32_t* units = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* qrank = (uint32_t*)malloc((size_t)n * 4);
   uint32_t* sbytes = (uint32_t*)malloc((size_t)n * 4);
+  uint32_t* sbytes_k = (uint32_t*)malloc((size_t)n * 4);
   ora_offsets((int32_t)n, tier, units, qrank);
   ora_scale_offsets((int32_t)n, tier, g.e8, g.e4, sbytes);
+  ora_scale_offsets((int32_t)n, tier, g.ek8, g.ek4, sbytes_k);
   int bad = cnt[T_FP16] != p.n_sink + p.n_fp16 || cnt[T_INT8] != p.n_int8 ||
             cnt[T_INT4] != p.n_int4 || cnt[T_DROP] != p.n_drop;
   for (int64_t ch = 0; ch < g.nchunks && !bad; ++ch) {
     const uint8_t* e = payload + g.chunkidx_off + g.cidx_entry * (uint64_t)ch;
     bad = get32(e) != units[ch * ORA_CHUNK] || get32(e + 4) != qrank[ch * ORA_CHUNK];
-    if (!bad && g.cidx_entry == 16) bad = get32(e + 8) != sbytes[ch * ORA_CHUNK] || get32(e + 12) != 0;
+    if (!bad && g.cidx_entry == 16)
+      bad = get32(e + 8) != sbytes[ch * ORA_CHUNK] ||
+            get32(e + 12) != (any_channel(c) ? sbytes_k[ch * ORA_CHUNK] : 0u);
   }
   for (int64_t t = 0; t < (n + block_size - 1) / block_size && !bad; ++t)
     bad = block_table[t] < 0 || block_table[t] >= num_blocks;
   if (bad) {
-    free(tier); free(units); free(qrank); free(sbytes);
+    free(tier); free(units); free(qrank); free(sbytes); free(sbytes_k);
     return ORA_ERR_FORMAT;
   }
   uint64_t rowunit = (uint64_t)d / 2;
@@ -869,18 +989,40 @@ int ora_unpack(const ora_config* c, const uint8_t* payload, uint64_t bytes, uint
     const uint8_t* lb = payload + g.layers_off + (uint64_t)l * g.layer_stride;
     for (int kv = 0; kv < 2; ++kv)
       for (int64_t h = 0; h < H; ++h) {
-        const uint8_t* seg = lb + g.scales_bytes + (uint64_t)(kv * H + h) * g.seg_stride;
-        const uint8_t* sc = lb + (uint64_t)(kv * H + h) * g.seg_scale_bytes;
+        const uint8_t* seg = lb + g.scales_bytes + g.channel_bytes + (uint64_t)(kv * H + h) * g.seg_stride;
+        const uint8_t* sc = lb + seg_meta_off(&g, H, kv, h);
+        const uint32_t* so = kv == 0 ? sbytes_k : sbytes;
         uint16_t* cache = kv == 0 ? kc : vc;
         for (int64_t t = 0; t < n; ++t) {
           int32_t q = tier[t] == T_INT8 ? c->quant_int8 : c->quant_int4;
           int64_t blk = block_table[t / block_size], slot = t % block_size;
           uint16_t* dst = cache + (((l * num_blocks + blk) * block_size + slot) * H + h) * d;
-          ora_decode_row_q(tier[t], q, (int32_t)d, seg + units[t] * rowunit, sc + sbytes[t], dst);
+          const uint8_t* row = seg + units[t] * rowunit;
+          if (kv == 0 && (tier[t] == T_INT8 || tier[t] == T_INT4) && (q & QV_CHANNEL)) {
+            /* per-channel K row: element i with channel i's entry of the chunk */
+            const uint8_t* blkp = lb + chan_off(c, &g, h, t / ORA_CHUNK, tier[t]);
+            const int asym = (q & QV_ASYM) != 0, f16 = (q & QV_FP16) != 0;
+            for (int32_t i = 0; i < (int32_t)d; ++i) {
+              const uint8_t* m = blkp + (uint64_t)i * qv_group_entry(q);
+              float scale, lo = 0.0f;
+              if (f16) {
+                scale = half_to_float(get16(m));
+                if (asym) lo = half_to_float(get16(m + 2));
+              } else {
+                uint32_t b = get32(m);
+                memcpy(&scale, &b, 4);
+                if (asym) { b = get32(m + 4); memcpy(&lo, &b, 4); }
+              }
+              uint32_t raw = tier[t] == T_INT8 ? row[i] : (uint32_t)(row[i / 2] >> (4 * (i & 1))) & 0xFu;
+              dst[i] = decode_code(tier[t], asym, raw, scale, lo);
+            }
+          } else {
+            ora_decode_row_q(tier[t], q, (int32_t)d, row, sc + so[t], dst);
+          }
         }
       }
   }
-  free(tier); free(units); free(qrank); free(sbytes);
+  free(tier); free(units); free(qrank); free(sbytes); free(sbytes_k);
   return ORA_OK;
 }
 

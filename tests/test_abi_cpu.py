@@ -71,7 +71,7 @@ def test_invalid_configs_rejected_like_the_oracle(lib):
                          ("budget", 0.0), ("budget", 1.5), ("budget", float("nan")), ("first_ratio", -0.1),
                          ("num_tiers", 4), ("score_mode", 3), ("decay", -1.0), ("decay", float("inf")),
                          ("decay", 1.0), ("num_sink", -2), ("num_layers", 0), ("num_kv_heads", 0),
-                         ("quant_int8", 3), ("quant_int4", 16), ("quant_int4", -1)]:
+                         ("quant_int8", 3), ("quant_int4", 32), ("quant_int8", 19), ("quant_int4", -1)]:
         c = skv.config(**base)
         setattr(c, field, value)
         o = oracle.config(**base)

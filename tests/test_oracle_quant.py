@@ -189,7 +189,7 @@ def test_variant_payload_layout_and_round_trip(q8, q4):
 
 
 def test_invalid_descriptors_and_unsupported_paths():
-    for q in (3, 16, -1, 0x13):
+    for q in (3, 32, -1, 0x13, 0x30):
         assert oracle.validate(oracle.config(1, 1, 64, 100, 0.5, quant_int8=q)) == oracle.ERR_INVALID_ARG
     cfg = oracle.config(1, 1, 64, 100, 0.5, quant_int4=oracle.QUANT_ASYM)
     with pytest.raises(oracle.OracleError):
