@@ -70,6 +70,8 @@ def _load():
         "ora_encode_row_q": (ctypes.c_int, [ctypes.c_int, ctypes.c_int32, ctypes.c_int32, vp, vp, vp]),
         "ora_decode_row_q": (None, [ctypes.c_int, ctypes.c_int32, ctypes.c_int32, vp, vp, vp]),
         "ora_scale_offsets": (None, [ctypes.c_int32, vp, ctypes.c_uint64, ctypes.c_uint64, vp]),
+        "ora_quant_group": (ctypes.c_int, [ctypes.c_int, ctypes.c_int32, ctypes.c_int64, vp, vp, vp]),
+        "ora_decode_row_channel": (None, [ctypes.c_int, ctypes.c_int32, ctypes.c_int32, vp, vp, vp]),
         "ora_pack": (ctypes.c_int, [cfgp, vp, vp, vp, vp, ctypes.c_uint64]),
         "ora_check_header": (ctypes.c_int, [cfgp, vp, ctypes.c_uint64]),
         "ora_geometry": (ctypes.c_int, [cfgp, vp]),
@@ -204,6 +206,30 @@ def meta_bytes(q, d):
     g = d if q & 3 == 0 else (64 if q & 3 == 1 else 32)
     g = min(g, d)
     return (d // g) * (2 if q & QUANT_ASYM else 1) * (2 if q & QUANT_FP16 else 4)
+
+
+def channel_entry_bytes(q):
+    """Bytes of one per-channel (or group) entry under descriptor q: s, then lo."""
+    return (2 if q & QUANT_ASYM else 1) * (2 if q & QUANT_FP16 else 4)
+
+
+def quant_group(tier, q, values):
+    """One quantization group of binary16 values under descriptor q's bits 2-3:
+    returns (codes int32[cnt], metadata entry bytes, non-finite flag)."""
+    x = _u16(values)
+    codes = np.zeros(x.shape[0], np.int32)
+    meta = np.zeros(channel_entry_bytes(q), np.uint8)
+    bad = _lib.ora_quant_group(int(tier), int(q), int(x.shape[0]), _ptr(x), _ptr(codes), _ptr(meta))
+    return codes, meta, bool(bad)
+
+
+def decode_row_channel(tier, q, d, data, block):
+    """A per-channel K row decoded with its chunk's d channel entries."""
+    y = np.zeros(d, np.uint16)
+    data = np.ascontiguousarray(data, np.uint8)
+    block = np.ascontiguousarray(block, np.uint8)
+    _lib.ora_decode_row_channel(int(tier), int(q), int(d), _ptr(data), _ptr(block), _ptr(y))
+    return y
 
 
 def encode_row_q(tier, q, row):

@@ -632,6 +632,12 @@ static int quant_group(int tr, int32_t q, const uint16_t* x, int64_t stride, int
   return bad;
 }
 
+/* One quantization group of cnt contiguous values (exported for tests): codes
+ * and the group's metadata entry, as quant_group. */
+int ora_quant_group(int tr, int32_t q, int64_t cnt, const uint16_t* x, int32_t* codes, uint8_t* meta) {
+  return quant_group(tr, q, x, 1, cnt, codes, meta);
+}
+
 /* Stores d codes of tier tr: a byte each (INT8), or two nibbles per byte,
  * even element in the low nibble (INT4). */
 static void store_codes(int tr, int32_t d, const int32_t* codes, uint8_t* out) {
@@ -709,6 +715,26 @@ void ora_decode_row_q(int tr, int32_t q, int32_t d, const uint8_t* in, const uin
       uint32_t raw = tr == T_INT8 ? in[i] : (uint32_t)(in[i / 2] >> (4 * (i & 1))) & 0xFu;
       y[i] = decode_code(tr, asym, raw, scale, lo);
     }
+  }
+}
+
+/* Decodes a per-channel K row: element i with channel i's entry (s, then lo)
+ * in blk, by decode_code. */
+void ora_decode_row_channel(int tr, int32_t q, int32_t d, const uint8_t* in, const uint8_t* blk, uint16_t* y) {
+  const int asym = (q & QV_ASYM) != 0, f16 = (q & QV_FP16) != 0;
+  for (int32_t i = 0; i < d; ++i) {
+    const uint8_t* m = blk + (uint64_t)i * qv_group_entry(q);
+    float scale, lo = 0.0f;
+    if (f16) {
+      scale = half_to_float(get16(m));
+      if (asym) lo = half_to_float(get16(m + 2));
+    } else {
+      uint32_t b = get32(m);
+      memcpy(&scale, &b, 4);
+      if (asym) { b = get32(m + 4); memcpy(&lo, &b, 4); }
+    }
+    uint32_t raw = tr == T_INT8 ? in[i] : (uint32_t)(in[i / 2] >> (4 * (i & 1))) & 0xFu;
+    y[i] = decode_code(tr, asym, raw, scale, lo);
   }
 }
 
@@ -1000,22 +1026,7 @@ int ora_unpack(const ora_config* c, const uint8_t* payload, uint64_t bytes, uint
           const uint8_t* row = seg + units[t] * rowunit;
           if (kv == 0 && (tier[t] == T_INT8 || tier[t] == T_INT4) && (q & QV_CHANNEL)) {
             /* per-channel K row: element i with channel i's entry of the chunk */
-            const uint8_t* blkp = lb + chan_off(c, &g, h, t / ORA_CHUNK, tier[t]);
-            const int asym = (q & QV_ASYM) != 0, f16 = (q & QV_FP16) != 0;
-            for (int32_t i = 0; i < (int32_t)d; ++i) {
-              const uint8_t* m = blkp + (uint64_t)i * qv_group_entry(q);
-              float scale, lo = 0.0f;
-              if (f16) {
-                scale = half_to_float(get16(m));
-                if (asym) lo = half_to_float(get16(m + 2));
-              } else {
-                uint32_t b = get32(m);
-                memcpy(&scale, &b, 4);
-                if (asym) { b = get32(m + 4); memcpy(&lo, &b, 4); }
-              }
-              uint32_t raw = tier[t] == T_INT8 ? row[i] : (uint32_t)(row[i / 2] >> (4 * (i & 1))) & 0xFu;
-              dst[i] = decode_code(tier[t], asym, raw, scale, lo);
-            }
+            ora_decode_row_channel(tier[t], q, (int32_t)d, row, lb + chan_off(c, &g, h, t / ORA_CHUNK, tier[t]), dst);
           } else {
             ora_decode_row_q(tier[t], q, (int32_t)d, row, sc + so[t], dst);
           }
