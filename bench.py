@@ -33,8 +33,8 @@ CSRC = os.path.join(ROOT, "paper_2606_08635_amd", "csrc")
 # kernel sources they were taken on: the first 16 hex digits of SHA-256 over
 # the kernel's .hip file and every header of the library (source_digest).
 MEASURED_TRAFFIC = {
-    ("mistral7b_32k", "pack"): (6.5086e9, "pack.hip", "f1453a60af494d45"),
-    ("mistral7b_32k", "unpack"): (6.5125e9, "unpack.hip", "f372993299081d4d"),
+    ("mistral7b_32k", "pack"): (6.5085e9, "pack.hip", "4f414923925ec678"),
+    ("mistral7b_32k", "unpack"): (6.5125e9, "unpack.hip", "b7edaca997175b26"),
 }
 
 
@@ -428,6 +428,10 @@ def run_quant(args, w):
         "g32_sym_fp16": (skv.QUANT_GROUP32 | skv.QUANT_FP16, skv.QUANT_GROUP32 | skv.QUANT_FP16),
         "int4_g32_asym_fp16": (0, skv.QUANT_GROUP32 | skv.QUANT_ASYM | skv.QUANT_FP16),
         "g64_asym_fp32": (skv.QUANT_GROUP64 | skv.QUANT_ASYM, skv.QUANT_GROUP64 | skv.QUANT_ASYM),
+        # KIVI-style: keys per channel over each chunk's rows of the tier, values per row
+        "kchan_asym_fp16": (skv.QUANT_CHANNEL | skv.QUANT_ASYM | skv.QUANT_FP16,
+                            skv.QUANT_CHANNEL | skv.QUANT_ASYM | skv.QUANT_FP16),
+        "kchan_sym_fp32": (skv.QUANT_CHANNEL, skv.QUANT_CHANNEL),
     }
     out = {"workload": w.name}
     for name, (q8, q4) in variants.items():
@@ -450,9 +454,9 @@ def run_quant(args, w):
             raise RuntimeError(f"codec reported status {codec.status.cpu().tolist()}")
         tp = sum(e[0].elapsed_time(e[1]) for e in evs) / args.steps
         tu = sum(e[1].elapsed_time(e[2]) for e in evs) / args.steps
-        geo = codec.payload[:256].cpu().numpy().view("<u8")
+        hdr = codec.payload[:256].cpu().numpy().view("<u8")  # u64 words: 15 per-row metadata, 21 per-channel area
         out[name] = {"quant_int8": q8, "quant_int4": q4, "payload_bytes": codec.payload_bytes,
-                     "metadata_bytes_per_layer": int(geo[15]), "pack_ms": round(tp, 4), "unpack_ms": round(tu, 4),
+                     "metadata_bytes_per_layer": int(hdr[15] + hdr[21]), "pack_ms": round(tp, 4), "unpack_ms": round(tu, 4),
                      "fp16eq_gbps": round(w.fp16_bytes / ((tp + tu) / 1e3) / 1e9, 2)}
         del codec
         torch.cuda.empty_cache()

@@ -51,7 +51,9 @@
  *   layer 0, 104 u64 segment bytes, 112 u64 segment stride, 120 u64 scale
  *   section bytes per layer, 128 u64 layer stride, 136 u64 total bytes,
  *   144 u32 quantized rows holding a non-finite value, 148 u32 pack status,
- *   152 u32 tokens per chunk (256); all other bytes zero.
+ *   152 u32 tokens per chunk (256), 156/160 i32 INT8 / INT4 quantizer
+ *   descriptors, 168 u64 per-channel area bytes per layer (0 without a
+ *   per-channel tier); all other bytes zero.
  */
 #ifndef SKV_H_
 #define SKV_H_
@@ -132,11 +134,23 @@ typedef struct skv_config {
  * metadata (s, then lo if asymmetric; fp32 or binary16) in token order, and
  * chunk-index entries are 16 bytes: {units, quantized rows, metadata bytes
  * before the chunk, 0}; header words 39 and 40 hold the two descriptors.
+ * SKV_QUANT_CHANNEL (per-channel key scales, KIVI-style key quantization,
+ * Sec. 8 and Sec. 10): the K rows of the tier inside each 256-token chunk form
+ * one group per channel (that channel's element of each such row) with the
+ * ASYM/FP16 bits above; they carry no per-row metadata.  V rows keep the
+ * per-row groups of the other bits.  A chunk without rows of the tier gets
+ * zero entries.  With a per-channel tier each layer's per-row metadata holds
+ * the H K segments (n8 ek8 + n4 ek4 bytes each, ek = 0 for a per-channel tier)
+ * and then the H V segments; a per-channel area follows it (256-aligned,
+ * header u64 at byte 168): per (head, chunk) the d INT8 entries (if that tier
+ * is per-channel), then the d INT4 entries (if that tier is); the fourth
+ * chunk-index word holds the K-side metadata bytes before the chunk.
  * The cold-tier upgrade and the grouped calls require both descriptors 0. */
 #define SKV_QUANT_GROUP64 1
 #define SKV_QUANT_GROUP32 2
 #define SKV_QUANT_ASYM 4
 #define SKV_QUANT_FP16 8
+#define SKV_QUANT_CHANNEL 16
 
 /* Tier counts of a configuration.  n_fp16/n_int8/n_int4/n_drop count the
  * non-sink tokens; the n_sink sink tokens are FP16 as well.  Budget in

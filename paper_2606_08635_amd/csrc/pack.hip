@@ -33,7 +33,7 @@ constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
 // grid: one workgroup per request
 __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
   __shared__ uint32_t s_chunk[kMaxChunks];  // per chunk: units | quant << 16
-  __shared__ uint32_t s_meta[kMaxChunks];   // per chunk: metadata bytes (variant descriptors)
+  __shared__ uint32_t s_meta[kMaxChunks];   // per chunk: V-side | K-side << 16 metadata bytes (variants)
   __shared__ uint32_t s_cnt[4];
   __shared__ uint32_t s_bad;
   __shared__ uint64_t s_scan[16];
@@ -59,10 +59,12 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
     for (int i = 0; i < 4; ++i) cnt[i] += gi.count(i);
     bad |= gi.bad;
     const uint32_t u = sum16(gi.units), q = sum16(gi.quant);
+    // a chunk's metadata is at most 256 rows x 64 bytes: 16 bits per side
     const uint32_t m = sum16(gi.count(kINT8) * a.e8 + gi.count(kINT4) * a.e4);
+    const uint32_t mk = sum16(gi.count(kINT8) * a.ek8 + gi.count(kINT4) * a.ek4);
     if ((tid % kGroupsPerChunk) == 0 && g < ngroups) {
       s_chunk[g / kGroupsPerChunk] = u | (q << 16);
-      s_meta[g / kGroupsPerChunk] = m;
+      s_meta[g / kGroupsPerChunk] = m | (mk << 16);
     }
   }
 #pragma unroll
@@ -96,18 +98,21 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
       ru += s_chunk[c] & 0xFFFFu;
       rq += s_chunk[c] >> 16;
     }
-  } else {  // 16-byte entries {units, quantized rows, metadata bytes, 0}
+  } else {  // 16-byte entries {units, quantized rows, V-side metadata bytes, K-side metadata bytes or 0}
+    const bool chan = ((a.q8 | a.q4) & kQuantChannel) != 0;
     uint64_t mrun = 0;
-    for (int c = c0; c < c1; ++c) mrun += s_meta[c];
-    uint32_t rm = static_cast<uint32_t>(block_exclusive_scan_1024(mrun, s_scan2));
+    for (int c = c0; c < c1; ++c) mrun += (s_meta[c] & 0xFFFFu) | (static_cast<uint64_t>(s_meta[c] >> 16) << 32);
+    const uint64_t mex = block_exclusive_scan_1024(mrun, s_scan2);
+    uint32_t rm = static_cast<uint32_t>(mex), rmk = static_cast<uint32_t>(mex >> 32);
     for (int c = c0; c < c1; ++c) {
       cidx[4 * c] = ru;
       cidx[4 * c + 1] = rq;
       cidx[4 * c + 2] = rm;
-      cidx[4 * c + 3] = 0u;
+      cidx[4 * c + 3] = chan ? rmk : 0u;
       ru += s_chunk[c] & 0xFFFFu;
       rq += s_chunk[c] >> 16;
-      rm += s_meta[c];
+      rm += s_meta[c] & 0xFFFFu;
+      rmk += s_meta[c] >> 16;
     }
   }
   const uint64_t entry = variant ? 16u : 8u;
@@ -141,38 +146,58 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   const int kv = (seg / H) & 1;
   const int l = a.layer_begin + seg / (2 * H);
   const int t0 = chunk * kChunkTokens;
+  // per-channel K tiers: their K rows carry no per-row metadata and use the
+  // K-side metadata offsets of the chunk index
+  const bool chan_k = VARIANT && kv == 0 && ((a.q8 | a.q4) & kQuantChannel) != 0;
 
   // row offsets of this chunk: chunk-index base + block exclusive scan
-  const VarCfg var{a.q8, a.q4, a.e8, a.e4};
+  const VarCfg var{a.q8, a.q4, kv == 0 ? a.ek8 : a.e8, kv == 0 ? a.ek4 : a.e4};
   {
     const int t = t0 + threadIdx.x;
     const int tr = t < n ? r.tier[t] : kDROP;
     const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off);
-    if constexpr (VARIANT) chunk_layout_var<D>(s, tr, cidx + 4 * chunk, var);
+    if constexpr (VARIANT) chunk_layout_var<D>(s, tr, cidx + 4 * chunk, chan_k ? 3 : 2, var);
     else chunk_layout<D>(s, tr, cidx + 2 * chunk);
   }
   __syncthreads();
 
   const uint16_t* src = (kv ? r.v : r.k) + (static_cast<size_t>(l) * H + h) * static_cast<size_t>(n) * D;
   uint8_t* lay = payload + r.layers_off + static_cast<uint64_t>(l) * r.layer_stride;
-  uint8_t* dst = lay + r.scales_bytes + static_cast<uint64_t>(kv * H + h) * r.seg_stride;
-  uint8_t* meta = lay + static_cast<uint64_t>(kv * H + h) * r.seg_scale_bytes;
+  uint8_t* dst = lay + r.scales_bytes + r.channel_bytes + static_cast<uint64_t>(kv * H + h) * r.seg_stride;
+  uint8_t* meta = lay + (kv == 0 ? static_cast<uint64_t>(h) * r.seg_scale_bytes_k
+                                 : static_cast<uint64_t>(H) * r.seg_scale_bytes_k + static_cast<uint64_t>(h) * r.seg_scale_bytes);
   uint32_t* nonfinite = reinterpret_cast<uint32_t*>(payload) + kHdrNonfinite;
-  if constexpr (VARIANT)
-    pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, src, dst, meta, nonfinite, t0, n, var);
-  else
+  if constexpr (VARIANT) {
+    if (chan_k) {
+      __shared__ ChanLds<D> c;
+      uint8_t* blk = lay + r.scales_bytes + (static_cast<uint64_t>(h) * nchunks + chunk) * (a.cb8 + a.cb4);
+      channel_params<D>(s, c, src, t0, n, var, blk, blk + a.cb8);
+      pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, true>(s, &c, src, dst, meta, nonfinite, t0, n, var);
+    } else {
+      pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, false>(s, nullptr, src, dst, meta, nonfinite, t0, n,
+                                                                           var);
+    }
+  } else {
     pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, src, dst, reinterpret_cast<float*>(meta), nonfinite,
                                                               t0, n);
+  }
 
-  // padding: segment tail (last chunk) and the layer's scale-section tail
+  // padding: segment tail (last chunk), the layer's per-row metadata tail and
+  // per-channel area tail
   if (chunk == nchunks - 1) {
     for (uint64_t b = r.seg_bytes + 16ull * threadIdx.x; b < r.seg_stride; b += 16ull * kRowThreads)
       st_nt16(dst + b, u32x4{0u, 0u, 0u, 0u});
   }
   if (chunk == 0 && kv == 0 && h == 0) {
-    const uint64_t used = 2ull * H * r.seg_scale_bytes;
-    for (uint64_t b = used + 4ull * threadIdx.x; b < r.scales_bytes; b += 4ull * kRowThreads)
-      *reinterpret_cast<uint32_t*>(lay + b) = 0u;
+    // every metadata entry is 2, 4 or 8 bytes, so the used sizes are only
+    // 2-byte aligned (the K and V halves differ with per-channel tiers):
+    // 16-bit stores end exactly at each section boundary
+    const uint64_t used = static_cast<uint64_t>(H) * (r.seg_scale_bytes_k + r.seg_scale_bytes);
+    for (uint64_t b = used + 2ull * threadIdx.x; b < r.scales_bytes; b += 2ull * kRowThreads)
+      *reinterpret_cast<uint16_t*>(lay + b) = 0u;
+    const uint64_t cused = static_cast<uint64_t>(H) * nchunks * (a.cb8 + a.cb4);
+    for (uint64_t b = cused + 2ull * threadIdx.x; b < r.channel_bytes; b += 2ull * kRowThreads)
+      *reinterpret_cast<uint16_t*>(lay + r.scales_bytes + b) = 0u;
   }
 }
 

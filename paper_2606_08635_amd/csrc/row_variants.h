@@ -5,6 +5,9 @@
 //   bits 0-1  elements per group: 0 the row (d), 1 64, 2 32 (capped at d)
 //   bit 2     asymmetric: codes 0..M (M = 255 / 15), x^ = code * s + lo
 //   bit 3     s (and lo) stored as binary16
+//   bit 4     per-channel K (KIVI-style key quantization): the K rows of the
+//             tier inside a 256-token chunk form one group per channel, with
+//             bits 2-3; V rows keep the per-row groups of bits 0-3
 // Per group, symmetric: s = RN32(a/Q), r = RN32(Q/a) (a = max |x|); with
 // binary16 metadata s = RN16(RN32(a/Q)), r = RN32(1/s) and codes clamped to
 // +-Q.  Asymmetric: lo, hi the group's minimum and maximum (-0 below +0),
@@ -25,11 +28,11 @@
 
 namespace skv {
 
-constexpr int32_t kQuantAsym = 4, kQuantFp16 = 8;
+constexpr int32_t kQuantAsym = 4, kQuantFp16 = 8, kQuantChannel = 16;
 
 struct VarCfg {
   int32_t q8, q4;  // descriptors of the INT8 and INT4 tiers
-  uint32_t e8, e4;  // metadata bytes of an INT8 / INT4 row
+  uint32_t e8, e4;  // per-row metadata bytes of an INT8 / INT4 row of this segment
 };
 
 __device__ __forceinline__ int var_group_lanes(int32_t q, int D) {
@@ -66,6 +69,103 @@ __device__ __forceinline__ uint32_t load_u32_from_halves(const uint8_t* p) {
          (static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(p)[1]) << 16);
 }
 
+// Parameters of one quantization group from its reductions: amax (largest
+// magnitude bits), kmin / kmax (order keys of the minimum and maximum).
+struct GroupParams {
+  float scale, r, lo;
+  uint32_t s16, lo16;  // binary16 metadata
+  bool zero;           // all codes zero (non-finite, zero a or range, binary16 underflow)
+};
+
+__device__ __forceinline__ GroupParams group_params(uint32_t amax, uint32_t kmin, uint32_t kmax, int tr, int32_t q) {
+  const bool asym = (q & kQuantAsym) != 0, f16 = (q & kQuantFp16) != 0;
+  const int Q = tr == kINT8 ? 127 : 7, M = tr == kINT8 ? 255 : 15;
+  GroupParams g;
+  g.scale = 0.0f;
+  g.r = 0.0f;
+  g.lo = 0.0f;
+  g.s16 = 0;
+  g.lo16 = key_to_half(kmin);
+  g.zero = false;
+  if (amax >= 0x7C00u) {  // the group holds an inf/NaN
+    g.scale = __builtin_bit_cast(float, 0x7FC00000u);
+    g.lo = g.scale;
+    g.s16 = g.lo16 = 0x7E00u;
+    g.zero = true;
+  } else if (!asym) {
+    if (amax == 0u) {
+      g.zero = true;
+    } else {
+      const float a = half_lo(amax);
+      g.scale = scale_of(a, static_cast<float>(Q), Q == 127 ? 1.0f / 127.0f : 1.0f / 7.0f);
+      if (f16) {
+        g.s16 = __builtin_bit_cast(uint16_t, static_cast<_Float16>(g.scale));
+        g.scale = half_lo(g.s16);
+        g.zero = g.s16 == 0u;
+        g.r = g.zero ? 0.0f : 1.0f / g.scale;  // correctly rounded division
+      } else {
+        g.r = recip_scale_of(a, static_cast<float>(Q));
+      }
+    }
+  } else {
+    g.lo = half_lo(g.lo16);
+    const float range = half_lo(key_to_half(kmax)) - g.lo;
+    if (range == 0.0f) {
+      g.zero = true;
+    } else {
+      g.scale = range / static_cast<float>(M);
+      if (f16) {
+        g.s16 = __builtin_bit_cast(uint16_t, static_cast<_Float16>(g.scale));
+        g.scale = half_lo(g.s16);
+        g.zero = g.s16 == 0u;
+        g.r = g.zero ? 0.0f : 1.0f / g.scale;
+      } else {
+        g.r = static_cast<float>(M) / range;
+      }
+    }
+  }
+  return g;
+}
+
+// Code of x in a group (as the float-magic integer base + code, clamped).
+__device__ __forceinline__ uint32_t group_code(float x, float r, float lo, bool zero, bool asym, int tr) {
+  const int Q = tr == kINT8 ? 127 : 7, M = tr == kINT8 ? 255 : 15;
+  const int32_t base = 0x4B400000;
+  const int32_t cmin = asym ? base : base - Q, cmax = asym ? base + M : base + Q;
+  const float y = asym ? (x - lo) * r : x * r;
+  const int32_t c = min(max(__builtin_bit_cast(int32_t, y + 12582912.0f), cmin), cmax);
+  return static_cast<uint32_t>(zero ? base : c);
+}
+
+// Writes a group's metadata entry (s, then lo if asymmetric; fp32 or binary16).
+__device__ __forceinline__ void store_entry(uint8_t* e, const GroupParams& g, int32_t q) {
+  const bool asym = (q & kQuantAsym) != 0;
+  if (q & kQuantFp16) {
+    reinterpret_cast<uint16_t*>(e)[0] = static_cast<uint16_t>(g.s16);
+    if (asym) reinterpret_cast<uint16_t*>(e)[1] = static_cast<uint16_t>(g.lo16);
+  } else {
+    store_u32_as_halves(e, __builtin_bit_cast(uint32_t, g.scale));
+    if (asym) store_u32_as_halves(e + 4, __builtin_bit_cast(uint32_t, g.lo));
+  }
+}
+
+__device__ __forceinline__ uint32_t entry_bytes(int32_t q) {
+  return ((q & kQuantAsym) ? 2u : 1u) * ((q & kQuantFp16) ? 2u : 4u);
+}
+
+// Order-key minimum and maximum of the lane's 8 elements.
+__device__ __forceinline__ void lane_key_range(u32x4 x, uint32_t& kmin, uint32_t& kmax) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  kmin = 0xFFFFu;
+  kmax = 0u;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t k0 = order_key16(w[i] & 0xFFFFu), k1 = order_key16(w[i] >> 16);
+    kmin = min(kmin, min(k0, k1));
+    kmax = max(kmax, max(k0, k1));
+  }
+}
+
 // Quantizes the lane's 8 elements of a row at tier tr under descriptor q and
 // writes the group's metadata at meta (the row's metadata) from the group's
 // first lane.  All lanes of the wavefront call it (reductions).
@@ -74,94 +174,37 @@ __device__ __forceinline__ LaneCodes quantize_lane_var(u32x4 x, int tr, int32_t 
                                                        bool write_meta) {
   constexpr int D = LPR * 8;
   const int gl = var_group_lanes(q, D);
-  const bool asym = (q & kQuantAsym) != 0, f16 = (q & kQuantFp16) != 0;
-  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-  uint32_t kmin = 0xFFFFu, kmax = 0u;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t k0 = order_key16(w[i] & 0xFFFFu), k1 = order_key16(w[i] >> 16);
-    kmin = min(kmin, min(k0, k1));
-    kmax = max(kmax, max(k0, k1));
-  }
+  const bool asym = (q & kQuantAsym) != 0;
+  uint32_t kmin, kmax;
+  lane_key_range(x, kmin, kmax);
   const uint32_t lane_amax = absmax_bits8(x);
   const uint32_t amax = group_reduce<LPR, true>(lane_amax, gl);
   kmin = group_reduce<LPR, false>(kmin, gl);
   kmax = group_reduce<LPR, true>(kmax, gl);
-  const bool bad = amax >= 0x7C00u;  // this group holds an inf/NaN
+  const GroupParams g = group_params(amax, kmin, kmax, tr, q);
 
   LaneCodes out;
   out.nonfinite = group_max<LPR>(lane_amax) >= 0x7C00u;  // some group of the row does
-  const int Q = tr == kINT8 ? 127 : 7, M = tr == kINT8 ? 255 : 15;
-  float scale = 0.0f, r = 0.0f, lo = 0.0f;
-  uint32_t s16 = 0, lo16 = key_to_half(kmin);
-  bool zero = false;
-  if (bad) {
-    scale = __builtin_bit_cast(float, 0x7FC00000u);
-    lo = scale;
-    s16 = lo16 = 0x7E00u;
-    zero = true;
-  } else if (!asym) {
-    if (amax == 0u) {
-      zero = true;
-    } else {
-      const float a = half_lo(amax);
-      scale = scale_of(a, static_cast<float>(Q), Q == 127 ? 1.0f / 127.0f : 1.0f / 7.0f);
-      if (f16) {
-        s16 = __builtin_bit_cast(uint16_t, static_cast<_Float16>(scale));
-        scale = half_lo(s16);
-        zero = s16 == 0u;
-        r = zero ? 0.0f : 1.0f / scale;  // correctly rounded division
-      } else {
-        r = recip_scale_of(a, static_cast<float>(Q));
-      }
-    }
-  } else {
-    lo = half_lo(lo16);
-    const float range = half_lo(key_to_half(kmax)) - lo;
-    if (range == 0.0f) {
-      zero = true;
-    } else {
-      scale = range / static_cast<float>(M);
-      if (f16) {
-        s16 = __builtin_bit_cast(uint16_t, static_cast<_Float16>(scale));
-        scale = half_lo(s16);
-        zero = s16 == 0u;
-        r = zero ? 0.0f : 1.0f / scale;
-      } else {
-        r = static_cast<float>(M) / range;
-      }
-    }
-  }
-  out.scale = scale;
-  const int32_t base = 0x4B400000;
-  const int32_t cmin = asym ? base : base - Q, cmax = asym ? base + M : base + Q;
+  out.scale = g.scale;
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    float y0, y1;
-    if (asym) {
-      y0 = (half_lo(w[i]) - lo) * r;
-      y1 = (half_hi(w[i]) - lo) * r;
-    } else {
-      y0 = half_lo(w[i]) * r;
-      y1 = half_hi(w[i]) * r;
-    }
-    const int32_t c0 = min(max(__builtin_bit_cast(int32_t, y0 + 12582912.0f), cmin), cmax);
-    const int32_t c1 = min(max(__builtin_bit_cast(int32_t, y1 + 12582912.0f), cmin), cmax);
-    out.c[2 * i] = static_cast<uint32_t>(zero ? base : c0);
-    out.c[2 * i + 1] = static_cast<uint32_t>(zero ? base : c1);
+    out.c[2 * i] = group_code(half_lo(w[i]), g.r, g.lo, g.zero, asym, tr);
+    out.c[2 * i + 1] = group_code(half_hi(w[i]), g.r, g.lo, g.zero, asym, tr);
   }
-  if (write_meta && (lane % gl) == 0) {
-    uint8_t* e = meta + (lane / gl) * (asym ? 2 : 1) * (f16 ? 2 : 4);
-    if (f16) {
-      reinterpret_cast<uint16_t*>(e)[0] = static_cast<uint16_t>(s16);
-      if (asym) reinterpret_cast<uint16_t*>(e)[1] = static_cast<uint16_t>(lo16);
-    } else {
-      store_u32_as_halves(e, __builtin_bit_cast(uint32_t, scale));
-      if (asym) store_u32_as_halves(e + 4, __builtin_bit_cast(uint32_t, lo));
-    }
-  }
+  if (write_meta && (lane % gl) == 0) store_entry(meta + (lane / gl) * entry_bytes(q), g, q);
   return out;
 }
+
+// Per-channel K parameters of one chunk (descriptor bit SKV_QUANT_CHANNEL):
+// channel c of tier t uses r[t][c], lo[t][c], zero[t][c] (t = 0 INT8, 1 INT4).
+template <int D>
+struct ChanLds {
+  uint32_t amax[2][D], kmin[2][D], kmax[2][D];
+  float r[2][D], lo[2][D];
+  uint32_t zero[2][D];
+  uint32_t rows[2];
+};
 
 // Row-width units and metadata bytes of one token (scan value of the variant
 // layout: units | metadata bytes << 12).
@@ -173,18 +216,115 @@ __device__ __forceinline__ uint32_t var_scan_value(int tr, const VarCfg& v) {
 
 // chunk_layout for the variant layout: s.q receives the byte offset of the
 // row's metadata inside its segment's metadata.  cidx_entry: {units, quantized
-// rows, metadata bytes, 0} of the chunk.  Contains __syncthreads().
+// rows, V-side metadata bytes, K-side metadata bytes (0 unless a tier is
+// per-channel)} of the chunk; meta_word selects the side (2 or 3).  Contains
+// __syncthreads().
 template <int D>
-__device__ __forceinline__ void chunk_layout_var(ChunkLds& s, int tr, const uint32_t* cidx_entry, const VarCfg& v) {
+__device__ __forceinline__ void chunk_layout_var(ChunkLds& s, int tr, const uint32_t* cidx_entry, int meta_word,
+                                                 const VarCfg& v) {
   uint32_t total;
   const uint32_t ex = block_exclusive_scan_256(var_scan_value(tr, v), s.scan, &total);
   s.tier[threadIdx.x] = static_cast<uint8_t>(tr);
   s.off[threadIdx.x] = (cidx_entry[0] + (ex & 0xFFFu)) * static_cast<uint32_t>(D / 2);
-  s.q[threadIdx.x] = cidx_entry[2] + (ex >> 12);
+  s.q[threadIdx.x] = cidx_entry[meta_word] + (ex >> 12);
 }
 
-template <int D, int ROWS_IN_FLIGHT, bool NT>
-__device__ __forceinline__ void pack_chunk_var(const ChunkLds& s, const uint16_t* __restrict__ src,
+// Reduces the chunk's K rows of each per-channel tier into c (amax, order-key
+// minimum and maximum per channel, rows per tier), then derives the channel
+// parameters and writes the entries: INT8 at blk8, INT4 at blk4 (zeros for a
+// tier without rows in the chunk).  Contains __syncthreads().
+template <int D>
+__device__ __forceinline__ void channel_params(const ChunkLds& s, ChanLds<D>& c, const uint16_t* __restrict__ src,
+                                               int t0, int n, const VarCfg& v, uint8_t* blk8, uint8_t* blk4) {
+  constexpr int LPR = D / 8;
+  constexpr int RPI = kRowThreads / LPR;
+  constexpr int ITERS = kChunkTokens / RPI;
+  const int lane = threadIdx.x % LPR;
+  const int rsub = threadIdx.x / LPR;
+  for (int i = threadIdx.x; i < 2 * D; i += kRowThreads) {
+    (&c.amax[0][0])[i] = 0u;
+    (&c.kmin[0][0])[i] = 0xFFFFu;
+    (&c.kmax[0][0])[i] = 0u;
+  }
+  if (threadIdx.x < 2) c.rows[threadIdx.x] = 0u;
+  __syncthreads();
+  const bool ch8 = (v.q8 & kQuantChannel) != 0, ch4 = (v.q4 & kQuantChannel) != 0;
+  uint32_t am[2][8], kn[2][8], kx[2][8];
+#pragma unroll
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      am[t][e] = 0u;
+      kn[t][e] = 0xFFFFu;
+      kx[t][e] = 0u;
+    }
+  uint32_t rows8 = 0, rows4 = 0;
+#pragma unroll 4
+  for (int it = 0; it < ITERS; ++it) {
+    const int row = it * RPI + rsub;
+    const int tr = s.tier[row];
+    const bool take = (tr == kINT8 && ch8) || (tr == kINT4 && ch4);
+    if (!take) continue;
+    const u32x4 x = *reinterpret_cast<const u32x4*>(src + static_cast<size_t>(t0 + row) * D + lane * 8);
+    const int t = tr == kINT8 ? 0 : 1;
+    rows8 += tr == kINT8;
+    rows4 += tr == kINT4;
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t h = (w[e / 2] >> (16 * (e & 1))) & 0xFFFFu;
+      const uint32_t k = order_key16(h);
+      // unrolled over t so the arrays stay in registers
+      if (t == 0) {
+        am[0][e] = max(am[0][e], h & 0x7FFFu);
+        kn[0][e] = min(kn[0][e], k);
+        kx[0][e] = max(kx[0][e], k);
+      } else {
+        am[1][e] = max(am[1][e], h & 0x7FFFu);
+        kn[1][e] = min(kn[1][e], k);
+        kx[1][e] = max(kx[1][e], k);
+      }
+    }
+  }
+  // integer max / min are order-independent: shared-memory atomics keep the result deterministic
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    if (!(t == 0 ? ch8 : ch4)) continue;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      atomicMax(&c.amax[t][lane * 8 + e], am[t][e]);
+      atomicMin(&c.kmin[t][lane * 8 + e], kn[t][e]);
+      atomicMax(&c.kmax[t][lane * 8 + e], kx[t][e]);
+    }
+  }
+  if (lane == 0) {
+    if (rows8) atomicAdd(&c.rows[0], rows8);
+    if (rows4) atomicAdd(&c.rows[1], rows4);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 2 * D; i += kRowThreads) {
+    const int t = i / D, ch = i % D;
+    const int32_t q = t == 0 ? v.q8 : v.q4;
+    if (!(q & kQuantChannel)) continue;
+    GroupParams g = group_params(c.amax[t][ch], c.kmin[t][ch], c.kmax[t][ch], t == 0 ? kINT8 : kINT4, q);
+    if (c.rows[t] == 0u) {  // no row of the tier in this chunk: zero entry
+      g.scale = g.r = g.lo = 0.0f;
+      g.s16 = g.lo16 = 0u;
+      g.zero = true;
+    }
+    c.r[t][ch] = g.r;
+    c.lo[t][ch] = g.lo;
+    c.zero[t][ch] = g.zero ? 1u : 0u;
+    store_entry((t == 0 ? blk8 : blk4) + ch * entry_bytes(q), g, q);
+  }
+  __syncthreads();
+}
+
+// Packs one chunk of a segment under the variant descriptors.  CHAN: a K
+// segment with a per-channel tier; its rows of that tier take their codes
+// from the channel parameters in c and write no per-row metadata.
+template <int D, int ROWS_IN_FLIGHT, bool NT, bool CHAN>
+__device__ __forceinline__ void pack_chunk_var(const ChunkLds& s, const ChanLds<D>* c, const uint16_t* __restrict__ src,
                                                uint8_t* __restrict__ dst, uint8_t* __restrict__ meta,
                                                uint32_t* nonfinite, int t0, int n, const VarCfg& v) {
   constexpr int LPR = D / 8;
@@ -208,14 +348,29 @@ __device__ __forceinline__ void pack_chunk_var(const ChunkLds& s, const uint16_t
       const int row = (it + u) * RPI + rsub;
       const int tr = s.tier[row];
       const bool quant = tr == kINT8 || tr == kINT4;
-      const LaneCodes q = quantize_lane_var<LPR>(x[u], tr, tr == kINT8 ? v.q8 : v.q4, lane, meta + s.q[row], quant);
+      const int32_t q = tr == kINT8 ? v.q8 : v.q4;
+      const bool chan = CHAN && quant && (q & kQuantChannel) != 0;
+      LaneCodes qc = quantize_lane_var<LPR>(x[u], tr, q, lane, meta + s.q[row], quant && !chan);
+      if constexpr (CHAN) {
+        if (chan) {
+          const int t = tr == kINT8 ? 0 : 1;
+          const bool asym = (q & kQuantAsym) != 0;
+          const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int ch = lane * 8 + e;
+            const float xv = (e & 1) ? half_hi(w[e / 2]) : half_lo(w[e / 2]);
+            qc.c[e] = group_code(xv, c->r[t][ch], c->lo[t][ch], c->zero[t][ch] != 0u, asym, tr);
+          }
+        }
+      }
       if (tr == kFP16) {
         store16<NT>(dst + s.off[row] + lane * 16, x[u]);
       } else if (quant) {
-        if (q.nonfinite && lane == 0) atomicAdd(nonfinite, 1u);
+        if (qc.nonfinite && lane == 0) atomicAdd(nonfinite, 1u);
         uint8_t* out_row = dst + s.off[row];
-        if (tr == kINT8) store8<NT>(out_row + lane * 8, pack_int8(q));
-        else store4<NT>(out_row + lane * 4, pack_int4(q));
+        if (tr == kINT8) store8<NT>(out_row + lane * 8, pack_int8(qc));
+        else store4<NT>(out_row + lane * 4, pack_int4(qc));
       }
     }
   }
@@ -254,8 +409,67 @@ __device__ __forceinline__ u32x4 decode_lane_var(int tr, int32_t q, u32x4 raw, c
   return u32x4{pack_half2(f[0], f[1]), pack_half2(f[2], f[3]), pack_half2(f[4], f[5]), pack_half2(f[6], f[7])};
 }
 
-template <int D, int ROWS_IN_FLIGHT, bool NT>
-__device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const uint8_t* __restrict__ src,
+// Per-channel K parameters of one chunk on the decode side: scale and
+// minimum of channel c of tier t (0 INT8, 1 INT4).
+template <int D>
+struct ChanDecLds {
+  float s[2][D], lo[2][D];
+};
+
+// Loads the chunk's per-channel entries (INT8 at blk8, INT4 at blk4) into c.
+// Contains __syncthreads().
+template <int D>
+__device__ __forceinline__ void load_channel_params(ChanDecLds<D>& c, const uint8_t* blk8, const uint8_t* blk4,
+                                                    const VarCfg& v) {
+  for (int i = threadIdx.x; i < 2 * D; i += kRowThreads) {
+    const int t = i / D, ch = i % D;
+    const int32_t q = t == 0 ? v.q8 : v.q4;
+    float sc = 0.0f, lo = 0.0f;
+    if (q & kQuantChannel) {
+      const uint8_t* e = (t == 0 ? blk8 : blk4) + ch * entry_bytes(q);
+      const bool asym = (q & kQuantAsym) != 0;
+      if (q & kQuantFp16) {
+        sc = half_lo(reinterpret_cast<const uint16_t*>(e)[0]);
+        if (asym) lo = half_lo(reinterpret_cast<const uint16_t*>(e)[1]);
+      } else {
+        sc = __builtin_bit_cast(float, load_u32_from_halves(e));
+        if (asym) lo = __builtin_bit_cast(float, load_u32_from_halves(e + 4));
+      }
+    }
+    c.s[t][ch] = sc;
+    c.lo[t][ch] = lo;
+  }
+  __syncthreads();
+}
+
+// The lane's 8 outputs of a per-channel K row: element e of channel
+// lane * 8 + e decoded with that channel's scale and minimum (NaN scale:
+// 0x7E00).
+template <int LPR>
+__device__ __forceinline__ u32x4 decode_lane_chan(int tr, int32_t q, u32x4 raw, const float* sc, const float* lo,
+                                                  int lane) {
+  const bool asym = (q & kQuantAsym) != 0;
+  uint32_t h[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    int32_t code;
+    if (tr == kINT8) {
+      const uint32_t b = ((i < 4 ? raw.x : raw.y) >> (8 * (i & 3))) & 0xFFu;
+      code = asym ? static_cast<int32_t>(b) : static_cast<int32_t>(static_cast<int8_t>(b));
+    } else {
+      const uint32_t nib = (raw.x >> (4 * i)) & 0xFu;
+      code = asym ? static_cast<int32_t>(nib) : (static_cast<int32_t>(nib << 28) >> 28);
+    }
+    const float s = sc[lane * 8 + i];
+    float f = static_cast<float>(code) * s;
+    if (asym) f = f + lo[lane * 8 + i];
+    h[i] = __builtin_isnan(s) ? 0x7E00u : static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(f)));
+  }
+  return u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+}
+
+template <int D, int ROWS_IN_FLIGHT, bool NT, bool CHAN>
+__device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDecLds<D>* c, const uint8_t* __restrict__ src,
                                                  const uint8_t* __restrict__ meta, uint16_t* __restrict__ cache,
                                                  int H, const VarCfg& v) {
   constexpr int LPR = D / 8;
@@ -276,9 +490,9 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const uint8_
       if (tr == kFP16) {
         raw[u] = ld_nt16(row + lane * 16);
       } else if (tr == kINT8) {
-        const u32x2 c = ld_nt8(row + lane * 8);
-        raw[u].x = c.x;
-        raw[u].y = c.y;
+        const u32x2 cc = ld_nt8(row + lane * 8);
+        raw[u].x = cc.x;
+        raw[u].y = cc.y;
       } else if (tr == kINT4) {
         raw[u].x = ld_nt4(row + lane * 4);
       }
@@ -289,7 +503,15 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const uint8_
       const int tr = s.tier[r];
       if (tr == kAbsent) continue;
       u32x4 o = raw[u];  // FP16 verbatim, DROP zeros
-      if (tr == kINT8 || tr == kINT4) o = decode_lane_var<LPR>(tr, tr == kINT8 ? v.q8 : v.q4, raw[u], meta + s.q[r], lane);
+      if (tr == kINT8 || tr == kINT4) {
+        const int32_t q = tr == kINT8 ? v.q8 : v.q4;
+        if (CHAN && (q & kQuantChannel)) {
+          const int t = tr == kINT8 ? 0 : 1;
+          o = decode_lane_chan<LPR>(tr, q, raw[u], c->s[t], c->lo[t], lane);
+        } else {
+          o = decode_lane_var<LPR>(tr, q, raw[u], meta + s.q[r], lane);
+        }
+      }
       store16<NT>(cache + static_cast<size_t>(s.pos[r]) * H * D + lane * 8, o);
     }
   }

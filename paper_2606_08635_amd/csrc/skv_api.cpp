@@ -32,7 +32,7 @@ skv_status check_config(const skv_config* c) {
     return SKV_ERR_INVALID_ARG;
   if (c->num_tiers != 2 && c->num_tiers != 3) return SKV_ERR_INVALID_ARG;
   for (const int32_t q : {c->quant_int8, c->quant_int4})
-    if ((q & ~15) != 0 || (q & 3) == 3) return SKV_ERR_INVALID_ARG;
+    if ((q & ~31) != 0 || (q & 3) == 3) return SKV_ERR_INVALID_ARG;
   switch (c->score_mode) {
     case SKV_SCORE_KVNORM:
     case SKV_SCORE_RECENCY:
@@ -93,11 +93,23 @@ skv_status plan_counts(const skv_config* c, skv_plan* p) {
   return SKV_OK;
 }
 
-// Metadata bytes of one quantized row under variant descriptor q.
-inline uint32_t variant_meta_bytes(int32_t q, int32_t d) {
+// Bytes of one group's metadata (s, then lo if asymmetric) under descriptor q.
+inline uint32_t variant_entry_bytes(int32_t q) {
+  return ((q & SKV_QUANT_ASYM) ? 2u : 1u) * ((q & SKV_QUANT_FP16) ? 2u : 4u);
+}
+
+// Per-row metadata bytes of one quantized row under variant descriptor q; K
+// rows of a per-channel tier carry none (their entries are per chunk).
+inline uint32_t variant_meta_bytes(int32_t q, int32_t d, bool k_row = false) {
+  if (k_row && (q & SKV_QUANT_CHANNEL)) return 0u;
   int32_t gs = (q & 3) == 0 ? d : (q & 3) == 1 ? 64 : 32;
   gs = std::min(gs, d);
-  return static_cast<uint32_t>(d / gs) * ((q & SKV_QUANT_ASYM) ? 2u : 1u) * ((q & SKV_QUANT_FP16) ? 2u : 4u);
+  return static_cast<uint32_t>(d / gs) * variant_entry_bytes(q);
+}
+
+// Per-channel entry bytes of one (head, chunk) for a tier under descriptor q.
+inline uint32_t channel_block_bytes(int32_t q, int32_t d) {
+  return (q & SKV_QUANT_CHANNEL) ? static_cast<uint32_t>(d) * variant_entry_bytes(q) : 0u;
 }
 
 inline uint32_t float_bits(float f) {
@@ -130,7 +142,12 @@ skv_status make_geometry(const skv_config* cfg, Geometry* g, skv_plan* plan_out)
   g->q4 = cfg->quant_int4;
   g->e8 = variant_meta_bytes(g->q8, cfg->head_dim);
   g->e4 = variant_meta_bytes(g->q4, cfg->head_dim);
+  g->ek8 = variant_meta_bytes(g->q8, cfg->head_dim, true);
+  g->ek4 = variant_meta_bytes(g->q4, cfg->head_dim, true);
+  g->cb8 = channel_block_bytes(g->q8, cfg->head_dim);
+  g->cb4 = channel_block_bytes(g->q4, cfg->head_dim);
   g->seg_scale_bytes = static_cast<uint64_t>(p.n_int8) * g->e8 + static_cast<uint64_t>(p.n_int4) * g->e4;
+  g->seg_scale_bytes_k = static_cast<uint64_t>(p.n_int8) * g->ek8 + static_cast<uint64_t>(p.n_int4) * g->ek4;
   g->cidx_entry = (g->q8 | g->q4) ? 16u : 8u;
   g->nchunks = (g->n + kChunkTokens - 1) / kChunkTokens;
   const uint64_t d = static_cast<uint64_t>(g->d), H = static_cast<uint64_t>(g->H);
@@ -140,8 +157,9 @@ skv_status make_geometry(const skv_config* cfg, Geometry* g, skv_plan* plan_out)
   g->seg_bytes = static_cast<uint64_t>(p.n_sink + p.n_fp16) * (2 * d) +
                  static_cast<uint64_t>(p.n_int8) * d + static_cast<uint64_t>(p.n_int4) * (d / 2);
   g->seg_stride = round_up_256(g->seg_bytes);
-  g->scales_bytes = round_up_256(2 * H * g->seg_scale_bytes);
-  g->layer_stride = g->scales_bytes + 2 * H * g->seg_stride;
+  g->scales_bytes = round_up_256(H * (g->seg_scale_bytes_k + g->seg_scale_bytes));
+  g->channel_bytes = round_up_256(H * static_cast<uint64_t>(g->nchunks) * (g->cb8 + g->cb4));
+  g->layer_stride = g->scales_bytes + g->channel_bytes + 2 * H * g->seg_stride;
   g->total = g->layers_off + static_cast<uint64_t>(g->L) * g->layer_stride;
   if (plan_out) *plan_out = p;
   return SKV_OK;
@@ -184,6 +202,10 @@ void fill_common(const skv_config* cfg, int32_t layer_begin, int32_t layer_count
   a->q4 = cfg->quant_int4;
   a->e8 = variant_meta_bytes(cfg->quant_int8, cfg->head_dim);
   a->e4 = variant_meta_bytes(cfg->quant_int4, cfg->head_dim);
+  a->ek8 = variant_meta_bytes(cfg->quant_int8, cfg->head_dim, true);
+  a->ek4 = variant_meta_bytes(cfg->quant_int4, cfg->head_dim, true);
+  a->cb8 = channel_block_bytes(cfg->quant_int8, cfg->head_dim);
+  a->cb4 = channel_block_bytes(cfg->quant_int4, cfg->head_dim);
 }
 
 void fill_desc(const Geometry& g, const skv_request& q, ReqDesc* r) {
@@ -198,6 +220,8 @@ void fill_desc(const Geometry& g, const skv_request& q, ReqDesc* r) {
   r->layers_off = g.layers_off;
   r->seg_bytes = g.seg_bytes;
   r->seg_scale_bytes = g.seg_scale_bytes;
+  r->seg_scale_bytes_k = g.seg_scale_bytes_k;
+  r->channel_bytes = g.channel_bytes;
   r->seg_stride = g.seg_stride;
   r->scales_bytes = g.scales_bytes;
   r->layer_stride = g.layer_stride;

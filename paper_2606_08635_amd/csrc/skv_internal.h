@@ -21,9 +21,13 @@ struct Geometry {
   int32_t n_sink, n16, n8, n4, nd;
   int64_t budget_units, used_units;
   int64_t nq;       // quantized rows per segment (n8 + n4)
-  int32_t q8, q4;   // quantizer variant descriptors (0: row-wise symmetric, fp32 scale)
-  uint32_t e8, e4;  // metadata bytes of an INT8 / INT4 row
-  uint64_t seg_scale_bytes, cidx_entry;  // metadata bytes of a segment; chunk-index entry bytes (8 or 16)
+  int32_t q8, q4;    // quantizer variant descriptors (0: row-wise symmetric, fp32 scale)
+  uint32_t e8, e4;   // per-row metadata bytes of an INT8 / INT4 V row
+  uint32_t ek8, ek4; // the same for a K row (0 for a per-channel tier)
+  uint32_t cb8, cb4; // per-channel entries of one (head, chunk): INT8 / INT4 tier (0 unless per-channel)
+  uint64_t seg_scale_bytes, seg_scale_bytes_k;  // per-row metadata of a V / K segment
+  uint64_t channel_bytes;  // the layer's per-channel area (256-aligned)
+  uint64_t cidx_entry;     // chunk-index entry bytes (8 or 16)
   int64_t nchunks;  // ceil(n / 256)
   uint64_t tiermap_off, chunkidx_off, layers_off;
   uint64_t seg_bytes, seg_stride, scales_bytes, layer_stride, total;
@@ -41,7 +45,9 @@ struct ReqDesc {
   const int32_t* block_table;   // unpack only
   uint64_t block_begin;         // first flat workgroup of this request in the row launch
   uint64_t chunkidx_off, layers_off, seg_bytes, seg_stride, scales_bytes, layer_stride, total;
-  uint64_t seg_scale_bytes;  // metadata bytes of one segment (4 * nq for descriptor 0)
+  uint64_t seg_scale_bytes;    // per-row metadata bytes of one V segment (4 * nq for descriptor 0)
+  uint64_t seg_scale_bytes_k;  // the same for a K segment (differs only with per-channel tiers)
+  uint64_t channel_bytes;      // per-channel area of a layer, after the per-row metadata
   int64_t nq, budget_units, used_units;
   int32_t n, nchunks, n_sink, n16, n8, n4, nd, pad;
 };
@@ -53,7 +59,9 @@ struct BatchArgs {
   int32_t count, L, H, d, layer_begin, layer_count, num_tiers, score_mode;
   uint32_t budget_bits, rho_bits, decay_bits, pad;
   int32_t q8, q4;    // quantizer variant descriptors of the INT8 and INT4 tiers
-  uint32_t e8, e4;   // metadata bytes of an INT8 / INT4 row
+  uint32_t e8, e4;   // per-row metadata bytes of an INT8 / INT4 V row
+  uint32_t ek8, ek4; // the same for a K row (0 for a per-channel tier)
+  uint32_t cb8, cb4; // per-channel entry bytes of one (head, chunk) for the INT8 / INT4 tier
   ReqDesc r[kMaxBatch];
 };
 static_assert(sizeof(BatchArgs) <= 4000, "kernel arguments");

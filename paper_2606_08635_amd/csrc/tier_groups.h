@@ -145,6 +145,8 @@ __device__ __forceinline__ uint32_t header_word(const BatchArgs& a, const ReqDes
     case 38: return static_cast<uint32_t>(kChunkTokens);
     case 39: return static_cast<uint32_t>(a.q8);
     case 40: return static_cast<uint32_t>(a.q4);
+    case 42: return lo(r.channel_bytes);
+    case 43: return hi(r.channel_bytes);
     default: return 0u;
   }
 }

@@ -36,7 +36,7 @@ constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
 __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a, int num_blocks,
                                                               int block_size) {
   __shared__ uint32_t s_chunk[kMaxChunks];
-  __shared__ uint32_t s_meta[kMaxChunks];  // per chunk: metadata bytes (variant descriptors)
+  __shared__ uint32_t s_meta[kMaxChunks];  // per chunk: V-side | K-side << 16 metadata bytes (variants)
   __shared__ uint32_t s_cnt[4];
   __shared__ uint32_t s_bad;
   __shared__ uint64_t s_scan[16];
@@ -76,9 +76,10 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
     for (int i = 0; i < 4; ++i) cnt[i] += gi.count(i);
     const uint32_t u = sum16(gi.units), q = sum16(gi.quant);
     const uint32_t m = sum16(gi.count(kINT8) * a.e8 + gi.count(kINT4) * a.e4);
+    const uint32_t mk = sum16(gi.count(kINT8) * a.ek8 + gi.count(kINT4) * a.ek4);
     if ((tid % kGroupsPerChunk) == 0 && g < ngroups) {
       s_chunk[g / kGroupsPerChunk] = u | (q << 16);
-      s_meta[g / kGroupsPerChunk] = m;
+      s_meta[g / kGroupsPerChunk] = m | (mk << 16);
     }
   }
 #pragma unroll
@@ -102,14 +103,18 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
       rq += s_chunk[c] >> 16;
     }
   } else {
+    const bool chan = ((a.q8 | a.q4) & kQuantChannel) != 0;
     uint64_t mrun = 0;
-    for (int c = c0; c < c1; ++c) mrun += s_meta[c];
-    uint32_t rm = static_cast<uint32_t>(block_exclusive_scan_1024(mrun, s_scan2));
+    for (int c = c0; c < c1; ++c) mrun += (s_meta[c] & 0xFFFFu) | (static_cast<uint64_t>(s_meta[c] >> 16) << 32);
+    const uint64_t mex = block_exclusive_scan_1024(mrun, s_scan2);
+    uint32_t rm = static_cast<uint32_t>(mex), rmk = static_cast<uint32_t>(mex >> 32);
     for (int c = c0; c < c1; ++c) {
-      bad |= cidx[4 * c] != ru || cidx[4 * c + 1] != rq || cidx[4 * c + 2] != rm || cidx[4 * c + 3] != 0u;
+      bad |= cidx[4 * c] != ru || cidx[4 * c + 1] != rq || cidx[4 * c + 2] != rm ||
+             cidx[4 * c + 3] != (chan ? rmk : 0u);
       ru += s_chunk[c] & 0xFFFFu;
       rq += s_chunk[c] >> 16;
-      rm += s_meta[c];
+      rm += s_meta[c] & 0xFFFFu;
+      rmk += s_meta[c] >> 16;
     }
   }
   if (bad) atomicOr(&s_bad, 1u);
@@ -138,6 +143,10 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
   const int kv = (seg / H) & 1;
   const int l = a.layer_begin + seg / (2 * H);
   const int t0 = chunk * kChunkTokens;
+  // per-channel K tiers: K rows of those tiers decode with the chunk's channel
+  // entries and use the K-side metadata offsets of the chunk index
+  const bool chan_k = VARIANT && kv == 0 && ((a.q8 | a.q4) & kQuantChannel) != 0;
+  const VarCfg var{a.q8, a.q4, kv == 0 ? a.ek8 : a.e8, kv == 0 ? a.ek4 : a.e4};
   {
     const int t = t0 + threadIdx.x;
     int tr = kAbsent;
@@ -148,23 +157,32 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
             static_cast<uint32_t>(t % block_size);
     }
     const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off);
-    if constexpr (VARIANT) chunk_layout_var<D>(s, tr, cidx + 4 * chunk, VarCfg{a.q8, a.q4, a.e8, a.e4});
+    if constexpr (VARIANT) chunk_layout_var<D>(s, tr, cidx + 4 * chunk, chan_k ? 3 : 2, var);
     else chunk_layout<D>(s, tr, cidx + 2 * chunk);
     s.pos[threadIdx.x] = pos;
   }
   __syncthreads();
 
   const uint8_t* lay = payload + r.layers_off + static_cast<uint64_t>(l) * r.layer_stride;
-  const uint8_t* src = lay + r.scales_bytes + static_cast<uint64_t>(kv * H + h) * r.seg_stride;
-  const uint8_t* meta = lay + static_cast<uint64_t>(kv * H + h) * r.seg_scale_bytes;
+  const uint8_t* src = lay + r.scales_bytes + r.channel_bytes + static_cast<uint64_t>(kv * H + h) * r.seg_stride;
+  const uint8_t* meta = lay + (kv == 0 ? static_cast<uint64_t>(h) * r.seg_scale_bytes_k
+                                       : static_cast<uint64_t>(H) * r.seg_scale_bytes_k +
+                                             static_cast<uint64_t>(h) * r.seg_scale_bytes);
   uint16_t* cache = (kv ? v_cache : k_cache) + static_cast<size_t>(l) * num_blocks * block_size * H * D +
                     static_cast<size_t>(h) * D;
-  if constexpr (VARIANT)
-    unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, meta, cache, H,
-                                                                         VarCfg{a.q8, a.q4, a.e8, a.e4});
-  else
+  if constexpr (VARIANT) {
+    if (chan_k) {
+      __shared__ ChanDecLds<D> c;
+      const uint8_t* blk = lay + r.scales_bytes + (static_cast<uint64_t>(h) * nchunks + chunk) * (a.cb8 + a.cb4);
+      load_channel_params<D>(c, blk, blk + a.cb8, var);
+      unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, true>(s, &c, src, meta, cache, H, var);
+    } else {
+      unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, false>(s, nullptr, src, meta, cache, H, var);
+    }
+  } else {
     unpack_chunk<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, reinterpret_cast<const float*>(meta),
                                                                      cache, H);
+  }
 }
 
 }  // namespace

@@ -20,7 +20,7 @@ FP16, INT8, INT4, DROP = 0, 1, 2, 3
 KVNORM, ATTN, RECENCY = 0, 1, 2
 UPGRADE_FP16, UPGRADE_RESIDUAL8 = 0, 1
 GROUP_TOKEN, GROUP_LAYER, GROUP_HEAD = 0, 1, 2
-QUANT_GROUP64, QUANT_GROUP32, QUANT_ASYM, QUANT_FP16 = 1, 2, 4, 8
+QUANT_GROUP64, QUANT_GROUP32, QUANT_ASYM, QUANT_FP16, QUANT_CHANNEL = 1, 2, 4, 8, 16
 ABI_VERSION = 2
 
 EXPORTED = ("skv_abi_version", "skv_status_string", "skv_plan_tiers", "skv_payload_size",

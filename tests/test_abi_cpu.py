@@ -52,7 +52,7 @@ def test_plan_and_payload_size_match_oracle(lib, seed):
         b = float(np.float32(rng.uniform(0.01, 1.0)))
         kw = dict(first_ratio=float(np.float32(rng.uniform(0, 0.1))), num_tiers=int(rng.integers(2, 4)),
                   decay=0.0, num_sink=int(rng.choice([-1, -1, 0, 5])),
-                  quant_int8=int(rng.choice([0, 0, 1, 2, 4, 8, 13, 14])), quant_int4=int(rng.choice([0, 0, 5, 10, 12])))
+                  quant_int8=int(rng.choice([0, 0, 1, 2, 4, 8, 13, 14, 16, 28])), quant_int4=int(rng.choice([0, 0, 5, 10, 12, 17, 22])))
         c, o = _pair(L, H, d, n, b, **kw)
         try:
             want = oracle.plan(o)

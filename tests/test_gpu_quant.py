@@ -1,11 +1,13 @@
 """Per-tier quantizer variants on the GPU vs the oracle, through the C ABI.
 
 Bar: with any pair of descriptors (scale groups of 64/32, asymmetric codes,
-binary16 metadata) the payload (codes, per-group metadata, 16-byte chunk
-index) and the decoded caches are bit-identical to the oracle's, including
-rows with inf/NaN, zero rows, constant groups and subnormals; malformed
-variant chunk indexes are refused; at full size the launch the benchmark
-times is checked on the whole metadata and sampled rows.
+binary16 metadata, per-channel key scales) the payload (codes, per-group and
+per-channel metadata, 16-byte chunk index) and the decoded caches are
+bit-identical to the oracle's, including rows with inf/NaN, zero rows,
+constant groups and subnormals; malformed variant chunk indexes and channel
+prefixes are refused; at full size the launch the benchmark times is checked
+on the whole metadata and sampled rows (per-channel K rows against the
+oracle's groups of their chunk).
 """
 import pytest
 
@@ -66,6 +68,48 @@ def test_two_tier_variant():
     _run(2, 2, 128, 900, 0.3, Q.QUANT_GROUP32 | Q.QUANT_ASYM, 0, seed=5, tiers=2)
 
 
+CHAN = [Q.QUANT_CHANNEL | a | f for a in (0, Q.QUANT_ASYM) for f in (0, Q.QUANT_FP16)]
+
+
+@pytest.mark.parametrize("q", CHAN)
+def test_per_channel_keys_on_both_tiers(q):
+    say(f"per-channel keys q8=q4={q}")
+    _run(2, 2, 64, 777, 0.35, q, q, seed=q + 3)
+
+
+@pytest.mark.parametrize("d,n,b,q8,q4,tiers", [
+    (32, 300, 0.4, Q.QUANT_CHANNEL | Q.QUANT_GROUP32, Q.QUANT_ASYM, 3),               # per-channel INT8 only
+    (128, 1030, 0.3, Q.QUANT_GROUP64, Q.QUANT_CHANNEL | Q.QUANT_ASYM | Q.QUANT_GROUP32, 3),  # INT4 KIVI-style
+    (256, 513, 0.45, Q.QUANT_CHANNEL | Q.QUANT_FP16, Q.QUANT_CHANNEL | Q.QUANT_ASYM, 3),
+    (128, 257, 0.2, Q.QUANT_CHANNEL, Q.QUANT_CHANNEL | Q.QUANT_FP16, 3),               # INT4 + DROP regime
+    (64, 5, 0.5, Q.QUANT_CHANNEL, Q.QUANT_CHANNEL, 3),                                 # one partial chunk
+    (128, 900, 0.3, Q.QUANT_CHANNEL | Q.QUANT_ASYM, Q.QUANT_CHANNEL, 2),               # 2-tier, INT4 blocks unused
+])
+def test_per_channel_mixed(d, n, b, q8, q4, tiers):
+    say(f"per-channel mixed d={d} n={n} q8={q8} q4={q4} tiers={tiers}")
+    _run(2, 3, d, n, b, q8, q4, seed=d + n + 1, tiers=tiers)
+
+
+def test_malformed_channel_prefix_is_refused():
+    L, H, d, n = 1, 2, 64, 700
+    cfg, ocfg = _pair(L, H, d, n, 0.35, Q.QUANT_GROUP32, Q.QUANT_CHANNEL | Q.QUANT_ASYM)
+    k, v = workloads.make_kv(L, H, n, d, seed=6)
+    tier = oracle.assign(ocfg, oracle.score(ocfg, u16(k), u16(v)))
+    good = oracle.pack(ocfg, u16(k), u16(v), tier)
+    geo = oracle.geometry(ocfg)
+    bs = 16
+    nb = workloads.blocks_for(n, bs)
+    bt = workloads.make_block_table(n, bs, nb, seed=6)
+    for off in (geo["chunkidx_off"] + 16 + 12, geo["chunkidx_off"] + 32 + 12, 168):
+        pay = good.copy()
+        pay[off] ^= 0x01
+        okc = np.full((L, nb, bs, H, d), 0xABCD, np.uint16)
+        assert oracle.unpack(ocfg, pay, okc, okc.copy(), bt.numpy(), bs) == oracle.ERR_FORMAT
+        kc, vc, st = gpu_decode(cfg, torch.from_numpy(pay).cuda(), L, H, d, n, bs, nb, bt.cuda())
+        assert st == skv.ERR_FORMAT, off
+        assert bool((kc.view(torch.int16) == -21555).all())
+
+
 def test_malformed_variant_chunk_index_is_refused():
     L, H, d, n = 2, 2, 64, 700
     cfg, ocfg = _pair(L, H, d, n, 0.35, Q.QUANT_GROUP32, Q.QUANT_ASYM | Q.QUANT_FP16)
@@ -90,7 +134,8 @@ SAMPLES = 1500
 
 
 @pytest.mark.parametrize("q8,q4", [(Q.QUANT_GROUP32 | Q.QUANT_FP16, Q.QUANT_ASYM | Q.QUANT_GROUP32),
-                                   (Q.QUANT_FP16, Q.QUANT_FP16)])
+                                   (Q.QUANT_FP16, Q.QUANT_FP16),
+                                   (Q.QUANT_CHANNEL | Q.QUANT_FP16, Q.QUANT_CHANNEL | Q.QUANT_ASYM | Q.QUANT_FP16)])
 def test_full_size_variant(q8, q4):
     w = workloads.WORKLOADS["mistral7b_32k"]
     L, H, d, n = w.layers, w.kv_heads, w.head_dim, w.tokens
@@ -115,21 +160,51 @@ def test_full_size_variant(q8, q4):
     gmeta[144:148] = 0
     assert np.array_equal(gmeta, meta), "header / tier map / chunk index"
     units, _ = oracle.offsets(tier)
+    CH = Q.QUANT_CHANNEL
     e8, e4 = oracle.meta_bytes(q8, d), oracle.meta_bytes(q4, d)
     sb = oracle.scale_offsets(tier, e8, e4)
+    sbk = oracle.scale_offsets(tier, 0 if q8 & CH else e8, 0 if q4 & CH else e4)
+    cb8 = d * oracle.channel_entry_bytes(q8) if q8 & CH else 0
+    cb4 = d * oracle.channel_entry_bytes(q4) if q4 & CH else 0
+    nch = -(-n // 256)
     kh, vh = u16(k), u16(v)
     btn = bt.cpu().numpy()
+    pay = codec.payload
     rng = np.random.default_rng(q8 * 16 + q4)
+    groups = {}
     for (l, kv, h, t) in sample_rows(rng, L, H, n, SAMPLES):
         tr = tier[t]
         q = q8 if tr == oracle.INT8 else q4
-        data, mb, _ = oracle.encode_row_q(tr, q, (kh if kv == 0 else vh)[l, h, t])
         lay = geo["layers_off"] + l * geo["layer_stride"]
-        off = lay + geo["scales_bytes"] + (kv * H + h) * geo["seg_stride"] + int(units[t]) * (d // 2)
-        assert np.array_equal(codec.payload[off:off + data.size].cpu().numpy(), data), (l, kv, h, t, int(tr))
-        if mb.size:
-            mo = lay + (kv * H + h) * geo["seg_scale_bytes"] + int(sb[t])
-            assert np.array_equal(codec.payload[mo:mo + mb.size].cpu().numpy(), mb), ("meta", l, kv, h, t)
+        off = lay + geo["scales_bytes"] + geo["channel_bytes"] + (kv * H + h) * geo["seg_stride"] + int(units[t]) * (d // 2)
         cache = kc if kv == 0 else vc
         grow = cache[l, int(btn[t // bs]), t % bs, h].cpu().numpy().view(np.uint16)
+        if kv == 0 and tr in (oracle.INT8, oracle.INT4) and q & CH:
+            # per-channel K row: the oracle's groups of its chunk, channel by channel
+            c = t // 256
+            key = (l, h, c, int(tr))
+            if key not in groups:
+                rows = [u for u in range(c * 256, min(n, (c + 1) * 256)) if tier[u] == tr]
+                ent, codes = [], np.zeros((len(rows), d), np.int32)
+                for i in range(d):
+                    cc, m, _ = oracle.quant_group(tr, q, kh[l, h, rows, i])
+                    codes[:, i] = cc
+                    ent.append(m)
+                groups[key] = (rows, codes, np.concatenate(ent))
+            rows, codes, block = groups[key]
+            boff = lay + geo["scales_bytes"] + (h * nch + c) * (cb8 + cb4) + (cb8 if tr == oracle.INT4 else 0)
+            assert np.array_equal(pay[boff:boff + block.size].cpu().numpy(), block), ("channel block", key)
+            cj = codes[rows.index(t)]
+            want = (cj & 0xFF).astype(np.uint8) if tr == oracle.INT8 else \
+                ((cj[0::2] & 0xF) | ((cj[1::2] & 0xF) << 4)).astype(np.uint8)
+            data = pay[off:off + want.size].cpu().numpy()
+            assert np.array_equal(data, want), ("channel row", l, h, t)
+            assert np.array_equal(grow, oracle.decode_row_channel(tr, q, d, data, block)), ("cache", l, kv, h, t)
+            continue
+        data, mb, _ = oracle.encode_row_q(tr, q, (kh if kv == 0 else vh)[l, h, t])
+        assert np.array_equal(pay[off:off + data.size].cpu().numpy(), data), (l, kv, h, t, int(tr))
+        if mb.size:
+            base = h * geo["seg_scale_bytes_k"] if kv == 0 else H * geo["seg_scale_bytes_k"] + h * geo["seg_scale_bytes"]
+            mo = lay + base + int((sbk if kv == 0 else sb)[t])
+            assert np.array_equal(pay[mo:mo + mb.size].cpu().numpy(), mb), ("meta", l, kv, h, t)
         assert np.array_equal(grow, oracle.decode_row_q(tr, q, d, data, mb)), ("cache", l, kv, h, t)
