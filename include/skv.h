@@ -179,8 +179,9 @@ typedef struct skv_request {
 /* ABI version of the loaded library (SKV_ABI_VERSION at build time). */
 int32_t skv_abi_version(void);
 
-/* Human-readable name of a status code; never NULL. */
-const char* skv_status_string(skv_status status);
+/* Human-readable name of a status code (any int32 value; values that are not
+ * an skv_status give "unknown status"); never NULL. */
+const char* skv_status_string(int32_t status);
 
 /* Host only, pure.  Tier counts for cfg: sinks pinned first and charged to the
  * budget (Sec. 4.4), then the budget-to-tier mapping of Sec. 4.4 over the

@@ -421,7 +421,7 @@ extern "C" {
 
 int32_t skv_abi_version(void) { return SKV_ABI_VERSION; }
 
-const char* skv_status_string(skv_status status) {
+const char* skv_status_string(int32_t status) {
   switch (status) {
     case SKV_OK: return "ok";
     case SKV_ERR_INVALID_ARG: return "invalid argument";
