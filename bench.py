@@ -145,6 +145,17 @@ def cpu_baseline(w, layers: int):
                       f"{threads} layers, one per thread on {threads} threads ({t4 - t3:.2f} s)"}
 
 
+def input_digest(k, v, seed):
+    """Identifies the seeded synthetic inputs: the generator, its seed and the
+    SHA-256 of layer 0 of K and of V as stored (binary16 bytes)."""
+    import hashlib
+
+    out = {"generator": "paper_2606_08635_amd.workloads.make_kv", "seed": seed}
+    for name, t in (("k", k), ("v", v)):
+        out[f"sha256_layer0_{name}"] = hashlib.sha256(t[0].contiguous().cpu().numpy().tobytes()).hexdigest()
+    return out
+
+
 def _events(count):
     import torch
     return [torch.cuda.Event(enable_timing=True) for _ in range(count)]
@@ -616,6 +627,7 @@ def main():
                    "budget": w.budget, "num_tiers": w.num_tiers, "first_ratio": w.first_ratio, "decay": w.decay,
                    "score": args.score, "block_size": bs, "link": args.link, "fp16_bytes": F,
                    "payload_bytes": codec.payload_bytes},
+        "inputs": input_digest(k, v, seed=0),
         "tokens_per_s": round(n / t_codec, 1),
         "alg_gbps": round(alg_gbs, 2),
         "pct_hbm_peak": round(100 * alg_gbs / HBM_PEAK_GBS, 2),
