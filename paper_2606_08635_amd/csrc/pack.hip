@@ -127,8 +127,10 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
 }
 
 // grid: sum over requests of nchunks * 2 * H * layer_count workgroups.
-// VARIANT: some tier uses a quantizer variant (row_variants.h).
-template <int D, bool VARIANT>
+// VARIANT: some tier uses a quantizer variant (row_variants.h); CHAN: some
+// tier has per-channel keys (its own instantiation, so the register budget of
+// the other paths is unaffected).
+template <int D, bool VARIANT, bool CHAN = false>
 __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   __shared__ ChunkLds s;
   const uint64_t bid = blockIdx.x;
@@ -148,7 +150,7 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   const int t0 = chunk * kChunkTokens;
   // per-channel K tiers: their K rows carry no per-row metadata and use the
   // K-side metadata offsets of the chunk index
-  const bool chan_k = VARIANT && kv == 0 && ((a.q8 | a.q4) & kQuantChannel) != 0;
+  const bool chan_k = CHAN && kv == 0;
 
   // row offsets of this chunk: chunk-index base + block exclusive scan
   const VarCfg var{a.q8, a.q4, kv == 0 ? a.ek8 : a.e8, kv == 0 ? a.ek4 : a.e4};
@@ -167,16 +169,24 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   uint8_t* meta = lay + (kv == 0 ? static_cast<uint64_t>(h) * r.seg_scale_bytes_k
                                  : static_cast<uint64_t>(H) * r.seg_scale_bytes_k + static_cast<uint64_t>(h) * r.seg_scale_bytes);
   uint32_t* nonfinite = reinterpret_cast<uint32_t*>(payload) + kHdrNonfinite;
-  if constexpr (VARIANT) {
+  if constexpr (CHAN) {
     if (chan_k) {
       __shared__ ChanLds<D> c;
       uint8_t* blk = lay + r.scales_bytes + (static_cast<uint64_t>(h) * nchunks + chunk) * (a.cb8 + a.cb4);
-      channel_params<D>(s, c, src, t0, n, var, blk, blk + a.cb8);
-      pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, true>(s, &c, src, dst, meta, nonfinite, t0, n, var);
+      if constexpr (D <= 128) {  // the thread's rows fit in registers: one read of the chunk
+        pack_chunk_chan<D, SKV_PACK_NT_STORE>(s, c, src, dst, meta, nonfinite, t0, n, var, blk, blk + a.cb8);
+      } else {
+        channel_params<D>(s, c, src, t0, var, blk, blk + a.cb8);
+        pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, true>(s, &c, src, dst, meta, nonfinite, t0, n,
+                                                                            var);
+      }
     } else {
       pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, false>(s, nullptr, src, dst, meta, nonfinite, t0, n,
                                                                            var);
     }
+  } else if constexpr (VARIANT) {
+    pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, false>(s, nullptr, src, dst, meta, nonfinite, t0, n,
+                                                                         var);
   } else {
     pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, src, dst, reinterpret_cast<float*>(meta), nonfinite,
                                                               t0, n);
@@ -210,15 +220,20 @@ hipError_t launch_pack(const BatchArgs& a, uint64_t rows, hipStream_t stream) {
     if (e != hipSuccess) return e;
   }
   const bool variant = (a.q8 | a.q4) != 0;
-  switch (a.d * 2 + (variant ? 1 : 0)) {
-    case 64: pack_rows<32, false><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 128: pack_rows<64, false><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 256: pack_rows<128, false><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 512: pack_rows<256, false><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 65: pack_rows<32, true><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 129: pack_rows<64, true><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 257: pack_rows<128, true><<<rows, kRowThreads, 0, stream>>>(a); break;
-    case 513: pack_rows<256, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+  const bool chan = ((a.q8 | a.q4) & kQuantChannel) != 0;
+  switch (a.d * 4 + (chan ? 2 : variant ? 1 : 0)) {
+    case 128: pack_rows<32, false><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 256: pack_rows<64, false><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 512: pack_rows<128, false><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 1024: pack_rows<256, false><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 129: pack_rows<32, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 257: pack_rows<64, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 513: pack_rows<128, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 1025: pack_rows<256, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 130: pack_rows<32, true, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 258: pack_rows<64, true, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 514: pack_rows<128, true, true><<<rows, kRowThreads, 0, stream>>>(a); break;
+    case 1026: pack_rows<256, true, true><<<rows, kRowThreads, 0, stream>>>(a); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -48,14 +48,22 @@ __device__ __forceinline__ uint32_t key_to_half(uint32_t k) {
   return (k & 0x8000u) ? (k & 0x7FFFu) : (~k & 0xFFFFu);
 }
 
-// Reduction over aligned groups of gl lanes (gl a power of two <= LPR); every
-// lane of the wavefront must call it.
+// Reduction over aligned groups of gl lanes (gl a power of two, 4 <= gl <=
+// LPR, uniform over the wavefront); every lane of each group must be active.
+// Quad butterfly and row mirrors as in group_max, chosen by gl.
 template <int LPR, bool MAX>
 __device__ __forceinline__ uint32_t group_reduce(uint32_t v, int gl) {
-#pragma unroll
-  for (int o = 1; o < LPR; o <<= 1) {
-    const uint32_t p = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), o));
-    if (o < gl) v = MAX ? max(v, p) : min(v, p);
+  auto op = [](uint32_t a, uint32_t b) { return MAX ? max(a, b) : min(a, b); };
+  v = op(v, dpp_mov<0xB1>(v));  // quad_perm [1,0,3,2]
+  v = op(v, dpp_mov<0x4E>(v));  // quad_perm [2,3,0,1]
+  if constexpr (LPR >= 8) {
+    if (gl >= 8) v = op(v, dpp_mov<0x141>(v));  // row_half_mirror
+  }
+  if constexpr (LPR >= 16) {
+    if (gl >= 16) v = op(v, dpp_mov<0x140>(v));  // row_mirror
+  }
+  if constexpr (LPR >= 32) {
+    if (gl >= 32) v = op(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 16)));
   }
   return v;
 }
@@ -229,84 +237,96 @@ __device__ __forceinline__ void chunk_layout_var(ChunkLds& s, int tr, const uint
   s.q[threadIdx.x] = cidx_entry[meta_word] + (ex >> 12);
 }
 
-// Reduces the chunk's K rows of each per-channel tier into c (amax, order-key
-// minimum and maximum per channel, rows per tier), then derives the channel
-// parameters and writes the entries: INT8 at blk8, INT4 at blk4 (zeros for a
-// tier without rows in the chunk).  Contains __syncthreads().
+// Per-thread partial reductions of the per-channel tiers (t = 0 INT8, 1 INT4)
+// over the rows the thread holds, for its 8 channels: symmetric tiers keep the
+// largest magnitude bits in a, asymmetric tiers the order-key minimum in a and
+// maximum in b.
+struct ChanAcc {
+  uint32_t a[2][8], b[2][8];
+  uint32_t rows[2];
+};
+
+__device__ __forceinline__ void chan_acc_init(ChanAcc& acc, const VarCfg& v) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const bool asym = ((t == 0 ? v.q8 : v.q4) & kQuantAsym) != 0;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      acc.a[t][e] = asym ? 0xFFFFu : 0u;
+      acc.b[t][e] = 0u;
+    }
+    acc.rows[t] = 0u;
+  }
+}
+
+template <int T>
+__device__ __forceinline__ void chan_acc_row_t(ChanAcc& acc, u32x4 x, bool asym) {
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  ++acc.rows[T];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const uint32_t h = (w[e / 2] >> (16 * (e & 1))) & 0xFFFFu;
+    if (asym) {
+      const uint32_t k = order_key16(h);
+      acc.a[T][e] = min(acc.a[T][e], k);
+      acc.b[T][e] = max(acc.b[T][e], k);
+    } else {
+      acc.a[T][e] = max(acc.a[T][e], h & 0x7FFFu);
+    }
+  }
+}
+
+// Adds the row x of tier tr to acc if tr is a per-channel tier.
+__device__ __forceinline__ void chan_acc_row(ChanAcc& acc, u32x4 x, int tr, const VarCfg& v) {
+  if (tr == kINT8 && (v.q8 & kQuantChannel)) chan_acc_row_t<0>(acc, x, (v.q8 & kQuantAsym) != 0);
+  else if (tr == kINT4 && (v.q4 & kQuantChannel)) chan_acc_row_t<1>(acc, x, (v.q4 & kQuantAsym) != 0);
+}
+
+// Clears the shared reduction arrays (before any chan_combine; the caller
+// synchronizes).
 template <int D>
-__device__ __forceinline__ void channel_params(const ChunkLds& s, ChanLds<D>& c, const uint16_t* __restrict__ src,
-                                               int t0, int n, const VarCfg& v, uint8_t* blk8, uint8_t* blk4) {
-  constexpr int LPR = D / 8;
-  constexpr int RPI = kRowThreads / LPR;
-  constexpr int ITERS = kChunkTokens / RPI;
-  const int lane = threadIdx.x % LPR;
-  const int rsub = threadIdx.x / LPR;
+__device__ __forceinline__ void chan_lds_init(ChanLds<D>& c) {
   for (int i = threadIdx.x; i < 2 * D; i += kRowThreads) {
     (&c.amax[0][0])[i] = 0u;
     (&c.kmin[0][0])[i] = 0xFFFFu;
     (&c.kmax[0][0])[i] = 0u;
   }
   if (threadIdx.x < 2) c.rows[threadIdx.x] = 0u;
-  __syncthreads();
-  const bool ch8 = (v.q8 & kQuantChannel) != 0, ch4 = (v.q4 & kQuantChannel) != 0;
-  uint32_t am[2][8], kn[2][8], kx[2][8];
-#pragma unroll
-  for (int t = 0; t < 2; ++t)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      am[t][e] = 0u;
-      kn[t][e] = 0xFFFFu;
-      kx[t][e] = 0u;
-    }
-  uint32_t rows8 = 0, rows4 = 0;
-#pragma unroll 4
-  for (int it = 0; it < ITERS; ++it) {
-    const int row = it * RPI + rsub;
-    const int tr = s.tier[row];
-    const bool take = (tr == kINT8 && ch8) || (tr == kINT4 && ch4);
-    if (!take) continue;
-    const u32x4 x = *reinterpret_cast<const u32x4*>(src + static_cast<size_t>(t0 + row) * D + lane * 8);
-    const int t = tr == kINT8 ? 0 : 1;
-    rows8 += tr == kINT8;
-    rows4 += tr == kINT4;
-    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t h = (w[e / 2] >> (16 * (e & 1))) & 0xFFFFu;
-      const uint32_t k = order_key16(h);
-      // unrolled over t so the arrays stay in registers
-      if (t == 0) {
-        am[0][e] = max(am[0][e], h & 0x7FFFu);
-        kn[0][e] = min(kn[0][e], k);
-        kx[0][e] = max(kx[0][e], k);
-      } else {
-        am[1][e] = max(am[1][e], h & 0x7FFFu);
-        kn[1][e] = min(kn[1][e], k);
-        kx[1][e] = max(kx[1][e], k);
-      }
-    }
-  }
-  // integer max / min are order-independent: shared-memory atomics keep the result deterministic
+}
+
+// Combines every thread's partials into c with shared-memory integer max/min
+// atomics (order-independent, so deterministic), then derives each channel's
+// parameters and writes its entry (INT8 at blk8, INT4 at blk4; zeros for a
+// tier without rows in the chunk).  Contains __syncthreads().
+template <int D>
+__device__ __forceinline__ void chan_finish(ChanLds<D>& c, const ChanAcc& acc, int lane, const VarCfg& v,
+                                            uint8_t* blk8, uint8_t* blk4) {
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
-    if (!(t == 0 ? ch8 : ch4)) continue;
+    const int32_t q = t == 0 ? v.q8 : v.q4;
+    if (!(q & kQuantChannel)) continue;
+    if (q & kQuantAsym) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      atomicMax(&c.amax[t][lane * 8 + e], am[t][e]);
-      atomicMin(&c.kmin[t][lane * 8 + e], kn[t][e]);
-      atomicMax(&c.kmax[t][lane * 8 + e], kx[t][e]);
+      for (int e = 0; e < 8; ++e) {
+        atomicMin(&c.kmin[t][lane * 8 + e], acc.a[t][e]);
+        atomicMax(&c.kmax[t][lane * 8 + e], acc.b[t][e]);
+      }
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) atomicMax(&c.amax[t][lane * 8 + e], acc.a[t][e]);
     }
-  }
-  if (lane == 0) {
-    if (rows8) atomicAdd(&c.rows[0], rows8);
-    if (rows4) atomicAdd(&c.rows[1], rows4);
+    if (lane == 0 && acc.rows[t]) atomicAdd(&c.rows[t], acc.rows[t]);
   }
   __syncthreads();
   for (int i = threadIdx.x; i < 2 * D; i += kRowThreads) {
     const int t = i / D, ch = i % D;
     const int32_t q = t == 0 ? v.q8 : v.q4;
     if (!(q & kQuantChannel)) continue;
-    GroupParams g = group_params(c.amax[t][ch], c.kmin[t][ch], c.kmax[t][ch], t == 0 ? kINT8 : kINT4, q);
+    uint32_t amax = c.amax[t][ch];
+    const uint32_t kmin = c.kmin[t][ch], kmax = c.kmax[t][ch];
+    // asymmetric groups track order keys only: an inf/NaN is a key beyond +-inf's
+    if (q & kQuantAsym) amax = (kmax >= 0xFC00u || kmin <= 0x03FFu) ? 0x7C00u : 0u;
+    GroupParams g = group_params(amax, kmin, kmax, t == 0 ? kINT8 : kINT4, q);
     if (c.rows[t] == 0u) {  // no row of the tier in this chunk: zero entry
       g.scale = g.r = g.lo = 0.0f;
       g.s16 = g.lo16 = 0u;
@@ -320,9 +340,74 @@ __device__ __forceinline__ void channel_params(const ChunkLds& s, ChanLds<D>& c,
   __syncthreads();
 }
 
+// Per-channel parameters of a chunk whose rows are re-read from src (the
+// rows of a thread do not fit its registers at d = 256).  Contains
+// __syncthreads().
+template <int D>
+__device__ __forceinline__ void channel_params(const ChunkLds& s, ChanLds<D>& c, const uint16_t* __restrict__ src,
+                                               int t0, const VarCfg& v, uint8_t* blk8, uint8_t* blk4) {
+  constexpr int LPR = D / 8;
+  constexpr int RPI = kRowThreads / LPR;
+  constexpr int ITERS = kChunkTokens / RPI;
+  const int lane = threadIdx.x % LPR;
+  const int rsub = threadIdx.x / LPR;
+  chan_lds_init<D>(c);
+  ChanAcc acc;
+  chan_acc_init(acc, v);
+#pragma unroll 4
+  for (int it = 0; it < ITERS; ++it) {
+    const int row = it * RPI + rsub;
+    const int tr = s.tier[row];  // rows at or beyond n are DROP
+    const bool take = (tr == kINT8 && (v.q8 & kQuantChannel)) || (tr == kINT4 && (v.q4 & kQuantChannel));
+    if (!take) continue;
+    chan_acc_row(acc, *reinterpret_cast<const u32x4*>(src + static_cast<size_t>(t0 + row) * D + lane * 8), tr, v);
+  }
+  __syncthreads();  // shared arrays cleared before any atomic
+  chan_finish<D>(c, acc, lane, v, blk8, blk4);
+}
+
+// Quantizes and stores one row held by this lane (x: its 8 elements).  CHAN:
+// rows of a per-channel tier take their codes from c and write no per-row
+// metadata.  Every lane of the wavefront calls it (reductions).
+template <int D, bool NT, bool CHAN>
+__device__ __forceinline__ void pack_row_var(const ChunkLds& s, const ChanLds<D>* c, u32x4 x, int row,
+                                             uint8_t* __restrict__ dst, uint8_t* __restrict__ meta,
+                                             uint32_t* nonfinite, const VarCfg& v, int lane) {
+  constexpr int LPR = D / 8;
+  const int tr = s.tier[row];
+  const bool quant = tr == kINT8 || tr == kINT4;
+  const int32_t q = tr == kINT8 ? v.q8 : v.q4;
+  const bool chan = CHAN && quant && (q & kQuantChannel) != 0;
+  LaneCodes qc;
+  // a row's lanes are one aligned group, so this branch is uniform per row and
+  // the cross-lane reductions below stay inside active lanes
+  if (chan) {
+    const int t = tr == kINT8 ? 0 : 1;
+    const bool asym = (q & kQuantAsym) != 0;
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+    qc.nonfinite = group_max<LPR>(absmax_bits8(x)) >= 0x7C00u;
+    qc.scale = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int ch = lane * 8 + e;
+      const float xv = (e & 1) ? half_hi(w[e / 2]) : half_lo(w[e / 2]);
+      qc.c[e] = group_code(xv, c->r[t][ch], c->lo[t][ch], c->zero[t][ch] != 0u, asym, tr);
+    }
+  } else {
+    qc = quantize_lane_var<LPR>(x, tr, q, lane, meta + s.q[row], quant);
+  }
+  if (tr == kFP16) {
+    store16<NT>(dst + s.off[row] + lane * 16, x);
+  } else if (quant) {
+    if (qc.nonfinite && lane == 0) atomicAdd(nonfinite, 1u);
+    uint8_t* out_row = dst + s.off[row];
+    if (tr == kINT8) store8<NT>(out_row + lane * 8, pack_int8(qc));
+    else store4<NT>(out_row + lane * 4, pack_int4(qc));
+  }
+}
+
 // Packs one chunk of a segment under the variant descriptors.  CHAN: a K
-// segment with a per-channel tier; its rows of that tier take their codes
-// from the channel parameters in c and write no per-row metadata.
+// segment with a per-channel tier whose parameters are already in c.
 template <int D, int ROWS_IN_FLIGHT, bool NT, bool CHAN>
 __device__ __forceinline__ void pack_chunk_var(const ChunkLds& s, const ChanLds<D>* c, const uint16_t* __restrict__ src,
                                                uint8_t* __restrict__ dst, uint8_t* __restrict__ meta,
@@ -344,36 +429,42 @@ __device__ __forceinline__ void pack_chunk_var(const ChunkLds& s, const ChanLds<
       if (t < n && s.tier[row] != kDROP) x[u] = ld_nt16(src + static_cast<size_t>(t) * D + lane * 8);
     }
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int row = (it + u) * RPI + rsub;
-      const int tr = s.tier[row];
-      const bool quant = tr == kINT8 || tr == kINT4;
-      const int32_t q = tr == kINT8 ? v.q8 : v.q4;
-      const bool chan = CHAN && quant && (q & kQuantChannel) != 0;
-      LaneCodes qc = quantize_lane_var<LPR>(x[u], tr, q, lane, meta + s.q[row], quant && !chan);
-      if constexpr (CHAN) {
-        if (chan) {
-          const int t = tr == kINT8 ? 0 : 1;
-          const bool asym = (q & kQuantAsym) != 0;
-          const uint32_t w[4] = {x[u].x, x[u].y, x[u].z, x[u].w};
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int ch = lane * 8 + e;
-            const float xv = (e & 1) ? half_hi(w[e / 2]) : half_lo(w[e / 2]);
-            qc.c[e] = group_code(xv, c->r[t][ch], c->lo[t][ch], c->zero[t][ch] != 0u, asym, tr);
-          }
-        }
-      }
-      if (tr == kFP16) {
-        store16<NT>(dst + s.off[row] + lane * 16, x[u]);
-      } else if (quant) {
-        if (qc.nonfinite && lane == 0) atomicAdd(nonfinite, 1u);
-        uint8_t* out_row = dst + s.off[row];
-        if (tr == kINT8) store8<NT>(out_row + lane * 8, pack_int8(qc));
-        else store4<NT>(out_row + lane * 4, pack_int4(qc));
-      }
-    }
+    for (int u = 0; u < U; ++u)
+      pack_row_var<D, NT, CHAN>(s, c, x[u], (it + u) * RPI + rsub, dst, meta, nonfinite, v, lane);
   }
+}
+
+// K segment with a per-channel tier, d <= 128: the thread's rows of the chunk
+// (at most 16) are loaded once into registers, reduced per channel, and then
+// quantized from the same registers.  Contains __syncthreads().
+template <int D, bool NT>
+__device__ __forceinline__ void pack_chunk_chan(const ChunkLds& s, ChanLds<D>& c, const uint16_t* __restrict__ src,
+                                                uint8_t* __restrict__ dst, uint8_t* __restrict__ meta,
+                                                uint32_t* nonfinite, int t0, int n, const VarCfg& v, uint8_t* blk8,
+                                                uint8_t* blk4) {
+  constexpr int LPR = D / 8;
+  constexpr int RPI = kRowThreads / LPR;
+  constexpr int ITERS = kChunkTokens / RPI;
+  static_assert(ITERS <= 16, "rows of a thread held in registers");
+  const int lane = threadIdx.x % LPR;
+  const int rsub = threadIdx.x / LPR;
+  u32x4 x[ITERS];
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int row = it * RPI + rsub;
+    const int t = t0 + row;
+    x[it] = u32x4{0u, 0u, 0u, 0u};
+    if (t < n && s.tier[row] != kDROP) x[it] = ld_nt16(src + static_cast<size_t>(t) * D + lane * 8);
+  }
+  chan_lds_init<D>(c);
+  ChanAcc acc;
+  chan_acc_init(acc, v);
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) chan_acc_row(acc, x[it], s.tier[it * RPI + rsub], v);
+  __syncthreads();  // shared arrays cleared before any atomic
+  chan_finish<D>(c, acc, lane, v, blk8, blk4);
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) pack_row_var<D, NT, true>(s, &c, x[it], it * RPI + rsub, dst, meta, nonfinite, v, lane);
 }
 
 // The lane's 8 outputs of a quantized row under descriptor q.

@@ -123,8 +123,9 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
 }
 
 // grid: sum over requests of nchunks * 2 * H * layer_count workgroups.
-// VARIANT: some tier uses a quantizer variant (row_variants.h).
-template <int D, bool VARIANT>
+// VARIANT: some tier uses a quantizer variant (row_variants.h); CHAN: some
+// tier has per-channel keys (its own instantiation).
+template <int D, bool VARIANT, bool CHAN = false>
 __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, uint16_t* __restrict__ k_cache,
                                                            uint16_t* __restrict__ v_cache, int num_blocks,
                                                            int block_size) {
@@ -145,7 +146,7 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
   const int t0 = chunk * kChunkTokens;
   // per-channel K tiers: K rows of those tiers decode with the chunk's channel
   // entries and use the K-side metadata offsets of the chunk index
-  const bool chan_k = VARIANT && kv == 0 && ((a.q8 | a.q4) & kQuantChannel) != 0;
+  const bool chan_k = CHAN && kv == 0;
   const VarCfg var{a.q8, a.q4, kv == 0 ? a.ek8 : a.e8, kv == 0 ? a.ek4 : a.e4};
   {
     const int t = t0 + threadIdx.x;
@@ -170,7 +171,7 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
                                              static_cast<uint64_t>(h) * r.seg_scale_bytes);
   uint16_t* cache = (kv ? v_cache : k_cache) + static_cast<size_t>(l) * num_blocks * block_size * H * D +
                     static_cast<size_t>(h) * D;
-  if constexpr (VARIANT) {
+  if constexpr (CHAN) {
     if (chan_k) {
       __shared__ ChanDecLds<D> c;
       const uint8_t* blk = lay + r.scales_bytes + (static_cast<uint64_t>(h) * nchunks + chunk) * (a.cb8 + a.cb4);
@@ -179,6 +180,8 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
     } else {
       unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, false>(s, nullptr, src, meta, cache, H, var);
     }
+  } else if constexpr (VARIANT) {
+    unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, false>(s, nullptr, src, meta, cache, H, var);
   } else {
     unpack_chunk<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, reinterpret_cast<const float*>(meta),
                                                                      cache, H);
@@ -195,17 +198,22 @@ hipError_t launch_unpack(const BatchArgs& a, uint64_t rows, uint16_t* k_cache, u
     if (e != hipSuccess) return e;
   }
   const bool variant = (a.q8 | a.q4) != 0;
-#define SKV_UNPACK_LAUNCH(D, V) \
-  unpack_rows<D, V><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size)
-  switch (a.d * 2 + (variant ? 1 : 0)) {
-    case 64: SKV_UNPACK_LAUNCH(32, false); break;
-    case 128: SKV_UNPACK_LAUNCH(64, false); break;
-    case 256: SKV_UNPACK_LAUNCH(128, false); break;
-    case 512: SKV_UNPACK_LAUNCH(256, false); break;
-    case 65: SKV_UNPACK_LAUNCH(32, true); break;
-    case 129: SKV_UNPACK_LAUNCH(64, true); break;
-    case 257: SKV_UNPACK_LAUNCH(128, true); break;
-    case 513: SKV_UNPACK_LAUNCH(256, true); break;
+  const bool chan = ((a.q8 | a.q4) & kQuantChannel) != 0;
+#define SKV_UNPACK_LAUNCH(D, V, C) \
+  unpack_rows<D, V, C><<<rows, kRowThreads, 0, stream>>>(a, k_cache, v_cache, num_blocks, block_size)
+  switch (a.d * 4 + (chan ? 2 : variant ? 1 : 0)) {
+    case 128: SKV_UNPACK_LAUNCH(32, false, false); break;
+    case 256: SKV_UNPACK_LAUNCH(64, false, false); break;
+    case 512: SKV_UNPACK_LAUNCH(128, false, false); break;
+    case 1024: SKV_UNPACK_LAUNCH(256, false, false); break;
+    case 129: SKV_UNPACK_LAUNCH(32, true, false); break;
+    case 257: SKV_UNPACK_LAUNCH(64, true, false); break;
+    case 513: SKV_UNPACK_LAUNCH(128, true, false); break;
+    case 1025: SKV_UNPACK_LAUNCH(256, true, false); break;
+    case 130: SKV_UNPACK_LAUNCH(32, true, true); break;
+    case 258: SKV_UNPACK_LAUNCH(64, true, true); break;
+    case 514: SKV_UNPACK_LAUNCH(128, true, true); break;
+    case 1026: SKV_UNPACK_LAUNCH(256, true, true); break;
     default: return hipErrorInvalidValue;
   }
 #undef SKV_UNPACK_LAUNCH
