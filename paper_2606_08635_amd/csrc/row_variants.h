@@ -467,6 +467,16 @@ __device__ __forceinline__ void pack_chunk_chan(const ChunkLds& s, ChanLds<D>& c
   for (int it = 0; it < ITERS; ++it) pack_row_var<D, NT, true>(s, &c, x[it], it * RPI + rsub, dst, meta, nonfinite, v, lane);
 }
 
+// Two binary32 values rounded to binary16 and packed low|high, any NaN as the
+// canonical 0x7E00 (a payload whose metadata was corrupted can make code * s
+// + lo a NaN of any sign and payload; the decoded cache then still matches a
+// reference that writes every NaN as 0x7E00).
+__device__ __forceinline__ uint32_t pack_half2_canon(float a, float b) {
+  const uint32_t ha = __builtin_isnan(a) ? 0x7E00u : __builtin_bit_cast(uint16_t, static_cast<_Float16>(a));
+  const uint32_t hb = __builtin_isnan(b) ? 0x7E00u : __builtin_bit_cast(uint16_t, static_cast<_Float16>(b));
+  return ha | (hb << 16);
+}
+
 // The lane's 8 outputs of a quantized row under descriptor q.
 template <int LPR>
 __device__ __forceinline__ u32x4 decode_lane_var(int tr, int32_t q, u32x4 raw, const uint8_t* meta, int lane) {
@@ -497,7 +507,8 @@ __device__ __forceinline__ u32x4 decode_lane_var(int tr, int32_t q, u32x4 raw, c
     f[i] = static_cast<float>(code) * s;
     if (asym) f[i] = f[i] + lo;
   }
-  return u32x4{pack_half2(f[0], f[1]), pack_half2(f[2], f[3]), pack_half2(f[4], f[5]), pack_half2(f[6], f[7])};
+  return u32x4{pack_half2_canon(f[0], f[1]), pack_half2_canon(f[2], f[3]), pack_half2_canon(f[4], f[5]),
+               pack_half2_canon(f[6], f[7])};
 }
 
 // Per-channel K parameters of one chunk on the decode side: scale and
@@ -554,7 +565,7 @@ __device__ __forceinline__ u32x4 decode_lane_chan(int tr, int32_t q, u32x4 raw, 
     const float s = sc[lane * 8 + i];
     float f = static_cast<float>(code) * s;
     if (asym) f = f + lo[lane * 8 + i];
-    h[i] = __builtin_isnan(s) ? 0x7E00u : static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(f)));
+    h[i] = __builtin_isnan(f) ? 0x7E00u : static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(f)));
   }
   return u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
 }
