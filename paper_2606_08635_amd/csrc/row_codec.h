@@ -80,15 +80,28 @@ __device__ __forceinline__ uint32_t pack_int4(const LaneCodes& q) {
 }
 
 // 8 signed codes times the row scale, rounded to binary32 and then to binary16.
+// code * s rounded to binary32 (the value the binary16 conversion then
+// rounds).  The register pin keeps the product a binary32 value: left free,
+// the backend folds multiply and conversion into one mixed-precision FMA that
+// rounds the exact product straight to binary16.  The two agree for every
+// scale the quantizer produces (RN32(a / Q), checked exhaustively over a and
+// the codes), but not for arbitrary scales, such as a payload's corrupted or
+// externally written ones.
+__device__ __forceinline__ float scaled(float code, float s) {
+  float p = code * s;
+  asm("" : "+v"(p));
+  return p;
+}
+
 __device__ __forceinline__ u32x4 dequant_int8(u32x2 c, float s) {
   const uint32_t w[2] = {c.x, c.y};
   uint32_t o[4];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
-    const float f0 = static_cast<float>(static_cast<int32_t>(w[i] << 24) >> 24) * s;
-    const float f1 = static_cast<float>(static_cast<int32_t>(w[i] << 16) >> 24) * s;
-    const float f2 = static_cast<float>(static_cast<int32_t>(w[i] << 8) >> 24) * s;
-    const float f3 = static_cast<float>(static_cast<int32_t>(w[i]) >> 24) * s;
+    const float f0 = scaled(static_cast<float>(static_cast<int32_t>(w[i] << 24) >> 24), s);
+    const float f1 = scaled(static_cast<float>(static_cast<int32_t>(w[i] << 16) >> 24), s);
+    const float f2 = scaled(static_cast<float>(static_cast<int32_t>(w[i] << 8) >> 24), s);
+    const float f3 = scaled(static_cast<float>(static_cast<int32_t>(w[i]) >> 24), s);
     o[2 * i] = pack_half2(f0, f1);
     o[2 * i + 1] = pack_half2(f2, f3);
   }
@@ -99,8 +112,8 @@ __device__ __forceinline__ u32x4 dequant_int4(uint32_t w, float s) {
   uint32_t o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const float f0 = static_cast<float>(static_cast<int32_t>(w << (28 - 8 * i)) >> 28) * s;
-    const float f1 = static_cast<float>(static_cast<int32_t>(w << (24 - 8 * i)) >> 28) * s;
+    const float f0 = scaled(static_cast<float>(static_cast<int32_t>(w << (28 - 8 * i)) >> 28), s);
+    const float f1 = scaled(static_cast<float>(static_cast<int32_t>(w << (24 - 8 * i)) >> 28), s);
     o[i] = pack_half2(f0, f1);
   }
   return u32x4{o[0], o[1], o[2], o[3]};

@@ -1,14 +1,19 @@
 """Corrupted payloads: the GPU decoder agrees with the oracle on every one.
 
-Seeded single-byte corruptions anywhere in a payload (header, tier map,
+Seeded single-bit corruptions anywhere in a payload (header, tier map,
 chunk index, per-row metadata, per-channel entries, codes) for the default
-and a variant layout.  For each, the oracle's unpack either refuses the
+and a variant layout, and in upgrade payloads (both modes) and grouped
+payloads.  For each, the oracle's unpack either refuses the
 payload (format error) or decodes it; the GPU must return the same status,
 leave the caches untouched when it refuses, and otherwise write exactly the
 oracle's bytes (corrupted scales included: NaN, infinities and overflow
 follow IEEE arithmetic on both sides).  Every offset the GPU decoder follows
 comes from the header, chunk index and 2-bit map it has validated, so no
 corruption can move a read outside the payload.
+
+A directed case replaces every scale with one the quantizer never produces,
+where rounding the product once to binary16 and rounding it to binary32
+first disagree: the decoder must take the oracle's two roundings.
 """
 import pytest
 
@@ -17,6 +22,13 @@ from gpu_helpers import *  # noqa: F401,F403
 pytestmark = pytest.mark.gpu
 
 TRIALS = 120
+
+
+def same(got, want, what):
+    """Equality of two uint16 arrays, reporting the first differing elements."""
+    bad = np.argwhere(got != want)
+    assert bad.size == 0, (f"{what}: {len(bad)} elements differ; first {bad[:4].tolist()} "
+                           f"got {[hex(got[tuple(i)]) for i in bad[:4]]} want {[hex(want[tuple(i)]) for i in bad[:4]]}")
 
 
 @pytest.mark.parametrize("q8,q4", [(0, 0), (skv.QUANT_CHANNEL | skv.QUANT_FP16, skv.QUANT_GROUP32 | skv.QUANT_ASYM)])
@@ -43,7 +55,133 @@ def test_random_corruptions_match_oracle(q8, q4):
         okc, ovc, ost = oracle_decode(ocfg, pay, L, H, d, bs, nb, btn)
         kc, vc, gst = gpu_decode(cfg, torch.from_numpy(pay).cuda(), L, H, d, n, bs, nb, btd)
         assert gst == ost, (i, int(off), gst, ost)
-        assert np.array_equal(u16(kc), okc) and np.array_equal(u16(vc), ovc), (i, int(off))
+        same(u16(kc), okc, f"trial {i} offset {int(off)} K")
+        same(u16(vc), ovc, f"trial {i} offset {int(off)} V")
         refused += ost != 0
     # the metadata corruptions are nearly all caught (the non-finite counter and padding are not checked)
     assert refused >= TRIALS // 4, refused
+
+
+@pytest.mark.parametrize("mode", [skv.UPGRADE_FP16, skv.UPGRADE_RESIDUAL8])
+def test_random_upgrade_corruptions_match_oracle(mode):
+    """Upgrade payloads: the decoder applies or refuses exactly as the oracle."""
+    L, H, d, n, bs = 2, 2, 64, 700, 16
+    say(f"fuzz upgrade mode={mode}")
+    cfg, ocfg = configs(L, H, d, n, 0.3, 3)
+    k, v = workloads.make_kv(L, H, n, d, seed=31)
+    tier = oracle.assign(ocfg, oracle.score(ocfg, u16(k), u16(v)))
+    rng = np.random.default_rng(77 + mode)
+    tokens = np.sort(rng.choice(n, size=300, replace=False)).astype(np.int32)
+    good = oracle.pack_upgrade(ocfg, u16(k), u16(v), tier, tokens, mode)
+    payload = oracle.pack(ocfg, u16(k), u16(v), tier)
+    nb = workloads.blocks_for(n, bs) + 1
+    bt = workloads.make_block_table(n, bs, nb, seed=31)
+    base_k, base_v, st = oracle_decode(ocfg, payload, L, H, d, bs, nb, bt.numpy())
+    assert st == 0
+    for i in range(60):
+        pay = good.copy()
+        off = int(rng.integers(0, pay.size)) if i % 2 else int(rng.integers(0, min(pay.size, 4096)))
+        pay[off] ^= np.uint8(1 << int(rng.integers(0, 8)))
+        okc, ovc = base_k.copy(), base_v.copy()
+        ost = oracle.unpack_upgrade(ocfg, pay, okc, ovc, bt.numpy(), bs)
+        kc = torch.from_numpy(base_k.view(np.int16)).cuda().view(torch.float16)
+        vc = torch.from_numpy(base_v.view(np.int16)).cuda().view(torch.float16)
+        ust = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+        skv.unpack_upgrade(cfg, torch.from_numpy(pay).cuda(), tokens.size, mode, kc, vc, bt.cuda(), bs, ust)
+        torch.cuda.synchronize()
+        assert int(ust.item()) == (0 if ost == 0 else skv.ERR_FORMAT), (i, off, int(ust.item()), ost)
+        same(u16(kc), okc, f"trial {i} offset {off} K")
+        same(u16(vc), ovc, f"trial {i} offset {off} V")
+
+
+def test_random_grouped_corruptions_match_oracle():
+    """Grouped payloads (one map per layer): refused or decoded exactly as the oracle."""
+    L, H, d, n, bs = 3, 2, 64, 700, 16
+    say("fuzz grouped")
+    gran = oracle.GRAN_LAYER
+    budgets = np.float32([0.8, 0.45, 0.2])
+    cfg, ocfg = configs(L, H, d, n, 0.5, 3)
+    groups = skv.Groups(gran, budgets)
+    ws = torch.empty(skv.group_workspace_size(cfg, groups), dtype=torch.uint8, device="cuda")
+    skv.prepare_groups(cfg, groups, ws)
+    k, v = workloads.make_kv(L, H, n, d, seed=41)
+    otier = oracle.assign_groups(ocfg, gran, oracle.score_groups(ocfg, gran, u16(k), u16(v)), budgets)
+    good = oracle.pack_groups(ocfg, gran, u16(k), u16(v), otier, budgets)
+    nb = workloads.blocks_for(n, bs) + 1
+    bt = workloads.make_block_table(n, bs, nb, seed=41)
+    rng = np.random.default_rng(4141)
+    for i in range(80):
+        pay = good.copy()
+        off = int(rng.integers(0, pay.size)) if i % 2 else int(rng.integers(0, min(pay.size, 8192)))
+        pay[off] ^= np.uint8(1 << int(rng.integers(0, 8)))
+        okc = np.full((L, nb, bs, H, d), 0xABCD, np.uint16)
+        ovc = okc.copy()
+        ost = oracle.unpack_groups(ocfg, gran, pay, okc, ovc, bt.numpy(), bs, budgets)
+        kc, vc = caches(L, nb, bs, H, d, "cuda")
+        st = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+        skv.unpack_groups(cfg, groups, ws, torch.from_numpy(pay).cuda(), kc, vc, bt.cuda(), bs, st)
+        torch.cuda.synchronize()
+        assert int(st.item()) == (0 if ost == 0 else skv.ERR_FORMAT), (i, off, int(st.item()), ost)
+        same(u16(kc), okc, f"trial {i} offset {off} K")
+        same(u16(vc), ovc, f"trial {i} offset {off} V")
+
+
+# Scales the quantizer never produces (it writes RN32(amax / Q)), chosen so
+# that code * scale rounded once to binary16 differs from rounding it to
+# binary32 first at the codes +-Q, which every quantized row holds.
+FOREIGN_SCALES = {oracle.INT8: 0x3D92F5EC, oracle.INT4: 0x3EFFA492}
+
+
+@pytest.mark.parametrize("grouped", [False, True])
+def test_foreign_scales_decode_like_the_oracle(grouped):
+    """Every INT8 / INT4 scale replaced by a foreign one: the decoder rounds the
+    product to binary32 before the binary16 conversion, as the oracle does."""
+    L, H, d, n, bs = 2, 2, 64, 700, 16
+    say(f"foreign scales grouped={grouped}")
+    cfg, ocfg = configs(L, H, d, n, 0.35, 3)
+    k, v = workloads.make_kv(L, H, n, d, seed=5)
+    nb = workloads.blocks_for(n, bs) + 1
+    bt = workloads.make_block_table(n, bs, nb, seed=5)
+    if grouped:
+        gran, budgets = oracle.GRAN_LAYER, np.float32([0.6, 0.3])
+        tiers = oracle.assign_groups(ocfg, gran, oracle.score_groups(ocfg, gran, u16(k), u16(v)), budgets)
+        pay = oracle.pack_groups(ocfg, gran, u16(k), u16(v), tiers, budgets)
+        segtab_off = int(pay[104:112].view(np.uint64)[0])
+        segtab = pay[segtab_off:segtab_off + 32 * L * H].view(np.uint64)
+        base = lambda l, kv, h: int(segtab[2 * ((l * 2 + kv) * H + h)])  # noqa: E731
+    else:
+        tier = oracle.assign(ocfg, oracle.score(ocfg, u16(k), u16(v)))
+        tiers = np.stack([tier] * L)
+        pay = oracle.pack(ocfg, u16(k), u16(v), tier)
+        geo = oracle.geometry(ocfg)
+        base = lambda l, kv, h: geo["layers_off"] + l * geo["layer_stride"] + (kv * H + h) * geo["nq"] * 4  # noqa: E731
+    words = pay.view(np.uint32)
+    replaced = 0
+    for l in range(L):
+        _, qrank = oracle.offsets(tiers[l])
+        for kv in range(2):
+            for h in range(H):
+                b4 = base(l, kv, h) // 4
+                for tr, bits in FOREIGN_SCALES.items():
+                    sel = tiers[l] == tr
+                    words[b4 + qrank[sel].astype(np.int64)] = bits
+                    replaced += int(sel.sum())
+    assert replaced > 0
+    okc = np.full((L, nb, bs, H, d), 0xABCD, np.uint16)
+    ovc = okc.copy()
+    if grouped:
+        ost = oracle.unpack_groups(ocfg, gran, pay, okc, ovc, bt.numpy(), bs, budgets)
+        groups = skv.Groups(gran, budgets)
+        ws = torch.empty(skv.group_workspace_size(cfg, groups), dtype=torch.uint8, device="cuda")
+        skv.prepare_groups(cfg, groups, ws)
+        kc, vc = caches(L, nb, bs, H, d, "cuda")
+        st = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+        skv.unpack_groups(cfg, groups, ws, torch.from_numpy(pay).cuda(), kc, vc, bt.cuda(), bs, st)
+        torch.cuda.synchronize()
+        gst = int(st.item())
+    else:
+        ost = oracle.unpack(ocfg, pay, okc, ovc, bt.numpy(), bs)
+        kc, vc, gst = gpu_decode(cfg, torch.from_numpy(pay).cuda(), L, H, d, n, bs, nb, bt.cuda())
+    assert ost == 0 and gst == 0
+    same(u16(kc), okc, "K")
+    same(u16(vc), ovc, "V")

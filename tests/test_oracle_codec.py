@@ -193,3 +193,28 @@ def test_nonfinite_rows_are_counted():
     v[0, 0, 9, 0] = -np.inf
     payload = oracle.pack(cfg, k.view(np.uint16), v.view(np.uint16), tier)
     assert payload[:256].view(np.uint32)[36] == 2
+
+
+# Scales the quantizer never produces, chosen so that code * scale rounded once
+# to binary16 differs from rounding it to binary32 first: the decoder's product
+# is a binary32 value, then converted (round to nearest even at both steps).
+FOREIGN_SCALES = {oracle.INT8: (0x3D92F5EC, 127), oracle.INT4: (0x3EFFA492, 7)}
+
+
+@pytest.mark.parametrize("tier", [oracle.INT8, oracle.INT4])
+def test_decode_rounds_the_product_to_binary32_first(tier):
+    bits, code = FOREIGN_SCALES[tier]
+    s = np.uint32(bits).view(np.float32)
+    twice = np.float16(np.float32(code) * s).view(np.uint16)
+    once = np.float16(np.float64(code) * np.float64(s)).view(np.uint16)
+    assert twice != once  # the case discriminates the two readings
+    d = 32
+    codes = np.zeros(d, np.int64)
+    codes[3], codes[4] = code, -code
+    if tier == oracle.INT8:
+        data = codes.astype(np.int8).view(np.uint8)
+    else:
+        data = ((codes[0::2] & 0xF) | ((codes[1::2] & 0xF) << 4)).astype(np.uint8)
+    y = oracle.decode_row(tier, d, data, float(s))
+    assert y[3] == twice and y[4] == (twice ^ 0x8000)
+    assert np.all(np.delete(y, [3, 4]) == 0)
