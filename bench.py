@@ -6,8 +6,10 @@ assign tiers -> pack -> emulated link (device-to-device copy of the payload)
 timed region.  The reported metric is the paper-shaped codec throughput:
 fp16-equivalent bytes F = 4 L H d n per (pack + unpack) second.  Per-stage
 times come from HIP events recorded on the stream the library launches on;
-before each stage a 1 GiB write evicts the 256 MB Infinity Cache (outside the
-events; --no-flush skips it).  The line also carries the p10/p50/p90 of the
+before each stage a 1 GiB write evicts the 256 MB Infinity Cache and the L2s,
+then a 1 GiB read evicts the write's own dirty lines, so a stage neither reads
+what the previous one left in cache nor pays for writing the flush back
+(outside the events; --no-flush skips it).  The line also carries the p10/p50/p90 of the
 per-step pack + unpack time, a same-process device copy of F bytes as the
 achievable-bandwidth reference, and the oracle's host rate on one thread and
 on every host thread (cpu_baseline).
@@ -33,8 +35,8 @@ CSRC = os.path.join(ROOT, "paper_2606_08635_amd", "csrc")
 # kernel sources they were taken on: the first 16 hex digits of SHA-256 over
 # the kernel's .hip file and every header of the library (source_digest).
 MEASURED_TRAFFIC = {
-    ("mistral7b_32k", "pack"): (6.5086e9, "pack.hip", "fcb56decc063f590"),
-    ("mistral7b_32k", "unpack"): (6.5125e9, "unpack.hip", "1cf142bd1fcc92fc"),
+    ("mistral7b_32k", "pack"): (6.5084e9, "pack.hip", "045ef78396a9423a"),
+    ("mistral7b_32k", "unpack"): (6.5125e9, "unpack.hip", "76d66077509e35dc"),
 }
 
 
@@ -486,7 +488,7 @@ def main():
                     help="importance statistic; attn uses a W-query observation window per query head")
     ap.add_argument("--obs-window", type=int, default=32)
     ap.add_argument("--no-flush", dest="flush_cache", action="store_false",
-                    help="do not evict the Infinity Cache (1 GiB write) before each stage")
+                    help="do not evict the caches (1 GiB write, then 1 GiB read) before each stage")
     ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade", "groups", "quant"], default="step",
                     help="step: the headline codec step; batch: per-request vs batched launches over "
                          "a multi-request workload; pipeline: layer-pipelined handoff latency; "
@@ -553,9 +555,12 @@ def main():
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
-    # A 1 GiB write between stages evicts the 256 MB Infinity Cache, so no stage
-    # reads what the previous one left there; it runs outside the stage events.
+    # Between stages, outside the stage events: a 1 GiB write evicts the 256 MB
+    # Infinity Cache and the L2s, so no stage reads what the previous one left
+    # there; a 1 GiB read then evicts the write's dirty lines, so no stage pays
+    # for writing the flush back.
     flush_buf = torch.empty(1 << 30, dtype=torch.uint8, device=dev) if args.flush_cache else None
+    flush_read = torch.ones(1 << 28, dtype=torch.float32, device=dev) if args.flush_cache else None
     names = ["score", "assign", "pack", "link", "unpack"]
 
     def step(ev=None):
@@ -567,6 +572,7 @@ def main():
         for i, call in enumerate(calls):
             if flush_buf is not None:
                 flush_buf.fill_(i)
+                flush_read.sum()
             if ev: ev[2 * i].record(stream)
             call()
             if ev: ev[2 * i + 1].record(stream)
@@ -654,7 +660,7 @@ def main():
         out["score_kvnorm"] = {"ms": round(stage_ms["score"], 4),
                                "read_gbps": round(F / (stage_ms["score"] / 1e3) / 1e9, 2)}
     if args.cpu_layers > 0:
-        del kc, vc, rx, flush_buf
+        del kc, vc, rx, flush_buf, flush_read
         torch.cuda.empty_cache()
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_layers)
     print(json.dumps(out), flush=True)

@@ -203,7 +203,6 @@ __global__ __launch_bounds__(kRowThreads) void gpack_rows(const GroupArgs a) {
   __shared__ ChunkLds s;
   uint8_t* __restrict__ payload = a.payload;
   uint32_t* hdr = reinterpret_cast<uint32_t*>(payload);
-  if (hdr[kGHdrStatus] != 0u) return;  // a tier map is off its plan: nothing to pack
   const int n = a.n, H = a.H, nchunks = a.nchunks;
   const int chunk = static_cast<int>(blockIdx.x % static_cast<unsigned>(nchunks));
   const int seg = static_cast<int>(blockIdx.x / static_cast<unsigned>(nchunks));  // (l * 2 + kv) * H + h
@@ -211,6 +210,11 @@ __global__ __launch_bounds__(kRowThreads) void gpack_rows(const GroupArgs a) {
   const int g = group_of(a, l, h);
   const int t0 = chunk * kChunkTokens;
   const uint8_t* tier = a.tier + static_cast<size_t>(g) * n;
+  const uint16_t* src = (kv ? a.v : a.k) + (static_cast<size_t>(l) * H + h) * static_cast<size_t>(n) * D;
+  // the first rows are loaded before the status check and the layout scan
+  RowBatch<D, SKV_PACK_ROWS_IN_FLIGHT> first;
+  pack_first_batch<D, SKV_PACK_ROWS_IN_FLIGHT>(first, src, tier, t0, n);
+  if (hdr[kGHdrStatus] != 0u) return;  // a tier map is off its plan: nothing to pack
   {
     const int t = t0 + threadIdx.x;
     chunk_layout<D>(s, t < n ? tier[t] : kDROP,
@@ -220,9 +224,9 @@ __global__ __launch_bounds__(kRowThreads) void gpack_rows(const GroupArgs a) {
   }
   __syncthreads();
   const uint64_t sc_off = a.segtab[2 * seg], row_off = a.segtab[2 * seg + 1];
-  const uint16_t* src = (kv ? a.v : a.k) + (static_cast<size_t>(l) * H + h) * static_cast<size_t>(n) * D;
   uint8_t* dst = payload + row_off;
-  pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, src, dst, reinterpret_cast<float*>(payload + sc_off),
+  pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, first, src, dst,
+                                                            reinterpret_cast<float*>(payload + sc_off),
                                                             hdr + kGHdrNonfinite, t0, n);
   const uint32_t* e = a.group_table + 8 * g;
   if (chunk == nchunks - 1) {  // segment tail

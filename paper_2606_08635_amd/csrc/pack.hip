@@ -137,7 +137,6 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   const ReqDesc& r = a.r[request_of_block(a, bid)];
   uint8_t* __restrict__ payload = r.payload;
   const uint32_t* hdr = reinterpret_cast<const uint32_t*>(payload);
-  if (hdr[kHdrStatus] != 0u) return;  // tier map off plan: nothing to pack
 
   const int n = r.n, H = a.H, nchunks = r.nchunks;
   // a launch has fewer than 2^32 workgroups: 32-bit index arithmetic
@@ -148,6 +147,12 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   const int kv = (seg / H) & 1;
   const int l = a.layer_begin + seg / (2 * H);
   const int t0 = chunk * kChunkTokens;
+  const uint16_t* src = (kv ? r.v : r.k) + (static_cast<size_t>(l) * H + h) * static_cast<size_t>(n) * D;
+  // default quantizer: the first rows are loaded before the status check and
+  // the layout scan (the reads stay inside K/V whatever the status)
+  RowBatch<D, SKV_PACK_ROWS_IN_FLIGHT> first;
+  if constexpr (!VARIANT) pack_first_batch<D, SKV_PACK_ROWS_IN_FLIGHT>(first, src, r.tier, t0, n);
+  if (hdr[kHdrStatus] != 0u) return;  // tier map off plan: nothing to pack
   // per-channel K tiers: their K rows carry no per-row metadata and use the
   // K-side metadata offsets of the chunk index
   const bool chan_k = CHAN && kv == 0;
@@ -163,7 +168,6 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   }
   __syncthreads();
 
-  const uint16_t* src = (kv ? r.v : r.k) + (static_cast<size_t>(l) * H + h) * static_cast<size_t>(n) * D;
   uint8_t* lay = payload + r.layers_off + static_cast<uint64_t>(l) * r.layer_stride;
   uint8_t* dst = lay + r.scales_bytes + r.channel_bytes + static_cast<uint64_t>(kv * H + h) * r.seg_stride;
   uint8_t* meta = lay + (kv == 0 ? static_cast<uint64_t>(h) * r.seg_scale_bytes_k
@@ -188,8 +192,8 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
     pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, false>(s, nullptr, src, dst, meta, nonfinite, t0, n,
                                                                          var);
   } else {
-    pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, src, dst, reinterpret_cast<float*>(meta), nonfinite,
-                                                              t0, n);
+    pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, first, src, dst, reinterpret_cast<float*>(meta),
+                                                              nonfinite, t0, n);
   }
 
   // padding: segment tail (last chunk), the layer's per-row metadata tail and

@@ -4,8 +4,10 @@
 //   chunk_layout_*  give every token of the chunk its tier, the byte offset
 //                   of its row inside the segment and the index of its scale
 //                   (chunk-index base + a block scan of the row widths);
-//   pack_chunk      reads the chunk's rows (d/8 lanes per row, 16 bytes each,
-//                   several rows in flight), quantizes and stores them;
+//   pack_first_batch / pack_chunk
+//                   read the chunk's rows (d/8 lanes per row, 16 bytes each,
+//                   several rows in flight; the first batch is issued before
+//                   the layout scan), quantize and store them;
 //   unpack_chunk    loads the rows at their tier widths, dequantizes and
 //                   writes them into their paged slots.
 #pragma once
@@ -41,16 +43,44 @@ __device__ __forceinline__ void chunk_layout(ChunkLds& s, int tr, const uint32_t
   s.q[threadIdx.x] = cidx_entry[1] + (ex >> 16);
 }
 
-// Quantizes and stores the rows of one chunk.  src: the segment's plane
-// [n][D]; dst: the segment's rows; scales: the segment's scales.
+// The rows a thread quantizes in one batch: lanes per row (16 bytes each),
+// rows per block-wide iteration, iterations per chunk, rows in flight.
+template <int D, int ROWS_IN_FLIGHT>
+struct RowBatch {
+  static constexpr int LPR = D / 8;
+  static constexpr int RPI = kRowThreads / LPR;
+  static constexpr int ITERS = kChunkTokens / RPI;
+  static constexpr int U = ITERS < ROWS_IN_FLIGHT ? ITERS : ROWS_IN_FLIGHT;
+  u32x4 x[U];
+};
+
+// Issues the loads of a thread's first batch of rows of the chunk at t0,
+// taking their tiers from the caller's tier map (tier[t], t < n) rather than
+// from the chunk layout: the loads are then in flight while the layout is
+// scanned.  Reads only rows t < n of tiers other than DROP.
+template <int D, int ROWS_IN_FLIGHT>
+__device__ __forceinline__ void pack_first_batch(RowBatch<D, ROWS_IN_FLIGHT>& b, const uint16_t* __restrict__ src,
+                                                 const uint8_t* __restrict__ tier, int t0, int n) {
+  using B = RowBatch<D, ROWS_IN_FLIGHT>;
+  const int lane = threadIdx.x % B::LPR;
+  const int rsub = threadIdx.x / B::LPR;
+#pragma unroll
+  for (int u = 0; u < B::U; ++u) {
+    const int t = t0 + u * B::RPI + rsub;
+    b.x[u] = u32x4{0u, 0u, 0u, 0u};
+    if (t < n && tier[t] != kDROP) b.x[u] = ld_nt16(src + static_cast<size_t>(t) * D + lane * 8);
+  }
+}
+
+// Quantizes and stores the rows of one chunk.  first: the thread's first
+// batch (pack_first_batch); src: the segment's plane [n][D]; dst: the
+// segment's rows; scales: the segment's scales.
 template <int D, int ROWS_IN_FLIGHT, bool NT>
-__device__ __forceinline__ void pack_chunk(const ChunkLds& s, const uint16_t* __restrict__ src,
-                                           uint8_t* __restrict__ dst, float* __restrict__ scales,
-                                           uint32_t* nonfinite, int t0, int n) {
-  constexpr int LPR = D / 8;                // lanes per row, 16 bytes each
-  constexpr int RPI = kRowThreads / LPR;    // rows per block-wide iteration
-  constexpr int ITERS = kChunkTokens / RPI;
-  constexpr int U = ITERS < ROWS_IN_FLIGHT ? ITERS : ROWS_IN_FLIGHT;  // rows in flight per thread
+__device__ __forceinline__ void pack_chunk(const ChunkLds& s, const RowBatch<D, ROWS_IN_FLIGHT>& first,
+                                           const uint16_t* __restrict__ src, uint8_t* __restrict__ dst,
+                                           float* __restrict__ scales, uint32_t* nonfinite, int t0, int n) {
+  using B = RowBatch<D, ROWS_IN_FLIGHT>;
+  constexpr int LPR = B::LPR, RPI = B::RPI, ITERS = B::ITERS, U = B::U;
   const int lane = threadIdx.x % LPR;
   const int rsub = threadIdx.x / LPR;
 #pragma unroll 1
@@ -60,8 +90,12 @@ __device__ __forceinline__ void pack_chunk(const ChunkLds& s, const uint16_t* __
     for (int u = 0; u < U; ++u) {
       const int row = (it + u) * RPI + rsub;
       const int t = t0 + row;
-      x[u] = u32x4{0u, 0u, 0u, 0u};
-      if (t < n && s.tier[row] != kDROP) x[u] = ld_nt16(src + static_cast<size_t>(t) * D + lane * 8);
+      if (it == 0) {
+        x[u] = first.x[u];
+      } else {
+        x[u] = u32x4{0u, 0u, 0u, 0u};
+        if (t < n && s.tier[row] != kDROP) x[u] = ld_nt16(src + static_cast<size_t>(t) * D + lane * 8);
+      }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
