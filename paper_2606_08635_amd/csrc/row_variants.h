@@ -504,9 +504,13 @@ __device__ __forceinline__ u32x4 decode_lane_var(int tr, int32_t q, u32x4 raw, c
       const uint32_t nib = (raw.x >> (4 * i)) & 0xFu;
       code = asym ? static_cast<int32_t>(nib) : (static_cast<int32_t>(nib << 28) >> 28);
     }
-    f[i] = static_cast<float>(code) * s;
+    f[i] = static_cast<float>(code) * s;  // no fused conversion here (a directed test checks)
     if (asym) f[i] = f[i] + lo;
   }
+  // with a finite scale and minimum, code * s + lo is finite or an infinity:
+  // only non-finite metadata can make a NaN to canonicalize
+  if (__builtin_isfinite(s) && __builtin_isfinite(lo))
+    return u32x4{pack_half2(f[0], f[1]), pack_half2(f[2], f[3]), pack_half2(f[4], f[5]), pack_half2(f[6], f[7])};
   return u32x4{pack_half2_canon(f[0], f[1]), pack_half2_canon(f[2], f[3]), pack_half2_canon(f[4], f[5]),
                pack_half2_canon(f[6], f[7])};
 }
@@ -518,11 +522,13 @@ struct ChanDecLds {
   float s[2][D], lo[2][D];
 };
 
-// Loads the chunk's per-channel entries (INT8 at blk8, INT4 at blk4) into c.
-// Contains __syncthreads().
+// Loads the chunk's per-channel entries (INT8 at blk8, INT4 at blk4) into c;
+// returns, to every thread, whether all of them are finite (then no decoded
+// value can be a NaN).  Contains a block barrier.
 template <int D>
-__device__ __forceinline__ void load_channel_params(ChanDecLds<D>& c, const uint8_t* blk8, const uint8_t* blk4,
+__device__ __forceinline__ bool load_channel_params(ChanDecLds<D>& c, const uint8_t* blk8, const uint8_t* blk4,
                                                     const VarCfg& v) {
+  int bad = 0;
   for (int i = threadIdx.x; i < 2 * D; i += kRowThreads) {
     const int t = i / D, ch = i % D;
     const int32_t q = t == 0 ? v.q8 : v.q4;
@@ -540,8 +546,9 @@ __device__ __forceinline__ void load_channel_params(ChanDecLds<D>& c, const uint
     }
     c.s[t][ch] = sc;
     c.lo[t][ch] = lo;
+    bad |= !(__builtin_isfinite(sc) && __builtin_isfinite(lo));
   }
-  __syncthreads();
+  return __syncthreads_or(bad) == 0;
 }
 
 // The lane's 8 outputs of a per-channel K row: element e of channel
@@ -549,7 +556,7 @@ __device__ __forceinline__ void load_channel_params(ChanDecLds<D>& c, const uint
 // 0x7E00).
 template <int LPR>
 __device__ __forceinline__ u32x4 decode_lane_chan(int tr, int32_t q, u32x4 raw, const float* sc, const float* lo,
-                                                  int lane) {
+                                                  int lane, bool finite) {
   const bool asym = (q & kQuantAsym) != 0;
   uint32_t h[8];
 #pragma unroll
@@ -565,15 +572,16 @@ __device__ __forceinline__ u32x4 decode_lane_chan(int tr, int32_t q, u32x4 raw, 
     const float s = sc[lane * 8 + i];
     float f = static_cast<float>(code) * s;
     if (asym) f = f + lo[lane * 8 + i];
-    h[i] = __builtin_isnan(f) ? 0x7E00u : static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(f)));
+    const uint32_t hv = __builtin_bit_cast(uint16_t, static_cast<_Float16>(f));
+    h[i] = (!finite && __builtin_isnan(f)) ? 0x7E00u : hv;
   }
   return u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
 }
 
 template <int D, int ROWS_IN_FLIGHT, bool NT, bool CHAN>
-__device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDecLds<D>* c, const uint8_t* __restrict__ src,
-                                                 const uint8_t* __restrict__ meta, uint16_t* __restrict__ cache,
-                                                 int H, const VarCfg& v) {
+__device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDecLds<D>* c, bool chan_finite,
+                                                 const uint8_t* __restrict__ src, const uint8_t* __restrict__ meta,
+                                                 uint16_t* __restrict__ cache, int H, const VarCfg& v) {
   constexpr int LPR = D / 8;
   constexpr int RPI = kRowThreads / LPR;
   constexpr int ITERS = kChunkTokens / RPI;
@@ -609,7 +617,7 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDe
         const int32_t q = tr == kINT8 ? v.q8 : v.q4;
         if (CHAN && (q & kQuantChannel)) {
           const int t = tr == kINT8 ? 0 : 1;
-          o = decode_lane_chan<LPR>(tr, q, raw[u], c->s[t], c->lo[t], lane);
+          o = decode_lane_chan<LPR>(tr, q, raw[u], c->s[t], c->lo[t], lane, chan_finite);
         } else {
           o = decode_lane_var<LPR>(tr, q, raw[u], meta + s.q[r], lane);
         }

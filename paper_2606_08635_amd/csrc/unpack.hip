@@ -175,13 +175,16 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
     if (chan_k) {
       __shared__ ChanDecLds<D> c;
       const uint8_t* blk = lay + r.scales_bytes + (static_cast<uint64_t>(h) * nchunks + chunk) * (a.cb8 + a.cb4);
-      load_channel_params<D>(c, blk, blk + a.cb8, var);
-      unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, true>(s, &c, src, meta, cache, H, var);
+      const bool finite = load_channel_params<D>(c, blk, blk + a.cb8, var);
+      unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, true>(s, &c, finite, src, meta, cache, H,
+                                                                                 var);
     } else {
-      unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, false>(s, nullptr, src, meta, cache, H, var);
+      unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, false>(s, nullptr, true, src, meta, cache, H,
+                                                                                  var);
     }
   } else if constexpr (VARIANT) {
-    unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, false>(s, nullptr, src, meta, cache, H, var);
+    unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, false>(s, nullptr, true, src, meta, cache, H,
+                                                                                var);
   } else {
     unpack_chunk<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, reinterpret_cast<const float*>(meta),
                                                                      cache, H);

@@ -185,3 +185,66 @@ def test_foreign_scales_decode_like_the_oracle(grouped):
     assert ost == 0 and gst == 0
     same(u16(kc), okc, "K")
     same(u16(vc), ovc, "V")
+
+
+@pytest.mark.parametrize("q8,q4", [(skv.QUANT_GROUP64, skv.QUANT_GROUP32 | skv.QUANT_ASYM),
+                                   (skv.QUANT_CHANNEL, skv.QUANT_CHANNEL | skv.QUANT_ASYM)])
+def test_foreign_variant_scales_decode_like_the_oracle(q8, q4):
+    """Variant layouts with binary32 metadata: every group scale and every
+    per-channel scale replaced by a seeded random binary32 value (minimums
+    kept).  Some products then round differently once than through binary32
+    (4 of the 121 344 INT8 elements of the group-64 case alone); the decoder
+    must match the oracle bit for bit."""
+    L, H, d, n, bs = 2, 2, 64, 700, 16
+    say(f"foreign variant scales q8={q8} q4={q4}")
+    CH = skv.QUANT_CHANNEL
+    kw = dict(num_tiers=3, quant_int8=q8, quant_int4=q4)
+    cfg, ocfg = skv.config(L, H, d, n, 0.35, **kw), oracle.config(L, H, d, n, 0.35, **kw)
+    k, v = workloads.make_kv(L, H, n, d, seed=9)
+    tier = oracle.assign(ocfg, oracle.score(ocfg, u16(k), u16(v)))
+    pay = oracle.pack(ocfg, u16(k), u16(v), tier)
+    geo = oracle.geometry(ocfg)
+    e8, e4 = oracle.meta_bytes(q8, d), oracle.meta_bytes(q4, d)
+    sb = oracle.scale_offsets(tier, e8, e4)
+    sbk = oracle.scale_offsets(tier, 0 if q8 & CH else e8, 0 if q4 & CH else e4)
+    eb = {oracle.INT8: oracle.channel_entry_bytes(q8), oracle.INT4: oracle.channel_entry_bytes(q4)}
+    cb8 = d * eb[oracle.INT8] if q8 & CH else 0
+    cb4 = d * eb[oracle.INT4] if q4 & CH else 0
+    nch = -(-n // 256)
+    rng = np.random.default_rng(q8 * 32 + q4)
+
+    def foreign(count):
+        return rng.uniform(2.0 ** -9, 2.0 ** -2, count).astype(np.float32).view(np.uint8).reshape(count, 4)
+
+    replaced = 0
+    quantized = np.flatnonzero((tier == oracle.INT8) | (tier == oracle.INT4))
+    for l in range(L):
+        lay = geo["layers_off"] + l * geo["layer_stride"]
+        for kv in range(2):
+            for h in range(H):
+                base = h * geo["seg_scale_bytes_k"] if kv == 0 else H * geo["seg_scale_bytes_k"] + h * geo["seg_scale_bytes"]
+                for t in quantized:
+                    q = q8 if tier[t] == oracle.INT8 else q4
+                    if kv == 0 and q & CH:
+                        continue  # per-channel K rows carry no per-row metadata
+                    mo = lay + base + int((sbk if kv == 0 else sb)[t])
+                    for e in range(oracle.meta_bytes(q, d) // eb[tier[t]]):
+                        pay[mo + e * eb[tier[t]]:mo + e * eb[tier[t]] + 4] = foreign(1)[0]
+                        replaced += 1
+        for h in range(H):
+            for c in range(nch):
+                for tr, q, off in ((oracle.INT8, q8, 0), (oracle.INT4, q4, cb8)):
+                    if not q & CH:
+                        continue
+                    boff = lay + geo["scales_bytes"] + (h * nch + c) * (cb8 + cb4) + off
+                    for ch in range(d):
+                        pay[boff + ch * eb[tr]:boff + ch * eb[tr] + 4] = foreign(1)[0]
+                        replaced += 1
+    assert replaced > 0
+    nb = workloads.blocks_for(n, bs) + 1
+    bt = workloads.make_block_table(n, bs, nb, seed=9)
+    okc, ovc, ost = oracle_decode(ocfg, pay, L, H, d, bs, nb, bt.numpy())
+    kc, vc, gst = gpu_decode(cfg, torch.from_numpy(pay).cuda(), L, H, d, n, bs, nb, bt.cuda())
+    assert ost == 0 and gst == 0
+    same(u16(kc), okc, "K")
+    same(u16(vc), ovc, "V")
