@@ -49,22 +49,40 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
   if (tid == 0) s_bad = 0;
   __syncthreads();
 
-  // 1. tier counts and per-chunk sums (a chunk's 16 groups sit in 16 lanes)
+  // 1. tier counts and per-chunk sums (a chunk's 16 groups sit in 16 lanes).
+  //    A pass takes two groups per thread, both loaded before either is
+  //    tallied; the first pass's 2-bit map words stay in registers for step 4.
   uint32_t cnt[4] = {0, 0, 0, 0};
   bool bad = false;
-  for (int base = 0; base < ngroups; base += kPrepThreads) {  // block-uniform trip count
-    const int g = base + tid;
-    const TierGroup gi = g < ngroups ? group_from_bytes(tier, n, g) : empty_group();
+  uint32_t map_first[2] = {0u, 0u};
+  for (int base = 0; base < ngroups; base += 2 * kPrepThreads) {  // block-uniform trip count
+    int gs[2];
+    bool word[2];
+    u32x4 w[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) cnt[i] += gi.count(i);
-    bad |= gi.bad;
-    const uint32_t u = sum16(gi.units), q = sum16(gi.quant);
-    // a chunk's metadata is at most 256 rows x 64 bytes: 16 bits per side
-    const uint32_t m = sum16(gi.count(kINT8) * a.e8 + gi.count(kINT4) * a.e4);
-    const uint32_t mk = sum16(gi.count(kINT8) * a.ek8 + gi.count(kINT4) * a.ek4);
-    if ((tid % kGroupsPerChunk) == 0 && g < ngroups) {
-      s_chunk[g / kGroupsPerChunk] = u | (q << 16);
-      s_meta[g / kGroupsPerChunk] = m | (mk << 16);
+    for (int k = 0; k < 2; ++k) {
+      gs[k] = base + k * kPrepThreads + tid;
+      word[k] = gs[k] < ngroups && tier_group_is_word(tier, n, gs[k]);
+      w[k] = word[k] ? *reinterpret_cast<const u32x4*>(tier + static_cast<size_t>(gs[k]) * kGroupTokens)
+                     : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int g = gs[k];
+      const TierGroup gi = word[k] ? group_from_tier_words(w[k])
+                                   : g < ngroups ? group_from_bytes(tier, n, g) : empty_group();
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cnt[i] += gi.count(i);
+      bad |= gi.bad;
+      const uint32_t u = sum16(gi.units), q = sum16(gi.quant);
+      // a chunk's metadata is at most 256 rows x 64 bytes: 16 bits per side
+      const uint32_t m = sum16(gi.count(kINT8) * a.e8 + gi.count(kINT4) * a.e4);
+      const uint32_t mk = sum16(gi.count(kINT8) * a.ek8 + gi.count(kINT4) * a.ek4);
+      if ((tid % kGroupsPerChunk) == 0 && g < ngroups) {
+        s_chunk[g / kGroupsPerChunk] = u | (q << 16);
+        s_meta[g / kGroupsPerChunk] = m | (mk << 16);
+      }
+      if (base == 0) map_first[k] = gi.map2;
     }
   }
 #pragma unroll
@@ -119,9 +137,18 @@ __global__ __launch_bounds__(kPrepThreads) void pack_prep(const BatchArgs a) {
   for (uint64_t b = r.chunkidx_off + entry * nchunks + 4ull * tid; b < r.layers_off; b += 4ull * kPrepThreads)
     *reinterpret_cast<uint32_t*>(payload + b) = 0u;
 
-  // 4. the 2-bit tier map (4 bytes per group of 16 tokens), then its padding
-  for (int g = tid; g < ngroups; g += kPrepThreads)
-    *reinterpret_cast<uint32_t*>(payload + 256 + 4ull * g) = group_from_bytes(tier, n, g).map2;
+  // 4. the 2-bit tier map (4 bytes per group of 16 tokens), then its padding;
+  //    up to two groups per thread the words are still in registers
+  if (ngroups <= 2 * kPrepThreads) {
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int g = k * kPrepThreads + tid;
+      if (g < ngroups) *reinterpret_cast<uint32_t*>(payload + 256 + 4ull * g) = map_first[k];
+    }
+  } else {
+    for (int g = tid; g < ngroups; g += kPrepThreads)
+      *reinterpret_cast<uint32_t*>(payload + 256 + 4ull * g) = group_from_bytes(tier, n, g).map2;
+  }
   for (uint64_t b = 256 + 4ull * ngroups + 4ull * tid; b < r.chunkidx_off; b += 4ull * kPrepThreads)
     *reinterpret_cast<uint32_t*>(payload + b) = 0u;
 }

@@ -22,15 +22,16 @@ struct TierGroup {
   __device__ __forceinline__ uint32_t count(int tier) const { return (cnt4 >> (8 * tier)) & 0xFFu; }
 };
 
+// Branch-free: a code outside 0..3 sets bad, keeps its low two bits in the
+// map and is not counted.
 __device__ __forceinline__ void tally(TierGroup& gi, uint32_t code, int j) {
-  gi.map2 |= (code & 3u) << (2 * j);
-  if (code > 3u) {
-    gi.bad = true;
-    return;
-  }
-  gi.cnt4 += 1u << (8 * code);
-  gi.units += (0x124u >> (4 * code)) & 0xFu;  // 4, 2, 1, 0 for FP16, INT8, INT4, DROP
-  gi.quant += (0x6u >> code) & 1u;            // INT8 and INT4 carry a scale
+  const uint32_t c = code & 3u;
+  const uint32_t ok = code <= 3u ? 1u : 0u;
+  gi.map2 |= c << (2 * j);
+  gi.bad |= ok == 0u;
+  gi.cnt4 += ok << (8 * c);
+  gi.units += ok * ((0x124u >> (4 * c)) & 0xFu);  // 4, 2, 1, 0 for FP16, INT8, INT4, DROP
+  gi.quant += ok & (0x6u >> c);                   // INT8 and INT4 carry a scale
 }
 
 __device__ __forceinline__ TierGroup empty_group() {
@@ -56,23 +57,48 @@ __device__ __forceinline__ TierGroup group_from_bytes(const uint8_t* __restrict_
   return gi;
 }
 
-// Codes from the payload's 2-bit tier map; codes of tokens >= n are ignored.
-__device__ __forceinline__ TierGroup group_from_map(const uint8_t* __restrict__ map, int n, int g) {
+// Codes of group g from its 16 tier bytes already loaded as w (a whole,
+// 16-byte-aligned group).
+__device__ __forceinline__ TierGroup group_from_tier_words(u32x4 w) {
+  TierGroup gi = empty_group();
+  const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int j = 0; j < 16; ++j) tally(gi, (ws[j >> 2] >> (8 * (j & 3))) & 0xFFu, j);
+  return gi;
+}
+
+// Whether group g of a uint8[n] tier array is whole and 16-byte aligned (then
+// its 16 bytes are one load).
+__device__ __forceinline__ bool tier_group_is_word(const uint8_t* tier, int n, int g) {
+  const int t0 = g * kGroupTokens;
+  return t0 + kGroupTokens <= n && (reinterpret_cast<uintptr_t>(tier + t0) & 15u) == 0;
+}
+
+// Codes of group g from its map word w (the payload's 2-bit tier map); codes
+// of tokens >= n are ignored.
+__device__ __forceinline__ TierGroup group_from_map_word(uint32_t w, int n, int g) {
   TierGroup gi = empty_group();
   const int t0 = g * kGroupTokens;
-  const uint32_t w = *reinterpret_cast<const uint32_t*>(map + 4 * g);
 #pragma unroll
   for (int j = 0; j < kGroupTokens; ++j)
     if (t0 + j < n) tally(gi, (w >> (2 * j)) & 3u, j);
   return gi;
 }
 
-// Sum over aligned 16-lane groups; every lane gets its group's sum.
+// Codes from the payload's 2-bit tier map; codes of tokens >= n are ignored.
+__device__ __forceinline__ TierGroup group_from_map(const uint8_t* __restrict__ map, int n, int g) {
+  return group_from_map_word(*reinterpret_cast<const uint32_t*>(map + 4 * g), n, g);
+}
+
+// Sum over aligned 16-lane groups (the DPP rows); every lane gets its group's
+// sum: quad swaps leave each lane its quad's sum, then the half-row mirror
+// (lane i <-> 7 - i) pairs the quads of each half and the row mirror
+// (i <-> 15 - i) the halves.  Every lane of the row must be active.
 __device__ __forceinline__ uint32_t sum16(uint32_t v) {
-  v += static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 1));
-  v += static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 2));
-  v += static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 4));
-  v += static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 8));
+  v += dpp_mov<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_mov<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_mov<0x141>(v);  // row_half_mirror
+  v += dpp_mov<0x140>(v);  // row_mirror
   return v;
 }
 

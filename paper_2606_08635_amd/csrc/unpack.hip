@@ -46,16 +46,43 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
   const uint8_t* __restrict__ payload = r.payload;
   const int n = r.n, nchunks = r.nchunks;
   const int tid = threadIdx.x;
+  const int nbt = (n + block_size - 1) / block_size;
+  const int ngroups = (n + kGroupTokens - 1) / kGroupTokens;
+  const uint8_t* map = payload + 256;
+  const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off);
+  const int entry = variant ? 4 : 2;  // chunk-index words per chunk
+  const int per = (nchunks + kCheckThreads - 1) / kCheckThreads;
+  const int c0 = min(nchunks, tid * per), c1 = min(nchunks, c0 + per);
+  // The first pass of every check loads up front, so that one memory latency
+  // covers them all: the header word, two block-table entries, two map words
+  // and the first chunk-index entry of this thread.  Every address lies in
+  // the payload's metadata or the block table whatever their contents.
+  const uint32_t hword = tid < 64 ? reinterpret_cast<const uint32_t*>(payload)[tid] : 0u;
+  int bt_first[2];
+  uint32_t map_first[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const int i = k * kCheckThreads + tid;
+    bt_first[k] = i < nbt ? r.block_table[i] : 0;
+    map_first[k] = i < ngroups ? reinterpret_cast<const uint32_t*>(map)[i] : 0u;
+  }
+  uint32_t cidx_first[4] = {0u, 0u, 0u, 0u};
+  if (c0 < c1) {
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+      if (w < entry) cidx_first[w] = cidx[entry * c0 + w];
+  }
   if (tid < 4) s_cnt[tid] = 0;
   if (tid == 0) s_bad = 0;
   __syncthreads();
   bool bad = false;
   // header: every word but the non-finite row counter must match
-  if (tid < 64 && tid != kHdrNonfinite)
-    bad |= reinterpret_cast<const uint32_t*>(payload)[tid] != header_word(a, r, tid);
+  if (tid < 64 && tid != kHdrNonfinite) bad |= hword != header_word(a, r, tid);
   // block table entries in range
-  const int nbt = (n + block_size - 1) / block_size;
-  for (int i = tid; i < nbt; i += kCheckThreads) {
+#pragma unroll
+  for (int k = 0; k < 2; ++k)
+    if (k * kCheckThreads + tid < nbt) bad |= bt_first[k] < 0 || bt_first[k] >= num_blocks;
+  for (int i = 2 * kCheckThreads + tid; i < nbt; i += kCheckThreads) {
     const int b = r.block_table[i];
     bad |= b < 0 || b >= num_blocks;
   }
@@ -65,13 +92,14 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
     if (tid == 0) *r.status = static_cast<uint32_t>(SKV_ERR_FORMAT);
     return;
   }
-  // tier counts and chunk sums from the 2-bit map
-  const int ngroups = (n + kGroupTokens - 1) / kGroupTokens;
+  // tier counts and chunk sums from the 2-bit map (a chunk's 16 groups sit
+  // in 16 lanes)
   uint32_t cnt[4] = {0, 0, 0, 0};
-  const uint8_t* map = payload + 256;
-  for (int base = 0; base < ngroups; base += kCheckThreads) {
+  for (int base = 0; base < ngroups; base += kCheckThreads) {  // block-uniform trip count
     const int g = base + tid;
-    const TierGroup gi = g < ngroups ? group_from_map(map, n, g) : empty_group();
+    const int pass = base / kCheckThreads;
+    TierGroup gi = empty_group();
+    if (g < ngroups) gi = pass < 2 ? group_from_map_word(map_first[pass & 1], n, g) : group_from_map(map, n, g);
 #pragma unroll
     for (int i = 0; i < 4; ++i) cnt[i] += gi.count(i);
     const uint32_t u = sum16(gi.units), q = sum16(gi.quant);
@@ -89,16 +117,14 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
   bad = s_cnt[0] != static_cast<uint32_t>(r.n_sink + r.n16) || s_cnt[1] != static_cast<uint32_t>(r.n8) ||
         s_cnt[2] != static_cast<uint32_t>(r.n4) || s_cnt[3] != static_cast<uint32_t>(r.nd);
   // chunk index must equal the running sums
-  const int per = (nchunks + kCheckThreads - 1) / kCheckThreads;
-  const int c0 = min(nchunks, tid * per), c1 = min(nchunks, c0 + per);
   uint64_t run = 0;
   for (int c = c0; c < c1; ++c) run += (s_chunk[c] & 0xFFFFu) | (static_cast<uint64_t>(s_chunk[c] >> 16) << 32);
   const uint64_t ex = block_exclusive_scan_1024(run, s_scan);
   uint32_t ru = static_cast<uint32_t>(ex), rq = static_cast<uint32_t>(ex >> 32);
-  const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off);
   if (!variant) {
     for (int c = c0; c < c1; ++c) {
-      bad |= cidx[2 * c] != ru || cidx[2 * c + 1] != rq;
+      const uint32_t w0 = c == c0 ? cidx_first[0] : cidx[2 * c], w1 = c == c0 ? cidx_first[1] : cidx[2 * c + 1];
+      bad |= w0 != ru || w1 != rq;
       ru += s_chunk[c] & 0xFFFFu;
       rq += s_chunk[c] >> 16;
     }
@@ -109,8 +135,10 @@ __global__ __launch_bounds__(kCheckThreads) void unpack_check(const BatchArgs a,
     const uint64_t mex = block_exclusive_scan_1024(mrun, s_scan2);
     uint32_t rm = static_cast<uint32_t>(mex), rmk = static_cast<uint32_t>(mex >> 32);
     for (int c = c0; c < c1; ++c) {
-      bad |= cidx[4 * c] != ru || cidx[4 * c + 1] != rq || cidx[4 * c + 2] != rm ||
-             cidx[4 * c + 3] != (chan ? rmk : 0u);
+      uint32_t w[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) w[i] = c == c0 ? cidx_first[i] : cidx[4 * c + i];
+      bad |= w[0] != ru || w[1] != rq || w[2] != rm || w[3] != (chan ? rmk : 0u);
       ru += s_chunk[c] & 0xFFFFu;
       rq += s_chunk[c] >> 16;
       rm += s_meta[c] & 0xFFFFu;
