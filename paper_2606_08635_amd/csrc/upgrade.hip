@@ -195,11 +195,28 @@ __global__ __launch_bounds__(kUpgThreads) void upg_rows(const UpgArgs a) {
   __shared__ int32_t s_tok[kUpgThreads];
   __shared__ uint8_t s_tier[kUpgThreads];
   uint8_t* up = a.up;
-  if (reinterpret_cast<const uint32_t*>(up)[kUpgHdrStatus] != 0u) return;
   const int nch = (a.m + kUpgThreads - 1) / kUpgThreads;
   const int chunk = blockIdx.x % nch, seg = blockIdx.x / nch;
   const int h = seg % a.H, kv = (seg / a.H) & 1, l = seg / (2 * a.H);
   const int i0 = chunk * kUpgThreads;
+  const uint16_t* src = (kv ? a.v : a.k) + (static_cast<size_t>(l) * a.H + h) * static_cast<size_t>(a.n) * D;
+  const int lane = threadIdx.x % LPR, rsub = threadIdx.x / LPR;
+  // The thread's first rows are loaded before the header check, the tier
+  // gather and the barrier, with their token ids read straight from the list
+  // and clamped into [0, n): the reads stay inside K/V even for a list the
+  // check refuses (then nothing is written), and the clamp changes nothing
+  // for a valid list.
+  u32x4 first[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int i = i0 + u * RPI + rsub;
+    first[u] = u32x4{0u, 0u, 0u, 0u};
+    if (i < a.m) {
+      const int t = min(max(a.tokens[i], 0), a.n - 1);
+      first[u] = ld_nt16(src + static_cast<size_t>(t) * D + lane * 8);
+    }
+  }
+  if (reinterpret_cast<const uint32_t*>(up)[kUpgHdrStatus] != 0u) return;
   {
     const int i = i0 + threadIdx.x;
     const int t = i < a.m ? a.tokens[i] : 0;
@@ -207,16 +224,15 @@ __global__ __launch_bounds__(kUpgThreads) void upg_rows(const UpgArgs a) {
     s_tier[threadIdx.x] = i < a.m ? a.tier[t] : kDROP;
   }
   __syncthreads();
-  const uint16_t* src = (kv ? a.v : a.k) + (static_cast<size_t>(l) * a.H + h) * static_cast<size_t>(a.n) * D;
   const uint64_t seg_rows = static_cast<uint64_t>(seg) * a.m;
-  const int lane = threadIdx.x % LPR, rsub = threadIdx.x / LPR;
 #pragma unroll 1
   for (int it = 0; it < ITERS; it += U) {
     u32x4 x[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = (it + u) * RPI + rsub;
-      x[u] = i0 + r < a.m ? ld_nt16(src + static_cast<size_t>(s_tok[r]) * D + lane * 8) : u32x4{0u, 0u, 0u, 0u};
+      if (it == 0) x[u] = first[u];
+      else x[u] = i0 + r < a.m ? ld_nt16(src + static_cast<size_t>(s_tok[r]) * D + lane * 8) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
