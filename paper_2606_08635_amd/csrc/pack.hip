@@ -202,7 +202,7 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   uint32_t* nonfinite = reinterpret_cast<uint32_t*>(payload) + kHdrNonfinite;
   if constexpr (CHAN) {
     if (chan_k) {
-      __shared__ ChanLds<D> c;
+      __shared__ __align__(16) ChanLds<D> c;
       uint8_t* blk = lay + r.scales_bytes + (static_cast<uint64_t>(h) * nchunks + chunk) * (a.cb8 + a.cb4);
       if constexpr (D <= 128) {  // the thread's rows fit in registers: one read of the chunk
         pack_chunk_chan<D, SKV_PACK_NT_STORE>(s, c, src, dst, meta, nonfinite, t0, n, var, blk, blk + a.cb8);

@@ -28,6 +28,8 @@
 
 namespace skv {
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 constexpr int32_t kQuantAsym = 4, kQuantFp16 = 8, kQuantChannel = 16;
 
 struct VarCfg {
@@ -434,6 +436,37 @@ __device__ __forceinline__ void pack_chunk_var(const ChunkLds& s, const ChanLds<
   }
 }
 
+// Quantizes and stores a row of a per-channel tier (tr) with its chunk's
+// channel parameters in c: the lane's 8 channels are contiguous, so their
+// scales and minimums are two 16-byte shared-memory reads each.  zero_bits:
+// bit 8 t + e marks channel lane * 8 + e of tier t as all-zero codes.  Every
+// lane of the row's group calls it.
+template <int D, bool NT>
+__device__ __forceinline__ void pack_row_chan(const ChunkLds& s, const ChanLds<D>& c, uint32_t zero_bits, u32x4 x,
+                                              int row, int tr, bool asym, uint8_t* __restrict__ dst,
+                                              uint32_t* nonfinite, int lane) {
+  constexpr int LPR = D / 8;
+  const int t = tr == kINT8 ? 0 : 1;
+  const f32x4* rp = reinterpret_cast<const f32x4*>(&c.r[t][lane * 8]);
+  const f32x4* lp = reinterpret_cast<const f32x4*>(&c.lo[t][lane * 8]);
+  const f32x4 r0 = rp[0], r1 = rp[1], l0 = lp[0], l1 = lp[1];
+  const float rs[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+  const float ls[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  LaneCodes qc;
+  qc.nonfinite = group_max<LPR>(absmax_bits8(x)) >= 0x7C00u;
+  qc.scale = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float xv = (e & 1) ? half_hi(w[e / 2]) : half_lo(w[e / 2]);
+    qc.c[e] = group_code(xv, rs[e], ls[e], ((zero_bits >> (8 * t + e)) & 1u) != 0u, asym, tr);
+  }
+  if (qc.nonfinite && lane == 0) atomicAdd(nonfinite, 1u);
+  uint8_t* out_row = dst + s.off[row];
+  if (tr == kINT8) store8<NT>(out_row + lane * 8, pack_int8(qc));
+  else store4<NT>(out_row + lane * 4, pack_int4(qc));
+}
+
 // K segment with a per-channel tier, d <= 128: the thread's rows of the chunk
 // (at most 16) are loaded once into registers, reduced per channel, and then
 // quantized from the same registers.  Contains __syncthreads().
@@ -463,8 +496,23 @@ __device__ __forceinline__ void pack_chunk_chan(const ChunkLds& s, ChanLds<D>& c
   for (int it = 0; it < ITERS; ++it) chan_acc_row(acc, x[it], s.tier[it * RPI + rsub], v);
   __syncthreads();  // shared arrays cleared before any atomic
   chan_finish<D>(c, acc, lane, v, blk8, blk4);
+  // the thread's 8 channels are the same in all its rows: their all-zero
+  // flags of both tiers, as bits
+  uint32_t zero_bits = 0u;
 #pragma unroll
-  for (int it = 0; it < ITERS; ++it) pack_row_var<D, NT, true>(s, &c, x[it], it * RPI + rsub, dst, meta, nonfinite, v, lane);
+  for (int t = 0; t < 2; ++t)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) zero_bits |= (c.zero[t][lane * 8 + e] != 0u ? 1u : 0u) << (8 * t + e);
+#pragma unroll
+  for (int it = 0; it < ITERS; ++it) {
+    const int row = it * RPI + rsub;
+    const int tr = s.tier[row];
+    const int32_t q = tr == kINT8 ? v.q8 : v.q4;
+    if ((tr == kINT8 || tr == kINT4) && (q & kQuantChannel))  // uniform per row
+      pack_row_chan<D, NT>(s, c, zero_bits, x[it], row, tr, (q & kQuantAsym) != 0, dst, nonfinite, lane);
+    else
+      pack_row_var<D, NT, true>(s, &c, x[it], row, dst, meta, nonfinite, v, lane);
+  }
 }
 
 // Two binary32 values rounded to binary16 and packed low|high, any NaN as the
