@@ -525,21 +525,34 @@ __device__ __forceinline__ uint32_t pack_half2_canon(float a, float b) {
   return ha | (hb << 16);
 }
 
-// The lane's 8 outputs of a quantized row under descriptor q.
+// The scale and minimum (0 if symmetric) of the lane's group of a quantized
+// row under descriptor q, read from the row's metadata entry.
+struct LaneMeta {
+  float s, lo;
+};
 template <int LPR>
-__device__ __forceinline__ u32x4 decode_lane_var(int tr, int32_t q, u32x4 raw, const uint8_t* meta, int lane) {
+__device__ __forceinline__ LaneMeta load_lane_meta(int32_t q, const uint8_t* meta, int lane) {
   constexpr int D = LPR * 8;
   const int gl = var_group_lanes(q, D);
   const bool asym = (q & kQuantAsym) != 0, f16 = (q & kQuantFp16) != 0;
   const uint8_t* e = meta + (lane / gl) * (asym ? 2 : 1) * (f16 ? 2 : 4);
-  float s, lo = 0.0f;
+  LaneMeta m;
+  m.lo = 0.0f;
   if (f16) {
-    s = half_lo(reinterpret_cast<const uint16_t*>(e)[0]);
-    if (asym) lo = half_lo(reinterpret_cast<const uint16_t*>(e)[1]);
+    m.s = half_lo(reinterpret_cast<const uint16_t*>(e)[0]);
+    if (asym) m.lo = half_lo(reinterpret_cast<const uint16_t*>(e)[1]);
   } else {
-    s = __builtin_bit_cast(float, load_u32_from_halves(e));
-    if (asym) lo = __builtin_bit_cast(float, load_u32_from_halves(e + 4));
+    m.s = __builtin_bit_cast(float, load_u32_from_halves(e));
+    if (asym) m.lo = __builtin_bit_cast(float, load_u32_from_halves(e + 4));
   }
+  return m;
+}
+
+// The lane's 8 outputs of a quantized row under descriptor q, with its
+// group's metadata m.
+__device__ __forceinline__ u32x4 decode_lane_var(int tr, int32_t q, u32x4 raw, LaneMeta m) {
+  const bool asym = (q & kQuantAsym) != 0;
+  const float s = m.s, lo = m.lo;
   if (__builtin_isnan(s)) return u32x4{kNaNHalf2, kNaNHalf2, kNaNHalf2, kNaNHalf2};
   float f[8];
 #pragma unroll
@@ -639,12 +652,14 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDe
 #pragma unroll 1
   for (int it = 0; it < ITERS; it += U) {
     u32x4 raw[U];
+    LaneMeta mt[U];  // per-row metadata, loaded with the codes
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = (it + u) * RPI + rsub;
       const int tr = s.tier[r];
       const uint8_t* row = src + s.off[r];
       raw[u] = u32x4{0u, 0u, 0u, 0u};
+      mt[u] = LaneMeta{0.0f, 0.0f};
       if (tr == kFP16) {
         raw[u] = ld_nt16(row + lane * 16);
       } else if (tr == kINT8) {
@@ -653,6 +668,10 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDe
         raw[u].y = cc.y;
       } else if (tr == kINT4) {
         raw[u].x = ld_nt4(row + lane * 4);
+      }
+      if (tr == kINT8 || tr == kINT4) {
+        const int32_t q = tr == kINT8 ? v.q8 : v.q4;
+        if (!(CHAN && (q & kQuantChannel))) mt[u] = load_lane_meta<LPR>(q, meta + s.q[r], lane);
       }
     }
 #pragma unroll
@@ -667,7 +686,7 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDe
           const int t = tr == kINT8 ? 0 : 1;
           o = decode_lane_chan<LPR>(tr, q, raw[u], c->s[t], c->lo[t], lane, chan_finite);
         } else {
-          o = decode_lane_var<LPR>(tr, q, raw[u], meta + s.q[r], lane);
+          o = decode_lane_var(tr, q, raw[u], mt[u]);
         }
       }
       store16<NT>(cache + static_cast<size_t>(s.pos[r]) * H * D + lane * 8, o);
