@@ -128,7 +128,8 @@ typedef struct skv_config {
  * minimum and maximum (-0 below +0), range = RN32(hi - lo), s = RN32(range/M),
  * r = RN32(M/range) (binary16: s = RN16(RN32(range/M)), r = RN32(1/s)),
  * code = clamp(rne(RN32(RN32(x - lo) r)), 0, M); decode RN16(RN32(RN32(code s)
- * + lo)).  A group with an inf/NaN gets NaN metadata and decodes to 0x7E00; a
+ * + lo)), any NaN written as 0x7E00.  A group with an inf/NaN gets NaN
+ * metadata and decodes to 0x7E00; a
  * zero a or range, or a binary16 s that underflows, gives zero codes.  With
  * any nonzero descriptor the payload stores per quantized row its groups'
  * metadata (s, then lo if asymmetric; fp32 or binary16) in token order, and
@@ -249,7 +250,9 @@ skv_status skv_pack(const skv_config* cfg, const void* k, const void* v, const u
                     void* payload, uint64_t capacity, uint32_t* dev_status, hipStream_t stream);
 
 /* Dequantizes a payload into the paged fp16 cache (Sec. 4.2: dequantize per
- * tier after receipt).  INT8/INT4 elements become RN16(RN32(code * scale));
+ * tier after receipt).  INT8/INT4 elements become RN16(RN32(code * scale))
+ * (the product is rounded to binary32 first; a NaN product, possible only
+ * for a non-finite scale, is written as 0x7E00);
  * FP16 rows are copied bit for bit; DROP rows are written as +0 (the consumer
  * masks them, Sec. 5 "data hygiene"); elements of a row with a NaN scale are
  * written as 0x7E00.  Cache slots of tokens >= n are not touched.

@@ -121,6 +121,16 @@ __device__ __forceinline__ u32x4 dequant_int4(uint32_t w, float s) {
 
 constexpr uint32_t kNaNHalf2 = 0x7E007E00u;
 
+// A pair of binary16 values with every NaN replaced by the canonical 0x7E00
+// (the hardware's NaN from an invalid product, 0 * inf, has its sign set).
+__device__ __forceinline__ uint32_t canon_nan_half2(uint32_t w) {
+  const uint32_t lo = w & 0xFFFFu, hi = w >> 16;
+  return ((lo & 0x7FFFu) > 0x7C00u ? 0x7E00u : lo) | (((hi & 0x7FFFu) > 0x7C00u ? 0x7E00u : hi) << 16);
+}
+__device__ __forceinline__ u32x4 canon_nan_lane(u32x4 o) {
+  return u32x4{canon_nan_half2(o.x), canon_nan_half2(o.y), canon_nan_half2(o.z), canon_nan_half2(o.w)};
+}
+
 // The lane's 8 reconstructed values of a row held at tier tr (what unpack
 // writes): FP16 verbatim, DROP zeros, INT8/INT4 dequantized, NaN scale -> 0x7E00.
 __device__ __forceinline__ u32x4 held_lane(int tr, u32x4 x, uint32_t amax) {

@@ -136,11 +136,13 @@ __device__ __forceinline__ void load_row(int tr, const uint8_t* row, const float
 }
 
 // The lane's 8 output elements of a row: FP16 verbatim, DROP zeros, INT8/INT4
-// dequantized, a NaN scale giving 0x7E00.
+// dequantized, a NaN scale giving 0x7E00 (and any NaN product, 0x7E00).
 __device__ __forceinline__ u32x4 decode_row(int tr, u32x4 raw, float sc) {
   if (tr == kINT8 || tr == kINT4) {
     if (__builtin_isnan(sc)) return u32x4{kNaNHalf2, kNaNHalf2, kNaNHalf2, kNaNHalf2};
-    return tr == kINT8 ? dequant_int8(u32x2{raw.x, raw.y}, sc) : dequant_int4(raw.x, sc);
+    const u32x4 o = tr == kINT8 ? dequant_int8(u32x2{raw.x, raw.y}, sc) : dequant_int4(raw.x, sc);
+    // only an infinite scale makes a NaN product (code 0): written as 0x7E00
+    return __builtin_isinf(sc) ? canon_nan_lane(o) : o;
   }
   return raw;
 }

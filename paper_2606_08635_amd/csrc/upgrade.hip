@@ -296,7 +296,10 @@ __device__ __forceinline__ u32x4 add_residual(u32x4 held, u32x2 c, float scale) 
     const float c1 = static_cast<float>(static_cast<int32_t>(w << (16 - sh)) >> 24) * scale;
     o[j] = pack_half2(half_lo(hs[j]) + c0, half_hi(hs[j]) + c1);
   }
-  return u32x4{o[0], o[1], o[2], o[3]};
+  const u32x4 out{o[0], o[1], o[2], o[3]};
+  // only an infinite scale makes a NaN (code 0, or an infinity of the other
+  // sign): written as 0x7E00
+  return __builtin_isinf(scale) ? canon_nan_lane(out) : out;
 }
 
 template <int D, int MODE>

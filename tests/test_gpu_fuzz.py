@@ -248,3 +248,65 @@ def test_foreign_variant_scales_decode_like_the_oracle(q8, q4):
     assert ost == 0 and gst == 0
     same(u16(kc), okc, "K")
     same(u16(vc), ovc, "V")
+
+
+def test_infinite_scales_decode_like_the_oracle():
+    """Rows whose scale is +inf or -inf: code 0 gives a NaN product (written
+    as 0x7E00), other codes an infinity; the decoder matches the oracle."""
+    L, H, d, n, bs = 1, 2, 64, 600, 16
+    say("infinite scales")
+    cfg, ocfg = configs(L, H, d, n, 0.4, 3)
+    k, v = workloads.make_kv(L, H, n, d, seed=13)
+    tier = oracle.assign(ocfg, oracle.score(ocfg, u16(k), u16(v)))
+    pay = oracle.pack(ocfg, u16(k), u16(v), tier)
+    geo = oracle.geometry(ocfg)
+    _, qrank = oracle.offsets(tier)
+    words = pay.view(np.uint32)
+    quantized = np.flatnonzero((tier == oracle.INT8) | (tier == oracle.INT4))
+    for kv in range(2):
+        for h in range(H):
+            base = (geo["layers_off"] + ((kv * H + h) * geo["nq"]) * 4) // 4
+            for i, t in enumerate(quantized[:120]):
+                words[base + int(qrank[t])] = 0x7F800000 if i % 2 else 0xFF800000
+    nb = workloads.blocks_for(n, bs) + 1
+    bt = workloads.make_block_table(n, bs, nb, seed=13)
+    okc, ovc, ost = oracle_decode(ocfg, pay, L, H, d, bs, nb, bt.numpy())
+    kc, vc, gst = gpu_decode(cfg, torch.from_numpy(pay).cuda(), L, H, d, n, bs, nb, bt.cuda())
+    assert ost == 0 and gst == 0
+    assert (okc == 0x7E00).any() and ((okc & 0x7FFF) == 0x7C00).any()  # the case has both outcomes
+    same(u16(kc), okc, "K")
+    same(u16(vc), ovc, "V")
+
+
+def test_infinite_residual_scales_apply_like_the_oracle():
+    """RESIDUAL8 upgrade rows whose scale is +inf or -inf: held + code * scale
+    is an infinity or, for code 0, a NaN written as 0x7E00, as in the oracle."""
+    L, H, d, n, bs = 1, 2, 64, 600, 16
+    say("infinite residual scales")
+    cfg, ocfg = configs(L, H, d, n, 0.3, 3)
+    k, v = workloads.make_kv(L, H, n, d, seed=17)
+    tier = oracle.assign(ocfg, oracle.score(ocfg, u16(k), u16(v)))
+    tokens = np.flatnonzero(tier != oracle.FP16).astype(np.int32)[:200]
+    mode = skv.UPGRADE_RESIDUAL8
+    up = oracle.pack_upgrade(ocfg, u16(k), u16(v), tier, tokens, mode)
+    m = tokens.size
+    scales_off = int(up[48:56].view(np.uint64)[0])  # header: u64 scales_off at byte 48
+    sc = up[scales_off:scales_off + 8 * L * H * m].view(np.uint32)
+    sc[0::3] = 0x7F800000
+    sc[1::3] = 0xFF800000
+    payload = oracle.pack(ocfg, u16(k), u16(v), tier)
+    nb = workloads.blocks_for(n, bs) + 1
+    bt = workloads.make_block_table(n, bs, nb, seed=17)
+    bk, bv, st = oracle_decode(ocfg, payload, L, H, d, bs, nb, bt.numpy())
+    assert st == 0
+    okc, ovc = bk.copy(), bv.copy()
+    assert oracle.unpack_upgrade(ocfg, up, okc, ovc, bt.numpy(), bs) == 0
+    assert (okc == 0x7E00).any() or (ovc == 0x7E00).any()
+    kc = torch.from_numpy(bk.view(np.int16)).cuda().view(torch.float16)
+    vc = torch.from_numpy(bv.view(np.int16)).cuda().view(torch.float16)
+    ust = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    skv.unpack_upgrade(cfg, torch.from_numpy(up).cuda(), m, mode, kc, vc, bt.cuda(), bs, ust)
+    torch.cuda.synchronize()
+    assert int(ust.item()) == 0
+    same(u16(kc), okc, "K")
+    same(u16(vc), ovc, "V")
