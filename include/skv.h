@@ -219,8 +219,11 @@ skv_status skv_prepare(const skv_config* cfg, void* ws, hipStream_t stream);
  * Attention mode: score[t] = A_t exp(-lambda (n-1-t)), A_t the mean over
  * (layer, query head, observation query) of softmax over all n keys of
  * q.k/sqrt(d), query head hq reading KV head hq/(Hq/H); fp32 MFMA logits, so
- * within a stated relative tolerance of the binary64 definition.  Recency
- * mode: score[t] = exp(-lambda (n-1-t)). */
+ * within a stated relative tolerance of the binary64 definition.  Non-finite
+ * inputs follow IEEE softmax: a NaN or +inf logit in any query row makes that
+ * row's normalizer NaN and so every score NaN (assignment ranks NaN as +0); a
+ * -inf logit only contributes nothing.  Recency mode: score[t] =
+ * exp(-lambda (n-1-t)). */
 skv_status skv_score(const skv_config* cfg, const void* k, const void* v, const void* q_obs,
                      double* score, void* ws, hipStream_t stream);
 

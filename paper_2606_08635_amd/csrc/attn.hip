@@ -392,12 +392,19 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
     stage_issue<D>(kbase, key0, n, s_k, wave);
     half8 qr[D / 16];
     float beta[16];  // c * log2(e) of the lane's 16 rows; +inf for padding rows
+    // padding rows of a partial query tile: their zero queries can still make
+    // a NaN logit against an infinite key element (0 * inf), so their terms
+    // are masked out explicitly rather than relying on exp2(z - inf) = 0
+    uint32_t valid_rows = 0xFFFFu;
+    const bool padded = role.active && role.qtile * 32 + 32 > M;  // uniform per wave
     if (role.active) {
       const int qrow = role.qtile * 32 + j;
       load_rows<D>(qbase, qrow, qrow < M, qr);
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
+      for (int r = 0; r < 16; ++r) {
         beta[r] = cstat[static_cast<size_t>(lh) * Mpad + role.qtile * 32 + acc_row(r, hf)] * kLog2e;
+        if (role.qtile * 32 + acc_row(r, hf) >= M) valid_rows &= ~(1u << r);
+      }
     }
     // adds the query tiles' partial sums of stage st (tile order) onto the
     // stored sums (round order); thread i owns key i of every stage
@@ -445,6 +452,10 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
           float e[16];
 #pragma unroll
           for (int r = 0; r < 16; ++r) e[r] = exp2_fast(__builtin_fmaf(acc[r], alpha, -beta[r]));
+          if (padded) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) e[r] = (valid_rows >> r) & 1u ? e[r] : 0.0f;
+          }
           float p = tree_sum<16>(e);
           p += __shfl_xor(p, 32);  // the other lane-half holds the other 16 rows
           if (hf == 0) part[ti * 32 + j] = p;

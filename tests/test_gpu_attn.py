@@ -5,7 +5,9 @@ relative tolerance (1e-4 on every token, the bar stated for this mode), not
 bit for bit.  The later stages stay exact: the GPU tier map equals the
 oracle's assignment of the GPU scores, pack/unpack equal the oracle's bytes,
 and the tier map differs from the oracle's own (binary64-score) map only on
-tokens whose two scores straddle a cut within that tolerance.
+tokens whose two scores straddle a cut within that tolerance.  With
+infinities and NaNs in the keys or queries the scores are NaN on exactly the
+oracle's tokens (IEEE softmax), and finite elsewhere within the tolerance.
 """
 import pytest
 
@@ -74,3 +76,39 @@ def test_identical_keys_share_mass_equally():
     q = workloads.make_qobs(L, Hq, W, d, seed=2, device="cuda")
     codec = gpu_encode(cfg, k, k, q=q)
     assert np.allclose(codec.scores.cpu().numpy(), 1.0 / n, rtol=1e-5)
+
+
+@pytest.mark.parametrize("where", ["k", "q", "k_neg_inf"])
+def test_attention_scores_with_special_values(where):
+    """Infinities, NaNs, subnormals and signed zeros in the keys or the
+    observation queries.  In binary64 softmax a NaN or +inf logit makes its
+    query row's normalizer NaN, so every token's mass turns NaN (ranked as +0);
+    a -inf logit only contributes nothing (that case keeps every score finite).  The GPU scores must be NaN on
+    exactly the oracle's tokens and within the tolerance elsewhere, and the
+    tier map and payload must follow the GPU scores exactly."""
+    L, H, Hq, W, d, n, b = 2, 2, 4, 8, 64, 600, 0.5
+    say(f"attention specials in {where}")
+    cfg, ocfg = configs(L, H, d, n, b, 3, mode=oracle.ATTN, Hq=Hq, W=W)
+    k, v = workloads.make_kv(L, H, n, d, seed=5)
+    q = workloads.make_qobs(L, Hq, W, d, seed=5)
+    if where == "k":
+        plant_specials(k, v, seed=5)
+    elif where == "q":
+        qb = q.view(torch.int16)
+        qb[1, 2, 3, 7] = 0x7C00  # +inf in one query element of layer 1
+        qb[0, 0, 0, 0] = 0x0001  # a subnormal
+    else:
+        # one key element -inf against +1 in every query row that reads its head:
+        # the logit is exactly -inf (no NaN), so that key gets no mass there
+        k.view(torch.int16)[0, 1, 17, 5] = -1024
+        q.view(torch.int16)[0, 2:4, :, 5] = 0x3C00
+    okey = oracle.score(ocfg, u16(k), u16(v), u16(q))
+    codec = gpu_encode(cfg, k.cuda(), v.cuda(), q=q.cuda())
+    gkey = codec.scores.cpu().numpy()
+    assert np.array_equal(np.isnan(gkey), np.isnan(okey)), (int(np.isnan(gkey).sum()), int(np.isnan(okey).sum()))
+    fin = ~np.isnan(okey)
+    if fin.any():
+        np.testing.assert_allclose(gkey[fin], okey[fin], rtol=RTOL, atol=0)
+    gtier = codec.tier.cpu().numpy()
+    assert np.array_equal(gtier, oracle.assign(ocfg, gkey))
+    assert np.array_equal(codec.payload.cpu().numpy(), oracle.pack(ocfg, u16(k), u16(v), gtier))
