@@ -259,8 +259,10 @@ skv_status skv_pack(const skv_config* cfg, const void* k, const void* v, const u
  * FP16 rows are copied bit for bit; DROP rows are written as +0 (the consumer
  * masks them, Sec. 5 "data hygiene"); elements of a row with a NaN scale are
  * written as 0x7E00.  Cache slots of tokens >= n are not touched.
- * block_table: int32[ceil(n / block_size)], each in [0, num_blocks);
- * block_size >= 1.  dev_status (required): set to 0 on success or to
+ * block_table: int32[ceil(n / block_size)], each in [0, num_blocks), the
+ * entries distinct (unchecked: with a repeated entry the shared block's
+ * contents are unspecified); block_size >= 1.  k_cache, v_cache and payload
+ * must not overlap.  dev_status (required): set to 0 on success or to
  * SKV_ERR_FORMAT when the header, tier counts or chunk index disagree with cfg
  * or a block-table entry is out of range; in that case nothing is written.
  * Returns SKV_ERR_FORMAT (host-side) when payload_bytes is below
