@@ -78,7 +78,7 @@ def test_identical_keys_share_mass_equally():
     assert np.allclose(codec.scores.cpu().numpy(), 1.0 / n, rtol=1e-5)
 
 
-@pytest.mark.parametrize("where", ["k", "q", "k_neg_inf"])
+@pytest.mark.parametrize("where", ["k", "q", "k_neg_inf", "row_all_neg_inf"])
 def test_attention_scores_with_special_values(where):
     """Infinities, NaNs, subnormals and signed zeros in the keys or the
     observation queries.  In binary64 softmax a NaN or +inf logit makes its
@@ -97,6 +97,12 @@ def test_attention_scores_with_special_values(where):
         qb = q.view(torch.int16)
         qb[1, 2, 3, 7] = 0x7C00  # +inf in one query element of layer 1
         qb[0, 0, 0, 0] = 0x0001  # a subnormal
+    elif where == "row_all_neg_inf":
+        # every key of layer 0, head 0 has -inf at element 5 and every query row
+        # reading that head has +1 there: those rows' logits are all -inf, so
+        # their softmax is -inf - (-inf) = NaN (head 1's rows stay finite)
+        k.view(torch.int16)[0, 0, :, 5] = -1024
+        q.view(torch.int16)[0, 0:2, :, 5] = 0x3C00
     else:
         # one key element -inf against +1 in every query row that reads its head:
         # the logit is exactly -inf (no NaN), so that key gets no mass there
@@ -109,6 +115,24 @@ def test_attention_scores_with_special_values(where):
     fin = ~np.isnan(okey)
     if fin.any():
         np.testing.assert_allclose(gkey[fin], okey[fin], rtol=RTOL, atol=0)
+    gtier = codec.tier.cpu().numpy()
+    assert np.array_equal(gtier, oracle.assign(ocfg, gkey))
+    assert np.array_equal(codec.payload.cpu().numpy(), oracle.pack(ocfg, u16(k), u16(v), gtier))
+
+
+@pytest.mark.parametrize("n", [1, 2, 31, 33])
+def test_attention_scores_short_requests(n):
+    """A single partial key tile (n < 32) and one tile plus a ragged key."""
+    L, H, Hq, W, d = 1, 2, 4, 3, 64
+    say(f"attention short n={n}")
+    # no sinks: at n = 1 one FP16 sink alone would exceed the budget
+    cfg, ocfg = configs(L, H, d, n, 0.5, 3, rho=0.0, mode=oracle.ATTN, Hq=Hq, W=W)
+    k, v = workloads.make_kv(L, H, n, d, seed=n + 100)
+    q = workloads.make_qobs(L, Hq, W, d, seed=n + 100)
+    okey = oracle.score(ocfg, u16(k), u16(v), u16(q))
+    codec = gpu_encode(cfg, k.cuda(), v.cuda(), q=q.cuda())
+    gkey = codec.scores.cpu().numpy()
+    np.testing.assert_allclose(gkey, okey, rtol=RTOL, atol=0)
     gtier = codec.tier.cpu().numpy()
     assert np.array_equal(gtier, oracle.assign(ocfg, gkey))
     assert np.array_equal(codec.payload.cpu().numpy(), oracle.pack(ocfg, u16(k), u16(v), gtier))
