@@ -393,6 +393,10 @@ typedef struct skv_group_spec {
   const float* budgets;  /* host, G budgets in (0, 1], or NULL: cfg->budget each */
 } skv_group_spec;
 
+/* The grouped calls quantize with the default (row, symmetric, fp32)
+ * quantizer: cfg->quant_int8 and cfg->quant_int4 must be 0, and every
+ * grouped call but skv_group_count returns SKV_ERR_INVALID_ARG otherwise. */
+
 /* Host only.  G for cfg and spec. */
 skv_status skv_group_count(const skv_config* cfg, const skv_group_spec* spec, int32_t* count);
 

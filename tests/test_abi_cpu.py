@@ -222,6 +222,11 @@ def test_grouped_argument_errors(lib):
         with pytest.raises(skv.SkvError) as e:
             skv.grouped_payload_size(cfg, skv.Groups(gran, budgets))
         assert e.value.status == skv.ERR_INVALID_ARG
+    for q8, q4 in ((skv.QUANT_FP16, 0), (0, skv.QUANT_CHANNEL)):  # grouped maps use the default quantizer
+        with pytest.raises(skv.SkvError) as e:
+            skv.grouped_payload_size(skv.config(2, 2, 64, 300, 0.5, quant_int8=q8, quant_int4=q4),
+                                     skv.Groups(skv.GROUP_LAYER))
+        assert e.value.status == skv.ERR_INVALID_ARG
     g = skv.Groups(skv.GROUP_LAYER, [0.9, 0.1])
     g.spec.reserved = 1
     with pytest.raises(skv.SkvError):
