@@ -15,9 +15,9 @@ def u16(t: torch.Tensor) -> np.ndarray:
     return t.cpu().numpy().view(np.uint16)
 
 
-def configs(L, H, d, n, b, tiers=3, rho=0.02, num_sink=-1, decay=0.005, mode=oracle.KVNORM, Hq=0, W=0):
+def configs(L, H, d, n, b, tiers=3, rho=0.02, num_sink=-1, decay=0.005, mode=oracle.KVNORM, Hq=0, W=0, q8=0, q4=0):
     kw = dict(first_ratio=rho, num_sink=num_sink, decay=decay, num_tiers=tiers, score_mode=mode,
-              num_q_heads=Hq, obs_window=W)
+              num_q_heads=Hq, obs_window=W, quant_int8=q8, quant_int4=q4)
     return skv.config(L, H, d, n, b, **kw), oracle.config(L, H, d, n, b, **kw)
 
 

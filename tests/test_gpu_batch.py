@@ -16,10 +16,10 @@ pytestmark = pytest.mark.gpu
 L, H, d, B, TIERS = 2, 2, 64, 0.4, 3
 
 
-def _requests(lengths, seed0=0):
+def _requests(lengths, seed0=0, q8=0, q4=0):
     out = []
     for i, n in enumerate(lengths):
-        cfg, ocfg = configs(L, H, d, n, B, TIERS)
+        cfg, ocfg = configs(L, H, d, n, B, TIERS, q8=q8, q4=q4)
         k, v = workloads.make_kv(L, H, n, d, seed=seed0 + 16 * i)
         key = oracle.score(ocfg, u16(k), u16(v))
         tier = oracle.assign(ocfg, key)
@@ -85,12 +85,19 @@ def test_batch_matches_oracle(lengths):
     assert np.array_equal(u16(kc), okc) and np.array_equal(u16(vc), ovc)
 
 
-def test_layer_ranges_equal_one_call():
+VARIANTS = [(0, 0), (skv.QUANT_GROUP64, skv.QUANT_GROUP32 | skv.QUANT_ASYM),
+            (skv.QUANT_CHANNEL | skv.QUANT_ASYM, skv.QUANT_GROUP32 | skv.QUANT_FP16),
+            (skv.QUANT_FP16, skv.QUANT_CHANNEL)]
+
+
+@pytest.mark.parametrize("q8,q4", VARIANTS, ids=lambda x: f"{x}")
+def test_layer_ranges_equal_one_call(q8, q4):
     global L
     L_saved, L = L, 4
     try:
+        say(f"layer ranges, quantizer descriptors int8={q8} int4={q4}")
         lengths = [700, 129]
-        reqs = _requests(lengths, seed0=5)
+        reqs = _requests(lengths, seed0=5, q8=q8, q4=q4)
         full, _ = _gpu_pack(reqs)
         parts, sts = _gpu_pack(reqs, layer_ranges=[(0, 1), (1, 2), (3, 1)])
         assert sts == [0, 0]
@@ -102,6 +109,8 @@ def test_layer_ranges_equal_one_call():
         kc2, vc2, st2 = _gpu_unpack(reqs, full, tables, pool, bs, layer_ranges=[(0, 2), (2, 1), (3, 1)])
         assert st2 == [0, 0] and torch.equal(kc1.view(torch.int16), kc2.view(torch.int16))
         assert torch.equal(vc1.view(torch.int16), vc2.view(torch.int16))
+        okc, ovc, ost = _oracle_unpack(reqs, [r["payload"] for r in reqs], tables, pool, bs)
+        assert ost == [oracle.OK] * 2 and np.array_equal(u16(kc2), okc) and np.array_equal(u16(vc2), ovc)
     finally:
         L = L_saved
 
