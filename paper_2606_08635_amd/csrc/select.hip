@@ -7,10 +7,18 @@
 // c_t is among the n16 largest keys, INT8 iff among the next n8, INT4 iff
 // among the next n4, DROP otherwise.  The kernel finds the three cut keys
 // T1 >= T2 >= T3 (the n16-th, (n16+n8)-th and (n16+n8+n4)-th largest) by one
-// radix select per cut over 11-bit digits (6 passes), all three sharing each
-// pass over the keys, then classifies every token against them.
-//   * One workgroup of 1024 threads.  Keys are recomputed from the scores on
-//     every pass (the scores stay in L2), eight loads in flight per thread.
+// radix select per cut over six digits (11, 11 and 10 bits of the key's high
+// word, then the same of its low word), all three sharing each pass over the
+// keys, then classifies every token against them.
+//   * One workgroup of 1024 threads.
+//   * Resident form (at most 32 non-sink tokens per thread): the scores are
+//     loaded once and the high words of the keys kept in LDS (128 KiB, next
+//     to the 24 KiB of histograms).  The three high-word passes and the
+//     classification read LDS only; the low-word passes reload a score only
+//     for a key whose high word equals a cut's, which after three digits is a
+//     handful of tokens.
+//   * Longer rows recompute the keys from the scores on every pass (the
+//     scores stay in L2), eight loads in flight per thread.
 //   * Cuts with the same decided prefix share one LDS histogram.
 //   * Consecutive keys of a thread that fall in the same bin are counted
 //     before one LDS atomic, so the first pass (where most keys share the
@@ -22,10 +30,17 @@ namespace skv {
 namespace {
 
 constexpr int kSelThreads = 1024;
-constexpr int kDigit = 11;
-constexpr int kBins = 1 << kDigit;
-constexpr int kPasses = 6;   // 5 digits of 11 bits and one of 9
-constexpr int kBatch = 8;  // scores loaded per thread before they are counted
+constexpr int kBins = 1 << 11;  // widest digit
+constexpr int kPasses = 6;
+constexpr int kBatch = 8;       // scores loaded per thread before they are counted
+constexpr int kResident = 32;   // keys per thread held by the resident form
+
+// Lowest key bit of digit `pass`: 53, 42, 32 in the high word, 21, 10, 0 in
+// the low word.
+__device__ __forceinline__ int digit_low_bit(int pass) {
+  const int q = pass < 3 ? pass : pass - 3;
+  return (pass < 3 ? 32 : 0) + (q == 2 ? 0 : 21 - 11 * q);
+}
 
 __device__ __forceinline__ uint64_t rank_key(double s, int t) {
   uint64_t bits = 0;
@@ -52,134 +67,220 @@ struct RunCounter {
   }
 };
 
+// LDS state of one row's selection.
+struct SelectState {
+  uint32_t hist[3][kBins];
+  uint64_t prefix[3];  // decided key bits of each cut
+  uint32_t rank[3];    // remaining rank (1-based) inside the current prefix
+  int group[3];        // which histogram a cut reads
+};
+
+// After a pass's histograms are complete: wave j walks cut j's histogram
+// from the top bin down and fixes the digit (at key bit `shift`) of the bin
+// that holds its remaining rank (32 bins per lane).
+__device__ __forceinline__ void choose_digits(SelectState& st, int shift, int lane, int wave) {
+  if (wave >= 3 || st.rank[wave] == 0) return;
+  const int j = wave;
+  constexpr int kPer = kBins / 64;  // 32 consecutive bins per lane, read 4 at a time
+  const u32x4* h4 = reinterpret_cast<const u32x4*>(st.hist[st.group[j]]);
+  const int b0 = kBins - kPer * (lane + 1);  // this lane's lowest bin; lane 0 holds the top
+  uint32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < kPer / 4; ++i) {
+    const u32x4 c = h4[b0 / 4 + i];
+    sum += c.x + c.y + c.z + c.w;
+  }
+  uint32_t inc = sum;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t y = static_cast<uint32_t>(__shfl_up(static_cast<int>(inc), o));
+    if (lane >= o) inc += y;
+  }
+  uint32_t run = inc - sum;  // keys in the bins above this lane's
+  const uint32_t want = st.rank[j];
+  if (run < want && want <= run + sum) {
+    const uint64_t prefix = st.prefix[j];
+#pragma unroll
+    for (int i = kPer / 4 - 1; i >= 0; --i) {  // descending bins
+      const u32x4 c = h4[b0 / 4 + i];
+      const uint32_t cs[4] = {c.w, c.z, c.y, c.x};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int b = b0 + 4 * i + (3 - e);
+        if (run < want && want <= run + cs[e]) {
+          st.prefix[j] = prefix | (static_cast<uint64_t>(b) << shift);
+          st.rank[j] = want - run;
+        }
+        run += cs[e];
+      }
+    }
+  }
+}
+
 // The whole assignment of one score row by one 1024-thread workgroup.
+// RESIDENT requires n - n_sink <= kResident * kSelThreads.
+template <bool RESIDENT>
 __device__ __forceinline__ void assign_row(const double* __restrict__ score, uint8_t* __restrict__ tier, int n,
                                            int n_sink, int n16, int n8, int n4) {
-  __shared__ __attribute__((aligned(16))) uint32_t hist[3][kBins];
-  __shared__ uint64_t s_prefix[3];
-  __shared__ uint32_t s_rank[3];  // remaining rank (1-based) inside the current prefix
-  __shared__ int s_group[3];      // which histogram a cut reads
+  __shared__ __attribute__((aligned(16))) SelectState st;
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const uint32_t cut_rank[3] = {static_cast<uint32_t>(n16), static_cast<uint32_t>(n16 + n8),
                                 static_cast<uint32_t>(n16 + n8 + n4)};
+  // resident form: key u of this thread belongs to token t0 + u * kSelThreads,
+  // valid for u < nk.  The loads are clamped to token n - 1 (n >= 1) so that
+  // all of them issue together without a branch each.
+  const int t0 = n_sink + tid;
+  const int nk = t0 < n ? (n - t0 + kSelThreads - 1) / kSelThreads : 0;
+  // high word of key u of this thread at hi[u][tid]
+  __shared__ uint32_t hi[RESIDENT ? kResident : 1][kSelThreads];
+  if constexpr (RESIDENT) {
+    double sc[kResident];
+#pragma unroll
+    for (int u = 0; u < kResident; ++u) sc[u] = score[min(t0 + u * kSelThreads, n - 1)];
+#pragma unroll
+    for (int u = 0; u < kResident; ++u)
+      hi[u][tid] = static_cast<uint32_t>(rank_key(sc[u], t0 + u * kSelThreads) >> 32);
+  }
   if (tid < 3) {
-    s_prefix[tid] = 0;
-    s_rank[tid] = tid == 0 ? cut_rank[0] : tid == 1 ? cut_rank[1] : cut_rank[2];
+    st.prefix[tid] = 0;
+    st.rank[tid] = tid == 0 ? cut_rank[0] : tid == 1 ? cut_rank[1] : cut_rank[2];
   }
   __syncthreads();
 
+  int hi_bit = 64;  // digit `pass` is key bits [low, hi_bit)
   for (int pass = 0; pass < kPasses; ++pass) {
-    const int hi_bit = 64 - kDigit * pass;
-    const int shift = hi_bit > kDigit ? hi_bit - kDigit : 0;
-    const uint32_t mask = (1u << (hi_bit - shift)) - 1u;
-    const uint64_t decided = pass == 0 ? 0ull : (~0ull << hi_bit);
+    const int low = digit_low_bit(pass);
+    const uint32_t mask = (1u << (hi_bit - low)) - 1u;
     if (tid < 3) {
       int grp = tid;
       for (int j = 0; j < tid; ++j)
-        if (s_rank[j] != 0 && s_prefix[j] == s_prefix[tid]) { grp = j; break; }
-      s_group[tid] = grp;
+        if (st.rank[j] != 0 && st.prefix[j] == st.prefix[tid]) { grp = j; break; }
+      st.group[tid] = grp;
     }
-    for (int i = tid; i < 3 * kBins; i += kSelThreads) (&hist[0][0])[i] = 0;
+    for (int i = tid; i < 3 * kBins; i += kSelThreads) (&st.hist[0][0])[i] = 0;
     __syncthreads();
-    const bool act0 = s_rank[0] != 0 && s_group[0] == 0;
-    const bool act1 = s_rank[1] != 0 && s_group[1] == 1;
-    const bool act2 = s_rank[2] != 0 && s_group[2] == 2;
-    const uint64_t pre0 = s_prefix[0], pre1 = s_prefix[1], pre2 = s_prefix[2];
+    const bool act0 = st.rank[0] != 0 && st.group[0] == 0;
+    const bool act1 = st.rank[1] != 0 && st.group[1] == 1;
+    const bool act2 = st.rank[2] != 0 && st.group[2] == 2;
+    const uint64_t pre0 = st.prefix[0], pre1 = st.prefix[1], pre2 = st.prefix[2];
     RunCounter r0, r1, r2;
-    for (int base = n_sink + tid; base < n; base += kBatch * kSelThreads) {
-      double sc[kBatch];
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int t = base + u * kSelThreads;
-        sc[u] = t < n ? score[t] : 0.0;
-      }
-#pragma unroll
-      for (int u = 0; u < kBatch; ++u) {
-        const int t = base + u * kSelThreads;
-        if (t >= n) break;
-        const uint64_t c = rank_key(sc[u], t);
-        const uint32_t bin = static_cast<uint32_t>(c >> shift) & mask;
-        const uint64_t hi = c & decided;
-        if (act0 && hi == pre0) r0.add(hist[0], bin);
-        if (act1 && hi == pre1) r1.add(hist[1], bin);
-        if (act2 && hi == pre2) r2.add(hist[2], bin);
-      }
-    }
-    flush(hist[0], r0.bin, r0.count);
-    flush(hist[1], r1.bin, r1.count);
-    flush(hist[2], r2.bin, r2.count);
-    __syncthreads();
-    // wave j walks cut j's histogram from the top bin down and picks the bin
-    // that holds its remaining rank (32 bins per lane)
-    if (wave < 3 && s_rank[wave] != 0) {
-      const int j = wave;
-      constexpr int kPer = kBins / 64;  // 32 consecutive bins per lane, read 4 at a time
-      const u32x4* h4 = reinterpret_cast<const u32x4*>(hist[s_group[j]]);
-      const int b0 = kBins - kPer * (lane + 1);  // this lane's lowest bin; lane 0 holds the top
-      u32x4 c4[kPer / 4];
-      uint32_t sum = 0;
-#pragma unroll
-      for (int i = 0; i < kPer / 4; ++i) {
-        c4[i] = h4[b0 / 4 + i];
-        sum += c4[i].x + c4[i].y + c4[i].z + c4[i].w;
-      }
-      uint32_t inc = sum;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = static_cast<uint32_t>(__shfl_up(static_cast<int>(inc), o));
-        if (lane >= o) inc += y;
-      }
-      uint32_t run = inc - sum;  // keys in the bins above this lane's
-      const uint32_t want = s_rank[j];
-      if (run < want && want <= run + sum) {
-        const uint64_t prefix = s_prefix[j];
-#pragma unroll
-        for (int i = kPer / 4 - 1; i >= 0; --i) {  // descending bins
-          const uint32_t cs[4] = {c4[i].w, c4[i].z, c4[i].y, c4[i].x};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int b = b0 + 4 * i + (3 - e);
-            if (run < want && want <= run + cs[e]) {
-              s_prefix[j] = prefix | (static_cast<uint64_t>(b) << shift);
-              s_rank[j] = want - run;
-            }
-            run += cs[e];
+    if constexpr (RESIDENT) {
+      const uint32_t h0 = static_cast<uint32_t>(pre0 >> 32), h1 = static_cast<uint32_t>(pre1 >> 32),
+                     h2 = static_cast<uint32_t>(pre2 >> 32);
+      if (pass < 3) {
+        // high word: the decided bits are those at or above hi_bit
+        const uint32_t dm = pass == 0 ? 0u : ~0u << (hi_bit - 32);
+        for (int u = 0; u < nk; ++u) {
+          const uint32_t w = hi[u][tid];
+          const uint32_t bin = (w >> (low - 32)) & mask, d = w & dm;
+          if (act0 && d == h0) r0.add(st.hist[0], bin);
+          if (act1 && d == h1) r1.add(st.hist[1], bin);
+          if (act2 && d == h2) r2.add(st.hist[2], bin);
+        }
+      } else {
+        // low word: a key takes part only if its whole high word is decided
+        const uint32_t dm = pass == 3 ? 0u : ~0u << hi_bit;
+        const uint32_t l0 = static_cast<uint32_t>(pre0), l1 = static_cast<uint32_t>(pre1),
+                       l2 = static_cast<uint32_t>(pre2);
+        for (int u = 0; u < nk; ++u) {
+          const uint32_t w = hi[u][tid];
+          const bool m0 = act0 && w == h0, m1 = act1 && w == h1, m2 = act2 && w == h2;
+          if (m0 || m1 || m2) {
+            const int t = t0 + u * kSelThreads;
+            const uint32_t lo = static_cast<uint32_t>(rank_key(score[t], t));
+            const uint32_t bin = (lo >> low) & mask, d = lo & dm;
+            if (m0 && d == l0) r0.add(st.hist[0], bin);
+            if (m1 && d == l1) r1.add(st.hist[1], bin);
+            if (m2 && d == l2) r2.add(st.hist[2], bin);
           }
         }
       }
+    } else {
+      const uint64_t decided = pass == 0 ? 0ull : (~0ull << hi_bit);
+      for (int base = t0; base < n; base += kBatch * kSelThreads) {
+        double sc[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          const int t = base + u * kSelThreads;
+          sc[u] = t < n ? score[t] : 0.0;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          const int t = base + u * kSelThreads;
+          if (t >= n) break;
+          const uint64_t c = rank_key(sc[u], t);
+          const uint32_t bin = static_cast<uint32_t>(c >> low) & mask;
+          const uint64_t d = c & decided;
+          if (act0 && d == pre0) r0.add(st.hist[0], bin);
+          if (act1 && d == pre1) r1.add(st.hist[1], bin);
+          if (act2 && d == pre2) r2.add(st.hist[2], bin);
+        }
+      }
     }
+    flush(st.hist[0], r0.bin, r0.count);
+    flush(st.hist[1], r1.bin, r1.count);
+    flush(st.hist[2], r2.bin, r2.count);
     __syncthreads();
+    choose_digits(st, low, lane, wave);
+    __syncthreads();
+    hi_bit = low;
   }
 
-  // s_prefix[j] is now the cut key itself (keys are distinct); a cut of rank 0
-  // admits no key.
-  const uint64_t T1 = s_prefix[0], T2 = s_prefix[1], T3 = s_prefix[2];
+  // st.prefix[j] is now the cut key itself (keys are distinct); a cut of rank
+  // 0 admits no key.
+  const uint64_t T1 = st.prefix[0], T2 = st.prefix[1], T3 = st.prefix[2];
   const bool has1 = cut_rank[0] != 0, has2 = cut_rank[1] != 0, has3 = cut_rank[2] != 0;
-  for (int t = tid; t < n; t += kSelThreads) {
-    uint8_t tr = kFP16;  // sinks
-    if (t >= n_sink) {
-      const uint64_t c = rank_key(score[t], t);
-      tr = (has1 && c >= T1) ? kFP16 : (has2 && c >= T2) ? kINT8 : (has3 && c >= T3) ? kINT4 : kDROP;
+  if constexpr (RESIDENT) {
+    // c >= T iff its high word is above T's, or equal with the low word at
+    // least T's; the low word is loaded only in the equal case
+    const uint32_t H1 = static_cast<uint32_t>(T1 >> 32), H2 = static_cast<uint32_t>(T2 >> 32),
+                   H3 = static_cast<uint32_t>(T3 >> 32);
+    const uint32_t L1 = static_cast<uint32_t>(T1), L2 = static_cast<uint32_t>(T2), L3 = static_cast<uint32_t>(T3);
+    for (int t = tid; t < n_sink && t < n; t += kSelThreads) tier[t] = kFP16;
+    for (int u = 0; u < nk; ++u) {
+      const int t = t0 + u * kSelThreads;
+      const uint32_t w = hi[u][tid];
+      uint32_t lo = 0;
+      if ((has1 && w == H1) || (has2 && w == H2) || (has3 && w == H3))
+        lo = static_cast<uint32_t>(rank_key(score[t], t));
+      const bool ge1 = has1 && (w > H1 || (w == H1 && lo >= L1));
+      const bool ge2 = has2 && (w > H2 || (w == H2 && lo >= L2));
+      const bool ge3 = has3 && (w > H3 || (w == H3 && lo >= L3));
+      tier[t] = ge1 ? kFP16 : ge2 ? kINT8 : ge3 ? kINT4 : kDROP;
     }
-    tier[t] = tr;
+  } else {
+    for (int t = tid; t < n; t += kSelThreads) {
+      uint8_t tr = kFP16;  // sinks
+      if (t >= n_sink) {
+        const uint64_t c = rank_key(score[t], t);
+        tr = (has1 && c >= T1) ? kFP16 : (has2 && c >= T2) ? kINT8 : (has3 && c >= T3) ? kINT4 : kDROP;
+      }
+      tier[t] = tr;
+    }
   }
 }
 
+bool fits_resident(int n, int n_sink) { return n - n_sink <= kResident * kSelThreads; }
+
+template <bool RESIDENT>
 __global__ __launch_bounds__(kSelThreads) void assign_tiers(const double* __restrict__ score,
                                                             uint8_t* __restrict__ tier, int n,
                                                             int n_sink, int n16, int n8, int n4) {
-  assign_row(score, tier, n, n_sink, n16, n8, n4);
+  assign_row<RESIDENT>(score, tier, n, n_sink, n16, n8, n4);
 }
 
 // grid: one workgroup per group; plan counts from the group table
 // (u32 [sinks, fp16, int8, int4, ...], 32 bytes per group).
+// RESIDENT requires n <= kResident * kSelThreads (every group's sinks count
+// down from there).
+template <bool RESIDENT>
 __global__ __launch_bounds__(kSelThreads) void assign_tiers_groups(const double* __restrict__ score,
                                                                    uint8_t* __restrict__ tier, int n,
                                                                    const uint32_t* __restrict__ group_table) {
   const uint32_t* e = group_table + 8 * blockIdx.x;
   const size_t row = static_cast<size_t>(blockIdx.x) * n;
-  assign_row(score + row, tier + row, n, static_cast<int>(e[0]), static_cast<int>(e[1]), static_cast<int>(e[2]),
+  assign_row<RESIDENT>(score + row, tier + row, n, static_cast<int>(e[0]), static_cast<int>(e[1]), static_cast<int>(e[2]),
              static_cast<int>(e[3]));
 }
 
@@ -187,13 +288,19 @@ __global__ __launch_bounds__(kSelThreads) void assign_tiers_groups(const double*
 
 hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier,
                          hipStream_t stream) {
-  assign_tiers<<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
+  if (fits_resident(g.n, g.n_sink))
+    assign_tiers<true><<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
+  else
+    assign_tiers<false><<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
   return hipGetLastError();
 }
 
 hipError_t launch_assign_groups(int32_t G, int32_t n, const uint32_t* group_table, const double* score,
                                 uint8_t* tier, hipStream_t stream) {
-  assign_tiers_groups<<<G, kSelThreads, 0, stream>>>(score, tier, n, group_table);
+  if (fits_resident(n, 0))
+    assign_tiers_groups<true><<<G, kSelThreads, 0, stream>>>(score, tier, n, group_table);
+  else
+    assign_tiers_groups<false><<<G, kSelThreads, 0, stream>>>(score, tier, n, group_table);
   return hipGetLastError();
 }
 

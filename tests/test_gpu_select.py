@@ -1,0 +1,64 @@
+"""Tier assignment on both sides of its two kernel forms vs the oracle.
+
+Rows with at most 32 * 1024 non-sink tokens keep the high words of their
+ranking keys resident in LDS; longer rows recompute the keys from the scores on
+every pass.  Each side of that boundary is checked bit for bit against the
+oracle's tier map, for one map and for per-layer grouped maps, with score sets
+that spread over many binades, that tie in the keys' high 32 bits and differ
+only below them, and that hold exact ties, non-positive scores and NaN.
+"""
+import pytest
+
+from gpu_helpers import *  # noqa: F401,F403
+
+pytestmark = pytest.mark.gpu
+
+RESIDENT_MAX = 32 * 1024  # non-sink tokens per row of the resident form
+
+
+def _scores(kind, shape, seed):
+    rng = np.random.default_rng(seed)
+    if kind == "binades":
+        return np.ldexp(1.0 + rng.random(shape), rng.integers(-40, 40, shape))
+    if kind == "low_word":
+        # equal exponent and top 21 mantissa bits: keys tie in their high word
+        # and differ in mantissa bits 30..20 (and then in the token index)
+        return 1.0 + rng.integers(0, 2048, shape) * 2.0 ** -32
+    s = np.round(rng.random(shape) * 4) / 4
+    s[rng.random(shape) < 0.1] = -1.0
+    s[rng.random(shape) < 0.01] = np.nan
+    return s
+
+
+@pytest.mark.parametrize("kind,b", [("binades", 0.7), ("low_word", 0.4), ("ties", 0.15)])
+@pytest.mark.parametrize("extra", [0, 1], ids=["resident", "past_resident"])
+def test_single_map_at_the_form_boundary(kind, b, extra):
+    n_sink = 100
+    n = n_sink + RESIDENT_MAX + extra
+    say(f"assign n={n} sinks={n_sink} b={b} scores={kind}")
+    cfg, ocfg = configs(1, 1, 32, n, b, 3, num_sink=n_sink)
+    key = _scores(kind, n, seed=n + len(kind))
+    want = oracle.assign(ocfg, key)
+    tier = torch.empty(n, dtype=torch.uint8, device="cuda")
+    skv.assign_tiers(cfg, torch.from_numpy(key).cuda(), tier)
+    torch.cuda.synchronize()
+    assert np.array_equal(tier.cpu().numpy(), want)
+
+
+@pytest.mark.parametrize("kind", ["binades", "low_word", "ties"])
+@pytest.mark.parametrize("n", [RESIDENT_MAX, RESIDENT_MAX + 1], ids=["resident", "past_resident"])
+def test_grouped_maps_at_the_form_boundary(kind, n):
+    L = 3
+    say(f"grouped assign L={L} n={n} scores={kind}")
+    cfg, ocfg = configs(L, 1, 32, n, 0.4, 3)
+    gran = oracle.GRAN_LAYER
+    budgets = np.float32([0.7, 0.3, 0.05])
+    groups = skv.Groups(gran, budgets)
+    key = _scores(kind, (L, n), seed=7 * n + len(kind))
+    want = oracle.assign_groups(ocfg, gran, key, budgets)
+    ws = torch.empty(skv.group_workspace_size(cfg, groups), dtype=torch.uint8, device="cuda")
+    skv.prepare_groups(cfg, groups, ws)
+    tier = torch.empty(L * n, dtype=torch.uint8, device="cuda")
+    skv.assign_groups(cfg, groups, torch.from_numpy(key.ravel()).cuda(), tier, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(tier.cpu().numpy().reshape(L, n), want)
