@@ -8,7 +8,7 @@
  * and assigns each remaining token FP16, INT8 or INT4 (or drops it) by
  * importance under a normalized byte budget (Sec. 2.1, Sec. 4.4, Algorithm 1
  * steps 2-3), then quantizes K and V independently per tier into one
- * compacted payload (Algorithm 1 step 4).  On the decode side it dequantizes
+ * compacted payload (Algorithm 1, transfer).  On the decode side it dequantizes
  * the payload into an fp16 paged KV cache (Sec. 4.2, Fig. "sysarch").
  *
  * Conventions shared by every entry point
@@ -210,7 +210,7 @@ skv_status skv_workspace_size(const skv_config* cfg, uint64_t* bytes);
  * three values.  Sec. 4.3, eq. "importance". */
 skv_status skv_prepare(const skv_config* cfg, void* ws, hipStream_t stream);
 
-/* Scores every token (Sec. 4.3; Algorithm 1 step 2).  k, v: [L][H][n][d]
+/* Scores every token (Sec. 4.3; Algorithm 1, scoring).  k, v: [L][H][n][d]
  * binary16; q_obs: [L][Hq][W][d] binary16 in attention mode, else ignored;
  * score: double[n], written.  ws must be prepared for cfg by skv_prepare.
  * KV-norm mode: score[t] = RN64(RN64(S_t) * exp(-2 lambda (n-1-t))), S_t the
@@ -227,7 +227,7 @@ skv_status skv_prepare(const skv_config* cfg, void* ws, hipStream_t stream);
 skv_status skv_score(const skv_config* cfg, const void* k, const void* v, const void* q_obs,
                      double* score, void* ws, hipStream_t stream);
 
-/* Assigns tiers (Sec. 2.3 Prop. 1; Algorithm 1 steps 2-3).  score: double[n]
+/* Assigns tiers (Sec. 2.3 Prop. 1; Algorithm 1, scoring and tier assignment).  score: double[n]
  * (any values; NaN and non-positive scores rank as +0); tier: uint8[n],
  * written.  Tokens t < n_sink get FP16.  The other tokens are ranked by
  * descending composite key ((bits(score) >> 20) << 21) | t, i.e. by score cut
@@ -237,7 +237,7 @@ skv_status skv_score(const skv_config* cfg, const void* k, const void* v, const 
 skv_status skv_assign_tiers(const skv_config* cfg, const double* score, uint8_t* tier, void* ws,
                             hipStream_t stream);
 
-/* Quantizes K and V per tier and packs the payload (Algorithm 1 step 4;
+/* Quantizes K and V per tier and packs the payload (Algorithm 1, transfer;
  * "standard symmetric" quantizer, Sec. 8).  tier: uint8[n] whose counts must
  * equal skv_plan_tiers(cfg) (sinks included in FP16).  payload: capacity bytes,
  * at least skv_payload_size(cfg); exactly that many bytes are written.

@@ -19,7 +19,7 @@
  * Functions and the passages they follow:
  *   ora_plan            normalized budget (Sec. 2.1, eq. "budget"), the
  *                       budget-to-tier mapping (Sec. 4.4), sink reservation
- *                       (Sec. 4.4, Algorithm 1 step 2), the 2-tier drop rule
+ *                       (Sec. 4.4, Algorithm 1, scoring), the 2-tier drop rule
  *                       (Sec. 7.4.3 / probe ablation).
  *   ora_decay_table     the recency factor exp(-lambda*Delta) of eq.
  *                       "importance" (Sec. 4.3).
@@ -30,7 +30,7 @@
  *                       (Sec. 2.3 Prop. 1 "exchange argument"; Algorithm 1
  *                       steps 2-3).
  *   ora_pack            per-tier quantization of K and V, independently,
- *                       into one mixed-precision payload (Algorithm 1 step 4;
+ *                       into one mixed-precision payload (Algorithm 1, transfer;
  *                       "standard symmetric" quantizer, Sec. 8).
  *   ora_unpack          decode-side dequantization into a paged fp16 cache
  *                       (Sec. 4.2, Fig. "sysarch").
@@ -389,7 +389,7 @@ int ora_score(const ora_config* c, const uint16_t* k, const uint16_t* v, const u
 }
 
 /* ------------------------------------------------------------------------ */
-/* Tier assignment (Sec. 2.3 Prop. 1; Algorithm 1 steps 2-3).                  */
+/* Tier assignment (Sec. 2.3 Prop. 1; Algorithm 1, scoring and tier assignment).                  */
 /* ------------------------------------------------------------------------ */
 
 /* Ranking key: the score's binary64 pattern cut to 32 fraction bits, with the
@@ -739,7 +739,7 @@ void ora_decode_row_channel(int tr, int32_t q, int32_t d, const uint8_t* in, con
 }
 
 /* ------------------------------------------------------------------------ */
-/* Payload writer (Algorithm 1 step 4) and reader (decode side, Sec. 4.2).     */
+/* Payload writer (Algorithm 1, transfer) and reader (decode side, Sec. 4.2).     */
 /* ------------------------------------------------------------------------ */
 
 static void put32(uint8_t* p, uint32_t v) { memcpy(p, &v, 4); }

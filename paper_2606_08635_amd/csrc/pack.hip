@@ -1,4 +1,4 @@
-// Quantize-and-pack (Algorithm 1 step 4; "standard symmetric" quantizer of
+// Quantize-and-pack (Algorithm 1, transfer; "standard symmetric" quantizer of
 // Sec. 8), batched over requests of different lengths.
 //
 // pack_prep (one workgroup per request) checks the tier map against the plan,

@@ -1,5 +1,5 @@
 // Tier assignment: sink pinning + importance-sorted cuts (Sec. 2.3 Prop. 1;
-// Sec. 4.4; Algorithm 1 steps 2-3).
+// Sec. 4.4; Algorithm 1, scoring and tier assignment).
 //
 // Non-sink token t carries the 64-bit ranking key
 //   c_t = ((bits(score_t) >> 20) << 21) | t     (score <= 0 or NaN ranks as +0),

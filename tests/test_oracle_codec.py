@@ -1,7 +1,7 @@
 """Pins for the oracle's row quantizer, payload writer and reader.
 
 The quantizer is the symmetric per-row absmax scheme ("standard symmetric",
-Sec. 8) applied to keys and values independently (Algorithm 1 step 4).
+Sec. 8) applied to keys and values independently (Algorithm 1, transfer).
 Checks: the half-step error bound, exact round-trips on lattice rows and at
 the row's absmax element, bit-exact FP16 rows, the nibble layout written out
 by hand, b = 1 round-trips, and the payload's structural fields.

@@ -2,7 +2,7 @@
 
 Sources: eq. "budget" (Sec. 2.1), the budget-to-tier mapping (Sec. 4.4), the
 2-tier drop rule (Sec. 7.4.3), sink reservation charged to the budget
-(Sec. 4.4, Algorithm 1 step 2) and the fractions the paper prints
+(Sec. 4.4, Algorithm 1, scoring) and the fractions the paper prints
 (tests/golden/paper_tier_fractions.txt).
 """
 import math

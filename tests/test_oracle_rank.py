@@ -3,7 +3,7 @@
 Proposition 1 (Sec. 2.3, exchange argument): for fixed tier counts an
 optimal assignment never gives a lower-precision tier to a more important
 token than to a less important one.  Sinks are pinned to FP16 before ranking
-(Sec. 4.4; Algorithm 1 step 2).  Checked by brute force over every placement
+(Sec. 4.4; Algorithm 1, scoring).  Checked by brute force over every placement
 on tiny inputs, by the monotonicity property on large ones, and by the closed
 form of the recency-only score.
 """
