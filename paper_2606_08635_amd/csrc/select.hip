@@ -20,9 +20,12 @@
 //   * Longer rows recompute the keys from the scores on every pass (the
 //     scores stay in L2), eight loads in flight per thread.
 //   * Cuts with the same decided prefix share one LDS histogram.
-//   * Consecutive keys of a thread that fall in the same bin are counted
-//     before one LDS atomic, so the first pass (where most keys share the
-//     binary64 exponent, hence the top digit) does not serialize on one bin.
+//   * Neighbouring tokens mostly share the first digit (the binary64
+//     exponent; the decay orders exponents by position), so that pass must
+//     not serialize on one bin.  In the resident form a wave's lanes that
+//     share the first counting lane's bin add to it with one atomic; later
+//     passes, and the other form, count consecutive keys of a thread that fall
+//     in the same bin before one atomic.
 #include "device_util.h"
 #include "skv_internal.h"
 
@@ -66,6 +69,23 @@ struct RunCounter {
     ++count;
   }
 };
+
+// Adds one to bin `bin` of h for every lane with `pred`: the lanes whose bin
+// equals that of the first such lane by one atomic from that lane, the rest
+// one atomic each.  Every active lane of the wave must call it.
+__device__ __forceinline__ void wave_count(uint32_t* h, bool pred, uint32_t bin, int lane) {
+  const uint64_t m = __ballot(pred);
+  if (m == 0) return;  // wave-uniform
+  const int leader = __ffsll(static_cast<unsigned long long>(m)) - 1;
+  const uint32_t lb = static_cast<uint32_t>(__shfl(static_cast<int>(bin), leader));
+  const uint64_t same = __ballot(pred && bin == lb);
+  if (pred) {
+    if (bin != lb)
+      atomicAdd(&h[bin], 1u);
+    else if (lane == leader)
+      atomicAdd(&h[lb], static_cast<uint32_t>(__popcll(same)));
+  }
+}
 
 // LDS state of one row's selection.
 struct SelectState {
@@ -171,12 +191,20 @@ __device__ __forceinline__ void assign_row(const double* __restrict__ score, uin
       if (pass < 3) {
         // high word: the decided bits are those at or above hi_bit
         const uint32_t dm = pass == 0 ? 0u : ~0u << (hi_bit - 32);
-        for (int u = 0; u < nk; ++u) {
-          const uint32_t w = hi[u][tid];
-          const uint32_t bin = (w >> (low - 32)) & mask, d = w & dm;
-          if (act0 && d == h0) r0.add(st.hist[0], bin);
-          if (act1 && d == h1) r1.add(st.hist[1], bin);
-          if (act2 && d == h2) r2.add(st.hist[2], bin);
+        if (pass == 0) {
+          // every cut's prefix is still empty, so only the first cut of
+          // nonzero rank leads a group and every key counts in its histogram
+          const int lead = act0 ? 0 : act1 ? 1 : 2;
+          const bool any = act0 || act1 || act2;
+          for (int u = 0; u < nk; ++u) wave_count(st.hist[lead], any, (hi[u][tid] >> (low - 32)) & mask, lane);
+        } else {
+          for (int u = 0; u < nk; ++u) {
+            const uint32_t w = hi[u][tid];
+            const uint32_t bin = (w >> (low - 32)) & mask, d = w & dm;
+            if (act0 && d == h0) r0.add(st.hist[0], bin);
+            if (act1 && d == h1) r1.add(st.hist[1], bin);
+            if (act2 && d == h2) r2.add(st.hist[2], bin);
+          }
         }
       } else {
         // low word: a key takes part only if its whole high word is decided
