@@ -106,8 +106,8 @@ __device__ __forceinline__ void choose_digits(SelectState& st, int shift, int la
   const int b0 = kBins - kPer * (lane + 1);  // this lane's lowest bin; lane 0 holds the top
   uint32_t sum = 0;
 #pragma unroll
-  for (int i = 0; i < kPer / 4; ++i) {
-    const u32x4 c = h4[b0 / 4 + i];
+  for (int i = 0; i < kPer / 4; ++i) {  // rotated by lane: lanes 128 B apart would share banks
+    const u32x4 c = h4[b0 / 4 + ((i + lane) & (kPer / 4 - 1))];
     sum += c.x + c.y + c.z + c.w;
   }
   uint32_t inc = sum;
@@ -198,6 +198,7 @@ __device__ __forceinline__ void assign_row(const double* __restrict__ score, uin
           const bool any = act0 || act1 || act2;
           for (int u = 0; u < nk; ++u) wave_count(st.hist[lead], any, (hi[u][tid] >> (low - 32)) & mask, lane);
         } else {
+#pragma unroll 8
           for (int u = 0; u < nk; ++u) {
             const uint32_t w = hi[u][tid];
             const uint32_t bin = (w >> (low - 32)) & mask, d = w & dm;
@@ -211,6 +212,7 @@ __device__ __forceinline__ void assign_row(const double* __restrict__ score, uin
         const uint32_t dm = pass == 3 ? 0u : ~0u << hi_bit;
         const uint32_t l0 = static_cast<uint32_t>(pre0), l1 = static_cast<uint32_t>(pre1),
                        l2 = static_cast<uint32_t>(pre2);
+#pragma unroll 8
         for (int u = 0; u < nk; ++u) {
           const uint32_t w = hi[u][tid];
           const bool m0 = act0 && w == h0, m1 = act1 && w == h1, m2 = act2 && w == h2;
