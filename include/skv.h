@@ -17,8 +17,9 @@
  *    block_table, ws and dev_status are HIP device pointers (for example
  *    torch tensors' data_ptr()).  They must be 16-byte aligned.  The caller
  *    owns every buffer; the library allocates no device memory and keeps no
- *    global state, so calls on different streams with different buffers are
- *    independent.  Calls that share a buffer must be ordered by the caller.
+ *    global state (except skv_score_static's fixed scratch array), so calls
+ *    on different streams with different buffers are independent.  Calls that
+ *    share a buffer must be ordered by the caller.
  *  - Device entry points only enqueue work on `stream` and never synchronize
  *    with the host (skv_prepare is the one exception, see there).  A null
  *    stream means the legacy default stream.
@@ -73,7 +74,8 @@ typedef enum skv_status {
   SKV_OK = 0,
   SKV_ERR_INVALID_ARG = 1, /* bad shape, range, pointer or alignment           */
   SKV_ERR_BUDGET = 2,      /* the sinks alone exceed the budget (4s > floor(4bn)) */
-  SKV_ERR_CAPACITY = 3,    /* output buffer smaller than skv_payload_size       */
+  SKV_ERR_CAPACITY = 3,    /* output buffer smaller than skv_payload_size, or a
+                              request too large for skv_score_static's scratch */
   SKV_ERR_FORMAT = 4,      /* payload_bytes too small for the configuration     */
   SKV_ERR_DEVICE = 5       /* a HIP call or kernel launch failed                */
 } skv_status;
@@ -226,6 +228,30 @@ skv_status skv_prepare(const skv_config* cfg, void* ws, hipStream_t stream);
  * exp(-lambda (n-1-t)). */
 skv_status skv_score(const skv_config* cfg, const void* k, const void* v, const void* q_obs,
                      double* score, void* ws, hipStream_t stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): skv_score
+ * without a workspace argument.  Results are those of skv_score (same
+ * kernels); the decay table and score scratch live in a library-owned array
+ * of SKV_STATIC_SCRATCH_BYTES on each device, which each device holds from
+ * the first call until the process ends.  A request fits when
+ * skv_workspace_size(cfg) <= SKV_STATIC_SCRATCH_BYTES (the 32-layer x 8-head
+ * x 128-dim x 32768-token request fits in every score mode); a larger one
+ * returns SKV_ERR_CAPACITY before anything is enqueued.  The call works on
+ * the current device and allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine).  The decay table is kept between calls: a
+ * call whose (score mode's decay rate, n) needs entries the array does not
+ * hold computes them on the host and copies them in stream order in pieces
+ * from this thread's stack, waiting for each copy (a host synchronization,
+ * as in skv_prepare); otherwise nothing is copied and the call only
+ * enqueues.  Every call on a device shares that device's array and leaves
+ * its contents behind (the kernels write all scratch they read, so nothing
+ * needs clearing): calls that overlap on one device -- on different streams,
+ * or from different host threads without ordering -- race and give
+ * undefined scores.  Argument errors as skv_score. */
+#define SKV_STATIC_SCRATCH_BYTES (48u << 20)
+skv_status skv_score_static(const skv_config* cfg, const void* k, const void* v, const void* q_obs,
+                            double* score, hipStream_t stream);
 
 /* Assigns tiers (Sec. 2.3 Prop. 1; Algorithm 1, scoring and tier assignment).  score: double[n]
  * (any values; NaN and non-positive scores rank as +0); tier: uint8[n],

@@ -1,10 +1,11 @@
 // Host side of the C ABI declared in include/skv.h: argument checks, the tier
 // plan (Sec. 2.1 eq. "budget", Sec. 4.4), payload geometry, the decay table
-// and kernel launches.  Nothing here synchronizes with the device except
-// skv_prepare's one table upload.
+// and kernel launches.  Nothing here synchronizes with the device except the
+// decay-table uploads of skv_prepare and skv_score_static.
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <vector>
 
 #include "skv_internal.h"
@@ -185,6 +186,21 @@ uint64_t scratch_bytes(const skv_config* c) {
 }
 
 inline skv_status launched(hipError_t e) { return e == hipSuccess ? SKV_OK : SKV_ERR_DEVICE; }
+
+// Rate of the decay table: exp(-lambda * Delta) for attention and recency
+// scores, exp(-(2 lambda) * Delta) for the squared KV-norm score; the product
+// is exact in binary64.
+double decay_rate(const skv_config* c) {
+  return static_cast<double>(c->decay) * (c->score_mode == SKV_SCORE_KVNORM ? 2.0 : 1.0);
+}
+
+// out[i] = exp(-(rate * (begin + i))) for i in [0, count), with the C
+// library's binary64 exp (the argument is exact: rate has 25 significant bits
+// and the index at most 21).
+void fill_decay(double rate, int begin, int count, double* out) {
+#pragma clang loop vectorize(disable)
+  for (int i = 0; i < count; ++i) out[i] = std::exp(-(rate * static_cast<double>(begin + i)));
+}
 
 void fill_common(const skv_config* cfg, int32_t layer_begin, int32_t layer_count, BatchArgs* a) {
   std::memset(a, 0, sizeof(*a));
@@ -412,6 +428,104 @@ GroupLaunch group_launch(const GroupHost& gh, const void* ws) {
   return gl;
 }
 
+// Pointer checks of skv_score's inputs for cfg's score mode.
+skv_status check_score_inputs(const skv_config* cfg, const void* k, const void* v, const void* q_obs) {
+  switch (cfg->score_mode) {
+    case SKV_SCORE_KVNORM: return dev_ptr_ok(k) && dev_ptr_ok(v) ? SKV_OK : SKV_ERR_INVALID_ARG;
+    case SKV_SCORE_ATTN: return dev_ptr_ok(k) && dev_ptr_ok(q_obs) ? SKV_OK : SKV_ERR_INVALID_ARG;
+    default: return SKV_OK;
+  }
+}
+
+// The score launches of cfg's mode, with the decay table at `table` and the
+// mode's scratch at `scratch` (device memory).
+skv_status score_launch(const skv_config* cfg, const void* k, const void* v, const void* q_obs, double* score,
+                        const double* table, void* scratch, hipStream_t stream) {
+  Geometry g{};
+  g.L = cfg->num_layers;
+  g.H = cfg->num_kv_heads;
+  g.d = cfg->head_dim;
+  g.n = cfg->num_tokens;
+  switch (cfg->score_mode) {
+    case SKV_SCORE_KVNORM:
+      return launched(launch_score_kvnorm(g, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
+                                          table, static_cast<uint64_t*>(scratch), score, stream));
+    case SKV_SCORE_ATTN:
+      return launched(launch_score_attn(g, cfg->num_q_heads, cfg->obs_window, static_cast<const uint16_t*>(k),
+                                        static_cast<const uint16_t*>(q_obs), table, scratch, score, stream));
+    default:
+      return launched(launch_score_recency(g, table, score, stream));
+  }
+}
+
+}  // namespace
+}  // namespace skv
+
+// Library-owned scoring scratch of skv_score_static: [decay table | score
+// scratch], laid out as in a caller's workspace.  Each device holds its own
+// copy from the library's load until the process ends.  Host code never uses
+// this name as an address (on the host it is only a handle to the symbol):
+// the device address comes from hipGetSymbolAddress, per device.
+static __device__ __align__(256) uint8_t scratch[SKV_STATIC_SCRATCH_BYTES];
+
+namespace skv {
+namespace {
+
+constexpr int kMaxStaticDevices = 64;
+
+// Per device: the device address of `scratch` (null until first use) and the
+// decay table it holds, exp(-table_rate * Delta) for Delta in [0, table_count).
+struct StaticScratch {
+  uint8_t* base;
+  double table_rate;
+  int32_t table_count;
+};
+
+std::mutex g_static_mutex;
+StaticScratch g_static[kMaxStaticDevices];
+
+// Looks up the current device's copy of `scratch` (once per device) and makes
+// sure it starts with cfg's decay table: a table of the same rate is reused,
+// extended if it is shorter than n; otherwise it is rewritten.  The table is
+// computed on the host in pieces held on this thread's stack, each copied in
+// stream order and waited for before the piece is overwritten, so nothing is
+// allocated.  Since the score scratch follows the table of this call's n,
+// only the first n entries are recorded as resident afterwards.
+skv_status static_scratch_prepare(const skv_config* cfg, hipStream_t stream, uint8_t** base_out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return SKV_ERR_DEVICE;
+  if (dev >= kMaxStaticDevices) return SKV_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lock(g_static_mutex);
+  StaticScratch& ss = g_static[dev];
+  if (ss.base == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return SKV_ERR_DEVICE;
+    ss.base = static_cast<uint8_t*>(p);
+    ss.table_count = 0;
+  }
+  const int n = cfg->num_tokens;
+  const double rate = decay_rate(cfg);
+  int have = ss.table_rate == rate ? ss.table_count : 0;
+  if (have < n) {
+    ss.table_count = 0;  // invalid until every piece has landed
+    constexpr int kPiece = 4096;
+    double piece[kPiece];
+    for (int begin = have; begin < n; begin += kPiece) {
+      const int count = std::min(kPiece, n - begin);
+      fill_decay(rate, begin, count, piece);
+      if (hipMemcpyAsync(ss.base + static_cast<uint64_t>(begin) * sizeof(double), piece, count * sizeof(double),
+                         hipMemcpyHostToDevice, stream) != hipSuccess ||
+          hipStreamSynchronize(stream) != hipSuccess)
+        return SKV_ERR_DEVICE;
+    }
+    ss.table_rate = rate;
+    have = n;
+  }
+  ss.table_count = std::min(have, n);
+  *base_out = ss.base;
+  return SKV_OK;
+}
+
 }  // namespace
 }  // namespace skv
 
@@ -426,7 +540,7 @@ const char* skv_status_string(int32_t status) {
     case SKV_OK: return "ok";
     case SKV_ERR_INVALID_ARG: return "invalid argument";
     case SKV_ERR_BUDGET: return "sink tokens exceed the budget";
-    case SKV_ERR_CAPACITY: return "output buffer too small";
+    case SKV_ERR_CAPACITY: return "output buffer too small, or request too large for the static scratch";
     case SKV_ERR_FORMAT: return "payload does not match the configuration";
     case SKV_ERR_DEVICE: return "HIP launch or copy failed";
   }
@@ -460,12 +574,8 @@ skv_status skv_prepare(const skv_config* cfg, void* ws, hipStream_t stream) {
   if (st != SKV_OK) return st;
   if (!dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
   const int n = cfg->num_tokens;
-  // exp(-lambda * Delta) for attention/recency scores, exp(-(2 lambda) * Delta)
-  // for the squared KV-norm score; the argument is exact in binary64
-  const double rate = static_cast<double>(cfg->decay) * (cfg->score_mode == SKV_SCORE_KVNORM ? 2.0 : 1.0);
   std::vector<double> table(static_cast<size_t>(n));
-#pragma clang loop vectorize(disable)
-  for (int delta = 0; delta < n; ++delta) table[delta] = std::exp(-(rate * static_cast<double>(delta)));
+  fill_decay(decay_rate(cfg), 0, n, table.data());
   if (hipMemcpyAsync(ws, table.data(), table.size() * sizeof(double), hipMemcpyHostToDevice, stream) != hipSuccess)
     return SKV_ERR_DEVICE;
   return hipStreamSynchronize(stream) == hipSuccess ? SKV_OK : SKV_ERR_DEVICE;
@@ -476,25 +586,22 @@ skv_status skv_score(const skv_config* cfg, const void* k, const void* v, const 
   skv_status st = check_config(cfg);
   if (st != SKV_OK) return st;
   if (!dev_ptr_ok(score) || !dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
-  Geometry g{};
-  g.L = cfg->num_layers;
-  g.H = cfg->num_kv_heads;
-  g.d = cfg->head_dim;
-  g.n = cfg->num_tokens;
-  const double* table = static_cast<const double*>(ws);
-  void* scratch = static_cast<uint8_t*>(ws) + decay_table_bytes(cfg);
-  switch (cfg->score_mode) {
-    case SKV_SCORE_KVNORM:
-      if (!dev_ptr_ok(k) || !dev_ptr_ok(v)) return SKV_ERR_INVALID_ARG;
-      return launched(launch_score_kvnorm(g, static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v),
-                                          table, static_cast<uint64_t*>(scratch), score, stream));
-    case SKV_SCORE_ATTN:
-      if (!dev_ptr_ok(k) || !dev_ptr_ok(q_obs)) return SKV_ERR_INVALID_ARG;
-      return launched(launch_score_attn(g, cfg->num_q_heads, cfg->obs_window, static_cast<const uint16_t*>(k),
-                                        static_cast<const uint16_t*>(q_obs), table, scratch, score, stream));
-    default:
-      return launched(launch_score_recency(g, table, score, stream));
-  }
+  if (st = check_score_inputs(cfg, k, v, q_obs); st != SKV_OK) return st;
+  return score_launch(cfg, k, v, q_obs, score, static_cast<const double*>(ws),
+                      static_cast<uint8_t*>(ws) + decay_table_bytes(cfg), stream);
+}
+
+skv_status skv_score_static(const skv_config* cfg, const void* k, const void* v, const void* q_obs,
+                            double* score, hipStream_t stream) {
+  skv_status st = check_config(cfg);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(score)) return SKV_ERR_INVALID_ARG;
+  if (st = check_score_inputs(cfg, k, v, q_obs); st != SKV_OK) return st;
+  const uint64_t table_bytes = decay_table_bytes(cfg);
+  if (table_bytes + round_up_256(scratch_bytes(cfg)) > SKV_STATIC_SCRATCH_BYTES) return SKV_ERR_CAPACITY;
+  uint8_t* base = nullptr;
+  if (st = static_scratch_prepare(cfg, stream, &base); st != SKV_OK) return st;
+  return score_launch(cfg, k, v, q_obs, score, reinterpret_cast<const double*>(base), base + table_bytes, stream);
 }
 
 skv_status skv_assign_tiers(const skv_config* cfg, const double* score, uint8_t* tier, void* ws,

@@ -22,9 +22,10 @@ UPGRADE_FP16, UPGRADE_RESIDUAL8 = 0, 1
 GROUP_TOKEN, GROUP_LAYER, GROUP_HEAD = 0, 1, 2
 QUANT_GROUP64, QUANT_GROUP32, QUANT_ASYM, QUANT_FP16, QUANT_CHANNEL = 1, 2, 4, 8, 16
 ABI_VERSION = 2
+STATIC_SCRATCH_BYTES = 48 << 20  # SKV_STATIC_SCRATCH_BYTES
 
 EXPORTED = ("skv_abi_version", "skv_status_string", "skv_plan_tiers", "skv_payload_size",
-            "skv_workspace_size", "skv_prepare", "skv_score", "skv_assign_tiers", "skv_pack",
+            "skv_workspace_size", "skv_prepare", "skv_score", "skv_score_static", "skv_assign_tiers", "skv_pack",
             "skv_unpack", "skv_pack_batch", "skv_unpack_batch", "skv_link", "skv_upgrade_size",
             "skv_pack_upgrade", "skv_unpack_upgrade", "skv_group_count", "skv_plan_groups",
             "skv_grouped_payload_size", "skv_group_workspace_size", "skv_prepare_groups", "skv_score_groups",
@@ -87,6 +88,7 @@ def lib():
             "skv_workspace_size": (ctypes.c_int, [cfgp, P(u64)]),
             "skv_prepare": (ctypes.c_int, [cfgp, vp, vp]),
             "skv_score": (ctypes.c_int, [cfgp, vp, vp, vp, vp, vp, vp]),
+            "skv_score_static": (ctypes.c_int, [cfgp, vp, vp, vp, vp, vp]),
             "skv_assign_tiers": (ctypes.c_int, [cfgp, vp, vp, vp, vp]),
             "skv_pack": (ctypes.c_int, [cfgp, vp, vp, vp, vp, u64, vp, vp]),
             "skv_unpack": (ctypes.c_int, [cfgp, vp, u64, vp, vp, vp, i32, i32, vp, vp]),
@@ -188,6 +190,20 @@ def score(cfg: Config, k: torch.Tensor, v: torch.Tensor, q_obs: Optional[torch.T
         qp = _dev(q_obs, torch.float16, qn, "q_obs")
     _check(lib().skv_score(ctypes.byref(cfg), kp, vp, qp, _dev(out, torch.float64, cfg.num_tokens, "score"),
                            _dev(ws, torch.uint8, workspace_size(cfg), "ws"), _stream(stream)), "skv_score")
+
+
+def score_static(cfg: Config, k: torch.Tensor, v: torch.Tensor, q_obs: Optional[torch.Tensor],
+                 out: torch.Tensor, stream=None):
+    """skv_score_static: skv_score with the library's own scratch (no workspace)."""
+    n = _kv_numel(cfg)
+    kp = _dev(k, torch.float16, n, "k") if cfg.score_mode != RECENCY else ctypes.c_void_p(None)
+    vp = _dev(v, torch.float16, n, "v") if cfg.score_mode == KVNORM else ctypes.c_void_p(None)
+    qp = ctypes.c_void_p(None)
+    if cfg.score_mode == ATTN:
+        qn = cfg.num_layers * cfg.num_q_heads * cfg.obs_window * cfg.head_dim
+        qp = _dev(q_obs, torch.float16, qn, "q_obs")
+    _check(lib().skv_score_static(ctypes.byref(cfg), kp, vp, qp, _dev(out, torch.float64, cfg.num_tokens, "score"),
+                                  _stream(stream)), "skv_score_static")
 
 
 def assign_tiers(cfg: Config, scores: torch.Tensor, tier: torch.Tensor, stream=None):
