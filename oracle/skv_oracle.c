@@ -318,6 +318,12 @@ int ora_sumsq(const ora_config* c, const uint16_t* k, const uint16_t* v, int32_t
   return ORA_OK;
 }
 
+/* The exact values of `count` binary16 elements (a key plane is decoded once
+ * and read by every query of the heads that share it). */
+static void decode_plane(const uint16_t* src, int64_t count, double* out) {
+  for (int64_t i = 0; i < count; ++i) out[i] = ora_half_to_double(src[i]);
+}
+
 /* Mean attention mass of every key over the observation queries of all layers
  * and query heads (Sec. 3: aggregate over layers, heads and decode
  * observations; Sec. 4.3: A_j observed or approximated).  Binary64 throughout.
@@ -329,18 +335,20 @@ static void attention_mass(const ora_config* c, const uint16_t* k, const uint16_
   double inv_sqrt_d = 1.0 / sqrt((double)d);
   double* z = (double*)malloc((size_t)n * sizeof(double));
   double* qv = (double*)malloc((size_t)d * sizeof(double));
+  double* kv = (double*)malloc((size_t)(n * d) * sizeof(double));
   for (int64_t t = 0; t < n; ++t) A[t] = 0.0;
   for (int64_t l = 0; l < L; ++l)
     for (int64_t hq = 0; hq < Hq; ++hq) {
       int64_t h = hq / grp;
+      if (hq % grp == 0) decode_plane(k + (l * H + h) * n * d, n * d, kv);
       for (int64_t w = 0; w < W; ++w) {
         const uint16_t* qr = q + ((l * Hq + hq) * W + w) * d;
         for (int64_t i = 0; i < d; ++i) qv[i] = ora_half_to_double(qr[i]);
         double zmax = -INFINITY;
         for (int64_t t = 0; t < n; ++t) {
-          const uint16_t* kr = k + ((l * H + h) * n + t) * d;
+          const double* kr = kv + t * d;
           double dot = 0.0;
-          for (int64_t i = 0; i < d; ++i) dot += qv[i] * ora_half_to_double(kr[i]);
+          for (int64_t i = 0; i < d; ++i) dot += qv[i] * kr[i];
           z[t] = dot * inv_sqrt_d;
           if (z[t] > zmax) zmax = z[t];
         }
@@ -353,6 +361,7 @@ static void attention_mass(const ora_config* c, const uint16_t* k, const uint16_
   for (int64_t t = 0; t < n; ++t) A[t] /= count;
   free(z);
   free(qv);
+  free(kv);
 }
 
 /* key[t] for every token.  KV-norm mode ranks by I_t^2 = ||KV_t||^2 e^{-2 lambda Delta}
@@ -1392,19 +1401,21 @@ static void attention_mass_groups(const ora_config* c, int32_t gran, const uint1
   double inv_sqrt_d = 1.0 / sqrt((double)d);
   double* z = (double*)malloc((size_t)n * sizeof(double));
   double* qv = (double*)malloc((size_t)d * sizeof(double));
+  double* kv = (double*)malloc((size_t)(n * d) * sizeof(double));
   for (int64_t i = 0; i < G * n; ++i) A[i] = 0.0;
   for (int64_t l = 0; l < L; ++l)
     for (int64_t hq = 0; hq < Hq; ++hq) {
       int64_t h = hq / grp;
       double* Ag = A + group_of(c, gran, l, h) * n;
+      if (hq % grp == 0) decode_plane(k + (l * H + h) * n * d, n * d, kv);
       for (int64_t w = 0; w < W; ++w) {
         const uint16_t* qr = q + ((l * Hq + hq) * W + w) * d;
         for (int64_t i = 0; i < d; ++i) qv[i] = ora_half_to_double(qr[i]);
         double zmax = -INFINITY;
         for (int64_t t = 0; t < n; ++t) {
-          const uint16_t* kr = k + ((l * H + h) * n + t) * d;
+          const double* kr = kv + t * d;
           double dot = 0.0;
-          for (int64_t i = 0; i < d; ++i) dot += qv[i] * ora_half_to_double(kr[i]);
+          for (int64_t i = 0; i < d; ++i) dot += qv[i] * kr[i];
           z[t] = dot * inv_sqrt_d;
           if (z[t] > zmax) zmax = z[t];
         }
@@ -1417,6 +1428,7 @@ static void attention_mass_groups(const ora_config* c, int32_t gran, const uint1
   for (int64_t i = 0; i < G * n; ++i) A[i] /= rows;
   free(z);
   free(qv);
+  free(kv);
 }
 
 /* key[g*n + t]: the score of token t in group g (eq. "importance" with the

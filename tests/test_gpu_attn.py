@@ -26,6 +26,13 @@ CASES = [
     (3, 2, 8, 16, 128, 2500, 0.5, 3),    # 64 rows, several key blocks
     (1, 1, 8, 20, 128, 3100, 0.5, 3),    # 160 rows: a second round of query tiles, ragged last block
     (1, 2, 6, 3, 32, 2100, 0.5, 3),      # 9 rows: four key streams over eight-tile stages
+    # the benchmark's launch geometry at two of its 32 layers: 32 query heads on
+    # 8 KV heads, 32-query window (128 rows, four query tiles), 32768 keys (32
+    # key blocks merged per (layer, head))
+    (2, 8, 32, 32, 128, 32768, 0.5, 3),
+    # Gemma-2-9B shape at two of its 42 layers: 16 query heads on 8 KV heads
+    # (64 rows), head dim 256, 8192 keys
+    (2, 8, 16, 32, 256, 8192, 0.5, 3),
 ]
 
 
