@@ -476,6 +476,60 @@ def run_quant(args, w):
     return out
 
 
+CEILING_PATTERNS = ["read", "write_nt", "write_default", "copy", "read2_write1", "read1_write2_8b",
+                    "read1_write2_16b", "nhd_scatter"]  # skv_ceiling.h, in enum order
+
+
+def run_ceiling(args):
+    """Streaming reference kernels (libskv_ceiling.so): the HBM rate of plain
+    read/write mixes at `--ceiling-gib` GiB, each launch timed with HIP events
+    on the stream it runs on, back to back (buffers far larger than the
+    caches)."""
+    import ctypes
+
+    import torch
+
+    path = os.path.join(ROOT, "paper_2606_08635_amd", "libskv_ceiling.so")
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    lib.skv_ceiling_run.restype = ctypes.c_int
+    lib.skv_ceiling_run.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
+                                    ctypes.c_void_p, ctypes.c_void_p]
+    lib.skv_ceiling_bytes.restype = ctypes.c_uint64
+    lib.skv_ceiling_bytes.argtypes = [ctypes.c_int32, ctypes.c_uint64, ctypes.c_int32]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    nbytes = int(args.ceiling_gib * (1 << 30))
+    nbytes -= nbytes % (128 << 10)
+    src = torch.ones(nbytes, dtype=torch.uint8, device=dev)
+    dst = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(1024, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    out = {}
+    for pat, name in enumerate(CEILING_PATTERNS):
+        def launch():
+            rc = lib.skv_ceiling_run(pat, ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()), nbytes,
+                                     ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+            if rc != 0:
+                raise RuntimeError(f"skv_ceiling_run({name}) returned {rc}")
+        for _ in range(args.warmup):
+            launch()
+        ev = _events(2 * args.steps)
+        for i in range(args.steps):
+            ev[2 * i].record(stream)
+            launch()
+            ev[2 * i + 1].record(stream)
+        torch.cuda.synchronize()
+        ms = sorted(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps))
+        mean = sum(ms) / len(ms)
+        rd, wr = lib.skv_ceiling_bytes(pat, nbytes, 0), lib.skv_ceiling_bytes(pat, nbytes, 1)
+        out[name] = {"read_bytes": rd, "write_bytes": wr, "ms_mean": round(mean, 4), "ms_min": round(ms[0], 4),
+                     "gbps": round((rd + wr) / (mean / 1e3) / 1e9, 1)}
+        print(f"[ceiling] {name}: {out[name]['gbps']} GB/s", file=sys.stderr, flush=True)
+    return {"bytes": nbytes, "steps": args.steps, "warmup": args.warmup, "patterns": out}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -489,11 +543,14 @@ def main():
     ap.add_argument("--obs-window", type=int, default=32)
     ap.add_argument("--no-flush", dest="flush_cache", action="store_false",
                     help="do not evict the caches (1 GiB write, then 1 GiB read) before each stage")
-    ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade", "groups", "quant"], default="step",
+    ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade", "groups", "quant", "ceiling"],
+                    default="step",
                     help="step: the headline codec step; batch: per-request vs batched launches over "
                          "a multi-request workload; pipeline: layer-pipelined handoff latency; "
                          "upgrade: cold-tier precision upgrade after the step; "
-                         "groups: per-layer and per-head tier maps; quant: per-tier quantizer variants")
+                         "groups: per-layer and per-head tier maps; quant: per-tier quantizer variants; "
+                         "ceiling: streaming reference kernels (achievable HBM rate of the codec's read/write mixes)")
+    ap.add_argument("--ceiling-gib", type=float, default=4.0, help="buffer size of --mode ceiling")
     ap.add_argument("--group-layers", type=int, default=4, help="layers per pipeline stage (--mode pipeline)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only copy a MIB-sized buffer with skv_link (reference for byte counters)")
@@ -517,6 +574,9 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": nbytes, "copies": args.warmup + args.steps}), flush=True)
         return
 
+    if args.mode == "ceiling":
+        print(json.dumps({"mode": "ceiling", **run_ceiling(args)}), flush=True)
+        return
     w = workloads.WORKLOADS[args.workload]
     if args.mode == "batch":
         if not w.batch_tokens:

@@ -1,0 +1,56 @@
+/*
+ * skv_ceiling.h -- streaming reference kernels (libskv_ceiling.so), a
+ * measurement aid kept apart from the codec's ABI in skv.h.
+ *
+ * They report what HBM delivers on this GPU for plain access patterns with
+ * the codec's mixes of reads and writes (pack reads about two bytes per byte
+ * written, unpack the reverse, and unpack's writes land as 256-byte pieces
+ * of the paged cache's token slots).  Bandwidth is not part of the paper's
+ * method; these kernels only move bytes.
+ */
+#ifndef SKV_CEILING_H_
+#define SKV_CEILING_H_
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Access patterns.  `bytes` (a multiple of 128 KiB) sizes every pattern; the
+ * bytes each one reads and writes are given by skv_ceiling_bytes. */
+enum {
+  SKV_CEIL_READ = 0,              /* read `bytes` (16-byte loads)                  */
+  SKV_CEIL_WRITE = 1,             /* write `bytes` (16-byte non-temporal stores)   */
+  SKV_CEIL_WRITE_DEFAULT = 2,     /* write `bytes` (16-byte default-policy stores) */
+  SKV_CEIL_COPY = 3,              /* read and write `bytes`                        */
+  SKV_CEIL_READ2_WRITE1 = 4,      /* read `bytes`, write bytes/2 (pack's mix)      */
+  SKV_CEIL_READ1_WRITE2_8B = 5,   /* read bytes/2 (8-byte loads), write `bytes`,
+                                     both contiguous (unpack's mix)               */
+  SKV_CEIL_READ1_WRITE2_16B = 6,  /* the same with 16-byte loads                   */
+  SKV_CEIL_NHD_SCATTER = 7        /* unpack's pattern at d = 128 with 8 heads: one
+                                     workgroup per 256-token chunk of a head reads
+                                     its 128-byte rows contiguously (bytes/2 in
+                                     all) and writes each as 256 bytes into the
+                                     token's slot of a [token][8][128] binary16
+                                     array (`bytes`), 2 KiB apart               */
+};
+
+/* Enqueues one pass of `pattern` on `stream`.  src (device, 16-byte aligned)
+ * holds at least the bytes the pattern reads, dst (device) at least the bytes
+ * it writes; sink (device, 4 KiB) is needed by SKV_CEIL_READ only, which
+ * stores into it only for an input it never sees.  Returns 0 on success, 1 for
+ * a bad argument (nothing enqueued), 2 if the launch failed. */
+int skv_ceiling_run(int32_t pattern, void* dst, const void* src, uint64_t bytes, void* sink, hipStream_t stream);
+
+/* Bytes read (which = 0) or written (which = 1) by one call of
+ * skv_ceiling_run(pattern, ..., bytes, ...); 0 for an unknown pattern. */
+uint64_t skv_ceiling_bytes(int32_t pattern, uint64_t bytes, int32_t which);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SKV_CEILING_H_ */

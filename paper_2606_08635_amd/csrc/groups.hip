@@ -23,19 +23,6 @@
 namespace skv {
 namespace {
 
-#ifndef SKV_PACK_ROWS_IN_FLIGHT
-#define SKV_PACK_ROWS_IN_FLIGHT 4
-#endif
-#ifndef SKV_PACK_NT_STORE
-#define SKV_PACK_NT_STORE 1
-#endif
-#ifndef SKV_UNPACK_ROWS_IN_FLIGHT
-#define SKV_UNPACK_ROWS_IN_FLIGHT 4
-#endif
-#ifndef SKV_UNPACK_NT_STORE
-#define SKV_UNPACK_NT_STORE 1
-#endif
-
 constexpr int kPrepThreads = 1024;
 constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
 constexpr uint32_t kGroupMagic = 0x47564B53u;  // "SKVG"
@@ -212,8 +199,8 @@ __global__ __launch_bounds__(kRowThreads) void gpack_rows(const GroupArgs a) {
   const uint8_t* tier = a.tier + static_cast<size_t>(g) * n;
   const uint16_t* src = (kv ? a.v : a.k) + (static_cast<size_t>(l) * H + h) * static_cast<size_t>(n) * D;
   // the first rows are loaded before the status check and the layout scan
-  RowBatch<D, SKV_PACK_ROWS_IN_FLIGHT> first;
-  pack_first_batch<D, SKV_PACK_ROWS_IN_FLIGHT>(first, src, tier, t0, n);
+  RowBatch<D, pack_rows_in_flight<D>()> first;
+  pack_first_batch<D, pack_rows_in_flight<D>()>(first, src, tier, t0, n);
   if (hdr[kGHdrStatus] != 0u) return;  // a tier map is off its plan: nothing to pack
   {
     const int t = t0 + threadIdx.x;
@@ -225,7 +212,7 @@ __global__ __launch_bounds__(kRowThreads) void gpack_rows(const GroupArgs a) {
   __syncthreads();
   const uint64_t sc_off = a.segtab[2 * seg], row_off = a.segtab[2 * seg + 1];
   uint8_t* dst = payload + row_off;
-  pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, first, src, dst,
+  pack_chunk<D, pack_rows_in_flight<D>(), pack_nt_store<D>()>(s, first, src, dst,
                                                             reinterpret_cast<float*>(payload + sc_off),
                                                             hdr + kGHdrNonfinite, t0, n);
   const uint32_t* e = a.group_table + 8 * g;
@@ -364,7 +351,7 @@ __global__ __launch_bounds__(kRowThreads) void gunpack_rows(const GroupArgs a, u
   const float* scales = reinterpret_cast<const float*>(payload + a.segtab[2 * seg]);
   uint16_t* cache = (kv ? v_cache : k_cache) + static_cast<size_t>(l) * a.num_blocks * block_size * H * D +
                     static_cast<size_t>(h) * D;
-  unpack_chunk<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, scales, cache, H);
+  unpack_chunk<D, unpack_rows_in_flight<D>(), unpack_nt_store<D>()>(s, src, scales, cache, H);
 }
 
 GroupArgs group_args(const GroupLaunch& gl) {

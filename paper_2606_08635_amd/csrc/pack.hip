@@ -19,14 +19,6 @@
 namespace skv {
 namespace {
 
-// Build-time tuning knobs (defaults are the measured best on MI355X).
-#ifndef SKV_PACK_ROWS_IN_FLIGHT
-#define SKV_PACK_ROWS_IN_FLIGHT 4
-#endif
-#ifndef SKV_PACK_NT_STORE
-#define SKV_PACK_NT_STORE 1
-#endif
-
 constexpr int kPrepThreads = 1024;
 constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
 
@@ -177,8 +169,10 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
   const uint16_t* src = (kv ? r.v : r.k) + (static_cast<size_t>(l) * H + h) * static_cast<size_t>(n) * D;
   // default quantizer: the first rows are loaded before the status check and
   // the layout scan (the reads stay inside K/V whatever the status)
-  RowBatch<D, SKV_PACK_ROWS_IN_FLIGHT> first;
-  if constexpr (!VARIANT) pack_first_batch<D, SKV_PACK_ROWS_IN_FLIGHT>(first, src, r.tier, t0, n);
+  constexpr int kRows = pack_rows_in_flight<D>();
+  constexpr bool kNT = pack_nt_store<D>();
+  RowBatch<D, kRows> first;
+  if constexpr (!VARIANT) pack_first_batch<D, kRows>(first, src, r.tier, t0, n);
   if (hdr[kHdrStatus] != 0u) return;  // tier map off plan: nothing to pack
   // per-channel K tiers: their K rows carry no per-row metadata and use the
   // K-side metadata offsets of the chunk index
@@ -205,21 +199,21 @@ __global__ __launch_bounds__(kRowThreads) void pack_rows(const BatchArgs a) {
       __shared__ __align__(16) ChanLds<D> c;
       uint8_t* blk = lay + r.scales_bytes + (static_cast<uint64_t>(h) * nchunks + chunk) * (a.cb8 + a.cb4);
       if constexpr (D <= 128) {  // the thread's rows fit in registers: one read of the chunk
-        pack_chunk_chan<D, SKV_PACK_NT_STORE>(s, c, src, dst, meta, nonfinite, t0, n, var, blk, blk + a.cb8);
+        pack_chunk_chan<D, kNT>(s, c, src, dst, meta, nonfinite, t0, n, var, blk, blk + a.cb8);
       } else {
         channel_params<D>(s, c, src, t0, var, blk, blk + a.cb8);
-        pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, true>(s, &c, src, dst, meta, nonfinite, t0, n,
+        pack_chunk_var<D, SKV_VAR_ROWS_IN_FLIGHT, kNT, true>(s, &c, src, dst, meta, nonfinite, t0, n,
                                                                             var);
       }
     } else {
-      pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, false>(s, nullptr, src, dst, meta, nonfinite, t0, n,
+      pack_chunk_var<D, SKV_VAR_ROWS_IN_FLIGHT, kNT, false>(s, nullptr, src, dst, meta, nonfinite, t0, n,
                                                                            var);
     }
   } else if constexpr (VARIANT) {
-    pack_chunk_var<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE, false>(s, nullptr, src, dst, meta, nonfinite, t0, n,
+    pack_chunk_var<D, SKV_VAR_ROWS_IN_FLIGHT, kNT, false>(s, nullptr, src, dst, meta, nonfinite, t0, n,
                                                                          var);
   } else {
-    pack_chunk<D, SKV_PACK_ROWS_IN_FLIGHT, SKV_PACK_NT_STORE>(s, first, src, dst, reinterpret_cast<float*>(meta),
+    pack_chunk<D, kRows, kNT>(s, first, src, dst, reinterpret_cast<float*>(meta),
                                                               nonfinite, t0, n);
   }
 

@@ -21,14 +21,6 @@
 namespace skv {
 namespace {
 
-// Build-time tuning knobs (defaults are the measured best on MI355X).
-#ifndef SKV_UNPACK_ROWS_IN_FLIGHT
-#define SKV_UNPACK_ROWS_IN_FLIGHT 4
-#endif
-#ifndef SKV_UNPACK_NT_STORE
-#define SKV_UNPACK_NT_STORE 1
-#endif
-
 constexpr int kCheckThreads = 1024;
 constexpr int kMaxChunks = kMaxTokens / kChunkTokens;
 
@@ -204,17 +196,17 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
       __shared__ ChanDecLds<D> c;
       const uint8_t* blk = lay + r.scales_bytes + (static_cast<uint64_t>(h) * nchunks + chunk) * (a.cb8 + a.cb4);
       const bool finite = load_channel_params<D>(c, blk, blk + a.cb8, var);
-      unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, true>(s, &c, finite, src, meta, cache, H,
+      unpack_chunk_var<D, SKV_VAR_ROWS_IN_FLIGHT, unpack_nt_store<D>(), true>(s, &c, finite, src, meta, cache, H,
                                                                                  var);
     } else {
-      unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, false>(s, nullptr, true, src, meta, cache, H,
+      unpack_chunk_var<D, SKV_VAR_ROWS_IN_FLIGHT, unpack_nt_store<D>(), false>(s, nullptr, true, src, meta, cache, H,
                                                                                   var);
     }
   } else if constexpr (VARIANT) {
-    unpack_chunk_var<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE, false>(s, nullptr, true, src, meta, cache, H,
+    unpack_chunk_var<D, SKV_VAR_ROWS_IN_FLIGHT, unpack_nt_store<D>(), false>(s, nullptr, true, src, meta, cache, H,
                                                                                 var);
   } else {
-    unpack_chunk<D, SKV_UNPACK_ROWS_IN_FLIGHT, SKV_UNPACK_NT_STORE>(s, src, reinterpret_cast<const float*>(meta),
+    unpack_chunk<D, unpack_rows_in_flight<D>(), unpack_nt_store<D>()>(s, src, reinterpret_cast<const float*>(meta),
                                                                      cache, H);
   }
 }
