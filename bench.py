@@ -35,8 +35,14 @@ CSRC = os.path.join(ROOT, "paper_2606_08635_amd", "csrc")
 # kernel sources they were taken on: the first 16 hex digits of SHA-256 over
 # the kernel's .hip file and every header of the library (source_digest).
 MEASURED_TRAFFIC = {
-    ("mistral7b_32k", "pack"): (6.5085e9, "pack.hip", "63cb70f0aff2569a"),
-    ("mistral7b_32k", "unpack"): (6.5125e9, "unpack.hip", "c509ea6966e7e1ca"),
+    ("mistral7b_32k", "pack"): (6.5085e9, "pack.hip", "81be23e26ec164a1"),
+    ("mistral7b_32k", "unpack"): (6.5128e9, "unpack.hip", "4c12f2ee3ba311ea"),
+    ("gemma9b_b0.3", "pack"): (3.6862e9, "pack.hip", "81be23e26ec164a1"),
+    ("gemma9b_b0.3", "unpack"): (3.6907e9, "unpack.hip", "4c12f2ee3ba311ea"),
+    ("gemma9b_b0.5", "pack"): (4.2500e9, "pack.hip", "81be23e26ec164a1"),
+    ("gemma9b_b0.5", "unpack"): (4.2545e9, "unpack.hip", "4c12f2ee3ba311ea"),
+    ("gemma9b_b0.7", "pack"): (4.8051e9, "pack.hip", "81be23e26ec164a1"),
+    ("gemma9b_b0.7", "unpack"): (4.8079e9, "unpack.hip", "4c12f2ee3ba311ea"),
 }
 
 
@@ -482,9 +488,10 @@ CEILING_PATTERNS = ["read", "write_nt", "write_default", "copy", "read2_write1",
 
 def run_ceiling(args):
     """Streaming reference kernels (libskv_ceiling.so): the HBM rate of plain
-    read/write mixes at `--ceiling-gib` GiB, each launch timed with HIP events
-    on the stream it runs on, back to back (buffers far larger than the
-    caches)."""
+    read/write mixes at `--ceiling-gib` GiB and 4, 8 or 16 loads in flight per
+    thread (the best of the three is the pattern's reference), each launch
+    timed with HIP events on the stream it runs on, back to back (buffers far
+    larger than the caches)."""
     import ctypes
 
     import torch
@@ -494,8 +501,8 @@ def run_ceiling(args):
         raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build()")
     lib = ctypes.CDLL(path)
     lib.skv_ceiling_run.restype = ctypes.c_int
-    lib.skv_ceiling_run.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
-                                    ctypes.c_void_p, ctypes.c_void_p]
+    lib.skv_ceiling_run.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p]
     lib.skv_ceiling_bytes.restype = ctypes.c_uint64
     lib.skv_ceiling_bytes.argtypes = [ctypes.c_int32, ctypes.c_uint64, ctypes.c_int32]
     dev = torch.device("cuda:0")
@@ -508,25 +515,29 @@ def run_ceiling(args):
     stream = torch.cuda.current_stream()
     out = {}
     for pat, name in enumerate(CEILING_PATTERNS):
-        def launch():
-            rc = lib.skv_ceiling_run(pat, ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()), nbytes,
-                                     ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
-            if rc != 0:
-                raise RuntimeError(f"skv_ceiling_run({name}) returned {rc}")
-        for _ in range(args.warmup):
-            launch()
-        ev = _events(2 * args.steps)
-        for i in range(args.steps):
-            ev[2 * i].record(stream)
-            launch()
-            ev[2 * i + 1].record(stream)
-        torch.cuda.synchronize()
-        ms = sorted(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps))
-        mean = sum(ms) / len(ms)
         rd, wr = lib.skv_ceiling_bytes(pat, nbytes, 0), lib.skv_ceiling_bytes(pat, nbytes, 1)
-        out[name] = {"read_bytes": rd, "write_bytes": wr, "ms_mean": round(mean, 4), "ms_min": round(ms[0], 4),
-                     "gbps": round((rd + wr) / (mean / 1e3) / 1e9, 1)}
-        print(f"[ceiling] {name}: {out[name]['gbps']} GB/s", file=sys.stderr, flush=True)
+        depths = (4,) if name.startswith("write") else (4, 8, 16)
+        res = {}
+        for depth in depths:
+            def launch():
+                rc = lib.skv_ceiling_run(pat, depth, ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()),
+                                         nbytes, ctypes.c_void_p(sink.data_ptr()), ctypes.c_void_p(stream.cuda_stream))
+                if rc != 0:
+                    raise RuntimeError(f"skv_ceiling_run({name}, {depth}) returned {rc}")
+            for _ in range(args.warmup):
+                launch()
+            ev = _events(2 * args.steps)
+            for i in range(args.steps):
+                ev[2 * i].record(stream)
+                launch()
+                ev[2 * i + 1].record(stream)
+            torch.cuda.synchronize()
+            mean = sum(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)) / args.steps
+            res[depth] = {"ms_mean": round(mean, 4), "gbps": round((rd + wr) / (mean / 1e3) / 1e9, 1)}
+        best = max(res, key=lambda k: res[k]["gbps"])
+        out[name] = {"read_bytes": rd, "write_bytes": wr, "best_gbps": res[best]["gbps"], "best_inflight": best,
+                     "by_inflight": res}
+        print(f"[ceiling] {name}: {out[name]['best_gbps']} GB/s ({best} in flight)", file=sys.stderr, flush=True)
     return {"bytes": nbytes, "steps": args.steps, "warmup": args.warmup, "patterns": out}
 
 

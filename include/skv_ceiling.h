@@ -38,12 +38,15 @@ enum {
                                      array (`bytes`), 2 KiB apart               */
 };
 
-/* Enqueues one pass of `pattern` on `stream`.  src (device, 16-byte aligned)
- * holds at least the bytes the pattern reads, dst (device) at least the bytes
- * it writes; sink (device, 4 KiB) is needed by SKV_CEIL_READ only, which
- * stores into it only for an input it never sees.  Returns 0 on success, 1 for
- * a bad argument (nothing enqueued), 2 if the launch failed. */
-int skv_ceiling_run(int32_t pattern, void* dst, const void* src, uint64_t bytes, void* sink, hipStream_t stream);
+/* Enqueues one pass of `pattern` on `stream`, each thread keeping `inflight`
+ * (4, 8 or 16) loads in flight before it uses them (the write-only patterns
+ * ignore it).  src (device, 16-byte aligned) holds at least the bytes the
+ * pattern reads, dst (device) at least the bytes it writes; sink (device,
+ * 4 KiB) is needed by SKV_CEIL_READ only, which stores into it only for an
+ * input it never sees.  Returns 0 on success, 1 for a bad argument (nothing
+ * enqueued), 2 if the launch failed. */
+int skv_ceiling_run(int32_t pattern, int32_t inflight, void* dst, const void* src, uint64_t bytes, void* sink,
+                    hipStream_t stream);
 
 /* Bytes read (which = 0) or written (which = 1) by one call of
  * skv_ceiling_run(pattern, ..., bytes, ...); 0 for an unknown pattern. */

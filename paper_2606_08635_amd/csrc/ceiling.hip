@@ -5,8 +5,9 @@
 // bytes and computes nothing.
 //
 // Every kernel runs 256 threads per workgroup; a thread moves 16-byte units
-// with four loads in flight, like the codec's row kernels.  Stores are
-// non-temporal (the codec's policy) unless noted.
+// with F = 4, 8 or 16 loads in flight (issued before any of them is used),
+// as the codec's row kernels do with their rows.  Stores are non-temporal
+// (the codec's policy) unless noted.
 #include <stdint.h>
 
 #include <hip/hip_runtime.h>
@@ -37,16 +38,17 @@ __device__ __forceinline__ void st16(void* p, u32x4 v) {
 // Read-only: every 16-byte unit of the workgroup's tile is loaded; the xor of
 // everything read is stored only if it equals a value no input here holds,
 // which the compiler cannot know, so no load is dropped.
+template <int F>
 __global__ __launch_bounds__(kThreads) void read_only(const uint8_t* __restrict__ src, uint32_t* __restrict__ sink) {
   const uint8_t* base = src + blockIdx.x * kTile + threadIdx.x * 16;
   u32x4 acc{0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int s = 0; s < kSteps; s += 4) {
-    u32x4 x[4];
+  for (int s = 0; s < kSteps; s += F) {
+    u32x4 x[F];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) x[u] = ld16(base + (s + u) * kThreads * 16);
+    for (int u = 0; u < F; ++u) x[u] = ld16(base + (s + u) * kThreads * 16);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) acc ^= x[u];
+    for (int u = 0; u < F; ++u) acc ^= x[u];
   }
   if ((acc.x ^ acc.y ^ acc.z ^ acc.w) == 0x9E3779B9u) sink[blockIdx.x & 1023] = acc.x;
 }
@@ -60,30 +62,32 @@ __global__ __launch_bounds__(kThreads) void write_only(uint8_t* __restrict__ dst
 }
 
 // Copy: the tile read and written once.
+template <int F>
 __global__ __launch_bounds__(kThreads) void copy_1to1(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst) {
   const uint64_t off = blockIdx.x * kTile + threadIdx.x * 16;
 #pragma unroll
-  for (int s = 0; s < kSteps; s += 4) {
-    u32x4 x[4];
+  for (int s = 0; s < kSteps; s += F) {
+    u32x4 x[F];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) x[u] = ld16(src + off + (s + u) * kThreads * 16);
+    for (int u = 0; u < F; ++u) x[u] = ld16(src + off + (s + u) * kThreads * 16);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) st16<true>(dst + off + (s + u) * kThreads * 16, x[u]);
+    for (int u = 0; u < F; ++u) st16<true>(dst + off + (s + u) * kThreads * 16, x[u]);
   }
 }
 
 // Two bytes read per byte written (pack's mix): a 128 KiB read tile, a
 // 64 KiB write tile.
+template <int F>
 __global__ __launch_bounds__(kThreads) void read2_write1(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst) {
   const uint8_t* in = src + 2 * blockIdx.x * kTile + threadIdx.x * 16;
   uint8_t* out = dst + blockIdx.x * kTile + threadIdx.x * 16;
 #pragma unroll
-  for (int s = 0; s < kSteps; s += 2) {
-    u32x4 x[4];
+  for (int s = 0; s < kSteps; s += F / 2) {
+    u32x4 x[F];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) x[u] = ld16(in + (2 * s + u) * kThreads * 16);
-    st16<true>(out + s * kThreads * 16, x[0] ^ x[1]);
-    st16<true>(out + (s + 1) * kThreads * 16, x[2] ^ x[3]);
+    for (int u = 0; u < F; ++u) x[u] = ld16(in + (2 * s + u) * kThreads * 16);
+#pragma unroll
+    for (int u = 0; u < F / 2; ++u) st16<true>(out + (s + u) * kThreads * 16, x[2 * u] ^ x[2 * u + 1]);
   }
 }
 
@@ -91,29 +95,30 @@ __global__ __launch_bounds__(kThreads) void read2_write1(const uint8_t* __restri
 // thread reads 8 bytes and writes the 16 bytes that follow from them, like an
 // INT8 row slice decoded to binary16.  RB = 8: 8-byte reads (a 32 KiB read
 // tile per workgroup); RB = 16: 16-byte reads, 32 bytes written per read.
-template <int RB>
+template <int RB, int F>
 __global__ __launch_bounds__(kThreads) void read1_write2(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst) {
   if constexpr (RB == 8) {
     const uint8_t* in = src + blockIdx.x * (kTile / 2) + threadIdx.x * 8;
     uint8_t* out = dst + blockIdx.x * kTile + threadIdx.x * 16;
 #pragma unroll
-    for (int s = 0; s < kSteps; s += 4) {
-      u32x2 x[4];
+    for (int s = 0; s < kSteps; s += F) {
+      u32x2 x[F];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) x[u] = ld8(in + (s + u) * kThreads * 8);
+      for (int u = 0; u < F; ++u) x[u] = ld8(in + (s + u) * kThreads * 8);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) st16<true>(out + (s + u) * kThreads * 16, u32x4{x[u].x, x[u].y, x[u].x, x[u].y});
+      for (int u = 0; u < F; ++u) st16<true>(out + (s + u) * kThreads * 16, u32x4{x[u].x, x[u].y, x[u].x, x[u].y});
     }
   } else {
+    constexpr int G = F < kSteps / 2 ? F : kSteps / 2;
     const uint8_t* in = src + blockIdx.x * (kTile / 2) + threadIdx.x * 16;
     uint8_t* out = dst + blockIdx.x * kTile + threadIdx.x * 32;
 #pragma unroll
-    for (int s = 0; s < kSteps / 2; s += 4) {
-      u32x4 x[4];
+    for (int s = 0; s < kSteps / 2; s += G) {
+      u32x4 x[G];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) x[u] = ld16(in + (s + u) * kThreads * 16);
+      for (int u = 0; u < G; ++u) x[u] = ld16(in + (s + u) * kThreads * 16);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int u = 0; u < G; ++u) {
         st16<true>(out + (s + u) * kThreads * 32, x[u]);
         st16<true>(out + (s + u) * kThreads * 32 + 16, x[u] ^ u32x4{1u, 1u, 1u, 1u});
       }
@@ -129,6 +134,7 @@ __global__ __launch_bounds__(kThreads) void read1_write2(const uint8_t* __restri
 // pieces of one workgroup land 2 KiB apart.
 constexpr int kNhdHeads = 8;
 constexpr int kNhdRow = 128;  // bytes read per token row
+template <int F>
 __global__ __launch_bounds__(kThreads) void nhd_scatter(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst,
                                                         uint32_t tokens) {
   const uint32_t nchunks = tokens / 256;
@@ -136,23 +142,50 @@ __global__ __launch_bounds__(kThreads) void nhd_scatter(const uint8_t* __restric
   const int lane = threadIdx.x % 16, rsub = threadIdx.x / 16;
   const uint8_t* seg = src + (static_cast<uint64_t>(h) * tokens + chunk * 256) * kNhdRow;
 #pragma unroll
-  for (int s = 0; s < 16; s += 4) {
-    u32x2 x[4];
+  for (int s = 0; s < 16; s += F) {
+    u32x2 x[F];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) x[u] = ld8(seg + ((s + u) * 16 + rsub) * kNhdRow + lane * 8);
+    for (int u = 0; u < F; ++u) x[u] = ld8(seg + ((s + u) * 16 + rsub) * kNhdRow + lane * 8);
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < F; ++u) {
       const uint64_t t = chunk * 256 + (s + u) * 16 + rsub;
       st16<true>(dst + (t * kNhdHeads + h) * (2 * kNhdRow) + lane * 16, u32x4{x[u].x, x[u].y, x[u].x, x[u].y});
     }
   }
 }
 
+template <int F>
+int run_pattern(int32_t pattern, uint8_t* out, const uint8_t* in, uint64_t bytes, uint64_t tiles, uint32_t* sink,
+                hipStream_t stream) {
+  switch (pattern) {
+    case SKV_CEIL_READ:
+      if (sink == nullptr) return 1;
+      read_only<F><<<tiles, kThreads, 0, stream>>>(in, sink);
+      break;
+    case SKV_CEIL_WRITE: write_only<true><<<tiles, kThreads, 0, stream>>>(out); break;
+    case SKV_CEIL_WRITE_DEFAULT: write_only<false><<<tiles, kThreads, 0, stream>>>(out); break;
+    case SKV_CEIL_COPY: copy_1to1<F><<<tiles, kThreads, 0, stream>>>(in, out); break;
+    case SKV_CEIL_READ2_WRITE1: read2_write1<F><<<tiles / 2, kThreads, 0, stream>>>(in, out); break;
+    case SKV_CEIL_READ1_WRITE2_8B: read1_write2<8, F><<<tiles, kThreads, 0, stream>>>(in, out); break;
+    case SKV_CEIL_READ1_WRITE2_16B: read1_write2<16, F><<<tiles, kThreads, 0, stream>>>(in, out); break;
+    case SKV_CEIL_NHD_SCATTER: {
+      // bytes written = tokens * 8 heads * 256 B; tokens a multiple of 256
+      const uint64_t tokens = bytes / (kNhdHeads * 2 * kNhdRow);
+      if (tokens % 256 != 0 || tokens > 0xFFFFFFFFu) return 1;
+      nhd_scatter<F><<<(tokens / 256) * kNhdHeads, kThreads, 0, stream>>>(in, out, static_cast<uint32_t>(tokens));
+      break;
+    }
+    default: return 1;
+  }
+  return hipGetLastError() == hipSuccess ? 0 : 2;
+}
+
 }  // namespace
 
 extern "C" {
 
-int skv_ceiling_run(int32_t pattern, void* dst, const void* src, uint64_t bytes, void* sink, hipStream_t stream) {
+int skv_ceiling_run(int32_t pattern, int32_t inflight, void* dst, const void* src, uint64_t bytes, void* sink,
+                    hipStream_t stream) {
   if (bytes == 0 || bytes % (2 * kTile) != 0 || dst == nullptr) return 1;
   const uint8_t* in = static_cast<const uint8_t*>(src);
   uint8_t* out = static_cast<uint8_t*>(dst);
@@ -160,27 +193,13 @@ int skv_ceiling_run(int32_t pattern, void* dst, const void* src, uint64_t bytes,
   if (tiles > 0x7FFFFFFFu) return 1;
   const bool reads = pattern != SKV_CEIL_WRITE && pattern != SKV_CEIL_WRITE_DEFAULT;
   if (reads && src == nullptr) return 1;
-  switch (pattern) {
-    case SKV_CEIL_READ:
-      if (sink == nullptr) return 1;
-      read_only<<<tiles, kThreads, 0, stream>>>(in, static_cast<uint32_t*>(sink));
-      break;
-    case SKV_CEIL_WRITE: write_only<true><<<tiles, kThreads, 0, stream>>>(out); break;
-    case SKV_CEIL_WRITE_DEFAULT: write_only<false><<<tiles, kThreads, 0, stream>>>(out); break;
-    case SKV_CEIL_COPY: copy_1to1<<<tiles, kThreads, 0, stream>>>(in, out); break;
-    case SKV_CEIL_READ2_WRITE1: read2_write1<<<tiles / 2, kThreads, 0, stream>>>(in, out); break;
-    case SKV_CEIL_READ1_WRITE2_8B: read1_write2<8><<<tiles, kThreads, 0, stream>>>(in, out); break;
-    case SKV_CEIL_READ1_WRITE2_16B: read1_write2<16><<<tiles, kThreads, 0, stream>>>(in, out); break;
-    case SKV_CEIL_NHD_SCATTER: {
-      // bytes written = tokens * 8 heads * 256 B; tokens a multiple of 256
-      const uint64_t tokens = bytes / (kNhdHeads * 2 * kNhdRow);
-      if (tokens % 256 != 0 || tokens > 0xFFFFFFFFu) return 1;
-      nhd_scatter<<<(tokens / 256) * kNhdHeads, kThreads, 0, stream>>>(in, out, static_cast<uint32_t>(tokens));
-      break;
-    }
+  uint32_t* sk = static_cast<uint32_t*>(sink);
+  switch (inflight) {
+    case 4: return run_pattern<4>(pattern, out, in, bytes, tiles, sk, stream);
+    case 8: return run_pattern<8>(pattern, out, in, bytes, tiles, sk, stream);
+    case 16: return run_pattern<16>(pattern, out, in, bytes, tiles, sk, stream);
     default: return 1;
   }
-  return hipGetLastError() == hipSuccess ? 0 : 2;
 }
 
 uint64_t skv_ceiling_bytes(int32_t pattern, uint64_t bytes, int32_t which) {

@@ -22,8 +22,8 @@ def lib():
     L.skv_ceiling_bytes.restype = ctypes.c_uint64
     L.skv_ceiling_bytes.argtypes = [ctypes.c_int32, ctypes.c_uint64, ctypes.c_int32]
     L.skv_ceiling_run.restype = ctypes.c_int
-    L.skv_ceiling_run.argtypes = [ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
-                                  ctypes.c_void_p, ctypes.c_void_p]
+    L.skv_ceiling_run.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                  ctypes.c_uint64, ctypes.c_void_p, ctypes.c_void_p]
     return L
 
 
@@ -45,8 +45,9 @@ def test_byte_accounting(lib):
 
 def test_bad_arguments_refused_before_launch(lib):
     fake = ctypes.c_void_p(1 << 20)
-    assert lib.skv_ceiling_run(3, fake, fake, 12345, None, None) == 1       # not a multiple of 128 KiB
-    assert lib.skv_ceiling_run(3, None, fake, 1 << 20, None, None) == 1     # no destination
-    assert lib.skv_ceiling_run(3, fake, None, 1 << 20, None, None) == 1     # a reading pattern without a source
-    assert lib.skv_ceiling_run(0, fake, fake, 1 << 20, None, None) == 1     # read-only needs the sink
-    assert lib.skv_ceiling_run(99, fake, fake, 1 << 20, None, None) == 1    # unknown pattern
+    assert lib.skv_ceiling_run(3, 4, fake, fake, 12345, None, None) == 1       # not a multiple of 128 KiB
+    assert lib.skv_ceiling_run(3, 4, None, fake, 1 << 20, None, None) == 1     # no destination
+    assert lib.skv_ceiling_run(3, 4, fake, None, 1 << 20, None, None) == 1     # a reading pattern without a source
+    assert lib.skv_ceiling_run(0, 4, fake, fake, 1 << 20, None, None) == 1     # read-only needs the sink
+    assert lib.skv_ceiling_run(99, 4, fake, fake, 1 << 20, None, None) == 1    # unknown pattern
+    assert lib.skv_ceiling_run(3, 5, fake, fake, 1 << 20, None, None) == 1     # unsupported depth
