@@ -170,8 +170,8 @@ def _events(count):
 
 
 def run_batch(args, w):
-    """Per-request pack/unpack calls vs one batched launch per stage over the
-    workload's requests (NEXT-1).  Returns a JSON-able dict."""
+    """Per-request calls vs batched launches (score, assign, pack, unpack) over
+    the workload's requests (NEXT-1).  Returns a JSON-able dict."""
     import torch
 
     from paper_2606_08635_amd import skv, workloads
@@ -202,6 +202,21 @@ def run_batch(args, w):
     pst = [c.status[0:1] for c in codecs]
     ust = [c.status[1:2] for c in codecs]
 
+    bcfg = skv.config(L, H, d, max(lens), w.budget, first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers)
+    bscores = [torch.empty(n, dtype=torch.float64, device="cuda") for n in lens]
+    btiers = [torch.empty(n, dtype=torch.uint8, device="cuda") for n in lens]
+    bws = torch.empty(max(skv.batch_workspace_size(bcfg, bscores), skv.workspace_size(bcfg)), dtype=torch.uint8,
+                      device="cuda")
+    skv.prepare(bcfg, bws)
+
+    def single_score():
+        for c, k, v in zip(codecs, ks, vs):
+            skv.score(c.cfg, k, v, None, c.scores, c.ws)
+
+    def single_assign():
+        for c in codecs:
+            skv.assign_tiers(c.cfg, c.scores, c.tier)
+
     def single():
         for c, k, v in zip(codecs, ks, vs):
             skv.pack(c.cfg, k, v, c.tier, c.payload, c.status[0:1])
@@ -210,33 +225,46 @@ def run_batch(args, w):
         for c, t in zip(codecs, tables):
             skv.unpack(c.cfg, c.payload, kc, vc, t, bs, c.status[1:2])
 
+    def batched_score():
+        skv.score_batch(bcfg, ks, vs, bscores, bws)
+
+    def batched_assign():
+        skv.assign_batch(bcfg, bscores, btiers)
+
     def batched():
-        skv.pack_batch(base, ks, vs, tiers, pays, pst)
+        skv.pack_batch(base, ks, vs, btiers, pays, pst)
 
     def batched_unpack():
         skv.unpack_batch(base, pays, lens, tables, kc, vc, bs, ust)
 
     out = {}
-    for name, fp, fu in (("per_request", single, single_unpack), ("batched", batched, batched_unpack)):
+    F = sum(4 * L * H * d * n for n in lens)
+    for name, stages in (("per_request", (single_score, single_assign, single, single_unpack)),
+                         ("batched", (batched_score, batched_assign, batched, batched_unpack))):
         for _ in range(args.warmup):
-            fp()
-            fu()
-        ev = [_events(3) for _ in range(args.steps)]
+            for f in stages:
+                f()
+        ev = [_events(5) for _ in range(args.steps)]
         for e in ev:
             e[0].record()
-            fp()
-            e[1].record()
-            fu()
-            e[2].record()
+            for i, f in enumerate(stages):
+                f()
+                e[i + 1].record()
         torch.cuda.synchronize()
-        tp = sum(e[0].elapsed_time(e[1]) for e in ev) / args.steps
-        tu = sum(e[1].elapsed_time(e[2]) for e in ev) / args.steps
-        F = sum(4 * L * H * d * n for n in lens)
-        out[name] = {"pack_ms": round(tp, 4), "unpack_ms": round(tu, 4),
+        t = [sum(e[i].elapsed_time(e[i + 1]) for e in ev) / args.steps for i in range(4)]
+        ts, ta, tp, tu = t
+        out[name] = {"score_ms": round(ts, 4), "assign_ms": round(ta, 4), "pack_ms": round(tp, 4),
+                     "unpack_ms": round(tu, 4), "encode_ms": round(ts + ta + tp, 4),
                      "fp16eq_gbps": round(F / ((tp + tu) / 1e3) / 1e9, 2),
-                     "tokens_per_s": round(sum(lens) / ((tp + tu) / 1e3), 1)}
+                     "tokens_per_s": round(sum(lens) / ((tp + tu) / 1e3), 1),
+                     "encode_tokens_per_s": round(sum(lens) / ((ts + ta + tp) / 1e3), 1),
+                     "handoff_tokens_per_s": round(sum(lens) / ((ts + ta + tp + tu) / 1e3), 1)}
         if any(int(c.status[0].item()) != 0 or int(c.status[1].item()) != 0 for c in codecs):
             raise RuntimeError("codec reported a nonzero status")
+    # the batched maps and payloads are the per-request ones
+    for c, bt in zip(codecs, btiers):
+        if not torch.equal(c.tier, bt):
+            raise RuntimeError("batched tier map differs from the per-request one")
     return {"requests": len(lens), "tokens": sum(lens), **out}
 
 
@@ -482,6 +510,53 @@ def run_quant(args, w):
     return out
 
 
+def run_select(args):
+    """The tier cut alone (skv_assign_tiers / skv_assign_batch) on seeded
+    random scores: the resident form at 32768 tokens, the general form at
+    2^21, and 64 requests of 2048 tokens per request vs batched.  HIP events,
+    mean over the timed launches."""
+    import torch
+
+    from paper_2606_08635_amd import skv
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        ev = _events(2 * args.steps)
+        for i in range(args.steps):
+            ev[2 * i].record()
+            fn()
+            ev[2 * i + 1].record()
+        torch.cuda.synchronize()
+        return sum(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)) / args.steps
+
+    out = {}
+    for n in (32768, 1 << 21):
+        cfg = skv.config(32, 8, 128, n, 0.5, decay=1e-4)
+        sc = torch.rand(n, generator=g, device=dev, dtype=torch.float64)
+        tier = torch.empty(n, dtype=torch.uint8, device=dev)
+        ms = timed(lambda: skv.assign_tiers(cfg, sc, tier))
+        out[f"single_n{n}"] = {"ms": round(ms, 4), "tokens_per_s": round(n / (ms / 1e3), 1)}
+    lens = [2048] * 64
+    cfgs = [skv.config(32, 8, 128, n, 0.5) for n in lens]
+    bcfg = skv.config(32, 8, 128, max(lens), 0.5)
+    scores = [torch.rand(n, generator=g, device=dev, dtype=torch.float64) for n in lens]
+    tiers = [torch.empty(n, dtype=torch.uint8, device=dev) for n in lens]
+
+    def per_request():
+        for c, s_, t_ in zip(cfgs, scores, tiers):
+            skv.assign_tiers(c, s_, t_)
+
+    out["per_request_64x2048"] = {"ms": round(timed(per_request), 4)}
+    out["batched_64x2048"] = {"ms": round(timed(lambda: skv.assign_batch(bcfg, scores, tiers)), 4)}
+    return out
+
+
 CEILING_PATTERNS = ["read", "write_nt", "write_default", "copy", "read2_write1", "read1_write2_8b",
                     "read1_write2_16b", "nhd_scatter"]  # skv_ceiling.h, in enum order
 
@@ -554,13 +629,14 @@ def main():
     ap.add_argument("--obs-window", type=int, default=32)
     ap.add_argument("--no-flush", dest="flush_cache", action="store_false",
                     help="do not evict the caches (1 GiB write, then 1 GiB read) before each stage")
-    ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade", "groups", "quant", "ceiling"],
+    ap.add_argument("--mode", choices=["step", "batch", "pipeline", "upgrade", "groups", "quant", "ceiling", "select"],
                     default="step",
                     help="step: the headline codec step; batch: per-request vs batched launches over "
                          "a multi-request workload; pipeline: layer-pipelined handoff latency; "
                          "upgrade: cold-tier precision upgrade after the step; "
                          "groups: per-layer and per-head tier maps; quant: per-tier quantizer variants; "
-                         "ceiling: streaming reference kernels (achievable HBM rate of the codec's read/write mixes)")
+                         "ceiling: streaming reference kernels (achievable HBM rate of the codec's read/write mixes); "
+                         "select: the tier cut alone at 32768 and 2^21 tokens and over 64 short requests")
     ap.add_argument("--ceiling-gib", type=float, default=4.0, help="buffer size of --mode ceiling")
     ap.add_argument("--group-layers", type=int, default=4, help="layers per pipeline stage (--mode pipeline)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -587,6 +663,9 @@ def main():
 
     if args.mode == "ceiling":
         print(json.dumps({"mode": "ceiling", **run_ceiling(args)}), flush=True)
+        return
+    if args.mode == "select":
+        print(json.dumps({"mode": "select", **run_select(args)}), flush=True)
         return
     w = workloads.WORKLOADS[args.workload]
     if args.mode == "batch":

@@ -324,6 +324,44 @@ skv_status skv_unpack_batch(const skv_config* cfg, const skv_request* reqs, int3
                             void* k_cache, void* v_cache, int32_t num_blocks, int32_t block_size,
                             int32_t layer_begin, int32_t layer_count, hipStream_t stream);
 
+/* One request of a batched score / assign (skv_score_batch,
+ * skv_assign_batch).  Device pointers, 16-byte aligned (tier: any). */
+typedef struct skv_score_request {
+  int32_t num_tokens; /* n of this request (1 .. cfg->num_tokens)              */
+  int32_t reserved;   /* must be 0                                             */
+  const void* k;      /* K, binary16 [L][H][n][d] (KV-norm mode; else unused)  */
+  const void* v;      /* V, binary16 [L][H][n][d] (KV-norm mode; else unused)  */
+  double* score;      /* double[n]: written by skv_score_batch, read by
+                         skv_assign_batch                                      */
+  uint8_t* tier;      /* uint8[n]: written by skv_assign_batch                 */
+} skv_score_request;
+
+/* Host only.  Workspace bytes of skv_score_batch for these requests: the
+ * decay table of cfg (cfg->num_tokens entries, at least every request's n)
+ * followed by each request's partial sums.  Errors as skv_score_batch's host
+ * checks. */
+skv_status skv_batch_workspace_size(const skv_config* cfg, const skv_score_request* reqs, int32_t count,
+                                    uint64_t* bytes);
+
+/* Batched scoring (Sec. 4.3; Sec. 9 (i), batching many requests): the
+ * `count` requests share every field of cfg except the token count (each
+ * carries its own n <= cfg->num_tokens); each request's scores are exactly
+ * those of skv_score on that request alone.  KV-norm and recency modes only
+ * (attention mode: SKV_ERR_INVALID_ARG).  One launch per kernel covers up to
+ * 48 requests (larger batches are split).  ws: at least
+ * skv_batch_workspace_size bytes, prepared by skv_prepare(cfg, ...) -- one
+ * decay table serves every request, since its entry for Delta does not depend
+ * on n.  Every request is checked before anything is enqueued. */
+skv_status skv_score_batch(const skv_config* cfg, const skv_score_request* reqs, int32_t count, void* ws,
+                           hipStream_t stream);
+
+/* Batched tier assignment (Sec. 2.3 Prop. 1; Sec. 4.4): each request's tier
+ * map is exactly skv_assign_tiers' on its scores with the plan of cfg at its
+ * own n (SKV_ERR_BUDGET if some request's sinks exceed its budget).  One
+ * workgroup per request, one launch for up to 48 requests. */
+skv_status skv_assign_batch(const skv_config* cfg, const skv_score_request* reqs, int32_t count,
+                            hipStream_t stream);
+
 /* Cold-tier precision upgrade (Sec. 4.2 and its architecture figure: tokens
  * the decoder holds at low precision are upgraded by an on-demand fetch;
  * Sec. 8, cold-tier fetch design).  Upgrade payload, little-endian, sections

@@ -13,6 +13,8 @@
 //     128-bit integer arithmetic across lanes and layer groups.
 // A non-finite input turns an accumulator into inf/NaN; only then does the
 // thread redo its sum with non-finite elements skipped.
+#include <algorithm>
+
 #include "device_util.h"
 #include "skv_internal.h"
 
@@ -86,18 +88,17 @@ __device__ __forceinline__ void acc16(u32x4 x, double& ah, double& al) {
 // pairs_per_group).  Writes the 128-bit partial sum of each token and part in
 // units of 2^-48 to partial[(part * n + t) * 2 + {0: lo, 1: hi}].
 template <int D>
-__global__ __launch_bounds__(kThreads) void kvnorm_partial(const uint16_t* __restrict__ k,
-                                                          const uint16_t* __restrict__ v, int n,
-                                                          int pairs, int pairs_per_group, int parts_per_block,
-                                                          uint64_t* __restrict__ partial) {
+__device__ __forceinline__ void kvnorm_partial_block(const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+                                                     int n, int pairs, int pairs_per_group, int parts_per_block,
+                                                     uint64_t* __restrict__ partial, int tok_block, int part_block) {
   constexpr int LPR = D / 8;
   constexpr int TOK = kThreads / LPR;
   __shared__ U128 s_part[kThreads];
   const int lane = threadIdx.x % LPR;
   const int r = threadIdx.x / LPR;
-  const int t = blockIdx.x * TOK + r;
+  const int t = tok_block * TOK + r;
   for (int pb = 0; pb < parts_per_block; ++pb) {  // block-uniform
-  const int part = blockIdx.y * parts_per_block + pb;
+  const int part = part_block * parts_per_block + pb;
   const int p0 = part * pairs_per_group;
   if (p0 >= pairs) break;
   const int p1 = min(pairs, p0 + pairs_per_group);
@@ -166,12 +167,33 @@ __global__ __launch_bounds__(kThreads) void kvnorm_partial(const uint16_t* __res
   }
 }
 
-__global__ __launch_bounds__(kThreads) void kvnorm_finish(const uint64_t* __restrict__ partial,
-                                                         int groups, int n,
-                                                         const double* __restrict__ w2,
-                                                         double* __restrict__ score) {
-  const int t = blockIdx.x * kThreads + threadIdx.x;
-  if (t >= n) return;
+template <int D>
+__global__ __launch_bounds__(kThreads) void kvnorm_partial(const uint16_t* __restrict__ k,
+                                                          const uint16_t* __restrict__ v, int n,
+                                                          int pairs, int pairs_per_group, int parts_per_block,
+                                                          uint64_t* __restrict__ partial) {
+  kvnorm_partial_block<D>(k, v, n, pairs, pairs_per_group, parts_per_block, partial, blockIdx.x, blockIdx.y);
+}
+
+// Request of a batched launch that owns flat block `b` (the last whose first
+// block is at most b; requests are in block order).
+__device__ __forceinline__ int score_request_of(const ScoreBatchArgs& a, uint32_t b, bool finish) {
+  int r = 0;
+  for (int i = 1; i < a.count; ++i)
+    if ((finish ? a.r[i].fin_block_begin : a.r[i].tok_block_begin) <= b) r = i;
+  return r;
+}
+
+// grid: (sum over requests of their token blocks, part blocks)
+template <int D>
+__global__ __launch_bounds__(kThreads) void kvnorm_partial_batch(const ScoreBatchArgs a) {
+  const ScoreDesc& q = a.r[score_request_of(a, blockIdx.x, false)];
+  kvnorm_partial_block<D>(q.k, q.v, q.n, a.pairs, a.pairs_per_group, a.parts_per_block, q.partial,
+                          static_cast<int>(blockIdx.x - q.tok_block_begin), blockIdx.y);
+}
+
+__device__ __forceinline__ void kvnorm_finish_token(const uint64_t* __restrict__ partial, int groups, int n, int t,
+                                                    const double* __restrict__ w2, double* __restrict__ score) {
   U128 s{0, 0};
   for (int g = 0; g < groups; ++g) {
     const uint64_t* p = partial + (static_cast<size_t>(g) * n + t) * 2;
@@ -180,6 +202,28 @@ __global__ __launch_bounds__(kThreads) void kvnorm_finish(const uint64_t* __rest
   // RN64(S) then an exact scaling by 2^-48 (the result is 0 or >= 2^-48)
   const double sd = u128_to_double(s) * 0x1p-48;
   score[t] = sd * w2[n - 1 - t];
+}
+
+__global__ __launch_bounds__(kThreads) void kvnorm_finish(const uint64_t* __restrict__ partial,
+                                                         int groups, int n,
+                                                         const double* __restrict__ w2,
+                                                         double* __restrict__ score) {
+  const int t = blockIdx.x * kThreads + threadIdx.x;
+  if (t < n) kvnorm_finish_token(partial, groups, n, t, w2, score);
+}
+
+// grid: sum over requests of ceil(n / 256) blocks.  One decay table serves
+// every request: entry Delta does not depend on n.
+__global__ __launch_bounds__(kThreads) void kvnorm_finish_batch(const ScoreBatchArgs a, const double* __restrict__ w2) {
+  const ScoreDesc& q = a.r[score_request_of(a, blockIdx.x, true)];
+  const int t = static_cast<int>(blockIdx.x - q.fin_block_begin) * kThreads + threadIdx.x;
+  if (t < q.n) kvnorm_finish_token(q.partial, a.groups, q.n, t, w2, q.score);
+}
+
+__global__ __launch_bounds__(kThreads) void recency_score_batch(const ScoreBatchArgs a, const double* __restrict__ w1) {
+  const ScoreDesc& q = a.r[score_request_of(a, blockIdx.x, true)];
+  const int t = static_cast<int>(blockIdx.x - q.fin_block_begin) * kThreads + threadIdx.x;
+  if (t < q.n) q.score[t] = w1[q.n - 1 - t];
 }
 
 // grid: (token blocks, groups).  Group g's sum is the sum of its
@@ -312,6 +356,52 @@ hipError_t launch_score_kvnorm(const Geometry& g, const uint16_t* k, const uint1
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   kvnorm_finish<<<(g.n + kThreads - 1) / kThreads, kThreads, 0, stream>>>(partial, s.groups, g.n, w2, score);
+  return hipGetLastError();
+}
+
+void kvnorm_batch_shape(int32_t L, int32_t H, int32_t d, const int32_t* ns, int32_t count, ScoreBatchArgs* a) {
+  uint64_t blocks = 0;
+  const int tok = kThreads / (d / 8);
+  for (int i = 0; i < count; ++i) blocks += (ns[i] + tok - 1) / tok;
+  Geometry g{};
+  g.L = L;
+  g.H = H;
+  g.d = d;
+  // the single-request shape for a request as long as the whole batch: the
+  // same number of workgroups per part, so the launch streams alike
+  g.n = static_cast<int32_t>(std::min<uint64_t>(blocks * tok, kMaxTokens));
+  const KvnormLaunch s = kvnorm_shape(g);
+  a->pairs = s.pairs;
+  a->pairs_per_group = s.pairs_per_group;
+  a->groups = s.groups;
+  a->parts_per_block = s.parts_per_block;
+}
+
+hipError_t launch_score_kvnorm_batch(const ScoreBatchArgs& a, int32_t d, const double* w2, hipStream_t stream) {
+  const int tok = kThreads / (d / 8);
+  uint32_t blocks = 0, fin = 0;
+  for (int i = 0; i < a.count; ++i) {
+    blocks += (a.r[i].n + tok - 1) / tok;
+    fin += (a.r[i].n + kThreads - 1) / kThreads;
+  }
+  const dim3 grid(blocks, (a.groups + a.parts_per_block - 1) / a.parts_per_block);
+  switch (d) {
+    case 32: kvnorm_partial_batch<32><<<grid, kThreads, 0, stream>>>(a); break;
+    case 64: kvnorm_partial_batch<64><<<grid, kThreads, 0, stream>>>(a); break;
+    case 128: kvnorm_partial_batch<128><<<grid, kThreads, 0, stream>>>(a); break;
+    case 256: kvnorm_partial_batch<256><<<grid, kThreads, 0, stream>>>(a); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  kvnorm_finish_batch<<<fin, kThreads, 0, stream>>>(a, w2);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_recency_batch(const ScoreBatchArgs& a, const double* w1, hipStream_t stream) {
+  uint32_t fin = 0;
+  for (int i = 0; i < a.count; ++i) fin += (a.r[i].n + kThreads - 1) / kThreads;
+  recency_score_batch<<<fin, kThreads, 0, stream>>>(a, w1);
   return hipGetLastError();
 }
 

@@ -314,7 +314,24 @@ __global__ __launch_bounds__(kSelThreads) void assign_tiers_groups(const double*
              static_cast<int>(e[3]));
 }
 
+// grid: one workgroup per request of the launch
+template <bool RESIDENT>
+__global__ __launch_bounds__(kSelThreads) void assign_tiers_batch(const ScoreBatchArgs a) {
+  const ScoreDesc& q = a.r[blockIdx.x];
+  assign_row<RESIDENT>(q.score, q.tier, q.n, q.n_sink, q.n16, q.n8, q.n4);
+}
+
 }  // namespace
+
+bool assign_fits_resident(int32_t n, int32_t n_sink) { return fits_resident(n, n_sink); }
+
+hipError_t launch_assign_batch(const ScoreBatchArgs& a, bool resident, hipStream_t stream) {
+  if (resident)
+    assign_tiers_batch<true><<<a.count, kSelThreads, 0, stream>>>(a);
+  else
+    assign_tiers_batch<false><<<a.count, kSelThreads, 0, stream>>>(a);
+  return hipGetLastError();
+}
 
 hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier,
                          hipStream_t stream) {

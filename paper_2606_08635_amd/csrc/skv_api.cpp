@@ -458,6 +458,47 @@ skv_status score_launch(const skv_config* cfg, const void* k, const void* v, con
   }
 }
 
+// Host checks of a batched score / assign: cfg, the mode, every request's
+// length and pointers; fills each request's plan (cfg at its own n).
+skv_status check_score_requests(const skv_config* cfg, const skv_score_request* reqs, int32_t count,
+                                bool for_assign, std::vector<skv_plan>* plans) {
+  skv_status st = check_config(cfg);
+  if (st != SKV_OK) return st;
+  if (cfg->score_mode == SKV_SCORE_ATTN) return SKV_ERR_INVALID_ARG;
+  if (count < 0 || (count > 0 && reqs == nullptr)) return SKV_ERR_INVALID_ARG;
+  plans->resize(static_cast<size_t>(count));
+  for (int32_t i = 0; i < count; ++i) {
+    const skv_score_request& q = reqs[i];
+    if (q.reserved != 0 || q.num_tokens < 1 || q.num_tokens > cfg->num_tokens) return SKV_ERR_INVALID_ARG;
+    if (!dev_ptr_ok(q.score)) return SKV_ERR_INVALID_ARG;
+    if (for_assign && q.tier == nullptr) return SKV_ERR_INVALID_ARG;
+    if (!for_assign && cfg->score_mode == SKV_SCORE_KVNORM && (!dev_ptr_ok(q.k) || !dev_ptr_ok(q.v)))
+      return SKV_ERR_INVALID_ARG;
+    skv_config c = *cfg;
+    c.num_tokens = q.num_tokens;
+    if (for_assign && (st = plan_counts(&c, &(*plans)[i])) != SKV_OK) return st;
+  }
+  return SKV_OK;
+}
+
+// Partial-sum layout of a batched KV-norm score: the shape shared by the
+// batch and each request's byte offset after the decay table.
+uint64_t score_batch_layout(const skv_config* cfg, const skv_score_request* reqs, int32_t count, ScoreBatchArgs* shape,
+                            std::vector<uint64_t>* offsets) {
+  std::vector<int32_t> ns(static_cast<size_t>(count));
+  for (int32_t i = 0; i < count; ++i) ns[i] = reqs[i].num_tokens;
+  std::memset(shape, 0, sizeof(*shape));
+  if (count > 0) kvnorm_batch_shape(cfg->num_layers, cfg->num_kv_heads, cfg->head_dim, ns.data(), count, shape);
+  uint64_t off = decay_table_bytes(cfg);
+  offsets->resize(static_cast<size_t>(count));
+  for (int32_t i = 0; i < count; ++i) {
+    (*offsets)[i] = off;
+    if (cfg->score_mode == SKV_SCORE_KVNORM)
+      off += round_up_256(static_cast<uint64_t>(shape->groups) * static_cast<uint64_t>(ns[i]) * 16u);
+  }
+  return off;
+}
+
 }  // namespace
 }  // namespace skv
 
@@ -602,6 +643,88 @@ skv_status skv_score_static(const skv_config* cfg, const void* k, const void* v,
   uint8_t* base = nullptr;
   if (st = static_scratch_prepare(cfg, stream, &base); st != SKV_OK) return st;
   return score_launch(cfg, k, v, q_obs, score, reinterpret_cast<const double*>(base), base + table_bytes, stream);
+}
+
+skv_status skv_batch_workspace_size(const skv_config* cfg, const skv_score_request* reqs, int32_t count,
+                                    uint64_t* bytes) {
+  if (bytes == nullptr) return SKV_ERR_INVALID_ARG;
+  std::vector<skv_plan> plans;
+  const skv_status st = check_score_requests(cfg, reqs, count, false, &plans);
+  if (st != SKV_OK) return st;
+  ScoreBatchArgs shape;
+  std::vector<uint64_t> offsets;
+  *bytes = score_batch_layout(cfg, reqs, count, &shape, &offsets);
+  return SKV_OK;
+}
+
+skv_status skv_score_batch(const skv_config* cfg, const skv_score_request* reqs, int32_t count, void* ws,
+                           hipStream_t stream) {
+  std::vector<skv_plan> plans;
+  const skv_status st = check_score_requests(cfg, reqs, count, false, &plans);
+  if (st != SKV_OK) return st;
+  if (!dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
+  ScoreBatchArgs a;
+  std::vector<uint64_t> offsets;
+  score_batch_layout(cfg, reqs, count, &a, &offsets);
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  const double* table = static_cast<const double*>(ws);
+  const int tok = 256 / (cfg->head_dim / 8);  // tokens per partial-sum workgroup
+  for (int32_t first = 0; first < count; first += kMaxScoreBatch) {
+    a.count = std::min(kMaxScoreBatch, count - first);
+    uint32_t tb = 0, fb = 0;
+    for (int32_t i = 0; i < a.count; ++i) {
+      const skv_score_request& q = reqs[first + i];
+      ScoreDesc& d = a.r[i];
+      std::memset(&d, 0, sizeof(d));
+      d.k = static_cast<const uint16_t*>(q.k);
+      d.v = static_cast<const uint16_t*>(q.v);
+      d.score = q.score;
+      d.partial = reinterpret_cast<uint64_t*>(base + offsets[first + i]);
+      d.n = q.num_tokens;
+      d.tok_block_begin = tb;
+      d.fin_block_begin = fb;
+      tb += static_cast<uint32_t>((q.num_tokens + tok - 1) / tok);
+      fb += static_cast<uint32_t>((q.num_tokens + 255) / 256);
+    }
+    const hipError_t e = cfg->score_mode == SKV_SCORE_KVNORM
+                             ? launch_score_kvnorm_batch(a, cfg->head_dim, table, stream)
+                             : launch_score_recency_batch(a, table, stream);
+    if (e != hipSuccess) return SKV_ERR_DEVICE;
+  }
+  return SKV_OK;
+}
+
+skv_status skv_assign_batch(const skv_config* cfg, const skv_score_request* reqs, int32_t count,
+                            hipStream_t stream) {
+  std::vector<skv_plan> plans;
+  const skv_status st = check_score_requests(cfg, reqs, count, true, &plans);
+  if (st != SKV_OK) return st;
+  // requests whose non-sink keys fit the resident form go to resident
+  // launches, the rest to launches of the general form
+  for (const bool resident : {true, false}) {
+    ScoreBatchArgs a;
+    std::memset(&a, 0, sizeof(a));
+    for (int32_t i = 0; i <= count; ++i) {
+      const bool flush = i == count || a.count == kMaxScoreBatch;
+      if (flush && a.count > 0) {
+        if (launch_assign_batch(a, resident, stream) != hipSuccess) return SKV_ERR_DEVICE;
+        a.count = 0;
+      }
+      if (i == count) break;
+      const skv_plan& p = plans[i];
+      if (assign_fits_resident(reqs[i].num_tokens, p.n_sink) != resident) continue;
+      ScoreDesc& d = a.r[a.count++];
+      std::memset(&d, 0, sizeof(d));
+      d.score = reqs[i].score;
+      d.tier = reqs[i].tier;
+      d.n = reqs[i].num_tokens;
+      d.n_sink = p.n_sink;
+      d.n16 = p.n_fp16;
+      d.n8 = p.n_int8;
+      d.n4 = p.n_int4;
+    }
+  }
+  return SKV_OK;
 }
 
 skv_status skv_assign_tiers(const skv_config* cfg, const double* score, uint8_t* tier, void* ws,

@@ -66,6 +66,28 @@ struct BatchArgs {
 };
 static_assert(sizeof(BatchArgs) <= 4000, "kernel arguments");
 
+// One request of a batched score / assign launch.  tok_block_begin: its
+// first workgroup in the partial-sum launch (token blocks of 256 / (d / 8)
+// tokens); fin_block_begin: its first 256-token block in the finish, recency
+// and (one workgroup per request) assign launches count requests instead.
+struct ScoreDesc {
+  const uint16_t* k;
+  const uint16_t* v;
+  double* score;
+  uint8_t* tier;
+  uint64_t* partial;  // KV-norm partial sums: groups x n x 16 bytes
+  uint32_t tok_block_begin, fin_block_begin;
+  int32_t n, n_sink, n16, n8, n4, pad;
+};
+
+constexpr int kMaxScoreBatch = 48;  // requests per launch (descriptors travel as kernel arguments)
+
+struct ScoreBatchArgs {
+  int32_t count, pairs, pairs_per_group, groups, parts_per_block, pad;
+  ScoreDesc r[kMaxScoreBatch];
+};
+static_assert(sizeof(ScoreBatchArgs) <= 4000, "kernel arguments");
+
 // Kernel launchers.  Each returns the launch status; none synchronizes.
 hipError_t launch_score_kvnorm(const Geometry& g, const uint16_t* k, const uint16_t* v,
                                const double* w2, uint64_t* partial, double* score,
@@ -81,6 +103,20 @@ uint64_t attn_scratch_bytes(const Geometry& g, int32_t Hq, int32_t W);
 
 hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier,
                          hipStream_t stream);
+
+// Batched scoring and assignment (every request shares L, H, d and the
+// policy; each has its own n).  kvnorm_batch_shape fills pairs,
+// pairs_per_group, groups and parts_per_block of `a` for requests of lengths
+// ns[0..count) (one shape for the whole batch, so that every launch chunk of
+// it uses the same partial layout).  The launches cover a.count <=
+// kMaxScoreBatch requests whose descriptors are complete.
+void kvnorm_batch_shape(int32_t L, int32_t H, int32_t d, const int32_t* ns, int32_t count, ScoreBatchArgs* a);
+hipError_t launch_score_kvnorm_batch(const ScoreBatchArgs& a, int32_t d, const double* w2, hipStream_t stream);
+hipError_t launch_score_recency_batch(const ScoreBatchArgs& a, const double* w1, hipStream_t stream);
+// One workgroup per request; RESIDENT chooses the resident form, which every
+// request of the launch must fit (n - n_sink <= 32768).
+hipError_t launch_assign_batch(const ScoreBatchArgs& a, bool resident, hipStream_t stream);
+bool assign_fits_resident(int32_t n, int32_t n_sink);
 
 // Batched launches over a.count requests and layers [layer_begin, layer_begin +
 // layer_count); `rows` is the total number of row workgroups (sum of

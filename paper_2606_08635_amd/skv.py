@@ -29,7 +29,8 @@ EXPORTED = ("skv_abi_version", "skv_status_string", "skv_plan_tiers", "skv_paylo
             "skv_unpack", "skv_pack_batch", "skv_unpack_batch", "skv_link", "skv_upgrade_size",
             "skv_pack_upgrade", "skv_unpack_upgrade", "skv_group_count", "skv_plan_groups",
             "skv_grouped_payload_size", "skv_group_workspace_size", "skv_prepare_groups", "skv_score_groups",
-            "skv_assign_groups", "skv_pack_groups", "skv_unpack_groups")
+            "skv_assign_groups", "skv_pack_groups", "skv_unpack_groups", "skv_batch_workspace_size",
+            "skv_score_batch", "skv_assign_batch")
 
 
 class SkvError(RuntimeError):
@@ -53,6 +54,11 @@ class Request(ctypes.Structure):
                 ("v", ctypes.c_void_p), ("tier", ctypes.c_void_p), ("payload", ctypes.c_void_p),
                 ("payload_bytes", ctypes.c_uint64), ("block_table", ctypes.c_void_p),
                 ("dev_status", ctypes.c_void_p)]
+
+
+class ScoreRequest(ctypes.Structure):
+    _fields_ = [("num_tokens", ctypes.c_int32), ("reserved", ctypes.c_int32), ("k", ctypes.c_void_p),
+                ("v", ctypes.c_void_p), ("score", ctypes.c_void_p), ("tier", ctypes.c_void_p)]
 
 
 class GroupSpec(ctypes.Structure):
@@ -107,6 +113,9 @@ def lib():
             "skv_unpack_groups": (ctypes.c_int, [cfgp, P(GroupSpec), vp, vp, u64, vp, vp, vp, i32, i32, vp, vp]),
             "skv_pack_upgrade": (ctypes.c_int, [cfgp, vp, vp, vp, vp, i32, i32, vp, u64, vp, vp]),
             "skv_unpack_upgrade": (ctypes.c_int, [cfgp, vp, u64, i32, i32, vp, vp, vp, i32, i32, vp, vp]),
+            "skv_batch_workspace_size": (ctypes.c_int, [cfgp, P(ScoreRequest), i32, P(u64)]),
+            "skv_score_batch": (ctypes.c_int, [cfgp, P(ScoreRequest), i32, vp, vp]),
+            "skv_assign_batch": (ctypes.c_int, [cfgp, P(ScoreRequest), i32, vp]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -406,6 +415,51 @@ def pack_batch(cfg: Config, ks, vs, tiers, payloads, statuses=None, layer_begin=
     lc = cfg.num_layers - layer_begin if layer_count is None else layer_count
     _check(lib().skv_pack_batch(ctypes.byref(cfg), reqs, count, layer_begin, lc, _stream(stream)),
            "skv_pack_batch")
+
+
+def _score_requests(cfg: Config, scores, ks=None, vs=None, tiers=None):
+    count = len(scores)
+    reqs = (ScoreRequest * count)()
+    for i in range(count):
+        n = scores[i].numel()
+        reqs[i].num_tokens = n
+        reqs[i].score = _dev(scores[i], torch.float64, n, "score").value
+        if ks is not None and cfg.score_mode == KVNORM:
+            kv_n = _kv_numel(_with_tokens(cfg, n))
+            reqs[i].k = _dev(ks[i], torch.float16, kv_n, "k").value
+            reqs[i].v = _dev(vs[i], torch.float16, kv_n, "v").value
+        if tiers is not None:
+            reqs[i].tier = _dev(tiers[i], torch.uint8, n, "tier").value
+    return reqs, count
+
+
+def batch_workspace_size(cfg: Config, scores) -> int:
+    """Workspace bytes of score_batch for requests of these lengths (cfg.num_tokens >= every n)."""
+    count = len(scores)
+    reqs = (ScoreRequest * count)()
+    for i in range(count):
+        reqs[i].num_tokens = scores[i].numel()
+        reqs[i].score = 256  # sizes only: the pointers are not dereferenced
+        reqs[i].k = reqs[i].v = 256
+    out = ctypes.c_uint64()
+    _check(lib().skv_batch_workspace_size(ctypes.byref(cfg), reqs, count, ctypes.byref(out)),
+           "skv_batch_workspace_size")
+    return out.value
+
+
+def score_batch(cfg: Config, ks, vs, scores, ws: torch.Tensor, stream=None):
+    """Scores len(scores) requests (n = each score buffer's length) in batched
+    launches; ws prepared by prepare(cfg, ws) with cfg.num_tokens >= every n."""
+    reqs, count = _score_requests(cfg, scores, ks, vs)
+    _check(lib().skv_score_batch(ctypes.byref(cfg), reqs, count,
+                                 _dev(ws, torch.uint8, batch_workspace_size(cfg, scores), "ws"), _stream(stream)),
+           "skv_score_batch")
+
+
+def assign_batch(cfg: Config, scores, tiers, stream=None):
+    """Assigns the tiers of len(scores) requests, one workgroup per request."""
+    reqs, count = _score_requests(cfg, scores, tiers=tiers)
+    _check(lib().skv_assign_batch(ctypes.byref(cfg), reqs, count, _stream(stream)), "skv_assign_batch")
 
 
 def unpack_batch(cfg: Config, payloads, token_counts, block_tables, k_cache: torch.Tensor,

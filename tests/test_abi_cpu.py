@@ -249,3 +249,41 @@ def test_grouped_argument_errors(lib):
     assert L.skv_assign_groups(by, g.ref, fake, fake, None, None) == skv.ERR_INVALID_ARG
     assert L.skv_prepare_groups(by, g.ref, None, None) == skv.ERR_INVALID_ARG
     assert L.skv_score_groups(by, None, fake, fake, None, fake, fake, None) == skv.ERR_INVALID_ARG
+
+
+def _score_reqs(lengths, ptr=256):
+    reqs = (skv.ScoreRequest * len(lengths))()
+    for i, n in enumerate(lengths):
+        reqs[i].num_tokens = n
+        reqs[i].k = reqs[i].v = reqs[i].score = reqs[i].tier = ptr
+    return reqs
+
+
+def test_batched_score_host_checks(lib):
+    """Argument errors of the batched score / assign are caught on the host
+    (placeholder aligned addresses are never dereferenced)."""
+    import ctypes
+    cfg = skv.config(2, 2, 64, 1000, 0.5)
+    out = ctypes.c_uint64()
+    reqs = _score_reqs([1000, 10, 999])
+    assert lib.skv_batch_workspace_size(ctypes.byref(cfg), reqs, 3, ctypes.byref(out)) == skv.OK
+    table = 8 * 1000
+    assert out.value >= -(-table // 256) * 256 + 16 * (1000 + 10 + 999)
+    one = ctypes.c_uint64()
+    assert lib.skv_batch_workspace_size(ctypes.byref(cfg), _score_reqs([10]), 1, ctypes.byref(one)) == skv.OK
+    assert one.value < out.value
+    assert lib.skv_batch_workspace_size(ctypes.byref(cfg), reqs, 0, ctypes.byref(one)) == skv.OK
+    # a request longer than the configured table
+    assert lib.skv_batch_workspace_size(ctypes.byref(cfg), _score_reqs([1001]), 1, ctypes.byref(out)) \
+        == skv.ERR_INVALID_ARG
+    bad = _score_reqs([10])
+    bad[0].reserved = 1
+    assert lib.skv_score_batch(ctypes.byref(cfg), bad, 1, ctypes.c_void_p(256), None) == skv.ERR_INVALID_ARG
+    # attention mode has no batched form
+    acfg = skv.config(2, 2, 64, 1000, 0.5, score_mode=skv.ATTN, num_q_heads=4, obs_window=8)
+    assert lib.skv_score_batch(ctypes.byref(acfg), _score_reqs([10]), 1, ctypes.c_void_p(256), None) \
+        == skv.ERR_INVALID_ARG
+    # misaligned score pointer
+    assert lib.skv_assign_batch(ctypes.byref(cfg), _score_reqs([10], ptr=258), 1, None) == skv.ERR_INVALID_ARG
+    # a request whose sinks exceed its own budget: one token, one sink, b = 0.5
+    assert lib.skv_assign_batch(ctypes.byref(cfg), _score_reqs([10, 1]), 2, None) == skv.ERR_BUDGET

@@ -127,3 +127,64 @@ def test_bad_payload_only_disables_its_request():
     okc, ovc, ost = _oracle_unpack([reqs[0], reqs[2]], [reqs[0]["payload"], reqs[2]["payload"]],
                                    [tables[0], tables[2]], pool, bs)
     assert np.array_equal(u16(kc), okc) and np.array_equal(u16(vc), ovc)  # request 1's blocks untouched
+
+
+SCORE_CASES = [
+    # L, H, d, lengths, budget, tiers, mode
+    (2, 2, 64, [3, 5, 255, 256, 257, 1000, 4099, 4], 0.4, 3, oracle.KVNORM),
+    # 50 requests: two launches of the 48-request descriptor table
+    (1, 2, 32, [30 + 11 * i for i in range(50)], 0.3, 2, oracle.KVNORM),
+    # more than 32768 non-sink tokens (the general form of the select) next to
+    # short ones (the resident form) in one call
+    (1, 1, 32, [33000, 100, 40000], 0.5, 3, oracle.KVNORM),
+    (1, 2, 256, [2048, 777], 0.7, 3, oracle.KVNORM),
+    (2, 1, 128, [7, 3000, 512], 0.5, 3, oracle.RECENCY),
+]
+
+
+@pytest.mark.parametrize("case", SCORE_CASES, ids=[f"L{c[0]}H{c[1]}d{c[2]}x{len(c[3])}m{c[6]}" for c in SCORE_CASES])
+def test_batched_score_and_assign_match_oracle(case):
+    """skv_score_batch and skv_assign_batch give every request exactly the
+    oracle's scores and tier map for that request alone."""
+    Lb, Hb, db, lengths, b, tiers, mode = case
+    say(f"batched score/assign {case[:3]} {len(lengths)} requests mode {mode}")
+    cfg, _ = configs(Lb, Hb, db, max(lengths), b, tiers, mode=mode)
+    ks, vs, want_key, want_tier = [], [], [], []
+    for i, n in enumerate(lengths):
+        _, ocfg = configs(Lb, Hb, db, n, b, tiers, mode=mode)
+        k, v = workloads.make_kv(Lb, Hb, n, db, seed=100 + 16 * i)
+        key = oracle.score(ocfg, u16(k), u16(v))
+        want_key.append(key)
+        want_tier.append(oracle.assign(ocfg, key))
+        ks.append(k.cuda())
+        vs.append(v.cuda())
+    scores = [torch.full((n,), float("nan"), dtype=torch.float64, device="cuda") for n in lengths]
+    tier_out = [torch.full((n,), 0xEE, dtype=torch.uint8, device="cuda") for n in lengths]
+    ws = torch.empty(max(skv.batch_workspace_size(cfg, scores), skv.workspace_size(cfg)), dtype=torch.uint8,
+                     device="cuda")
+    skv.prepare(cfg, ws)
+    skv.score_batch(cfg, ks, vs, scores, ws)
+    skv.assign_batch(cfg, scores, tier_out)
+    torch.cuda.synchronize()
+    for i, n in enumerate(lengths):
+        assert np.array_equal(bits64(scores[i].cpu().numpy()), bits64(want_key[i])), f"scores of request {i} (n={n})"
+        assert np.array_equal(tier_out[i].cpu().numpy(), want_tier[i]), f"tier map of request {i} (n={n})"
+
+
+def test_batched_assign_of_foreign_scores():
+    """The batched assignment takes any scores, like skv_assign_tiers: ties,
+    zeros, negatives and NaN rank as the oracle ranks them."""
+    lengths = [600, 3, 2500]
+    cfg, _ = configs(1, 1, 32, max(lengths), 0.45, 3)
+    rng = np.random.default_rng(7)
+    scores, want = [], []
+    for n in lengths:
+        _, ocfg = configs(1, 1, 32, n, 0.45, 3)
+        s = rng.choice(np.array([0.0, -1.0, np.nan, 1.0, 2.0, 2.0, 3.5]), size=n)
+        scores.append(torch.from_numpy(s).cuda())
+        want.append(oracle.assign(ocfg, s))
+    tiers = [torch.empty(n, dtype=torch.uint8, device="cuda") for n in lengths]
+    skv.assign_batch(cfg, scores, tiers)
+    torch.cuda.synchronize()
+    for t, w in zip(tiers, want):
+        assert np.array_equal(t.cpu().numpy(), w)
