@@ -23,6 +23,10 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxPairsPerGroup = 512;  // 2 tensors * 8 elements * 512 = 2^13 terms per thread
+#ifndef SKV_KVNORM_PAIR_ROWS
+#define SKV_KVNORM_PAIR_ROWS 4
+#endif
+constexpr int kPairRows = SKV_KVNORM_PAIR_ROWS;  // row slices in flight per thread, one-pair parts
 
 struct U128 {
   uint64_t lo, hi;
@@ -175,6 +179,105 @@ __global__ __launch_bounds__(kThreads) void kvnorm_partial(const uint16_t* __res
   kvnorm_partial_block<D>(k, v, n, pairs, pairs_per_group, parts_per_block, partial, blockIdx.x, blockIdx.y);
 }
 
+// Every lane of each aligned group of G lanes (G = 4 .. 32) receives the sum
+// of the group's binary64 values: butterfly steps by DPP lane moves inside
+// 16-lane rows (each 64-bit value moved as two 32-bit halves), then one
+// shuffle across the two rows of a 32-lane group.  The caller's values are
+// integers in a common unit below 2^53 with their sum, so every order of
+// addition gives the same exact result.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const uint64_t b = __builtin_bit_cast(uint64_t, x);
+  const uint32_t lo = dpp_mov<CTRL>(static_cast<uint32_t>(b));
+  const uint32_t hi = dpp_mov<CTRL>(static_cast<uint32_t>(b >> 32));
+  return __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+template <int G>
+__device__ __forceinline__ double group_sum_f64(double x) {
+  static_assert(G == 4 || G == 8 || G == 16 || G == 32, "group size");
+  x += dpp_f64<0xB1>(x);                          // quad_perm [1,0,3,2]
+  x += dpp_f64<0x4E>(x);                          // quad_perm [2,3,0,1]
+  if constexpr (G >= 8) x += dpp_f64<0x141>(x);   // row_half_mirror
+  if constexpr (G >= 16) x += dpp_f64<0x140>(x);  // row_mirror
+  if constexpr (G == 32) x += __shfl_xor(x, 16);
+  return x;
+}
+
+// Partial sums with one (layer, head) pair per part (per-head maps): block
+// (x, y) covers pair y and the T * TOK consecutive tokens from x * T * TOK,
+// i.e. one contiguous run of each of the pair's K and V planes (T even).  A
+// thread takes its T row slices two at a time, all four loads issued before
+// any is added, and the lanes of a row combine their sums in binary64 by
+// butterfly lane moves instead of through LDS.  That stays exact: a lane's
+// sums hold 16 terms (8 K and 8 V elements), so over the LPR <= 32 lanes of
+// a row the integer parts stay below 512 * 2^40 = 2^49 and the fractions,
+// multiples of 2^-40, below 2^9; both are exact binary64 integers in their
+// units, whatever the order.  A non-finite sum is redone from the registers
+// without the non-finite elements.  The 128-bit sum is kvnorm_partial's.
+// FINAL (each pair is a whole group): the block writes the group's score,
+// RN64(S) * w2[n-1-t], into score[p * n + t], the value kvnorm_finish_groups
+// would compute from the partial.
+template <int D, int T, bool FINAL>
+__global__ __launch_bounds__(kThreads) void kvnorm_partial_pairs(const uint16_t* __restrict__ k,
+                                                                const uint16_t* __restrict__ v, int n,
+                                                                uint64_t* __restrict__ partial,
+                                                                const double* __restrict__ w2,
+                                                                double* __restrict__ score) {
+  constexpr int LPR = D / 8;
+  constexpr int TOK = kThreads / LPR;
+  const int lane = threadIdx.x % LPR;
+  const int t0 = blockIdx.x * (T * TOK) + threadIdx.x / LPR;
+  const int p = blockIdx.y;
+  const size_t plane = static_cast<size_t>(p) * n * D;
+#pragma unroll 1
+  for (int i0 = 0; i0 < T; i0 += 2) {  // two row slices (four 16-byte loads) in flight
+    u32x4 kx[2], vx[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int t = t0 + (i0 + u) * TOK;
+      kx[u] = u32x4{0u, 0u, 0u, 0u};
+      vx[u] = u32x4{0u, 0u, 0u, 0u};
+      if (t < n) {
+        const size_t off = plane + static_cast<size_t>(t) * D + lane * 8;
+        kx[u] = ld_nt16(k + off);
+        vx[u] = ld_nt16(v + off);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int t = t0 + (i0 + u) * TOK;
+      double ah = 0.0, al = 0.0;
+      acc16(kx[u], ah, al);
+      acc16(vx[u], ah, al);
+      if (!(__builtin_isfinite(ah) && __builtin_isfinite(al))) {
+        ah = 0.0;
+        al = 0.0;
+        const uint32_t w[8] = {kx[u].x, kx[u].y, kx[u].z, kx[u].w, vx[u].x, vx[u].y, vx[u].z, vx[u].w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc_word_finite(w[e], ah, al);
+      }
+      ah = group_sum_f64<LPR>(ah);  // every lane of the row is active
+      al = group_sum_f64<LPR>(al);
+      if (lane == 0 && t < n) {
+        const size_t idx = static_cast<size_t>(p) * n + t;
+        if constexpr (FINAL) {
+          // S = (ah + al) * 2^-8 exactly, and one binary64 addition of the two
+          // exact terms is the correctly rounded sum: RN64(S) without the
+          // 128-bit detour (the scaling by 2^-8 is exact: S is 0 or >= 2^-48)
+          score[idx] = ((ah + al) * 0x1p-8) * w2[n - 1 - t];
+        } else {
+          const uint64_t a = static_cast<uint64_t>(ah);
+          const uint64_t b = static_cast<uint64_t>(al * 1099511627776.0);  // * 2^40, exact
+          const uint64_t lo = (a << 40) + b;
+          partial[idx * 2] = lo;
+          partial[idx * 2 + 1] = (a >> 24) + (lo < b ? 1u : 0u);
+        }
+      }
+    }
+  }
+}
+
 // Request of a batched launch that owns flat block `b` (the last whose first
 // block is at most b; requests are in block order).
 __device__ __forceinline__ int score_request_of(const ScoreBatchArgs& a, uint32_t b, bool finish) {
@@ -304,6 +407,7 @@ KvnormLaunch kvnorm_shape_groups(const Geometry& g, int gran, int* parts_per_gro
 uint64_t kvnorm_scratch_bytes_groups(const Geometry& g, int32_t gran) {
   int ppg;
   const KvnormLaunch s = kvnorm_shape_groups(g, gran, &ppg);
+  if (s.pairs_per_group == 1 && ppg == 1) return 0;  // one pair per group: scores written directly
   return static_cast<uint64_t>(s.groups) * g.n * 16u;
 }
 
@@ -314,7 +418,28 @@ hipError_t launch_score_kvnorm_groups(const Geometry& g, int32_t gran, int32_t G
   const KvnormLaunch s = kvnorm_shape_groups(g, gran, &ppg);
   const dim3 grid(s.blocks_tok, (s.groups + s.parts_per_block - 1) / s.parts_per_block);
   const int ppb = s.parts_per_block;
-  switch (g.d) {
+  if (s.pairs_per_group == 1) {
+    // one pair per part: each block streams a contiguous token run of one
+    // pair; a part that is a whole group (per-head maps) writes its scores
+    const bool final_scores = ppg == 1;
+#define SKV_PAIRS_LAUNCH(D)                                                                                      \
+  {                                                                                                             \
+    const dim3 pgrid((g.n + kPairRows * (kThreads / (D / 8)) - 1) / (kPairRows * (kThreads / (D / 8))), s.pairs); \
+    if (final_scores)                                                                                           \
+      kvnorm_partial_pairs<D, kPairRows, true><<<pgrid, kThreads, 0, stream>>>(k, v, g.n, partial, w2, score);  \
+    else                                                                                                        \
+      kvnorm_partial_pairs<D, kPairRows, false><<<pgrid, kThreads, 0, stream>>>(k, v, g.n, partial, w2, score); \
+  }
+    switch (g.d) {
+      case 32: SKV_PAIRS_LAUNCH(32); break;
+      case 64: SKV_PAIRS_LAUNCH(64); break;
+      case 128: SKV_PAIRS_LAUNCH(128); break;
+      case 256: SKV_PAIRS_LAUNCH(256); break;
+      default: return hipErrorInvalidValue;
+    }
+#undef SKV_PAIRS_LAUNCH
+    if (final_scores) return hipGetLastError();
+  } else switch (g.d) {
     case 32: kvnorm_partial<32><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
     case 64: kvnorm_partial<64><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
     case 128: kvnorm_partial<128><<<grid, kThreads, 0, stream>>>(k, v, g.n, s.pairs, s.pairs_per_group, ppb, partial); break;
