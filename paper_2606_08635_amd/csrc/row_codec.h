@@ -32,6 +32,17 @@ __device__ __forceinline__ float recip_scale_of(float a, float Qf) {
   const float e = __builtin_fmaf(-q0, a, Qf);
   return __builtin_fmaf(e, r0, q0);
 }
+// RN32(Qf / a) for any positive normal binary32 a and Qf in {15, 255}: the
+// sequence above after one refinement of the reciprocal (checked exhaustively
+// over every binary32 significand and any hardware reciprocal within 2 ulp;
+// without the refinement a few binary32 a round wrongly).
+__device__ __forceinline__ float recip_scale_of_f32(float a, float Qf) {
+  const float r0 = __builtin_amdgcn_rcpf(a);
+  const float y = __builtin_fmaf(__builtin_fmaf(-a, r0, 1.0f), r0, r0);
+  const float q0 = Qf * y;
+  const float e = __builtin_fmaf(-q0, a, Qf);
+  return __builtin_fmaf(e, y, q0);
+}
 
 // amax: the row's largest magnitude pattern (bits & 0x7FFF, reduced over the
 // row's lanes).  code = clamp(rne(RN32(x * RN32(Q / a))), -Q, Q); for a finite

@@ -112,7 +112,9 @@ __device__ __forceinline__ GroupParams group_params(uint32_t amax, uint32_t kmin
         g.s16 = __builtin_bit_cast(uint16_t, static_cast<_Float16>(g.scale));
         g.scale = half_lo(g.s16);
         g.zero = g.s16 == 0u;
-        g.r = g.zero ? 0.0f : 1.0f / g.scale;  // correctly rounded division
+        // RN32(1/s) by reciprocal + one correction: correctly rounded for
+        // every positive binary16 s (checked exhaustively in exact arithmetic)
+        g.r = g.zero ? 0.0f : recip_scale_of(g.scale, 1.0f);
       } else {
         g.r = recip_scale_of(a, static_cast<float>(Q));
       }
@@ -123,14 +125,17 @@ __device__ __forceinline__ GroupParams group_params(uint32_t amax, uint32_t kmin
     if (range == 0.0f) {
       g.zero = true;
     } else {
-      g.scale = range / static_cast<float>(M);
+      // RN32(range / M) and RN32(M / range) without a division: correctly
+      // rounded for every binary32 range (checked exhaustively)
+      const float Mf = static_cast<float>(M);
+      g.scale = scale_of(range, Mf, M == 255 ? 1.0f / 255.0f : 1.0f / 15.0f);
       if (f16) {
         g.s16 = __builtin_bit_cast(uint16_t, static_cast<_Float16>(g.scale));
         g.scale = half_lo(g.s16);
         g.zero = g.s16 == 0u;
-        g.r = g.zero ? 0.0f : 1.0f / g.scale;
+        g.r = g.zero ? 0.0f : recip_scale_of(g.scale, 1.0f);  // as above
       } else {
-        g.r = static_cast<float>(M) / range;
+        g.r = recip_scale_of_f32(range, Mf);
       }
     }
   }
@@ -138,12 +143,17 @@ __device__ __forceinline__ GroupParams group_params(uint32_t amax, uint32_t kmin
 }
 
 // Code of x in a group (as the float-magic integer base + code, clamped).
-__device__ __forceinline__ uint32_t group_code(float x, float r, float lo, bool zero, bool asym, int tr) {
+// clamp = false only where the clamp provably never binds: symmetric groups
+// with fp32 metadata, whose r = RN32(Q/a) keeps |RN32(x r)| < Q + 1/2 for
+// every |x| <= a (the row quantizer's exhaustive check, any binary16 a).
+__device__ __forceinline__ uint32_t group_code(float x, float r, float lo, bool zero, bool asym, int tr,
+                                               bool clamp = true) {
   const int Q = tr == kINT8 ? 127 : 7, M = tr == kINT8 ? 255 : 15;
   const int32_t base = 0x4B400000;
   const int32_t cmin = asym ? base : base - Q, cmax = asym ? base + M : base + Q;
   const float y = asym ? (x - lo) * r : x * r;
-  const int32_t c = min(max(__builtin_bit_cast(int32_t, y + 12582912.0f), cmin), cmax);
+  int32_t c = __builtin_bit_cast(int32_t, y + 12582912.0f);
+  if (clamp) c = min(max(c, cmin), cmax);
   return static_cast<uint32_t>(zero ? base : c);
 }
 
@@ -163,17 +173,21 @@ __device__ __forceinline__ uint32_t entry_bytes(int32_t q) {
   return ((q & kQuantAsym) ? 2u : 1u) * ((q & kQuantFp16) ? 2u : 4u);
 }
 
-// Order-key minimum and maximum of the lane's 8 elements.
+// Order keys of the two binary16 values of a word at once: h ^ 0x8000, and
+// the other 15 bits flipped too when the sign is set (order_key16 per half).
+__device__ __forceinline__ u16x2 order_key16x2(uint32_t w) {
+  const uint32_t neg = ((w >> 15) & 0x00010001u) * 0x7FFFu;  // 0x7FFF in each negative half
+  return __builtin_bit_cast(u16x2, w ^ 0x80008000u ^ neg);
+}
+
+// Order-key minimum and maximum of the lane's 8 elements (packed 16-bit
+// integer minimum / maximum over the two halves of each word).
 __device__ __forceinline__ void lane_key_range(u32x4 x, uint32_t& kmin, uint32_t& kmax) {
-  const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-  kmin = 0xFFFFu;
-  kmax = 0u;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t k0 = order_key16(w[i] & 0xFFFFu), k1 = order_key16(w[i] >> 16);
-    kmin = min(kmin, min(k0, k1));
-    kmax = max(kmax, max(k0, k1));
-  }
+  const u16x2 k0 = order_key16x2(x.x), k1 = order_key16x2(x.y), k2 = order_key16x2(x.z), k3 = order_key16x2(x.w);
+  const u16x2 lo = __builtin_elementwise_min(__builtin_elementwise_min(k0, k1), __builtin_elementwise_min(k2, k3));
+  const u16x2 hi = __builtin_elementwise_max(__builtin_elementwise_max(k0, k1), __builtin_elementwise_max(k2, k3));
+  kmin = min(static_cast<uint32_t>(lo.x), static_cast<uint32_t>(lo.y));
+  kmax = max(static_cast<uint32_t>(hi.x), static_cast<uint32_t>(hi.y));
 }
 
 // Quantizes the lane's 8 elements of a row at tier tr under descriptor q and
@@ -184,23 +198,44 @@ __device__ __forceinline__ LaneCodes quantize_lane_var(u32x4 x, int tr, int32_t 
                                                        bool write_meta) {
   constexpr int D = LPR * 8;
   const int gl = var_group_lanes(q, D);
-  const bool asym = (q & kQuantAsym) != 0;
-  uint32_t kmin, kmax;
-  lane_key_range(x, kmin, kmax);
+  const bool asym = (q & kQuantAsym) != 0;  // uniform over the row's lanes
   const uint32_t lane_amax = absmax_bits8(x);
-  const uint32_t amax = group_reduce<LPR, true>(lane_amax, gl);
-  kmin = group_reduce<LPR, false>(kmin, gl);
-  kmax = group_reduce<LPR, true>(kmax, gl);
+  uint32_t amax, kmin = 0xFFFFu, kmax = 0u;
+  if (asym) {
+    // minimum and maximum only; an inf or NaN sorts outside the finite keys
+    // [0x0400, 0xFBFF], which is all group_params needs of amax here
+    lane_key_range(x, kmin, kmax);
+    kmin = group_reduce<LPR, false>(kmin, gl);
+    kmax = group_reduce<LPR, true>(kmax, gl);
+    amax = (kmin < 0x0400u || kmax > 0xFBFFu) ? 0x7C00u : 0u;
+  } else {
+    amax = group_reduce<LPR, true>(lane_amax, gl);
+  }
   const GroupParams g = group_params(amax, kmin, kmax, tr, q);
 
   LaneCodes out;
-  out.nonfinite = group_max<LPR>(lane_amax) >= 0x7C00u;  // some group of the row does
+  {
+    // some group of the row holds an inf/NaN: one ballot over the wavefront,
+    // masked to the row's aligned lanes
+    const uint64_t nf = __ballot(lane_amax >= 0x7C00u);
+    const int first = (threadIdx.x & 63) & ~(LPR - 1);
+    const uint64_t row_lanes = (LPR >= 64 ? ~0ull : ((1ull << LPR) - 1ull)) << first;
+    out.nonfinite = (nf & row_lanes) != 0ull;
+  }
   out.scale = g.scale;
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+  if (!asym && !(q & kQuantFp16)) {  // uniform per row: the clamp cannot bind
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    out.c[2 * i] = group_code(half_lo(w[i]), g.r, g.lo, g.zero, asym, tr);
-    out.c[2 * i + 1] = group_code(half_hi(w[i]), g.r, g.lo, g.zero, asym, tr);
+    for (int i = 0; i < 4; ++i) {
+      out.c[2 * i] = group_code(half_lo(w[i]), g.r, g.lo, g.zero, false, tr, false);
+      out.c[2 * i + 1] = group_code(half_hi(w[i]), g.r, g.lo, g.zero, false, tr, false);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      out.c[2 * i] = group_code(half_lo(w[i]), g.r, g.lo, g.zero, asym, tr);
+      out.c[2 * i + 1] = group_code(half_hi(w[i]), g.r, g.lo, g.zero, asym, tr);
+    }
   }
   if (write_meta && (lane % gl) == 0) store_entry(meta + (lane / gl) * entry_bytes(q), g, q);
   return out;
@@ -244,7 +279,7 @@ __device__ __forceinline__ void chunk_layout_var(ChunkLds& s, int tr, const uint
 // largest magnitude bits in a, asymmetric tiers the order-key minimum in a and
 // maximum in b.
 struct ChanAcc {
-  uint32_t a[2][8], b[2][8];
+  u16x2 a[2][4], b[2][4];  // channels 2i (low half) and 2i + 1 (high half) of the lane
   uint32_t rows[2];
 };
 
@@ -253,27 +288,27 @@ __device__ __forceinline__ void chan_acc_init(ChanAcc& acc, const VarCfg& v) {
   for (int t = 0; t < 2; ++t) {
     const bool asym = ((t == 0 ? v.q8 : v.q4) & kQuantAsym) != 0;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      acc.a[t][e] = asym ? 0xFFFFu : 0u;
-      acc.b[t][e] = 0u;
+    for (int e = 0; e < 4; ++e) {
+      acc.a[t][e] = asym ? u16x2{0xFFFFu, 0xFFFFu} : u16x2{0u, 0u};
+      acc.b[t][e] = u16x2{0u, 0u};
     }
     acc.rows[t] = 0u;
   }
 }
 
+// Two channels per packed 16-bit integer minimum / maximum.
 template <int T>
 __device__ __forceinline__ void chan_acc_row_t(ChanAcc& acc, u32x4 x, bool asym) {
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
   ++acc.rows[T];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const uint32_t h = (w[e / 2] >> (16 * (e & 1))) & 0xFFFFu;
+  for (int e = 0; e < 4; ++e) {
     if (asym) {
-      const uint32_t k = order_key16(h);
-      acc.a[T][e] = min(acc.a[T][e], k);
-      acc.b[T][e] = max(acc.b[T][e], k);
+      const u16x2 k = order_key16x2(w[e]);
+      acc.a[T][e] = __builtin_elementwise_min(acc.a[T][e], k);
+      acc.b[T][e] = __builtin_elementwise_max(acc.b[T][e], k);
     } else {
-      acc.a[T][e] = max(acc.a[T][e], h & 0x7FFFu);
+      acc.a[T][e] = __builtin_elementwise_max(acc.a[T][e], __builtin_bit_cast(u16x2, w[e] & 0x7FFF7FFFu));
     }
   }
 }
@@ -310,12 +345,12 @@ __device__ __forceinline__ void chan_finish(ChanLds<D>& c, const ChanAcc& acc, i
     if (q & kQuantAsym) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        atomicMin(&c.kmin[t][lane * 8 + e], acc.a[t][e]);
-        atomicMax(&c.kmax[t][lane * 8 + e], acc.b[t][e]);
+        atomicMin(&c.kmin[t][lane * 8 + e], static_cast<uint32_t>(acc.a[t][e / 2][e & 1]));
+        atomicMax(&c.kmax[t][lane * 8 + e], static_cast<uint32_t>(acc.b[t][e / 2][e & 1]));
       }
     } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) atomicMax(&c.amax[t][lane * 8 + e], acc.a[t][e]);
+      for (int e = 0; e < 8; ++e) atomicMax(&c.amax[t][lane * 8 + e], static_cast<uint32_t>(acc.a[t][e / 2][e & 1]));
     }
     if (lane == 0 && acc.rows[t]) atomicAdd(&c.rows[t], acc.rows[t]);
   }

@@ -1,5 +1,8 @@
 """Exact-arithmetic proof of the shortcuts the GPU row quantizer takes.
 
+(Q = 1 in the reciprocal sequence is the quantizer variants' binary16
+metadata: r = RN32(1/s) for a stored binary16 scale s.)
+
 The quantizer of the "standard symmetric" scheme (Sec. 8) needs, per row with
 absmax a (a positive finite binary16 value) and Q in {7, 127}:
     scale = RN32(a / Q),  r = RN32(Q / a),  code = clamp(rne(RN32(x r)), -Q, Q).
@@ -75,7 +78,7 @@ def test_scale_sequence_is_correctly_rounded(Q):
         assert _rn32(s0 + e * c) == _rn32(a / Q), hex(h)
 
 
-@pytest.mark.parametrize("Q", [7, 127])
+@pytest.mark.parametrize("Q", [1, 7, 127])
 def test_reciprocal_sequence_is_correctly_rounded(Q):
     for h in _positive_halves():
         a = _half(h)
@@ -97,3 +100,24 @@ def test_clamp_never_binds(Q):
         a = _half(h)
         r = _rn32(Fraction(Q) / a)
         assert _rn32(a * r) < Q + Fraction(1, 2), hex(h)  # |x| <= a and RN is monotone
+
+
+def test_binary32_quotient_sequences_exhaustive(tmp_path):
+    """The asymmetric quantizer variants divide a binary32 group range by M
+    and M by the range (M in {15, 255}).  The GPU computes RN32(range/M) with
+    the scale sequence above and RN32(M/range) with the reciprocal sequence
+    after one refinement of the reciprocal, y = RN(r0 + RN(1 - range r0) r0).
+    tests/native/quotient_sweep.c checks both against IEEE division for every
+    binary32 significand in [1, 2) and any r0 within 2 ulp of RN(1/range)
+    (plus three other binades: both sequences commute with scaling by powers
+    of two while every intermediate stays normal, which holds for ranges in
+    [2^-24, 2^17]).  Built with gcc, correctly rounded fmaf, no contraction."""
+    import os
+    import subprocess
+    src = os.path.join(os.path.dirname(__file__), "native", "quotient_sweep.c")
+    exe = str(tmp_path / "quotient_sweep")
+    subprocess.run(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math", "-o", exe, src, "-lm"], check=True)
+    for lo, hi in ((0, 1), (-24, -23), (-10, -9), (16, 17)):
+        res = subprocess.run([exe, str(lo), str(hi)], capture_output=True, text=True)
+        assert res.returncode == 0, res.stdout + res.stderr
+        assert res.stdout.strip().endswith(" 0 failures"), res.stdout
