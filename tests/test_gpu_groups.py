@@ -60,6 +60,9 @@ CASES = [
     (2, 2, 128, 1, oracle.GRAN_LAYER, [1.0, 1.0], {}),
     (2, 2, 64, 600, oracle.GRAN_HEAD, "ramp", {"mode": oracle.RECENCY}),
     (1, 4, 64, 1031, oracle.GRAN_HEAD, "ramp", {"specials": True}),
+    # more than 512 KV heads: a layer's partial sums are taken one pair at a
+    # time (the per-pair kernel's partial form) and added by the finish
+    (2, 520, 32, 90, oracle.GRAN_LAYER, None, {"specials": True}),
 ]
 
 
