@@ -143,9 +143,11 @@ __device__ __forceinline__ GroupParams group_params(uint32_t amax, uint32_t kmin
 }
 
 // Code of x in a group (as the float-magic integer base + code, clamped).
-// clamp = false only where the clamp provably never binds: symmetric groups
-// with fp32 metadata, whose r = RN32(Q/a) keeps |RN32(x r)| < Q + 1/2 for
-// every |x| <= a (the row quantizer's exhaustive check, any binary16 a).
+// clamp = false only where the clamp provably never binds, i.e. with fp32
+// metadata: symmetric, r = RN32(Q/a) keeps |RN32(x r)| < Q + 1/2 for every
+// |x| <= a (exhaustive over binary16 a); asymmetric, 0 <= RN32(x - lo) <=
+// range and RN32(range RN32(M/range)) < M + 1/2 for every binary32 range
+// (exhaustive), so the code lies in [0, M].
 __device__ __forceinline__ uint32_t group_code(float x, float r, float lo, bool zero, bool asym, int tr,
                                                bool clamp = true) {
   const int Q = tr == kINT8 ? 127 : 7, M = tr == kINT8 ? 255 : 15;
@@ -224,11 +226,11 @@ __device__ __forceinline__ LaneCodes quantize_lane_var(u32x4 x, int tr, int32_t 
   }
   out.scale = g.scale;
   const uint32_t w[4] = {x.x, x.y, x.z, x.w};
-  if (!asym && !(q & kQuantFp16)) {  // uniform per row: the clamp cannot bind
+  if (!(q & kQuantFp16)) {  // uniform per row: with fp32 metadata the clamp cannot bind
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      out.c[2 * i] = group_code(half_lo(w[i]), g.r, g.lo, g.zero, false, tr, false);
-      out.c[2 * i + 1] = group_code(half_hi(w[i]), g.r, g.lo, g.zero, false, tr, false);
+      out.c[2 * i] = group_code(half_lo(w[i]), g.r, g.lo, g.zero, asym, tr, false);
+      out.c[2 * i + 1] = group_code(half_hi(w[i]), g.r, g.lo, g.zero, asym, tr, false);
     }
   } else {
 #pragma unroll

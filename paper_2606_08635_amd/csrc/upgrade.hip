@@ -26,6 +26,10 @@
 namespace skv {
 namespace {
 
+#ifndef SKV_UPG_ROWS_IN_FLIGHT
+#define SKV_UPG_ROWS_IN_FLIGHT 4  // listed rows whose loads a thread issues before it processes any
+#endif
+
 constexpr int kUpgThreads = 256;  // listed tokens per row workgroup
 constexpr int kUpgCheckThreads = 1024;
 constexpr uint32_t kUpgMagic = 0x55564B53u;  // "SKVU"
@@ -145,20 +149,20 @@ __global__ __launch_bounds__(kUpgCheckThreads) void upg_prep(const UpgArgs a) {
 // |e| pattern is emax (bits & 0x7FFFFFFF, reduced over the row).
 __device__ __forceinline__ u32x2 quantize_residual(const float (&e)[8], uint32_t emax, float* scale) {
   LaneCodes q;
-  int32_t lo = 0x4B400000, hi = 0x4B400000;
   if (emax >= 0x7F800000u) {
     *scale = __builtin_bit_cast(float, 0x7FC00000u);
   } else if (emax == 0u) {
     *scale = 0.0f;
   } else {
+    // RN32(a/127) and RN32(127/a) for the binary32 residual maximum a without
+    // a division, and no clamp: both sequences are correctly rounded and
+    // RN32(a RN32(127/a)) < 127.5 for every binary32 a (checked
+    // exhaustively), so |e| <= a never codes beyond +-127
     const float amag = __builtin_bit_cast(float, emax);
-    *scale = amag / 127.0f;
-    const float rcp = 127.0f / amag;
-    lo -= 127;
-    hi += 127;
+    *scale = scale_of(amag, 127.0f, 1.0f / 127.0f);
+    const float rcp = recip_scale_of_f32(amag, 127.0f);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-      q.c[i] = static_cast<uint32_t>(min(max(__builtin_bit_cast(int32_t, e[i] * rcp + 12582912.0f), lo), hi));
+    for (int i = 0; i < 8; ++i) q.c[i] = __builtin_bit_cast(uint32_t, e[i] * rcp + 12582912.0f);
     return pack_int8(q);
   }
   return u32x2{0u, 0u};
@@ -191,7 +195,7 @@ __global__ __launch_bounds__(kUpgThreads) void upg_rows(const UpgArgs a) {
   constexpr int LPR = D / 8;                 // lanes per row, 16 bytes each
   constexpr int RPI = kUpgThreads / LPR;     // rows per block-wide iteration
   constexpr int ITERS = kUpgThreads / RPI;
-  constexpr int U = ITERS < 4 ? ITERS : 4;   // rows in flight per thread
+  constexpr int U = ITERS < SKV_UPG_ROWS_IN_FLIGHT ? ITERS : SKV_UPG_ROWS_IN_FLIGHT;  // rows in flight per thread
   __shared__ int32_t s_tok[kUpgThreads];
   __shared__ uint8_t s_tier[kUpgThreads];
   uint8_t* up = a.up;

@@ -104,9 +104,11 @@ def test_clamp_never_binds(Q):
 
 def test_binary32_quotient_sequences_exhaustive(tmp_path):
     """The asymmetric quantizer variants divide a binary32 group range by M
-    and M by the range (M in {15, 255}).  The GPU computes RN32(range/M) with
-    the scale sequence above and RN32(M/range) with the reciprocal sequence
-    after one refinement of the reciprocal, y = RN(r0 + RN(1 - range r0) r0).
+    and M by the range (M in {15, 255}), the cold-tier upgrade's INT8 residual
+    a binary32 maximum by 127 and 127 by it.  The GPU computes RN32(a/M) with
+    the scale sequence above and RN32(M/a) with the reciprocal sequence after
+    one refinement of the reciprocal, y = RN(r0 + RN(1 - a r0) r0), and skips
+    the code clamp because RN32(a RN32(M/a)) < M + 1/2.
     tests/native/quotient_sweep.c checks both against IEEE division for every
     binary32 significand in [1, 2) and any r0 within 2 ulp of RN(1/range)
     (plus three other binades: both sequences commute with scaling by powers
