@@ -188,3 +188,42 @@ def test_batched_assign_of_foreign_scores():
     torch.cuda.synchronize()
     for t, w in zip(tiers, want):
         assert np.array_equal(t.cpu().numpy(), w)
+
+
+def test_batched_score_and_assign_full_size():
+    """The 64 x 2048-token batch the benchmark times (32 layers x 8 KV heads x
+    128): every request's batched scores and tier map equal the per-request
+    calls' (bit for bit), and four requests spread over both launches of the
+    batch are recomputed by the oracle."""
+    w = workloads.WORKLOADS["short_batch"]
+    L_, H_, d_ = w.layers, w.kv_heads, w.head_dim
+    lens = list(w.batch_tokens)
+    kw = dict(first_ratio=w.first_ratio, decay=w.decay, num_tiers=w.num_tiers)
+    bcfg = skv.config(L_, H_, d_, max(lens), w.budget, **kw)
+    ks, vs, scores, tiers = [], [], [], []
+    for r, n in enumerate(lens):
+        k, v = workloads.make_kv(L_, H_, n, d_, seed=16 * r, outliers=w.outliers, device="cuda")
+        ks.append(k)
+        vs.append(v)
+        scores.append(torch.full((n,), float("nan"), dtype=torch.float64, device="cuda"))
+        tiers.append(torch.full((n,), 0xEE, dtype=torch.uint8, device="cuda"))
+    ws = torch.empty(max(skv.batch_workspace_size(bcfg, scores), skv.workspace_size(bcfg)), dtype=torch.uint8,
+                     device="cuda")
+    skv.prepare(bcfg, ws)
+    say("short_batch: batched score and assign")
+    skv.score_batch(bcfg, ks, vs, scores, ws)
+    skv.assign_batch(bcfg, scores, tiers)
+    torch.cuda.synchronize()
+    for r, n in enumerate(lens):
+        c = skv.Codec(skv.config(L_, H_, d_, n, w.budget, **kw))
+        skv.score(c.cfg, ks[r], vs[r], None, c.scores, c.ws)
+        skv.assign_tiers(c.cfg, c.scores, c.tier)
+        torch.cuda.synchronize()
+        assert torch.equal(c.scores.view(torch.int64), scores[r].view(torch.int64)), f"scores of request {r}"
+        assert torch.equal(c.tier, tiers[r]), f"tier map of request {r}"
+    for r in (0, 17, 47, 63):
+        say(f"short_batch: oracle request {r}")
+        ocfg = oracle.config(L_, H_, d_, lens[r], w.budget, **kw)
+        okey = oracle.score(ocfg, u16(ks[r]), u16(vs[r]))
+        assert np.array_equal(bits64(scores[r].cpu().numpy()), bits64(okey)), f"oracle scores of request {r}"
+        assert np.array_equal(tiers[r].cpu().numpy(), oracle.assign(ocfg, okey)), f"oracle tier map of request {r}"
