@@ -558,7 +558,7 @@ def run_select(args):
 
 
 CEILING_PATTERNS = ["read", "write_nt", "write_default", "copy", "read2_write1", "read1_write2_8b",
-                    "read1_write2_16b", "nhd_scatter"]  # skv_ceiling.h, in enum order
+                    "read1_write2_16b", "nhd_scatter", "read1_write4"]  # skv_ceiling.h, in enum order
 
 
 def run_ceiling(args):

@@ -30,12 +30,15 @@ enum {
   SKV_CEIL_READ1_WRITE2_8B = 5,   /* read bytes/2 (8-byte loads), write `bytes`,
                                      both contiguous (unpack's mix)               */
   SKV_CEIL_READ1_WRITE2_16B = 6,  /* the same with 16-byte loads                   */
-  SKV_CEIL_NHD_SCATTER = 7        /* unpack's pattern at d = 128 with 8 heads: one
+  SKV_CEIL_NHD_SCATTER = 7,       /* unpack's pattern at d = 128 with 8 heads: one
                                      workgroup per 256-token chunk of a head reads
                                      its 128-byte rows contiguously (bytes/2 in
                                      all) and writes each as 256 bytes into the
                                      token's slot of a [token][8][128] binary16
                                      array (`bytes`), 2 KiB apart               */
+  SKV_CEIL_READ1_WRITE4 = 8       /* read bytes/4 (4-byte loads), write `bytes`
+                                     (16-byte default-policy stores), both
+                                     contiguous (unpack's mix at INT4)           */
 };
 
 /* Enqueues one pass of `pattern` on `stream`, each thread keeping `inflight`

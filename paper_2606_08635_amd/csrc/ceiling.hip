@@ -126,6 +126,23 @@ __global__ __launch_bounds__(kThreads) void read1_write2(const uint8_t* __restri
   }
 }
 
+// One byte read per four written (unpack's mix when most rows are INT4): a
+// thread reads 4 bytes and writes 16, both contiguous; default-policy stores
+// (the codec's d = 256 unpack), 16 KiB read and 64 KiB written per workgroup.
+template <int F>
+__global__ __launch_bounds__(kThreads) void read1_write4(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst) {
+  const uint8_t* in = src + blockIdx.x * (kTile / 4) + threadIdx.x * 4;
+  uint8_t* out = dst + blockIdx.x * kTile + threadIdx.x * 16;
+#pragma unroll
+  for (int s = 0; s < kSteps; s += F) {
+    uint32_t x[F];
+#pragma unroll
+    for (int u = 0; u < F; ++u) x[u] = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(in + (s + u) * kThreads * 4));
+#pragma unroll
+    for (int u = 0; u < F; ++u) st16<false>(out + (s + u) * kThreads * 16, u32x4{x[u], x[u] ^ 1u, x[u] ^ 2u, x[u] ^ 3u});
+  }
+}
+
 // Unpack's access pattern without the decode: one workgroup per 256-token
 // chunk of one of H = 8 head segments (segment-major workgroup order, as in
 // the codec), each token's row of 128 bytes (an INT8 row at d = 128) read
@@ -168,6 +185,7 @@ int run_pattern(int32_t pattern, uint8_t* out, const uint8_t* in, uint64_t bytes
     case SKV_CEIL_READ2_WRITE1: read2_write1<F><<<tiles / 2, kThreads, 0, stream>>>(in, out); break;
     case SKV_CEIL_READ1_WRITE2_8B: read1_write2<8, F><<<tiles, kThreads, 0, stream>>>(in, out); break;
     case SKV_CEIL_READ1_WRITE2_16B: read1_write2<16, F><<<tiles, kThreads, 0, stream>>>(in, out); break;
+    case SKV_CEIL_READ1_WRITE4: read1_write4<F><<<tiles, kThreads, 0, stream>>>(in, out); break;
     case SKV_CEIL_NHD_SCATTER: {
       // bytes written = tokens * 8 heads * 256 B; tokens a multiple of 256
       const uint64_t tokens = bytes / (kNhdHeads * 2 * kNhdRow);
@@ -213,6 +231,7 @@ uint64_t skv_ceiling_bytes(int32_t pattern, uint64_t bytes, int32_t which) {
     case SKV_CEIL_READ1_WRITE2_8B:
     case SKV_CEIL_READ1_WRITE2_16B:
     case SKV_CEIL_NHD_SCATTER: return which == 0 ? bytes / 2 : bytes;
+    case SKV_CEIL_READ1_WRITE4: return which == 0 ? bytes / 4 : bytes;
     default: return 0;
   }
 }

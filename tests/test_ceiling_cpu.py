@@ -37,10 +37,10 @@ def test_declared_symbols_exported(lib):
 def test_byte_accounting(lib):
     B = 1 << 30
     want = {0: (B, 0), 1: (0, B), 2: (0, B), 3: (B, B), 4: (B, B // 2), 5: (B // 2, B), 6: (B // 2, B),
-            7: (B // 2, B)}
+            7: (B // 2, B), 8: (B // 4, B)}
     for pat, (rd, wr) in want.items():
         assert (lib.skv_ceiling_bytes(pat, B, 0), lib.skv_ceiling_bytes(pat, B, 1)) == (rd, wr)
-    assert lib.skv_ceiling_bytes(8, B, 0) == 0
+    assert lib.skv_ceiling_bytes(9, B, 0) == 0
 
 
 def test_bad_arguments_refused_before_launch(lib):
