@@ -344,14 +344,14 @@ __global__ __launch_bounds__(kRowThreads) void gunpack_rows(const GroupArgs a, u
                     reinterpret_cast<const uint32_t*>(payload + a.chunkidx_off +
                                                       static_cast<uint64_t>(g) * a.chunkidx_stride) +
                         2 * chunk);
+    stage_scale(s, tr, reinterpret_cast<const float*>(payload + a.segtab[2 * seg]));
     s.pos[threadIdx.x] = pos;
   }
   __syncthreads();
   const uint8_t* src = payload + a.segtab[2 * seg + 1];
-  const float* scales = reinterpret_cast<const float*>(payload + a.segtab[2 * seg]);
   uint16_t* cache = (kv ? v_cache : k_cache) + static_cast<size_t>(l) * a.num_blocks * block_size * H * D +
                     static_cast<size_t>(h) * D;
-  unpack_chunk<D, unpack_rows_in_flight<D>(), unpack_nt_store<D>()>(s, src, scales, cache, H);
+  unpack_chunk<D, unpack_rows_in_flight<D>(), unpack_nt_store<D>()>(s, src, cache, H);
 }
 
 GroupArgs group_args(const GroupLaunch& gl) {

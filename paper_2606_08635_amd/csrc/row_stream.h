@@ -69,8 +69,17 @@ struct ChunkLds {
   uint32_t off[kChunkTokens];  // byte offset of the row inside its segment
   uint32_t q[kChunkTokens];    // index of the row's scale
   uint32_t pos[kChunkTokens];  // unpack: physical block * block_size + slot
+  float scale[kChunkTokens];   // unpack: the row's scale (quantized rows)
   uint32_t scan[4];
 };
+
+// Unpack: stages the scale of the chunk's row of this thread's scan slot
+// (tier code tr) in shared memory, read with one load per quantized row
+// rather than one per lane of each row.  The scale index is this thread's
+// own s.q entry; the caller's barrier after chunk_layout publishes it.
+__device__ __forceinline__ void stage_scale(ChunkLds& s, int tr, const float* __restrict__ scales) {
+  s.scale[threadIdx.x] = (tr == kINT8 || tr == kINT4) ? scales[s.q[threadIdx.x]] : 0.0f;
+}
 
 // Fills s.tier/off/q of the chunk starting at t0 from the token's tier code
 // tr (kDROP for pack slots past n, kAbsent for unpack slots past n) and the
@@ -158,22 +167,18 @@ __device__ __forceinline__ void pack_chunk(const ChunkLds& s, const RowBatch<D, 
   }
 }
 
-// Loads one row slice of a lane (16 B of FP16, 8 B of INT8 codes or 4 B of
-// INT4 codes) and its scale.
-__device__ __forceinline__ void load_row(int tr, const uint8_t* row, const float* scale_ptr, int lane,
-                                         u32x4& raw, float& sc) {
+// Loads one row slice of a lane: 16 B of FP16, 8 B of INT8 codes or 4 B of
+// INT4 codes.
+__device__ __forceinline__ void load_row(int tr, const uint8_t* row, int lane, u32x4& raw) {
   raw = u32x4{0u, 0u, 0u, 0u};
-  sc = 0.0f;
   if (tr == kFP16) {
     raw = ld_nt16(row + lane * 16);
   } else if (tr == kINT8) {
     const u32x2 c = ld_nt8(row + lane * 8);
     raw.x = c.x;
     raw.y = c.y;
-    sc = *scale_ptr;
   } else if (tr == kINT4) {
     raw.x = ld_nt4(row + lane * 4);
-    sc = *scale_ptr;
   }
 }
 
@@ -190,12 +195,11 @@ __device__ __forceinline__ u32x4 decode_row(int tr, u32x4 raw, float sc) {
 }
 
 // Dequantizes the rows of one chunk into their paged slots.  src: the
-// segment's rows; scales: its scales; cache: the (layer, head) column of the
-// paged cache (slot stride H * D elements).
+// segment's rows; the scales are staged in s.scale (stage_scale); cache: the
+// (layer, head) column of the paged cache (slot stride H * D elements).
 template <int D, int ROWS_IN_FLIGHT, bool NT>
 __device__ __forceinline__ void unpack_chunk(const ChunkLds& s, const uint8_t* __restrict__ src,
-                                             const float* __restrict__ scales, uint16_t* __restrict__ cache,
-                                             int H) {
+                                             uint16_t* __restrict__ cache, int H) {
   constexpr int LPR = D / 8;
   constexpr int RPI = kRowThreads / LPR;
   constexpr int ITERS = kChunkTokens / RPI;
@@ -209,7 +213,8 @@ __device__ __forceinline__ void unpack_chunk(const ChunkLds& s, const uint8_t* _
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int r = (it + u) * RPI + rsub;
-      load_row(s.tier[r], src + s.off[r], scales + s.q[r], lane, raw[u], sc[u]);
+      load_row(s.tier[r], src + s.off[r], lane, raw[u]);
+      sc[u] = s.scale[r];
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {

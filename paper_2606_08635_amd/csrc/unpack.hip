@@ -178,8 +178,14 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
             static_cast<uint32_t>(t % block_size);
     }
     const uint32_t* cidx = reinterpret_cast<const uint32_t*>(payload + r.chunkidx_off);
-    if constexpr (VARIANT) chunk_layout_var<D>(s, tr, cidx + 4 * chunk, chan_k ? 3 : 2, var);
-    else chunk_layout<D>(s, tr, cidx + 2 * chunk);
+    if constexpr (VARIANT) {
+      chunk_layout_var<D>(s, tr, cidx + 4 * chunk, chan_k ? 3 : 2, var);
+    } else {
+      chunk_layout<D>(s, tr, cidx + 2 * chunk);
+      // the layer's scales of this segment (descriptor 0: one fp32 per quantized row)
+      const uint8_t* lay0 = payload + r.layers_off + static_cast<uint64_t>(l) * r.layer_stride;
+      stage_scale(s, tr, reinterpret_cast<const float*>(lay0 + static_cast<uint64_t>(kv * H + h) * r.seg_scale_bytes));
+    }
     s.pos[threadIdx.x] = pos;
   }
   __syncthreads();
@@ -206,8 +212,7 @@ __global__ __launch_bounds__(kRowThreads) void unpack_rows(const BatchArgs a, ui
     unpack_chunk_var<D, SKV_VAR_ROWS_IN_FLIGHT, unpack_nt_store<D>(), false>(s, nullptr, true, src, meta, cache, H,
                                                                                 var);
   } else {
-    unpack_chunk<D, unpack_rows_in_flight<D>(), unpack_nt_store<D>()>(s, src, reinterpret_cast<const float*>(meta),
-                                                                     cache, H);
+    unpack_chunk<D, unpack_rows_in_flight<D>(), unpack_nt_store<D>()>(s, src, cache, H);
   }
 }
 
