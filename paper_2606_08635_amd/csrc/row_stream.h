@@ -23,8 +23,9 @@ namespace skv {
 // issues before it processes any of them, and non-temporal or default-policy
 // stores.  More rows in flight cover HBM latency (8 rows: pack 6.7 % and
 // unpack 1 % faster than 4 at d = 128); at d = 256 a thread's quantized rows
-// are narrow (4 or 8 bytes per lane), so unpack keeps 16 in flight and its
-// write-heavy mix runs faster with default-policy stores.
+// are narrow (4 or 8 bytes per lane), so unpack keeps 16 in flight.  Unpack's
+// write-heavy mix runs faster with default-policy stores (0.8 % at d = 128,
+// 1 % at d = 256); pack's with non-temporal ones.
 #ifndef SKV_PACK_ROWS_IN_FLIGHT
 #define SKV_PACK_ROWS_IN_FLIGHT 8
 #endif
@@ -41,10 +42,7 @@ namespace skv {
 #define SKV_UNPACK_ROWS_IN_FLIGHT_D256 16
 #endif
 #ifndef SKV_UNPACK_NT_STORE
-#define SKV_UNPACK_NT_STORE 1
-#endif
-#ifndef SKV_UNPACK_NT_STORE_D256
-#define SKV_UNPACK_NT_STORE_D256 0
+#define SKV_UNPACK_NT_STORE 0
 #endif
 // The quantizer-variant kernels hold more per row (group metadata): 4 rows.
 #ifndef SKV_VAR_ROWS_IN_FLIGHT
@@ -58,7 +56,7 @@ constexpr bool pack_nt_store() { return SKV_PACK_NT_STORE != 0; }
 template <int D>
 constexpr int unpack_rows_in_flight() { return D >= 256 ? SKV_UNPACK_ROWS_IN_FLIGHT_D256 : SKV_UNPACK_ROWS_IN_FLIGHT; }
 template <int D>
-constexpr bool unpack_nt_store() { return (D >= 256 ? SKV_UNPACK_NT_STORE_D256 : SKV_UNPACK_NT_STORE) != 0; }
+constexpr bool unpack_nt_store() { return SKV_UNPACK_NT_STORE != 0; }
 
 constexpr int kRowThreads = 256;  // == kChunkTokens: one token per thread in the scan
 static_assert(kRowThreads == kChunkTokens, "one scan slot per token of a chunk");
