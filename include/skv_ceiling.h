@@ -36,17 +36,25 @@ enum {
                                      all) and writes each as 256 bytes into the
                                      token's slot of a [token][8][128] binary16
                                      array (`bytes`), 2 KiB apart               */
-  SKV_CEIL_READ1_WRITE4 = 8       /* read bytes/4 (4-byte loads), write `bytes`
+  SKV_CEIL_READ1_WRITE4 = 8,      /* read bytes/4 (4-byte loads), write `bytes`
                                      (16-byte default-policy stores), both
                                      contiguous (unpack's mix at INT4)           */
+  SKV_CEIL_STAGE_DIRECT = 9,      /* the attention score's key stream: each
+                                     workgroup reads 256 KiB into shared memory
+                                     in 16 KiB stages, a barrier per stage, with
+                                     direct global-to-LDS loads (`bytes` rounded
+                                     down to 256 KiB; writes nothing)           */
+  SKV_CEIL_STAGE_REGS = 10        /* the same stages loaded into registers and
+                                     written to shared memory by the threads    */
 };
 
 /* Enqueues one pass of `pattern` on `stream`, each thread keeping `inflight`
  * (4, 8 or 16) loads in flight before it uses them (the write-only patterns
- * ignore it).  src (device, 16-byte aligned) holds at least the bytes the
- * pattern reads, dst (device) at least the bytes it writes; sink (device,
- * 4 KiB) is needed by SKV_CEIL_READ only, which stores into it only for an
- * input it never sees.  Returns 0 on success, 1 for a bad argument (nothing
+ * ignore it; the stage patterns keep 1, 2 or 3 stages in flight).  src
+ * (device, 16-byte aligned) holds at least the bytes the pattern reads, dst
+ * (device) at least the bytes it writes; sink (device, 4 KiB) is needed by
+ * SKV_CEIL_READ and the stage patterns only, which store into it only for an
+ * input they never see.  Returns 0 on success, 1 for a bad argument (nothing
  * enqueued), 2 if the launch failed. */
 int skv_ceiling_run(int32_t pattern, int32_t inflight, void* dst, const void* src, uint64_t bytes, void* sink,
                     hipStream_t stream);

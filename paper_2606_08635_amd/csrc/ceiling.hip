@@ -171,6 +171,95 @@ __global__ __launch_bounds__(kThreads) void nhd_scatter(const uint8_t* __restric
   }
 }
 
+// The attention score's key stream: each workgroup reads 256 KiB in 16 KiB
+// stages into shared memory, the 256 threads filling a stage as consecutive
+// 16-byte pieces (thread i: pieces i, i + 256, i + 512, i + 768), with a
+// workgroup barrier per stage.  stage_direct uses gfx950's direct
+// global-to-LDS loads with NB stage buffers (NB - 1 stages in flight);
+// stage_regs loads RS stages ahead into registers and writes each stage into
+// one of two buffers once the previous one is done.  One 32-bit word per
+// thread and stage is read back from shared memory, so every stage is used.
+constexpr int kStageBytes = 16 << 10, kStreamBytes = 256 << 10, kStagePieces = kStageBytes / (kThreads * 16);
+constexpr int kStreamStages = kStreamBytes / kStageBytes;
+
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Waits until at most N of this wave's vector memory loads are outstanding.
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+  asm volatile("" ::: "memory");
+}
+
+template <int NB>
+__global__ __launch_bounds__(kThreads) void stage_direct(const uint8_t* __restrict__ src, uint32_t* __restrict__ sink) {
+  static_assert(NB >= 2 && NB <= 4, "two to four stage buffers");
+  __shared__ __align__(16) uint8_t buf[NB * kStageBytes];
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const uint8_t* blk = src + static_cast<uint64_t>(blockIdx.x) * kStreamBytes;
+  const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t*)buf));
+  auto issue = [&](int st) {
+#pragma unroll
+    for (int u = 0; u < kStagePieces; ++u) {
+      // the wave's 64 lanes land 16 bytes each at consecutive LDS addresses from m0
+      const uint32_t m0 = lds + (st % NB) * kStageBytes + (u * kThreads + wave * 64) * 16;
+      const uint8_t* p = blk + st * kStageBytes + (u * kThreads + threadIdx.x) * 16;
+      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(p), "s"(__builtin_amdgcn_readfirstlane(m0))
+                   : "memory", "m0");
+    }
+  };
+  uint32_t acc = 0;
+  for (int st = 0; st < NB - 1; ++st) issue(st);
+  for (int st = 0; st < kStreamStages; ++st) {
+    const int later = min(NB - 2, kStreamStages - 1 - st);  // stages issued after st
+    if (later >= 2) wait_vm<2 * kStagePieces>();
+    else if (later == 1) wait_vm<kStagePieces>();
+    else wait_vm<0>();
+    lds_barrier();
+    if (st + NB - 1 < kStreamStages) issue(st + NB - 1);
+    acc ^= *reinterpret_cast<const uint32_t*>(buf + (st % NB) * kStageBytes + threadIdx.x * 64);
+  }
+  if (acc == 0x9E3779B9u) sink[blockIdx.x & 1023] = acc;
+}
+
+template <int RS>
+__global__ __launch_bounds__(kThreads) void stage_regs(const uint8_t* __restrict__ src, uint32_t* __restrict__ sink) {
+  __shared__ __align__(16) uint8_t buf[2 * kStageBytes];
+  const uint8_t* blk = src + static_cast<uint64_t>(blockIdx.x) * kStreamBytes + threadIdx.x * 16;
+  u32x4 r[RS][kStagePieces];
+#pragma unroll
+  for (int a = 0; a < RS; ++a)
+#pragma unroll
+    for (int u = 0; u < kStagePieces; ++u) r[a][u] = ld16(blk + a * kStageBytes + u * kThreads * 16);
+  uint32_t acc = 0;
+  for (int st0 = 0; st0 < kStreamStages; st0 += RS) {
+#pragma unroll
+    for (int a = 0; a < RS; ++a) {
+      const int st = st0 + a;
+      if (st >= kStreamStages) break;
+      // every thread is done reading the buffer this stage overwrites (stage st - 2)
+      lds_barrier();
+#pragma unroll
+      for (int u = 0; u < kStagePieces; ++u)
+        *reinterpret_cast<u32x4*>(buf + (st & 1) * kStageBytes + (u * kThreads + threadIdx.x) * 16) = r[a][u];
+      if (st + RS < kStreamStages) {
+#pragma unroll
+        for (int u = 0; u < kStagePieces; ++u) r[a][u] = ld16(blk + (st + RS) * kStageBytes + u * kThreads * 16);
+      }
+      lds_barrier();
+      acc ^= *reinterpret_cast<const uint32_t*>(buf + (st & 1) * kStageBytes + ((threadIdx.x * 67) & 1023) * 16);
+    }
+  }
+  if (acc == 0x9E3779B9u) sink[blockIdx.x & 1023] = acc;
+}
+
 template <int F>
 int run_pattern(int32_t pattern, uint8_t* out, const uint8_t* in, uint64_t bytes, uint64_t tiles, uint32_t* sink,
                 hipStream_t stream) {
@@ -193,6 +282,16 @@ int run_pattern(int32_t pattern, uint8_t* out, const uint8_t* in, uint64_t bytes
       nhd_scatter<F><<<(tokens / 256) * kNhdHeads, kThreads, 0, stream>>>(in, out, static_cast<uint32_t>(tokens));
       break;
     }
+    case SKV_CEIL_STAGE_DIRECT:
+    case SKV_CEIL_STAGE_REGS: {
+      // F = 4, 8, 16: one, two or three stages in flight
+      const uint64_t blocks = bytes / kStreamBytes;
+      if (sink == nullptr || blocks == 0) return 1;
+      constexpr int ahead = F == 4 ? 1 : F == 8 ? 2 : 3;
+      if (pattern == SKV_CEIL_STAGE_DIRECT) stage_direct<ahead + 1><<<blocks, kThreads, 0, stream>>>(in, sink);
+      else stage_regs<ahead><<<blocks, kThreads, 0, stream>>>(in, sink);
+      break;
+    }
     default: return 1;
   }
   return hipGetLastError() == hipSuccess ? 0 : 2;
@@ -210,6 +309,8 @@ int skv_ceiling_run(int32_t pattern, int32_t inflight, void* dst, const void* sr
   const uint64_t tiles = bytes / kTile;
   if (tiles > 0x7FFFFFFFu) return 1;
   const bool reads = pattern != SKV_CEIL_WRITE && pattern != SKV_CEIL_WRITE_DEFAULT;
+  if ((pattern == SKV_CEIL_STAGE_DIRECT || pattern == SKV_CEIL_STAGE_REGS) && bytes / kStreamBytes > 0x7FFFFFFFu)
+    return 1;
   if (reads && src == nullptr) return 1;
   uint32_t* sk = static_cast<uint32_t*>(sink);
   switch (inflight) {
@@ -232,6 +333,8 @@ uint64_t skv_ceiling_bytes(int32_t pattern, uint64_t bytes, int32_t which) {
     case SKV_CEIL_READ1_WRITE2_16B:
     case SKV_CEIL_NHD_SCATTER: return which == 0 ? bytes / 2 : bytes;
     case SKV_CEIL_READ1_WRITE4: return which == 0 ? bytes / 4 : bytes;
+    case SKV_CEIL_STAGE_DIRECT:
+    case SKV_CEIL_STAGE_REGS: return which == 0 ? bytes / kStreamBytes * kStreamBytes : 0;
     default: return 0;
   }
 }

@@ -23,9 +23,11 @@ namespace skv {
 // issues before it processes any of them, and non-temporal or default-policy
 // stores.  More rows in flight cover HBM latency (8 rows: pack 6.7 % and
 // unpack 1 % faster than 4 at d = 128); at d = 256 a thread's quantized rows
-// are narrow (4 or 8 bytes per lane), so unpack keeps 16 in flight.  Unpack's
-// write-heavy mix runs faster with default-policy stores (0.8 % at d = 128,
-// 1 % at d = 256); pack's with non-temporal ones.
+// are narrow (4 or 8 bytes per lane), so unpack keeps 16 in flight.  Both
+// kernels store non-temporally: default-policy stores leave up to the caches'
+// size of dirty lines behind when the kernel ends, and the kernels after it
+// pay their write-back (pack + unpack back to back: 2.7 % slower at d = 128,
+// 1.7-2.9 % at d = 256).
 #ifndef SKV_PACK_ROWS_IN_FLIGHT
 #define SKV_PACK_ROWS_IN_FLIGHT 8
 #endif
@@ -42,7 +44,7 @@ namespace skv {
 #define SKV_UNPACK_ROWS_IN_FLIGHT_D256 16
 #endif
 #ifndef SKV_UNPACK_NT_STORE
-#define SKV_UNPACK_NT_STORE 0
+#define SKV_UNPACK_NT_STORE 1
 #endif
 // The quantizer-variant kernels hold more per row (group metadata): 4 rows.
 #ifndef SKV_VAR_ROWS_IN_FLIGHT

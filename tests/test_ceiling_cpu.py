@@ -37,10 +37,12 @@ def test_declared_symbols_exported(lib):
 def test_byte_accounting(lib):
     B = 1 << 30
     want = {0: (B, 0), 1: (0, B), 2: (0, B), 3: (B, B), 4: (B, B // 2), 5: (B // 2, B), 6: (B // 2, B),
-            7: (B // 2, B), 8: (B // 4, B)}
+            7: (B // 2, B), 8: (B // 4, B), 9: (B, 0), 10: (B, 0)}
     for pat, (rd, wr) in want.items():
         assert (lib.skv_ceiling_bytes(pat, B, 0), lib.skv_ceiling_bytes(pat, B, 1)) == (rd, wr)
-    assert lib.skv_ceiling_bytes(9, B, 0) == 0
+    # the stage streams read whole 256 KiB workgroup streams
+    assert lib.skv_ceiling_bytes(9, 384 << 10, 0) == lib.skv_ceiling_bytes(10, 384 << 10, 0) == 256 << 10
+    assert lib.skv_ceiling_bytes(11, B, 0) == 0
 
 
 def test_bad_arguments_refused_before_launch(lib):
@@ -51,3 +53,5 @@ def test_bad_arguments_refused_before_launch(lib):
     assert lib.skv_ceiling_run(0, 4, fake, fake, 1 << 20, None, None) == 1     # read-only needs the sink
     assert lib.skv_ceiling_run(99, 4, fake, fake, 1 << 20, None, None) == 1    # unknown pattern
     assert lib.skv_ceiling_run(3, 5, fake, fake, 1 << 20, None, None) == 1     # unsupported depth
+    assert lib.skv_ceiling_run(9, 4, fake, fake, 1 << 20, None, None) == 1     # stage streams need the sink
+    assert lib.skv_ceiling_run(10, 4, fake, fake, 128 << 10, fake, None) == 1  # no whole 256 KiB stream
