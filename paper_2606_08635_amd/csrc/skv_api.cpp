@@ -847,15 +847,62 @@ skv_status skv_unpack_upgrade(const skv_config* cfg, const void* upgrade, uint64
                                         block_table, num_blocks, block_size, dev_status, stream));
 }
 
+namespace {
+
+// The host link's second direction runs on a stream of the library's own (one
+// per device, default priority, created on first use and kept until the
+// process ends), ordered against the caller's stream by two events.
+constexpr uint64_t kLinkPiece = 32ull << 20;
+constexpr int kMaxLinkDevices = 64;
+
+struct LinkLane {
+  hipStream_t up;         // host-to-device copies
+  hipEvent_t down_done;   // recorded on the caller's stream after a piece went down
+  hipEvent_t up_done;     // recorded on `up` after the last piece went up
+};
+
+std::mutex g_link_mutex;
+LinkLane g_link[kMaxLinkDevices];
+
+}  // namespace
+
 skv_status skv_link(void* dst, const void* src, uint64_t bytes, void* host_staging,
                     hipStream_t stream) {
   if (bytes == 0) return SKV_OK;
   if (dst == nullptr || src == nullptr) return SKV_ERR_INVALID_ARG;
   if (host_staging == nullptr)
     return launched(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream));
-  if (hipMemcpyAsync(host_staging, src, bytes, hipMemcpyDeviceToHost, stream) != hipSuccess)
-    return SKV_ERR_DEVICE;
-  return launched(hipMemcpyAsync(dst, host_staging, bytes, hipMemcpyHostToDevice, stream));
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return SKV_ERR_DEVICE;
+  if (dev >= kMaxLinkDevices) return SKV_ERR_INVALID_ARG;
+  std::lock_guard<std::mutex> lock(g_link_mutex);
+  LinkLane& lane = g_link[dev];
+  if (lane.up == nullptr) {
+    if (hipEventCreateWithFlags(&lane.down_done, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&lane.up_done, hipEventDisableTiming) != hipSuccess ||
+        hipStreamCreateWithFlags(&lane.up, hipStreamNonBlocking) != hipSuccess) {
+      lane.up = nullptr;
+      return SKV_ERR_DEVICE;
+    }
+  }
+  // piece i goes down on the caller's stream, then up on `up` once it is in
+  // host memory, so the way up of piece i overlaps the way down of piece i + 1
+  // (PCIe carries both directions at once); `up` runs after everything enqueued
+  // on the caller's stream before this call, and the caller's stream resumes
+  // only after the last piece is up, so the call orders like one copy
+  const uint8_t* s8 = static_cast<const uint8_t*>(src);
+  uint8_t* d8 = static_cast<uint8_t*>(dst);
+  uint8_t* h8 = static_cast<uint8_t*>(host_staging);
+  for (uint64_t off = 0; off < bytes; off += kLinkPiece) {
+    const uint64_t len = std::min(kLinkPiece, bytes - off);
+    if (hipMemcpyAsync(h8 + off, s8 + off, len, hipMemcpyDeviceToHost, stream) != hipSuccess ||
+        hipEventRecord(lane.down_done, stream) != hipSuccess ||
+        hipStreamWaitEvent(lane.up, lane.down_done, 0) != hipSuccess ||
+        hipMemcpyAsync(d8 + off, h8 + off, len, hipMemcpyHostToDevice, lane.up) != hipSuccess)
+      return SKV_ERR_DEVICE;
+  }
+  if (hipEventRecord(lane.up_done, lane.up) != hipSuccess) return SKV_ERR_DEVICE;
+  return launched(hipStreamWaitEvent(stream, lane.up_done, 0));
 }
 
 skv_status skv_group_count(const skv_config* cfg, const skv_group_spec* spec, int32_t* count) {

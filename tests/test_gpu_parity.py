@@ -187,6 +187,24 @@ def test_deterministic_and_stream_ordered():
     assert np.array_equal(outs[0][1], outs[1][1])
 
 
+def test_host_link_pieces_overlap_in_order():
+    """Several 32 MiB pieces and a ragged tail through one pinned buffer, twice
+    in a row with different data; the copies made right after each call on the
+    same stream, with no synchronization, must see the whole payload."""
+    n = 3 * (32 << 20) + 12345
+    host = torch.empty(n, dtype=torch.uint8, pin_memory=True)
+    x1 = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+    x2 = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+    z1, z2 = torch.zeros_like(x1), torch.zeros_like(x2)
+    stream = torch.cuda.current_stream()
+    skv.link(z1, x1, n, host_staging=host, stream=stream)
+    w1 = z1.clone()
+    skv.link(z2, x2, n, host_staging=host, stream=stream)
+    w2 = z2.clone()
+    torch.cuda.synchronize()
+    assert torch.equal(w1, x1) and torch.equal(w2, x2)
+
+
 def test_link_emulation_round_trip():
     x = torch.randint(0, 255, (1 << 20,), dtype=torch.uint8, device="cuda")
     y = torch.zeros_like(x)
