@@ -272,7 +272,9 @@ def run_batch(args, w):
 
 def run_pipeline(args, w, group):
     """Prefill->decode handoff latency of one request: pack, link and unpack in
-    sequence vs layer groups pipelined over three streams (NEXT-1)."""
+    sequence vs layer groups pipelined over three streams (NEXT-1).  With
+    --link host the link goes through pinned host memory (PCIe and the copy
+    engines), which the pack and unpack of other layer groups can overlap."""
     import torch
 
     from paper_2606_08635_amd import skv, workloads
@@ -287,6 +289,7 @@ def run_pipeline(args, w, group):
     kc = torch.empty(L, nb, bs, H, d, dtype=torch.float16, device="cuda")
     vc = torch.empty_like(kc)
     rx = torch.empty_like(codec.payload)
+    staging = torch.empty(codec.payload_bytes, dtype=torch.uint8, pin_memory=True) if args.link == "host" else None
     geo = codec.payload[:256].cpu().numpy().view("<u8")
     layers_off, layer_stride = int(geo[12]), int(geo[16])
     torch.cuda.synchronize()
@@ -295,7 +298,7 @@ def run_pipeline(args, w, group):
 
     def sequential():
         skv.pack(cfg, k, v, codec.tier, codec.payload, codec.status[0:1])
-        skv.link(rx, codec.payload, codec.payload_bytes)
+        skv.link(rx, codec.payload, codec.payload_bytes, staging)
         skv.unpack(cfg, rx, kc, vc, bt, bs, codec.status[1:2])
 
     def pipelined():
@@ -309,7 +312,8 @@ def run_pipeline(args, w, group):
             hi = layers_off + (g0 + gc) * layer_stride
             with torch.cuda.stream(s_link):
                 s_link.wait_event(e1)
-                skv.link(rx[lo:hi], codec.payload[lo:hi], hi - lo)
+                skv.link(rx[lo:hi], codec.payload[lo:hi], hi - lo, None if staging is None else staging[lo:hi],
+                         stream=s_link)
                 e2 = torch.cuda.Event()
                 e2.record()
             with torch.cuda.stream(s_unpack):
@@ -317,7 +321,7 @@ def run_pipeline(args, w, group):
                 skv.unpack_batch(cfg, [rx], [n], [bt], kc, vc, bs, [rst], g0, gc)
         torch.cuda.current_stream().wait_stream(s_unpack)
 
-    out = {"group_layers": group}
+    out = {"group_layers": group, "link": args.link}
     for name, fn in (("sequential", sequential), ("pipelined", pipelined)):
         for _ in range(args.warmup):
             fn()
