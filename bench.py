@@ -565,7 +565,7 @@ def run_select(args):
 
 CEILING_PATTERNS = ["read", "write_nt", "write_default", "copy", "read2_write1", "read1_write2_8b",
                     "read1_write2_16b", "nhd_scatter", "read1_write4", "stage_direct",
-                    "stage_regs"]  # skv_ceiling.h, in enum order
+                    "stage_regs", "stage_direct_cached"]  # skv_ceiling.h, in enum order
 
 
 def run_ceiling(args):

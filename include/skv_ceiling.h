@@ -42,10 +42,14 @@ enum {
   SKV_CEIL_STAGE_DIRECT = 9,      /* the attention score's key stream: each
                                      workgroup reads 256 KiB into shared memory
                                      in 16 KiB stages, a barrier per stage, with
-                                     direct global-to-LDS loads (`bytes` rounded
-                                     down to 256 KiB; writes nothing)           */
-  SKV_CEIL_STAGE_REGS = 10        /* the same stages loaded into registers and
-                                     written to shared memory by the threads    */
+                                     non-temporal direct global-to-LDS loads
+                                     (`bytes` rounded down to 256 KiB; writes
+                                     nothing)                                   */
+  SKV_CEIL_STAGE_REGS = 10,       /* the same stages loaded into registers
+                                     (non-temporal) and written to shared memory
+                                     by the threads                             */
+  SKV_CEIL_STAGE_DIRECT_CACHED = 11 /* as STAGE_DIRECT with the default cache
+                                     policy                                      */
 };
 
 /* Enqueues one pass of `pattern` on `stream`, each thread keeping `inflight`

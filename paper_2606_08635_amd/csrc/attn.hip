@@ -9,10 +9,11 @@
 // in fp32).  A workgroup owns 1024 keys of one (l, h); its four waves take
 // one 32-row query tile each (with fewer tiles, the key tiles are split into
 // interleaved streams).  The keys pass through shared memory in stages of
-// 8-16 KB (32 KB at d = 256): each key byte leaves HBM once per pass with
-// contiguous 16-byte loads into registers, one stage ahead of the stage being
-// multiplied, and is written to shared memory once that stage is done.  The
-// waves take their MFMA operands from the
+// 8-16 KB (32 KB at d = 256), filled by gfx950's direct global-to-LDS loads:
+// each key byte leaves HBM once per pass with contiguous 16-byte reads and
+// never occupies registers on the way, and the next stage is in flight while
+// the current one is multiplied.  The loads are non-temporal: with the default
+// cache policy the same stage stream runs 11 % slower.  The waves take their MFMA operands from the
 // stage through an XOR swizzle that keeps the 16-byte operand reads free of
 // bank conflicts; the wave role is scalar and the stage and tile loops are
 // unrolled, so control flow is scalar and every operand read is one lane
@@ -39,8 +40,8 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-#ifndef SKV_ATTN_WAVES
-#define SKV_ATTN_WAVES 3  // waves per SIMD up to d = 128
+#ifndef SKV_ATTN_BUFFERS
+#define SKV_ATTN_BUFFERS 2  // key stages resident per workgroup (d <= 128)
 #endif
 
 constexpr int kWaves = 4;
@@ -80,9 +81,10 @@ __device__ __forceinline__ void load_rows(const uint16_t* base, int row, bool ok
   for (int s = 0; s < D / 16; ++s) out[s] = ok ? __builtin_bit_cast(half8, *reinterpret_cast<const u32x4*>(p + 16 * s)) : half8{};
 }
 
-// A stage of keys in shared memory: kKeys rows of D binary16 values, written
-// as consecutive 16-byte pieces (thread i of the workgroup writes pieces
-// u * 256 + i); piece p holds row p / kCpr, chunk (p % kCpr) ^ swz(row) of the keys
+// A stage of keys in shared memory: kKeys rows of D binary16 values, filled
+// by direct global-to-LDS loads.  Each 16-byte load of a wave lands at LDS
+// address base + 16 * lane, so a stage is written as consecutive 16-byte
+// pieces; piece p holds row p / kCpr, chunk (p % kCpr) ^ swz(row) of the keys
 // (kCpr = D / 8 chunks of 8 elements per row).  The XOR swizzle spreads the
 // 16-byte operand reads of 8 consecutive rows (same chunk) over all 32 banks;
 // it depends on the row only modulo 32, so a lane's read offsets are the same
@@ -96,20 +98,41 @@ struct Stage {
   static constexpr int kPieces = kKeys * kCpr / (kWaves * 64);   // 16-byte loads per thread per stage
   static constexpr int kTileBytes = 32 * D * 2;
   static constexpr int kBytes = kKeys * D * 2;
-  // two stage buffers: one being multiplied while the next is written
-  static constexpr int kBuffers = 2;
-  // register budget: the stage in flight takes 4 * kPieces registers, so
-  // three waves per SIMD up to d = 128 (no spills), two at d = 256
-  static constexpr int kWavesPerSimd = D >= 256 ? 2 : SKV_ATTN_WAVES;
+  // one stage being multiplied, the others in flight; at d = 256 a stage is 32 KB
+  static constexpr int kBuffers = D >= 256 ? 2 : SKV_ATTN_BUFFERS;
+  // register budget: four waves per SIMD up to d = 128 (no spills), two at d = 256
+  static constexpr int kWavesPerSimd = D >= 256 ? 2 : 4;
   static_assert(kPieces * kWaves * 64 == kKeys * kCpr, "a stage is whole 16-byte pieces per thread");
   static_assert(kBlockKeys % kKeys == 0, "a block is whole stages");
+  static_assert(kBuffers >= 2 && kBuffers <= 4 && (kBuffers - 2) * kPieces < 64, "outstanding loads fit vmcnt");
   __device__ static __forceinline__ int swz(int row) { return (row / kRowsPer128) % kCpr; }
 };
 
+// Waits until at most N of this wave's vector memory loads are outstanding
+// (loads complete in issue order, so the older ones have landed).
+template <int N>
+__device__ __forceinline__ void wait_loads() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  asm volatile("" ::: "memory");
+  // s_waitcnt: vmcnt bits 3:0 and 15:14; expcnt (6:4) and lgkmcnt (11:8) at their maxima
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+  asm volatile("" ::: "memory");
+}
+
+// Waits until the loads of a stage have landed when `later` stages were
+// issued after it (later <= 2).
+template <int D>
+__device__ __forceinline__ void wait_stage(int later) {
+  constexpr int P = Stage<D>::kPieces;
+  if (later == 0) wait_loads<0>();
+  else if (later == 1) wait_loads<P>();
+  else wait_loads<2 * P>();
+}
+
 // Workgroup barrier for shared memory only: waits for this wave's LDS
 // accesses (lgkmcnt 0) but, unlike __syncthreads, not for the global loads in
-// flight (the next stage's keys); the empty asm statements keep the compiler
-// from moving memory accesses across it.
+// flight; the empty asm statements keep the compiler from moving memory
+// accesses across it.
 __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0); vmcnt and expcnt at their maxima
@@ -117,27 +140,30 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Loads this thread's pieces of the stage of keys t0 .. t0 + kKeys - 1 into
-// registers.  Rows at or beyond n repeat row n - 1 (a valid address); their
-// logits are masked or never stored.
+// One direct global-to-LDS load, non-temporal (the keys are streamed once
+// per pass): the 16 bytes at src (per lane) land at LDS byte address
+// lds_base + 16 * lane.  Issued from inline assembly so that the
+// compiler does not count it among its own loads: the stage loop waits for it
+// explicitly (wait_stage), and the compiler's own waits for its loads stay
+// correct because they can only wait longer.
+__device__ __forceinline__ void load_to_lds(const void* src, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(src), "s"(lds_base) : "memory", "m0");
+}
+
+// Issues the direct loads of keys t0 .. t0 + kKeys - 1 into the stage at sk.
+// Rows at or beyond n repeat row n - 1 (a valid address); their logits are
+// masked or never stored.
 template <int D>
-__device__ __forceinline__ void stage_fetch(const uint16_t* kbase, int t0, int n, u32x4 (&r)[Stage<D>::kPieces]) {
+__device__ __forceinline__ void stage_issue(const uint16_t* kbase, int t0, int n, uint8_t* sk, int wave) {
   using S = Stage<D>;
+  const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t*)sk));
 #pragma unroll
   for (int u = 0; u < S::kPieces; ++u) {
     const int p = u * kWaves * 64 + static_cast<int>(threadIdx.x);
     const int row = p / S::kCpr, chunk = (p % S::kCpr) ^ S::swz(row);
     const uint16_t* src = kbase + static_cast<size_t>(min(t0 + row, n - 1)) * D + 8 * chunk;
-    r[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src));
+    load_to_lds(src, __builtin_amdgcn_readfirstlane(base + static_cast<uint32_t>((u * kWaves * 64 + wave * 64) * 16)));
   }
-}
-
-// Writes this thread's fetched pieces into the stage buffer at sk.
-template <int D>
-__device__ __forceinline__ void stage_store(uint8_t* sk, const u32x4 (&r)[Stage<D>::kPieces]) {
-#pragma unroll
-  for (int u = 0; u < Stage<D>::kPieces; ++u)
-    *reinterpret_cast<u32x4*>(sk + 16 * (u * kWaves * 64 + static_cast<int>(threadIdx.x))) = r[u];
 }
 
 typedef __attribute__((address_space(3))) const half8* lds_half8_ptr;
@@ -264,43 +290,44 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
   lane_addresses<D>(s_k, raddr);
   for (int round = 0; 4 * round < MT; ++round) {
     const WaveRole role = wave_role(MT, round, wave);
-    // stage 0 goes to shared memory with the query rows; while a stage is
-    // multiplied, the next one waits in registers to be written into the
-    // other buffer and the one after it is loading
-    u32x4 nxt[S::kPieces];
-    stage_fetch<D>(kbase, key0, n, nxt);
+    // up to kBuffers - 1 later stages are in flight while a stage is
+    // multiplied; the query rows are waited for once, with stage 0, so that
+    // no load of the compiler's own is pending inside the stage loop
+    stage_issue<D>(kbase, key0, n, s_k, wave);
     half8 qr[D / 16];
     const int qrow = role.qtile * 32 + j;
     if (role.active) load_rows<D>(qbase, qrow, qrow < M, qr);
-    stage_store<D>(s_k, nxt);
-    if (nstages > 1) stage_fetch<D>(kbase, key0 + S::kKeys, n, nxt);
+    wait_loads<0>();
+    for (int st = 1; st < S::kBuffers - 1 && st < nstages; ++st)
+      stage_issue<D>(kbase, key0 + st * S::kKeys, n, s_k + st * S::kBytes, wave);
     float m = -INFINITY, sum = 0.0f;  // m in base-2 units (logit * scale * log2 e)
     for (int st0 = 0; st0 < nstages; st0 += S::kBuffers) {
 #pragma unroll
       for (int b = 0; b < S::kBuffers; ++b) {
         const int st = st0 + b;  // stage st lives in buffer b
         if (st >= nstages) break;
-        // every thread's pieces of stage st are in shared memory, and every
-        // wave is done with stage st - 1, whose buffer receives stage st + 1
+        wait_stage<D>(min(S::kBuffers - 2, nstages - 1 - st));  // later stages may still be loading
+        // every thread's pieces of stage st have landed, and every wave is done
+        // with stage st - 1, whose buffer the next issue overwrites
         lds_barrier();
-        if (role.active) {
-          const int ts = key0 + st * S::kKeys;  // first key of the stage
+        if (st + S::kBuffers - 1 < nstages)
+          stage_issue<D>(kbase, key0 + (st + S::kBuffers - 1) * S::kKeys, n,
+                         s_k + ((b + S::kBuffers - 1) % S::kBuffers) * S::kBytes, wave);
+        if (!role.active) continue;
+        const int ts = key0 + st * S::kKeys;  // first key of the stage
 #pragma unroll
-          for (int ti = 0; ti < S::kTiles; ++ti) {
-            // this wave's tiles: global tile index = stream (mod nstreams, a power of two)
-            const int t0 = ts + ti * 32;
-            if (((st * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
-            half8 kr[D / 16];
-            stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
-            floatx16 acc{};
+        for (int ti = 0; ti < S::kTiles; ++ti) {
+          // this wave's tiles: global tile index = stream (mod nstreams, a power of two)
+          const int t0 = ts + ti * 32;
+          if (((st * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
+          half8 kr[D / 16];
+          stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
+          floatx16 acc{};
 #pragma unroll
-            for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[s], qr[s], acc, 0, 0, 0);
-            if (t0 + 32 <= n) tile_update<false>(acc, alpha, t0, hf, n, m, sum);
-            else tile_update<true>(acc, alpha, t0, hf, n, m, sum);
-          }
+          for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[s], qr[s], acc, 0, 0, 0);
+          if (t0 + 32 <= n) tile_update<false>(acc, alpha, t0, hf, n, m, sum);
+          else tile_update<true>(acc, alpha, t0, hf, n, m, sum);
         }
-        if (st + 1 < nstages) stage_store<D>(s_k + (1 - b) * S::kBytes, nxt);
-        if (st + 2 < nstages) stage_fetch<D>(kbase, key0 + (st + 2) * S::kKeys, n, nxt);
       }
     }
     if (role.active) {
@@ -364,8 +391,7 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
   lane_addresses<D>(s_k, raddr);
   for (int round = 0; 4 * round < MT; ++round) {
     const WaveRole role = wave_role(MT, round, wave);
-    u32x4 nxt[S::kPieces];  // the next stage's pieces of this thread
-    stage_fetch<D>(kbase, key0, n, nxt);
+    stage_issue<D>(kbase, key0, n, s_k, wave);
     half8 qr[D / 16];
     float beta[16];  // c * log2(e) of the lane's 16 rows; +inf for padding rows
     // padding rows of a partial query tile: their zero queries can still make
@@ -394,55 +420,53 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
         out[t] = round == 0 ? v : out[t] + v;
       }
     };
-    // this wave's tiles of stage st (in buffer b): the sums over the lane's
-    // 16 rows of p = 2^(acc * alpha - beta), then over both lane-halves, go to
-    // s_part[st & 1][wave]
-    auto colsum_stage = [&](int st, int b) {
-      float* part = s_part[st & 1][wave];
-      const int ts = key0 + st * S::kKeys;
-#pragma unroll
-      for (int ti = 0; ti < S::kTiles; ++ti) {
-        const int t0 = ts + ti * 32;
-        if (((st * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
-        half8 kr[D / 16];
-        stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
-        floatx16 acc{};
-#pragma unroll
-        for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[s], kr[s], acc, 0, 0, 0);
-        float e[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) e[r] = exp2_fast(__builtin_fmaf(acc[r], alpha, -beta[r]));
-        if (padded) {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) e[r] = (valid_rows >> r) & 1u ? e[r] : 0.0f;
-        }
-        float p = tree_sum<16>(e);
-        p += __shfl_xor(p, 32);  // the other lane-half holds the other 16 rows
-        if (hf == 0) part[ti * 32 + j] = p;
-      }
-    };
-    // stage 0 goes to shared memory with the query rows and row constants;
-    // while a stage is multiplied, the next one waits in registers to be
-    // written into the other buffer and the one after it is loading
-    stage_store<D>(s_k, nxt);
-    if (nstages > 1) stage_fetch<D>(kbase, key0 + S::kKeys, n, nxt);
+    // the query rows and row constants are waited for once, with stage 0;
+    // up to kBuffers - 1 later stages are in flight while a stage is multiplied
+    wait_loads<0>();
+    for (int st = 1; st < S::kBuffers - 1 && st < nstages; ++st)
+      stage_issue<D>(kbase, key0 + st * S::kKeys, n, s_k + st * S::kBytes, wave);
     for (int st0 = 0; st0 < nstages; st0 += S::kBuffers) {
 #pragma unroll
       for (int b = 0; b < S::kBuffers; ++b) {
         const int st = st0 + b;  // stage st lives in buffer b
         if (st >= nstages) break;
-        // stage st is in shared memory; every wave is done with stage st - 1
-        // (its buffer receives stage st + 1) and has written its partial sums
+        wait_stage<D>(min(S::kBuffers - 2, nstages - 1 - st));  // later stages may still be loading
+        // stage st has landed everywhere; every wave is done with stage st - 1
+        // (its buffer is reloaded next) and has written its partial sums
         lds_barrier();
+        if (st + S::kBuffers - 1 < nstages)
+          stage_issue<D>(kbase, key0 + (st + S::kBuffers - 1) * S::kKeys, n,
+                         s_k + ((b + S::kBuffers - 1) % S::kBuffers) * S::kBytes, wave);
         if (st > 0) flush(st - 1);
-        if (role.active) colsum_stage(st, b);
-        if (st + 1 < nstages) stage_store<D>(s_k + (1 - b) * S::kBytes, nxt);
-        if (st + 2 < nstages) stage_fetch<D>(kbase, key0 + (st + 2) * S::kKeys, n, nxt);
+        if (!role.active) continue;
+        float* part = s_part[st & 1][wave];
+        const int ts = key0 + st * S::kKeys;
+#pragma unroll
+        for (int ti = 0; ti < S::kTiles; ++ti) {
+          const int t0 = ts + ti * 32;
+          if (((st * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
+          half8 kr[D / 16];
+          stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
+          floatx16 acc{};
+#pragma unroll
+          for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[s], kr[s], acc, 0, 0, 0);
+          // sum over the lane's 16 rows of p = 2^(acc * alpha - beta), then over both lane-halves
+          float e[16];
+#pragma unroll
+          for (int r = 0; r < 16; ++r) e[r] = exp2_fast(__builtin_fmaf(acc[r], alpha, -beta[r]));
+          if (padded) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) e[r] = (valid_rows >> r) & 1u ? e[r] : 0.0f;
+          }
+          float p = tree_sum<16>(e);
+          p += __shfl_xor(p, 32);  // the other lane-half holds the other 16 rows
+          if (hf == 0) part[ti * 32 + j] = p;
+        }
       }
     }
     lds_barrier();
     flush(nstages - 1);
-    __syncthreads();  // the next round's first stage overwrites the first stage buffer
+    __syncthreads();  // the next round's first loads overwrite the first stage buffers
   }
 }
 

@@ -175,9 +175,10 @@ __global__ __launch_bounds__(kThreads) void nhd_scatter(const uint8_t* __restric
 // stages into shared memory, the 256 threads filling a stage as consecutive
 // 16-byte pieces (thread i: pieces i, i + 256, i + 512, i + 768), with a
 // workgroup barrier per stage.  stage_direct uses gfx950's direct
-// global-to-LDS loads with NB stage buffers (NB - 1 stages in flight);
-// stage_regs loads RS stages ahead into registers and writes each stage into
-// one of two buffers once the previous one is done.  One 32-bit word per
+// global-to-LDS loads with NB stage buffers (NB - 1 stages in flight),
+// non-temporal (NT) or with the default cache policy; stage_regs loads RS
+// stages ahead into registers (non-temporal) and writes each stage into one
+// of two buffers once the previous one is done.  One 32-bit word per
 // thread and stage is read back from shared memory, so every stage is used.
 constexpr int kStageBytes = 16 << 10, kStreamBytes = 256 << 10, kStagePieces = kStageBytes / (kThreads * 16);
 constexpr int kStreamStages = kStreamBytes / kStageBytes;
@@ -198,7 +199,7 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("" ::: "memory");
 }
 
-template <int NB>
+template <int NB, bool NT>
 __global__ __launch_bounds__(kThreads) void stage_direct(const uint8_t* __restrict__ src, uint32_t* __restrict__ sink) {
   static_assert(NB >= 2 && NB <= 4, "two to four stage buffers");
   __shared__ __align__(16) uint8_t buf[NB * kStageBytes];
@@ -211,8 +212,12 @@ __global__ __launch_bounds__(kThreads) void stage_direct(const uint8_t* __restri
       // the wave's 64 lanes land 16 bytes each at consecutive LDS addresses from m0
       const uint32_t m0 = lds + (st % NB) * kStageBytes + (u * kThreads + wave * 64) * 16;
       const uint8_t* p = blk + st * kStageBytes + (u * kThreads + threadIdx.x) * 16;
-      asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(p), "s"(__builtin_amdgcn_readfirstlane(m0))
-                   : "memory", "m0");
+      if (NT)
+        asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off nt" ::"v"(p), "s"(__builtin_amdgcn_readfirstlane(m0))
+                     : "memory", "m0");
+      else
+        asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(p), "s"(__builtin_amdgcn_readfirstlane(m0))
+                     : "memory", "m0");
     }
   };
   uint32_t acc = 0;
@@ -283,12 +288,15 @@ int run_pattern(int32_t pattern, uint8_t* out, const uint8_t* in, uint64_t bytes
       break;
     }
     case SKV_CEIL_STAGE_DIRECT:
+    case SKV_CEIL_STAGE_DIRECT_CACHED:
     case SKV_CEIL_STAGE_REGS: {
       // F = 4, 8, 16: one, two or three stages in flight
       const uint64_t blocks = bytes / kStreamBytes;
       if (sink == nullptr || blocks == 0) return 1;
       constexpr int ahead = F == 4 ? 1 : F == 8 ? 2 : 3;
-      if (pattern == SKV_CEIL_STAGE_DIRECT) stage_direct<ahead + 1><<<blocks, kThreads, 0, stream>>>(in, sink);
+      if (pattern == SKV_CEIL_STAGE_DIRECT) stage_direct<ahead + 1, true><<<blocks, kThreads, 0, stream>>>(in, sink);
+      else if (pattern == SKV_CEIL_STAGE_DIRECT_CACHED)
+        stage_direct<ahead + 1, false><<<blocks, kThreads, 0, stream>>>(in, sink);
       else stage_regs<ahead><<<blocks, kThreads, 0, stream>>>(in, sink);
       break;
     }
@@ -309,7 +317,8 @@ int skv_ceiling_run(int32_t pattern, int32_t inflight, void* dst, const void* sr
   const uint64_t tiles = bytes / kTile;
   if (tiles > 0x7FFFFFFFu) return 1;
   const bool reads = pattern != SKV_CEIL_WRITE && pattern != SKV_CEIL_WRITE_DEFAULT;
-  if ((pattern == SKV_CEIL_STAGE_DIRECT || pattern == SKV_CEIL_STAGE_REGS) && bytes / kStreamBytes > 0x7FFFFFFFu)
+  if ((pattern == SKV_CEIL_STAGE_DIRECT || pattern == SKV_CEIL_STAGE_DIRECT_CACHED || pattern == SKV_CEIL_STAGE_REGS) &&
+      bytes / kStreamBytes > 0x7FFFFFFFu)
     return 1;
   if (reads && src == nullptr) return 1;
   uint32_t* sk = static_cast<uint32_t*>(sink);
@@ -334,6 +343,7 @@ uint64_t skv_ceiling_bytes(int32_t pattern, uint64_t bytes, int32_t which) {
     case SKV_CEIL_NHD_SCATTER: return which == 0 ? bytes / 2 : bytes;
     case SKV_CEIL_READ1_WRITE4: return which == 0 ? bytes / 4 : bytes;
     case SKV_CEIL_STAGE_DIRECT:
+    case SKV_CEIL_STAGE_DIRECT_CACHED:
     case SKV_CEIL_STAGE_REGS: return which == 0 ? bytes / kStreamBytes * kStreamBytes : 0;
     default: return 0;
   }
