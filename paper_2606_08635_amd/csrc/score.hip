@@ -23,10 +23,13 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kMaxPairsPerGroup = 512;  // 2 tensors * 8 elements * 512 = 2^13 terms per thread
-#ifndef SKV_KVNORM_PAIR_ROWS
-#define SKV_KVNORM_PAIR_ROWS 4
+#ifndef SKV_KVNORM_PAIR_INFLIGHT
+#define SKV_KVNORM_PAIR_INFLIGHT 4  // row slices whose loads are issued together, one-pair parts
 #endif
-constexpr int kPairRows = SKV_KVNORM_PAIR_ROWS;  // row slices in flight per thread, one-pair parts
+#ifndef SKV_KVNORM_PAIR_ROWS
+#define SKV_KVNORM_PAIR_ROWS 8
+#endif
+constexpr int kPairRows = SKV_KVNORM_PAIR_ROWS;  // row slices per thread, one-pair parts
 
 struct U128 {
   uint64_t lo, hi;
@@ -206,10 +209,12 @@ __device__ __forceinline__ double group_sum_f64(double x) {
 
 // Partial sums with one (layer, head) pair per part (per-head maps): block
 // (x, y) covers pair y and the T * TOK consecutive tokens from x * T * TOK,
-// i.e. one contiguous run of each of the pair's K and V planes (T even).  A
-// thread takes its T row slices two at a time, all four loads issued before
-// any is added, and the lanes of a row combine their sums in binary64 by
-// butterfly lane moves instead of through LDS.  That stays exact: a lane's
+// i.e. one contiguous run of each of the pair's K and V planes.  A thread
+// takes its T row slices S at a time, all 2 S loads issued before any is
+// added (8 slices four at a time: 56 registers, 1 % faster than 4 slices two
+// at a time; 4 slices four at a time or 8 eight at a time unroll into 114 or
+// 502 registers and run far slower), and the lanes of a row combine their
+// sums in binary64 by butterfly lane moves instead of through LDS.  That stays exact: a lane's
 // sums hold 16 terms (8 K and 8 V elements), so over the LPR <= 32 lanes of
 // a row the integer parts stay below 512 * 2^40 = 2^49 and the fractions,
 // multiples of 2^-40, below 2^9; both are exact binary64 integers in their
@@ -230,11 +235,13 @@ __global__ __launch_bounds__(kThreads) void kvnorm_partial_pairs(const uint16_t*
   const int t0 = blockIdx.x * (T * TOK) + threadIdx.x / LPR;
   const int p = blockIdx.y;
   const size_t plane = static_cast<size_t>(p) * n * D;
+  constexpr int S = SKV_KVNORM_PAIR_INFLIGHT < T ? SKV_KVNORM_PAIR_INFLIGHT : T;
+  static_assert(T % S == 0, "whole groups of row slices");
 #pragma unroll 1
-  for (int i0 = 0; i0 < T; i0 += 2) {  // two row slices (four 16-byte loads) in flight
-    u32x4 kx[2], vx[2];
+  for (int i0 = 0; i0 < T; i0 += S) {  // S row slices (2 S 16-byte loads) in flight
+    u32x4 kx[S], vx[S];
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < S; ++u) {
       const int t = t0 + (i0 + u) * TOK;
       kx[u] = u32x4{0u, 0u, 0u, 0u};
       vx[u] = u32x4{0u, 0u, 0u, 0u};
@@ -245,7 +252,7 @@ __global__ __launch_bounds__(kThreads) void kvnorm_partial_pairs(const uint16_t*
       }
     }
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
+    for (int u = 0; u < S; ++u) {
       const int t = t0 + (i0 + u) * TOK;
       double ah = 0.0, al = 0.0;
       acc16(kx[u], ah, al);
