@@ -6,8 +6,9 @@
 //   A_t = (1 / (L*Hq*W)) * sum over (l, h, m) of softmax_t(z[m, :])[t].
 // Q.K^T is a dense contraction, so it runs on the matrix cores
 // (v_mfma_f32_32x32x16_f16, fp32 accumulation; binary16 products are exact
-// in fp32).  A workgroup owns 1024 keys of one (l, h); its four waves take
-// one 32-row query tile each (with fewer tiles, the key tiles are split into
+// in fp32).  A workgroup walks a run of two 1024-key blocks of one (l, h)
+// (consecutive workgroups take different pairs); its four waves take one
+// 32-row query tile each (with fewer tiles, the key tiles are split into
 // interleaved streams).  The keys pass through shared memory in stages of
 // 8-16 KB (32 KB at d = 256), filled by gfx950's direct global-to-LDS loads:
 // each key byte leaves HBM once per pass with contiguous 16-byte reads and
@@ -40,12 +41,32 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
+// Tuning (measured on MI355X, alternating forms on one box; the macros
+// override them for sweeps): two key stages of two 32-key tiles per
+// workgroup (one tile per stage with three or four stages was 1-3 % slower at
+// d = 128 and 3-7 % at d = 256), and runs of two blocks per workgroup (one
+// block per workgroup was 1.5-2.5 % slower, four blocks lost 13 % at d = 256
+// for want of workgroups; 2048-key blocks instead of runs came within 2 %
+// of runs of two, with different partial sums).
 #ifndef SKV_ATTN_BUFFERS
 #define SKV_ATTN_BUFFERS 2  // key stages resident per workgroup (d <= 128)
 #endif
+#ifndef SKV_ATTN_BUFFERS_D256
+#define SKV_ATTN_BUFFERS_D256 2
+#endif
+#ifndef SKV_ATTN_TILES_D128
+#define SKV_ATTN_TILES_D128 2  // 32-key tiles per stage at d = 128
+#endif
+#ifndef SKV_ATTN_TILES_D256
+#define SKV_ATTN_TILES_D256 2
+#endif
+#ifndef SKV_ATTN_RUN_BLOCKS
+#define SKV_ATTN_RUN_BLOCKS 2
+#endif
 
 constexpr int kWaves = 4;
-constexpr int kBlockKeys = 1024;              // keys per workgroup
+constexpr int kBlockKeys = 1024;                 // keys per block of partial results
+constexpr int kRunBlocks = SKV_ATTN_RUN_BLOCKS;  // key blocks a workgroup walks
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -91,7 +112,7 @@ __device__ __forceinline__ void load_rows(const uint16_t* base, int row, bool ok
 // for every tile and every stage.
 template <int D>
 struct Stage {
-  static constexpr int kTiles = D < 128 ? 4 : 2;                 // 32-key tiles per stage
+  static constexpr int kTiles = D < 128 ? 4 : D == 128 ? SKV_ATTN_TILES_D128 : SKV_ATTN_TILES_D256;  // 32-key tiles per stage
   static constexpr int kKeys = kTiles * 32;
   static constexpr int kCpr = D / 8;                             // 16-byte chunks per row
   static constexpr int kRowsPer128 = kCpr >= 8 ? 1 : 8 / kCpr;   // rows sharing one 128-byte bank line
@@ -99,7 +120,7 @@ struct Stage {
   static constexpr int kTileBytes = 32 * D * 2;
   static constexpr int kBytes = kKeys * D * 2;
   // one stage being multiplied, the others in flight; at d = 256 a stage is 32 KB
-  static constexpr int kBuffers = D >= 256 ? 2 : SKV_ATTN_BUFFERS;
+  static constexpr int kBuffers = D >= 256 ? SKV_ATTN_BUFFERS_D256 : SKV_ATTN_BUFFERS;
   // register budget: four waves per SIMD up to d = 128 (no spills), two at d = 256
   static constexpr int kWavesPerSimd = D >= 256 ? 2 : 4;
   static_assert(kPieces * kWaves * 64 == kKeys * kCpr, "a stage is whole 16-byte pieces per thread");
@@ -264,90 +285,141 @@ __device__ __forceinline__ void tile_update(const floatx16& acc, float alpha, in
   m = mn;
 }
 
-// grid (L*H, key blocks); pstat[(lh * nkb + kb) * Mpad + row] = (max of z, sum of exp(z - max))
-// over the block's keys.  The logits are formed transposed (keys as MFMA rows,
-// queries as columns), so a lane holds 16 keys of one query and keeps that
-// query's running (max, sum) in two registers: one exponential per logit.
-// The stage loop is unrolled over the stage buffers and the tiles of a stage,
-// so every shared-memory read is a lane offset plus an immediate.
+// A workgroup owns a run of consecutive key blocks of one (l, h) pair and
+// walks it stage by stage, so the next stages are in flight across block
+// boundaries and the pair's query rows are loaded once.  Workgroup w takes
+// pair w % LH (consecutive workgroups read different pairs) and run
+// w / LH of the pair's R runs.  Every block still gets its own partial
+// results, so the arithmetic does not depend on the run length.
+template <int D>
+struct BlockRun {
+  static constexpr int kFull = kBlockKeys / Stage<D>::kKeys;  // stages of a whole block
+  int nkb;       // key blocks per pair
+  int last;      // stages of a pair's last block
+  int lh;        // the pair
+  int kb0, kb1;  // its blocks kb0 .. kb1 - 1
+  int nst;       // their stages
+  __device__ __forceinline__ BlockRun(int n, int LH, int R) {
+    nkb = (n + kBlockKeys - 1) / kBlockKeys;
+    last = (n - (nkb - 1) * kBlockKeys + Stage<D>::kKeys - 1) / Stage<D>::kKeys;
+    lh = static_cast<int>(blockIdx.x % static_cast<uint32_t>(LH));
+    const int r = static_cast<int>(blockIdx.x / static_cast<uint32_t>(LH));
+    kb0 = r * nkb / R;
+    kb1 = (r + 1) * nkb / R;
+    nst = (kb1 - kb0) * kFull - (kb1 == nkb ? kFull - last : 0);
+  }
+  __device__ __forceinline__ int stages(int kb) const { return kb == nkb - 1 ? last : kFull; }
+};
+
+// grid: LH * R workgroups (BlockRun); pstat[(lh * nkb + kb) * Mpad + row] =
+// (max of z, sum of exp(z - max)) over the keys of block kb of pair lh.  The
+// logits are formed transposed (keys as MFMA rows, queries as columns), so a
+// lane holds 16 keys of one query and keeps that query's running (max, sum)
+// in two registers: one exponential per logit.  The stage loop is unrolled
+// over the stage buffers and the tiles of a stage, so every shared-memory
+// read is a lane offset plus an immediate.
 template <int D>
 __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Stage<D>::kWavesPerSimd))) void attn_stats(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ q, int n, int H, int Hq, int W, float scale,
-    float2* __restrict__ pstat) {
+    int runs, float2* __restrict__ pstat) {
   using S = Stage<D>;
-  const int lh = blockIdx.x, kb = blockIdx.y, nkb = gridDim.y;
-  const int l = lh / H, h = lh % H, G = Hq / H, M = G * W, MT = (M + 31) / 32, Mpad = MT * 32;
+  const int G = Hq / H, M = G * W, MT = (M + 31) / 32, Mpad = MT * 32;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);  // uniform per wave
   const int lane = threadIdx.x & 63, hf = lane >> 5, j = lane & 31;
+  const float alpha = scale * kLog2e;
+  const BlockRun<D> run(n, static_cast<int>(gridDim.x) / runs, runs);
+  const int lh = run.lh, l = lh / H, h = lh % H, nst = run.nst;
   const uint16_t* kbase = k + static_cast<size_t>(lh) * n * D;
   const uint16_t* qbase = q + (static_cast<size_t>(l) * Hq + static_cast<size_t>(h) * G) * W * D;
-  const float alpha = scale * kLog2e;
-  const int key0 = kb * kBlockKeys;
-  const int nstages = (min(n - key0, kBlockKeys) + S::kKeys - 1) / S::kKeys;
+  float2* out = pstat + static_cast<size_t>(lh) * run.nkb * Mpad;
   __shared__ __align__(16) uint8_t s_k[S::kBuffers * S::kBytes];
-  __shared__ float2 s_stat[kWaves][32];
+  __shared__ float2 s_stat[2][kWaves][32];  // per block parity, wave and query
   uint32_t raddr[D / 16];
   lane_addresses<D>(s_k, raddr);
   for (int round = 0; 4 * round < MT; ++round) {
     const WaveRole role = wave_role(MT, round, wave);
+    // the next stage to issue: stage ist of block ikb
+    int ikb = run.kb0, ist = 0;
+    auto issue = [&](uint8_t* buf) {
+      stage_issue<D>(kbase, ikb * kBlockKeys + ist * S::kKeys, n, buf, wave);
+      if (++ist == run.stages(ikb)) {
+        ist = 0;
+        ++ikb;
+      }
+    };
+    // merges the streams of each query of block kb (stream order; m to z units)
+    auto write_stats = [&](int kb) {
+      for (int idx = threadIdx.x; idx < role.qg * 32; idx += kWaves * 64) {
+        const int qt = idx / 32, jj = idx % 32;
+        float mm = -INFINITY, ss = 0.0f;
+        for (int st = 0; st < role.nstreams; ++st) {
+          const float2 v = s_stat[kb & 1][st * role.qg + qt][jj];
+          lse_merge2(mm, ss, v.x, v.y, 1.0f);
+        }
+        // (max, sum) in logit units: max z = m / log2(e)
+        out[static_cast<size_t>(kb) * Mpad + (4 * round + qt) * 32 + jj] = float2{mm * kLn2, ss};
+      }
+    };
     // up to kBuffers - 1 later stages are in flight while a stage is
     // multiplied; the query rows are waited for once, with stage 0, so that
     // no load of the compiler's own is pending inside the stage loop
-    stage_issue<D>(kbase, key0, n, s_k, wave);
+    issue(s_k);
     half8 qr[D / 16];
     const int qrow = role.qtile * 32 + j;
     if (role.active) load_rows<D>(qbase, qrow, qrow < M, qr);
     wait_loads<0>();
-    for (int st = 1; st < S::kBuffers - 1 && st < nstages; ++st)
-      stage_issue<D>(kbase, key0 + st * S::kKeys, n, s_k + st * S::kBytes, wave);
+    for (int g = 1; g < S::kBuffers - 1 && g < nst; ++g) issue(s_k + g * S::kBytes);
     float m = -INFINITY, sum = 0.0f;  // m in base-2 units (logit * scale * log2 e)
-    for (int st0 = 0; st0 < nstages; st0 += S::kBuffers) {
+    int ckb = run.kb0, cst = 0;       // the stage being multiplied: stage cst of block ckb
+    int pending = -1;                 // a block whose per-wave stats wait in s_stat
+    for (int g0 = 0; g0 < nst; g0 += S::kBuffers) {
 #pragma unroll
       for (int b = 0; b < S::kBuffers; ++b) {
-        const int st = st0 + b;  // stage st lives in buffer b
-        if (st >= nstages) break;
-        wait_stage<D>(min(S::kBuffers - 2, nstages - 1 - st));  // later stages may still be loading
-        // every thread's pieces of stage st have landed, and every wave is done
-        // with stage st - 1, whose buffer the next issue overwrites
+        const int g = g0 + b;  // stage g of the run lives in buffer b
+        if (g >= nst) break;
+        wait_stage<D>(min(S::kBuffers - 2, nst - 1 - g));  // later stages may still be loading
+        // every thread's pieces of stage g have landed, every wave is done
+        // with stage g - 1, whose buffer the next issue overwrites, and has
+        // written the stats of a block that ended there
         lds_barrier();
-        if (st + S::kBuffers - 1 < nstages)
-          stage_issue<D>(kbase, key0 + (st + S::kBuffers - 1) * S::kKeys, n,
-                         s_k + ((b + S::kBuffers - 1) % S::kBuffers) * S::kBytes, wave);
-        if (!role.active) continue;
-        const int ts = key0 + st * S::kKeys;  // first key of the stage
+        if (g + S::kBuffers - 1 < nst) issue(s_k + ((b + S::kBuffers - 1) % S::kBuffers) * S::kBytes);
+        if (pending >= 0) {
+          write_stats(pending);
+          pending = -1;
+        }
+        if (role.active) {
+          const int ts = ckb * kBlockKeys + cst * S::kKeys;  // first key of the stage
 #pragma unroll
-        for (int ti = 0; ti < S::kTiles; ++ti) {
-          // this wave's tiles: global tile index = stream (mod nstreams, a power of two)
-          const int t0 = ts + ti * 32;
-          if (((st * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
-          half8 kr[D / 16];
-          stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
-          floatx16 acc{};
+          for (int ti = 0; ti < S::kTiles; ++ti) {
+            // this wave's tiles: tile index in the block = stream (mod nstreams, a power of two)
+            const int t0 = ts + ti * 32;
+            if (((cst * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
+            half8 kr[D / 16];
+            stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
+            floatx16 acc{};
 #pragma unroll
-          for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[s], qr[s], acc, 0, 0, 0);
-          if (t0 + 32 <= n) tile_update<false>(acc, alpha, t0, hf, n, m, sum);
-          else tile_update<true>(acc, alpha, t0, hf, n, m, sum);
+            for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kr[s], qr[s], acc, 0, 0, 0);
+            if (t0 + 32 <= n) tile_update<false>(acc, alpha, t0, hf, n, m, sum);
+            else tile_update<true>(acc, alpha, t0, hf, n, m, sum);
+          }
+        }
+        if (++cst == run.stages(ckb)) {  // the end of block ckb
+          if (role.active) {
+            // the two lane-halves saw different keys of the same query
+            lse_merge2(m, sum, __shfl_xor(m, 32), __shfl_xor(sum, 32), 1.0f);
+            if (hf == 0) s_stat[ckb & 1][wave][j] = float2{m, sum};
+          }
+          m = -INFINITY;
+          sum = 0.0f;
+          pending = ckb;
+          cst = 0;
+          ++ckb;
         }
       }
     }
-    if (role.active) {
-      // the two lane-halves saw different keys of the same query
-      lse_merge2(m, sum, __shfl_xor(m, 32), __shfl_xor(sum, 32), 1.0f);
-      if (hf == 0) s_stat[wave][j] = float2{m, sum};
-    }
-    __syncthreads();
-    // merge the streams of each query in stream order; m to z units
-    for (int idx = threadIdx.x; idx < role.qg * 32; idx += kWaves * 64) {
-      const int qt = idx / 32, jj = idx % 32;
-      float mm = -INFINITY, ss = 0.0f;
-      for (int st = 0; st < role.nstreams; ++st) {
-        const float2 v = s_stat[st * role.qg + qt][jj];
-        lse_merge2(mm, ss, v.x, v.y, 1.0f);
-      }
-      // (max, sum) in logit units: max z = m / log2(e)
-      pstat[(static_cast<size_t>(lh) * nkb + kb) * Mpad + (4 * round + qt) * 32 + jj] = float2{mm * kLn2, ss};
-    }
-    __syncthreads();
+    lds_barrier();
+    if (pending >= 0) write_stats(pending);
+    __syncthreads();  // the next round's first loads overwrite the first stage buffers
   }
 }
 
@@ -365,33 +437,41 @@ __global__ __launch_bounds__(256) void attn_merge(const float2* __restrict__ pst
   cstat[idx] = row < M ? mm + __logf(ss) : INFINITY;  // padding rows: exp(z - inf) = 0
 }
 
-// grid (L*H, key blocks); colsum[lh * n + t] = sum over the group's rows of p[row, t].
-// Logits with queries as MFMA rows: a lane holds 16 rows of one key and sums
-// their probabilities, the two lane-halves are added by a shuffle, and the
-// query tiles of a stage are added in tile order from shared memory one stage
-// later (rounds of query tiles add onto the stored sums in round order).
+// grid: LH * R workgroups, as attn_stats; colsum[lh * n + t] = sum over the
+// group's rows of p[row, t].  Logits with queries as MFMA rows: a lane holds
+// 16 rows of one key and sums their probabilities, the two lane-halves are
+// added by a shuffle, and the query tiles of a stage are added in tile order
+// from shared memory one stage later (rounds of query tiles add onto the
+// stored sums in round order).
 template <int D>
 __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Stage<D>::kWavesPerSimd))) void attn_colsum(
     const uint16_t* __restrict__ k, const uint16_t* __restrict__ q, int n, int H, int Hq, int W, float scale,
-    const float* __restrict__ cstat, float* __restrict__ colsum) {
+    int runs, const float* __restrict__ cstat, float* __restrict__ colsum) {
   using S = Stage<D>;
-  const int lh = blockIdx.x, kb = blockIdx.y;
-  const int l = lh / H, h = lh % H, G = Hq / H, M = G * W, MT = (M + 31) / 32, Mpad = MT * 32;
+  const int G = Hq / H, M = G * W, MT = (M + 31) / 32, Mpad = MT * 32;
   const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);  // uniform per wave
   const int lane = threadIdx.x & 63, hf = lane >> 5, j = lane & 31;
+  const float alpha = scale * kLog2e;
+  const BlockRun<D> run(n, static_cast<int>(gridDim.x) / runs, runs);
+  const int lh = run.lh, l = lh / H, h = lh % H, nst = run.nst;
   const uint16_t* kbase = k + static_cast<size_t>(lh) * n * D;
   const uint16_t* qbase = q + (static_cast<size_t>(l) * Hq + static_cast<size_t>(h) * G) * W * D;
   float* out = colsum + static_cast<size_t>(lh) * n;
-  const float alpha = scale * kLog2e;
-  const int key0 = kb * kBlockKeys;
-  const int nstages = (min(n - key0, kBlockKeys) + S::kKeys - 1) / S::kKeys;
   __shared__ __align__(16) uint8_t s_k[S::kBuffers * S::kBytes];
   __shared__ float s_part[2][kWaves][S::kKeys];  // per stage (double-buffered), per wave, per key
   uint32_t raddr[D / 16];
   lane_addresses<D>(s_k, raddr);
   for (int round = 0; 4 * round < MT; ++round) {
     const WaveRole role = wave_role(MT, round, wave);
-    stage_issue<D>(kbase, key0, n, s_k, wave);
+    int ikb = run.kb0, ist = 0;  // the next stage to issue: stage ist of block ikb
+    auto issue = [&](uint8_t* buf) {
+      stage_issue<D>(kbase, ikb * kBlockKeys + ist * S::kKeys, n, buf, wave);
+      if (++ist == run.stages(ikb)) {
+        ist = 0;
+        ++ikb;
+      }
+    };
+    issue(s_k);
     half8 qr[D / 16];
     float beta[16];  // c * log2(e) of the lane's 16 rows; +inf for padding rows
     // padding rows of a partial query tile: their zero queries can still make
@@ -408,64 +488,73 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
         if (role.qtile * 32 + acc_row(r, hf) >= M) valid_rows &= ~(1u << r);
       }
     }
-    // adds the query tiles' partial sums of stage st (tile order) onto the
-    // stored sums (round order); thread i owns key i of every stage
-    auto flush = [&](int st) {
+    // the stage whose partial sums wait in s_part: its first key, its index
+    // in the run and its stage index in its block
+    int fl_t0 = 0, fl_g = 0, fl_cst = 0;
+    // adds the query tiles' partial sums of that stage (tile order) onto the
+    // stored sums (round order); thread i owns key i of the stage
+    auto flush = [&]() {
       const int i = threadIdx.x;
-      const int t = key0 + st * S::kKeys + i;
+      const int t = fl_t0 + i;
       if (i < S::kKeys && t < n) {
-        const int stream = (st * S::kTiles + i / 32) & (role.nstreams - 1);
-        float v = s_part[st & 1][stream * role.qg][i];
-        for (int qt = 1; qt < role.qg; ++qt) v += s_part[st & 1][stream * role.qg + qt][i];
+        const int stream = (fl_cst * S::kTiles + i / 32) & (role.nstreams - 1);
+        float v = s_part[fl_g & 1][stream * role.qg][i];
+        for (int qt = 1; qt < role.qg; ++qt) v += s_part[fl_g & 1][stream * role.qg + qt][i];
         out[t] = round == 0 ? v : out[t] + v;
       }
     };
     // the query rows and row constants are waited for once, with stage 0;
     // up to kBuffers - 1 later stages are in flight while a stage is multiplied
     wait_loads<0>();
-    for (int st = 1; st < S::kBuffers - 1 && st < nstages; ++st)
-      stage_issue<D>(kbase, key0 + st * S::kKeys, n, s_k + st * S::kBytes, wave);
-    for (int st0 = 0; st0 < nstages; st0 += S::kBuffers) {
+    for (int g = 1; g < S::kBuffers - 1 && g < nst; ++g) issue(s_k + g * S::kBytes);
+    int ckb = run.kb0, cst = 0;  // the stage being multiplied: stage cst of block ckb
+    for (int g0 = 0; g0 < nst; g0 += S::kBuffers) {
 #pragma unroll
       for (int b = 0; b < S::kBuffers; ++b) {
-        const int st = st0 + b;  // stage st lives in buffer b
-        if (st >= nstages) break;
-        wait_stage<D>(min(S::kBuffers - 2, nstages - 1 - st));  // later stages may still be loading
-        // stage st has landed everywhere; every wave is done with stage st - 1
+        const int g = g0 + b;  // stage g of the run lives in buffer b
+        if (g >= nst) break;
+        wait_stage<D>(min(S::kBuffers - 2, nst - 1 - g));  // later stages may still be loading
+        // stage g has landed everywhere; every wave is done with stage g - 1
         // (its buffer is reloaded next) and has written its partial sums
         lds_barrier();
-        if (st + S::kBuffers - 1 < nstages)
-          stage_issue<D>(kbase, key0 + (st + S::kBuffers - 1) * S::kKeys, n,
-                         s_k + ((b + S::kBuffers - 1) % S::kBuffers) * S::kBytes, wave);
-        if (st > 0) flush(st - 1);
-        if (!role.active) continue;
-        float* part = s_part[st & 1][wave];
-        const int ts = key0 + st * S::kKeys;
+        if (g + S::kBuffers - 1 < nst) issue(s_k + ((b + S::kBuffers - 1) % S::kBuffers) * S::kBytes);
+        if (g > 0) flush();
+        const int ts = ckb * kBlockKeys + cst * S::kKeys;  // first key of the stage
+        if (role.active) {
+          float* part = s_part[g & 1][wave];
 #pragma unroll
-        for (int ti = 0; ti < S::kTiles; ++ti) {
-          const int t0 = ts + ti * 32;
-          if (((st * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
-          half8 kr[D / 16];
-          stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
-          floatx16 acc{};
+          for (int ti = 0; ti < S::kTiles; ++ti) {
+            const int t0 = ts + ti * 32;
+            if (((cst * S::kTiles + ti) & (role.nstreams - 1)) != role.stream || t0 >= n) continue;
+            half8 kr[D / 16];
+            stage_rows<D>(raddr, b * S::kBytes + ti * S::kTileBytes, kr);
+            floatx16 acc{};
 #pragma unroll
-          for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[s], kr[s], acc, 0, 0, 0);
-          // sum over the lane's 16 rows of p = 2^(acc * alpha - beta), then over both lane-halves
-          float e[16];
+            for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(qr[s], kr[s], acc, 0, 0, 0);
+            // sum over the lane's 16 rows of p = 2^(acc * alpha - beta), then over both lane-halves
+            float e[16];
 #pragma unroll
-          for (int r = 0; r < 16; ++r) e[r] = exp2_fast(__builtin_fmaf(acc[r], alpha, -beta[r]));
-          if (padded) {
+            for (int r = 0; r < 16; ++r) e[r] = exp2_fast(__builtin_fmaf(acc[r], alpha, -beta[r]));
+            if (padded) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) e[r] = (valid_rows >> r) & 1u ? e[r] : 0.0f;
+              for (int r = 0; r < 16; ++r) e[r] = (valid_rows >> r) & 1u ? e[r] : 0.0f;
+            }
+            float p = tree_sum<16>(e);
+            p += __shfl_xor(p, 32);  // the other lane-half holds the other 16 rows
+            if (hf == 0) part[ti * 32 + j] = p;
           }
-          float p = tree_sum<16>(e);
-          p += __shfl_xor(p, 32);  // the other lane-half holds the other 16 rows
-          if (hf == 0) part[ti * 32 + j] = p;
+        }
+        fl_t0 = ts;
+        fl_g = g;
+        fl_cst = cst;
+        if (++cst == run.stages(ckb)) {
+          cst = 0;
+          ++ckb;
         }
       }
     }
     lds_barrier();
-    flush(nstages - 1);
+    flush();
     __syncthreads();  // the next round's first loads overwrite the first stage buffers
   }
 }
@@ -524,14 +613,18 @@ template <int D>
 hipError_t launch_d(const Geometry& g, const AttnShape& s, int Hq, int W, const uint16_t* k, const uint16_t* q,
                     float2* pstat, float* cstat, float* colsum, hipStream_t stream) {
   const float scale = static_cast<float>(1.0 / sqrt(static_cast<double>(D)));
-  const dim3 grid(s.LH, s.nkb);
-  attn_stats<D><<<grid, kWaves * 64, 0, stream>>>(k, q, g.n, g.H, Hq, W, scale, pstat);
+  // a pair's key blocks in runs of about kRunBlocks, each run one workgroup;
+  // workgroup w takes pair w % LH, so the workgroups in flight read many pairs
+  const int runs = (s.nkb + kRunBlocks - 1) / kRunBlocks;
+  if (static_cast<int64_t>(s.LH) * runs > INT32_MAX) return hipErrorInvalidValue;
+  const int grid = s.LH * runs;
+  attn_stats<D><<<grid, kWaves * 64, 0, stream>>>(k, q, g.n, g.H, Hq, W, scale, runs, pstat);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   attn_merge<<<(s.LH * s.Mpad + 255) / 256, 256, 0, stream>>>(pstat, s.LH, s.nkb, s.Mpad, s.M, cstat);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  attn_colsum<D><<<grid, kWaves * 64, 0, stream>>>(k, q, g.n, g.H, Hq, W, scale, cstat, colsum);
+  attn_colsum<D><<<grid, kWaves * 64, 0, stream>>>(k, q, g.n, g.H, Hq, W, scale, runs, cstat, colsum);
   return hipGetLastError();
 }
 
