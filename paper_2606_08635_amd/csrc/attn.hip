@@ -47,7 +47,10 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 // d = 128 and 3-7 % at d = 256), and runs of two blocks per workgroup (one
 // block per workgroup was 1.5-2.5 % slower, four blocks lost 13 % at d = 256
 // for want of workgroups; 2048-key blocks instead of runs came within 2 %
-// of runs of two, with different partial sums).
+// of runs of two, with different partial sums), four waves per workgroup
+// (eight waves, two query-tile streams each, with two to four 16 KB stage
+// buffers: 9-20 % slower although they keep up to 96 KB of keys in flight
+// per CU against 64 KB).
 #ifndef SKV_ATTN_BUFFERS
 #define SKV_ATTN_BUFFERS 2  // key stages resident per workgroup (d <= 128)
 #endif
@@ -64,7 +67,10 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 #define SKV_ATTN_RUN_BLOCKS 2
 #endif
 
-constexpr int kWaves = 4;
+#ifndef SKV_ATTN_WAVES
+#define SKV_ATTN_WAVES 4
+#endif
+constexpr int kWaves = SKV_ATTN_WAVES;  // waves per workgroup
 constexpr int kBlockKeys = 1024;                 // keys per block of partial results
 constexpr int kRunBlocks = SKV_ATTN_RUN_BLOCKS;  // key blocks a workgroup walks
 constexpr float kLog2e = 1.4426950408889634f;
@@ -123,6 +129,7 @@ struct Stage {
   static constexpr int kBuffers = D >= 256 ? SKV_ATTN_BUFFERS_D256 : SKV_ATTN_BUFFERS;
   // register budget: four waves per SIMD up to d = 128 (no spills), two at d = 256
   static constexpr int kWavesPerSimd = D >= 256 ? 2 : 4;
+  static_assert(kWaves == 4 || kWaves == 8, "four or eight waves per workgroup");
   static_assert(kPieces * kWaves * 64 == kKeys * kCpr, "a stage is whole 16-byte pieces per thread");
   static_assert(kBlockKeys % kKeys == 0, "a block is whole stages");
   static_assert(kBuffers >= 2 && kBuffers <= 4 && (kBuffers - 2) * kPieces < 64, "outstanding loads fit vmcnt");
@@ -212,7 +219,7 @@ __device__ __forceinline__ void stage_rows(const uint32_t (&addr)[D / 16], uint3
   for (int s = 0; s < D / 16; ++s) out[s] = *reinterpret_cast<lds_half8_ptr>(static_cast<uintptr_t>(addr[s] + offset));
 }
 
-// Work of wave w in round r: query tiles r*4 .. r*4+qg-1 (qg = min(4, MT - 4r))
+// Work of wave w in round r: query tiles r*kWaves .. + qg-1 (qg = min(kWaves, MT - r*kWaves))
 // are spread over the waves; with fewer than 4 tiles the key tiles of the
 // block are split into nstreams interleaved streams so every wave works.
 struct WaveRole {
@@ -221,10 +228,11 @@ struct WaveRole {
 };
 __device__ __forceinline__ WaveRole wave_role(int MT, int round, int wave) {
   WaveRole r;
-  r.qg = min(4, MT - 4 * round);
-  r.nstreams = r.qg == 1 ? 4 : r.qg == 2 ? 2 : 1;
+  r.qg = min(kWaves, MT - kWaves * round);
+  r.nstreams = 1;  // the largest power of two with qg * nstreams <= kWaves
+  while (2 * r.nstreams * r.qg <= kWaves) r.nstreams *= 2;
   r.active = wave < r.qg * r.nstreams;
-  r.qtile = 4 * round + wave % r.qg;
+  r.qtile = kWaves * round + wave % r.qg;
   r.stream = wave / r.qg;
   return r;
 }
@@ -336,7 +344,7 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
   __shared__ float2 s_stat[2][kWaves][32];  // per block parity, wave and query
   uint32_t raddr[D / 16];
   lane_addresses<D>(s_k, raddr);
-  for (int round = 0; 4 * round < MT; ++round) {
+  for (int round = 0; kWaves * round < MT; ++round) {
     const WaveRole role = wave_role(MT, round, wave);
     // the next stage to issue: stage ist of block ikb
     int ikb = run.kb0, ist = 0;
@@ -357,7 +365,7 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
           lse_merge2(mm, ss, v.x, v.y, 1.0f);
         }
         // (max, sum) in logit units: max z = m / log2(e)
-        out[static_cast<size_t>(kb) * Mpad + (4 * round + qt) * 32 + jj] = float2{mm * kLn2, ss};
+        out[static_cast<size_t>(kb) * Mpad + (kWaves * round + qt) * 32 + jj] = float2{mm * kLn2, ss};
       }
     };
     // up to kBuffers - 1 later stages are in flight while a stage is
@@ -461,7 +469,7 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
   __shared__ float s_part[2][kWaves][S::kKeys];  // per stage (double-buffered), per wave, per key
   uint32_t raddr[D / 16];
   lane_addresses<D>(s_k, raddr);
-  for (int round = 0; 4 * round < MT; ++round) {
+  for (int round = 0; kWaves * round < MT; ++round) {
     const WaveRole role = wave_role(MT, round, wave);
     int ikb = run.kb0, ist = 0;  // the next stage to issue: stage ist of block ikb
     auto issue = [&](uint8_t* buf) {
