@@ -518,9 +518,10 @@ def run_quant(args, w):
 
 def run_select(args):
     """The tier cut alone (skv_assign_tiers / skv_assign_batch) on seeded
-    random scores: the resident form at 32768 tokens, the general form at
-    2^21, and 64 requests of 2048 tokens per request vs batched.  HIP events,
-    mean over the timed launches."""
+    random scores: the resident form at 32768 tokens; past it, the split form
+    (workspace given) and the one-workgroup form (no workspace) at 65536 and
+    2^21 tokens; and 64 requests of 2048 tokens per request vs batched.  HIP
+    events, mean over the timed launches."""
     import torch
 
     from paper_2606_08635_amd import skv
@@ -542,12 +543,15 @@ def run_select(args):
         return sum(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(args.steps)) / args.steps
 
     out = {}
-    for n in (32768, 1 << 21):
+    for n in (32768, 65536, 1 << 21):
         cfg = skv.config(32, 8, 128, n, 0.5, decay=1e-4)
         sc = torch.rand(n, generator=g, device=dev, dtype=torch.float64)
         tier = torch.empty(n, dtype=torch.uint8, device=dev)
-        ms = timed(lambda: skv.assign_tiers(cfg, sc, tier))
-        out[f"single_n{n}"] = {"ms": round(ms, 4), "tokens_per_s": round(n / (ms / 1e3), 1)}
+        ws = torch.empty(skv.workspace_size(cfg), dtype=torch.uint8, device=dev)
+        forms = [("single", None)] if n <= 32768 else [("split", ws), ("one_workgroup", None)]
+        for name, w in forms:
+            ms = timed(lambda: skv.assign_tiers(cfg, sc, tier, ws=w))
+            out[f"{name}_n{n}"] = {"ms": round(ms, 4), "tokens_per_s": round(n / (ms / 1e3), 1)}
     lens = [2048] * 64
     cfgs = [skv.config(32, 8, 128, n, 0.5) for n in lens]
     bcfg = skv.config(32, 8, 128, max(lens), 0.5)
@@ -722,7 +726,7 @@ def main():
 
     def step(ev=None):
         calls = [lambda: skv.score(cfg, k, v, q_obs, codec.scores, codec.ws),
-                 lambda: skv.assign_tiers(cfg, codec.scores, codec.tier),
+                 lambda: skv.assign_tiers(cfg, codec.scores, codec.tier, ws=codec.ws),
                  lambda: skv.pack(cfg, k, v, codec.tier, codec.payload, codec.status[0:1]),
                  lambda: skv.link(rx, codec.payload, codec.payload_bytes, staging),
                  lambda: skv.unpack(cfg, rx, kc, vc, bt, bs, codec.status[1:2])]

@@ -200,7 +200,8 @@ skv_status skv_plan_tiers(const skv_config* cfg, skv_plan* out);
 skv_status skv_payload_size(const skv_config* cfg, uint64_t* bytes);
 
 /* Host only.  Device workspace bytes needed by skv_prepare, skv_score and
- * skv_assign_tiers for cfg (the decay table plus scratch). */
+ * skv_assign_tiers for cfg (the decay table plus scratch; the scratch of the
+ * tier cut, for rows past 32768 tokens, shares the area of the score's). */
 skv_status skv_workspace_size(const skv_config* cfg, uint64_t* bytes);
 
 /* Fills the decay table exp(-lambda Delta) (attention and recency modes) or
@@ -259,7 +260,13 @@ skv_status skv_score_static(const skv_config* cfg, const void* k, const void* v,
  * descending composite key ((bits(score) >> 20) << 21) | t, i.e. by score cut
  * to 32 fraction bits with ties going to the more recent token, and the first
  * n_fp16 get FP16, the next n_int8 INT8, the next n_int4 INT4, the rest DROP.
- * One workgroup, radix select; ws is not used and may be NULL. */
+ * Radix select over six digits of the key.  Rows of at most 32768 non-sink
+ * tokens run on one workgroup and do not use ws.  Longer rows run split over
+ * the GPU (one counting launch per digit) when ws is the request's workspace
+ * (skv_workspace_size(cfg) bytes; its scratch area after the decay table is
+ * overwritten, the decay table is not), or on one workgroup when ws is NULL;
+ * both give the same tier map.  Calls that share a workspace (this one,
+ * skv_score) must be ordered on one stream. */
 skv_status skv_assign_tiers(const skv_config* cfg, const double* score, uint8_t* tier, void* ws,
                             hipStream_t stream);
 

@@ -10,7 +10,9 @@
 // radix select per cut over six digits (11, 11 and 10 bits of the key's high
 // word, then the same of its low word), all three sharing each pass over the
 // keys, then classifies every token against them.
-//   * One workgroup of 1024 threads.
+//   * One workgroup of 1024 threads, or, for rows past the resident form
+//     when the caller gives scratch, the split form below (one launch per
+//     pass over the whole GPU; the same cut keys).
 //   * Resident form (at most 32 non-sink tokens per thread): the scores are
 //     loaded once and the high words of the keys kept in LDS (128 KiB, next
 //     to the 24 KiB of histograms).  The three high-word passes and the
@@ -293,6 +295,169 @@ __device__ __forceinline__ void assign_row(const double* __restrict__ score, uin
 
 bool fits_resident(int n, int n_sink) { return n - n_sink <= kResident * kSelThreads; }
 
+// Split form, for rows past the resident form when the caller gives scratch:
+// the same six passes and digit choices, but each pass is one launch over
+// the whole GPU.  sel_count gives every workgroup kBatch * 1024 consecutive
+// non-sink tokens, counts their digits into shared-memory histograms and adds
+// the nonzero bins into the row's histogram in device memory (integer
+// atomics, so the totals do not depend on the order); sel_choose (one
+// workgroup) picks each cut's digit from the totals exactly as the one-
+// workgroup form does and clears the histogram of the next pass; sel_classify
+// then assigns every token against the three cut keys.  The cut keys, and so
+// the tier map, equal the one-workgroup form's.
+struct SelScratch {
+  uint32_t hist[2][3][kBins];  // per pass parity: the cut groups' digit counts
+  uint64_t prefix[3];          // decided key bits of each cut
+  uint32_t rank[3];            // remaining rank inside the prefix
+};
+
+// Cut j reads the histogram of the first cut (in cut order) with a nonzero
+// rank and the same decided prefix.
+__device__ __forceinline__ int cut_group(const uint64_t (&prefix)[3], const uint32_t (&rank)[3], int j) {
+  for (int i = 0; i < j; ++i)
+    if (rank[i] != 0 && prefix[i] == prefix[j]) return i;
+  return j;
+}
+
+// grid: one workgroup (256 threads); the cuts start undecided at their ranks
+__global__ __launch_bounds__(256) void sel_init(SelScratch* __restrict__ sc, int n16, int n8, int n4) {
+  if (threadIdx.x < 3) {
+    sc->prefix[threadIdx.x] = 0;
+    sc->rank[threadIdx.x] = static_cast<uint32_t>(threadIdx.x == 0 ? n16 : threadIdx.x == 1 ? n16 + n8 : n16 + n8 + n4);
+  }
+  for (int i = threadIdx.x; i < 3 * kBins; i += 256) (&sc->hist[0][0][0])[i] = 0;
+}
+
+// grid: ceil((n - n_sink) / (kBatch * 1024)) workgroups; pass `pass`
+__global__ __launch_bounds__(kSelThreads) void sel_count(const double* __restrict__ score, int n, int n_sink,
+                                                         SelScratch* __restrict__ sc, int pass) {
+  __shared__ uint32_t hist[3][kBins];
+  const int tid = threadIdx.x, lane = tid & 63;
+  uint64_t pre[3];
+  uint32_t rk[3];
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    pre[j] = sc->prefix[j];
+    rk[j] = sc->rank[j];
+  }
+  const bool act0 = rk[0] != 0, act1 = rk[1] != 0 && cut_group(pre, rk, 1) == 1,
+             act2 = rk[2] != 0 && cut_group(pre, rk, 2) == 2;
+  const int low = digit_low_bit(pass), hi_bit = pass == 0 ? 64 : digit_low_bit(pass - 1);
+  const uint32_t mask = (1u << (hi_bit - low)) - 1u;
+  const uint64_t decided = pass == 0 ? 0ull : (~0ull << hi_bit);
+  // this workgroup's tokens: base + u * 1024, u < kBatch
+  const int base = n_sink + blockIdx.x * kBatch * kSelThreads + tid;
+  double v[kBatch];
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u) {
+    const int t = base + u * kSelThreads;
+    v[u] = t < n ? score[t] : 0.0;
+  }
+  for (int i = tid; i < 3 * kBins; i += kSelThreads) (&hist[0][0])[i] = 0;
+  __syncthreads();
+  if (pass == 0) {
+    // every prefix is empty: the first cut of nonzero rank leads the only
+    // group, and neighbouring tokens mostly share the exponent digit
+    const int lead = act0 ? 0 : act1 ? 1 : 2;
+    const bool any = act0 || act1 || act2;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int t = base + u * kSelThreads;
+      const uint32_t bin = static_cast<uint32_t>(rank_key(v[u], t) >> low) & mask;
+      wave_count(hist[lead], any && t < n, bin, lane);
+    }
+  } else {
+    RunCounter r0, r1, r2;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int t = base + u * kSelThreads;
+      if (t >= n) break;
+      const uint64_t c = rank_key(v[u], t);
+      const uint32_t bin = static_cast<uint32_t>(c >> low) & mask;
+      const uint64_t d = c & decided;
+      if (act0 && d == pre[0]) r0.add(hist[0], bin);
+      if (act1 && d == pre[1]) r1.add(hist[1], bin);
+      if (act2 && d == pre[2]) r2.add(hist[2], bin);
+    }
+    flush(hist[0], r0.bin, r0.count);
+    flush(hist[1], r1.bin, r1.count);
+    flush(hist[2], r2.bin, r2.count);
+  }
+  __syncthreads();
+  uint32_t* out = &sc->hist[pass & 1][0][0];
+  for (int i = tid; i < 3 * kBins; i += kSelThreads) {
+    const uint32_t c = (&hist[0][0])[i];
+    if (c) atomicAdd(&out[i], c);
+  }
+}
+
+// grid: one workgroup; fixes each cut's digit of pass `pass`
+__global__ __launch_bounds__(kSelThreads) void sel_choose(SelScratch* __restrict__ sc, int pass) {
+  __shared__ __attribute__((aligned(16))) SelectState st;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint32_t* in = &sc->hist[pass & 1][0][0];
+  for (int i = tid; i < 3 * kBins; i += kSelThreads) (&st.hist[0][0])[i] = in[i];
+  if (tid < 3) {
+    uint64_t pre[3];
+    uint32_t rk[3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      pre[j] = sc->prefix[j];
+      rk[j] = sc->rank[j];
+    }
+    st.prefix[tid] = pre[tid];
+    st.rank[tid] = rk[tid];
+    st.group[tid] = cut_group(pre, rk, tid);
+  }
+  __syncthreads();
+  choose_digits(st, digit_low_bit(pass), lane, wave);
+  __syncthreads();
+  if (tid < 3) {
+    sc->prefix[tid] = st.prefix[tid];
+    sc->rank[tid] = st.rank[tid];
+  }
+  // the next pass counts into the other histogram
+  uint32_t* next = &sc->hist[(pass + 1) & 1][0][0];
+  for (int i = tid; i < 3 * kBins; i += kSelThreads) next[i] = 0;
+}
+
+// grid: ceil(n / 1024) workgroups; st.prefix[j] is now the cut key itself
+// (keys are distinct), and a cut of rank 0 admits no key
+__global__ __launch_bounds__(kSelThreads) void sel_classify(const double* __restrict__ score,
+                                                            uint8_t* __restrict__ tier, int n, int n_sink,
+                                                            const SelScratch* __restrict__ sc, bool has1, bool has2,
+                                                            bool has3) {
+  const int t = blockIdx.x * kSelThreads + threadIdx.x;
+  if (t >= n) return;
+  uint8_t tr = kFP16;  // sinks
+  if (t >= n_sink) {
+    const uint64_t c = rank_key(score[t], t);
+    tr = (has1 && c >= sc->prefix[0]) ? kFP16 : (has2 && c >= sc->prefix[1]) ? kINT8
+         : (has3 && c >= sc->prefix[2])                                       ? kINT4
+                                                                               : kDROP;
+  }
+  tier[t] = tr;
+}
+
+hipError_t launch_assign_split(const Geometry& g, const double* score, uint8_t* tier, SelScratch* sc,
+                               hipStream_t stream) {
+  sel_init<<<1, 256, 0, stream>>>(sc, g.n16, g.n8, g.n4);
+  hipError_t e = hipGetLastError();
+  const int per = kBatch * kSelThreads;
+  const int blocks = (g.n - g.n_sink + per - 1) / per;
+  for (int pass = 0; pass < kPasses && e == hipSuccess; ++pass) {
+    sel_count<<<blocks, kSelThreads, 0, stream>>>(score, g.n, g.n_sink, sc, pass);
+    e = hipGetLastError();
+    if (e != hipSuccess) break;
+    sel_choose<<<1, kSelThreads, 0, stream>>>(sc, pass);
+    e = hipGetLastError();
+  }
+  if (e != hipSuccess) return e;
+  sel_classify<<<(g.n + kSelThreads - 1) / kSelThreads, kSelThreads, 0, stream>>>(
+      score, tier, g.n, g.n_sink, sc, g.n16 != 0, g.n16 + g.n8 != 0, g.n16 + g.n8 + g.n4 != 0);
+  return hipGetLastError();
+}
+
 template <bool RESIDENT>
 __global__ __launch_bounds__(kSelThreads) void assign_tiers(const double* __restrict__ score,
                                                             uint8_t* __restrict__ tier, int n,
@@ -333,10 +498,16 @@ hipError_t launch_assign_batch(const ScoreBatchArgs& a, bool resident, hipStream
   return hipGetLastError();
 }
 
-hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier,
+uint64_t assign_scratch_bytes(int32_t n) {
+  return fits_resident(n, 0) ? 0 : (sizeof(SelScratch) + 255) / 256 * 256;
+}
+
+hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier, void* scratch,
                          hipStream_t stream) {
   if (fits_resident(g.n, g.n_sink))
     assign_tiers<true><<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
+  else if (scratch != nullptr)
+    return launch_assign_split(g, score, tier, static_cast<SelScratch*>(scratch), stream);
   else
     assign_tiers<false><<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
   return hipGetLastError();

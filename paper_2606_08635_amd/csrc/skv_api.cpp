@@ -178,11 +178,14 @@ uint64_t scratch_bytes(const skv_config* c) {
   g.H = c->num_kv_heads;
   g.d = c->head_dim;
   g.n = c->num_tokens;
+  uint64_t score_bytes = 0;
   switch (c->score_mode) {
-    case SKV_SCORE_KVNORM: return kvnorm_scratch_bytes(g);
-    case SKV_SCORE_ATTN: return attn_scratch_bytes(g, c->num_q_heads, c->obs_window);
-    default: return 0;
+    case SKV_SCORE_KVNORM: score_bytes = kvnorm_scratch_bytes(g); break;
+    case SKV_SCORE_ATTN: score_bytes = attn_scratch_bytes(g, c->num_q_heads, c->obs_window); break;
+    default: break;
   }
+  // tier assignment reuses the area after scoring (stream order)
+  return std::max(score_bytes, assign_scratch_bytes(g.n));
 }
 
 inline skv_status launched(hipError_t e) { return e == hipSuccess ? SKV_OK : SKV_ERR_DEVICE; }
@@ -729,12 +732,12 @@ skv_status skv_assign_batch(const skv_config* cfg, const skv_score_request* reqs
 
 skv_status skv_assign_tiers(const skv_config* cfg, const double* score, uint8_t* tier, void* ws,
                             hipStream_t stream) {
-  (void)ws;
   Geometry g;
   const skv_status st = make_geometry(cfg, &g, nullptr);
   if (st != SKV_OK) return st;
-  if (!dev_ptr_ok(score) || !dev_ptr_ok(tier)) return SKV_ERR_INVALID_ARG;
-  return launched(launch_assign(g, score, tier, stream));
+  if (!dev_ptr_ok(score) || !dev_ptr_ok(tier) || (ws != nullptr && !dev_ptr_ok(ws))) return SKV_ERR_INVALID_ARG;
+  void* scratch = ws == nullptr ? nullptr : static_cast<uint8_t*>(ws) + decay_table_bytes(cfg);
+  return launched(launch_assign(g, score, tier, scratch, stream));
 }
 
 skv_status skv_pack_batch(const skv_config* cfg, const skv_request* reqs, int32_t count,

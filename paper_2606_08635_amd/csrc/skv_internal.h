@@ -101,7 +101,11 @@ hipError_t launch_score_attn(const Geometry& g, int32_t Hq, int32_t W, const uin
 uint64_t kvnorm_scratch_bytes(const Geometry& g);
 uint64_t attn_scratch_bytes(const Geometry& g, int32_t Hq, int32_t W);
 
-hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier,
+// Tier assignment of one request.  Rows past the resident form's 32768
+// non-sink tokens run split over the GPU when scratch (assign_scratch_bytes,
+// 256-byte aligned device memory) is given, else on one workgroup.
+uint64_t assign_scratch_bytes(int32_t n);
+hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier, void* scratch,
                          hipStream_t stream);
 
 // Batched scoring and assignment (every request shares L, H, d and the

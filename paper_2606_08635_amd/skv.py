@@ -215,9 +215,13 @@ def score_static(cfg: Config, k: torch.Tensor, v: torch.Tensor, q_obs: Optional[
                                   _stream(stream)), "skv_score_static")
 
 
-def assign_tiers(cfg: Config, scores: torch.Tensor, tier: torch.Tensor, stream=None):
+def assign_tiers(cfg: Config, scores: torch.Tensor, tier: torch.Tensor, stream=None,
+                 ws: Optional[torch.Tensor] = None):
+    """ws: the request's workspace (workspace_size bytes), or None; with it,
+    rows past 32768 non-sink tokens are cut by the split form."""
+    wsp = ctypes.c_void_p(None) if ws is None else _dev(ws, torch.uint8, workspace_size(cfg), "ws")
     _check(lib().skv_assign_tiers(ctypes.byref(cfg), _dev(scores, torch.float64, cfg.num_tokens, "score"),
-                                  _dev(tier, torch.uint8, cfg.num_tokens, "tier"), ctypes.c_void_p(None),
+                                  _dev(tier, torch.uint8, cfg.num_tokens, "tier"), wsp,
                                   _stream(stream)), "skv_assign_tiers")
 
 
@@ -519,7 +523,7 @@ class Codec:
 
     def encode(self, k, v, q_obs=None, stream=None):
         score(self.cfg, k, v, q_obs, self.scores, self.ws, stream)
-        assign_tiers(self.cfg, self.scores, self.tier, stream)
+        assign_tiers(self.cfg, self.scores, self.tier, stream, ws=self.ws)
         pack(self.cfg, k, v, self.tier, self.payload, self.status[0:1], stream)
         return self.payload
 

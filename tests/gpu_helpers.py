@@ -28,7 +28,7 @@ def gpu_encode(cfg, k, v, q=None, scores=None, tier=None):
     skv.score(cfg, k, v, q, codec.scores, codec.ws)
     if scores is not None:
         codec.scores.copy_(torch.from_numpy(scores).to(k.device))
-    skv.assign_tiers(cfg, codec.scores, codec.tier)
+    skv.assign_tiers(cfg, codec.scores, codec.tier, ws=codec.ws)
     if tier is not None:
         codec.tier.copy_(torch.from_numpy(tier).to(k.device))
     skv.pack(cfg, k, v, codec.tier, codec.payload, codec.status[0:1])

@@ -91,6 +91,11 @@ def test_workspace_size(lib):
     assert ws >= 8 * 32768 and ws % 256 == 0
     c.score_mode = skv.RECENCY
     assert skv.workspace_size(c) == 8 * 32768
+    # past 32768 tokens the split tier cut needs its scratch after the decay
+    # table: two histograms of 3 x 2048 counts plus the cuts' state, 256-aligned
+    for n in (32769, 1 << 21):
+        c = skv.config(1, 1, 32, n, 0.5, score_mode=skv.RECENCY, decay=1e-4)
+        assert skv.workspace_size(c) == (8 * n + 255) // 256 * 256 + 49408
 
 
 def test_host_side_argument_errors(lib):

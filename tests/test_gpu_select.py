@@ -1,8 +1,10 @@
-"""Tier assignment on both sides of its two kernel forms vs the oracle.
+"""Tier assignment on both sides of its kernel forms vs the oracle.
 
 Rows with at most 32 * 1024 non-sink tokens keep the high words of their
 ranking keys resident in LDS; longer rows recompute the keys from the scores on
-every pass.  Each side of that boundary is checked bit for bit against the
+every pass, on one workgroup (no workspace) or split over the GPU (the
+request's workspace given: one counting launch per pass).  Each side of that
+boundary, and both forms past it, are checked bit for bit against the
 oracle's tier map, for one map and for per-layer grouped maps, with score sets
 that spread over many binades, that tie in the keys' high 32 bits and differ
 only below them, and that hold exact ties, non-positive scores and NaN.
@@ -39,10 +41,49 @@ def test_single_map_at_the_form_boundary(kind, b, extra):
     cfg, ocfg = configs(1, 1, 32, n, b, 3, num_sink=n_sink)
     key = _scores(kind, n, seed=n + len(kind))
     want = oracle.assign(ocfg, key)
+    dkey = torch.from_numpy(key).cuda()
+    ws = torch.empty(skv.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    for w in (None, ws):
+        tier = torch.empty(n, dtype=torch.uint8, device="cuda")
+        skv.assign_tiers(cfg, dkey, tier, ws=w)
+        torch.cuda.synchronize()
+        assert np.array_equal(tier.cpu().numpy(), want), "workspace given" if w is not None else "no workspace"
+
+
+# plans whose cuts coincide or vanish: no FP16 cut (b = 0.15, 3-tier: INT4 +
+# DROP), INT8 + INT4 only, FP16 + INT8 (the INT4 cut equals the INT8 one), all
+# FP16 (every cut at the last rank), 2-tier with and without DROP
+@pytest.mark.parametrize("b,tiers", [(0.15, 3), (0.4, 3), (0.7, 3), (1.0, 3), (0.3, 2), (0.6, 2)])
+@pytest.mark.parametrize("kind", ["binades", "low_word", "ties"])
+def test_split_form_long_rows(kind, b, tiers):
+    n_sink = 37
+    n = (1 << 18) + 12345
+    say(f"split assign n={n} sinks={n_sink} b={b} tiers={tiers} scores={kind}")
+    # decay 1e-3: 2 lambda (n - 1) = 549 stays inside the decay table's range (<= 700)
+    cfg, ocfg = configs(1, 1, 32, n, b, tiers, num_sink=n_sink, decay=1e-3)
+    key = _scores(kind, n, seed=n + 31 * len(kind) + tiers)
+    want = oracle.assign(ocfg, key)
+    ws = torch.empty(skv.workspace_size(cfg), dtype=torch.uint8, device="cuda")
     tier = torch.empty(n, dtype=torch.uint8, device="cuda")
-    skv.assign_tiers(cfg, torch.from_numpy(key).cuda(), tier)
+    skv.assign_tiers(cfg, torch.from_numpy(key).cuda(), tier, ws=ws)
     torch.cuda.synchronize()
     assert np.array_equal(tier.cpu().numpy(), want)
+
+
+def test_split_form_decayed_kvnorm_scores_twice():
+    """Realistic keys (KV-norm times decay: exponents ordered by position),
+    two requests in a row through one workspace, the second shorter."""
+    for n, b in ((200_003, 0.5), (70_001, 0.3)):
+        say(f"split assign, decayed scores, n={n} b={b}")
+        cfg, ocfg = configs(1, 2, 64, n, b, 3, decay=0.0015)
+        k, v = workloads.make_kv(1, 2, n, 64, seed=n)
+        key = oracle.score(ocfg, u16(k), u16(v))
+        want = oracle.assign(ocfg, key)
+        ws = torch.empty(skv.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+        tier = torch.empty(n, dtype=torch.uint8, device="cuda")
+        skv.assign_tiers(cfg, torch.from_numpy(key).cuda(), tier, ws=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(tier.cpu().numpy(), want)
 
 
 @pytest.mark.parametrize("kind", ["binades", "low_word", "ties"])
