@@ -63,3 +63,35 @@ def test_captured_step_replays_match_eager(q8, q4):
         assert torch.equal(codec.payload, ref.payload), seed
         assert torch.equal(kc.view(torch.int16), rkc.view(torch.int16)), seed
         assert torch.equal(vc.view(torch.int16), rvc.view(torch.int16)), seed
+
+
+def test_captured_split_tier_cut_replays_match_oracle():
+    """The split tier cut (a row past 32768 non-sink tokens, workspace given:
+    14 launches that clear their histograms with kernels, not memsets) under
+    capture: every replay on new scores equals the oracle's map."""
+    n = 100_003
+    say(f"graph capture, split tier cut n={n}")
+    cfg, ocfg = configs(1, 1, 32, n, 0.4, 3, decay=1e-3)
+    ws = torch.empty(skv.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    scores = torch.empty(n, dtype=torch.float64, device="cuda")
+    tier = torch.empty(n, dtype=torch.uint8, device="cuda")
+    rng = np.random.default_rng(5)
+    scores.copy_(torch.from_numpy(rng.random(n)))
+    skv.assign_tiers(cfg, scores, tier, ws=ws)  # warm-up outside capture
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        skv.assign_tiers(cfg, scores, tier, ws=ws)
+    torch.cuda.synchronize()
+    for seed in (21, 22, 23):
+        key = np.ldexp(1.0 + np.random.default_rng(seed).random(n), np.random.default_rng(seed + 1).integers(-30, 30, n))
+        scores.copy_(torch.from_numpy(key))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(tier.cpu().numpy(), oracle.assign(ocfg, key)), seed
+        # eager work between replays on the same buffers
+        skv.assign_tiers(cfg, scores, tier, ws=ws)
+        torch.cuda.synchronize()
