@@ -413,8 +413,13 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
         }
         if (++cst == run.stages(ckb)) {  // the end of block ckb
           if (role.active) {
-            // the two lane-halves saw different keys of the same query
-            lse_merge2(m, sum, __shfl_xor(m, 32), __shfl_xor(sum, 32), 1.0f);
+            // the two lane-halves saw different keys of the same query:
+            // the lower half's stats merged with the upper half's
+            const LanePair mp = lane_pair32(__builtin_bit_cast(uint32_t, m));
+            const LanePair sp = lane_pair32(__builtin_bit_cast(uint32_t, sum));
+            m = __builtin_bit_cast(float, mp.lo);
+            sum = __builtin_bit_cast(float, sp.lo);
+            lse_merge2(m, sum, __builtin_bit_cast(float, mp.hi), __builtin_bit_cast(float, sp.hi), 1.0f);
             if (hf == 0) s_stat[ckb & 1][wave][j] = float2{m, sum};
           }
           m = -INFINITY;
@@ -548,7 +553,9 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(Sta
               for (int r = 0; r < 16; ++r) e[r] = (valid_rows >> r) & 1u ? e[r] : 0.0f;
             }
             float p = tree_sum<16>(e);
-            p += __shfl_xor(p, 32);  // the other lane-half holds the other 16 rows
+            // the other lane-half holds the other 16 rows: lower + upper
+            const LanePair pp = lane_pair32(__builtin_bit_cast(uint32_t, p));
+            p = __builtin_bit_cast(float, pp.lo) + __builtin_bit_cast(float, pp.hi);
             if (hf == 0) part[ti * 32 + j] = p;
           }
         }

@@ -59,13 +59,34 @@ __device__ __forceinline__ uint32_t dpp_mov(uint32_t v) {
   return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), CTRL, 0xF, 0xF, true));
 }
 
+// The values of lanes i and i ^ 16 (lane_pair16) or i and i ^ 32
+// (lane_pair32), the lower lane's as lo, in both lanes: gfx950's
+// v_permlane16_swap / v_permlane32_swap, one vector instruction each instead
+// of a shuffle through the LDS unit and its address arithmetic.  The lanes
+// exchanged stay inside aligned groups of 32 (lane_pair16) or the wave
+// (lane_pair32), and every lane of such a group in use must be active.
+struct LanePair {
+  uint32_t lo, hi;
+};
+__device__ __forceinline__ LanePair lane_pair16(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return LanePair{r[0], r[1]};
+}
+__device__ __forceinline__ LanePair lane_pair32(uint32_t v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return LanePair{r[0], r[1]};
+}
+
 // Maximum over aligned groups of G consecutive lanes (G = 4, 8, 16 or 32);
 // every lane of a group receives the group's maximum.  Must be called with
 // every lane of each group active.
 template <int G>
 __device__ __forceinline__ uint32_t group_max(uint32_t v) {
   static_assert(G == 4 || G == 8 || G == 16 || G == 32, "group size");
-  if constexpr (G == 32) v = max(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 16)));
+  if constexpr (G == 32) {
+    const LanePair p = lane_pair16(v);  // lanes i and i ^ 16
+    v = max(p.lo, p.hi);
+  }
   if constexpr (G >= 16) v = max(v, dpp_mov<0x140>(v));  // row_mirror: lane i <-> 15-i
   if constexpr (G >= 8) v = max(v, dpp_mov<0x141>(v));   // row_half_mirror: i <-> 7-i
   v = max(v, dpp_mov<0xB1>(v));                          // quad_perm [1,0,3,2]

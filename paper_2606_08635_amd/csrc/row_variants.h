@@ -65,7 +65,10 @@ __device__ __forceinline__ uint32_t group_reduce(uint32_t v, int gl) {
     if (gl >= 16) v = op(v, dpp_mov<0x140>(v));  // row_mirror
   }
   if constexpr (LPR >= 32) {
-    if (gl >= 32) v = op(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 16)));
+    if (gl >= 32) {
+      const LanePair p = lane_pair16(v);  // lanes i and i ^ 16
+      v = op(p.lo, p.hi);
+    }
   }
   return v;
 }

@@ -203,7 +203,12 @@ __device__ __forceinline__ double group_sum_f64(double x) {
   x += dpp_f64<0x4E>(x);                          // quad_perm [2,3,0,1]
   if constexpr (G >= 8) x += dpp_f64<0x141>(x);   // row_half_mirror
   if constexpr (G >= 16) x += dpp_f64<0x140>(x);  // row_mirror
-  if constexpr (G == 32) x += __shfl_xor(x, 16);
+  if constexpr (G == 32) {  // lanes i and i ^ 16: lower + upper, the same sum in both (addition commutes)
+    const uint64_t b = __builtin_bit_cast(uint64_t, x);
+    const LanePair lo = lane_pair16(static_cast<uint32_t>(b)), hi = lane_pair16(static_cast<uint32_t>(b >> 32));
+    x = __builtin_bit_cast(double, (static_cast<uint64_t>(hi.lo) << 32) | lo.lo) +
+        __builtin_bit_cast(double, (static_cast<uint64_t>(hi.hi) << 32) | lo.hi);
+  }
   return x;
 }
 
