@@ -520,7 +520,8 @@ def run_select(args):
     """The tier cut alone (skv_assign_tiers / skv_assign_batch) on seeded
     random scores: the resident form at 32768 tokens; past it, the split form
     (workspace given) and the one-workgroup form (no workspace) at 65536 and
-    2^21 tokens; and 64 requests of 2048 tokens per request vs batched.  HIP
+    2^21 tokens; 32 per-layer maps of 2^21 tokens (split form); and 64
+    requests of 2048 tokens per request vs batched.  HIP
     events, mean over the timed launches."""
     import torch
 
@@ -552,6 +553,19 @@ def run_select(args):
         for name, w in forms:
             ms = timed(lambda: skv.assign_tiers(cfg, sc, tier, ws=w))
             out[f"{name}_n{n}"] = {"ms": round(ms, 4), "tokens_per_s": round(n / (ms / 1e3), 1)}
+    # grouped maps past the resident form: 32 per-layer rows of 2^21 tokens,
+    # cut together by the split form
+    import numpy as np
+    n = 1 << 21
+    gcfg = skv.config(32, 8, 128, n, 0.5, decay=1e-4)
+    groups = skv.Groups(skv.GROUP_LAYER, np.linspace(0.7, 0.3, 32).astype(np.float32))
+    gws = torch.empty(skv.group_workspace_size(gcfg, groups), dtype=torch.uint8, device=dev)
+    skv.prepare_groups(gcfg, groups, gws)
+    gsc = torch.rand(32 * n, generator=g, device=dev, dtype=torch.float64)
+    gtier = torch.empty(32 * n, dtype=torch.uint8, device=dev)
+    ms = timed(lambda: skv.assign_groups(gcfg, groups, gsc, gtier, gws))
+    out["groups_layer_32x2097152_split"] = {"ms": round(ms, 4), "tokens_per_s": round(32 * n / (ms / 1e3), 1)}
+    del gws, gsc, gtier
     lens = [2048] * 64
     cfgs = [skv.config(32, 8, 128, n, 0.5) for n in lens]
     bcfg = skv.config(32, 8, 128, max(lens), 0.5)

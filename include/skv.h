@@ -498,9 +498,13 @@ skv_status skv_score_groups(const skv_config* cfg, const skv_group_spec* spec, c
                             const void* q_obs, double* score, void* ws, hipStream_t stream);
 
 /* Assigns every group's tiers from its scores (skv_assign_tiers per group, with
- * the group's plan): tier is uint8[G][n].  One workgroup per group. */
+ * the group's plan): tier is uint8[G][n].  Rows of at most 32768 tokens: one
+ * workgroup per group.  Longer rows run split over the GPU, their scratch in
+ * the workspace's area after the tables (overwritten; the decay, group and
+ * segment tables are not), so calls sharing a workspace must be ordered on
+ * one stream. */
 skv_status skv_assign_groups(const skv_config* cfg, const skv_group_spec* spec, const double* score,
-                             uint8_t* tier, const void* ws, hipStream_t stream);
+                             uint8_t* tier, void* ws, hipStream_t stream);
 
 /* Packs the grouped payload (rows quantized exactly as skv_pack; segment
  * (l, K/V, h) uses its group's map).  tier: uint8[G][n], each map on its

@@ -298,17 +298,42 @@ bool fits_resident(int n, int n_sink) { return n - n_sink <= kResident * kSelThr
 // Split form, for rows past the resident form when the caller gives scratch:
 // the same six passes and digit choices, but each pass is one launch over
 // the whole GPU.  sel_count gives every workgroup kBatch * 1024 consecutive
-// non-sink tokens, counts their digits into shared-memory histograms and adds
-// the nonzero bins into the row's histogram in device memory (integer
-// atomics, so the totals do not depend on the order); sel_choose (one
-// workgroup) picks each cut's digit from the totals exactly as the one-
-// workgroup form does and clears the histogram of the next pass; sel_classify
-// then assigns every token against the three cut keys.  The cut keys, and so
-// the tier map, equal the one-workgroup form's.
+// non-sink tokens of one row, counts their digits into shared-memory
+// histograms and adds the nonzero bins into the row's histogram in device
+// memory (integer atomics, so the totals do not depend on the order);
+// sel_choose (one workgroup per row) picks each cut's digit from the totals
+// exactly as the one-workgroup form does and clears the histogram of the
+// next pass; sel_classify then assigns every token against the three cut
+// keys.  The cut keys, and so the tier maps, equal the one-workgroup form's.
+// Rows share n; row r's scores and tiers sit at r * n, and its counts come
+// from the group table (8 words per row: sinks, fp16, int8, int4, ...) or,
+// for a single row, from the arguments.
 struct SelScratch {
   uint32_t hist[2][3][kBins];  // per pass parity: the cut groups' digit counts
   uint64_t prefix[3];          // decided key bits of each cut
   uint32_t rank[3];            // remaining rank inside the prefix
+};
+
+struct SelRows {
+  const double* score;
+  uint8_t* tier;
+  int n;
+  const uint32_t* table;  // per-row counts, or null: the counts below
+  int n_sink, n16, n8, n4;
+  __device__ __forceinline__ void counts(int row, int& s, int& c16, int& c8, int& c4) const {
+    if (table != nullptr) {
+      const uint32_t* e = table + 8 * row;
+      s = static_cast<int>(e[0]);
+      c16 = static_cast<int>(e[1]);
+      c8 = static_cast<int>(e[2]);
+      c4 = static_cast<int>(e[3]);
+    } else {
+      s = n_sink;
+      c16 = n16;
+      c8 = n8;
+      c4 = n4;
+    }
+  }
 };
 
 // Cut j reads the histogram of the first cut (in cut order) with a nonzero
@@ -319,19 +344,31 @@ __device__ __forceinline__ int cut_group(const uint64_t (&prefix)[3], const uint
   return j;
 }
 
-// grid: one workgroup (256 threads); the cuts start undecided at their ranks
-__global__ __launch_bounds__(256) void sel_init(SelScratch* __restrict__ sc, int n16, int n8, int n4) {
+// grid: one workgroup (256 threads) per row; the cuts start undecided at
+// their ranks
+__global__ __launch_bounds__(256) void sel_init(const SelRows a, SelScratch* __restrict__ scratch) {
+  SelScratch* sc = scratch + blockIdx.x;
+  int s, c16, c8, c4;
+  a.counts(blockIdx.x, s, c16, c8, c4);
   if (threadIdx.x < 3) {
     sc->prefix[threadIdx.x] = 0;
-    sc->rank[threadIdx.x] = static_cast<uint32_t>(threadIdx.x == 0 ? n16 : threadIdx.x == 1 ? n16 + n8 : n16 + n8 + n4);
+    sc->rank[threadIdx.x] = static_cast<uint32_t>(threadIdx.x == 0 ? c16 : threadIdx.x == 1 ? c16 + c8 : c16 + c8 + c4);
   }
   for (int i = threadIdx.x; i < 3 * kBins; i += 256) (&sc->hist[0][0][0])[i] = 0;
 }
 
-// grid: ceil((n - n_sink) / (kBatch * 1024)) workgroups; pass `pass`
-__global__ __launch_bounds__(kSelThreads) void sel_count(const double* __restrict__ score, int n, int n_sink,
-                                                         SelScratch* __restrict__ sc, int pass) {
+// grid: (ceil(n / (kBatch * 1024)), rows); pass `pass`.  Workgroups past a
+// row's last non-sink token count nothing.
+__global__ __launch_bounds__(kSelThreads) void sel_count(const SelRows a, SelScratch* __restrict__ scratch,
+                                                         int pass) {
   __shared__ uint32_t hist[3][kBins];
+  const int row = blockIdx.y;
+  SelScratch* sc = scratch + row;
+  int n_sink, c16, c8, c4;
+  a.counts(row, n_sink, c16, c8, c4);
+  const int n = a.n;
+  if (n_sink + static_cast<int>(blockIdx.x) * kBatch * kSelThreads >= n) return;  // uniform per workgroup
+  const double* __restrict__ score = a.score + static_cast<size_t>(row) * n;
   const int tid = threadIdx.x, lane = tid & 63;
   uint64_t pre[3];
   uint32_t rk[3];
@@ -391,9 +428,10 @@ __global__ __launch_bounds__(kSelThreads) void sel_count(const double* __restric
   }
 }
 
-// grid: one workgroup; fixes each cut's digit of pass `pass`
-__global__ __launch_bounds__(kSelThreads) void sel_choose(SelScratch* __restrict__ sc, int pass) {
+// grid: one workgroup per row; fixes each cut's digit of pass `pass`
+__global__ __launch_bounds__(kSelThreads) void sel_choose(SelScratch* __restrict__ scratch, int pass) {
   __shared__ __attribute__((aligned(16))) SelectState st;
+  SelScratch* sc = scratch + blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const uint32_t* in = &sc->hist[pass & 1][0][0];
   for (int i = tid; i < 3 * kBins; i += kSelThreads) (&st.hist[0][0])[i] = in[i];
@@ -421,40 +459,41 @@ __global__ __launch_bounds__(kSelThreads) void sel_choose(SelScratch* __restrict
   for (int i = tid; i < 3 * kBins; i += kSelThreads) next[i] = 0;
 }
 
-// grid: ceil(n / 1024) workgroups; st.prefix[j] is now the cut key itself
+// grid: (ceil(n / 1024), rows); sc->prefix[j] is now the cut key itself
 // (keys are distinct), and a cut of rank 0 admits no key
-__global__ __launch_bounds__(kSelThreads) void sel_classify(const double* __restrict__ score,
-                                                            uint8_t* __restrict__ tier, int n, int n_sink,
-                                                            const SelScratch* __restrict__ sc, bool has1, bool has2,
-                                                            bool has3) {
+__global__ __launch_bounds__(kSelThreads) void sel_classify(const SelRows a,
+                                                            const SelScratch* __restrict__ scratch) {
+  const int row = blockIdx.y, n = a.n;
   const int t = blockIdx.x * kSelThreads + threadIdx.x;
   if (t >= n) return;
+  const SelScratch* sc = scratch + row;
+  int n_sink, c16, c8, c4;
+  a.counts(row, n_sink, c16, c8, c4);
+  const bool has1 = c16 != 0, has2 = c16 + c8 != 0, has3 = c16 + c8 + c4 != 0;
   uint8_t tr = kFP16;  // sinks
   if (t >= n_sink) {
-    const uint64_t c = rank_key(score[t], t);
+    const uint64_t c = rank_key(a.score[static_cast<size_t>(row) * n + t], t);
     tr = (has1 && c >= sc->prefix[0]) ? kFP16 : (has2 && c >= sc->prefix[1]) ? kINT8
          : (has3 && c >= sc->prefix[2])                                       ? kINT4
                                                                                : kDROP;
   }
-  tier[t] = tr;
+  a.tier[static_cast<size_t>(row) * n + t] = tr;
 }
 
-hipError_t launch_assign_split(const Geometry& g, const double* score, uint8_t* tier, SelScratch* sc,
-                               hipStream_t stream) {
-  sel_init<<<1, 256, 0, stream>>>(sc, g.n16, g.n8, g.n4);
+hipError_t launch_assign_split(const SelRows& a, int rows, SelScratch* sc, hipStream_t stream) {
+  sel_init<<<rows, 256, 0, stream>>>(a, sc);
   hipError_t e = hipGetLastError();
   const int per = kBatch * kSelThreads;
-  const int blocks = (g.n - g.n_sink + per - 1) / per;
+  const dim3 count_grid((a.n + per - 1) / per, rows);
   for (int pass = 0; pass < kPasses && e == hipSuccess; ++pass) {
-    sel_count<<<blocks, kSelThreads, 0, stream>>>(score, g.n, g.n_sink, sc, pass);
+    sel_count<<<count_grid, kSelThreads, 0, stream>>>(a, sc, pass);
     e = hipGetLastError();
     if (e != hipSuccess) break;
-    sel_choose<<<1, kSelThreads, 0, stream>>>(sc, pass);
+    sel_choose<<<rows, kSelThreads, 0, stream>>>(sc, pass);
     e = hipGetLastError();
   }
   if (e != hipSuccess) return e;
-  sel_classify<<<(g.n + kSelThreads - 1) / kSelThreads, kSelThreads, 0, stream>>>(
-      score, tier, g.n, g.n_sink, sc, g.n16 != 0, g.n16 + g.n8 != 0, g.n16 + g.n8 + g.n4 != 0);
+  sel_classify<<<dim3((a.n + kSelThreads - 1) / kSelThreads, rows), kSelThreads, 0, stream>>>(a, sc);
   return hipGetLastError();
 }
 
@@ -466,17 +505,15 @@ __global__ __launch_bounds__(kSelThreads) void assign_tiers(const double* __rest
 }
 
 // grid: one workgroup per group; plan counts from the group table
-// (u32 [sinks, fp16, int8, int4, ...], 32 bytes per group).
-// RESIDENT requires n <= kResident * kSelThreads (every group's sinks count
-// down from there).
-template <bool RESIDENT>
+// (u32 [sinks, fp16, int8, int4, ...], 32 bytes per group).  Rows of at most
+// kResident * kSelThreads tokens (longer rows take the split form).
 __global__ __launch_bounds__(kSelThreads) void assign_tiers_groups(const double* __restrict__ score,
                                                                    uint8_t* __restrict__ tier, int n,
                                                                    const uint32_t* __restrict__ group_table) {
   const uint32_t* e = group_table + 8 * blockIdx.x;
   const size_t row = static_cast<size_t>(blockIdx.x) * n;
-  assign_row<RESIDENT>(score + row, tier + row, n, static_cast<int>(e[0]), static_cast<int>(e[1]), static_cast<int>(e[2]),
-             static_cast<int>(e[3]));
+  assign_row<true>(score + row, tier + row, n, static_cast<int>(e[0]), static_cast<int>(e[1]), static_cast<int>(e[2]),
+                   static_cast<int>(e[3]));
 }
 
 // grid: one workgroup per request of the launch
@@ -498,8 +535,8 @@ hipError_t launch_assign_batch(const ScoreBatchArgs& a, bool resident, hipStream
   return hipGetLastError();
 }
 
-uint64_t assign_scratch_bytes(int32_t n) {
-  return fits_resident(n, 0) ? 0 : (sizeof(SelScratch) + 255) / 256 * 256;
+uint64_t assign_scratch_bytes(int32_t n, int32_t rows) {
+  return fits_resident(n, 0) ? 0 : (static_cast<uint64_t>(rows) * sizeof(SelScratch) + 255) / 256 * 256;
 }
 
 hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier, void* scratch,
@@ -507,18 +544,21 @@ hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier, 
   if (fits_resident(g.n, g.n_sink))
     assign_tiers<true><<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
   else if (scratch != nullptr)
-    return launch_assign_split(g, score, tier, static_cast<SelScratch*>(scratch), stream);
+    return launch_assign_split(SelRows{score, tier, g.n, nullptr, g.n_sink, g.n16, g.n8, g.n4}, 1,
+                               static_cast<SelScratch*>(scratch), stream);
   else
     assign_tiers<false><<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
   return hipGetLastError();
 }
 
 hipError_t launch_assign_groups(int32_t G, int32_t n, const uint32_t* group_table, const double* score,
-                                uint8_t* tier, hipStream_t stream) {
-  if (fits_resident(n, 0))
-    assign_tiers_groups<true><<<G, kSelThreads, 0, stream>>>(score, tier, n, group_table);
-  else
-    assign_tiers_groups<false><<<G, kSelThreads, 0, stream>>>(score, tier, n, group_table);
+                                uint8_t* tier, void* scratch, hipStream_t stream) {
+  if (!fits_resident(n, 0)) {
+    if (scratch == nullptr) return hipErrorInvalidValue;
+    return launch_assign_split(SelRows{score, tier, n, group_table, 0, 0, 0, 0}, G,
+                               static_cast<SelScratch*>(scratch), stream);
+  }
+  assign_tiers_groups<<<G, kSelThreads, 0, stream>>>(score, tier, n, group_table);
   return hipGetLastError();
 }
 

@@ -185,7 +185,7 @@ uint64_t scratch_bytes(const skv_config* c) {
     default: break;
   }
   // tier assignment reuses the area after scoring (stream order)
-  return std::max(score_bytes, assign_scratch_bytes(g.n));
+  return std::max(score_bytes, assign_scratch_bytes(g.n, 1));
 }
 
 inline skv_status launched(hipError_t e) { return e == hipSuccess ? SKV_OK : SKV_ERR_DEVICE; }
@@ -418,6 +418,8 @@ skv_status group_host(const skv_config* cfg, const skv_group_spec* spec, GroupHo
   uint64_t scratch = 0;
   if (cfg->score_mode == SKV_SCORE_KVNORM) scratch = kvnorm_scratch_bytes_groups(geo, gran);
   if (cfg->score_mode == SKV_SCORE_ATTN) scratch = attn_scratch_bytes(geo, cfg->num_q_heads, cfg->obs_window);
+  // the split tier cut (rows past 32768 tokens) reuses the area after scoring
+  scratch = std::max(scratch, assign_scratch_bytes(gl.n, G));
   out->ws_total = out->ws_scratch_off + round_up_256(scratch);
   return SKV_OK;
 }
@@ -994,13 +996,14 @@ skv_status skv_score_groups(const skv_config* cfg, const skv_group_spec* spec, c
 }
 
 skv_status skv_assign_groups(const skv_config* cfg, const skv_group_spec* spec, const double* score,
-                             uint8_t* tier, const void* ws, hipStream_t stream) {
+                             uint8_t* tier, void* ws, hipStream_t stream) {
   GroupHost gh;
   const skv_status st = group_host(cfg, spec, &gh);
   if (st != SKV_OK) return st;
   if (!dev_ptr_ok(score) || tier == nullptr || !dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
   const GroupLaunch gl = group_launch(gh, ws);
-  return launched(launch_assign_groups(gl.G, gl.n, gl.group_table, score, tier, stream));
+  void* scratch = static_cast<uint8_t*>(ws) + gh.ws_scratch_off;
+  return launched(launch_assign_groups(gl.G, gl.n, gl.group_table, score, tier, scratch, stream));
 }
 
 skv_status skv_pack_groups(const skv_config* cfg, const skv_group_spec* spec, const void* k, const void* v,

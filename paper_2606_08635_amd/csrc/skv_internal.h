@@ -102,9 +102,10 @@ uint64_t kvnorm_scratch_bytes(const Geometry& g);
 uint64_t attn_scratch_bytes(const Geometry& g, int32_t Hq, int32_t W);
 
 // Tier assignment of one request.  Rows past the resident form's 32768
-// non-sink tokens run split over the GPU when scratch (assign_scratch_bytes,
-// 256-byte aligned device memory) is given, else on one workgroup.
-uint64_t assign_scratch_bytes(int32_t n);
+// non-sink tokens run split over the GPU when scratch (assign_scratch_bytes
+// for `rows` rows of n tokens, 256-byte aligned device memory) is given,
+// else on one workgroup per row.
+uint64_t assign_scratch_bytes(int32_t n, int32_t rows);
 hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier, void* scratch,
                          hipStream_t stream);
 
@@ -156,7 +157,7 @@ hipError_t launch_unpack_groups(const GroupLaunch& gl, const uint8_t* payload, u
                                 const int32_t* block_table, int32_t num_blocks, int32_t block_size,
                                 uint32_t* status, hipStream_t stream);
 hipError_t launch_assign_groups(int32_t G, int32_t n, const uint32_t* group_table, const double* score,
-                                uint8_t* tier, hipStream_t stream);
+                                uint8_t* tier, void* scratch, hipStream_t stream);
 uint64_t kvnorm_scratch_bytes_groups(const Geometry& g, int32_t gran);
 hipError_t launch_score_kvnorm_groups(const Geometry& g, int32_t gran, int32_t G, const uint16_t* k,
                                       const uint16_t* v, const double* w2, uint64_t* partial, double* score,

@@ -3,7 +3,8 @@
 Rows with at most 32 * 1024 non-sink tokens keep the high words of their
 ranking keys resident in LDS; longer rows recompute the keys from the scores on
 every pass, on one workgroup (no workspace) or split over the GPU (the
-request's workspace given: one counting launch per pass).  Each side of that
+request's workspace given: one counting launch per pass; grouped maps always
+take the split form past 32768 tokens, one row per group).  Each side of that
 boundary, and both forms past it, are checked bit for bit against the
 oracle's tier map, for one map and for per-layer grouped maps, with score sets
 that spread over many binades, that tie in the keys' high 32 bits and differ
@@ -103,3 +104,26 @@ def test_grouped_maps_at_the_form_boundary(kind, n):
     skv.assign_groups(cfg, groups, torch.from_numpy(key.ravel()).cuda(), tier, ws)
     torch.cuda.synchronize()
     assert np.array_equal(tier.cpu().numpy().reshape(L, n), want)
+
+
+@pytest.mark.parametrize("kind", ["binades", "low_word", "ties"])
+def test_split_form_per_head_maps(kind):
+    """Per-head maps (one group per (layer, KV head)) past the resident form:
+    eight rows cut together by the split form, budgets from all-FP16 down to
+    INT4 + DROP, each row's map equal to the oracle's."""
+    L, H, n = 2, 4, 70_001
+    say(f"grouped split assign L={L} H={H} n={n} scores={kind}")
+    cfg, ocfg = configs(L, H, 32, n, 0.4, 3, decay=1e-3)
+    gran = oracle.GRAN_HEAD
+    budgets = np.float32([1.0, 0.9, 0.6, 0.5, 0.4, 0.3, 0.2, 0.1])
+    groups = skv.Groups(gran, budgets)
+    key = _scores(kind, (L * H, n), seed=11 * n + len(kind))
+    want = oracle.assign_groups(ocfg, gran, key, budgets)
+    ws = torch.empty(skv.group_workspace_size(cfg, groups), dtype=torch.uint8, device="cuda")
+    skv.prepare_groups(cfg, groups, ws)
+    tier = torch.empty(L * H * n, dtype=torch.uint8, device="cuda")
+    skv.assign_groups(cfg, groups, torch.from_numpy(key.ravel()).cuda(), tier, ws)
+    torch.cuda.synchronize()
+    got = tier.cpu().numpy().reshape(L * H, n)
+    for g in range(L * H):
+        assert np.array_equal(got[g], want[g]), f"group {g} (b = {budgets[g]})"
