@@ -191,6 +191,21 @@ def test_upgrade_size_and_argument_errors(lib):
     assert L.skv_unpack_upgrade(by, odd, size, 10, 1, fake, fake, fake, 20, 16, fake, None) == skv.ERR_INVALID_ARG
 
 
+def test_grouped_workspace_holds_the_split_tier_cut(lib):
+    """Past 32768 tokens the grouped tier cut keeps one row of split-form
+    scratch per group (two 3 x 2048 count histograms and the cuts' state,
+    49192 bytes) after the tables; the recency score needs no other scratch,
+    so the workspace grows by exactly that, 256-aligned."""
+    for n in (32768, 32769, 100_000):
+        for gran, G in ((skv.GROUP_LAYER, 3), (skv.GROUP_HEAD, 6)):
+            c = skv.config(3, 2, 32, n, 0.5, score_mode=skv.RECENCY, decay=1e-3)
+            size = skv.group_workspace_size(c, skv.Groups(gran, None))
+            # decay table, group table (32 B per group), segment table (32 B per (layer, head))
+            tables = (8 * n + 255) // 256 * 256 + (32 * G + 255) // 256 * 256 + (32 * 6 + 255) // 256 * 256
+            extra = 0 if n <= 32768 else (G * 49192 + 255) // 256 * 256
+            assert size == tables + extra, (n, gran)
+
+
 @pytest.mark.parametrize("seed", range(3))
 def test_grouped_plans_and_sizes_match_oracle(lib, seed):
     rng = np.random.default_rng(100 + seed)
