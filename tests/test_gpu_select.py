@@ -127,3 +127,26 @@ def test_split_form_per_head_maps(kind):
     got = tier.cpu().numpy().reshape(L * H, n)
     for g in range(L * H):
         assert np.array_equal(got[g], want[g]), f"group {g} (b = {budgets[g]})"
+
+
+@pytest.mark.parametrize("tiers", [2, 3])
+@pytest.mark.parametrize("extra", [0, 200_000], ids=["resident", "split"])
+def test_budget_of_the_sinks_only_drops_every_other_token(tiers, extra):
+    """A budget that pays for the sinks alone: every cut has rank 0, so both
+    forms must leave the sinks FP16 and drop every other token."""
+    n_sink = 37
+    n = n_sink + 30_000 + extra
+    b = float(np.float32((4 * n_sink + 0.5) / (4 * n)))  # floor(4 b n) = 4 * n_sink: nothing left after the sinks
+    say(f"sinks-only budget n={n} b={b} tiers={tiers}")
+    cfg, ocfg = configs(1, 1, 32, n, b, tiers, num_sink=n_sink, decay=1e-3)
+    plan = skv.plan_tiers(cfg)
+    assert plan["n_fp16"] == plan["n_int8"] == plan["n_int4"] == 0 and plan["n_drop"] == n - n_sink
+    key = _scores("binades", n, seed=n)
+    want = oracle.assign(ocfg, key)
+    ws = torch.empty(skv.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+    tier = torch.empty(n, dtype=torch.uint8, device="cuda")
+    skv.assign_tiers(cfg, torch.from_numpy(key).cuda(), tier, ws=ws)
+    torch.cuda.synchronize()
+    got = tier.cpu().numpy()
+    assert np.array_equal(got, want)
+    assert (got[:n_sink] == oracle.FP16).all() and (got[n_sink:] == oracle.DROP).all()
