@@ -150,3 +150,42 @@ def test_budget_of_the_sinks_only_drops_every_other_token(tiers, extra):
     got = tier.cpu().numpy()
     assert np.array_equal(got, want)
     assert (got[:n_sink] == oracle.FP16).all() and (got[n_sink:] == oracle.DROP).all()
+
+
+def _random_case(rng):
+    """A random long row: length past the resident form, sinks, budget, tier
+    policy and score distribution (with heavy ties in some)."""
+    n = int(rng.integers(32_769, 400_000))
+    n_sink = int(rng.choice([0, 1, 37, int(rng.integers(0, 5_000))]))
+    tiers = int(rng.choice([2, 3]))
+    kind = str(rng.choice(["binades", "low_word", "ties", "few_values", "decayed"]))
+    if kind == "few_values":  # exact ties across the whole row
+        key = rng.choice(np.array([0.0, 1e-300, 0.5, 1.0, 2.0, np.inf]), n)
+    elif kind == "decayed":  # magnitudes times an exponential decay by position
+        key = rng.random(n) * np.exp(-float(rng.uniform(0, 1e-3)) * (n - 1 - np.arange(n)))
+    else:
+        key = _scores(kind, n, seed=int(rng.integers(1 << 30)))
+    return n, n_sink, tiers, kind, key
+
+
+def test_split_form_random_rows():
+    """Forty seeded random long rows through the split form (each with the
+    budget drawn until the sinks fit), every map equal to the oracle's."""
+    rng = np.random.default_rng(2606)
+    done = 0
+    while done < 40:
+        n, n_sink, tiers, kind, key = _random_case(rng)
+        b = float(np.float32(rng.uniform(0.0, 1.0)))
+        if not (0.0 < b <= 1.0) or 4 * n_sink > int(4 * np.float64(np.float32(b)) * n):
+            continue
+        say(f"random split assign #{done} n={n} sinks={n_sink} b={b} tiers={tiers} scores={kind}")
+        # decay 1e-4: 2 lambda (n - 1) < 80, inside the decay table's range (<= 700)
+        cfg, ocfg = configs(1, 1, 32, n, b, tiers, num_sink=n_sink, decay=1e-4)
+        want = oracle.assign(ocfg, key)
+        ws = torch.empty(skv.workspace_size(cfg), dtype=torch.uint8, device="cuda")
+        tier = torch.empty(n, dtype=torch.uint8, device="cuda")
+        skv.assign_tiers(cfg, torch.from_numpy(key).cuda(), tier, ws=ws)
+        torch.cuda.synchronize()
+        got = tier.cpu().numpy()
+        assert np.array_equal(got, want), f"case {done}: {int((got != want).sum())} tokens differ"
+        done += 1
