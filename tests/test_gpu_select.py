@@ -189,3 +189,29 @@ def test_split_form_random_rows():
         got = tier.cpu().numpy()
         assert np.array_equal(got, want), f"case {done}: {int((got != want).sum())} tokens differ"
         done += 1
+
+
+def test_split_form_random_grouped_rows():
+    """Twelve seeded random grouped cuts past the resident form (per layer or
+    per head, random budgets per group), every group's map equal to the
+    oracle's."""
+    rng = np.random.default_rng(9)
+    for case in range(12):
+        L, H = int(rng.integers(1, 4)), int(rng.integers(1, 5))
+        gran = int(rng.choice([oracle.GRAN_LAYER, oracle.GRAN_HEAD]))
+        n = int(rng.integers(32_769, 120_000))
+        tiers = int(rng.choice([2, 3]))
+        cfg, ocfg = configs(L, H, 32, n, 0.5, tiers, decay=1e-4)
+        G = oracle.group_count(ocfg, gran)
+        budgets = np.float32(rng.uniform(0.03, 1.0, G))
+        kind = str(rng.choice(["binades", "low_word", "ties"]))
+        key = _scores(kind, (G, n), seed=int(rng.integers(1 << 30)))
+        say(f"random grouped split assign #{case} L={L} H={H} gran={gran} n={n} tiers={tiers} scores={kind}")
+        want = oracle.assign_groups(ocfg, gran, key, budgets)
+        groups = skv.Groups(gran, budgets)
+        ws = torch.empty(skv.group_workspace_size(cfg, groups), dtype=torch.uint8, device="cuda")
+        skv.prepare_groups(cfg, groups, ws)
+        tier = torch.empty(G * n, dtype=torch.uint8, device="cuda")
+        skv.assign_groups(cfg, groups, torch.from_numpy(key.ravel()).cuda(), tier, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(tier.cpu().numpy().reshape(G, n), want), f"case {case}"
