@@ -231,7 +231,7 @@ def run_batch(args, w):
         skv.score_batch(bcfg, ks, vs, bscores, bws)
 
     def batched_assign():
-        skv.assign_batch(bcfg, bscores, btiers)
+        skv.assign_batch(bcfg, bscores, btiers, ws=bws)
 
     def batched():
         skv.pack_batch(base, ks, vs, btiers, pays, pst)
@@ -520,9 +520,9 @@ def run_select(args):
     """The tier cut alone (skv_assign_tiers / skv_assign_batch) on seeded
     random scores: the resident form at 32768 tokens; past it, the split form
     (workspace given) and the one-workgroup form (no workspace) at 65536 and
-    2^21 tokens; 32 per-layer maps of 2^21 tokens (split form); and 64
-    requests of 2048 tokens per request vs batched.  HIP
-    events, mean over the timed launches."""
+    2^21 tokens; 32 per-layer maps of 2^21 tokens (split form); 64
+    requests of 2048 tokens per request vs batched; and 8 batched requests of
+    2^18 tokens in both forms.  HIP events, mean over the timed launches."""
     import torch
 
     from paper_2606_08635_amd import skv
@@ -578,6 +578,16 @@ def run_select(args):
 
     out["per_request_64x2048"] = {"ms": round(timed(per_request), 4)}
     out["batched_64x2048"] = {"ms": round(timed(lambda: skv.assign_batch(bcfg, scores, tiers)), 4)}
+    # eight requests of 2^18 tokens: split form (workspace given) vs one
+    # workgroup per request
+    lens = [1 << 18] * 8
+    lcfg = skv.config(32, 8, 128, max(lens), 0.5, decay=1e-4)
+    scores = [torch.rand(n, generator=g, device=dev, dtype=torch.float64) for n in lens]
+    tiers = [torch.empty(n, dtype=torch.uint8, device=dev) for n in lens]
+    lws = torch.empty(skv.batch_workspace_size(lcfg, scores), dtype=torch.uint8, device=dev)
+    for name, w in (("split", lws), ("one_workgroup", None)):
+        ms = timed(lambda: skv.assign_batch(lcfg, scores, tiers, ws=w))
+        out[f"batched_8x262144_{name}"] = {"ms": round(ms, 4), "tokens_per_s": round(sum(lens) / (ms / 1e3), 1)}
     return out
 
 

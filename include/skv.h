@@ -343,10 +343,12 @@ typedef struct skv_score_request {
   uint8_t* tier;      /* uint8[n]: written by skv_assign_batch                 */
 } skv_score_request;
 
-/* Host only.  Workspace bytes of skv_score_batch for these requests: the
- * decay table of cfg (cfg->num_tokens entries, at least every request's n)
- * followed by each request's partial sums.  Errors as skv_score_batch's host
- * checks. */
+/* Host only.  Workspace bytes of skv_score_batch and skv_assign_batch for
+ * these requests: the decay table of cfg (cfg->num_tokens entries, at least
+ * every request's n) followed by the larger of each request's partial sums
+ * (KV-norm mode) and the split tier cut's select state (49192 bytes for each
+ * request longer than 32768 tokens, at most 48 of them).  Errors as
+ * skv_score_batch's host checks. */
 skv_status skv_batch_workspace_size(const skv_config* cfg, const skv_score_request* reqs, int32_t count,
                                     uint64_t* bytes);
 
@@ -364,9 +366,18 @@ skv_status skv_score_batch(const skv_config* cfg, const skv_score_request* reqs,
 
 /* Batched tier assignment (Sec. 2.3 Prop. 1; Sec. 4.4): each request's tier
  * map is exactly skv_assign_tiers' on its scores with the plan of cfg at its
- * own n (SKV_ERR_BUDGET if some request's sinks exceed its budget).  One
- * workgroup per request, one launch for up to 48 requests. */
-skv_status skv_assign_batch(const skv_config* cfg, const skv_score_request* reqs, int32_t count,
+ * own n (SKV_ERR_BUDGET if some request's sinks exceed its budget).  Requests
+ * of at most 32768 non-sink tokens take one workgroup each, one launch for up
+ * to 48 of them.  Longer requests, up to 48 per launch sequence, run split
+ * over the whole GPU (14 launches) when ws is given, else on one workgroup
+ * each; both give the same tier maps.  ws: NULL, or a workspace of
+ * skv_batch_workspace_size bytes for these requests (device memory, 16-byte
+ * aligned; its area after the decay table is overwritten, the decay table is
+ * not, and the split form clears what it needs with kernels, so the call can
+ * be captured in a HIP graph).  Calls that share ws (this one,
+ * skv_score_batch) must be ordered on one stream.  Every request is checked
+ * before anything is enqueued. */
+skv_status skv_assign_batch(const skv_config* cfg, const skv_score_request* reqs, int32_t count, void* ws,
                             hipStream_t stream);
 
 /* Cold-tier precision upgrade (Sec. 4.2 and its architecture figure: tokens

@@ -305,21 +305,26 @@ bool fits_resident(int n, int n_sink) { return n - n_sink <= kResident * kSelThr
 // exactly as the one-workgroup form does and clears the histogram of the
 // next pass; sel_classify then assigns every token against the three cut
 // keys.  The cut keys, and so the tier maps, equal the one-workgroup form's.
-// Rows share n; row r's scores and tiers sit at r * n, and its counts come
-// from the group table (8 words per row: sinks, fp16, int8, int4, ...) or,
-// for a single row, from the arguments.
+// The rows are those of a grouped map (one length; counts from the group
+// table, 8 words per row: sinks, fp16, int8, int4, ...), a single request, or
+// the requests of a batched launch.
 struct SelScratch {
   uint32_t hist[2][3][kBins];  // per pass parity: the cut groups' digit counts
   uint64_t prefix[3];          // decided key bits of each cut
   uint32_t rank[3];            // remaining rank inside the prefix
 };
 
+// Rows of one shared length n: row r's scores and tiers sit at r * n, its
+// counts come from the group table or, for a single row, the arguments.
 struct SelRows {
   const double* score;
   uint8_t* tier;
   int n;
   const uint32_t* table;  // per-row counts, or null: the counts below
   int n_sink, n16, n8, n4;
+  __device__ __forceinline__ const double* row_score(int row) const { return score + static_cast<size_t>(row) * n; }
+  __device__ __forceinline__ uint8_t* row_tier(int row) const { return tier + static_cast<size_t>(row) * n; }
+  __device__ __forceinline__ int row_n(int) const { return n; }
   __device__ __forceinline__ void counts(int row, int& s, int& c16, int& c8, int& c4) const {
     if (table != nullptr) {
       const uint32_t* e = table + 8 * row;
@@ -336,6 +341,22 @@ struct SelRows {
   }
 };
 
+// The requests of one batched launch, each with its own length, buffers and
+// counts.
+struct BatchRows {
+  ScoreBatchArgs a;
+  __device__ __forceinline__ const double* row_score(int row) const { return a.r[row].score; }
+  __device__ __forceinline__ uint8_t* row_tier(int row) const { return a.r[row].tier; }
+  __device__ __forceinline__ int row_n(int row) const { return a.r[row].n; }
+  __device__ __forceinline__ void counts(int row, int& s, int& c16, int& c8, int& c4) const {
+    const ScoreDesc& q = a.r[row];
+    s = q.n_sink;
+    c16 = q.n16;
+    c8 = q.n8;
+    c4 = q.n4;
+  }
+};
+
 // Cut j reads the histogram of the first cut (in cut order) with a nonzero
 // rank and the same decided prefix.
 __device__ __forceinline__ int cut_group(const uint64_t (&prefix)[3], const uint32_t (&rank)[3], int j) {
@@ -346,7 +367,8 @@ __device__ __forceinline__ int cut_group(const uint64_t (&prefix)[3], const uint
 
 // grid: one workgroup (256 threads) per row; the cuts start undecided at
 // their ranks
-__global__ __launch_bounds__(256) void sel_init(const SelRows a, SelScratch* __restrict__ scratch) {
+template <typename Rows>
+__global__ __launch_bounds__(256) void sel_init(const Rows a, SelScratch* __restrict__ scratch) {
   SelScratch* sc = scratch + blockIdx.x;
   int s, c16, c8, c4;
   a.counts(blockIdx.x, s, c16, c8, c4);
@@ -357,18 +379,18 @@ __global__ __launch_bounds__(256) void sel_init(const SelRows a, SelScratch* __r
   for (int i = threadIdx.x; i < 3 * kBins; i += 256) (&sc->hist[0][0][0])[i] = 0;
 }
 
-// grid: (ceil(n / (kBatch * 1024)), rows); pass `pass`.  Workgroups past a
-// row's last non-sink token count nothing.
-__global__ __launch_bounds__(kSelThreads) void sel_count(const SelRows a, SelScratch* __restrict__ scratch,
-                                                         int pass) {
+// grid: (ceil(longest row / (kBatch * 1024)), rows); pass `pass`.
+// Workgroups past a row's last non-sink token count nothing.
+template <typename Rows>
+__global__ __launch_bounds__(kSelThreads) void sel_count(const Rows a, SelScratch* __restrict__ scratch, int pass) {
   __shared__ uint32_t hist[3][kBins];
   const int row = blockIdx.y;
   SelScratch* sc = scratch + row;
   int n_sink, c16, c8, c4;
   a.counts(row, n_sink, c16, c8, c4);
-  const int n = a.n;
+  const int n = a.row_n(row);
   if (n_sink + static_cast<int>(blockIdx.x) * kBatch * kSelThreads >= n) return;  // uniform per workgroup
-  const double* __restrict__ score = a.score + static_cast<size_t>(row) * n;
+  const double* __restrict__ score = a.row_score(row);
   const int tid = threadIdx.x, lane = tid & 63;
   uint64_t pre[3];
   uint32_t rk[3];
@@ -459,11 +481,11 @@ __global__ __launch_bounds__(kSelThreads) void sel_choose(SelScratch* __restrict
   for (int i = tid; i < 3 * kBins; i += kSelThreads) next[i] = 0;
 }
 
-// grid: (ceil(n / 1024), rows); sc->prefix[j] is now the cut key itself
-// (keys are distinct), and a cut of rank 0 admits no key
-__global__ __launch_bounds__(kSelThreads) void sel_classify(const SelRows a,
-                                                            const SelScratch* __restrict__ scratch) {
-  const int row = blockIdx.y, n = a.n;
+// grid: (ceil(longest row / 1024), rows); sc->prefix[j] is now the cut key
+// itself (keys are distinct), and a cut of rank 0 admits no key
+template <typename Rows>
+__global__ __launch_bounds__(kSelThreads) void sel_classify(const Rows a, const SelScratch* __restrict__ scratch) {
+  const int row = blockIdx.y, n = a.row_n(row);
   const int t = blockIdx.x * kSelThreads + threadIdx.x;
   if (t >= n) return;
   const SelScratch* sc = scratch + row;
@@ -472,19 +494,21 @@ __global__ __launch_bounds__(kSelThreads) void sel_classify(const SelRows a,
   const bool has1 = c16 != 0, has2 = c16 + c8 != 0, has3 = c16 + c8 + c4 != 0;
   uint8_t tr = kFP16;  // sinks
   if (t >= n_sink) {
-    const uint64_t c = rank_key(a.score[static_cast<size_t>(row) * n + t], t);
+    const uint64_t c = rank_key(a.row_score(row)[t], t);
     tr = (has1 && c >= sc->prefix[0]) ? kFP16 : (has2 && c >= sc->prefix[1]) ? kINT8
          : (has3 && c >= sc->prefix[2])                                       ? kINT4
                                                                                : kDROP;
   }
-  a.tier[static_cast<size_t>(row) * n + t] = tr;
+  a.row_tier(row)[t] = tr;
 }
 
-hipError_t launch_assign_split(const SelRows& a, int rows, SelScratch* sc, hipStream_t stream) {
+// max_n: the longest row
+template <typename Rows>
+hipError_t launch_assign_split(const Rows& a, int rows, int max_n, SelScratch* sc, hipStream_t stream) {
   sel_init<<<rows, 256, 0, stream>>>(a, sc);
   hipError_t e = hipGetLastError();
   const int per = kBatch * kSelThreads;
-  const dim3 count_grid((a.n + per - 1) / per, rows);
+  const dim3 count_grid((max_n + per - 1) / per, rows);
   for (int pass = 0; pass < kPasses && e == hipSuccess; ++pass) {
     sel_count<<<count_grid, kSelThreads, 0, stream>>>(a, sc, pass);
     e = hipGetLastError();
@@ -493,7 +517,7 @@ hipError_t launch_assign_split(const SelRows& a, int rows, SelScratch* sc, hipSt
     e = hipGetLastError();
   }
   if (e != hipSuccess) return e;
-  sel_classify<<<dim3((a.n + kSelThreads - 1) / kSelThreads, rows), kSelThreads, 0, stream>>>(a, sc);
+  sel_classify<<<dim3((max_n + kSelThreads - 1) / kSelThreads, rows), kSelThreads, 0, stream>>>(a, sc);
   return hipGetLastError();
 }
 
@@ -527,7 +551,12 @@ __global__ __launch_bounds__(kSelThreads) void assign_tiers_batch(const ScoreBat
 
 bool assign_fits_resident(int32_t n, int32_t n_sink) { return fits_resident(n, n_sink); }
 
-hipError_t launch_assign_batch(const ScoreBatchArgs& a, bool resident, hipStream_t stream) {
+hipError_t launch_assign_batch(const ScoreBatchArgs& a, bool resident, void* scratch, hipStream_t stream) {
+  if (!resident && scratch != nullptr) {
+    int max_n = 0;
+    for (int i = 0; i < a.count; ++i) max_n = a.r[i].n > max_n ? a.r[i].n : max_n;
+    return launch_assign_split(BatchRows{a}, a.count, max_n, static_cast<SelScratch*>(scratch), stream);
+  }
   if (resident)
     assign_tiers_batch<true><<<a.count, kSelThreads, 0, stream>>>(a);
   else
@@ -544,7 +573,7 @@ hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier, 
   if (fits_resident(g.n, g.n_sink))
     assign_tiers<true><<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
   else if (scratch != nullptr)
-    return launch_assign_split(SelRows{score, tier, g.n, nullptr, g.n_sink, g.n16, g.n8, g.n4}, 1,
+    return launch_assign_split(SelRows{score, tier, g.n, nullptr, g.n_sink, g.n16, g.n8, g.n4}, 1, g.n,
                                static_cast<SelScratch*>(scratch), stream);
   else
     assign_tiers<false><<<1, kSelThreads, 0, stream>>>(score, tier, g.n, g.n_sink, g.n16, g.n8, g.n4);
@@ -555,7 +584,7 @@ hipError_t launch_assign_groups(int32_t G, int32_t n, const uint32_t* group_tabl
                                 uint8_t* tier, void* scratch, hipStream_t stream) {
   if (!fits_resident(n, 0)) {
     if (scratch == nullptr) return hipErrorInvalidValue;
-    return launch_assign_split(SelRows{score, tier, n, group_table, 0, 0, 0, 0}, G,
+    return launch_assign_split(SelRows{score, tier, n, group_table, 0, 0, 0, 0}, G, n,
                                static_cast<SelScratch*>(scratch), stream);
   }
   assign_tiers_groups<<<G, kSelThreads, 0, stream>>>(score, tier, n, group_table);

@@ -658,7 +658,18 @@ skv_status skv_batch_workspace_size(const skv_config* cfg, const skv_score_reque
   if (st != SKV_OK) return st;
   ScoreBatchArgs shape;
   std::vector<uint64_t> offsets;
-  *bytes = score_batch_layout(cfg, reqs, count, &shape, &offsets);
+  const uint64_t score_bytes = score_batch_layout(cfg, reqs, count, &shape, &offsets);
+  // skv_assign_batch's split tier cut reuses the partial-sum region: one
+  // select state per long request of a launch
+  int32_t longest = 0, long_rows = 0;
+  for (int32_t i = 0; i < count; ++i)
+    if (assign_scratch_bytes(reqs[i].num_tokens, 1) != 0) {
+      longest = std::max(longest, reqs[i].num_tokens);
+      ++long_rows;
+    }
+  const uint64_t assign_bytes =
+      decay_table_bytes(cfg) + assign_scratch_bytes(longest, std::min(long_rows, kMaxScoreBatch));
+  *bytes = std::max(score_bytes, assign_bytes);
   return SKV_OK;
 }
 
@@ -699,20 +710,23 @@ skv_status skv_score_batch(const skv_config* cfg, const skv_score_request* reqs,
   return SKV_OK;
 }
 
-skv_status skv_assign_batch(const skv_config* cfg, const skv_score_request* reqs, int32_t count,
+skv_status skv_assign_batch(const skv_config* cfg, const skv_score_request* reqs, int32_t count, void* ws,
                             hipStream_t stream) {
   std::vector<skv_plan> plans;
   const skv_status st = check_score_requests(cfg, reqs, count, true, &plans);
   if (st != SKV_OK) return st;
+  if (ws != nullptr && !dev_ptr_ok(ws)) return SKV_ERR_INVALID_ARG;
+  void* scratch = ws == nullptr ? nullptr : static_cast<uint8_t*>(ws) + decay_table_bytes(cfg);
   // requests whose non-sink keys fit the resident form go to resident
-  // launches, the rest to launches of the general form
+  // launches, the rest to split launches (workspace given) or launches of the
+  // one-workgroup general form
   for (const bool resident : {true, false}) {
     ScoreBatchArgs a;
     std::memset(&a, 0, sizeof(a));
     for (int32_t i = 0; i <= count; ++i) {
       const bool flush = i == count || a.count == kMaxScoreBatch;
       if (flush && a.count > 0) {
-        if (launch_assign_batch(a, resident, stream) != hipSuccess) return SKV_ERR_DEVICE;
+        if (launch_assign_batch(a, resident, scratch, stream) != hipSuccess) return SKV_ERR_DEVICE;
         a.count = 0;
       }
       if (i == count) break;

@@ -118,9 +118,11 @@ hipError_t launch_assign(const Geometry& g, const double* score, uint8_t* tier, 
 void kvnorm_batch_shape(int32_t L, int32_t H, int32_t d, const int32_t* ns, int32_t count, ScoreBatchArgs* a);
 hipError_t launch_score_kvnorm_batch(const ScoreBatchArgs& a, int32_t d, const double* w2, hipStream_t stream);
 hipError_t launch_score_recency_batch(const ScoreBatchArgs& a, const double* w1, hipStream_t stream);
-// One workgroup per request; RESIDENT chooses the resident form, which every
-// request of the launch must fit (n - n_sink <= 32768).
-hipError_t launch_assign_batch(const ScoreBatchArgs& a, bool resident, hipStream_t stream);
+// `resident`: every request of the launch fits the resident form
+// (n - n_sink <= 32768) and each takes one workgroup.  Otherwise the requests
+// run split over the GPU when scratch (assign_scratch_bytes for a.count rows
+// of more than 32768 tokens) is given, else on one workgroup each.
+hipError_t launch_assign_batch(const ScoreBatchArgs& a, bool resident, void* scratch, hipStream_t stream);
 bool assign_fits_resident(int32_t n, int32_t n_sink);
 
 // Batched launches over a.count requests and layers [layer_begin, layer_begin +

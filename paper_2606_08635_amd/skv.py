@@ -115,7 +115,7 @@ def lib():
             "skv_unpack_upgrade": (ctypes.c_int, [cfgp, vp, u64, i32, i32, vp, vp, vp, i32, i32, vp, vp]),
             "skv_batch_workspace_size": (ctypes.c_int, [cfgp, P(ScoreRequest), i32, P(u64)]),
             "skv_score_batch": (ctypes.c_int, [cfgp, P(ScoreRequest), i32, vp, vp]),
-            "skv_assign_batch": (ctypes.c_int, [cfgp, P(ScoreRequest), i32, vp]),
+            "skv_assign_batch": (ctypes.c_int, [cfgp, P(ScoreRequest), i32, vp, vp]),
         }
         for name, (res, args) in sigs.items():
             fn = getattr(L, name)
@@ -438,7 +438,8 @@ def _score_requests(cfg: Config, scores, ks=None, vs=None, tiers=None):
 
 
 def batch_workspace_size(cfg: Config, scores) -> int:
-    """Workspace bytes of score_batch for requests of these lengths (cfg.num_tokens >= every n)."""
+    """Workspace bytes of score_batch and assign_batch for requests of these
+    lengths (cfg.num_tokens >= every n)."""
     count = len(scores)
     reqs = (ScoreRequest * count)()
     for i in range(count):
@@ -460,10 +461,13 @@ def score_batch(cfg: Config, ks, vs, scores, ws: torch.Tensor, stream=None):
            "skv_score_batch")
 
 
-def assign_batch(cfg: Config, scores, tiers, stream=None):
-    """Assigns the tiers of len(scores) requests, one workgroup per request."""
+def assign_batch(cfg: Config, scores, tiers, stream=None, ws=None):
+    """Assigns the tiers of len(scores) requests: one workgroup per request of
+    at most 32768 non-sink tokens; longer requests split over the GPU when ws
+    (batch_workspace_size bytes) is given, else one workgroup each."""
     reqs, count = _score_requests(cfg, scores, tiers=tiers)
-    _check(lib().skv_assign_batch(ctypes.byref(cfg), reqs, count, _stream(stream)), "skv_assign_batch")
+    w = ctypes.c_void_p(None) if ws is None else _dev(ws, torch.uint8, batch_workspace_size(cfg, scores), "ws")
+    _check(lib().skv_assign_batch(ctypes.byref(cfg), reqs, count, w, _stream(stream)), "skv_assign_batch")
 
 
 def unpack_batch(cfg: Config, payloads, token_counts, block_tables, k_cache: torch.Tensor,

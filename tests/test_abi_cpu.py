@@ -304,6 +304,30 @@ def test_batched_score_host_checks(lib):
     assert lib.skv_score_batch(ctypes.byref(acfg), _score_reqs([10]), 1, ctypes.c_void_p(256), None) \
         == skv.ERR_INVALID_ARG
     # misaligned score pointer
-    assert lib.skv_assign_batch(ctypes.byref(cfg), _score_reqs([10], ptr=258), 1, None) == skv.ERR_INVALID_ARG
+    assert lib.skv_assign_batch(ctypes.byref(cfg), _score_reqs([10], ptr=258), 1, None, None) == skv.ERR_INVALID_ARG
+    # misaligned workspace
+    assert lib.skv_assign_batch(ctypes.byref(cfg), _score_reqs([10]), 1, ctypes.c_void_p(264), None) \
+        == skv.ERR_INVALID_ARG
     # a request whose sinks exceed its own budget: one token, one sink, b = 0.5
-    assert lib.skv_assign_batch(ctypes.byref(cfg), _score_reqs([10, 1]), 2, None) == skv.ERR_BUDGET
+    assert lib.skv_assign_batch(ctypes.byref(cfg), _score_reqs([10, 1]), 2, None, None) == skv.ERR_BUDGET
+
+
+def test_batched_workspace_holds_the_split_tier_cut(lib):
+    """The batch workspace holds, after the decay table, either the KV-norm
+    partial sums or the split tier cut's select state (49192 bytes per request
+    past 32768 tokens, at most 48 per launch), whichever is larger."""
+    import ctypes
+    state = 49192
+    for mode in (skv.KVNORM, skv.RECENCY):
+        cfg = skv.config(2, 2, 64, 200_000, 0.5, score_mode=mode, decay=1e-4)
+        table = -(-8 * 200_000 // 256) * 256
+        for lengths, longs in (([100], 0), ([32768, 20_000], 0), ([32769], 1), ([200_000, 5, 40_000], 2),
+                               ([40_000] * 50, 48)):
+            out = ctypes.c_uint64()
+            assert lib.skv_batch_workspace_size(ctypes.byref(cfg), _score_reqs(lengths), len(lengths),
+                                                ctypes.byref(out)) == skv.OK
+            select = -(-longs * state // 256) * 256
+            if mode == skv.KVNORM:
+                assert out.value >= table + max(16 * sum(lengths), select), (mode, lengths)
+            else:  # no partial sums: the select state alone
+                assert out.value == table + select, (mode, lengths)

@@ -95,3 +95,36 @@ def test_captured_split_tier_cut_replays_match_oracle():
         # eager work between replays on the same buffers
         skv.assign_tiers(cfg, scores, tier, ws=ws)
         torch.cuda.synchronize()
+
+
+def test_captured_batched_split_tier_cut_replays_match_oracle():
+    """skv_assign_batch with its workspace under capture: three requests past
+    the resident form and one inside it; every replay on new scores equals the
+    oracle's maps."""
+    lengths = [100_003, 1000, 40_000, 33_000]
+    cfg, _ = configs(1, 1, 32, max(lengths), 0.45, 3, decay=1e-3)
+    ocfgs = [configs(1, 1, 32, n, 0.45, 3, decay=1e-3)[1] for n in lengths]
+    say(f"graph capture, batched split tier cut {lengths}")
+    scores = [torch.rand(n, dtype=torch.float64, device="cuda") for n in lengths]
+    tiers = [torch.empty(n, dtype=torch.uint8, device="cuda") for n in lengths]
+    ws = torch.empty(skv.batch_workspace_size(cfg, scores), dtype=torch.uint8, device="cuda")
+    skv.assign_batch(cfg, scores, tiers, ws=ws)  # warm-up outside capture
+    torch.cuda.synchronize()
+    stream = torch.cuda.Stream()
+    stream.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        skv.assign_batch(cfg, scores, tiers, ws=ws)
+    torch.cuda.synchronize()
+    for seed in (31, 32, 33):
+        rng = np.random.default_rng(seed)
+        keys = [np.ldexp(1.0 + rng.random(n), rng.integers(-30, 30, n)) for n in lengths]
+        for s, k in zip(scores, keys):
+            s.copy_(torch.from_numpy(k))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (t, k) in enumerate(zip(tiers, keys)):
+            assert np.array_equal(t.cpu().numpy(), oracle.assign(ocfgs[i], k)), (seed, i)
+        skv.assign_batch(cfg, scores, tiers, ws=ws)  # eager work between replays
+        torch.cuda.synchronize()

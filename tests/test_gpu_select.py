@@ -215,3 +215,60 @@ def test_split_form_random_grouped_rows():
         skv.assign_groups(cfg, groups, torch.from_numpy(key.ravel()).cuda(), tier, ws)
         torch.cuda.synchronize()
         assert np.array_equal(tier.cpu().numpy().reshape(G, n), want), f"case {case}"
+
+
+@pytest.mark.parametrize("tiers,b", [(3, 0.4), (2, 0.7)])
+def test_batched_split_form_matches_oracle(tiers, b):
+    """skv_assign_batch with requests on both sides of the resident form
+    (4 sinks: 32772 tokens fit it, 32773 do not) and up to 250k tokens: with
+    the workspace (split form) and without (one workgroup per request) every
+    request's map equals the oracle's for that request alone; a second call on
+    the same workspace with other scores and fewer requests starts clean."""
+    lengths = [32_772, 32_773, 100_003, 40, 250_000, 40_000, 2048, 65_536]
+    kinds = ["binades", "low_word", "ties"]
+    cfg, _ = configs(1, 1, 32, max(lengths), b, tiers, num_sink=4, decay=1e-4)
+
+    def case(lens, seed):
+        keys = [_scores(kinds[i % 3], n, seed=seed + i) for i, n in enumerate(lens)]
+        want = [oracle.assign(configs(1, 1, 32, n, b, tiers, num_sink=4, decay=1e-4)[1], k)
+                for n, k in zip(lens, keys)]
+        return [torch.from_numpy(k).cuda() for k in keys], want
+
+    scores, want = case(lengths, 500)
+    ws = torch.empty(skv.batch_workspace_size(cfg, scores), dtype=torch.uint8, device="cuda")
+    for w in (ws, None):
+        say(f"batched assign {len(lengths)} requests tiers={tiers} b={b} ws={w is not None}")
+        out = [torch.full((n,), 0xEE, dtype=torch.uint8, device="cuda") for n in lengths]
+        skv.assign_batch(cfg, scores, out, ws=w)
+        torch.cuda.synchronize()
+        for i, (t, wt) in enumerate(zip(out, want)):
+            assert np.array_equal(t.cpu().numpy(), wt), f"request {i} (n={lengths[i]}), ws={w is not None}"
+    sub = [100_003, 32_773, 70_001]
+    scores, want = case(sub, 900)
+    say(f"batched assign, second call {sub}")
+    out = [torch.full((n,), 0xEE, dtype=torch.uint8, device="cuda") for n in sub]
+    skv.assign_batch(cfg, scores, out, ws=ws)
+    torch.cuda.synchronize()
+    for i, (t, wt) in enumerate(zip(out, want)):
+        assert np.array_equal(t.cpu().numpy(), wt), f"second call, request {i} (n={sub[i]})"
+
+
+def test_batched_split_form_more_than_one_launch():
+    """Fifty long requests (two split launch sequences of at most 48 sharing
+    one select state area) with seeded random lengths, score kinds and sink
+    counts under one budget: every map equals the oracle's."""
+    rng = np.random.default_rng(31)
+    lengths = [int(x) for x in rng.integers(32_769, 60_000, 50)]
+    b, tiers, n_sink = 0.35, 3, 16
+    cfg, _ = configs(1, 1, 32, max(lengths), b, tiers, num_sink=n_sink, decay=1e-4)
+    kinds = ["binades", "low_word", "ties"]
+    keys = [_scores(kinds[int(rng.integers(3))], n, seed=int(rng.integers(1 << 30))) for n in lengths]
+    scores = [torch.from_numpy(k).cuda() for k in keys]
+    out = [torch.full((n,), 0xEE, dtype=torch.uint8, device="cuda") for n in lengths]
+    ws = torch.empty(skv.batch_workspace_size(cfg, scores), dtype=torch.uint8, device="cuda")
+    say("batched assign, 50 long requests")
+    skv.assign_batch(cfg, scores, out, ws=ws)
+    torch.cuda.synchronize()
+    for i, n in enumerate(lengths):
+        want = oracle.assign(configs(1, 1, 32, n, b, tiers, num_sink=n_sink, decay=1e-4)[1], keys[i])
+        assert np.array_equal(out[i].cpu().numpy(), want), f"request {i} (n={n})"
