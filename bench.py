@@ -593,7 +593,9 @@ def run_select(args):
 
 CEILING_PATTERNS = ["read", "write_nt", "write_default", "copy", "read2_write1", "read1_write2_8b",
                     "read1_write2_16b", "nhd_scatter", "read1_write4", "stage_direct",
-                    "stage_regs", "stage_direct_cached"]  # skv_ceiling.h, in enum order
+                    "stage_regs", "stage_direct_cached",
+                    "write_cpol_default", "write_cpol_sc0", "write_cpol_nt", "write_cpol_sc0_nt", "write_cpol_sc1",
+                    "write_cpol_sc0_sc1", "write_cpol_nt_sc1", "write_cpol_sc0_nt_sc1"]  # skv_ceiling.h, in enum order
 
 
 def run_ceiling(args):
@@ -647,6 +649,26 @@ def run_ceiling(args):
         best = max(res, key=lambda k: res[k]["gbps"])
         out[name] = {"read_bytes": rd, "write_bytes": wr, "best_gbps": res[best]["gbps"], "best_inflight": best,
                      "by_inflight": res}
+        if name.startswith("write"):
+            # the write followed by a read of the other buffer (16 in flight),
+            # pairs back to back: what the write leaves in the caches is paid
+            # for inside the pair
+            def pair():
+                for p_, b_ in ((pat, 4), (0, 16)):
+                    if lib.skv_ceiling_run(p_, b_, ctypes.c_void_p(dst.data_ptr()), ctypes.c_void_p(src.data_ptr()),
+                                           nbytes, ctypes.c_void_p(sink.data_ptr()),
+                                           ctypes.c_void_p(stream.cuda_stream)) != 0:
+                        raise RuntimeError(f"skv_ceiling_run({p_}) failed")
+            for _ in range(args.warmup):
+                pair()
+            ev = _events(2 * args.steps)
+            for i in range(args.steps):
+                ev[2 * i].record(stream)
+                pair()
+                ev[2 * i + 1].record(stream)
+            torch.cuda.synchronize()
+            out[name]["then_read_ms"] = round(sum(ev[2 * i].elapsed_time(ev[2 * i + 1])
+                                                  for i in range(args.steps)) / args.steps, 4)
         print(f"[ceiling] {name}: {out[name]['best_gbps']} GB/s ({best} in flight)", file=sys.stderr, flush=True)
     return {"bytes": nbytes, "steps": args.steps, "warmup": args.warmup, "patterns": out}
 

@@ -48,8 +48,11 @@ enum {
   SKV_CEIL_STAGE_REGS = 10,       /* the same stages loaded into registers
                                      (non-temporal) and written to shared memory
                                      by the threads                             */
-  SKV_CEIL_STAGE_DIRECT_CACHED = 11 /* as STAGE_DIRECT with the default cache
+  SKV_CEIL_STAGE_DIRECT_CACHED = 11, /* as STAGE_DIRECT with the default cache
                                      policy                                      */
+  SKV_CEIL_WRITE_CPOL = 12        /* 12 + p, p in 0..7: write `bytes` with 16-byte
+                                     buffer stores whose cache-policy modifiers
+                                     are sc0 if p & 1, nt if p & 2, sc1 if p & 4 */
 };
 
 /* Enqueues one pass of `pattern` on `stream`, each thread keeping `inflight`

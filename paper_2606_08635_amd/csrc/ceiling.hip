@@ -61,6 +61,20 @@ __global__ __launch_bounds__(kThreads) void write_only(uint8_t* __restrict__ dst
   for (int s = 0; s < kSteps; ++s) st16<NT>(base + s * kThreads * 16, v);
 }
 
+// Write-only through buffer stores whose cache-policy bits are CPOL (bit 0
+// sc0, bit 1 nt, bit 4 sc1: the instruction's own modifiers).  Each
+// workgroup's buffer descriptor covers its own 64 KiB tile, so the hardware's
+// range check also bounds every store.
+template <int CPOL>
+__global__ __launch_bounds__(kThreads) void write_cpol(uint8_t* __restrict__ dst) {
+  const __amdgpu_buffer_rsrc_t r =
+      __builtin_amdgcn_make_buffer_rsrc(dst + blockIdx.x * kTile, 0, static_cast<int>(kTile), 0x00020000);
+  const u32x4 v{blockIdx.x, threadIdx.x, 0x3C003C00u, 0u};
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s)
+    __builtin_amdgcn_raw_buffer_store_b128(v, r, (s * kThreads + static_cast<int>(threadIdx.x)) * 16, 0, CPOL);
+}
+
 // Copy: the tile read and written once.
 template <int F>
 __global__ __launch_bounds__(kThreads) void copy_1to1(const uint8_t* __restrict__ src, uint8_t* __restrict__ dst) {
@@ -280,6 +294,14 @@ int run_pattern(int32_t pattern, uint8_t* out, const uint8_t* in, uint64_t bytes
     case SKV_CEIL_READ1_WRITE2_8B: read1_write2<8, F><<<tiles, kThreads, 0, stream>>>(in, out); break;
     case SKV_CEIL_READ1_WRITE2_16B: read1_write2<16, F><<<tiles, kThreads, 0, stream>>>(in, out); break;
     case SKV_CEIL_READ1_WRITE4: read1_write4<F><<<tiles, kThreads, 0, stream>>>(in, out); break;
+    case SKV_CEIL_WRITE_CPOL + 0: write_cpol<0><<<tiles, kThreads, 0, stream>>>(out); break;
+    case SKV_CEIL_WRITE_CPOL + 1: write_cpol<1><<<tiles, kThreads, 0, stream>>>(out); break;
+    case SKV_CEIL_WRITE_CPOL + 2: write_cpol<2><<<tiles, kThreads, 0, stream>>>(out); break;
+    case SKV_CEIL_WRITE_CPOL + 3: write_cpol<3><<<tiles, kThreads, 0, stream>>>(out); break;
+    case SKV_CEIL_WRITE_CPOL + 4: write_cpol<16><<<tiles, kThreads, 0, stream>>>(out); break;
+    case SKV_CEIL_WRITE_CPOL + 5: write_cpol<17><<<tiles, kThreads, 0, stream>>>(out); break;
+    case SKV_CEIL_WRITE_CPOL + 6: write_cpol<18><<<tiles, kThreads, 0, stream>>>(out); break;
+    case SKV_CEIL_WRITE_CPOL + 7: write_cpol<19><<<tiles, kThreads, 0, stream>>>(out); break;
     case SKV_CEIL_NHD_SCATTER: {
       // bytes written = tokens * 8 heads * 256 B; tokens a multiple of 256
       const uint64_t tokens = bytes / (kNhdHeads * 2 * kNhdRow);
@@ -316,7 +338,8 @@ int skv_ceiling_run(int32_t pattern, int32_t inflight, void* dst, const void* sr
   uint8_t* out = static_cast<uint8_t*>(dst);
   const uint64_t tiles = bytes / kTile;
   if (tiles > 0x7FFFFFFFu) return 1;
-  const bool reads = pattern != SKV_CEIL_WRITE && pattern != SKV_CEIL_WRITE_DEFAULT;
+  const bool reads = pattern != SKV_CEIL_WRITE && pattern != SKV_CEIL_WRITE_DEFAULT &&
+                     !(pattern >= SKV_CEIL_WRITE_CPOL && pattern < SKV_CEIL_WRITE_CPOL + 8);
   if ((pattern == SKV_CEIL_STAGE_DIRECT || pattern == SKV_CEIL_STAGE_DIRECT_CACHED || pattern == SKV_CEIL_STAGE_REGS) &&
       bytes / kStreamBytes > 0x7FFFFFFFu)
     return 1;
@@ -345,7 +368,9 @@ uint64_t skv_ceiling_bytes(int32_t pattern, uint64_t bytes, int32_t which) {
     case SKV_CEIL_STAGE_DIRECT:
     case SKV_CEIL_STAGE_DIRECT_CACHED:
     case SKV_CEIL_STAGE_REGS: return which == 0 ? bytes / kStreamBytes * kStreamBytes : 0;
-    default: return 0;
+    default:
+      if (pattern >= SKV_CEIL_WRITE_CPOL && pattern < SKV_CEIL_WRITE_CPOL + 8) return which == 0 ? 0 : bytes;
+      return 0;
   }
 }
 

@@ -38,11 +38,12 @@ def test_byte_accounting(lib):
     B = 1 << 30
     want = {0: (B, 0), 1: (0, B), 2: (0, B), 3: (B, B), 4: (B, B // 2), 5: (B // 2, B), 6: (B // 2, B),
             7: (B // 2, B), 8: (B // 4, B), 9: (B, 0), 10: (B, 0), 11: (B, 0)}
+    want.update({12 + p: (0, B) for p in range(8)})  # writes with each store cache policy
     for pat, (rd, wr) in want.items():
         assert (lib.skv_ceiling_bytes(pat, B, 0), lib.skv_ceiling_bytes(pat, B, 1)) == (rd, wr)
     # the stage streams read whole 256 KiB workgroup streams
     assert lib.skv_ceiling_bytes(9, 384 << 10, 0) == lib.skv_ceiling_bytes(10, 384 << 10, 0) == 256 << 10
-    assert lib.skv_ceiling_bytes(12, B, 0) == 0
+    assert lib.skv_ceiling_bytes(20, B, 0) == lib.skv_ceiling_bytes(20, B, 1) == 0  # unknown pattern
 
 
 def test_bad_arguments_refused_before_launch(lib):
