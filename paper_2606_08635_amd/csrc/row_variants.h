@@ -567,23 +567,34 @@ __device__ __forceinline__ uint32_t pack_half2_canon(float a, float b) {
 
 // The scale and minimum (0 if symmetric) of the lane's group of a quantized
 // row under descriptor q, read from the row's metadata entry.
+// A lane's group metadata as stored, kept as bits so that its loads stay in
+// flight until the row is decoded: binary16 entries in a (the scale in the
+// low half, an asymmetric group's minimum in the high half), binary32 entries
+// in a (scale) and b (minimum); unused bits are zero.
 struct LaneMeta {
-  float s, lo;
+  uint32_t a, b;
 };
+// Byte offset of a lane's group entry inside a row's metadata.
 template <int LPR>
-__device__ __forceinline__ LaneMeta load_lane_meta(int32_t q, const uint8_t* meta, int lane) {
+__device__ __forceinline__ uint32_t lane_meta_offset(int32_t q, int lane) {
   constexpr int D = LPR * 8;
-  const int gl = var_group_lanes(q, D);
-  const bool asym = (q & kQuantAsym) != 0, f16 = (q & kQuantFp16) != 0;
-  const uint8_t* e = meta + (lane / gl) * (asym ? 2 : 1) * (f16 ? 2 : 4);
-  LaneMeta m;
-  m.lo = 0.0f;
-  if (f16) {
-    m.s = half_lo(reinterpret_cast<const uint16_t*>(e)[0]);
-    if (asym) m.lo = half_lo(reinterpret_cast<const uint16_t*>(e)[1]);
+  return static_cast<uint32_t>(lane / var_group_lanes(q, D)) * entry_bytes(q);
+}
+// 32 bits at a 2-byte aligned address (one load; global memory takes
+// unaligned dword loads).
+typedef uint32_t u32_align2 __attribute__((aligned(2)));
+__device__ __forceinline__ uint32_t load_u32_align2(const uint8_t* p) {
+  return *reinterpret_cast<const u32_align2*>(p);
+}
+// e: the lane's entry (row metadata + lane_meta_offset)
+__device__ __forceinline__ LaneMeta load_lane_meta(int32_t q, const uint8_t* e) {
+  const bool asym = (q & kQuantAsym) != 0;
+  LaneMeta m{0u, 0u};
+  if (q & kQuantFp16) {
+    m.a = asym ? load_u32_align2(e) : static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(e)[0]);
   } else {
-    m.s = __builtin_bit_cast(float, load_u32_from_halves(e));
-    if (asym) m.lo = __builtin_bit_cast(float, load_u32_from_halves(e + 4));
+    m.a = load_u32_align2(e);
+    if (asym) m.b = load_u32_align2(e + 4);
   }
   return m;
 }
@@ -592,7 +603,9 @@ __device__ __forceinline__ LaneMeta load_lane_meta(int32_t q, const uint8_t* met
 // group's metadata m.
 __device__ __forceinline__ u32x4 decode_lane_var(int tr, int32_t q, u32x4 raw, LaneMeta m) {
   const bool asym = (q & kQuantAsym) != 0;
-  const float s = m.s, lo = m.lo;
+  const bool f16 = (q & kQuantFp16) != 0;
+  const float s = f16 ? half_lo(m.a) : __builtin_bit_cast(float, m.a);
+  const float lo = f16 ? half_hi(m.a) : __builtin_bit_cast(float, m.b);
   if (__builtin_isnan(s)) return u32x4{kNaNHalf2, kNaNHalf2, kNaNHalf2, kNaNHalf2};
   float f[8];
 #pragma unroll
@@ -689,6 +702,7 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDe
   constexpr int U = ITERS < ROWS_IN_FLIGHT ? ITERS : ROWS_IN_FLIGHT;
   const int lane = threadIdx.x % LPR;
   const int rsub = threadIdx.x / LPR;
+  const uint32_t moff8 = lane_meta_offset<LPR>(v.q8, lane), moff4 = lane_meta_offset<LPR>(v.q4, lane);
 #pragma unroll 1
   for (int it = 0; it < ITERS; it += U) {
     u32x4 raw[U];
@@ -699,7 +713,7 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDe
       const int tr = s.tier[r];
       const uint8_t* row = src + s.off[r];
       raw[u] = u32x4{0u, 0u, 0u, 0u};
-      mt[u] = LaneMeta{0.0f, 0.0f};
+      mt[u] = LaneMeta{0u, 0u};
       if (tr == kFP16) {
         raw[u] = ld_nt16(row + lane * 16);
       } else if (tr == kINT8) {
@@ -711,7 +725,7 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDe
       }
       if (tr == kINT8 || tr == kINT4) {
         const int32_t q = tr == kINT8 ? v.q8 : v.q4;
-        if (!(CHAN && (q & kQuantChannel))) mt[u] = load_lane_meta<LPR>(q, meta + s.q[r], lane);
+        if (!(CHAN && (q & kQuantChannel))) mt[u] = load_lane_meta(q, meta + s.q[r] + (tr == kINT8 ? moff8 : moff4));
       }
     }
 #pragma unroll
