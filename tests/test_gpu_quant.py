@@ -208,3 +208,29 @@ def test_full_size_variant(q8, q4):
             mo = lay + base + int((sbk if kv == 0 else sb)[t])
             assert np.array_equal(pay[mo:mo + mb.size].cpu().numpy(), mb), ("meta", l, kv, h, t)
         assert np.array_equal(grow, oracle.decode_row_q(tr, q, d, data, mb)), ("cache", l, kv, h, t)
+
+
+DESCRIPTORS = [g | a | f | c for g in (0, Q.QUANT_GROUP64, Q.QUANT_GROUP32) for a in (0, Q.QUANT_ASYM)
+               for f in (0, Q.QUANT_FP16) for c in (0, Q.QUANT_CHANNEL)]
+
+
+def _random_pair_case(rng):
+    """A seeded random shape, budget, tier policy and descriptor pair (every
+    group size, asymmetric codes, binary16 metadata and per-channel keys, so
+    metadata entries of different widths interleave at 2-byte offsets)."""
+    d = int(rng.choice([32, 64, 128, 256]))
+    n = int(rng.integers(64, 1500))
+    b = float(np.float32(rng.uniform(0.1, 1.0)))
+    tiers = int(rng.choice([2, 3]))
+    q8, q4 = (int(x) for x in rng.choice(DESCRIPTORS, 2))
+    return int(rng.integers(1, 3)), int(rng.integers(1, 4)), d, n, b, q8, q4, tiers
+
+
+def test_random_descriptor_pairs():
+    """Twenty-four seeded random descriptor pairs on random shapes: payload and
+    decoded caches bit-identical to the oracle's."""
+    rng = np.random.default_rng(4242)
+    for case in range(24):
+        L, H, d, n, b, q8, q4, tiers = _random_pair_case(rng)
+        say(f"random descriptor pair #{case}: L={L} H={H} d={d} n={n} b={b} q8={q8} q4={q4} tiers={tiers}")
+        _run(L, H, d, n, b, q8, q4, seed=1000 + case, tiers=tiers)
