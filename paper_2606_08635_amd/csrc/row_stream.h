@@ -102,6 +102,7 @@ struct RowBatch {
   static constexpr int RPI = kRowThreads / LPR;
   static constexpr int ITERS = kChunkTokens / RPI;
   static constexpr int U = ITERS < ROWS_IN_FLIGHT ? ITERS : ROWS_IN_FLIGHT;
+  static_assert(ITERS % U == 0, "rows in flight must divide a thread's rows of the chunk");
   u32x4 x[U];
 };
 
@@ -204,6 +205,7 @@ __device__ __forceinline__ void unpack_chunk(const ChunkLds& s, const uint8_t* _
   constexpr int RPI = kRowThreads / LPR;
   constexpr int ITERS = kChunkTokens / RPI;
   constexpr int U = ITERS < ROWS_IN_FLIGHT ? ITERS : ROWS_IN_FLIGHT;
+  static_assert(ITERS % U == 0, "rows in flight must divide a thread's rows of the chunk");
   const int lane = threadIdx.x % LPR;
   const int rsub = threadIdx.x / LPR;
 #pragma unroll 1

@@ -458,6 +458,7 @@ __device__ __forceinline__ void pack_chunk_var(const ChunkLds& s, const ChanLds<
   constexpr int RPI = kRowThreads / LPR;
   constexpr int ITERS = kChunkTokens / RPI;
   constexpr int U = ITERS < ROWS_IN_FLIGHT ? ITERS : ROWS_IN_FLIGHT;
+  static_assert(ITERS % U == 0, "rows in flight must divide a thread's rows of the chunk");
   const int lane = threadIdx.x % LPR;
   const int rsub = threadIdx.x / LPR;
 #pragma unroll 1
@@ -700,6 +701,7 @@ __device__ __forceinline__ void unpack_chunk_var(const ChunkLds& s, const ChanDe
   constexpr int RPI = kRowThreads / LPR;
   constexpr int ITERS = kChunkTokens / RPI;
   constexpr int U = ITERS < ROWS_IN_FLIGHT ? ITERS : ROWS_IN_FLIGHT;
+  static_assert(ITERS % U == 0, "rows in flight must divide a thread's rows of the chunk");
   const int lane = threadIdx.x % LPR;
   const int rsub = threadIdx.x / LPR;
   const uint32_t moff8 = lane_meta_offset<LPR>(v.q8, lane), moff4 = lane_meta_offset<LPR>(v.q4, lane);

@@ -196,6 +196,7 @@ __global__ __launch_bounds__(kUpgThreads) void upg_rows(const UpgArgs a) {
   constexpr int RPI = kUpgThreads / LPR;     // rows per block-wide iteration
   constexpr int ITERS = kUpgThreads / RPI;
   constexpr int U = ITERS < SKV_UPG_ROWS_IN_FLIGHT ? ITERS : SKV_UPG_ROWS_IN_FLIGHT;  // rows in flight per thread
+  static_assert(ITERS % U == 0, "rows in flight must divide a thread's rows of the chunk");
   __shared__ int32_t s_tok[kUpgThreads];
   __shared__ uint8_t s_tier[kUpgThreads];
   uint8_t* up = a.up;
@@ -312,6 +313,7 @@ __global__ __launch_bounds__(kUpgThreads) void upg_apply(const UpgArgs a) {
   constexpr int RPI = kUpgThreads / LPR;
   constexpr int ITERS = kUpgThreads / RPI;
   constexpr int U = ITERS < 4 ? ITERS : 4;
+  static_assert(ITERS % U == 0, "rows in flight must divide a thread's rows of the chunk");
   __shared__ uint32_t s_pos[kUpgThreads];
   if (*a.status != 0u) return;
   const uint8_t* up = a.up;
