@@ -258,3 +258,59 @@ def test_every_binary16_row_maximum(d):
     kc, vc, gst = gpu_decode(cfg, pay, L, H, d, n, bs, nb, bt.cuda())
     assert ost == 0 and gst == 0
     assert np.array_equal(u16(kc), okc) and np.array_equal(u16(vc), ovc)
+
+
+def _random_request(rng):
+    """A seeded random request: shape, budget, tier policy, sinks, decay,
+    score mode, input distribution and paged block size, redrawn until the
+    oracle's plan accepts it (sinks within the budget, decay table in range)."""
+    while True:
+        L, H = int(rng.integers(1, 4)), int(rng.integers(1, 5))
+        d = int(rng.choice([32, 64, 128, 256]))
+        n = int(np.exp(rng.uniform(0.0, np.log(6000.0))))
+        b = float(np.float32(rng.uniform(0.02, 1.0)))
+        tiers = int(rng.choice([2, 3]))
+        rho = float(rng.choice([0.0, 0.02, 0.1]))
+        num_sink = int(rng.choice([-1, -1, int(rng.integers(0, min(n, 64) + 1))]))
+        decay = float(rng.choice([1e-4, 1e-3, 5e-3, 1e-2]))
+        mode = int(rng.choice([oracle.KVNORM, oracle.RECENCY]))
+        cfg, ocfg = configs(L, H, d, n, b, tiers, rho=rho, num_sink=num_sink, decay=decay, mode=mode)
+        if oracle.validate(ocfg) != oracle.OK:
+            continue
+        try:
+            oracle.plan(ocfg)
+        except oracle.OracleError:
+            continue
+        extra = dict(outliers=str(rng.choice(["x8", "student_t", "none"])), specials=bool(rng.integers(0, 2)),
+                     bs=int(rng.choice([1, 8, 16, 32])))
+        return (L, H, d, n, b, tiers, rho, num_sink, decay, mode), cfg, ocfg, extra
+
+
+def test_random_requests_bit_exact():
+    """Thirty seeded random requests end to end (score, assign, pack, unpack
+    into a paged cache with a random block size): every stage bit-identical to
+    the oracle."""
+    rng = np.random.default_rng(8635)
+    for case in range(30):
+        shape, cfg, ocfg, extra = _random_request(rng)
+        L, H, d, n = shape[:4]
+        say(f"random request #{case}: {shape} {extra}")
+        k, v = workloads.make_kv(L, H, n, d, seed=case, outliers=extra["outliers"])
+        if extra["specials"]:
+            plant_specials(k, v, case)
+        kh, vh = u16(k), u16(v)
+        okey = oracle.score(ocfg, kh, vh)
+        otier = oracle.assign(ocfg, okey)
+        opay = oracle.pack(ocfg, kh, vh, otier)
+        codec = gpu_encode(cfg, k.cuda(), v.cuda())
+        assert np.array_equal(bits64(codec.scores.cpu().numpy()), bits64(okey)), f"case {case}: scores"
+        assert np.array_equal(codec.tier.cpu().numpy(), otier), f"case {case}: tier map"
+        assert codec.status[0].item() == 0
+        assert np.array_equal(codec.payload.cpu().numpy(), opay), f"case {case}: payload"
+        bs = extra["bs"]
+        nb = workloads.blocks_for(n, bs) + 2
+        bt = workloads.make_block_table(n, bs, nb, seed=case)
+        kc, vc, st = gpu_decode(cfg, codec.payload, L, H, d, n, bs, nb, bt.cuda())
+        okc, ovc, ost = oracle_decode(ocfg, opay, L, H, d, bs, nb, bt.numpy())
+        assert st == 0 and ost == oracle.OK, f"case {case}: status {st} / {ost}"
+        assert np.array_equal(u16(kc), okc) and np.array_equal(u16(vc), ovc), f"case {case}: caches"
