@@ -143,3 +143,35 @@ def test_attention_scores_short_requests(n):
     gtier = codec.tier.cpu().numpy()
     assert np.array_equal(gtier, oracle.assign(ocfg, gkey))
     assert np.array_equal(codec.payload.cpu().numpy(), oracle.pack(ocfg, u16(k), u16(v), gtier))
+
+
+def test_random_attention_requests():
+    """Sixteen seeded random attention-mode requests (layers, KV heads, query
+    heads per group, window, head dim, keys, budget, tier policy): every token
+    within the tolerance of the binary64 oracle and the tier map the exact
+    assignment of the GPU scores."""
+    rng = np.random.default_rng(355)
+    case = 0
+    while case < 16:
+        L, H = int(rng.integers(1, 3)), int(rng.integers(1, 5))
+        Hq = H * int(rng.choice([1, 2, 4, 8]))
+        W = int(rng.integers(1, 41))
+        d = int(rng.choice([32, 64, 128, 256]))
+        n = int(np.exp(rng.uniform(0.0, np.log(5000.0))))
+        b = float(np.float32(rng.uniform(0.1, 1.0)))
+        tiers = int(rng.choice([2, 3]))
+        cfg, ocfg = configs(L, H, d, n, b, tiers, decay=1e-3, mode=oracle.ATTN, Hq=Hq, W=W)
+        try:
+            oracle.plan(ocfg)  # the sinks must fit the budget
+        except oracle.OracleError:
+            continue
+        say(f"random attention #{case}: L={L} H={H} Hq={Hq} W={W} d={d} n={n} b={b} tiers={tiers}")
+        k, v = workloads.make_kv(L, H, n, d, seed=700 + case)
+        q = workloads.make_qobs(L, Hq, W, d, seed=700 + case)
+        okey = oracle.score(ocfg, u16(k), u16(v), u16(q))
+        codec = gpu_encode(cfg, k.cuda(), v.cuda(), q=q.cuda())
+        gkey = codec.scores.cpu().numpy()
+        rel = np.abs(gkey - okey) / np.abs(okey)
+        assert rel.max() < RTOL, (case, rel.max(), int(rel.argmax()))
+        assert np.array_equal(codec.tier.cpu().numpy(), oracle.assign(ocfg, gkey)), case
+        case += 1
