@@ -356,6 +356,7 @@ struct BatchRows {
     c4 = q.n4;
   }
 };
+static_assert(sizeof(BatchRows) + sizeof(void*) + sizeof(int) <= 4000, "kernel arguments");
 
 // Cut j reads the histogram of the first cut (in cut order) with a nonzero
 // rank and the same decided prefix.

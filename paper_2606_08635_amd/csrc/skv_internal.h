@@ -68,8 +68,9 @@ static_assert(sizeof(BatchArgs) <= 4000, "kernel arguments");
 
 // One request of a batched score / assign launch.  tok_block_begin: its
 // first workgroup in the partial-sum launch (token blocks of 256 / (d / 8)
-// tokens); fin_block_begin: its first 256-token block in the finish, recency
-// and (one workgroup per request) assign launches count requests instead.
+// tokens); fin_block_begin: its first 256-token block in the finish and
+// recency launches.  The assign launches index requests directly (one
+// workgroup per request, or one row per request in the split form).
 struct ScoreDesc {
   const uint16_t* k;
   const uint16_t* v;
