@@ -42,8 +42,12 @@ def test_source_digest_covers_the_kernel_and_every_header(tmp_path, monkeypatch)
     for name in ("unpack.hip", "row_codec.h"):
         path = src / name
         original = path.read_bytes()
-        path.write_bytes(original + b"\n")
+        # a line of code changes the digest
+        path.write_bytes(original + b"\nstatic_assert(true, \"\");\n")
         assert bench.source_digest("unpack.hip") != before, name
+        # comments and blank space do not
+        path.write_bytes(original + b"\n// a note\n/* another\n note */\n\n")
+        assert bench.source_digest("unpack.hip") == before, name
         path.write_bytes(original)
         assert bench.source_digest("unpack.hip") == before
 
