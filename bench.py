@@ -37,14 +37,14 @@ CSRC = os.path.join(ROOT, "paper_2606_08635_amd", "csrc")
 # kernel sources they were taken on: the first 16 hex digits of SHA-256 over
 # the kernel's .hip file and every header of the library (source_digest).
 MEASURED_TRAFFIC = {
-    ("mistral7b_32k", "pack"): (6.5084e9, "pack.hip", "53be8a7e37799a28"),
-    ("mistral7b_32k", "unpack"): (6.5127e9, "unpack.hip", "fc7d271f3728540e"),
-    ("gemma9b_b0.3", "pack"): (3.6863e9, "pack.hip", "53be8a7e37799a28"),
-    ("gemma9b_b0.3", "unpack"): (3.6886e9, "unpack.hip", "fc7d271f3728540e"),
-    ("gemma9b_b0.5", "pack"): (4.2500e9, "pack.hip", "53be8a7e37799a28"),
-    ("gemma9b_b0.5", "unpack"): (4.2524e9, "unpack.hip", "fc7d271f3728540e"),
-    ("gemma9b_b0.7", "pack"): (4.8051e9, "pack.hip", "53be8a7e37799a28"),
-    ("gemma9b_b0.7", "unpack"): (4.8081e9, "unpack.hip", "fc7d271f3728540e"),
+    ("mistral7b_32k", "pack"): (6.5085e9, "pack.hip", "0502305a78d59ddf"),
+    ("mistral7b_32k", "unpack"): (6.5127e9, "unpack.hip", "1a37b814f06ffd0e"),
+    ("gemma9b_b0.3", "pack"): (3.6863e9, "pack.hip", "0502305a78d59ddf"),
+    ("gemma9b_b0.3", "unpack"): (3.6886e9, "unpack.hip", "1a37b814f06ffd0e"),
+    ("gemma9b_b0.5", "pack"): (4.2500e9, "pack.hip", "0502305a78d59ddf"),
+    ("gemma9b_b0.5", "unpack"): (4.2524e9, "unpack.hip", "1a37b814f06ffd0e"),
+    ("gemma9b_b0.7", "pack"): (4.8051e9, "pack.hip", "0502305a78d59ddf"),
+    ("gemma9b_b0.7", "unpack"): (4.8079e9, "unpack.hip", "1a37b814f06ffd0e"),
 }
 
 
@@ -705,7 +705,7 @@ def main():
     ap.add_argument("--ceiling-gib", type=float, default=4.0, help="buffer size of --mode ceiling")
     ap.add_argument("--group-layers", type=int, default=4, help="layers per pipeline stage (--mode pipeline)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
-                    help="only copy a MIB-sized buffer with skv_link (reference for byte counters)")
+                    help="only copy a MIB-sized buffer with the runtime's device copy (reference for byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures the codec on one GPU; --gpus {args.gpus} is not supported "
@@ -721,7 +721,7 @@ def main():
         src = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         for _ in range(args.warmup + args.steps):
-            skv.link(dst, src, nbytes)
+            dst.copy_(src)  # the runtime's device copy: a fixed reference kernel
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": nbytes, "copies": args.warmup + args.steps}), flush=True)
         return

@@ -535,9 +535,11 @@ skv_status skv_unpack_groups(const skv_config* cfg, const skv_group_spec* spec, 
                              int32_t num_blocks, int32_t block_size, uint32_t* dev_status, hipStream_t stream);
 
 /* Link emulation for a one-GPU setup (Sec. 4.2: the payload crosses the
- * network between prefill and decode).  Copies `bytes` from src to dst,
- * ordered on stream like one copy: device to device when host_staging is
- * NULL, otherwise device to pinned host (host_staging, at least `bytes`,
+ * network between prefill and decode).  Copies `bytes` from src to dst (the
+ * two ranges must not overlap), ordered on stream like one copy: device to
+ * device when host_staging is NULL (the library's streaming copy kernel when
+ * both pointers are 16-byte aligned and bytes is a multiple of 16, else the
+ * runtime's copy), otherwise device to pinned host (host_staging, at least `bytes`,
  * allocated with hipHostMalloc) and back to device in 32 MiB pieces, the way
  * up of each piece overlapping the way down of the next on a second stream
  * that the library creates per device on first use (default priority, kept

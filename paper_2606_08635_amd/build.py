@@ -19,7 +19,8 @@ CEILING_LIB = os.path.join(HERE, "libskv_ceiling.so")
 CEILING_SOURCES = ["ceiling.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["skv_api.cpp", "score.hip", "attn.hip", "select.hip", "pack.hip", "unpack.hip", "upgrade.hip", "groups.hip"]
+SOURCES = ["skv_api.cpp", "score.hip", "attn.hip", "select.hip", "pack.hip", "unpack.hip", "upgrade.hip", "groups.hip",
+           "link.hip"]
 FLAGS = [
     "-x", "hip", "-std=c++17", "-O3", "--offload-arch=gfx950", "-fPIC",
     "-ffp-contract=off", "-fhip-fp32-correctly-rounded-divide-sqrt",

@@ -889,8 +889,11 @@ skv_status skv_link(void* dst, const void* src, uint64_t bytes, void* host_stagi
                     hipStream_t stream) {
   if (bytes == 0) return SKV_OK;
   if (dst == nullptr || src == nullptr) return SKV_ERR_INVALID_ARG;
-  if (host_staging == nullptr)
+  if (host_staging == nullptr) {
+    if (aligned(dst, 16) && aligned(src, 16) && bytes % 16 == 0)
+      return launched(launch_link_copy(dst, src, bytes, stream));
     return launched(hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream));
+  }
   int dev = -1;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0) return SKV_ERR_DEVICE;
   if (dev >= kMaxLinkDevices) return SKV_ERR_INVALID_ARG;

@@ -90,6 +90,11 @@ struct ScoreBatchArgs {
 static_assert(sizeof(ScoreBatchArgs) <= 4000, "kernel arguments");
 
 // Kernel launchers.  Each returns the launch status; none synchronizes.
+
+// Device-to-device copy of `bytes` (a multiple of 16; both pointers 16-byte
+// aligned; the ranges do not overlap).
+hipError_t launch_link_copy(void* dst, const void* src, uint64_t bytes, hipStream_t stream);
+
 hipError_t launch_score_kvnorm(const Geometry& g, const uint16_t* k, const uint16_t* v,
                                const double* w2, uint64_t* partial, double* score,
                                hipStream_t stream);

@@ -216,6 +216,23 @@ def test_link_emulation_round_trip():
     assert torch.equal(x, y) and torch.equal(x, z)
 
 
+def test_link_device_copy_sizes_and_alignment():
+    """The device-to-device link: the library's copy kernel (aligned, whole
+    16-byte units: one unit, one workgroup's 4096 units and one more, a ragged
+    last workgroup) and the runtime copy it hands other cases to (odd sizes,
+    pointers off 16-byte alignment) move exactly nbytes and nothing past them."""
+    say("link device copy")
+    total = (1 << 20) + 4096
+    src = torch.randint(0, 255, (total,), dtype=torch.uint8, device="cuda")
+    for off, nbytes in [(0, 16), (0, 65536), (0, 65536 + 16), (0, 65536 * 3 + 16 * 7), (0, 1 << 20),
+                        (0, 100003), (4, 4096), (16, (1 << 19) + 5), (8, 65536 * 2)]:
+        dst = torch.full((total,), 0x5A, dtype=torch.uint8, device="cuda")
+        skv.link(dst[off:], src[off:], nbytes)
+        torch.cuda.synchronize()
+        assert torch.equal(dst[off:off + nbytes], src[off:off + nbytes]), (off, nbytes)
+        assert bool((dst[:off] == 0x5A).all()) and bool((dst[off + nbytes:] == 0x5A).all()), (off, nbytes)
+
+
 @pytest.mark.parametrize("d", [32, 128])
 def test_every_binary16_row_maximum(d):
     """Rows whose absmax runs over every positive finite binary16 value, once
